@@ -1,0 +1,248 @@
+#!/usr/bin/env python3
+"""Throughput benchmark of libhexconv on one MI355X.
+
+Default workload (the headline metric's configuration): camera-shaped hex
+convolution, fp32, N=256 images of 40x40 (hexagonal 1027-pixel footprint,
+log-normal x Bernoulli(0.1) amplitudes), 1 -> 16 channels, kernel size 2
+(19 taps), stride 1.  One step = forward + backward-data + backward-weight
+(with bias gradient) over one batch.  Value = effective GFLOP/s counting
+2*N*H_out*W_out*C_in*C_out*T per op (hex taps only).
+
+Inputs are resident in HBM before timing starts.  Each step works on a
+different batch from a rotating set whose total size exceeds the 256 MB
+Infinity Cache, so reads and writes go to HBM rather than staying cached.
+
+Other workloads (--config c3 / c4 / c5) print their own line; they are
+parity workloads measured on request.
+
+Prints one JSON line.  With --gpus > 1 it exits: this build runs on one GPU.
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import glob
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+from paper_1903_01814_amd import hexconv as hx          # noqa: E402
+from paper_1903_01814_amd import inputs as gen         # noqa: E402
+
+HBM_PEAK_GBS = 8000.0
+BF16_MFMA_PEAK_TFLOPS = 2500.0
+CACHE_BYTES = 256 << 20
+ROTATE_MIN_BYTES = 3 * CACHE_BYTES
+
+
+def source_hash():
+    h = hashlib.sha1()
+    for p in sorted(glob.glob(os.path.join(ROOT, "paper_1903_01814_amd", "csrc", "*"))):
+        with open(p, "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:12]
+
+
+def read_counters(workload, kernel):
+    """HBM bytes per launch from the committed rocprofv3 --pmc summary, if it
+    was taken on the current kernel sources."""
+    path = os.path.join(ROOT, "profiles", "counters_%s.txt" % workload)
+    if not os.path.exists(path):
+        return None
+    kv = {}
+    for line in open(path):
+        if ":" in line and not line.startswith("#"):
+            a, b = line.split(":", 1)
+            kv[a.strip()] = b.strip()
+    if kv.get("source_hash") != source_hash() or kv.get("kernel") != kernel:
+        return None
+    try:
+        return float(kv["hbm_bytes_per_launch"])
+    except (KeyError, ValueError):
+        return None
+
+
+class Timer:
+    """HIP events on the stream the kernels are launched on."""
+
+    def __init__(self, torch, stream):
+        self.torch, self.stream = torch, stream
+
+    def run(self, fn, reps):
+        t = self.torch
+        a = t.cuda.Event(enable_timing=True)
+        b = t.cuda.Event(enable_timing=True)
+        t.cuda.synchronize()
+        a.record(self.stream)
+        for i in range(reps):
+            fn(i)
+        b.record(self.stream)
+        t.cuda.synchronize()
+        return a.elapsed_time(b) / reps          # ms per call
+
+
+def conv_flop(N, Ci, Co, Ho, Wo, T):
+    return 2.0 * N * Ho * Wo * Ci * Co * T
+
+
+def dev(torch, a, dtype):
+    return torch.from_numpy(np.ascontiguousarray(a)).to(dtype).to("cuda:0")
+
+
+def cpu_baseline_conv(cfg, d, k, s, seconds):
+    """The fp64 oracle on the same full-batch workload (fwd + bwd), repeated
+    until `seconds` of CPU time have elapsed; returns GFLOP/s and threads."""
+    import oracle
+    H, W = cfg["H"], cfg["W"]
+    Ho, Wo = oracle.out_shape(H, W, s)
+    T = oracle.num_taps(k)
+    flop = 3 * conv_flop(cfg["N"], cfg["C_in"], cfg["C_out"], Ho, Wo, T)
+    reps = 0
+    t0 = time.perf_counter()
+    while True:
+        oracle.conv_fwd(d["x"], d["w"], d["b"], k, s)
+        oracle.conv_bwd_data(d["dy"], d["w"], k, s, H, W)
+        oracle.conv_bwd_weight(d["x"], d["dy"], k, s)
+        reps += 1
+        el = time.perf_counter() - t0
+        if el >= seconds:
+            break
+    return flop * reps / el / 1e9, oracle.threads(), reps, el
+
+
+def bench_conv(args, torch, cfg_key):
+    cfg = gen.CONFIGS[cfg_key]
+    N, Ci, Co, H, W, k, s = (cfg[n] for n in ("N", "C_in", "C_out", "H", "W", "k", "stride"))
+    T = hx.hex_num_taps(k)
+    Ho, Wo = hx.hex_out_shape(H, W, s)
+    dt = torch.float32 if cfg["dtype"] == gen.F32 else torch.bfloat16
+    esz = 4 if dt == torch.float32 else 2
+    per_set = esz * (N * Ci * H * W * 2 + N * Co * Ho * Wo * 2)
+    nsets = max(1, -(-ROTATE_MIN_BYTES // per_set))
+    d0 = gen.conv_inputs(cfg, T, (Ho, Wo), seed=0)
+    sets = []
+    for b in range(nsets):
+        d = d0 if b == 0 else gen.conv_inputs(cfg, T, (Ho, Wo), seed=b)
+        sets.append(dict(x=dev(torch, d["x"], dt), dy=dev(torch, d["dy"], dt),
+                         y=torch.empty((N, Co, Ho, Wo), dtype=dt, device="cuda:0"),
+                         dx=torch.empty((N, Ci, H, W), dtype=dt, device="cuda:0")))
+        if b == 0:
+            w = dev(torch, d["w"], dt)
+            bias = dev(torch, d["b"], dt)
+    dw = torch.empty((Co, Ci, T), dtype=torch.float32, device="cuda:0")
+    db = torch.empty((Co,), dtype=torch.float32, device="cuda:0")
+    nws = hx.hexconv_bwd_weight_workspace(N, Ci, Co, H, W, k, s, hx.HEX_F32 if esz == 4 else hx.HEX_BF16)
+    ws = torch.empty(max(nws, 1), dtype=torch.uint8, device="cuda:0")
+    stream = torch.cuda.current_stream()
+
+    def fwd(i):
+        z = sets[i % nsets]
+        hx.hexconv_fwd(z["x"], w, bias, z["y"], k, s, stream=stream)
+
+    def bwd_data(i):
+        z = sets[i % nsets]
+        hx.hexconv_bwd_data(z["dy"], w, z["dx"], k, s, stream=stream)
+
+    def bwd_weight(i):
+        z = sets[i % nsets]
+        hx.hexconv_bwd_weight(z["x"], z["dy"], dw, db, ws, k, s, stream=stream)
+
+    def step(i):
+        fwd(i)
+        bwd_data(i)
+        bwd_weight(i)
+
+    timer = Timer(torch, stream)
+    for i in range(args.warmup):
+        step(i)
+    torch.cuda.synchronize()
+    ms_step = timer.run(step, args.steps)
+
+    # per-op launch durations, each op alone over the same rotation
+    ops = {}
+    bytes_alg = {
+        "fwd": esz * (N * Ci * H * W + Co * Ci * T + Co + N * Co * Ho * Wo),
+        "bwd_data": esz * (N * Co * Ho * Wo + Co * Ci * T + N * Ci * H * W),
+        "bwd_weight": esz * (N * Ci * H * W + N * Co * Ho * Wo) + 4 * (Co * Ci * T + Co),
+    }
+    for name, fn in (("fwd", fwd), ("bwd_data", bwd_data), ("bwd_weight", bwd_weight)):
+        for i in range(max(3, args.warmup // 2)):
+            fn(i)
+        ms = timer.run(fn, args.steps)
+        ops[name] = dict(ms=ms, gbs=bytes_alg[name] / (ms * 1e-3) / 1e9)
+    flop_op = conv_flop(N, Ci, Co, Ho, Wo, T)
+    flop_step = 3 * flop_op
+    value = flop_step / (ms_step * 1e-3) / 1e9
+
+    dom = max(ops, key=lambda n: ops[n]["ms"])
+    bound = "hbm" if cfg["dtype"] == gen.F32 or Ci * T < 64 else "mfma"
+    kernel_name = KERNEL_NAMES.get((cfg_key, dom), dom)
+    if bound == "hbm":
+        achieved = bytes_alg[dom] / (ops[dom]["ms"] * 1e-3) / 1e9
+        roof = dict(bound="hbm", achieved=round(achieved, 1), peak=HBM_PEAK_GBS, unit="GB/s",
+                    frac=round(achieved / HBM_PEAK_GBS, 4))
+    else:
+        achieved = flop_op / (ops[dom]["ms"] * 1e-3) / 1e12
+        roof = dict(bound="mfma", achieved=round(achieved, 2), peak=BF16_MFMA_PEAK_TFLOPS,
+                    unit="TFLOP/s", frac=round(achieved / BF16_MFMA_PEAK_TFLOPS, 4))
+    roof["kernel"] = kernel_name
+    roof["op"] = dom
+    roof["traffic"] = read_counters(cfg["name"], kernel_name)
+
+    out = dict(
+        metric="hex-conv effective GFLOP/s (fwd+bwd)", value=round(value, 2), unit="GFLOP/s",
+        n_gpus=1, steps=args.steps, warmup=args.warmup, ms_per_step=round(ms_step, 5),
+        higher_is_better=True, scaling="weak", vs_baseline=None,
+        dtype="f32" if esz == 4 else "bf16", data="synthetic",
+        config=dict(workload=cfg["name"], N=N, C_in=Ci, C_out=Co, H=H, W=W, k=k, stride=s,
+                    taps=T, H_out=Ho, W_out=Wo, rotating_batches=nsets),
+        samples_per_s=round(N / (ms_step * 1e-3), 1),
+        per_op={n: dict(ms=round(v["ms"], 5), alg_GBps=round(v["gbs"], 1),
+                        GFLOPs=round(flop_op / (v["ms"] * 1e-3) / 1e9, 1))
+                for n, v in ops.items()},
+        roofline=roof,
+    )
+    if not args.no_cpu_baseline:
+        d = d0
+        gfs, thr, reps, el = cpu_baseline_conv(cfg, d, k, s, args.cpu_seconds)
+        out["cpu_baseline"] = dict(
+            value=round(gfs, 3), unit="GFLOP/s", cores=thr, kind="oracle",
+            sample="full batch (N=%d) fwd+bwd_data+bwd_weight, fp64, repeated %d times in %.1f s"
+                   % (N, reps, el))
+    return out
+
+
+# kernel that dominates each op (as it appears in rocprofv3 traces)
+KERNEL_NAMES = {}
+
+
+def main():
+    p = argparse.ArgumentParser(description=__doc__.split("\n")[0])
+    p.add_argument("--gpus", type=int, default=1)
+    p.add_argument("--steps", type=int, default=200)
+    p.add_argument("--warmup", type=int, default=20)
+    p.add_argument("--config", default="c2", choices=["c2", "c4"])
+    p.add_argument("--no-cpu-baseline", action="store_true")
+    p.add_argument("--cpu-seconds", type=float, default=12.0)
+    args = p.parse_args()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py: this library runs on a single GPU; --gpus %d is not supported "
+              "(the batch would be sharded across GPUs, one process each)" % args.gpus, file=sys.stderr)
+        sys.exit(2)
+    import torch
+    if not torch.cuda.is_available():
+        print("bench.py: no GPU visible", file=sys.stderr)
+        sys.exit(1)
+    hx.load()
+    out = bench_conv(args, torch, args.config)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

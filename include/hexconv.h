@@ -1,0 +1,159 @@
+/*
+ * hexconv.h -- C ABI of libhexconv: hexagonal convolution and pooling on
+ * MI355X (gfx950).
+ *
+ * The operations are those of HexagDLy (Steppa & Holch, arXiv:1903.01814,
+ * Sec. 2), computed directly by HIP kernels:
+ *
+ *  Addressing (Sec. 2.1, Fig. 1): hexagonally sampled data in a rectangular
+ *  tensor whose columns are columns of vertically adjacent pixels, every
+ *  second column shifted by half a pitch so that rows line up.  Rows count
+ *  top to bottom, columns left to right.  Convention fixed here: the odd
+ *  columns (1, 3, ...) are the ones lying half a pitch lower in the
+ *  hexagonal array.  Blank tensor cells hold whatever the caller put there
+ *  and are computed on like any other value.
+ *
+ *  Kernel of size k (Sec. 2.2): the centre pixel plus k layers of neighbours,
+ *  T = 1 + 3k(k+1) taps.  Taps are numbered column by column (column offset
+ *  -k .. k), each column top to bottom; a weight belongs to one physical
+ *  direction, the same for both column parities.  hex_tap_table gives the
+ *  (column, row) offsets per centre-column parity.
+ *
+ *  Padding and stride (Sec. 2.3, Fig. 4): kernels are centred on tensor
+ *  elements only and taps outside the tensor read zero.  A stride s takes
+ *  equal steps of s pitches along the three lattice axes from the top-left
+ *  element: output (i, j) is centred on input row s*i + (j odd ? s/2 : 0)
+ *  (integer division), column s*j.  The output uses the same addressing.
+ *  W_out = (W-1)/s + 1; all output columns get the length of the shortest
+ *  one (H_out from hex_out_shape).
+ *
+ *  Pooling (Sec. 2.4): the same windows, padding and stride with a max or an
+ *  average.  Conventions fixed here: padded taps count as zeros in both; the
+ *  average divides by T; the max keeps the first maximal tap in tap order.
+ *
+ * Conventions for every entry point:
+ *  - H and W are always the INPUT sizes; output sizes come from
+ *    hex_out_shape.
+ *  - Tensors are dense NCHW device pointers: x[N][C_in][H][W],
+ *    y[N][C_out][H_out][W_out], w[C_out][C_in][T] (same dtype as x), bias
+ *    [C_out] (dtype of x).  Pointers must be 16-byte aligned.  dw and db are
+ *    float32 whatever the input dtype.
+ *  - The caller owns and allocates every buffer, including workspaces.  The
+ *    library never allocates, frees or synchronises; it only enqueues
+ *    kernels on `stream` (a hipStream_t; NULL = the default stream).
+ *  - Outputs are fully overwritten, never accumulated into.
+ *  - Arguments are validated on the host before anything is enqueued; a
+ *    rejected call returns a negative hex_status and enqueues nothing.
+ *  - bf16 paths read bf16, accumulate in float32 and round outputs to
+ *    nearest-even.  The ReLU flag applies max(0, .) before rounding.
+ *  - No function throws; all are safe to call from C.
+ */
+#ifndef HEXCONV_H
+#define HEXCONV_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+    HEX_OK = 0,
+    HEX_ERR_INVALID_ARG = -1, /* null pointer, bad size, k, stride, dtype */
+    HEX_ERR_UNSUPPORTED = -2, /* valid request this build cannot run */
+    HEX_ERR_LAUNCH = -3       /* a kernel launch reported an error */
+} hex_status;
+
+typedef enum { HEX_F32 = 0, HEX_BF16 = 1 } hex_dtype;
+
+typedef enum { HEX_POOL_MAX = 0, HEX_POOL_AVG = 1 } hex_pool_mode;
+
+enum { HEX_FLAG_RELU = 1 };
+
+#define HEX_MAX_K 8      /* largest kernel size accepted */
+#define HEX_MAX_STRIDE 8 /* largest stride accepted */
+
+/* Number of taps of a size-k kernel, 1 + 3k(k+1) (Sec. 2.2); negative
+ * hex_status for k outside [0, HEX_MAX_K]. */
+int hex_num_taps(int k);
+
+/* Output size of an H x W input under stride s (Sec. 2.3).  H_out may be 0
+ * when H is too small for the odd output columns.  Returns a hex_status. */
+int hex_out_shape(int H, int W, int stride, int *H_out, int *W_out);
+
+/* Tap offsets of a size-k kernel for a centre element in a column of the
+ * given parity (0 even, 1 odd): tap t reads element (r + drow[t],
+ * c + dcol[t]).  dcol and drow are host arrays of hex_num_taps(k) ints.
+ * Returns a hex_status. */
+int hex_tap_table(int k, int parity, int *dcol, int *drow);
+
+/*
+ * Forward convolution (Sec. 2.3):
+ *   y[n][co][i][j] = bias[co] + sum_ci sum_t w[co][ci][t] * x[n][ci][p_t]
+ * where p_t is tap t of the window centred on output (i, j), and x reads 0
+ * outside the tensor.  bias may be NULL.  flags: HEX_FLAG_RELU.
+ */
+int hexconv_fwd(const void *x, const void *w, const void *bias, void *y,
+                int N, int C_in, int C_out, int H, int W, int k, int stride,
+                hex_dtype dt, int flags, void *stream);
+
+/*
+ * Gradient of the forward map with respect to x (adjoint of hexconv_fwd
+ * without bias):
+ *   dx[n][ci][p] = sum over (co, i, j, t) with p_t(i, j) = p of
+ *                  w[co][ci][t] * dy[n][co][i][j].
+ * dy is [N][C_out][H_out][W_out]; dx is [N][C_in][H][W] in dtype dt.
+ */
+int hexconv_bwd_data(const void *dy, const void *w, void *dx, int N, int C_in,
+                     int C_out, int H, int W, int k, int stride, hex_dtype dt,
+                     void *stream);
+
+/* Bytes of device workspace hexconv_bwd_weight needs for these sizes
+ * (0 for invalid arguments). */
+size_t hexconv_bwd_weight_workspace(int N, int C_in, int C_out, int H, int W,
+                                    int k, int stride, hex_dtype dt);
+
+/*
+ * Gradient with respect to the weights and bias:
+ *   dw[co][ci][t] = sum_n sum_(i,j) dy[n][co][i][j] * x[n][ci][p_t(i, j)]
+ *   db[co]        = sum_n sum_(i,j) dy[n][co][i][j]          (db nullable)
+ * dw and db are float32 device buffers.  ws is a device workspace of at
+ * least hexconv_bwd_weight_workspace(...) bytes (may be NULL when that is
+ * 0).  The reduction order is fixed, so results are deterministic.
+ */
+int hexconv_bwd_weight(const void *x, const void *dy, float *dw, float *db,
+                       void *ws, size_t ws_bytes, int N, int C_in, int C_out,
+                       int H, int W, int k, int stride, hex_dtype dt,
+                       void *stream);
+
+/*
+ * Pooling (Sec. 2.4) over the windows of hexconv_fwd, per channel:
+ *   max: y = value of the first maximal tap (padding counts as 0);
+ *   avg: y = (sum of the T tap values, padding 0) / T.
+ * argmax_tap (nullable, uint8 [N][C][H_out][W_out]) receives the winning
+ * tap index for HEX_POOL_MAX; it is not written for HEX_POOL_AVG.
+ */
+int hexpool_fwd(const void *x, void *y, uint8_t *argmax_tap, int N, int C,
+                int H, int W, int k, int stride, hex_pool_mode mode,
+                hex_dtype dt, void *stream);
+
+/*
+ * Pooling gradient: max routes dy[o] to the element its argmax tap points
+ * at (dropped when that tap is padding; argmax_tap required); avg shares
+ * dy[o] / T over the in-tensor taps.  When relu_y is not NULL (the ReLU
+ * output that fed the pool, [N][C][H][W], dtype dt) the result is
+ * multiplied by [relu_y > 0].  dx is [N][C][H][W].
+ */
+int hexpool_bwd(const void *dy, const uint8_t *argmax_tap, const void *relu_y,
+                void *dx, int N, int C, int H, int W, int k, int stride,
+                hex_pool_mode mode, hex_dtype dt, void *stream);
+
+/* Static description of a hex_status value. */
+const char *hex_status_string(int status);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* HEXCONV_H */

@@ -1,0 +1,241 @@
+// hexconv_abi.hip -- the extern "C" entry points declared in hexconv.h:
+// argument validation (host only, before anything is enqueued), choice of
+// kernel per shape regime, and launch-status mapping.
+#include <stdint.h>
+#include <stdlib.h>
+#include <string.h>
+
+#include "../../include/hexconv.h"
+#include "hexgeom.h"
+#include "kernels.h"
+
+namespace {
+
+using hexk::ConvShape;
+using hexk::Dtype;
+
+constexpr long kMaxElems = (1L << 31) - 1; // per tensor, int32-indexable planes
+
+bool aligned16(const void *p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+bool dtype_ok(int dt) { return dt == HEX_F32 || dt == HEX_BF16; }
+
+size_t dtype_bytes(int dt) { return dt == HEX_F32 ? 4 : 2; }
+
+// Shape checks shared by every op.  Fills `sh`.  C_in/C_out both = C for pools.
+int check_shape(int N, int Ci, int Co, int H, int W, int k, int stride, int dt, ConvShape &sh)
+{
+    if (N < 0 || Ci < 1 || Co < 1 || H < 1 || W < 1)
+        return HEX_ERR_INVALID_ARG;
+    if (k < 0 || k > HEX_MAX_K || stride < 1 || stride > HEX_MAX_STRIDE)
+        return HEX_ERR_INVALID_ARG;
+    if (!dtype_ok(dt))
+        return HEX_ERR_INVALID_ARG;
+    if (H > 65535 || W > 65535)
+        return HEX_ERR_UNSUPPORTED;
+    const long hw = static_cast<long>(H) * W;
+    if (hw * N > kMaxElems / Ci || hw * N > kMaxElems / Co)
+        return HEX_ERR_UNSUPPORTED;
+    if (static_cast<long>(Co) * Ci * hexgeom::num_taps(k) > kMaxElems)
+        return HEX_ERR_UNSUPPORTED;
+    sh.N = N;
+    sh.Ci = Ci;
+    sh.Co = Co;
+    sh.H = H;
+    sh.W = W;
+    sh.k = k;
+    sh.s = stride;
+    sh.T = hexgeom::num_taps(k);
+    hexgeom::out_shape(H, W, stride, sh.Ho, sh.Wo);
+    return HEX_OK;
+}
+
+int ptrs_ok(std::initializer_list<const void *> required, std::initializer_list<const void *> optional)
+{
+    for (const void *p : required)
+        if (p == nullptr || !aligned16(p))
+            return HEX_ERR_INVALID_ARG;
+    for (const void *p : optional)
+        if (p != nullptr && !aligned16(p))
+            return HEX_ERR_INVALID_ARG;
+    return HEX_OK;
+}
+
+int launched(hipError_t e) { return e == hipSuccess ? HEX_OK : HEX_ERR_LAUNCH; }
+
+// HEXCONV_PATH=generic forces the generic kernels (used by tests to compare
+// the specialised kernels against them).
+bool force_generic()
+{
+    const char *v = getenv("HEXCONV_PATH");
+    return v != nullptr && strcmp(v, "generic") == 0;
+}
+
+} // namespace
+
+extern "C" {
+
+int hex_num_taps(int k)
+{
+    if (k < 0 || k > HEX_MAX_K)
+        return HEX_ERR_INVALID_ARG;
+    return hexgeom::num_taps(k);
+}
+
+int hex_out_shape(int H, int W, int stride, int *H_out, int *W_out)
+{
+    if (H < 1 || W < 1 || stride < 1 || stride > HEX_MAX_STRIDE || H_out == nullptr ||
+        W_out == nullptr)
+        return HEX_ERR_INVALID_ARG;
+    int ho = 0, wo = 0;
+    hexgeom::out_shape(H, W, stride, ho, wo);
+    *H_out = ho;
+    *W_out = wo;
+    return HEX_OK;
+}
+
+int hex_tap_table(int k, int parity, int *dcol, int *drow)
+{
+    if (k < 0 || k > HEX_MAX_K || (parity != 0 && parity != 1) || dcol == nullptr ||
+        drow == nullptr)
+        return HEX_ERR_INVALID_ARG;
+    const int T = hexgeom::num_taps(k);
+    for (int t = 0; t < T; ++t) {
+        int dq = 0, ds = 0;
+        hexgeom::tap_axial(k, t, dq, ds);
+        dcol[t] = dq;
+        drow[t] = hexgeom::tap_drow(dq, ds, parity);
+    }
+    return HEX_OK;
+}
+
+int hexconv_fwd(const void *x, const void *w, const void *bias, void *y, int N, int C_in,
+                int C_out, int H, int W, int k, int stride, hex_dtype dt, int flags, void *stream)
+{
+    ConvShape sh;
+    int rc = check_shape(N, C_in, C_out, H, W, k, stride, dt, sh);
+    if (rc != HEX_OK)
+        return rc;
+    if ((flags & ~HEX_FLAG_RELU) != 0)
+        return HEX_ERR_INVALID_ARG;
+    if ((rc = ptrs_ok({x, w, y}, {bias})) != HEX_OK)
+        return rc;
+    if (N == 0 || sh.Ho == 0)
+        return HEX_OK;
+    hipStream_t st = static_cast<hipStream_t>(stream);
+    const bool relu = (flags & HEX_FLAG_RELU) != 0;
+    const Dtype d = static_cast<Dtype>(dt);
+    (void)force_generic;
+    return launched(hexk::conv_fwd_generic(x, w, bias, y, sh, d, relu, st));
+}
+
+int hexconv_bwd_data(const void *dy, const void *w, void *dx, int N, int C_in, int C_out, int H,
+                     int W, int k, int stride, hex_dtype dt, void *stream)
+{
+    ConvShape sh;
+    int rc = check_shape(N, C_in, C_out, H, W, k, stride, dt, sh);
+    if (rc != HEX_OK)
+        return rc;
+    if ((rc = ptrs_ok({w, dx}, {dy})) != HEX_OK)
+        return rc;
+    if (dy == nullptr && N > 0 && sh.Ho > 0)
+        return HEX_ERR_INVALID_ARG;
+    if (N == 0)
+        return HEX_OK;
+    hipStream_t st = static_cast<hipStream_t>(stream);
+    const Dtype d = static_cast<Dtype>(dt);
+    return launched(hexk::conv_bwd_data_generic(dy, w, dx, sh, d, st));
+}
+
+size_t hexconv_bwd_weight_workspace(int N, int C_in, int C_out, int H, int W, int k, int stride,
+                                    hex_dtype dt)
+{
+    ConvShape sh;
+    if (check_shape(N, C_in, C_out, H, W, k, stride, dt, sh) != HEX_OK)
+        return 0;
+    if (N == 0 || sh.Ho == 0)
+        return 0;
+    return hexk::wgrad_generic_workspace(sh);
+}
+
+int hexconv_bwd_weight(const void *x, const void *dy, float *dw, float *db, void *ws,
+                       size_t ws_bytes, int N, int C_in, int C_out, int H, int W, int k,
+                       int stride, hex_dtype dt, void *stream)
+{
+    ConvShape sh;
+    int rc = check_shape(N, C_in, C_out, H, W, k, stride, dt, sh);
+    if (rc != HEX_OK)
+        return rc;
+    if ((rc = ptrs_ok({dw}, {x, dy, db, ws})) != HEX_OK)
+        return rc;
+    const bool empty = (N == 0 || sh.Ho == 0);
+    if (!empty && (x == nullptr || dy == nullptr))
+        return HEX_ERR_INVALID_ARG;
+    const size_t need = empty ? 0 : hexk::wgrad_generic_workspace(sh);
+    if (need > 0 && (ws == nullptr || ws_bytes < need))
+        return HEX_ERR_INVALID_ARG;
+    hipStream_t st = static_cast<hipStream_t>(stream);
+    if (empty)
+        return launched(hexk::fill_zero_f32(dw, db, sh, st));
+    const Dtype d = static_cast<Dtype>(dt);
+    return launched(hexk::wgrad_generic(x, dy, dw, db, ws, sh, d, st));
+}
+
+int hexpool_fwd(const void *x, void *y, uint8_t *argmax_tap, int N, int C, int H, int W, int k,
+                int stride, hex_pool_mode mode, hex_dtype dt, void *stream)
+{
+    ConvShape sh;
+    int rc = check_shape(N, C, C, H, W, k, stride, dt, sh);
+    if (rc != HEX_OK)
+        return rc;
+    if (mode != HEX_POOL_MAX && mode != HEX_POOL_AVG)
+        return HEX_ERR_INVALID_ARG;
+    if ((rc = ptrs_ok({x, y}, {argmax_tap})) != HEX_OK)
+        return rc;
+    if (N == 0 || sh.Ho == 0)
+        return HEX_OK;
+    hipStream_t st = static_cast<hipStream_t>(stream);
+    const Dtype d = static_cast<Dtype>(dt);
+    return launched(hexk::pool_fwd_generic(x, y, mode == HEX_POOL_MAX ? argmax_tap : nullptr, sh,
+                                           mode, d, st));
+}
+
+int hexpool_bwd(const void *dy, const uint8_t *argmax_tap, const void *relu_y, void *dx, int N,
+                int C, int H, int W, int k, int stride, hex_pool_mode mode, hex_dtype dt,
+                void *stream)
+{
+    ConvShape sh;
+    int rc = check_shape(N, C, C, H, W, k, stride, dt, sh);
+    if (rc != HEX_OK)
+        return rc;
+    if (mode != HEX_POOL_MAX && mode != HEX_POOL_AVG)
+        return HEX_ERR_INVALID_ARG;
+    if ((rc = ptrs_ok({dx}, {dy, argmax_tap, relu_y})) != HEX_OK)
+        return rc;
+    const bool empty_out = (sh.Ho == 0);
+    if (!empty_out && N > 0 && (dy == nullptr || (mode == HEX_POOL_MAX && argmax_tap == nullptr)))
+        return HEX_ERR_INVALID_ARG;
+    if (N == 0)
+        return HEX_OK;
+    hipStream_t st = static_cast<hipStream_t>(stream);
+    const Dtype d = static_cast<Dtype>(dt);
+    return launched(hexk::pool_bwd_generic(dy, argmax_tap, relu_y, dx, sh, mode, d, st));
+}
+
+const char *hex_status_string(int status)
+{
+    switch (status) {
+    case HEX_OK:
+        return "HEX_OK";
+    case HEX_ERR_INVALID_ARG:
+        return "HEX_ERR_INVALID_ARG: invalid argument";
+    case HEX_ERR_UNSUPPORTED:
+        return "HEX_ERR_UNSUPPORTED: valid request not supported by this build";
+    case HEX_ERR_LAUNCH:
+        return "HEX_ERR_LAUNCH: kernel launch failed";
+    default:
+        return "unknown hex_status";
+    }
+}
+
+} // extern "C"

@@ -1,0 +1,462 @@
+// k_generic.hip -- kernels that handle every kernel size, stride, channel
+// count and dtype.  The shape-specialised kernels in the other files take
+// over for the common cases; these remain the path for everything else.
+//
+// Conv forward: one output pixel per thread, a 2-D output tile per block,
+// the input region of the tile (with its k-wide halo, zero outside the
+// tensor) staged channel by channel in LDS as float.
+// Conv backward-data: gather form -- each input pixel looks up, per tap, the
+// output whose window reads it (a lattice test for strides > 1).
+// Weight gradient: per-chunk partial sums in a fixed tree order, then a
+// reduction kernel over chunks (deterministic).
+// Pool forward / backward: one output (input) element per thread.
+#include <algorithm>
+
+#include "hexdev.h"
+#include "kernels.h"
+
+namespace hexk {
+namespace {
+
+using namespace hexgeom;
+
+constexpr int kThreads = 256;
+constexpr int kCoBlock = 8; // output channels per block (forward)
+constexpr int kCiBlock = 8; // input channels per block (backward-data)
+constexpr int kTapGroup = 8; // taps accumulated per pass (weight gradient)
+
+__host__ __device__ inline int region_rows(int TI, int k, int s) { return s * (TI - 1) + (s >> 1) + 2 * k + 1; }
+__host__ __device__ inline int region_cols(int TJ, int k, int s) { return s * (TJ - 1) + 2 * k + 1; }
+
+template <typename T>
+__global__ __launch_bounds__(kThreads) void conv_fwd_generic_k(
+    const T *__restrict__ x, const T *__restrict__ w, const T *__restrict__ b,
+    T *__restrict__ y, ConvShape sh, int relu, int TI, int TJ, int tiles_j)
+{
+    extern __shared__ float region[];
+    __shared__ TapLds tl;
+    fill_taps(tl, sh.k);
+
+    const int tile = blockIdx.x;
+    const int n = blockIdx.y;
+    const int co0 = blockIdx.z * kCoBlock;
+    const int ti0 = (tile / tiles_j) * TI;
+    const int tj0 = (tile % tiles_j) * TJ;
+    const int r_lo = sh.s * ti0 - sh.k;
+    const int c_lo = sh.s * tj0 - sh.k;
+    const int RH = region_rows(TI, sh.k, sh.s);
+    const int RW = region_cols(TJ, sh.k, sh.s);
+
+    const int li = threadIdx.x / TJ, lj = threadIdx.x % TJ;
+    const int i = ti0 + li, j = tj0 + lj;
+    const bool active = threadIdx.x < TI * TJ && i < sh.Ho && j < sh.Wo;
+    int rr = 0, cc = 0, par = 0;
+    if (active) {
+        rr = centre_row(i, j, sh.s) - r_lo;
+        cc = centre_col(j, sh.s) - c_lo;
+        par = centre_col(j, sh.s) & 1;
+    }
+
+    float acc[kCoBlock];
+#pragma unroll
+    for (int cb = 0; cb < kCoBlock; ++cb)
+        acc[cb] = (b != nullptr && co0 + cb < sh.Co) ? to_f(b[co0 + cb]) : 0.f;
+
+    const size_t HW = static_cast<size_t>(sh.H) * sh.W;
+    for (int ci = 0; ci < sh.Ci; ++ci) {
+        __syncthreads();
+        const T *plane = x + (static_cast<size_t>(n) * sh.Ci + ci) * HW;
+        for (int e = threadIdx.x; e < RH * RW; e += kThreads) {
+            const int r = r_lo + e / RW, c = c_lo + e % RW;
+            region[e] = (r >= 0 && r < sh.H && c >= 0 && c < sh.W)
+                            ? to_f(plane[static_cast<size_t>(r) * sh.W + c])
+                            : 0.f;
+        }
+        __syncthreads();
+        if (active) {
+            for (int t = 0; t < sh.T; ++t) {
+                const float v = region[(rr + tl.drow[par][t]) * RW + cc + tl.dq[t]];
+#pragma unroll
+                for (int cb = 0; cb < kCoBlock; ++cb) {
+                    const int co = min(co0 + cb, sh.Co - 1);
+                    acc[cb] += to_f(w[(static_cast<size_t>(co) * sh.Ci + ci) * sh.T + t]) * v;
+                }
+            }
+        }
+    }
+    if (!active)
+        return;
+    const size_t HWo = static_cast<size_t>(sh.Ho) * sh.Wo;
+#pragma unroll
+    for (int cb = 0; cb < kCoBlock; ++cb) {
+        const int co = co0 + cb;
+        if (co >= sh.Co)
+            break;
+        float v = acc[cb];
+        if (relu)
+            v = fmaxf(v, 0.f);
+        y[(static_cast<size_t>(n) * sh.Co + co) * HWo + static_cast<size_t>(i) * sh.Wo + j] = from_f<T>(v);
+    }
+}
+
+template <typename T>
+__global__ __launch_bounds__(kThreads) void conv_bwd_data_generic_k(
+    const T *__restrict__ dy, const T *__restrict__ w, T *__restrict__ dx, ConvShape sh)
+{
+    __shared__ TapLds tl;
+    fill_taps(tl, sh.k);
+    __syncthreads();
+
+    const int p = blockIdx.x * kThreads + threadIdx.x;
+    const int n = blockIdx.y;
+    const int ci0 = blockIdx.z * kCiBlock;
+    if (p >= sh.H * sh.W)
+        return;
+    const int r = p / sh.W, c = p % sh.W;
+    const size_t HWo = static_cast<size_t>(sh.Ho) * sh.Wo;
+
+    float acc[kCiBlock];
+#pragma unroll
+    for (int cb = 0; cb < kCiBlock; ++cb)
+        acc[cb] = 0.f;
+
+    for (int t = 0; t < sh.T; ++t) {
+        int i = 0, j = 0;
+        if (!source_output(r, c, tl.dq[t], tl.ds[t], sh.s, sh.Ho, sh.Wo, i, j))
+            continue;
+        const size_t o = static_cast<size_t>(i) * sh.Wo + j;
+        for (int co = 0; co < sh.Co; ++co) {
+            const float g = to_f(dy[(static_cast<size_t>(n) * sh.Co + co) * HWo + o]);
+#pragma unroll
+            for (int cb = 0; cb < kCiBlock; ++cb) {
+                const int ci = min(ci0 + cb, sh.Ci - 1);
+                acc[cb] += to_f(w[(static_cast<size_t>(co) * sh.Ci + ci) * sh.T + t]) * g;
+            }
+        }
+    }
+    const size_t HW = static_cast<size_t>(sh.H) * sh.W;
+#pragma unroll
+    for (int cb = 0; cb < kCiBlock; ++cb) {
+        const int ci = ci0 + cb;
+        if (ci >= sh.Ci)
+            break;
+        dx[(static_cast<size_t>(n) * sh.Ci + ci) * HW + p] = from_f<T>(acc[cb]);
+    }
+}
+
+template <typename T>
+__global__ __launch_bounds__(kThreads) void wgrad_partial_generic_k(
+    const T *__restrict__ x, const T *__restrict__ dy, float *__restrict__ part_w,
+    float *__restrict__ part_b, ConvShape sh, int chunk)
+{
+    __shared__ TapLds tl;
+    __shared__ float red[kTapGroup + 1][kThreads];
+    fill_taps(tl, sh.k);
+    __syncthreads();
+
+    const int co = blockIdx.y, ci = blockIdx.z;
+    const long HWo = static_cast<long>(sh.Ho) * sh.Wo;
+    const long total = HWo * sh.N;
+    const long begin = static_cast<long>(blockIdx.x) * chunk;
+    const long end = min(begin + chunk, total);
+    const size_t HW = static_cast<size_t>(sh.H) * sh.W;
+    const bool do_bias = (ci == 0);
+
+    for (int tg = 0; tg < sh.T; tg += kTapGroup) {
+        float acc[kTapGroup];
+#pragma unroll
+        for (int u = 0; u < kTapGroup; ++u)
+            acc[u] = 0.f;
+        float accb = 0.f;
+        for (long e = begin + threadIdx.x; e < end; e += kThreads) {
+            const int n = static_cast<int>(e / HWo);
+            const int o = static_cast<int>(e % HWo);
+            const int i = o / sh.Wo, j = o % sh.Wo;
+            const float g = to_f(dy[(static_cast<size_t>(n) * sh.Co + co) * HWo + o]);
+            const int rc = centre_row(i, j, sh.s), cc = centre_col(j, sh.s);
+            const int par = cc & 1;
+            const T *plane = x + (static_cast<size_t>(n) * sh.Ci + ci) * HW;
+#pragma unroll
+            for (int u = 0; u < kTapGroup; ++u) {
+                const int t = tg + u;
+                if (t < sh.T) {
+                    const int r = rc + tl.drow[par][t], c = cc + tl.dq[t];
+                    if (r >= 0 && r < sh.H && c >= 0 && c < sh.W)
+                        acc[u] += g * to_f(plane[static_cast<size_t>(r) * sh.W + c]);
+                }
+            }
+            if (tg == 0)
+                accb += g;
+        }
+#pragma unroll
+        for (int u = 0; u < kTapGroup; ++u)
+            red[u][threadIdx.x] = acc[u];
+        red[kTapGroup][threadIdx.x] = accb;
+        for (int half = kThreads / 2; half > 0; half >>= 1) {
+            __syncthreads();
+            if (threadIdx.x < half) {
+#pragma unroll
+                for (int u = 0; u <= kTapGroup; ++u)
+                    red[u][threadIdx.x] += red[u][threadIdx.x + half];
+            }
+        }
+        __syncthreads();
+        const size_t EW = static_cast<size_t>(sh.Co) * sh.Ci * sh.T;
+        if (threadIdx.x < kTapGroup && tg + threadIdx.x < sh.T)
+            part_w[blockIdx.x * EW + (static_cast<size_t>(co) * sh.Ci + ci) * sh.T + tg + threadIdx.x] =
+                red[threadIdx.x][0];
+        if (tg == 0 && do_bias && threadIdx.x == 0)
+            part_b[static_cast<size_t>(blockIdx.x) * sh.Co + co] = red[kTapGroup][0];
+        __syncthreads();
+    }
+}
+
+__global__ __launch_bounds__(kThreads) void fill_zero_k(float *__restrict__ a, int na,
+                                                        float *__restrict__ b, int nb)
+{
+    const int e = blockIdx.x * kThreads + threadIdx.x;
+    if (e < na)
+        a[e] = 0.f;
+    else if (b != nullptr && e < na + nb)
+        b[e - na] = 0.f;
+}
+
+__global__ __launch_bounds__(kThreads) void wgrad_reduce_k(
+    const float *__restrict__ part_w, const float *__restrict__ part_b,
+    float *__restrict__ dw, float *__restrict__ db, int nchunks, int EW, int Co)
+{
+    const int e = blockIdx.x * kThreads + threadIdx.x;
+    if (e < EW) {
+        float s = 0.f;
+        for (int c = 0; c < nchunks; ++c)
+            s += part_w[static_cast<size_t>(c) * EW + e];
+        dw[e] = s;
+    } else if (db != nullptr && e < EW + Co) {
+        const int co = e - EW;
+        float s = 0.f;
+        for (int c = 0; c < nchunks; ++c)
+            s += part_b[static_cast<size_t>(c) * Co + co];
+        db[co] = s;
+    }
+}
+
+template <typename T, int MODE>
+__global__ __launch_bounds__(kThreads) void pool_fwd_generic_k(
+    const T *__restrict__ x, T *__restrict__ y, uint8_t *__restrict__ am,
+    ConvShape sh, long total)
+{
+    __shared__ TapLds tl;
+    fill_taps(tl, sh.k);
+    __syncthreads();
+    const long HWo = static_cast<long>(sh.Ho) * sh.Wo;
+    const size_t HW = static_cast<size_t>(sh.H) * sh.W;
+    for (long e = static_cast<long>(blockIdx.x) * kThreads + threadIdx.x; e < total;
+         e += static_cast<long>(gridDim.x) * kThreads) {
+        const long plane = e / HWo;
+        const int o = static_cast<int>(e % HWo);
+        const int i = o / sh.Wo, j = o % sh.Wo;
+        const int rc = centre_row(i, j, sh.s), cc = centre_col(j, sh.s);
+        const int par = cc & 1;
+        const T *src = x + plane * HW;
+        float best = 0.f, sum = 0.f;
+        int arg = 0;
+        for (int t = 0; t < sh.T; ++t) {
+            const int r = rc + tl.drow[par][t], c = cc + tl.dq[t];
+            const float v = (r >= 0 && r < sh.H && c >= 0 && c < sh.W)
+                                ? to_f(src[static_cast<size_t>(r) * sh.W + c])
+                                : 0.f;
+            sum += v;
+            if (t == 0 || v > best) {
+                best = v;
+                arg = t;
+            }
+        }
+        if (MODE == 0) {
+            y[e] = from_f<T>(best);
+            if (am != nullptr)
+                am[e] = static_cast<uint8_t>(arg);
+        } else {
+            y[e] = from_f<T>(sum / static_cast<float>(sh.T));
+        }
+    }
+}
+
+template <typename T, int MODE>
+__global__ __launch_bounds__(kThreads) void pool_bwd_generic_k(
+    const T *__restrict__ dy, const uint8_t *__restrict__ am,
+    const T *__restrict__ relu_y, T *__restrict__ dx, ConvShape sh, long total)
+{
+    __shared__ TapLds tl;
+    fill_taps(tl, sh.k);
+    __syncthreads();
+    const long HW = static_cast<long>(sh.H) * sh.W;
+    const size_t HWo = static_cast<size_t>(sh.Ho) * sh.Wo;
+    for (long e = static_cast<long>(blockIdx.x) * kThreads + threadIdx.x; e < total;
+         e += static_cast<long>(gridDim.x) * kThreads) {
+        const long plane = e / HW;
+        const int p = static_cast<int>(e % HW);
+        const int r = p / sh.W, c = p % sh.W;
+        float acc = 0.f;
+        for (int t = 0; t < sh.T; ++t) {
+            int i = 0, j = 0;
+            if (!source_output(r, c, tl.dq[t], tl.ds[t], sh.s, sh.Ho, sh.Wo, i, j))
+                continue;
+            const size_t o = plane * HWo + static_cast<size_t>(i) * sh.Wo + j;
+            if (MODE == 0) {
+                if (am[o] == t)
+                    acc += to_f(dy[o]);
+            } else {
+                acc += to_f(dy[o]);
+            }
+        }
+        if (MODE == 1)
+            acc = acc / static_cast<float>(sh.T);
+        if (relu_y != nullptr && !(to_f(relu_y[e]) > 0.f))
+            acc = 0.f;
+        dx[e] = from_f<T>(acc);
+    }
+}
+
+inline int cdiv(long a, long b) { return static_cast<int>((a + b - 1) / b); }
+
+constexpr size_t kGenericLdsLimit = 64 * 1024;
+
+void pick_fwd_tile(const ConvShape &sh, int &TI, int &TJ)
+{
+    static const int cand[][2] = {{8, 32}, {16, 16}, {4, 64}, {8, 16}, {4, 32}, {4, 16}, {2, 16}, {1, 16}, {1, 8}};
+    TI = 1;
+    TJ = 8;
+    for (auto &c : cand) {
+        const size_t bytes = sizeof(float) * static_cast<size_t>(region_rows(c[0], sh.k, sh.s)) *
+                             region_cols(c[1], sh.k, sh.s);
+        if (bytes <= kGenericLdsLimit) {
+            TI = c[0];
+            TJ = c[1];
+            return;
+        }
+    }
+}
+
+int wgrad_generic_chunks(const ConvShape &sh, int &chunk)
+{
+    const long total = static_cast<long>(sh.N) * sh.Ho * sh.Wo;
+    const long pairs = static_cast<long>(sh.Co) * sh.Ci;
+    long nchunks = (2048 + pairs - 1) / pairs;
+    nchunks = std::max(1L, std::min(nchunks, (total + 255) / 256));
+    nchunks = std::min(nchunks, 65535L);
+    chunk = static_cast<int>((total + nchunks - 1) / nchunks);
+    if (chunk < 1)
+        chunk = 1;
+    return static_cast<int>((total + chunk - 1) / chunk);
+}
+
+} // namespace
+
+hipError_t conv_fwd_generic(const void *x, const void *w, const void *b, void *y,
+                            const ConvShape &sh, Dtype dt, bool relu, hipStream_t st)
+{
+    int TI, TJ;
+    pick_fwd_tile(sh, TI, TJ);
+    const int tiles_i = cdiv(sh.Ho, TI), tiles_j = cdiv(sh.Wo, TJ);
+    const size_t lds = sizeof(float) * static_cast<size_t>(region_rows(TI, sh.k, sh.s)) *
+                       region_cols(TJ, sh.k, sh.s);
+    dim3 grid(tiles_i * tiles_j, sh.N, cdiv(sh.Co, kCoBlock));
+    if (dt == F32)
+        hipLaunchKernelGGL(conv_fwd_generic_k<float>, grid, dim3(kThreads), lds, st,
+                           (const float *)x, (const float *)w, (const float *)b, (float *)y, sh,
+                           relu ? 1 : 0, TI, TJ, tiles_j);
+    else
+        hipLaunchKernelGGL(conv_fwd_generic_k<bf16raw>, grid, dim3(kThreads), lds, st,
+                           (const bf16raw *)x, (const bf16raw *)w, (const bf16raw *)b,
+                           (bf16raw *)y, sh, relu ? 1 : 0, TI, TJ, tiles_j);
+    return hipGetLastError();
+}
+
+hipError_t conv_bwd_data_generic(const void *dy, const void *w, void *dx, const ConvShape &sh,
+                                 Dtype dt, hipStream_t st)
+{
+    dim3 grid(cdiv(static_cast<long>(sh.H) * sh.W, kThreads), sh.N, cdiv(sh.Ci, kCiBlock));
+    if (dt == F32)
+        hipLaunchKernelGGL(conv_bwd_data_generic_k<float>, grid, dim3(kThreads), 0, st,
+                           (const float *)dy, (const float *)w, (float *)dx, sh);
+    else
+        hipLaunchKernelGGL(conv_bwd_data_generic_k<bf16raw>, grid, dim3(kThreads), 0, st,
+                           (const bf16raw *)dy, (const bf16raw *)w, (bf16raw *)dx, sh);
+    return hipGetLastError();
+}
+
+size_t wgrad_generic_workspace(const ConvShape &sh)
+{
+    int chunk;
+    const int nchunks = wgrad_generic_chunks(sh, chunk);
+    return sizeof(float) * static_cast<size_t>(nchunks) *
+           (static_cast<size_t>(sh.Co) * sh.Ci * sh.T + sh.Co);
+}
+
+hipError_t wgrad_generic(const void *x, const void *dy, float *dw, float *db, void *ws,
+                         const ConvShape &sh, Dtype dt, hipStream_t st)
+{
+    int chunk;
+    const int nchunks = wgrad_generic_chunks(sh, chunk);
+    const size_t EW = static_cast<size_t>(sh.Co) * sh.Ci * sh.T;
+    float *part_w = static_cast<float *>(ws);
+    float *part_b = part_w + static_cast<size_t>(nchunks) * EW;
+    dim3 grid(nchunks, sh.Co, sh.Ci);
+    if (dt == F32)
+        hipLaunchKernelGGL(wgrad_partial_generic_k<float>, grid, dim3(kThreads), 0, st,
+                           (const float *)x, (const float *)dy, part_w, part_b, sh, chunk);
+    else
+        hipLaunchKernelGGL(wgrad_partial_generic_k<bf16raw>, grid, dim3(kThreads), 0, st,
+                           (const bf16raw *)x, (const bf16raw *)dy, part_w, part_b, sh, chunk);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess)
+        return e;
+    hipLaunchKernelGGL(wgrad_reduce_k, dim3(cdiv(static_cast<long>(EW) + sh.Co, kThreads)),
+                       dim3(kThreads), 0, st, part_w, part_b, dw, db, nchunks,
+                       static_cast<int>(EW), sh.Co);
+    return hipGetLastError();
+}
+
+hipError_t fill_zero_f32(float *dw, float *db, const ConvShape &sh, hipStream_t st)
+{
+    const long EW = static_cast<long>(sh.Co) * sh.Ci * sh.T;
+    hipLaunchKernelGGL(fill_zero_k, dim3(cdiv(EW + sh.Co, kThreads)), dim3(kThreads), 0, st, dw,
+                       static_cast<int>(EW), db, sh.Co);
+    return hipGetLastError();
+}
+
+hipError_t pool_fwd_generic(const void *x, void *y, uint8_t *am, const ConvShape &sh, int mode,
+                            Dtype dt, hipStream_t st)
+{
+    const long total = static_cast<long>(sh.N) * sh.Ci * sh.Ho * sh.Wo;
+    const int blocks = std::max(1, std::min(cdiv(total, kThreads), 65535 * 16));
+#define HEX_POOL_FWD(T, M)                                                                   \
+    hipLaunchKernelGGL((pool_fwd_generic_k<T, M>), dim3(blocks), dim3(kThreads), 0, st,     \
+                       (const T *)x, (T *)y, am, sh, total)
+    if (dt == F32) {
+        if (mode == 0) HEX_POOL_FWD(float, 0); else HEX_POOL_FWD(float, 1);
+    } else {
+        if (mode == 0) HEX_POOL_FWD(bf16raw, 0); else HEX_POOL_FWD(bf16raw, 1);
+    }
+#undef HEX_POOL_FWD
+    return hipGetLastError();
+}
+
+hipError_t pool_bwd_generic(const void *dy, const uint8_t *am, const void *relu_y, void *dx,
+                            const ConvShape &sh, int mode, Dtype dt, hipStream_t st)
+{
+    const long total = static_cast<long>(sh.N) * sh.Ci * sh.H * sh.W;
+    const int blocks = std::max(1, std::min(cdiv(total, kThreads), 65535 * 16));
+#define HEX_POOL_BWD(T, M)                                                                   \
+    hipLaunchKernelGGL((pool_bwd_generic_k<T, M>), dim3(blocks), dim3(kThreads), 0, st,     \
+                       (const T *)dy, am, (const T *)relu_y, (T *)dx, sh, total)
+    if (dt == F32) {
+        if (mode == 0) HEX_POOL_BWD(float, 0); else HEX_POOL_BWD(float, 1);
+    } else {
+        if (mode == 0) HEX_POOL_BWD(bf16raw, 0); else HEX_POOL_BWD(bf16raw, 1);
+    }
+#undef HEX_POOL_BWD
+    return hipGetLastError();
+}
+
+} // namespace hexk

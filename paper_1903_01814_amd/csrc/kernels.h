@@ -1,0 +1,41 @@
+// kernels.h -- host-side launchers of the HIP kernels (internal).
+//
+// Every launcher assumes its arguments were validated by the C ABI layer
+// (hexconv_abi.cpp): sizes positive, k and stride in range, shapes
+// consistent, pointers non-null where required.  Launchers enqueue on the
+// given stream and return the launch status.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace hexk {
+
+enum Dtype { F32 = 0, BF16 = 1 };
+
+struct ConvShape {
+    int N, Ci, Co, H, W, k, s, Ho, Wo, T;
+};
+
+// ---- generic kernels: any k, stride, channel count and dtype -----------
+hipError_t conv_fwd_generic(const void *x, const void *w, const void *b,
+                            void *y, const ConvShape &sh, Dtype dt, bool relu,
+                            hipStream_t st);
+hipError_t conv_bwd_data_generic(const void *dy, const void *w, void *dx,
+                                 const ConvShape &sh, Dtype dt,
+                                 hipStream_t st);
+size_t wgrad_generic_workspace(const ConvShape &sh);
+hipError_t wgrad_generic(const void *x, const void *dy, float *dw, float *db,
+                         void *ws, const ConvShape &sh, Dtype dt,
+                         hipStream_t st);
+// dw (and db if not null) := 0
+hipError_t fill_zero_f32(float *dw, float *db, const ConvShape &sh, hipStream_t st);
+hipError_t pool_fwd_generic(const void *x, void *y, uint8_t *am,
+                            const ConvShape &sh, int mode, Dtype dt,
+                            hipStream_t st);
+hipError_t pool_bwd_generic(const void *dy, const uint8_t *am,
+                            const void *relu_y, void *dx, const ConvShape &sh,
+                            int mode, Dtype dt, hipStream_t st);
+
+} // namespace hexk

@@ -1,0 +1,156 @@
+"""Host-side checks of libhexconv (no GPU needed): every symbol the public
+header declares is exported, the library's geometry tables agree bit for bit
+with the oracle's independent enumeration, and every argument error is
+rejected on the host before anything is enqueued."""
+import ctypes
+import os
+import re
+
+import pytest
+
+import oracle
+from paper_1903_01814_amd import hexconv as hx
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "hexconv.h")
+
+
+def declared_functions():
+    src = open(HEADER).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"^[A-Za-z_][\w\s\*]*?\b(hex\w+)\s*\(", src,
+                                 flags=re.M)))
+
+
+def test_header_declares_expected_entry_points():
+    names = declared_functions()
+    for n in ["hexconv_fwd", "hexconv_bwd_data", "hexconv_bwd_weight",
+              "hexconv_bwd_weight_workspace", "hexpool_fwd", "hexpool_bwd",
+              "hex_num_taps", "hex_out_shape", "hex_tap_table",
+              "hex_status_string"]:
+        assert n in names
+
+
+def test_library_exports_every_declared_symbol():
+    lib = hx.load()
+    for name in declared_functions():
+        assert hasattr(lib, name), name
+        assert name in hx.SIGNATURES, name
+
+
+@pytest.mark.parametrize("k", range(0, 9))
+@pytest.mark.parametrize("parity", [0, 1])
+def test_tap_table_matches_oracle(k, parity):
+    """Library tap tables vs the oracle's axial enumeration, bit-exact."""
+    assert hx.hex_num_taps(k) == oracle.num_taps(k)
+    dcol, drow = hx.hex_tap_table(k, parity)
+    dq, ds = oracle.taps(k)
+    r0, c0 = 20, 20 + parity
+    for t in range(len(dq)):
+        r, c = oracle.step(r0, c0, int(dq[t]), int(ds[t]))
+        assert (dcol[t], drow[t]) == (c - c0, r - r0)
+
+
+def test_out_shape_matches_oracle():
+    for s in range(1, 9):
+        for H in list(range(1, 20)) + [40, 48, 128, 257]:
+            for W in list(range(1, 14)) + [40, 48, 128, 255]:
+                assert hx.hex_out_shape(H, W, s) == oracle.out_shape(H, W, s), (H, W, s)
+
+
+def test_status_strings():
+    for st in (0, -1, -2, -3):
+        assert hx.status_string(st).startswith("HEX_")
+    assert "unknown" in hx.status_string(7)
+
+
+# ----------------------------------------------------------- error paths
+
+class FakePtr:
+    """Aligned, never-dereferenced addresses: validation must reject bad
+    arguments before touching memory or the GPU."""
+    A = 0x10000
+    B = 0x20000
+    C = 0x30000
+    D = 0x40000
+
+
+def _fwd(x=FakePtr.A, w=FakePtr.B, b=None, y=FakePtr.C, N=2, Ci=1, Co=4, H=8,
+         W=8, k=1, s=1, dt=0, flags=0):
+    return hx.load().hexconv_fwd(x, w, b, y, N, Ci, Co, H, W, k, s, dt, flags,
+                                 None)
+
+
+@pytest.mark.parametrize("kw", [
+    dict(x=None), dict(w=None), dict(y=None), dict(x=FakePtr.A + 4),
+    dict(b=FakePtr.D + 2), dict(N=-1), dict(Ci=0), dict(Co=0), dict(H=0),
+    dict(W=0), dict(k=-1), dict(k=9), dict(s=0), dict(s=9), dict(dt=2),
+    dict(dt=-1), dict(flags=2)])
+def test_fwd_rejects_invalid(kw):
+    assert _fwd(**kw) == hx.HEX_ERR_INVALID_ARG
+
+
+def test_fwd_rejects_oversize():
+    assert _fwd(N=1 << 20, Ci=64, H=256, W=256) == hx.HEX_ERR_UNSUPPORTED
+    assert _fwd(H=70000) == hx.HEX_ERR_UNSUPPORTED
+
+
+def test_fwd_empty_batch_is_noop():
+    # N == 0 or an empty output: nothing to compute, nothing enqueued
+    assert _fwd(N=0) == hx.HEX_OK
+    assert _fwd(H=1, W=5, s=2) == hx.HEX_OK
+
+
+def test_bwd_data_rejects_invalid():
+    lib = hx.load()
+    f = lambda dy=FakePtr.A, w=FakePtr.B, dx=FakePtr.C, k=1, s=1, dt=0: \
+        lib.hexconv_bwd_data(dy, w, dx, 2, 3, 4, 9, 9, k, s, dt, None)
+    assert f(dy=None) == hx.HEX_ERR_INVALID_ARG
+    assert f(w=None) == hx.HEX_ERR_INVALID_ARG
+    assert f(dx=None) == hx.HEX_ERR_INVALID_ARG
+    assert f(dx=FakePtr.C + 8) == hx.HEX_ERR_INVALID_ARG
+    assert f(k=12) == hx.HEX_ERR_INVALID_ARG
+    assert f(dt=5) == hx.HEX_ERR_INVALID_ARG
+
+
+def test_bwd_weight_workspace_and_errors():
+    lib = hx.load()
+    need = lib.hexconv_bwd_weight_workspace(4, 2, 3, 16, 16, 1, 1, 0)
+    assert need > 0
+    assert lib.hexconv_bwd_weight_workspace(4, 2, 3, 16, 16, -1, 1, 0) == 0
+    f = lambda x=FakePtr.A, dy=FakePtr.B, dw=FakePtr.C, db=None, ws=FakePtr.D, \
+        nb=need: lib.hexconv_bwd_weight(x, dy, dw, db, ws, nb, 4, 2, 3, 16, 16,
+                                        1, 1, 0, None)
+    assert f(ws=None) == hx.HEX_ERR_INVALID_ARG
+    assert f(nb=need - 1) == hx.HEX_ERR_INVALID_ARG
+    assert f(dw=None) == hx.HEX_ERR_INVALID_ARG
+    assert f(x=None) == hx.HEX_ERR_INVALID_ARG
+    assert f(db=FakePtr.C + 4) == hx.HEX_ERR_INVALID_ARG
+
+
+def test_pool_rejects_invalid():
+    lib = hx.load()
+    fw = lambda x=FakePtr.A, y=FakePtr.B, am=None, mode=0, k=1, s=2: \
+        lib.hexpool_fwd(x, y, am, 2, 3, 9, 9, k, s, mode, 1, None)
+    assert fw(x=None) == hx.HEX_ERR_INVALID_ARG
+    assert fw(mode=2) == hx.HEX_ERR_INVALID_ARG
+    assert fw(am=FakePtr.C + 1) == hx.HEX_ERR_INVALID_ARG
+    assert fw(s=0) == hx.HEX_ERR_INVALID_ARG
+    bw = lambda dy=FakePtr.A, am=FakePtr.B, ry=None, dx=FakePtr.C, mode=0: \
+        lib.hexpool_bwd(dy, am, ry, dx, 2, 3, 9, 9, 1, 2, mode, 1, None)
+    assert bw(am=None) == hx.HEX_ERR_INVALID_ARG          # max needs argmax
+    assert bw(dx=None) == hx.HEX_ERR_INVALID_ARG
+    assert bw(ry=FakePtr.D + 2) == hx.HEX_ERR_INVALID_ARG
+    assert bw(mode=3) == hx.HEX_ERR_INVALID_ARG
+
+
+def test_host_helper_errors():
+    lib = hx.load()
+    assert lib.hex_num_taps(-1) == hx.HEX_ERR_INVALID_ARG
+    assert lib.hex_num_taps(9) == hx.HEX_ERR_INVALID_ARG
+    a, b = ctypes.c_int(), ctypes.c_int()
+    assert lib.hex_out_shape(0, 5, 1, ctypes.byref(a), ctypes.byref(b)) == -1
+    assert lib.hex_out_shape(5, 5, 1, None, ctypes.byref(b)) == -1
+    buf = (ctypes.c_int * 7)()
+    assert lib.hex_tap_table(1, 2, buf, buf) == -1
+    assert lib.hex_tap_table(1, 0, None, buf) == -1
