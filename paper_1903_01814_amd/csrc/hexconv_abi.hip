@@ -31,7 +31,7 @@ int check_shape(int N, int Ci, int Co, int H, int W, int k, int stride, int dt, 
         return HEX_ERR_INVALID_ARG;
     if (!dtype_ok(dt))
         return HEX_ERR_INVALID_ARG;
-    if (H > 65535 || W > 65535)
+    if (H > 65535 || W > 65535 || N > 65535 || Ci > 65535 || Co > 65535)
         return HEX_ERR_UNSUPPORTED;
     const long hw = static_cast<long>(H) * W;
     if (hw * N > kMaxElems / Ci || hw * N > kMaxElems / Co)
