@@ -44,6 +44,11 @@
  *  - Outputs are fully overwritten, never accumulated into.
  *  - Arguments are validated on the host before anything is enqueued; a
  *    rejected call returns a negative hex_status and enqueues nothing.
+ *  - N = 0 is a valid empty batch and batch-shaped buffers may then be NULL:
+ *    forward, backward-data and pooling calls return HEX_OK and enqueue
+ *    nothing; hexconv_bwd_weight writes zeros to dw (and db).  When the
+ *    input is too small for any output (H_out = 0), forward calls write
+ *    nothing and gradient calls write zeros.
  *  - bf16 paths read bf16, accumulate in float32 and round outputs to
  *    nearest-even.  The ReLU flag applies max(0, .) before rounding.
  *  - No function throws; all are safe to call from C.

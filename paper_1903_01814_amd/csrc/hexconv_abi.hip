@@ -118,9 +118,11 @@ int hexconv_fwd(const void *x, const void *w, const void *bias, void *y, int N, 
         return rc;
     if ((flags & ~HEX_FLAG_RELU) != 0)
         return HEX_ERR_INVALID_ARG;
+    if (N == 0)
+        return HEX_OK; // empty batch: buffers may be NULL
     if ((rc = ptrs_ok({x, w, y}, {bias})) != HEX_OK)
         return rc;
-    if (N == 0 || sh.Ho == 0)
+    if (sh.Ho == 0)
         return HEX_OK;
     hipStream_t st = static_cast<hipStream_t>(stream);
     const bool relu = (flags & HEX_FLAG_RELU) != 0;
@@ -136,12 +138,12 @@ int hexconv_bwd_data(const void *dy, const void *w, void *dx, int N, int C_in, i
     int rc = check_shape(N, C_in, C_out, H, W, k, stride, dt, sh);
     if (rc != HEX_OK)
         return rc;
+    if (N == 0)
+        return HEX_OK; // empty batch: buffers may be NULL
     if ((rc = ptrs_ok({w, dx}, {dy})) != HEX_OK)
         return rc;
-    if (dy == nullptr && N > 0 && sh.Ho > 0)
+    if (dy == nullptr && sh.Ho > 0)
         return HEX_ERR_INVALID_ARG;
-    if (N == 0)
-        return HEX_OK;
     hipStream_t st = static_cast<hipStream_t>(stream);
     const Dtype d = static_cast<Dtype>(dt);
     return launched(hexk::conv_bwd_data_generic(dy, w, dx, sh, d, st));
@@ -190,9 +192,11 @@ int hexpool_fwd(const void *x, void *y, uint8_t *argmax_tap, int N, int C, int H
         return rc;
     if (mode != HEX_POOL_MAX && mode != HEX_POOL_AVG)
         return HEX_ERR_INVALID_ARG;
+    if (N == 0)
+        return HEX_OK; // empty batch: buffers may be NULL
     if ((rc = ptrs_ok({x, y}, {argmax_tap})) != HEX_OK)
         return rc;
-    if (N == 0 || sh.Ho == 0)
+    if (sh.Ho == 0)
         return HEX_OK;
     hipStream_t st = static_cast<hipStream_t>(stream);
     const Dtype d = static_cast<Dtype>(dt);
@@ -210,13 +214,12 @@ int hexpool_bwd(const void *dy, const uint8_t *argmax_tap, const void *relu_y, v
         return rc;
     if (mode != HEX_POOL_MAX && mode != HEX_POOL_AVG)
         return HEX_ERR_INVALID_ARG;
+    if (N == 0)
+        return HEX_OK; // empty batch: buffers may be NULL
     if ((rc = ptrs_ok({dx}, {dy, argmax_tap, relu_y})) != HEX_OK)
         return rc;
-    const bool empty_out = (sh.Ho == 0);
-    if (!empty_out && N > 0 && (dy == nullptr || (mode == HEX_POOL_MAX && argmax_tap == nullptr)))
+    if (sh.Ho > 0 && (dy == nullptr || (mode == HEX_POOL_MAX && argmax_tap == nullptr)))
         return HEX_ERR_INVALID_ARG;
-    if (N == 0)
-        return HEX_OK;
     hipStream_t st = static_cast<hipStream_t>(stream);
     const Dtype d = static_cast<Dtype>(dt);
     return launched(hexk::pool_bwd_generic(dy, argmax_tap, relu_y, dx, sh, mode, d, st));

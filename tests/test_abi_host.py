@@ -96,9 +96,18 @@ def test_fwd_rejects_oversize():
 
 
 def test_fwd_empty_batch_is_noop():
-    # N == 0 or an empty output: nothing to compute, nothing enqueued
+    # N == 0 or an empty output: nothing to compute, nothing enqueued; an
+    # empty batch may come with NULL buffers (empty tensors)
     assert _fwd(N=0) == hx.HEX_OK
+    assert _fwd(N=0, x=None, y=None, w=None) == hx.HEX_OK
     assert _fwd(H=1, W=5, s=2) == hx.HEX_OK
+    lib = hx.load()
+    assert lib.hexconv_bwd_data(None, None, None, 0, 1, 2, 8, 8, 1, 1, 0, None) == hx.HEX_OK
+    assert lib.hexpool_fwd(None, None, None, 0, 3, 8, 8, 1, 2, 0, 1, None) == hx.HEX_OK
+    assert lib.hexpool_bwd(None, None, None, None, 0, 3, 8, 8, 1, 2, 0, 1, None) == hx.HEX_OK
+    # the weight gradient of an empty batch is zero, so dw is still required
+    assert lib.hexconv_bwd_weight(None, None, None, None, None, 0, 0, 1, 2, 8, 8, 1,
+                                  1, 0, None) == hx.HEX_ERR_INVALID_ARG
 
 
 def test_bwd_data_rejects_invalid():
