@@ -8,7 +8,9 @@ log-normal x Bernoulli(0.1) amplitudes), 1 -> 16 channels, kernel size 2
 (with bias gradient) over one batch.  Value = effective GFLOP/s counting
 2*N*H_out*W_out*C_in*C_out*T per op (hex taps only).
 
-Inputs are resident in HBM before timing starts.  Each step works on a
+Inputs are resident in HBM before timing starts.  The K timed steps are
+captured once into a HIP graph and replayed (after W eager warm-up steps and
+one untimed replay), so the time is GPU execution, not Python launch cost.  Each step works on a
 different batch from a rotating set whose total size exceeds the 256 MB
 Infinity Cache, so reads and writes go to HBM rather than staying cached.
 
@@ -68,23 +70,56 @@ def read_counters(workload, kernel):
         return None
 
 
-class Timer:
-    """HIP events on the stream the kernels are launched on."""
+class EagerTimer:
+    """Plain launches bracketed by HIP events (used for counter collection,
+    where graph replay is not wanted)."""
 
-    def __init__(self, torch, stream):
-        self.torch, self.stream = torch, stream
+    def __init__(self, torch):
+        self.torch = torch
 
-    def run(self, fn, reps):
+    def time(self, fn, reps):
         t = self.torch
+        t.cuda.synchronize()
         a = t.cuda.Event(enable_timing=True)
         b = t.cuda.Event(enable_timing=True)
-        t.cuda.synchronize()
-        a.record(self.stream)
+        st = t.cuda.current_stream()
+        a.record(st)
         for i in range(reps):
             fn(i)
-        b.record(self.stream)
+        b.record(st)
         t.cuda.synchronize()
-        return a.elapsed_time(b) / reps          # ms per call
+        return a.elapsed_time(b) / reps
+
+
+class GraphTimer:
+    """Captures `reps` calls of a launch sequence into one HIP graph (the
+    library enqueues on torch's current stream, which is the capture stream
+    inside the capture) and times one replay with HIP events recorded on the
+    replay stream.  Host-side launch cost is thereby outside the timed
+    region; what remains is GPU execution of the kernels back to back."""
+
+    def __init__(self, torch):
+        self.torch = torch
+
+    def time(self, fn, reps):
+        t = self.torch
+        g = t.cuda.CUDAGraph()
+        t.cuda.synchronize()
+        with t.cuda.graph(g):
+            for i in range(reps):
+                fn(i)
+        g.replay()                                # upload + untimed first replay
+        t.cuda.synchronize()
+        a = t.cuda.Event(enable_timing=True)
+        b = t.cuda.Event(enable_timing=True)
+        st = t.cuda.current_stream()
+        a.record(st)
+        g.replay()
+        b.record(st)
+        t.cuda.synchronize()
+        ms = a.elapsed_time(b) / reps
+        del g
+        return ms                                 # ms per call
 
 
 def conv_flop(N, Ci, Co, Ho, Wo, T):
@@ -139,30 +174,30 @@ def bench_conv(args, torch, cfg_key):
     db = torch.empty((Co,), dtype=torch.float32, device="cuda:0")
     nws = hx.hexconv_bwd_weight_workspace(N, Ci, Co, H, W, k, s, hx.HEX_F32 if esz == 4 else hx.HEX_BF16)
     ws = torch.empty(max(nws, 1), dtype=torch.uint8, device="cuda:0")
-    stream = torch.cuda.current_stream()
-
+    # the binding enqueues on torch's current stream (the capture stream
+    # while a graph is being captured)
     def fwd(i):
         z = sets[i % nsets]
-        hx.hexconv_fwd(z["x"], w, bias, z["y"], k, s, stream=stream)
+        hx.hexconv_fwd(z["x"], w, bias, z["y"], k, s)
 
     def bwd_data(i):
         z = sets[i % nsets]
-        hx.hexconv_bwd_data(z["dy"], w, z["dx"], k, s, stream=stream)
+        hx.hexconv_bwd_data(z["dy"], w, z["dx"], k, s)
 
     def bwd_weight(i):
         z = sets[i % nsets]
-        hx.hexconv_bwd_weight(z["x"], z["dy"], dw, db, ws, k, s, stream=stream)
+        hx.hexconv_bwd_weight(z["x"], z["dy"], dw, db, ws, k, s)
 
     def step(i):
         fwd(i)
         bwd_data(i)
         bwd_weight(i)
 
-    timer = Timer(torch, stream)
+    timer = EagerTimer(torch) if args.eager else GraphTimer(torch)
     for i in range(args.warmup):
         step(i)
     torch.cuda.synchronize()
-    ms_step = timer.run(step, args.steps)
+    ms_step = timer.time(step, args.steps)
 
     # per-op launch durations, each op alone over the same rotation
     ops = {}
@@ -172,9 +207,7 @@ def bench_conv(args, torch, cfg_key):
         "bwd_weight": esz * (N * Ci * H * W + N * Co * Ho * Wo) + 4 * (Co * Ci * T + Co),
     }
     for name, fn in (("fwd", fwd), ("bwd_data", bwd_data), ("bwd_weight", bwd_weight)):
-        for i in range(max(3, args.warmup // 2)):
-            fn(i)
-        ms = timer.run(fn, args.steps)
+        ms = timer.time(fn, args.steps)
         ops[name] = dict(ms=ms, gbs=bytes_alg[name] / (ms * 1e-3) / 1e9)
     flop_op = conv_flop(N, Ci, Co, Ho, Wo, T)
     flop_step = 3 * flop_op
@@ -225,10 +258,12 @@ KERNEL_NAMES = {}
 def main():
     p = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     p.add_argument("--gpus", type=int, default=1)
-    p.add_argument("--steps", type=int, default=200)
+    p.add_argument("--steps", type=int, default=500)
     p.add_argument("--warmup", type=int, default=20)
     p.add_argument("--config", default="c2", choices=["c2", "c4"])
     p.add_argument("--no-cpu-baseline", action="store_true")
+    p.add_argument("--eager", action="store_true",
+                   help="launch eagerly instead of replaying a HIP graph (for counter runs)")
     p.add_argument("--cpu-seconds", type=float, default=12.0)
     args = p.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:

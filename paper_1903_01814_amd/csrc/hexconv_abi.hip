@@ -71,6 +71,29 @@ bool force_generic()
     return v != nullptr && strcmp(v, "generic") == 0;
 }
 
+// Weight-gradient kernel family for a shape; the workspace query and the
+// call must agree, so both go through this choice.
+enum class WgradPath { Generic, SmallF32 };
+
+WgradPath wgrad_path(const ConvShape &sh, Dtype d)
+{
+    if (force_generic())
+        return WgradPath::Generic;
+    if (d == hexk::F32 && hexk::smallc_f32_wgrad_ok(sh))
+        return WgradPath::SmallF32;
+    return WgradPath::Generic;
+}
+
+size_t wgrad_workspace(const ConvShape &sh, Dtype d)
+{
+    switch (wgrad_path(sh, d)) {
+    case WgradPath::SmallF32:
+        return hexk::smallc_f32_wgrad_workspace(sh);
+    default:
+        return hexk::wgrad_generic_workspace(sh);
+    }
+}
+
 } // namespace
 
 extern "C" {
@@ -127,7 +150,13 @@ int hexconv_fwd(const void *x, const void *w, const void *bias, void *y, int N, 
     hipStream_t st = static_cast<hipStream_t>(stream);
     const bool relu = (flags & HEX_FLAG_RELU) != 0;
     const Dtype d = static_cast<Dtype>(dt);
-    (void)force_generic;
+    if (!force_generic()) {
+        if (d == hexk::F32 && hexk::smallc_f32_fwd_ok(sh))
+            return launched(hexk::smallc_f32_fwd(static_cast<const float *>(x),
+                                                 static_cast<const float *>(w),
+                                                 static_cast<const float *>(bias),
+                                                 static_cast<float *>(y), sh, relu, st));
+    }
     return launched(hexk::conv_fwd_generic(x, w, bias, y, sh, d, relu, st));
 }
 
@@ -146,6 +175,12 @@ int hexconv_bwd_data(const void *dy, const void *w, void *dx, int N, int C_in, i
         return HEX_ERR_INVALID_ARG;
     hipStream_t st = static_cast<hipStream_t>(stream);
     const Dtype d = static_cast<Dtype>(dt);
+    if (!force_generic() && sh.Ho > 0) {
+        if (d == hexk::F32 && hexk::smallc_f32_bwd_data_ok(sh))
+            return launched(hexk::smallc_f32_bwd_data(static_cast<const float *>(dy),
+                                                      static_cast<const float *>(w),
+                                                      static_cast<float *>(dx), sh, st));
+    }
     return launched(hexk::conv_bwd_data_generic(dy, w, dx, sh, d, st));
 }
 
@@ -157,7 +192,7 @@ size_t hexconv_bwd_weight_workspace(int N, int C_in, int C_out, int H, int W, in
         return 0;
     if (N == 0 || sh.Ho == 0)
         return 0;
-    return hexk::wgrad_generic_workspace(sh);
+    return wgrad_workspace(sh, static_cast<Dtype>(dt));
 }
 
 int hexconv_bwd_weight(const void *x, const void *dy, float *dw, float *db, void *ws,
@@ -173,14 +208,21 @@ int hexconv_bwd_weight(const void *x, const void *dy, float *dw, float *db, void
     const bool empty = (N == 0 || sh.Ho == 0);
     if (!empty && (x == nullptr || dy == nullptr))
         return HEX_ERR_INVALID_ARG;
-    const size_t need = empty ? 0 : hexk::wgrad_generic_workspace(sh);
+    const Dtype d = static_cast<Dtype>(dt);
+    const size_t need = empty ? 0 : wgrad_workspace(sh, d);
     if (need > 0 && (ws == nullptr || ws_bytes < need))
         return HEX_ERR_INVALID_ARG;
     hipStream_t st = static_cast<hipStream_t>(stream);
     if (empty)
         return launched(hexk::fill_zero_f32(dw, db, sh, st));
-    const Dtype d = static_cast<Dtype>(dt);
-    return launched(hexk::wgrad_generic(x, dy, dw, db, ws, sh, d, st));
+    switch (wgrad_path(sh, d)) {
+    case WgradPath::SmallF32:
+        return launched(hexk::smallc_f32_wgrad(static_cast<const float *>(x),
+                                               static_cast<const float *>(dy), dw, db, ws, sh,
+                                               st));
+    default:
+        return launched(hexk::wgrad_generic(x, dy, dw, db, ws, sh, d, st));
+    }
 }
 
 int hexpool_fwd(const void *x, void *y, uint8_t *argmax_tap, int N, int C, int H, int W, int k,

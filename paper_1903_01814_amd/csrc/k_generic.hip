@@ -7,13 +7,14 @@
 // tensor) staged channel by channel in LDS as float.
 // Conv backward-data: gather form -- each input pixel looks up, per tap, the
 // output whose window reads it (a lattice test for strides > 1).
-// Weight gradient: per-chunk partial sums in a fixed tree order, then a
-// reduction kernel over chunks (deterministic).
+// Weight gradient: per-chunk partial sums in a fixed tree order, then the
+// fixed-order reduction over chunks of k_reduce.hip (deterministic).
 // Pool forward / backward: one output (input) element per thread.
 #include <algorithm>
 
 #include "hexdev.h"
 #include "kernels.h"
+#include "stage.h"
 
 namespace hexk {
 namespace {
@@ -65,13 +66,8 @@ __global__ __launch_bounds__(kThreads) void conv_fwd_generic_k(
     const size_t HW = static_cast<size_t>(sh.H) * sh.W;
     for (int ci = 0; ci < sh.Ci; ++ci) {
         __syncthreads();
-        const T *plane = x + (static_cast<size_t>(n) * sh.Ci + ci) * HW;
-        for (int e = threadIdx.x; e < RH * RW; e += kThreads) {
-            const int r = r_lo + e / RW, c = c_lo + e % RW;
-            region[e] = (r >= 0 && r < sh.H && c >= 0 && c < sh.W)
-                            ? to_f(plane[static_cast<size_t>(r) * sh.W + c])
-                            : 0.f;
-        }
+        stage_window<8>(region, x + (static_cast<size_t>(n) * sh.Ci + ci) * HW, sh.H, sh.W, r_lo,
+                        c_lo, RH, RW);
         __syncthreads();
         if (active) {
             for (int t = 0; t < sh.T; ++t) {
@@ -146,8 +142,8 @@ __global__ __launch_bounds__(kThreads) void conv_bwd_data_generic_k(
 
 template <typename T>
 __global__ __launch_bounds__(kThreads) void wgrad_partial_generic_k(
-    const T *__restrict__ x, const T *__restrict__ dy, float *__restrict__ part_w,
-    float *__restrict__ part_b, ConvShape sh, int chunk)
+    const T *__restrict__ x, const T *__restrict__ dy, float *__restrict__ part, ConvShape sh,
+    int chunk)
 {
     __shared__ TapLds tl;
     __shared__ float red[kTapGroup + 1][kThreads];
@@ -201,12 +197,13 @@ __global__ __launch_bounds__(kThreads) void wgrad_partial_generic_k(
             }
         }
         __syncthreads();
-        const size_t EW = static_cast<size_t>(sh.Co) * sh.Ci * sh.T;
+        // partial layout [e][chunk], e = co * (Ci*T + 1) + col
+        const size_t Jt = static_cast<size_t>(sh.Ci) * sh.T + 1;
         if (threadIdx.x < kTapGroup && tg + threadIdx.x < sh.T)
-            part_w[blockIdx.x * EW + (static_cast<size_t>(co) * sh.Ci + ci) * sh.T + tg + threadIdx.x] =
-                red[threadIdx.x][0];
+            part[(co * Jt + static_cast<size_t>(ci) * sh.T + tg + threadIdx.x) * gridDim.x +
+                 blockIdx.x] = red[threadIdx.x][0];
         if (tg == 0 && do_bias && threadIdx.x == 0)
-            part_b[static_cast<size_t>(blockIdx.x) * sh.Co + co] = red[kTapGroup][0];
+            part[(co * Jt + Jt - 1) * gridDim.x + blockIdx.x] = red[kTapGroup][0];
         __syncthreads();
     }
 }
@@ -219,25 +216,6 @@ __global__ __launch_bounds__(kThreads) void fill_zero_k(float *__restrict__ a, i
         a[e] = 0.f;
     else if (b != nullptr && e < na + nb)
         b[e - na] = 0.f;
-}
-
-__global__ __launch_bounds__(kThreads) void wgrad_reduce_k(
-    const float *__restrict__ part_w, const float *__restrict__ part_b,
-    float *__restrict__ dw, float *__restrict__ db, int nchunks, int EW, int Co)
-{
-    const int e = blockIdx.x * kThreads + threadIdx.x;
-    if (e < EW) {
-        float s = 0.f;
-        for (int c = 0; c < nchunks; ++c)
-            s += part_w[static_cast<size_t>(c) * EW + e];
-        dw[e] = s;
-    } else if (db != nullptr && e < EW + Co) {
-        const int co = e - EW;
-        float s = 0.f;
-        for (int c = 0; c < nchunks; ++c)
-            s += part_b[static_cast<size_t>(c) * Co + co];
-        db[co] = s;
-    }
 }
 
 template <typename T, int MODE>
@@ -398,23 +376,18 @@ hipError_t wgrad_generic(const void *x, const void *dy, float *dw, float *db, vo
 {
     int chunk;
     const int nchunks = wgrad_generic_chunks(sh, chunk);
-    const size_t EW = static_cast<size_t>(sh.Co) * sh.Ci * sh.T;
-    float *part_w = static_cast<float *>(ws);
-    float *part_b = part_w + static_cast<size_t>(nchunks) * EW;
+    float *part = static_cast<float *>(ws);
     dim3 grid(nchunks, sh.Co, sh.Ci);
     if (dt == F32)
         hipLaunchKernelGGL(wgrad_partial_generic_k<float>, grid, dim3(kThreads), 0, st,
-                           (const float *)x, (const float *)dy, part_w, part_b, sh, chunk);
+                           (const float *)x, (const float *)dy, part, sh, chunk);
     else
         hipLaunchKernelGGL(wgrad_partial_generic_k<bf16raw>, grid, dim3(kThreads), 0, st,
-                           (const bf16raw *)x, (const bf16raw *)dy, part_w, part_b, sh, chunk);
+                           (const bf16raw *)x, (const bf16raw *)dy, part, sh, chunk);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess)
         return e;
-    hipLaunchKernelGGL(wgrad_reduce_k, dim3(cdiv(static_cast<long>(EW) + sh.Co, kThreads)),
-                       dim3(kThreads), 0, st, part_w, part_b, dw, db, nchunks,
-                       static_cast<int>(EW), sh.Co);
-    return hipGetLastError();
+    return reduce_partials(part, nchunks, sh.Co, sh.Ci * sh.T, dw, db, st);
 }
 
 hipError_t fill_zero_f32(float *dw, float *db, const ConvShape &sh, hipStream_t st)

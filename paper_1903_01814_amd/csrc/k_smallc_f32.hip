@@ -1,0 +1,668 @@
+// k_smallc_f32.hip -- float32 kernels for few input channels at stride 1
+// (camera images: C_in*T <= 64).
+//
+// All three kernels stage their input tile (all channels, one batched pass)
+// into the sheared LDS layout of shear.h, where a hexagonal tap (dq, ds) is
+// the constant offset dq*P + ds from its centre for both column parities.
+// The forward and weight-gradient kernels are persistent: each block walks a
+// strided list of tiles and loads the next tile's input into registers while
+// it computes and stores the current one (weights are loaded once).
+//
+// Forward: implicit GEMM on the fp32 matrix cores.  For 16 consecutive
+// pixels of a tile, D[pixel][co] = sum_k A[pixel][k] * B[k][co] with
+// k = (ci, tap): A is read from LDS at centre + offset(k), B (weights) stays
+// in registers.  v_mfma_f32_16x16x4_f32 lane layout:
+//   a = A[lane % 16][lane / 16], b = B[lane / 16][lane % 16],
+//   d[j] = D[4 * (lane / 16) + j][lane % 16],
+// so each lane stores 4 consecutive pixels of one channel (16-byte store).
+//
+// Backward-data: at stride 1 the adjoint is a forward convolution of dy
+// with the point-reflected kernel (tap t <-> T-1-t) and C_in/C_out swapped.
+// With one or two output channels it is a matrix-vector product, so it runs
+// on the VALU: each thread owns R consecutive rows of one column; the
+// neighbourhood columns are contiguous runs in the sheared layout, read
+// once per input channel and reused by all taps of that column.
+//
+// Weight gradient: D[co][(ci,t)] = sum_pixels dy[co][p] * x[ci][p + tap t]
+// on the fp32 matrix cores with the pixels as the contraction index, so the
+// reduction over pixels happens inside the MFMA; an extra B column of ones
+// yields db.  Per-block partial sums are written to the workspace and added
+// in a fixed order by k_reduce.hip (deterministic).
+#include <algorithm>
+
+#include "hexdev.h"
+#include "kernels.h"
+#include "shear.h"
+
+namespace hexk {
+namespace {
+
+using namespace hexgeom;
+
+typedef float floatx4 __attribute__((ext_vector_type(4)));
+
+constexpr int kThreads = 256;
+constexpr int kWaves = kThreads / 64;
+
+// Blocks are handed to the 8 XCDs round-robin; give each XCD a contiguous
+// range of tiles so neighbouring tiles (shared halo rows) meet in one L2.
+__device__ __forceinline__ int xcd_remap(int b, int nb)
+{
+    constexpr int X = 8;
+    const int per = nb / X, rem = nb % X;
+    const int xcd = b % X, idx = b / X;
+    return xcd * per + min(xcd, rem) + idx;
+}
+
+// Tiling of the output plane (= input plane at stride 1) into TR x TW tiles.
+struct Tiling {
+    int TR, TW, tiles_c, tiles_per_img, ntiles, P, CS;
+    FastDiv fdw;  // division by TW
+    FastDiv fdtr; // division by TR
+    FastDiv fdlr; // division by TR + 2k (staged window rows)
+};
+
+struct TileOrigin {
+    int n, r0, c0, rows, cols;
+};
+
+__device__ __forceinline__ TileOrigin tile_of(int b, const Tiling &tg, const ConvShape &sh)
+{
+    TileOrigin o;
+    o.n = b / tg.tiles_per_img;
+    const int tt = b - o.n * tg.tiles_per_img;
+    const int tr = tt / tg.tiles_c;
+    o.r0 = tr * tg.TR;
+    o.c0 = (tt - tr * tg.tiles_c) * tg.TW;
+    o.rows = min(tg.TR, sh.H - o.r0);
+    o.cols = min(tg.TW, sh.W - o.c0);
+    return o;
+}
+
+__device__ __forceinline__ ShearTile window_of(const TileOrigin &o, const Tiling &tg, int K)
+{
+    return ShearTile{o.r0 - K, o.c0 - K, o.rows + 2 * K, o.cols + 2 * K, tg.P, tg.CS};
+}
+
+// Row-major copy of a tile of `nch` planes (no halo) staged through
+// registers: dst[ch * dstride + pr * TW + pc].  Work split: one 4-column group
+// per thread, (channel, row) pairs strided by blockDim / groups.
+template <int U> struct PlainPrefetch {
+    float v[U][4];
+    int da[U];
+    bool full;
+    int pc, cols;
+
+    __host__ __device__ static int groups(int TW) { return (TW + 3) / 4; }
+    __host__ __device__ static int rows_per_thread(int nch, int TR, int TW, int nt)
+    {
+        const int rstep = nt / groups(TW);
+        return rstep > 0 ? (nch * TR + rstep - 1) / rstep : 1 << 30;
+    }
+
+    __device__ __forceinline__ void load(const float *__restrict__ src, size_t src_plane,
+                                         int nch, int W, const TileOrigin &o, int TW, int dstride,
+                                         const FastDiv &fdtr, int TR)
+    {
+        const int ng = groups(TW);
+        const int rstep = blockDim.x / ng;
+        const int g = threadIdx.x % ng, fr0 = threadIdx.x / ng;
+        pc = 4 * g;
+        cols = o.cols;
+        full = pc + 3 < o.cols;
+        const int total = nch * TR;
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            const int fr = fr0 + u * rstep;
+            const int ch = static_cast<int>(fdiv(static_cast<uint32_t>(fr), fdtr));
+            const int pr = fr - ch * TR;
+            const bool ok = fr0 < rstep && fr < total && pr < o.rows && pc < o.cols;
+            da[u] = ok ? ch * dstride + pr * TW + pc : -1;
+            const float *row =
+                src + (ok ? ch * src_plane + static_cast<size_t>(o.r0 + pr) * W + o.c0 : 0);
+            if (full) {
+                Vec4Load<float>::load(row + (ok ? pc : 0), v[u]);
+            } else {
+#pragma unroll
+                for (int j = 0; j < 4; ++j)
+                    v[u][j] = row[(ok && pc + j < o.cols) ? pc + j : 0];
+            }
+        }
+    }
+
+    __device__ __forceinline__ void commit(float *__restrict__ dst) const
+    {
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            if (da[u] >= 0) {
+#pragma unroll
+                for (int j = 0; j < 4; ++j)
+                    if (pc + j < cols)
+                        dst[da[u] + j] = v[u][j];
+            }
+        }
+    }
+};
+
+// --------------------------------------------------------------- forward
+
+template <int K, int KS, int U>
+__global__ __launch_bounds__(kThreads) void fwd_f32_k(
+    const float *__restrict__ x, const float *__restrict__ w, const float *__restrict__ bias,
+    float *__restrict__ y, ConvShape sh, int relu, Tiling tg, int vec4)
+{
+    constexpr int T = num_taps(K);
+    extern __shared__ float xs[];
+    const size_t HW = static_cast<size_t>(sh.H) * sh.W;
+
+    // per-lane weights and tap offsets, loaded once per block
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int m = lane & 15, kq = lane >> 4;
+    const int co = blockIdx.y * 16 + m; // B and D column of this lane
+    int off[KS]; // LDS offset of k from the centre (may be negative)
+    bool kval[KS];
+    float bw[KS];
+#pragma unroll
+    for (int s = 0; s < KS; ++s) {
+        const int kk = kq + 4 * s;
+        off[s] = 0;
+        bw[s] = 0.f;
+        kval[s] = kk < sh.Ci * T;
+        if (kval[s]) {
+            const int ci = kk / T, t = kk - ci * T;
+            int dq = 0, ds = 0;
+            tap_axial(K, t, dq, ds);
+            off[s] = ci * tg.CS + dq * tg.P + ds;
+            if (co < sh.Co)
+                bw[s] = w[(static_cast<size_t>(co) * sh.Ci + ci) * T + t];
+        }
+    }
+    const float bco = (bias != nullptr && co < sh.Co) ? bias[co] : 0.f;
+
+    ShearPrefetch<U> pf;
+    int t = blockIdx.x;
+    if (t < tg.ntiles) {
+        const TileOrigin o = tile_of(t, tg, sh);
+        pf.load(x + static_cast<size_t>(o.n) * sh.Ci * HW, HW, sh.Ci, sh.H, sh.W,
+                window_of(o, tg, K), tg.TR + 2 * K, tg.fdlr);
+    }
+    for (; t < tg.ntiles; t += gridDim.x) {
+        const TileOrigin o = tile_of(t, tg, sh);
+        const ShearTile tl = window_of(o, tg, K);
+        __syncthreads(); // previous tile's reads of xs are done
+        pf.commit(xs);
+        __syncthreads();
+        const int tn = t + gridDim.x;
+        if (tn < tg.ntiles) {
+            const TileOrigin on = tile_of(tn, tg, sh);
+            pf.load(x + static_cast<size_t>(on.n) * sh.Ci * HW, HW, sh.Ci, sh.H, sh.W,
+                    window_of(on, tg, K), tg.TR + 2 * K, tg.fdlr);
+        }
+
+        const int nslot = o.rows * tg.TW;
+        const int ntile = (nslot + 15) / 16;
+        float *yb = y + (static_cast<size_t>(o.n) * sh.Co + co) * HW;
+        for (int mt = wave; mt < ntile; mt += kWaves) {
+            // A row of this lane: pixel slot p of the tile
+            const int p = mt * 16 + m;
+            const int pr = static_cast<int>(fdiv(p, tg.fdw));
+            const int pc = p - pr * tg.TW;
+            const bool pv = pr < o.rows && pc < o.cols;
+            // every read is issued (address clamped to 0 for padding lanes) so
+            // the KS reads overlap; padding values are then replaced by zero
+            const int centre = pv ? tl.addr(o.r0 + pr, o.c0 + pc) : 0;
+            float a[KS];
+#pragma unroll
+            for (int s = 0; s < KS; ++s)
+                a[s] = xs[(pv && kval[s]) ? centre + off[s] : 0];
+            floatx4 acc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+            for (int s = 0; s < KS; ++s)
+                acc = __builtin_amdgcn_mfma_f32_16x16x4f32((pv && kval[s]) ? a[s] : 0.f, bw[s],
+                                                           acc, 0, 0, 0);
+            if (co >= sh.Co)
+                continue;
+            // D rows of this lane: slots q0..q0+3 (same tile row since TW % 4 == 0)
+            const int q0 = mt * 16 + 4 * kq;
+            const int qr = static_cast<int>(fdiv(q0, tg.fdw));
+            const int qc = q0 - qr * tg.TW;
+            if (qr >= o.rows)
+                continue;
+            float v[4];
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                v[j] = acc[j] + bco;
+                if (relu)
+                    v[j] = fmaxf(v[j], 0.f);
+            }
+            float *dst = yb + static_cast<size_t>(o.r0 + qr) * sh.W + o.c0 + qc;
+            if (vec4 && qc + 3 < o.cols) {
+                *reinterpret_cast<float4 *>(dst) = make_float4(v[0], v[1], v[2], v[3]);
+            } else {
+#pragma unroll
+                for (int j = 0; j < 4; ++j)
+                    if (qc + j < o.cols)
+                        dst[j] = v[j];
+            }
+        }
+    }
+}
+
+// --------------------------------------------------------- backward-data
+
+// dx[n][oc][p] = sum_ic sum_u w[ic][oc][T-1-u] * dy[n][ic][p + tap u]
+// (ic runs over C_out, oc over C_in).  Thread = column c, rows
+// [strip*R, strip*R + R) of the tile; one output channel per block.
+template <int K, int R>
+__global__ __launch_bounds__(kThreads) void bwd_data_f32_k(
+    const float *__restrict__ dy, const float *__restrict__ w, float *__restrict__ dx,
+    ConvShape sh, Tiling tg, int ic_chunk, int vec4)
+{
+    constexpr int T = num_taps(K);
+    extern __shared__ float ds_[];
+    const TileOrigin o = tile_of(xcd_remap(blockIdx.x, gridDim.x), tg, sh);
+    const ShearTile tl = window_of(o, tg, K);
+    const int cs = tl.chan_stride();
+    const int oc = blockIdx.y;
+    const int ICN = sh.Co, OCN = sh.Ci;
+    const size_t HW = static_cast<size_t>(sh.H) * sh.W;
+
+    const int lc = threadIdx.x % tg.TW, strip = threadIdx.x / tg.TW;
+    const int S = tg.TR / R;
+    const bool active = strip < S && lc < o.cols && strip * R < o.rows;
+    // centre address of the strip's first row (valid for active threads)
+    const int a0 = active ? tl.addr(o.r0 + strip * R, o.c0 + lc) : 0;
+
+    float acc[R];
+#pragma unroll
+    for (int r = 0; r < R; ++r)
+        acc[r] = 0.f;
+
+    for (int ic0 = 0; ic0 < ICN; ic0 += ic_chunk) {
+        const int icn = min(ic_chunk, ICN - ic0);
+        if (ic0 > 0)
+            __syncthreads();
+        stage_shear<8>(ds_, dy + (static_cast<size_t>(o.n) * ICN + ic0) * HW, HW, icn, sh.H,
+                       sh.W, tl, tg.TR + 2 * K, tg.fdlr, vec4 != 0);
+        __syncthreads();
+        if (!active)
+            continue;
+        for (int icl = 0; icl < icn; ++icl) {
+            const int ic = ic0 + icl;
+            const float *wr = w + (static_cast<size_t>(ic) * OCN + oc) * T;
+            const float *src = ds_ + icl * cs + a0;
+            int t0 = 0;
+#pragma unroll
+            for (int dq = -K; dq <= K; ++dq) {
+                const int len = 2 * K + 1 - (dq < 0 ? -dq : dq);
+                const int dslo = dq < 0 ? -K - dq : -K;
+                const float *col = src + dq * tg.P + dslo;
+                float v[R + 2 * K];
+#pragma unroll
+                for (int j = 0; j < R + 2 * K; ++j)
+                    if (j < R + len - 1)
+                        v[j] = col[j];
+#pragma unroll
+                for (int u = 0; u < 2 * K + 1; ++u) {
+                    if (u < len) {
+                        const float wv = wr[T - 1 - (t0 + u)];
+#pragma unroll
+                        for (int r = 0; r < R; ++r)
+                            acc[r] += wv * v[r + u];
+                    }
+                }
+                t0 += len;
+            }
+        }
+    }
+    if (!active)
+        return;
+    float *dst = dx + (static_cast<size_t>(o.n) * OCN + oc) * HW + o.c0 + lc;
+#pragma unroll
+    for (int r = 0; r < R; ++r) {
+        const int row = strip * R + r;
+        if (row < o.rows)
+            dst[static_cast<size_t>(o.r0 + row) * sh.W] = acc[r];
+    }
+}
+
+// -------------------------------------------------------- weight gradient
+
+template <int K, int NT, int UX, int UD>
+__global__ __launch_bounds__(kThreads) void wgrad_f32_k(
+    const float *__restrict__ x, const float *__restrict__ dy, float *__restrict__ part,
+    ConvShape sh, Tiling tg, int dstride)
+{
+    constexpr int T = num_taps(K);
+    extern __shared__ float lds[];
+    const int b = blockIdx.x; // partial slot
+    float *xs = lds;                      // [Ci][CS]
+    float *dys = xs + sh.Ci * tg.CS;      // [16][dstride], pitch TW
+    float *red = dys + 16 * dstride;      // [kWaves][16][NT * 16]
+    const int mt = blockIdx.y;            // 16 output channels
+    const int nco = min(16, sh.Co - mt * 16);
+    const size_t HW = static_cast<size_t>(sh.H) * sh.W;
+
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int m = lane & 15, kq = lane >> 4;
+    const int J = sh.Ci * T; // tap columns; column J is the bias column
+    int off[NT];  // LDS offset of the tap from the centre (may be negative)
+    int kind[NT]; // 0: tap column, 1: ones (bias column), 2: unused
+#pragma unroll
+    for (int j = 0; j < NT; ++j) {
+        const int col = j * 16 + m;
+        off[j] = 0;
+        kind[j] = col < J ? 0 : (col == J ? 1 : 2);
+        if (col < J) {
+            const int ci = col / T, t = col - ci * T;
+            int dq = 0, ds = 0;
+            tap_axial(K, t, dq, ds);
+            off[j] = ci * tg.CS + dq * tg.P + ds;
+        }
+    }
+    const bool arow = m < nco; // A row (output channel) present
+
+    floatx4 acc[NT];
+#pragma unroll
+    for (int j = 0; j < NT; ++j)
+        acc[j] = floatx4{0.f, 0.f, 0.f, 0.f};
+
+    ShearPrefetch<UX> px;
+    PlainPrefetch<UD> pd;
+    int t = b;
+    if (t < tg.ntiles) {
+        const TileOrigin o = tile_of(t, tg, sh);
+        px.load(x + static_cast<size_t>(o.n) * sh.Ci * HW, HW, sh.Ci, sh.H, sh.W,
+                window_of(o, tg, K), tg.TR + 2 * K, tg.fdlr);
+        pd.load(dy + (static_cast<size_t>(o.n) * sh.Co + mt * 16) * HW, HW, nco, sh.W, o, tg.TW,
+                dstride, tg.fdtr, tg.TR);
+    }
+    for (; t < tg.ntiles; t += gridDim.x) {
+        const TileOrigin o = tile_of(t, tg, sh);
+        const ShearTile tl = window_of(o, tg, K);
+        __syncthreads();
+        px.commit(xs);
+        pd.commit(dys);
+        __syncthreads();
+        const int tn = t + gridDim.x;
+        if (tn < tg.ntiles) {
+            const TileOrigin on = tile_of(tn, tg, sh);
+            px.load(x + static_cast<size_t>(on.n) * sh.Ci * HW, HW, sh.Ci, sh.H, sh.W,
+                    window_of(on, tg, K), tg.TR + 2 * K, tg.fdlr);
+            pd.load(dy + (static_cast<size_t>(on.n) * sh.Co + mt * 16) * HW, HW, nco, sh.W, on,
+                    tg.TW, dstride, tg.fdtr, tg.TR);
+        }
+        const int nslot = o.rows * tg.TW;
+        const int nks = (nslot + 3) / 4;
+        for (int ks = wave; ks < nks; ks += kWaves) {
+            const int p = ks * 4 + kq;
+            const int pr = static_cast<int>(fdiv(p, tg.fdw));
+            const int pc = p - pr * tg.TW;
+            const bool pv = pr < o.rows && pc < o.cols;
+            // reads issued unconditionally (clamped addresses), then masked
+            float a = dys[(pv && arow) ? m * dstride + p : 0];
+            a = (pv && arow) ? a : 0.f;
+            const int centre = pv ? tl.addr(o.r0 + pr, o.c0 + pc) : 0;
+            float bx[NT];
+#pragma unroll
+            for (int j = 0; j < NT; ++j)
+                bx[j] = xs[(pv && kind[j] == 0) ? centre + off[j] : 0];
+#pragma unroll
+            for (int j = 0; j < NT; ++j) {
+                const float bv = !pv ? 0.f : (kind[j] == 0 ? bx[j] : (kind[j] == 1 ? 1.f : 0.f));
+                acc[j] = __builtin_amdgcn_mfma_f32_16x16x4f32(a, bv, acc[j], 0, 0, 0);
+            }
+        }
+    }
+    // sum the waves' D tiles in a fixed order, write this block's partial
+    __syncthreads();
+#pragma unroll
+    for (int j = 0; j < NT; ++j)
+#pragma unroll
+        for (int q = 0; q < 4; ++q)
+            red[(wave * 16 + 4 * kq + q) * (NT * 16) + j * 16 + m] = acc[j][q];
+    __syncthreads();
+    const int Jt = J + 1;
+    for (int e = threadIdx.x; e < 16 * Jt; e += kThreads) {
+        const int row = e / Jt, col = e - row * Jt;
+        float s = 0.f;
+        for (int wv = 0; wv < kWaves; ++wv)
+            s += red[(wv * 16 + row) * (NT * 16) + col];
+        const int cog = mt * 16 + row;
+        if (row < nco)
+            part[(static_cast<size_t>(cog) * Jt + col) * gridDim.x + b] = s;
+    }
+}
+
+inline int cdiv(long a, long b) { return static_cast<int>((a + b - 1) / b); }
+
+constexpr size_t kLdsLimit = 64 * 1024;
+
+// sheared column stride for a window of LR rows
+int shear_pitch(int LR) { return LR + 1; }
+
+// Output tiles: full rows when W <= 128, else 128-column tiles; about
+// `target` pixels per block.
+Tiling make_tiling(const ConvShape &sh, int target)
+{
+    Tiling tg;
+    tg.TW = std::min(sh.W, 128);
+    tg.TW = (tg.TW + 3) / 4 * 4; // 16-byte aligned rows within the tile
+    tg.TR = std::max(1, std::min(sh.H, target / tg.TW));
+    tg.tiles_c = cdiv(sh.W, tg.TW);
+    tg.tiles_per_img = tg.tiles_c * cdiv(sh.H, tg.TR);
+    tg.ntiles = tg.tiles_per_img * sh.N;
+    tg.P = shear_pitch(tg.TR + 2 * sh.k);
+    tg.CS = (tg.TW + 2 * sh.k) * tg.P;
+    tg.fdw = make_fastdiv(static_cast<uint32_t>(tg.TW));
+    tg.fdtr = make_fastdiv(static_cast<uint32_t>(tg.TR));
+    tg.fdlr = make_fastdiv(static_cast<uint32_t>(tg.TR + 2 * sh.k));
+    return tg;
+}
+
+size_t shear_bytes(const ConvShape &sh, const Tiling &tg, int nch)
+{
+    return sizeof(float) * static_cast<size_t>(nch) * (tg.TW + 2 * sh.k) * tg.P;
+}
+
+int wgrad_nt(const ConvShape &sh)
+{
+    const int NT = cdiv(sh.Ci * sh.T + 1, 16);
+    return NT <= 1 ? 1 : (NT <= 2 ? 2 : 4);
+}
+
+int wgrad_dstride(const Tiling &tg)
+{
+    // >= TR*TW and == 2 mod 32: conflict-free A reads (16 channels x 4 pixels)
+    const int need = tg.TR * tg.TW;
+    return (need + 29) / 32 * 32 + 2;
+}
+
+size_t wgrad_lds(const ConvShape &sh, const Tiling &tg)
+{
+    return shear_bytes(sh, tg, sh.Ci) +
+           sizeof(float) * (16 * static_cast<size_t>(wgrad_dstride(tg)) +
+                            kWaves * 16 * wgrad_nt(sh) * 16);
+}
+
+constexpr int kFwdTarget = 320;
+constexpr int kWgradTarget = 320;
+constexpr int kBwdR = 4;
+constexpr int kFwdBlocks = 1024;   // persistent grid caps
+constexpr int kWgradBlocks = 512;
+
+// prefetch depth (float4 per thread) for a sheared window, 0 if too deep
+int shear_depth(const ConvShape &sh, const Tiling &tg, int nch)
+{
+    if (ShearPrefetch<1>::groups(tg.TW + 2 * sh.k) > kThreads)
+        return 0;
+    const int r = ShearPrefetch<1>::rows_per_thread(nch, tg.TR + 2 * sh.k, tg.TW + 2 * sh.k,
+                                                    kThreads);
+    return r <= 1 ? 1 : r <= 2 ? 2 : r <= 4 ? 4 : r <= 8 ? 8 : 0;
+}
+
+int plain_depth(const Tiling &tg, int nch)
+{
+    if (PlainPrefetch<1>::groups(tg.TW) > kThreads)
+        return 0;
+    const int r = PlainPrefetch<1>::rows_per_thread(nch, tg.TR, tg.TW, kThreads);
+    return r <= 2 ? 2 : r <= 4 ? 4 : r <= 8 ? 8 : r <= 12 ? 12 : 0;
+}
+
+Tiling bwd_tiling(const ConvShape &sh)
+{
+    Tiling tg;
+    tg.TW = std::min(sh.W, 64);
+    const int S = std::max(1, kThreads / tg.TW);
+    tg.TR = S * kBwdR;
+    tg.tiles_c = cdiv(sh.W, tg.TW);
+    tg.tiles_per_img = tg.tiles_c * cdiv(sh.H, tg.TR);
+    tg.ntiles = tg.tiles_per_img * sh.N;
+    tg.P = shear_pitch(tg.TR + 2 * sh.k);
+    tg.CS = (tg.TW + 2 * sh.k) * tg.P;
+    tg.fdw = make_fastdiv(static_cast<uint32_t>(tg.TW));
+    tg.fdtr = make_fastdiv(static_cast<uint32_t>(tg.TR));
+    tg.fdlr = make_fastdiv(static_cast<uint32_t>(tg.TR + 2 * sh.k));
+    return tg;
+}
+
+int bwd_ic_chunk(const ConvShape &sh, const Tiling &tg)
+{
+    const size_t per = shear_bytes(sh, tg, 1);
+    const int fit = static_cast<int>(std::max<size_t>(1, (48 * 1024) / per));
+    return std::min(sh.Co, fit);
+}
+
+} // namespace
+
+// ------------------------------------------------------------- launchers
+
+bool smallc_f32_fwd_ok(const ConvShape &sh)
+{
+    if (sh.s != 1 || (sh.k != 1 && sh.k != 2) || sh.Ci * sh.T > 64 || sh.W % 4 != 0)
+        return false;
+    const Tiling tg = make_tiling(sh, kFwdTarget);
+    return shear_bytes(sh, tg, sh.Ci) <= kLdsLimit && shear_depth(sh, tg, sh.Ci) > 0;
+}
+
+hipError_t smallc_f32_fwd(const float *x, const float *w, const float *b, float *y,
+                          const ConvShape &sh, bool relu, hipStream_t st)
+{
+    const Tiling tg = make_tiling(sh, kFwdTarget);
+    const int KS = cdiv(sh.Ci * sh.T, 4);
+    const int U = shear_depth(sh, tg, sh.Ci);
+    dim3 grid(std::min(tg.ntiles, kFwdBlocks), cdiv(sh.Co, 16));
+    const size_t lds = shear_bytes(sh, tg, sh.Ci);
+#define HEX_FWD_F32(KV, KSV, UV)                                                             \
+    hipLaunchKernelGGL((fwd_f32_k<KV, KSV, UV>), grid, dim3(kThreads), lds, st, x, w, b, y,  \
+                       sh, relu ? 1 : 0, tg, 1)
+#define HEX_FWD_F32_U(KV, KSV)                                                               \
+    do {                                                                                     \
+        if (U == 1) HEX_FWD_F32(KV, KSV, 1);                                                 \
+        else if (U == 2) HEX_FWD_F32(KV, KSV, 2);                                            \
+        else if (U == 4) HEX_FWD_F32(KV, KSV, 4);                                            \
+        else HEX_FWD_F32(KV, KSV, 8);                                                        \
+    } while (0)
+    if (sh.k == 1) {
+        if (KS <= 2) HEX_FWD_F32_U(1, 2);
+        else if (KS <= 4) HEX_FWD_F32_U(1, 4);
+        else if (KS <= 8) HEX_FWD_F32_U(1, 8);
+        else HEX_FWD_F32_U(1, 16);
+    } else {
+        if (KS <= 5) HEX_FWD_F32_U(2, 5);
+        else if (KS <= 10) HEX_FWD_F32_U(2, 10);
+        else HEX_FWD_F32_U(2, 16);
+    }
+#undef HEX_FWD_F32_U
+#undef HEX_FWD_F32
+    return hipGetLastError();
+}
+
+bool smallc_f32_bwd_data_ok(const ConvShape &sh)
+{
+    return sh.s == 1 && (sh.k == 1 || sh.k == 2) && sh.Ci <= 4 &&
+           shear_bytes(sh, bwd_tiling(sh), 1) <= kLdsLimit;
+}
+
+hipError_t smallc_f32_bwd_data(const float *dy, const float *w, float *dx, const ConvShape &sh,
+                               hipStream_t st)
+{
+    const Tiling tg = bwd_tiling(sh);
+    const int ic_chunk = bwd_ic_chunk(sh, tg);
+    const size_t lds = shear_bytes(sh, tg, ic_chunk);
+    const int vec4 = (sh.W % 4 == 0) ? 1 : 0;
+    dim3 grid(tg.ntiles, sh.Ci);
+    if (sh.k == 1)
+        hipLaunchKernelGGL((bwd_data_f32_k<1, kBwdR>), grid, dim3(kThreads), lds, st, dy, w, dx,
+                           sh, tg, ic_chunk, vec4);
+    else
+        hipLaunchKernelGGL((bwd_data_f32_k<2, kBwdR>), grid, dim3(kThreads), lds, st, dy, w, dx,
+                           sh, tg, ic_chunk, vec4);
+    return hipGetLastError();
+}
+
+namespace {
+int wgrad_grid(const Tiling &tg) { return std::min(tg.ntiles, kWgradBlocks); }
+} // namespace
+
+bool smallc_f32_wgrad_ok(const ConvShape &sh)
+{
+    if (sh.s != 1 || (sh.k != 1 && sh.k != 2) || sh.Ci * sh.T + 1 > 64 || sh.W % 4 != 0)
+        return false;
+    const Tiling tg = make_tiling(sh, kWgradTarget);
+    return wgrad_lds(sh, tg) <= kLdsLimit && shear_depth(sh, tg, sh.Ci) > 0 &&
+           plain_depth(tg, 16) > 0;
+}
+
+size_t smallc_f32_wgrad_workspace(const ConvShape &sh)
+{
+    const Tiling tg = make_tiling(sh, kWgradTarget);
+    return sizeof(float) * static_cast<size_t>(wgrad_grid(tg)) * sh.Co * (sh.Ci * sh.T + 1);
+}
+
+hipError_t smallc_f32_wgrad(const float *x, const float *dy, float *dw, float *db, void *ws,
+                            const ConvShape &sh, hipStream_t st)
+{
+    const Tiling tg = make_tiling(sh, kWgradTarget);
+    const int nparts = wgrad_grid(tg);
+    const int NT = wgrad_nt(sh);
+    const int UX = shear_depth(sh, tg, sh.Ci);
+    const int UD = plain_depth(tg, 16);
+    const int dstride = wgrad_dstride(tg);
+    float *part = static_cast<float *>(ws);
+    dim3 grid(nparts, cdiv(sh.Co, 16));
+    const size_t lds = wgrad_lds(sh, tg);
+#define HEX_WG(KV, NTV, UXV, UDV)                                                            \
+    hipLaunchKernelGGL((wgrad_f32_k<KV, NTV, UXV, UDV>), grid, dim3(kThreads), lds, st, x, dy, \
+                       part, sh, tg, dstride)
+#define HEX_WG_UD(KV, NTV, UXV)                                                              \
+    do {                                                                                     \
+        if (UD <= 4) HEX_WG(KV, NTV, UXV, 4);                                                \
+        else if (UD <= 8) HEX_WG(KV, NTV, UXV, 8);                                           \
+        else HEX_WG(KV, NTV, UXV, 12);                                                       \
+    } while (0)
+#define HEX_WG_UX(KV, NTV)                                                                   \
+    do {                                                                                     \
+        if (UX <= 2) HEX_WG_UD(KV, NTV, 2);                                                  \
+        else if (UX <= 4) HEX_WG_UD(KV, NTV, 4);                                             \
+        else HEX_WG_UD(KV, NTV, 8);                                                          \
+    } while (0)
+    if (sh.k == 1) {
+        if (NT == 1) HEX_WG_UX(1, 1);
+        else if (NT == 2) HEX_WG_UX(1, 2);
+        else HEX_WG_UX(1, 4);
+    } else {
+        if (NT == 1) HEX_WG_UX(2, 1);
+        else if (NT == 2) HEX_WG_UX(2, 2);
+        else HEX_WG_UX(2, 4);
+    }
+#undef HEX_WG_UX
+#undef HEX_WG_UD
+#undef HEX_WG
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess)
+        return e;
+    return reduce_partials(part, nparts, sh.Co, sh.Ci * sh.T, dw, db, st);
+}
+
+} // namespace hexk

@@ -18,6 +18,12 @@ struct ConvShape {
     int N, Ci, Co, H, W, k, s, Ho, Wo, T;
 };
 
+// Sum weight-gradient partials laid out [e][slot], e = co*(J+1) + col
+// (col < J: dw[co][col]; col == J: db[co], skipped when db is null), in a
+// fixed order.  J = C_in * T.
+hipError_t reduce_partials(const float *part, int nparts, int Co, int J, float *dw, float *db,
+                           hipStream_t st);
+
 // ---- generic kernels: any k, stride, channel count and dtype -----------
 hipError_t conv_fwd_generic(const void *x, const void *w, const void *b,
                             void *y, const ConvShape &sh, Dtype dt, bool relu,
@@ -37,5 +43,17 @@ hipError_t pool_fwd_generic(const void *x, void *y, uint8_t *am,
 hipError_t pool_bwd_generic(const void *dy, const uint8_t *am,
                             const void *relu_y, void *dx, const ConvShape &sh,
                             int mode, Dtype dt, hipStream_t st);
+
+// ---- float32, few input channels (C_in*T <= 64), stride 1 -------------
+bool smallc_f32_fwd_ok(const ConvShape &sh);
+hipError_t smallc_f32_fwd(const float *x, const float *w, const float *b, float *y,
+                          const ConvShape &sh, bool relu, hipStream_t st);
+bool smallc_f32_bwd_data_ok(const ConvShape &sh);
+hipError_t smallc_f32_bwd_data(const float *dy, const float *w, float *dx, const ConvShape &sh,
+                               hipStream_t st);
+bool smallc_f32_wgrad_ok(const ConvShape &sh);
+size_t smallc_f32_wgrad_workspace(const ConvShape &sh);
+hipError_t smallc_f32_wgrad(const float *x, const float *dy, float *dw, float *db, void *ws,
+                            const ConvShape &sh, hipStream_t st);
 
 } // namespace hexk

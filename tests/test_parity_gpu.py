@@ -363,3 +363,55 @@ def test_specialised_matches_generic(dt, monkeypatch):
         monkeypatch.delenv("HEXCONV_PATH")
         mag = oracle.conv_fwd(np.abs(x), np.abs(w), None, k, 1) if dt == "bf16" else None
         check(dt, y_fast, y_gen, mag, "fast vs generic")
+
+
+@pytest.mark.parametrize("dt", ["f32", "bf16"])
+def test_graph_replay_matches_eager(dt):
+    """The library's launches captured into a HIP graph give, on every
+    replay, the same bits as eager calls (outputs are poisoned and other
+    eager work runs between replays)."""
+    torch = torch_mod()
+    rng = np.random.default_rng(21)
+    cases = [(8, 1, 16, 40, 40, 2), (2, 32, 64, 24, 24, 2)]
+    for (N, Ci, Co, H, W, k) in cases:
+        T = hx.hex_num_taps(k)
+        Ho, Wo = hx.hex_out_shape(H, W, 1)
+        x = to_dev(gen.round_to(rng.normal(size=(N, Ci, H, W)), dt), dt)
+        w = to_dev(gen.round_to(rng.normal(size=(Co, Ci, T)) * 0.1, dt), dt)
+        b = to_dev(gen.round_to(rng.normal(size=Co) * 0.1, dt), dt)
+        dy = to_dev(gen.round_to(rng.normal(size=(N, Co, Ho, Wo)), dt), dt)
+        y = empty((N, Co, Ho, Wo), dt)
+        dx = empty((N, Ci, H, W), dt)
+        dw = torch.empty((Co, Ci, T), dtype=torch.float32, device="cuda:0")
+        db = torch.empty((Co,), dtype=torch.float32, device="cuda:0")
+        yp = empty((N, Co, *hx.hex_out_shape(Ho, Wo, 2)), dt)
+        am = torch.empty(yp.shape, dtype=torch.uint8, device="cuda:0")
+        dxp = empty((N, Co, Ho, Wo), dt)
+        nws = hx.hexconv_bwd_weight_workspace(N, Ci, Co, H, W, k, 1,
+                                              hx.HEX_F32 if dt == "f32" else hx.HEX_BF16)
+        ws = torch.empty(max(nws, 1), dtype=torch.uint8, device="cuda:0")
+
+        def calls():
+            hx.hexconv_fwd(x, w, b, y, k, 1)
+            hx.hexconv_bwd_data(dy, w, dx, k, 1)
+            hx.hexconv_bwd_weight(x, dy, dw, db, ws, k, 1)
+            hx.hexpool_fwd(y, yp, am, 1, 2, hx.HEX_POOL_MAX)
+            hx.hexpool_bwd(yp, am, y, dxp, 1, 2, hx.HEX_POOL_MAX)
+
+        outs = (y, dx, dw, db, yp, am, dxp)
+        calls()
+        torch.cuda.synchronize()
+        ref = [o.clone() for o in outs]
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g):
+            calls()
+        scratch = empty((N, Co, Ho, Wo), dt)
+        for rep in range(3):
+            for o in outs:
+                o.fill_(7)
+            hx.hexconv_fwd(x, w, None, scratch, k, 1)        # unrelated eager work
+            torch.cuda.synchronize()
+            g.replay()
+            torch.cuda.synchronize()
+            for o, r in zip(outs, ref):
+                assert torch.equal(o, r), "replay %d differs" % rep
