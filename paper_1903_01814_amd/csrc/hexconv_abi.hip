@@ -156,6 +156,8 @@ int hexconv_fwd(const void *x, const void *w, const void *bias, void *y, int N, 
                                                  static_cast<const float *>(w),
                                                  static_cast<const float *>(bias),
                                                  static_cast<float *>(y), sh, relu, st));
+        if (d == hexk::BF16 && hexk::bf16_wide_ok(sh, sh.Ci, sh.Co))
+            return launched(hexk::bf16_wide_conv(x, w, bias, y, sh, false, relu, st));
     }
     return launched(hexk::conv_fwd_generic(x, w, bias, y, sh, d, relu, st));
 }
@@ -180,6 +182,8 @@ int hexconv_bwd_data(const void *dy, const void *w, void *dx, int N, int C_in, i
             return launched(hexk::smallc_f32_bwd_data(static_cast<const float *>(dy),
                                                       static_cast<const float *>(w),
                                                       static_cast<float *>(dx), sh, st));
+        if (d == hexk::BF16 && hexk::bf16_wide_ok(sh, sh.Co, sh.Ci))
+            return launched(hexk::bf16_wide_conv(dy, w, nullptr, dx, sh, true, false, st));
     }
     return launched(hexk::conv_bwd_data_generic(dy, w, dx, sh, d, st));
 }

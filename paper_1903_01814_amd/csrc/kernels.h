@@ -56,4 +56,11 @@ size_t smallc_f32_wgrad_workspace(const ConvShape &sh);
 hipError_t smallc_f32_wgrad(const float *x, const float *dy, float *dw, float *db, void *ws,
                             const ConvShape &sh, hipStream_t st);
 
+// ---- bf16 matrix-core convolution, input channels a multiple of 32 -----
+// forward (reflect = false: IC = C_in, OC = C_out) or stride-1 data
+// gradient (reflect = true: IC = C_out, OC = C_in)
+bool bf16_wide_ok(const ConvShape &sh, int IC, int OC);
+hipError_t bf16_wide_conv(const void *in, const void *w, const void *bias, void *out,
+                          const ConvShape &sh, bool reflect, bool relu, hipStream_t st);
+
 } // namespace hexk
