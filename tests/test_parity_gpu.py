@@ -254,7 +254,8 @@ SWEEP = [
     (2, 8, 8, 20, 21, 1, 1), (1, 16, 16, 18, 19, 2, 1), (1, 33, 17, 10, 14, 1, 1),
     (1, 64, 64, 12, 12, 1, 1), (1, 32, 64, 24, 24, 2, 1), (1, 1, 32, 48, 48, 2, 1),
     (2, 64, 16, 9, 70, 1, 1), (1, 7, 9, 6, 40, 2, 2), (1, 1, 1, 1, 1, 1, 1),
-    (1, 2, 2, 2, 9, 4, 2),
+    (1, 2, 2, 2, 9, 4, 2), (3, 3, 24, 37, 8, 2, 1), (1, 2, 70, 5, 256, 1, 1),
+    (2, 48, 40, 11, 32, 2, 1),
 ]
 
 
