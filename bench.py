@@ -4,9 +4,10 @@
 Default workload (the headline metric's configuration): camera-shaped hex
 convolution, fp32, N=256 images of 40x40 (hexagonal 1027-pixel footprint,
 log-normal x Bernoulli(0.1) amplitudes), 1 -> 16 channels, kernel size 2
-(19 taps), stride 1.  One step = forward + backward-data + backward-weight
-(with bias gradient) over one batch.  Value = effective GFLOP/s counting
-2*N*H_out*W_out*C_in*C_out*T per op (hex taps only).
+(19 taps), stride 1.  One step = forward, then both gradients (data, and
+weight with bias) through the combined backward entry point, over one batch.
+Value = effective GFLOP/s counting 2*N*H_out*W_out*C_in*C_out*T for each of
+the three products (hex taps only).
 
 Inputs are resident in HBM before timing starts.  The K timed steps are
 captured once into a HIP graph and replayed (after W eager warm-up steps and
@@ -172,13 +173,19 @@ def bench_conv(args, torch, cfg_key):
             bias = dev(torch, d["b"], dt)
     dw = torch.empty((Co, Ci, T), dtype=torch.float32, device="cuda:0")
     db = torch.empty((Co,), dtype=torch.float32, device="cuda:0")
-    nws = hx.hexconv_bwd_weight_workspace(N, Ci, Co, H, W, k, s, hx.HEX_F32 if esz == 4 else hx.HEX_BF16)
+    dtc = hx.HEX_F32 if esz == 4 else hx.HEX_BF16
+    nws = max(hx.hexconv_bwd_weight_workspace(N, Ci, Co, H, W, k, s, dtc),
+              hx.hexconv_bwd_workspace(N, Ci, Co, H, W, k, s, dtc))
     ws = torch.empty(max(nws, 1), dtype=torch.uint8, device="cuda:0")
     # the binding enqueues on torch's current stream (the capture stream
     # while a graph is being captured)
     def fwd(i):
         z = sets[i % nsets]
         hx.hexconv_fwd(z["x"], w, bias, z["y"], k, s)
+
+    def bwd(i):
+        z = sets[i % nsets]
+        hx.hexconv_bwd(z["x"], z["dy"], w, z["dx"], dw, db, ws, k, s)
 
     def bwd_data(i):
         z = sets[i % nsets]
@@ -190,8 +197,7 @@ def bench_conv(args, torch, cfg_key):
 
     def step(i):
         fwd(i)
-        bwd_data(i)
-        bwd_weight(i)
+        bwd(i)
 
     timer = EagerTimer(torch) if args.eager else GraphTimer(torch)
     for i in range(args.warmup):
@@ -199,21 +205,28 @@ def bench_conv(args, torch, cfg_key):
     torch.cuda.synchronize()
     ms_step = timer.time(step, args.steps)
 
-    # per-op launch durations, each op alone over the same rotation
+    # per-op durations, each op alone over the same rotation (HIP events on
+    # the launch stream); the step uses fwd and bwd, the separate gradient
+    # entry points are timed for reference
     ops = {}
+    x_b, y_b = esz * N * Ci * H * W, esz * N * Co * Ho * Wo
+    w_b, b_b, g_b = esz * Co * Ci * T, esz * Co, 4 * (Co * Ci * T + Co)
     bytes_alg = {
-        "fwd": esz * (N * Ci * H * W + Co * Ci * T + Co + N * Co * Ho * Wo),
-        "bwd_data": esz * (N * Co * Ho * Wo + Co * Ci * T + N * Ci * H * W),
-        "bwd_weight": esz * (N * Ci * H * W + N * Co * Ho * Wo) + 4 * (Co * Ci * T + Co),
+        "fwd": x_b + w_b + b_b + y_b,
+        "bwd": x_b + y_b + w_b + x_b + g_b,          # x, dy, w -> dx, dw, db
+        "bwd_data": y_b + w_b + x_b,
+        "bwd_weight": x_b + y_b + g_b,
     }
-    for name, fn in (("fwd", fwd), ("bwd_data", bwd_data), ("bwd_weight", bwd_weight)):
+    nprod = {"fwd": 1, "bwd": 2, "bwd_data": 1, "bwd_weight": 1}
+    for name, fn in (("fwd", fwd), ("bwd", bwd), ("bwd_data", bwd_data),
+                     ("bwd_weight", bwd_weight)):
         ms = timer.time(fn, args.steps)
         ops[name] = dict(ms=ms, gbs=bytes_alg[name] / (ms * 1e-3) / 1e9)
     flop_op = conv_flop(N, Ci, Co, Ho, Wo, T)
     flop_step = 3 * flop_op
     value = flop_step / (ms_step * 1e-3) / 1e9
 
-    dom = max(ops, key=lambda n: ops[n]["ms"])
+    dom = max(("fwd", "bwd"), key=lambda n: ops[n]["ms"])
     bound = "hbm" if cfg["dtype"] == gen.F32 or Ci * T < 64 else "mfma"
     kernel_name = KERNEL_NAMES.get((cfg_key, dom), dom)
     if bound == "hbm":
@@ -221,7 +234,7 @@ def bench_conv(args, torch, cfg_key):
         roof = dict(bound="hbm", achieved=round(achieved, 1), peak=HBM_PEAK_GBS, unit="GB/s",
                     frac=round(achieved / HBM_PEAK_GBS, 4))
     else:
-        achieved = flop_op / (ops[dom]["ms"] * 1e-3) / 1e12
+        achieved = nprod[dom] * flop_op / (ops[dom]["ms"] * 1e-3) / 1e12
         roof = dict(bound="mfma", achieved=round(achieved, 2), peak=BF16_MFMA_PEAK_TFLOPS,
                     unit="TFLOP/s", frac=round(achieved / BF16_MFMA_PEAK_TFLOPS, 4))
     roof["kernel"] = kernel_name
@@ -237,7 +250,7 @@ def bench_conv(args, torch, cfg_key):
                     taps=T, H_out=Ho, W_out=Wo, rotating_batches=nsets),
         samples_per_s=round(N / (ms_step * 1e-3), 1),
         per_op={n: dict(ms=round(v["ms"], 5), alg_GBps=round(v["gbs"], 1),
-                        GFLOPs=round(flop_op / (v["ms"] * 1e-3) / 1e9, 1))
+                        GFLOPs=round(nprod[n] * flop_op / (v["ms"] * 1e-3) / 1e9, 1))
                 for n, v in ops.items()},
         roofline=roof,
     )

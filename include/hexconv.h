@@ -132,6 +132,27 @@ int hexconv_bwd_weight(const void *x, const void *dy, float *dw, float *db,
                        int H, int W, int k, int stride, hex_dtype dt,
                        void *stream);
 
+/* Bytes of device workspace hexconv_bwd needs for these sizes (0 for
+ * invalid arguments). */
+size_t hexconv_bwd_workspace(int N, int C_in, int C_out, int H, int W, int k,
+                             int stride, hex_dtype dt);
+
+/*
+ * Both gradients of one convolution layer in one call (Sec. 2.4: the
+ * backward pass of a hexagonal layer): the results of hexconv_bwd_data
+ * (written to dx) and of hexconv_bwd_weight (dw, db), for the same
+ * arguments.  dx may be NULL (first layer: no data gradient); w may then be
+ * NULL too.  db is nullable.  ws: at least hexconv_bwd_workspace(...) bytes.
+ * Where a fused kernel exists for the shape (float32, few channels, stride
+ * 1) dy is read from memory once for both results; otherwise the two
+ * gradients are computed one after the other.  Every argument is checked
+ * before anything is enqueued.  Deterministic, like hexconv_bwd_weight.
+ */
+int hexconv_bwd(const void *x, const void *dy, const void *w, void *dx,
+                float *dw, float *db, void *ws, size_t ws_bytes, int N,
+                int C_in, int C_out, int H, int W, int k, int stride,
+                hex_dtype dt, void *stream);
+
 /*
  * Pooling (Sec. 2.4) over the windows of hexconv_fwd, per channel:
  *   max: y = value of the first maximal tap (padding counts as 0);

@@ -1,6 +1,7 @@
 // hexconv_abi.hip -- the extern "C" entry points declared in hexconv.h:
 // argument validation (host only, before anything is enqueued), choice of
 // kernel per shape regime, and launch-status mapping.
+#include <atomic>
 #include <stdint.h>
 #include <stdlib.h>
 #include <string.h>
@@ -8,6 +9,31 @@
 #include "../../include/hexconv.h"
 #include "hexgeom.h"
 #include "kernels.h"
+
+namespace hexk {
+
+int device_cus()
+{
+    constexpr int kMaxDev = 64;
+    static std::atomic<int> cache[kMaxDev];
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0)
+        return 256;
+    if (dev < kMaxDev) {
+        const int c = cache[dev].load(std::memory_order_relaxed);
+        if (c > 0)
+            return c;
+    }
+    int cus = 0;
+    if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+        cus <= 0)
+        cus = 256;
+    if (dev < kMaxDev)
+        cache[dev].store(cus, std::memory_order_relaxed);
+    return cus;
+}
+
+} // namespace hexk
 
 namespace {
 
@@ -84,6 +110,12 @@ WgradPath wgrad_path(const ConvShape &sh, Dtype d)
     if (d == hexk::BF16 && hexk::bf16_wgrad_ok(sh))
         return WgradPath::Bf16Mfma;
     return WgradPath::Generic;
+}
+
+// Fused data + weight gradient (hexconv_bwd) for this shape?
+bool bwd_fused(const ConvShape &sh, Dtype d)
+{
+    return !force_generic() && d == hexk::F32 && hexk::smallc_f32_bwd_fused_ok(sh);
 }
 
 size_t wgrad_workspace(const ConvShape &sh, Dtype d)
@@ -233,6 +265,54 @@ int hexconv_bwd_weight(const void *x, const void *dy, float *dw, float *db, void
     default:
         return launched(hexk::wgrad_generic(x, dy, dw, db, ws, sh, d, st));
     }
+}
+
+size_t hexconv_bwd_workspace(int N, int C_in, int C_out, int H, int W, int k, int stride,
+                             hex_dtype dt)
+{
+    ConvShape sh;
+    if (check_shape(N, C_in, C_out, H, W, k, stride, dt, sh) != HEX_OK)
+        return 0;
+    if (N == 0 || sh.Ho == 0)
+        return 0;
+    const Dtype d = static_cast<Dtype>(dt);
+    return bwd_fused(sh, d) ? hexk::smallc_f32_bwd_fused_workspace(sh) : wgrad_workspace(sh, d);
+}
+
+int hexconv_bwd(const void *x, const void *dy, const void *w, void *dx, float *dw, float *db,
+                void *ws, size_t ws_bytes, int N, int C_in, int C_out, int H, int W, int k,
+                int stride, hex_dtype dt, void *stream)
+{
+    ConvShape sh;
+    int rc = check_shape(N, C_in, C_out, H, W, k, stride, dt, sh);
+    if (rc != HEX_OK)
+        return rc;
+    // every check of both gradients first, so that a bad argument enqueues nothing
+    if ((rc = ptrs_ok({dw}, {x, dy, w, dx, db, ws})) != HEX_OK)
+        return rc;
+    const bool empty = (N == 0 || sh.Ho == 0);
+    if (!empty && (x == nullptr || dy == nullptr))
+        return HEX_ERR_INVALID_ARG;
+    if (dx != nullptr && w == nullptr)
+        return HEX_ERR_INVALID_ARG;
+    const Dtype d = static_cast<Dtype>(dt);
+    const bool fused = !empty && bwd_fused(sh, d);
+    const size_t need =
+        empty ? 0 : (fused ? hexk::smallc_f32_bwd_fused_workspace(sh) : wgrad_workspace(sh, d));
+    if (need > 0 && (ws == nullptr || ws_bytes < need))
+        return HEX_ERR_INVALID_ARG;
+    hipStream_t st = static_cast<hipStream_t>(stream);
+    if (fused)
+        return launched(hexk::smallc_f32_bwd_fused(
+            static_cast<const float *>(x), static_cast<const float *>(dy),
+            static_cast<const float *>(w), static_cast<float *>(dx), dw, db, ws, sh, st));
+    if (dx != nullptr && N > 0) {
+        rc = hexconv_bwd_data(dy, w, dx, N, C_in, C_out, H, W, k, stride, dt, stream);
+        if (rc != HEX_OK)
+            return rc;
+    }
+    return hexconv_bwd_weight(x, dy, dw, db, ws, ws_bytes, N, C_in, C_out, H, W, k, stride, dt,
+                              stream);
 }
 
 int hexpool_fwd(const void *x, void *y, uint8_t *argmax_tap, int N, int C, int H, int W, int k,

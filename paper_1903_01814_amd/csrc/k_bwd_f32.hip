@@ -1,0 +1,475 @@
+// k_bwd_f32.hip -- both gradients of a float32 layer with few input
+// channels (camera images) in one pass over dy.
+//
+//   dx[n][ci][p] = sum_co sum_t w[co][ci][T-1-t] * dy[n][co][p + tap t]
+//   dw[co][ci][t] = sum_n sum_p dy[n][co][p] * x[n][ci][p + tap t]
+//   db[co]        = sum_n sum_p dy[n][co][p]
+// (stride 1: the data gradient is the convolution of dy with the
+// point-reflected kernel, t <-> T-1-t).
+//
+// A tile is TR = 8 full-width rows of one image.  All C_out planes of dy and
+// the C_in planes of x are staged into LDS in the sheared column-major layout
+// (shear.h): element (r, c) of the window at (c - c_lo) * P + (r - r_lo) -
+// (floor(c/2) - floor(c_lo/2)), P = TR + 2k + 1, so that a tap (dq, ds) is
+// the parity-free offset dq * P + ds and a column is a run of consecutive
+// words.  TR and k are compile-time constants, so every offset inside a tile
+// is an instruction immediate.  The k halo columns are zeroed once per block;
+// rows outside the image are staged as zeros.  The next tile's loads are in
+// flight in registers while the current one is computed.
+//
+// Weight gradient on the fp32 matrix cores (v_mfma_f32_16x16x4f32,
+// a = A[lane % 16][lane / 16], b = B[lane / 16][lane % 16]): M = output
+// channels, N = (ci, t) plus a ones column for db, K = pixels, 4 consecutive
+// rows of one column per step.  Lanes without a channel or a tap read from a
+// plane of zeros, the bias column from a plane of ones, so the inner loop has
+// no selects.  Accumulators stay in registers for the whole kernel; each
+// block writes one partial sum per output element (reduced in a fixed order).
+//
+// Data gradient on the VALU: thread = (column, group of CG output channels),
+// all TR rows of the column; each tap column (fixed dq) is a run of
+// consecutive words, loaded once per channel and reused by all its taps.  The
+// channel groups' partial sums are added in LDS in a fixed order.
+#include <algorithm>
+
+#include "hexdev.h"
+#include "kernels.h"
+#include "shear.h" // FastDiv
+
+namespace hexk {
+namespace {
+
+using namespace hexgeom;
+
+typedef float floatx4 __attribute__((ext_vector_type(4)));
+
+constexpr int kThreads = 256;
+constexpr int kWaves = kThreads / 64;
+constexpr int kTR = 8; // rows per tile
+
+template <int K> struct Geo {
+    static constexpr int LR = kTR + 2 * K; // window rows
+    static constexpr int P = LR + 1;       // column pitch
+    // word of window element (r_local = r - r0, c) relative to the channel
+    // base: (c + K) * P + (r_local + K) - floor(c/2) + floor(-K/2)
+    __host__ __device__ static constexpr int colbase(int c) { return (c + K) * P - (c >> 1) - 1; }
+};
+
+struct BwdTiling {
+    int W4;            // float4 groups per row
+    int CS;            // LDS words per x channel and per constant plane
+    int CSD;           // LDS words per dy channel
+    int xo, zo, oo;    // LDS offsets: x planes, zeros plane, ones plane
+    int G;             // output-channel groups of the data gradient
+    int tiles_per_img, ntiles;
+    int nitems;        // float4 staging items per tile
+    int dxp;           // LDS offset of the data-gradient partials
+    int wl;            // LDS offset of the reflected weights
+    int dummy;         // LDS offset of a 4-word sink for dead staging items
+    FastDiv fdw4, fdlr;
+};
+
+// One tile's dy and x rows in registers: item i = tid + u * 256 is
+// (channel, window row, float4 column group).  The LDS word of an item and
+// its element offset inside the image do not depend on the tile, so they are
+// computed once (pk: LDS word | window row << 16 | dy item << 24 | live << 25).
+template <int K, int U> struct Stage {
+    float4 v[U];
+    int pk[U], goff[U];
+
+    __device__ __forceinline__ void init(const ConvShape &sh, const BwdTiling &bt)
+    {
+        using G = Geo<K>;
+        const int HW = sh.H * sh.W;
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            const int i = threadIdx.x + u * kThreads;
+            const int q = static_cast<int>(fdiv(static_cast<uint32_t>(i), bt.fdw4));
+            const int c4 = i - q * bt.W4;
+            const int ch = static_cast<int>(fdiv(static_cast<uint32_t>(q), bt.fdlr));
+            const int rr = q - ch * G::LR;
+            const bool live = i < bt.nitems;
+            const bool isdy = ch < sh.Co;
+            const int base = isdy ? ch * bt.CSD : bt.xo + (ch - sh.Co) * bt.CS;
+            const int dst = live ? base + G::colbase(4 * c4) + rr : bt.dummy;
+            pk[u] = dst | (rr << 16) | (isdy ? 1 << 24 : 0) | (live ? 1 << 25 : 0);
+            goff[u] = (isdy ? ch : ch - sh.Co) * HW + rr * sh.W + 4 * c4;
+        }
+    }
+
+    __device__ __forceinline__ void load(const float *__restrict__ x, const float *__restrict__ dy,
+                                         const ConvShape &sh, int n, int r0)
+    {
+        const size_t HW = static_cast<size_t>(sh.H) * sh.W;
+        // row r0 - K of image n, channel 0: items add their offsets to it
+        const long rofs = static_cast<long>(r0 - K) * sh.W;
+        const float *dyn = dy + static_cast<size_t>(n) * sh.Co * HW + rofs;
+        const float *xn = x + static_cast<size_t>(n) * sh.Ci * HW + rofs;
+        const int rlo = K - r0, rhi = sh.H - r0 + K; // window rows inside the image
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            const int rr = (pk[u] >> 16) & 0xff;
+            const bool ok = ((pk[u] >> 25) & 1) && rr >= rlo && rr < rhi;
+            const float *b = ((pk[u] >> 24) & 1) ? dyn : xn;
+            const float4 q4 = *reinterpret_cast<const float4 *>(ok ? b + goff[u] : x);
+            v[u] = ok ? q4 : make_float4(0.f, 0.f, 0.f, 0.f);
+        }
+    }
+
+    // columns 4c4 .. 4c4+3 of a row sit at +0, +P, +2P-1, +3P-1
+    __device__ __forceinline__ void commit(float *__restrict__ lds) const
+    {
+        using G = Geo<K>;
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            float *d = lds + (pk[u] & 0xffff);
+            d[0] = v[u].x;
+            d[G::P] = v[u].y;
+            d[2 * G::P - 1] = v[u].z;
+            d[3 * G::P - 1] = v[u].w;
+        }
+    }
+};
+
+#ifndef HEX_BWD_WPE
+#define HEX_BWD_WPE 2
+#endif
+
+template <int K, int CI, int MT, int NT, int CG, int U>
+__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(HEX_BWD_WPE, 8)))
+void bwd_f32_k(const float *__restrict__ x, const float *__restrict__ dy, const float *__restrict__ w,
+               float *__restrict__ dx, float *__restrict__ part, ConvShape sh, BwdTiling bt,
+               int do_dx)
+{
+    using Gm = Geo<K>;
+    constexpr int T = num_taps(K);
+    constexpr int J = CI * T; // tap columns; column J is the bias column
+    constexpr int P = Gm::P;
+    extern __shared__ __align__(16) float lds[];
+    float *dxp = lds + bt.dxp; // [G][CI][TR][W]
+    float *wl = lds + bt.wl;   // [C_out + 1][CI][T], reflected taps; row C_out = 0
+    const int W = sh.W, Co = sh.Co;
+    const int tid = threadIdx.x;
+    const int lane = tid & 63, wave = tid >> 6;
+    const int m = lane & 15, kq = lane >> 4;
+
+    // weight gradient operands of this lane (word offsets from a pixel)
+    int abase[MT];
+#pragma unroll
+    for (int i = 0; i < MT; ++i)
+        abase[i] = i * 16 + m < Co ? (i * 16 + m) * bt.CSD : bt.zo;
+    int bbase[NT];
+#pragma unroll
+    for (int j = 0; j < NT; ++j) {
+        const int col = j * 16 + m;
+        bbase[j] = col == J ? bt.oo : bt.zo;
+        if (col < J) {
+            const int ci = col / T, t = col - ci * T;
+            int dq = 0, ds = 0;
+            tap_axial(K, t, dq, ds);
+            bbase[j] = bt.xo + ci * bt.CS + dq * P + ds;
+        }
+    }
+    // K-steps of this wave: pixel quads (column c0w + 2i, rows 4 * (wave & 1) + 0..3)
+    const int c0w = wave >> 1;
+    const int p0 = Gm::colbase(c0w) + K + 4 * (wave & 1) + kq;
+    constexpr int PSTEP = 2 * P - 1; // two columns further
+    const int nsteps = (W - c0w + 1) / 2;
+    const int per = (nsteps + CG - 1) / CG + 1 & ~1; // steps per channel iteration, even
+    floatx4 acc[2][MT][NT];
+#pragma unroll
+    for (int h = 0; h < 2; ++h)
+#pragma unroll
+        for (int i = 0; i < MT; ++i)
+#pragma unroll
+            for (int j = 0; j < NT; ++j)
+                acc[h][i][j] = floatx4{0.f, 0.f, 0.f, 0.f};
+    // one K-step: 4 pixels of this wave's quad i into accumulator set h
+    auto kstep = [&](int i, int h) {
+        const int pa = p0 + i * PSTEP;
+        float a[MT], b[NT];
+#pragma unroll
+        for (int ii = 0; ii < MT; ++ii)
+            a[ii] = lds[abase[ii] + pa];
+#pragma unroll
+        for (int j = 0; j < NT; ++j)
+            b[j] = lds[bbase[j] + pa];
+#pragma unroll
+        for (int j = 0; j < NT; ++j)
+#pragma unroll
+            for (int ii = 0; ii < MT; ++ii)
+                acc[h][ii][j] =
+                    __builtin_amdgcn_mfma_f32_16x16x4f32(a[ii], b[j], acc[h][ii][j], 0, 0, 0);
+    };
+
+    // data gradient: this thread's column and channel group
+    const bool dxthr = do_dx != 0 && tid < bt.G * W;
+    const int g = dxthr ? tid / W : 0;
+    const int c = dxthr ? tid - g * W : 0;
+    const int cbase = Gm::colbase(c) + K; // word of (row r0, column c)
+
+    // the first tile's loads are in flight during the one-time set-up
+    Stage<K, U> stg;
+    stg.init(sh, bt);
+    int tile = blockIdx.x;
+    if (tile < bt.ntiles) {
+        const int n = tile / bt.tiles_per_img;
+        stg.load(x, dy, sh, n, (tile - n * bt.tiles_per_img) * kTR);
+    }
+
+    // once per block: zero halo columns of every channel, the zeros plane,
+    // the ones plane, the reflected weights
+    {
+        const int nch = Co + CI;
+        for (int e = tid; e < nch * 2 * K * Gm::LR; e += kThreads) {
+            const int rr = e % Gm::LR, rest = e / Gm::LR;
+            const int side = rest % (2 * K), ch = rest / (2 * K);
+            const int cc = side < K ? side - K : W + side - K;
+            const int base = ch < Co ? ch * bt.CSD : bt.xo + (ch - Co) * bt.CS;
+            lds[base + Gm::colbase(cc) + rr] = 0.f;
+        }
+        for (int e = tid; e < bt.CS; e += kThreads) {
+            lds[bt.zo + e] = 0.f;
+            lds[bt.oo + e] = 1.f;
+        }
+        for (int e = tid; e < (Co + 1) * CI * T; e += kThreads) {
+            const int co = e / (CI * T), rem = e - co * (CI * T);
+            const int ci = rem / T, t = rem - ci * T;
+            wl[e] = co < Co ? w[(static_cast<size_t>(co) * CI + ci) * T + (T - 1 - t)] : 0.f;
+        }
+    }
+
+    for (; tile < bt.ntiles; tile += gridDim.x) {
+        const int n = tile / bt.tiles_per_img;
+        const int r0 = (tile - n * bt.tiles_per_img) * kTR;
+        const int rows = min(kTR, sh.H - r0);
+        stg.commit(lds);
+        __syncthreads(); // tile staged (and, the first time, the constants)
+        const int tn = tile + gridDim.x;
+        if (tn < bt.ntiles) {
+            const int nn = tn / bt.tiles_per_img;
+            stg.load(x, dy, sh, nn, (tn - nn * bt.tiles_per_img) * kTR);
+        }
+
+        // Each channel iteration of the data gradient (VALU) is paired with
+        // a slice of the weight gradient's K-steps (matrix cores) so the two
+        // units work at the same time.  Rows past the image are zeros, so a
+        // short last tile needs no masking.
+        float gacc[CI][kTR];
+#pragma unroll
+        for (int ci = 0; ci < CI; ++ci)
+#pragma unroll
+            for (int r = 0; r < kTR; ++r)
+                gacc[ci][r] = 0.f;
+#pragma unroll 1
+        for (int cc = 0; cc < CG; ++cc) {
+            {
+                const int i1 = min(nsteps, (cc + 1) * per);
+                int i = cc * per;
+                for (; i + 1 < i1; i += 2) {
+                    kstep(i, 0);
+                    kstep(i + 1, 1);
+                }
+                if (i < i1)
+                    kstep(i, 0);
+            }
+            if (dxthr) {
+                const int co = g * CG + cc;
+                const bool ok = co < Co;
+                const float *src = lds + (ok ? co : 0) * bt.CSD + cbase;
+                const float *wc = wl + (ok ? co : Co) * CI * T;
+                int t0 = 0;
+#pragma unroll
+                for (int dq = -K; dq <= K; ++dq) {
+                    const int len = 2 * K + 1 - (dq < 0 ? -dq : dq);
+                    const int dslo = dq < 0 ? -K - dq : -K;
+                    const float *col = src + dq * P + dslo;
+                    float v[kTR + 2 * K];
+#pragma unroll
+                    for (int j = 0; j < kTR + 2 * K; ++j)
+                        if (j < kTR + len - 1)
+                            v[j] = col[j];
+#pragma unroll
+                    for (int u = 0; u < 2 * K + 1; ++u) {
+                        if (u < len) {
+#pragma unroll
+                            for (int ci = 0; ci < CI; ++ci) {
+                                const float wv = wc[ci * T + t0 + u];
+#pragma unroll
+                                for (int r = 0; r < kTR; ++r)
+                                    gacc[ci][r] += wv * v[r + u];
+                            }
+                        }
+                    }
+                    t0 += len;
+                }
+            }
+        }
+        if (dxthr) {
+#pragma unroll
+            for (int ci = 0; ci < CI; ++ci)
+#pragma unroll
+                for (int r = 0; r < kTR; ++r)
+                    dxp[((g * CI + ci) * kTR + r) * W + c] = gacc[ci][r];
+        }
+        __syncthreads(); // partials written; every read of the window done
+        if (do_dx != 0) {
+            const int perp = rows * W;
+            for (int e = tid; e < CI * perp; e += kThreads) {
+                const int ci = e / perp, rem = e - ci * perp;
+                float s = 0.f;
+                for (int gg = 0; gg < bt.G; ++gg)
+                    s += dxp[(gg * CI + ci) * kTR * W + rem];
+                dx[(static_cast<size_t>(n) * CI + ci) * sh.H * W + static_cast<size_t>(r0) * W + rem] = s;
+            }
+        }
+    }
+
+    // sum the accumulator sets and the waves in a fixed order; one partial
+    // per output element
+    __syncthreads();
+    float *red = lds; // [kWaves][MT * 16][NT * 16]
+#pragma unroll
+    for (int i = 0; i < MT; ++i)
+#pragma unroll
+        for (int j = 0; j < NT; ++j)
+#pragma unroll
+            for (int q = 0; q < 4; ++q)
+                red[((wave * MT + i) * 16 + 4 * kq + q) * (NT * 16) + j * 16 + m] =
+                    acc[0][i][j][q] + acc[1][i][j][q];
+    __syncthreads();
+    constexpr int Jt = J + 1;
+    for (int e = tid; e < Co * Jt; e += kThreads) {
+        const int row = e / Jt, col = e - row * Jt;
+        float s = 0.f;
+#pragma unroll
+        for (int wv = 0; wv < kWaves; ++wv)
+            s += red[(wv * MT * 16 + row) * (NT * 16) + col];
+        part[(static_cast<size_t>(row) * Jt + col) * gridDim.x + blockIdx.x] = s;
+    }
+}
+
+inline int cdiv(long a, long b) { return static_cast<int>((a + b - 1) / b); }
+
+constexpr size_t kLdsMax = 64 * 1024;
+
+int bwd_nt(const ConvShape &sh)
+{
+    const int nt = cdiv(sh.Ci * sh.T + 1, 16);
+    return nt <= 1 ? 1 : (nt <= 2 ? 2 : 4);
+}
+
+BwdTiling bwd_tiling(const ConvShape &sh)
+{
+    BwdTiling bt;
+    const int LR = kTR + 2 * sh.k, P = LR + 1, LC = sh.W + 2 * sh.k;
+    bt.W4 = sh.W / 4;
+    bt.CS = LC * P;
+    // dy channel stride == 2 mod 32: the 16 channels x 4 rows of an A
+    // fragment fall in distinct banks of each half-wave
+    bt.CSD = (bt.CS + 29) / 32 * 32 + 2;
+    bt.xo = sh.Co * bt.CSD;
+    bt.zo = bt.xo + sh.Ci * bt.CS;
+    bt.oo = bt.zo + bt.CS;
+    bt.G = std::max(1, std::min(sh.Co, kThreads / sh.W));
+    bt.tiles_per_img = cdiv(sh.H, kTR);
+    bt.ntiles = bt.tiles_per_img * sh.N;
+    bt.nitems = (sh.Co + sh.Ci) * LR * bt.W4;
+    bt.dxp = bt.oo + bt.CS;
+    bt.wl = bt.dxp + bt.G * sh.Ci * kTR * sh.W;
+    bt.dummy = bt.wl + (sh.Co + 1) * sh.Ci * sh.T;
+    bt.fdw4 = make_fastdiv(static_cast<uint32_t>(bt.W4));
+    bt.fdlr = make_fastdiv(static_cast<uint32_t>(LR));
+    return bt;
+}
+
+int bwd_cg(const ConvShape &sh, const BwdTiling &bt) { return cdiv(sh.Co, bt.G); }
+
+int bwd_u(const BwdTiling &bt) { return cdiv(bt.nitems, kThreads); }
+
+size_t bwd_lds(const ConvShape &sh, const BwdTiling &bt)
+{
+    const int P = kTR + 2 * sh.k + 1;
+    const size_t main = sizeof(float) * (static_cast<size_t>(bt.dummy) + 3 * P + 1);
+    const size_t red = sizeof(float) * kWaves * cdiv(sh.Co, 16) * 16 * bwd_nt(sh) * 16;
+    return std::max(main, red);
+}
+
+// Persistent grid: every block gets the same number of tiles, with at most
+// kBwdBlocksPerCU blocks per compute unit (the occupancy of bwd_f32_k).
+constexpr int kBwdBlocksPerCU = 3;
+
+int bwd_grid(const BwdTiling &bt)
+{
+    const int maxb = std::max(1, kBwdBlocksPerCU * device_cus());
+    const int per = cdiv(bt.ntiles, maxb);
+    return cdiv(bt.ntiles, per);
+}
+
+} // namespace
+
+bool smallc_f32_bwd_fused_ok(const ConvShape &sh)
+{
+    if (sh.s != 1 || (sh.k != 1 && sh.k != 2) || sh.Ci > 2 || sh.Co > 32 || sh.W % 4 != 0 ||
+        sh.W > kThreads || sh.Ci * sh.T + 1 > 64)
+        return false;
+    const BwdTiling bt = bwd_tiling(sh);
+    const int cg = bwd_cg(sh, bt);
+    return cg <= 4 && bwd_u(bt) <= 16 && bwd_lds(sh, bt) <= kLdsMax;
+}
+
+size_t smallc_f32_bwd_fused_workspace(const ConvShape &sh)
+{
+    const BwdTiling bt = bwd_tiling(sh);
+    return sizeof(float) * static_cast<size_t>(bwd_grid(bt)) * sh.Co * (sh.Ci * sh.T + 1);
+}
+
+hipError_t smallc_f32_bwd_fused(const float *x, const float *dy, const float *w, float *dx,
+                                float *dw, float *db, void *ws, const ConvShape &sh,
+                                hipStream_t st)
+{
+    const BwdTiling bt = bwd_tiling(sh);
+    const int nparts = bwd_grid(bt);
+    const int MT = cdiv(sh.Co, 16);
+    const int CG = std::max(2, bwd_cg(sh, bt));
+    const int U = bwd_u(bt);
+    float *part = static_cast<float *>(ws);
+    const size_t lds = bwd_lds(sh, bt);
+    const int do_dx = dx != nullptr ? 1 : 0;
+    dim3 grid(nparts);
+#define HEX_B(KV, CIV, MTV, NTV, CGV, UV)                                                     \
+    hipLaunchKernelGGL((bwd_f32_k<KV, CIV, MTV, NTV, CGV, UV>), grid, dim3(kThreads), lds, st, \
+                       x, dy, w, dx, part, sh, bt, do_dx)
+#define HEX_B_U(KV, CIV, MTV, NTV, CGV)                                                       \
+    do {                                                                                     \
+        if (U <= 8) HEX_B(KV, CIV, MTV, NTV, CGV, 8);                                        \
+        else HEX_B(KV, CIV, MTV, NTV, CGV, 16);                                              \
+    } while (0)
+#define HEX_B_CG(KV, CIV, MTV, NTV)                                                           \
+    do {                                                                                     \
+        if (CG == 2) HEX_B_U(KV, CIV, MTV, NTV, 2);                                          \
+        else if (CG == 3) HEX_B_U(KV, CIV, MTV, NTV, 3);                                     \
+        else HEX_B_U(KV, CIV, MTV, NTV, 4);                                                  \
+    } while (0)
+#define HEX_B_MT(KV, CIV, NTV)                                                                \
+    do {                                                                                     \
+        if (MT == 1) HEX_B_CG(KV, CIV, 1, NTV);                                              \
+        else HEX_B_CG(KV, CIV, 2, NTV);                                                      \
+    } while (0)
+    if (sh.k == 1) {
+        if (sh.Ci == 1) HEX_B_MT(1, 1, 1);     // J + 1 = 8
+        else HEX_B_MT(1, 2, 1);                // J + 1 = 15
+    } else {
+        if (sh.Ci == 1) HEX_B_MT(2, 1, 2);     // J + 1 = 20
+        else HEX_B_MT(2, 2, 4);                // J + 1 = 39
+    }
+#undef HEX_B_MT
+#undef HEX_B_CG
+#undef HEX_B_U
+#undef HEX_B
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess)
+        return e;
+    return reduce_partials(part, nparts, sh.Co, sh.Ci * sh.T, dw, db, st);
+}
+
+} // namespace hexk

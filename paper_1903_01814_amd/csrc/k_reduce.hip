@@ -1,52 +1,105 @@
 // k_reduce.hip -- deterministic reduction of weight-gradient partial sums.
 //
 // The weight-gradient kernels leave one partial sum per (output element,
-// partial slot) in the workspace, laid out [e][slot] with
-// e = co * (C_in*T + 1) + col: col < C_in*T is dw[co][col], col == C_in*T is
-// db[co].  One block per element sums its slots in a fixed order (strided
-// per thread, then a fixed LDS tree), so results do not depend on timing.
+// partial slot) in the workspace, with e = co * (C_in*T + 1) + col:
+// col < C_in*T is dw[co][col], col == C_in*T is db[co].  Two layouts:
+//  - [e][slot] (reduce_partials): one wave per element sums its slots;
+//  - chunked, part_index() in kernels.h (reduce_chunked): chunks of 64
+//    elements, each slot's 64 values contiguous, so a block writing its
+//    partials and the reduction reading them both touch whole lines.
+// Either way the slots are summed in a fixed order (strided per thread,
+// then a fixed tree), so results do not depend on timing.
 #include "hexdev.h"
 #include "kernels.h"
 
 namespace hexk {
 namespace {
 
-constexpr int kThreads = 256;
-
-__global__ __launch_bounds__(kThreads) void reduce_partials_k(
-    const float *__restrict__ part, int nparts, int J, float *__restrict__ dw,
-    float *__restrict__ db)
+// [e][slot] layout: one wave per element; each lane sums a strided subset of
+// the slots (four interleaved accumulators), then a butterfly over the wave.
+__global__ __launch_bounds__(64) void reduce_partials_k(const float *__restrict__ part, int nparts,
+                                                       int J, float *__restrict__ dw,
+                                                       float *__restrict__ db)
 {
-    __shared__ float red[kThreads];
     const int e = blockIdx.x;
+    const int lane = threadIdx.x;
     const float *src = part + static_cast<size_t>(e) * nparts;
-    float s = 0.f;
-    for (int p = threadIdx.x; p < nparts; p += kThreads)
-        s += src[p];
-    red[threadIdx.x] = s;
-    for (int half = kThreads / 2; half > 0; half >>= 1) {
-        __syncthreads();
-        if (threadIdx.x < half)
-            red[threadIdx.x] += red[threadIdx.x + half];
+    float s[4] = {0.f, 0.f, 0.f, 0.f};
+    int p = lane;
+    for (; p + 192 < nparts; p += 256) {
+#pragma unroll
+        for (int u = 0; u < 4; ++u)
+            s[u] += src[p + 64 * u];
     }
-    if (threadIdx.x == 0) {
+    for (; p < nparts; p += 64)
+        s[0] += src[p];
+    float v = (s[0] + s[1]) + (s[2] + s[3]);
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1)
+        v += __shfl_xor(v, off, 64);
+    if (lane == 0) {
         const int Jt = J + 1;
         const int co = e / Jt, col = e % Jt;
         if (col < J)
-            dw[static_cast<size_t>(co) * J + col] = red[0];
+            dw[static_cast<size_t>(co) * J + col] = v;
         else if (db != nullptr)
-            db[co] = red[0];
+            db[co] = v;
+    }
+}
+
+constexpr int kRedSlices = 16; // slot slices per chunk block (1024 threads)
+
+__global__ __launch_bounds__(kPartChunk * kRedSlices) void reduce_chunked_k(
+    const float *__restrict__ part, int nparts, int E, int J, float *__restrict__ dw,
+    float *__restrict__ db)
+{
+    __shared__ float red[kRedSlices][kPartChunk];
+    const int chunk = blockIdx.x;
+    const int el = threadIdx.x % kPartChunk, sl = threadIdx.x / kPartChunk;
+    const float *src = part + static_cast<size_t>(chunk) * nparts * kPartChunk + el;
+    float s[4] = {0.f, 0.f, 0.f, 0.f};
+    int p = sl;
+    for (; p + 3 * kRedSlices < nparts; p += 4 * kRedSlices) {
+#pragma unroll
+        for (int u = 0; u < 4; ++u)
+            s[u] += src[static_cast<size_t>(p + u * kRedSlices) * kPartChunk];
+    }
+    for (; p < nparts; p += kRedSlices)
+        s[0] += src[static_cast<size_t>(p) * kPartChunk];
+    red[sl][el] = (s[0] + s[1]) + (s[2] + s[3]);
+    for (int half = kRedSlices / 2; half > 0; half >>= 1) {
+        __syncthreads();
+        if (sl < half)
+            red[sl][el] += red[sl + half][el];
+    }
+    if (sl == 0) {
+        const int e = chunk * kPartChunk + el;
+        if (e < E) {
+            const int Jt = J + 1, co = e / Jt, col = e - co * Jt;
+            if (col < J)
+                dw[static_cast<size_t>(co) * J + col] = red[0][el];
+            else if (db != nullptr)
+                db[co] = red[0][el];
+        }
     }
 }
 
 } // namespace
 
+hipError_t reduce_chunked(const float *part, int nparts, int Co, int J, float *dw, float *db,
+                          hipStream_t st)
+{
+    const int E = Co * (J + 1);
+    hipLaunchKernelGGL(reduce_chunked_k, dim3((E + kPartChunk - 1) / kPartChunk),
+                       dim3(kPartChunk * kRedSlices), 0, st, part, nparts, E, J, dw, db);
+    return hipGetLastError();
+}
+
 hipError_t reduce_partials(const float *part, int nparts, int Co, int J, float *dw, float *db,
                            hipStream_t st)
 {
     const int E = Co * (J + 1);
-    hipLaunchKernelGGL(reduce_partials_k, dim3(E), dim3(kThreads), 0, st, part, nparts, J, dw,
-                       db);
+    hipLaunchKernelGGL(reduce_partials_k, dim3(E), dim3(64), 0, st, part, nparts, J, dw, db);
     return hipGetLastError();
 }
 

@@ -13,7 +13,7 @@
 // over full-width pixel tiles of one image and keep their accumulators in
 // registers; each block writes one partial sum per output element, laid out
 // in chunks of 64 elements so that both the writes and the fixed-order
-// reduction (reduce_partials_chunked) are contiguous.
+// reduction (reduce_chunked) are contiguous.
 //
 // Block = 4 waves; a block owns 4 channel tiles (64 co) x NB column tiles
 // (grid.y enumerates the (co, column) groups); wave w owns column tiles
@@ -34,7 +34,6 @@ typedef short shortx8 __attribute__((ext_vector_type(8)));
 
 constexpr int kThreads = 256;
 constexpr int kMB = 4;          // channel tiles (of 16 co) per block
-constexpr int kChunk = 64;      // partial-sum layout chunk
 constexpr int kXO = 8;          // slot column of plane column 0 in the x window
 
 struct WgTiling {
@@ -203,7 +202,7 @@ __global__ __launch_bounds__(kThreads) void wgrad_bf16_k(
     }
 
     // partial sums of this block: element e = co * Jt + col, chunked layout
-    // part[(e / 64) * nparts * 64 + slot * 64 + e % 64]
+    // part_index(e, slot): chunked layout
     const size_t slot = blockIdx.x;
 #pragma unroll
     for (int i = 0; i < kMB; ++i) {
@@ -218,7 +217,7 @@ __global__ __launch_bounds__(kThreads) void wgrad_bf16_k(
                 if (co >= sh.Co)
                     continue;
                 const size_t e = static_cast<size_t>(co) * tg.Jt + col;
-                part[(e / kChunk) * tg.nparts * kChunk + slot * kChunk + e % kChunk] = acc[i][j][q];
+                part[part_index(static_cast<int>(e), static_cast<int>(slot), tg.nparts)] = acc[i][j][q];
             }
         }
     }
@@ -233,41 +232,8 @@ __global__ __launch_bounds__(kThreads) void wgrad_bf16_k(
             const int co = co_blk + i * 16 + mm;
             if (co < sh.Co) {
                 const size_t e = static_cast<size_t>(co) * tg.Jt + tg.J;
-                part[(e / kChunk) * tg.nparts * kChunk + slot * kChunk + e % kChunk] = s;
+                part[part_index(static_cast<int>(e), static_cast<int>(slot), tg.nparts)] = s;
             }
-        }
-    }
-}
-
-__global__ __launch_bounds__(kThreads) void reduce_chunked_k(const float *__restrict__ part, int nparts,
-                                                            int E, int J, float *__restrict__ dw,
-                                                            float *__restrict__ db)
-{
-    // block = one chunk of 64 elements; 4 slices of the partial slots
-    __shared__ float red[4][kChunk];
-    const int chunk = blockIdx.x;
-    const int el = threadIdx.x % kChunk, sl = threadIdx.x / kChunk;
-    const float *src = part + static_cast<size_t>(chunk) * nparts * kChunk + el;
-    float s[4] = {0.f, 0.f, 0.f, 0.f};
-    int p = sl;
-    for (; p + 12 < nparts; p += 16) {
-#pragma unroll
-        for (int u = 0; u < 4; ++u)
-            s[u] += src[static_cast<size_t>(p + 4 * u) * kChunk];
-    }
-    for (; p < nparts; p += 4)
-        s[0] += src[static_cast<size_t>(p) * kChunk];
-    red[sl][el] = (s[0] + s[1]) + (s[2] + s[3]);
-    __syncthreads();
-    if (sl == 0) {
-        const int e = chunk * kChunk + el;
-        if (e < E) {
-            const float v = (red[0][el] + red[1][el]) + (red[2][el] + red[3][el]);
-            const int Jt = J + 1, co = e / Jt, col = e - co * Jt;
-            if (col < J)
-                dw[static_cast<size_t>(co) * J + col] = v;
-            else if (db != nullptr)
-                db[co] = v;
         }
     }
 }
@@ -335,7 +301,8 @@ size_t bf16_wgrad_workspace(const ConvShape &sh)
 {
     const WgTiling tg = wg_tiling(sh, wg_nbw(sh));
     const size_t E = static_cast<size_t>(sh.Co) * tg.Jt;
-    return sizeof(float) * static_cast<size_t>(cdiv(E, kChunk)) * kChunk * tg.nparts;
+    return sizeof(float) * static_cast<size_t>(part_chunks(static_cast<int>(E))) * kPartChunk *
+           tg.nparts;
 }
 
 hipError_t bf16_wgrad(const void *x, const void *dy, float *dw, float *db, void *ws,
@@ -371,10 +338,7 @@ hipError_t bf16_wgrad(const void *x, const void *dy, float *dw, float *db, void 
     hipError_t e = hipGetLastError();
     if (e != hipSuccess)
         return e;
-    const int E = sh.Co * tg.Jt;
-    hipLaunchKernelGGL(reduce_chunked_k, dim3(cdiv(E, kChunk)), dim3(kThreads), 0, st, part,
-                       tg.nparts, E, tg.J, dw, db);
-    return hipGetLastError();
+    return reduce_chunked(part, tg.nparts, sh.Co, tg.J, dw, db, st);
 }
 
 } // namespace hexk

@@ -24,6 +24,21 @@ struct ConvShape {
 hipError_t reduce_partials(const float *part, int nparts, int Co, int J, float *dw, float *db,
                            hipStream_t st);
 
+// Compute units of the current device (queried once per device).
+int device_cus();
+
+// Chunked partial-sum layout: element e (e = co * (C_in*T + 1) + col) of
+// partial slot `slot` lives at part_index(e, slot, nparts); reduced by
+// reduce_chunked.  Workspace: part_chunks(E) * kPartChunk * nparts floats.
+constexpr int kPartChunk = 64;
+__host__ __device__ inline size_t part_index(int e, int slot, int nparts)
+{
+    return (static_cast<size_t>(e / kPartChunk) * nparts + slot) * kPartChunk + e % kPartChunk;
+}
+inline int part_chunks(int E) { return (E + kPartChunk - 1) / kPartChunk; }
+hipError_t reduce_chunked(const float *part, int nparts, int Co, int J, float *dw, float *db,
+                          hipStream_t st);
+
 // ---- generic kernels: any k, stride, channel count and dtype -----------
 hipError_t conv_fwd_generic(const void *x, const void *w, const void *b,
                             void *y, const ConvShape &sh, Dtype dt, bool relu,
@@ -55,6 +70,11 @@ bool smallc_f32_wgrad_ok(const ConvShape &sh);
 size_t smallc_f32_wgrad_workspace(const ConvShape &sh);
 hipError_t smallc_f32_wgrad(const float *x, const float *dy, float *dw, float *db, void *ws,
                             const ConvShape &sh, hipStream_t st);
+bool smallc_f32_bwd_fused_ok(const ConvShape &sh);
+size_t smallc_f32_bwd_fused_workspace(const ConvShape &sh);
+hipError_t smallc_f32_bwd_fused(const float *x, const float *dy, const float *w, float *dx,
+                                float *dw, float *db, void *ws, const ConvShape &sh,
+                                hipStream_t st);
 
 // ---- bf16 matrix-core convolution, input channels a multiple of 32 -----
 // forward (reflect = false: IC = C_in, OC = C_out) or stride-1 data

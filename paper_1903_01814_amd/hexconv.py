@@ -39,6 +39,9 @@ SIGNATURES = {
     "hexconv_bwd_weight_workspace": ([_I, _I, _I, _I, _I, _I, _I, _I], _S),
     "hexconv_bwd_weight": ([_P, _P, _P, _P, _P, _S, _I, _I, _I, _I, _I, _I, _I,
                             _I, _P], _I),
+    "hexconv_bwd_workspace": ([_I, _I, _I, _I, _I, _I, _I, _I], _S),
+    "hexconv_bwd": ([_P, _P, _P, _P, _P, _P, _P, _S, _I, _I, _I, _I, _I, _I, _I,
+                     _I, _P], _I),
     "hexpool_fwd": ([_P, _P, _P, _I, _I, _I, _I, _I, _I, _I, _I, _P], _I),
     "hexpool_bwd": ([_P, _P, _P, _P, _I, _I, _I, _I, _I, _I, _I, _I, _P], _I),
     "hex_status_string": ([_I], ctypes.c_char_p),
@@ -201,6 +204,34 @@ def hexconv_bwd_weight(x, dy, dw, db, ws, k: int, stride: int = 1,
         ws_ptr, ws_bytes, N, Ci, Co, H, W, k, stride, dt, _stream(stream))
     _ok("hexconv_bwd_weight", rc)
     return dw, db
+
+
+def hexconv_bwd_workspace(N, C_in, C_out, H, W, k, stride, dt):
+    return load().hexconv_bwd_workspace(N, C_in, C_out, H, W, k, stride, dt)
+
+
+def hexconv_bwd(x, dy, w, dx, dw, db, ws, k: int, stride: int = 1,
+                stream=None):
+    """dx (may be None), dw, db (may be None) <- both gradients of one layer
+    in one call.  ws: uint8 device tensor of at least hexconv_bwd_workspace
+    bytes (or None when that is 0)."""
+    torch = _torch()
+    N, Ci, H, W = x.shape
+    Co = dw.shape[0]
+    dt = _dtype_code(x)
+    T = hex_num_taps(k)
+    Ho, Wo = hex_out_shape(H, W, stride)
+    if dw.dtype != torch.float32 or (db is not None and db.dtype != torch.float32):
+        raise TypeError("hexconv: dw and db must be float32")
+    ws_ptr = _dev(ws, "ws")
+    ws_bytes = 0 if ws is None else ws.numel() * ws.element_size()
+    rc = load().hexconv_bwd(
+        _dev(x, "x", dt), _dev(dy, "dy", dt, (N, Co, Ho, Wo)),
+        _dev(w, "w", dt, (Co, Ci, T)), _dev(dx, "dx", dt, (N, Ci, H, W)),
+        _dev(dw, "dw", None, (Co, Ci, T)), _dev(db, "db", None, (Co,)),
+        ws_ptr, ws_bytes, N, Ci, Co, H, W, k, stride, dt, _stream(stream))
+    _ok("hexconv_bwd", rc)
+    return dx, dw, db
 
 
 def hexpool_fwd(x, y, argmax_tap, k: int, stride: int, mode: int,

@@ -26,6 +26,7 @@ def test_header_declares_expected_entry_points():
     names = declared_functions()
     for n in ["hexconv_fwd", "hexconv_bwd_data", "hexconv_bwd_weight",
               "hexconv_bwd_weight_workspace", "hexpool_fwd", "hexpool_bwd",
+              "hexconv_bwd", "hexconv_bwd_workspace",
               "hex_num_taps", "hex_out_shape", "hex_tap_table",
               "hex_status_string"]:
         assert n in names
@@ -73,6 +74,8 @@ class FakePtr:
     B = 0x20000
     C = 0x30000
     D = 0x40000
+    E = 0x50000
+    F = 0x60000
 
 
 def _fwd(x=FakePtr.A, w=FakePtr.B, b=None, y=FakePtr.C, N=2, Ci=1, Co=4, H=8,
@@ -135,6 +138,31 @@ def test_bwd_weight_workspace_and_errors():
     assert f(dw=None) == hx.HEX_ERR_INVALID_ARG
     assert f(x=None) == hx.HEX_ERR_INVALID_ARG
     assert f(db=FakePtr.C + 4) == hx.HEX_ERR_INVALID_ARG
+
+
+def test_bwd_combined_workspace_and_errors():
+    """hexconv_bwd: every argument is checked before anything is enqueued,
+    for the fused float32 path (1 -> 16 channels, k = 2) and for the
+    fallback that runs the two gradients one after the other."""
+    lib = hx.load()
+    for (Ci, Co, k, dt) in [(1, 16, 2, 0), (3, 5, 1, 1)]:
+        need = lib.hexconv_bwd_workspace(4, Ci, Co, 16, 16, k, 1, dt)
+        assert need > 0
+        assert lib.hexconv_bwd_workspace(4, Ci, Co, 16, 16, -1, 1, dt) == 0
+        f = lambda x=FakePtr.A, dy=FakePtr.B, w=FakePtr.C, dx=FakePtr.D, \
+            dw=FakePtr.E, db=None, ws=FakePtr.F, nb=need: lib.hexconv_bwd(
+                x, dy, w, dx, dw, db, ws, nb, 4, Ci, Co, 16, 16, k, 1, dt, None)
+        assert f(ws=None) == hx.HEX_ERR_INVALID_ARG
+        assert f(nb=need - 1) == hx.HEX_ERR_INVALID_ARG
+        assert f(dw=None) == hx.HEX_ERR_INVALID_ARG
+        assert f(x=None) == hx.HEX_ERR_INVALID_ARG
+        assert f(dy=None) == hx.HEX_ERR_INVALID_ARG
+        assert f(w=None) == hx.HEX_ERR_INVALID_ARG        # dx wanted, no weights
+        assert f(dx=FakePtr.D + 4) == hx.HEX_ERR_INVALID_ARG
+        assert f(db=FakePtr.C + 4) == hx.HEX_ERR_INVALID_ARG
+        assert lib.hexconv_bwd(FakePtr.A, FakePtr.B, FakePtr.C, FakePtr.D, FakePtr.E,
+                               None, FakePtr.F, need, 4, Ci, Co, 16, 16, 9, 1, dt,
+                               None) == hx.HEX_ERR_INVALID_ARG
 
 
 def test_pool_rejects_invalid():

@@ -70,6 +70,25 @@ def run_bwd_weight(x, dy, k, s, dt, with_db=True):
     return from_dev(dw), (from_dev(db) if with_db else None)
 
 
+def run_bwd(x, dy, w, k, s, dt, want_dx=True):
+    """Both gradients through the combined entry point hexconv_bwd."""
+    torch = torch_mod()
+    N, Ci, H, W = x.shape
+    Co = dy.shape[1]
+    T = hx.hex_num_taps(k)
+    dx = empty((N, Ci, H, W), dt) if want_dx else None
+    if dx is not None:
+        dx.fill_(float("nan"))
+    dw = torch.full((Co, Ci, T), float("nan"), dtype=torch.float32, device="cuda:0")
+    db = torch.full((Co,), float("nan"), dtype=torch.float32, device="cuda:0")
+    nbytes = hx.hexconv_bwd_workspace(N, Ci, Co, H, W, k, s,
+                                      hx.HEX_F32 if dt == "f32" else hx.HEX_BF16)
+    ws = torch.empty(nbytes, dtype=torch.uint8, device="cuda:0") if nbytes else None
+    hx.hexconv_bwd(to_dev(x, dt), to_dev(dy, dt), to_dev(w, dt), dx, dw, db, ws, k, s)
+    _sync()
+    return (from_dev(dx) if want_dx else None), from_dev(dw), from_dev(db)
+
+
 def run_pool_fwd(x, k, s, mode, dt, want_argmax=True):
     torch = torch_mod()
     N, C, H, W = x.shape
@@ -115,6 +134,11 @@ def check_bwd_full(x, w, dy, k, s, dt, what="bwd"):
     # dw / db are float32 outputs; bf16 operands -> magnitude metric
     check(dt, dw, rw, mw, what + " dw")
     check(dt, db, rb, mb, what + " db")
+    # the combined entry point gives the same results (to the tolerance)
+    dx2, dw2, db2 = run_bwd(x, dy, w, k, s, dt)
+    check(dt, dx2, ref, mag, what + " bwd dx")
+    check(dt, dw2, rw, mw, what + " bwd dw")
+    check(dt, db2, rb, mb, what + " bwd db")
 
 
 # ------------------------------------------------------------ workloads
@@ -255,7 +279,8 @@ SWEEP = [
     (1, 64, 64, 12, 12, 1, 1), (1, 32, 64, 24, 24, 2, 1), (1, 1, 32, 48, 48, 2, 1),
     (2, 64, 16, 9, 70, 1, 1), (1, 7, 9, 6, 40, 2, 2), (1, 1, 1, 1, 1, 1, 1),
     (1, 2, 2, 2, 9, 4, 2), (3, 3, 24, 37, 8, 2, 1), (1, 2, 70, 5, 256, 1, 1),
-    (2, 48, 40, 11, 32, 2, 1),
+    (2, 48, 40, 11, 32, 2, 1), (3, 2, 20, 13, 68, 2, 1), (2, 1, 24, 9, 8, 1, 1),
+    (1, 2, 16, 5, 12, 2, 1),
 ]
 
 
@@ -304,6 +329,16 @@ def test_pool_sweep(case, mode, dt):
         rdx = oracle.pool_bwd(dy, ram if mode == 0 else None, relu_y, k, s, mode, H, W)
         mag = oracle.pool_bwd(np.abs(dy), ram if mode == 0 else None, relu_y, k, s, mode, H, W)
         check(dt, dx, rdx, mag, "pool bwd")
+
+
+def test_bwd_without_dx():
+    """hexconv_bwd with dx = NULL (a first layer) still gives dw and db."""
+    cfg = CFG["c2"]
+    d = _conv_inputs(cfg, N=24)
+    _, dw, db = run_bwd(d["x"], d["dy"], d["w"], cfg["k"], 1, "f32", want_dx=False)
+    rw, rb = oracle.conv_bwd_weight(d["x"], d["dy"], cfg["k"], 1)
+    check_f32(dw, rw, "dw")
+    check_f32(db, rb, "db")
 
 
 def test_debug_mode_golden():
