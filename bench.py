@@ -15,8 +15,9 @@ one untimed replay), so the time is GPU execution, not Python launch cost.  Each
 different batch from a rotating set whose total size exceeds the 256 MB
 Infinity Cache, so reads and writes go to HBM rather than staying cached.
 
-Other workloads (--config c3 / c4 / c5) print their own line; they are
-parity workloads measured on request.
+Other workloads print their own line on request: --config c3 (hex max and
+average pooling, bf16, GB/s), c4 (wide-channel bf16 convolution, GFLOP/s)
+and c5 (the five-layer bf16 stack, forward and backward, samples/s).
 
 Prints one JSON line.  With --gpus > 1 it exits: this build runs on one GPU.
 """
@@ -264,6 +265,275 @@ def bench_conv(args, torch, cfg_key):
     return out
 
 
+def cpu_baseline_pool(cfg, x, seconds):
+    """The fp64 oracle's max and average pooling on an 8-image slice,
+    repeated for `seconds`; returns GB/s of the same algorithmic bytes."""
+    import oracle
+    xs = x[:8]
+    k, s = cfg["k"], cfg["stride"]
+    Ho, Wo = oracle.out_shape(cfg["H"], cfg["W"], s)
+    nbytes = 2 * 2 * (xs.size + xs.shape[0] * xs.shape[1] * Ho * Wo)
+    reps, t0 = 0, time.perf_counter()
+    while True:
+        oracle.pool_fwd(xs, k, s, oracle.POOL_MAX)
+        oracle.pool_fwd(xs, k, s, oracle.POOL_AVG)
+        reps += 1
+        el = time.perf_counter() - t0
+        if el >= seconds:
+            break
+    return nbytes * reps / el / 1e9, oracle.threads(), reps, el
+
+
+def bench_pool(args, torch, cfg_key):
+    cfg = gen.CONFIGS[cfg_key]
+    N, C, H, W, k, s = (cfg[n] for n in ("N", "C", "H", "W", "k", "stride"))
+    Ho, Wo = hx.hex_out_shape(H, W, s)
+    dt = torch.bfloat16
+    esz = 2
+    in_b, out_b = esz * N * C * H * W, esz * N * C * Ho * Wo
+    nsets = max(1, -(-ROTATE_MIN_BYTES // (in_b + 2 * out_b)))
+    d0 = gen.pool_inputs(cfg, seed=0)
+    sets = []
+    for b in range(nsets):
+        d = d0 if b == 0 else gen.pool_inputs(cfg, seed=b)
+        sets.append(dict(x=dev(torch, d["x"], dt),
+                         ymax=torch.empty((N, C, Ho, Wo), dtype=dt, device="cuda:0"),
+                         yavg=torch.empty((N, C, Ho, Wo), dtype=dt, device="cuda:0")))
+
+    def pmax(i):
+        z = sets[i % nsets]
+        hx.hexpool_fwd(z["x"], z["ymax"], None, k, s, hx.HEX_POOL_MAX)
+
+    def pavg(i):
+        z = sets[i % nsets]
+        hx.hexpool_fwd(z["x"], z["yavg"], None, k, s, hx.HEX_POOL_AVG)
+
+    def step(i):
+        pmax(i)
+        pavg(i)
+
+    timer = EagerTimer(torch) if args.eager else GraphTimer(torch)
+    for i in range(args.warmup):
+        step(i)
+    torch.cuda.synchronize()
+    ms_step = timer.time(step, args.steps)
+    ops = {}
+    for name, fn in (("max", pmax), ("avg", pavg)):
+        ms = timer.time(fn, args.steps)
+        ops[name] = dict(ms=ms, gbs=(in_b + out_b) / (ms * 1e-3) / 1e9)
+    value = 2 * (in_b + out_b) / (ms_step * 1e-3) / 1e9
+    dom = max(ops, key=lambda n: ops[n]["ms"])
+    achieved = ops[dom]["gbs"]
+    roof = dict(bound="hbm", achieved=round(achieved, 1), peak=HBM_PEAK_GBS, unit="GB/s",
+                frac=round(achieved / HBM_PEAK_GBS, 4),
+                kernel=KERNEL_NAMES.get((cfg_key, dom), dom), op=dom)
+    roof["traffic"] = read_counters(cfg["name"], roof["kernel"])
+    out = dict(
+        metric="hex-pool HBM GB/s (max + avg, fwd)", value=round(value, 1), unit="GB/s",
+        n_gpus=1, steps=args.steps, warmup=args.warmup, ms_per_step=round(ms_step, 5),
+        higher_is_better=True, scaling="weak", vs_baseline=None, dtype="bf16",
+        data="synthetic",
+        config=dict(workload=cfg["name"], N=N, C=C, H=H, W=W, k=k, stride=s, H_out=Ho,
+                    W_out=Wo, rotating_batches=nsets),
+        per_op={n: dict(ms=round(v["ms"], 5), alg_GBps=round(v["gbs"], 1))
+                for n, v in ops.items()},
+        roofline=roof,
+    )
+    if not args.no_cpu_baseline:
+        gbs, thr, reps, el = cpu_baseline_pool(cfg, d0["x"], args.cpu_seconds)
+        out["cpu_baseline"] = dict(
+            value=round(gbs, 3), unit="GB/s", cores=thr, kind="oracle",
+            sample="8 of %d images, max and avg pooling, fp64, repeated %d times in %.1f s"
+                   % (N, reps, el))
+    return out
+
+
+def stack_shapes(cfg):
+    """Per layer: (kind, C_in, C_out, k, stride, relu, H_in, W_in, H_out, W_out)."""
+    H, W = cfg["H"], cfg["W"]
+    out = []
+    for layer in cfg["layers"]:
+        if layer[0] == "conv":
+            _, ci, co, k, s, relu = layer
+        else:
+            _, ci, k, s = layer
+            co, relu = ci, False
+        Ho, Wo = hx.hex_out_shape(H, W, s)
+        out.append((layer[0], ci, co, k, s, relu, H, W, Ho, Wo))
+        H, W = Ho, Wo
+    return out
+
+
+def stack_flop(cfg, N):
+    """Products per step: forward of every conv, data gradient of every conv
+    but the first, weight gradient of every conv."""
+    f = 0.0
+    for li, (kind, ci, co, k, s, relu, H, W, Ho, Wo) in enumerate(stack_shapes(cfg)):
+        if kind == "conv":
+            per = conv_flop(N, ci, co, Ho, Wo, hx.hex_num_taps(k))
+            f += per * (2 if li == 0 else 3)
+    return f
+
+
+def cpu_baseline_stack(cfg, d, seconds):
+    """The fp64 oracle running the whole stack forward and backward on a
+    2-image slice, repeated for `seconds`; returns samples/s."""
+    import oracle
+    n = 2
+    shapes = stack_shapes(cfg)
+    reps, t0 = 0, time.perf_counter()
+    while True:
+        acts, ams = [d["x"][:n]], []
+        for li, (kind, ci, co, k, s, relu, H, W, Ho, Wo) in enumerate(shapes):
+            a = acts[-1]
+            if kind == "conv":
+                p = d["params"][li]
+                y = oracle.conv_fwd(a, p["w"], p["b"], k, s)
+                acts.append(np.maximum(y, 0.0) if relu else y)
+                ams.append(None)
+            else:
+                y, am = oracle.pool_fwd(a, k, s, oracle.POOL_MAX)
+                acts.append(y)
+                ams.append(am)
+        g = d["dy"][:n]
+        for li in range(len(shapes) - 1, -1, -1):
+            kind, ci, co, k, s, relu, H, W, Ho, Wo = shapes[li]
+            if kind == "conv":
+                oracle.conv_bwd_weight(acts[li], g, k, s)
+                if li > 0:
+                    g = oracle.conv_bwd_data(g, d["params"][li]["w"], k, s, H, W)
+            else:
+                relu_y = acts[li] if shapes[li - 1][0] == "conv" and shapes[li - 1][5] else None
+                g = oracle.pool_bwd(g, ams[li], relu_y, k, s, oracle.POOL_MAX, H, W)
+        reps += 1
+        el = time.perf_counter() - t0
+        if el >= seconds:
+            break
+    return n * reps / el, oracle.threads(), reps, el
+
+
+def bench_stack(args, torch, cfg_key):
+    cfg = gen.CONFIGS[cfg_key]
+    N = cfg["N"]
+    dt = torch.bfloat16
+    shapes = stack_shapes(cfg)
+    Hl, Wl = shapes[-1][8], shapes[-1][9]
+    nsets = 2
+    dsets = [gen.stack_inputs(cfg, hx.hex_num_taps, (Hl, Wl), seed=b) for b in range(nsets)]
+    params = [None if p is None else dict(w=dev(torch, p["w"], dt), b=dev(torch, p["b"], dt))
+              for p in dsets[0]["params"]]
+    xs = [dev(torch, d["x"], dt) for d in dsets]
+    dys = [dev(torch, d["dy"], dt) for d in dsets]
+    acts = []     # output of each layer
+    grads = []    # gradient w.r.t. each layer's input (None for the image)
+    ams = []
+    wgr = []
+    nws = 0
+    for li, (kind, ci, co, k, s, relu, H, W, Ho, Wo) in enumerate(shapes):
+        acts.append(torch.empty((N, co, Ho, Wo), dtype=dt, device="cuda:0"))
+        grads.append(None if li == 0 else torch.empty((N, ci, H, W), dtype=dt, device="cuda:0"))
+        if kind == "conv":
+            T = hx.hex_num_taps(k)
+            ams.append(None)
+            wgr.append((torch.empty((co, ci, T), dtype=torch.float32, device="cuda:0"),
+                        torch.empty((co,), dtype=torch.float32, device="cuda:0")))
+            nws = max(nws, hx.hexconv_bwd_workspace(N, ci, co, H, W, k, s, hx.HEX_BF16))
+        else:
+            ams.append(torch.empty((N, co, Ho, Wo), dtype=torch.uint8, device="cuda:0"))
+            wgr.append(None)
+    ws = torch.empty(max(nws, 1), dtype=torch.uint8, device="cuda:0")
+
+    def forward(i):
+        a = xs[i % nsets]
+        for li, (kind, ci, co, k, s, relu, H, W, Ho, Wo) in enumerate(shapes):
+            if kind == "conv":
+                hx.hexconv_fwd(a, params[li]["w"], params[li]["b"], acts[li], k, s, relu=relu)
+            else:
+                hx.hexpool_fwd(a, acts[li], ams[li], k, s, hx.HEX_POOL_MAX)
+            a = acts[li]
+
+    def backward(i):
+        g = dys[i % nsets]
+        for li in range(len(shapes) - 1, -1, -1):
+            kind, ci, co, k, s, relu, H, W, Ho, Wo = shapes[li]
+            a_in = xs[i % nsets] if li == 0 else acts[li - 1]
+            if kind == "conv":
+                hx.hexconv_bwd(a_in, g, params[li]["w"], grads[li], wgr[li][0], wgr[li][1], ws,
+                               k, s)
+            else:
+                relu_y = a_in if shapes[li - 1][0] == "conv" and shapes[li - 1][5] else None
+                hx.hexpool_bwd(g, ams[li], relu_y, grads[li], k, s, hx.HEX_POOL_MAX)
+            g = grads[li]
+
+    def step(i):
+        forward(i)
+        backward(i)
+
+    timer = EagerTimer(torch) if args.eager else GraphTimer(torch)
+    for i in range(args.warmup):
+        step(i)
+    torch.cuda.synchronize()
+    ms_step = timer.time(step, args.steps)
+    # per-layer durations (each call alone, same inputs every time)
+    per_layer = []
+    for li, (kind, ci, co, k, s, relu, H, W, Ho, Wo) in enumerate(shapes):
+        a_in = xs[0] if li == 0 else acts[li - 1]
+        if kind == "conv":
+            f = lambda i, li=li, a_in=a_in, k=k, s=s, relu=relu: hx.hexconv_fwd(
+                a_in, params[li]["w"], params[li]["b"], acts[li], k, s, relu=relu)
+            b = lambda i, li=li, a_in=a_in, k=k, s=s: hx.hexconv_bwd(
+                a_in, acts[li], params[li]["w"], grads[li], wgr[li][0], wgr[li][1], ws, k, s)
+        else:
+            f = lambda i, li=li, a_in=a_in, k=k, s=s: hx.hexpool_fwd(
+                a_in, acts[li], ams[li], k, s, hx.HEX_POOL_MAX)
+            relu_y = a_in if shapes[li - 1][0] == "conv" and shapes[li - 1][5] else None
+            b = lambda i, li=li, k=k, s=s, relu_y=relu_y: hx.hexpool_bwd(
+                acts[li], ams[li], relu_y, grads[li], k, s, hx.HEX_POOL_MAX)
+        per_layer.append(dict(layer=li, kind=kind, C_in=ci, C_out=co, k=k, stride=s,
+                              fwd_ms=round(timer.time(f, args.steps), 5),
+                              bwd_ms=round(timer.time(b, args.steps), 5)))
+    flop = stack_flop(cfg, N)
+    out = dict(
+        metric="hex-CNN stack samples/s (fwd+bwd)", value=round(N / (ms_step * 1e-3), 1),
+        unit="samples/s", n_gpus=1, steps=args.steps, warmup=args.warmup,
+        ms_per_step=round(ms_step, 5), higher_is_better=True, scaling="weak",
+        vs_baseline=None, dtype="bf16", data="synthetic",
+        config=dict(workload=cfg["name"], N=N, H=cfg["H"], W=cfg["W"],
+                    layers=[list(l) for l in cfg["layers"]]),
+        GFLOPs=round(flop / (ms_step * 1e-3) / 1e9, 1),
+        per_layer=per_layer,
+    )
+    # dominant layer op against its roofline
+    best = max([(pl["fwd_ms"], li, "fwd") for li, pl in enumerate(per_layer)] +
+               [(pl["bwd_ms"], li, "bwd") for li, pl in enumerate(per_layer)])
+    ms, li, op = best
+    kind, ci, co, k, s, relu, H, W, Ho, Wo = shapes[li]
+    if kind == "conv" and ci >= 32:
+        fl = conv_flop(N, ci, co, Ho, Wo, hx.hex_num_taps(k)) * (1 if op == "fwd" else 2)
+        ach = fl / (ms * 1e-3) / 1e12
+        roof = dict(bound="mfma", achieved=round(ach, 2), peak=BF16_MFMA_PEAK_TFLOPS,
+                    unit="TFLOP/s", frac=round(ach / BF16_MFMA_PEAK_TFLOPS, 4))
+    else:
+        if kind == "conv":
+            nb = 2 * (N * ci * H * W + N * co * Ho * Wo) * (1 if op == "fwd" else 2)
+        else:
+            nb = 2 * (N * ci * H * W + N * co * Ho * Wo) + N * co * Ho * Wo
+        ach = nb / (ms * 1e-3) / 1e9
+        roof = dict(bound="hbm", achieved=round(ach, 1), peak=HBM_PEAK_GBS, unit="GB/s",
+                    frac=round(ach / HBM_PEAK_GBS, 4))
+    roof["op"] = "layer%d_%s" % (li, op)
+    roof["kernel"] = KERNEL_NAMES.get((cfg_key, roof["op"]), roof["op"])
+    roof["traffic"] = None
+    out["roofline"] = roof
+    if not args.no_cpu_baseline:
+        sps, thr, reps, el = cpu_baseline_stack(cfg, dsets[0], args.cpu_seconds)
+        out["cpu_baseline"] = dict(
+            value=round(sps, 3), unit="samples/s", cores=thr, kind="oracle",
+            sample="2 of %d images through the whole stack, fwd+bwd, fp64, repeated %d "
+                   "times in %.1f s" % (N, reps, el))
+    return out
+
+
 # kernel that dominates each op (as it appears in rocprofv3 traces)
 KERNEL_NAMES = {}
 
@@ -273,7 +543,7 @@ def main():
     p.add_argument("--gpus", type=int, default=1)
     p.add_argument("--steps", type=int, default=500)
     p.add_argument("--warmup", type=int, default=20)
-    p.add_argument("--config", default="c2", choices=["c2", "c4"])
+    p.add_argument("--config", default="c2", choices=["c2", "c3", "c4", "c5"])
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--eager", action="store_true",
                    help="launch eagerly instead of replaying a HIP graph (for counter runs)")
@@ -288,7 +558,12 @@ def main():
         print("bench.py: no GPU visible", file=sys.stderr)
         sys.exit(1)
     hx.load()
-    out = bench_conv(args, torch, args.config)
+    if args.config == "c3":
+        out = bench_pool(args, torch, args.config)
+    elif args.config == "c5":
+        out = bench_stack(args, torch, args.config)
+    else:
+        out = bench_conv(args, torch, args.config)
     print(json.dumps(out), flush=True)
 
 
