@@ -1,25 +1,38 @@
-// k_mfma_bf16.hip -- bf16 convolutions on the matrix cores (fp32 accumulate).
+// k_mfma_bf16.hip -- bf16 convolutions on the matrix cores (fp32 accumulate)
+// for input channel counts that are a multiple of 32, at stride 1.
 //
 // Implicit GEMM for the forward pass and, with the point-reflected kernel
 // and the channel roles swapped, for the stride-1 data gradient:
 //   D[pixel][oc] = sum_{t, ic} A[pixel][(t, ic)] * B[(t, ic)][oc]
 //   forward:        A = x at pixel + tap t,  B[(t, ic)][oc] = w[oc][ic][t]
 //   data gradient:  A = dy at pixel + tap t, B[(t, ic)][oc] = w[ic][oc][T-1-t]
-// v_mfma_f32_16x16x32_bf16, lane layout (checked on the device):
-//   a[i] = A[lane % 16][8 * (lane / 16) + i], b[i] = B[8 * (lane / 16) + i][lane % 16],
-//   d[j] = D[4 * (lane / 16) + j][lane % 16].
-// K runs over taps, then input channels in blocks of 32, so each lane's 8
-// A values are 8 consecutive channels of one pixel: the input tile is kept
-// channel-last in LDS (one 16-byte read per A fragment), pixel slots
-// row-major with the k-wide zero halo; a tap is one of two fixed slot offsets
-// chosen by the column parity of the lane's pixel.  The tile is staged from
-// NCHW through registers with an 8x8 bf16 transpose.
+// The contraction index runs over taps, then input channels, so the 8 A
+// values of a lane are 8 consecutive channels of one pixel.
 //
-// Block: full-width tile of TR rows, 64 output channels (grid.y covers more),
-// 4 waves = 2 channel halves x 2 pixel halves; each wave accumulates up to 8
-// pixel tiles x 2 channel tiles.  Weights (B) are held in registers, KC
-// K-steps at a time.  The result goes through LDS so that global stores are
-// contiguous 16-byte rows.
+// Common to both kernels below: the input window of a pixel tile (full-width
+// rows plus k halo rows, k zero columns on each side) is staged channel-last
+// in LDS from contiguous 8-pixel chunks of the NCHW planes through an 8x8
+// register transpose, so an A fragment is one 16-byte LDS read and a tap is
+// a fixed slot offset (one window row further for odd tap columns when the
+// pixel's column is odd).  The weights of a block's output channels are
+// copied once from global memory (16-byte coalesced loads) into LDS as
+// [oc][t][ic], where a B fragment is one 16-byte read, and then held in
+// registers or kept resident in LDS.  Results get bias, ReLU and round-to-
+// nearest-even in registers, go through LDS as [oc][pixel], and leave as
+// contiguous 16-byte stores.  LDS pitches follow measured bank behaviour of
+// gfx950: 16-byte fragment reads of 32 rows are conflict-free at a row pitch
+// that is an odd multiple of 16 bytes, of 16 rows at 32 mod 64 bytes;
+// 8-byte writes of 16 or 32 rows at 8 mod 16 bytes.
+//
+// conv_bf16_wide32_k (preferred): v_mfma_f32_32x32x16_bf16, one block of 8
+// waves per CU, each block a contiguous run of row tiles, the next tile's
+// window prefetched into registers while the current one is computed, the A
+// fragments of the next two K-steps in flight.  The 32x32 instruction keeps
+// the matrix cores at about 2 PFLOP/s with one or two waves per SIMD, where
+// the 16x16 one needs more waves than the registers allow.
+// conv_bf16_wide_k (fallback for other channel counts): 16x16x32, 4 waves,
+// two blocks per CU, pixel tiles handed out so that the blocks of one XCD
+// work on neighbouring tiles at the same time.
 #include <algorithm>
 
 #include "hexdev.h"
@@ -31,16 +44,29 @@ namespace {
 using namespace hexgeom;
 
 typedef float floatx4 __attribute__((ext_vector_type(4)));
+typedef float floatx16 __attribute__((ext_vector_type(16)));
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 
 constexpr int kThreads = 256;
-constexpr int kMT = 8; // pixel tiles (of 16) per wave
-constexpr int kOCB = 64; // output channels per block
+constexpr int kWaves = kThreads / 64;
+constexpr int kXcd = 8;
 
-struct WideTiling {
-    int TR, npix_max, LCP, CS; // LCP: slots per LDS row; CS: bf16 per pixel slot
-    int ntiles;              // tiles per image
-    int IC, OC, KS;          // input / output channels, K-steps (32 each)
+struct WideArgs {
+    int N, H, W;
+    int IC, OC;         // channels of the kernel's input and output tensors
+    int KS;             // K-steps: T * IC / 32
+    int TR, ntr;        // rows per pixel tile, pixel tiles per image
+    int ptiles;         // pixel tiles in the batch
+    int nocc;           // output-channel chunks
+    int spx;            // tile slots per XCD (per chunk)
+    int nslots;         // tile slots per chunk (= 8 * spx)
+    int LCP, CS;        // input window: slots per row, bf16 per slot
+    int OP;             // output staging pitch (bf16 per channel)
+    int WP;             // weight row pitch in LDS (bf16 per output channel)
+    int tile_off;       // byte offset of the tile region in LDS
+    int vec_out;        // 16-byte output stores allowed
+    int wgroups;        // channel groups whose weights are copied per pass (registers mode)
+    int per_block;      // pixel tiles per block (prefetching kernel)
 };
 
 __device__ __forceinline__ uint32_t perm(uint32_t hi, uint32_t lo, uint32_t sel)
@@ -48,262 +74,850 @@ __device__ __forceinline__ uint32_t perm(uint32_t hi, uint32_t lo, uint32_t sel)
     return __builtin_amdgcn_perm(hi, lo, sel);
 }
 
-// Stage a full-width window (rows r0-K .. r0+rows+K-1, columns -K .. W+K-1)
-// of IC channels into LDS, channel-last: element (r, c, ic) at
-// (((r - r_lo) * LCP + c - c_lo) * CS + ic).  Work item = (8-channel group, window row, 8-column
-// group): 8 loads of 16 bytes, an 8x8 transpose, 8 stores of 16 bytes.
-struct WideWindow {
-    int r_lo, c_lo, LR, LC;
-    __device__ __forceinline__ int slot(int r, int c, int LCP) const
-    {
-        return (r - r_lo) * LCP + (c - c_lo);
-    }
-};
+typedef float floatx2 __attribute__((ext_vector_type(2)));
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 
-__device__ __forceinline__ void stage_wide(bf16raw *__restrict__ lds, const bf16raw *__restrict__ src,
-                                           size_t HW, int H, int W, int IC, const WideWindow &tl,
-                                           int LCP, int CS)
+// two floats -> two bf16 (round to nearest even) in one dword, lo first;
+// gfx950 converts a pair in one instruction
+__device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi)
 {
-    const int a8 = (tl.c_lo >= 0 ? tl.c_lo : tl.c_lo - 7) / 8 * 8;
-    const int ng = (tl.c_lo + tl.LC - a8 + 7) / 8;
-    const int items = (IC / 8) * tl.LR * ng;
-    for (int it0 = threadIdx.x; it0 < items; it0 += 2 * kThreads) {
-        uint4 in[2][8];
-        int cq[2], rq[2], gq[2];
-        bool live[2], rowok[2];
+    return __builtin_bit_cast(uint32_t, __builtin_convertvector(floatx2{lo, hi}, bf16x2));
+}
+
+// Copy the weights of kernel-output channels [o_lo, o_lo + nrow) into LDS
+// as wl[ocl * WP + t * IC + ic] (zero for channels >= OC).  Every load of a
+// thread is issued before the first LDS write, so the copy costs about one
+// memory latency.
+//   forward, w[oc][ic][t]: the rows form one contiguous run whose length
+//     and start are multiples of 32 elements (IC % 32 == 0): 16-byte loads,
+//     8 consecutive (ic, t) per load;
+//   data gradient, w[ic][oc][t] (ic = the convolution's output channel):
+//     one run of nrow * T elements per ic, read element by element.
+template <int T, bool REFLECT, int NTHR = kThreads>
+__device__ __forceinline__ void stage_weights(bf16raw *__restrict__ wl, const bf16raw *__restrict__ w,
+                                              int o_lo, int nrow, int IC, int OC, int WP)
+{
+    const int nval = max(0, min(nrow, OC - o_lo)); // rows that exist
+    constexpr int U = 8;
+    if constexpr (!REFLECT) {
+        const int per = IC * T;                     // elements per row, a multiple of 32
+        const int nchunk = nrow * per / 8;
+        const int nvchunk = nval * per / 8;
+        const bf16raw *src = w + static_cast<size_t>(o_lo) * per;
+        for (int q0 = threadIdx.x; q0 < nchunk; q0 += U * NTHR) {
+            uint4 v[U];
 #pragma unroll
-        for (int h = 0; h < 2; ++h) {
-            const int it = it0 + h * kThreads;
-            live[h] = it < items;
-            const int g = it % ng;
-            const int rest = it / ng;
-            const int rr = rest % tl.LR;
-            const int cg = rest / tl.LR;
-            cq[h] = cg;
-            rq[h] = rr;
-            gq[h] = g;
-            const int r = tl.r_lo + rr;
-            const int c = a8 + 8 * g;
-            rowok[h] = live[h] && r >= 0 && r < H && c >= 0 && c + 7 < W;
+            for (int u = 0; u < U; ++u) {
+                const int q = q0 + u * NTHR;
+                v[u] = q < nvchunk ? *reinterpret_cast<const uint4 *>(src + 8 * static_cast<size_t>(q))
+                                   : make_uint4(0, 0, 0, 0);
+            }
 #pragma unroll
-            for (int j = 0; j < 8; ++j) {
-                const bf16raw *p =
-                    src + (rowok[h] ? (static_cast<size_t>(cg * 8 + j) * HW + static_cast<size_t>(r) * W + c)
-                                    : 0);
-                in[h][j] = *reinterpret_cast<const uint4 *>(p);
+            for (int u = 0; u < U; ++u) {
+                const int q = q0 + u * NTHR;
+                if (q >= nchunk)
+                    break;
+                const int ocl = (8 * q) / per;      // a chunk never straddles two rows
+                const int rem = 8 * q - ocl * per;
+                int ic = rem / T, t = rem - (rem / T) * T;
+                bf16raw *dst = wl + ocl * WP;
+                const bf16raw *e = reinterpret_cast<const bf16raw *>(&v[u]);
+#pragma unroll
+                for (int j = 0; j < 8; ++j) {
+                    dst[t * IC + ic] = e[j];
+                    if (++t == T) {
+                        t = 0;
+                        ++ic;
+                    }
+                }
             }
         }
+    } else {
+        const int run = nrow * T;                   // per ic
+        const int vrun = nval * T;
+        const int total = IC * run;
+        for (int e0 = threadIdx.x; e0 < total; e0 += U * NTHR) {
+            bf16raw v[U];
+            int dsti[U];
 #pragma unroll
-        for (int h = 0; h < 2; ++h) {
-            if (!live[h])
-                continue;
-            const int c = a8 + 8 * gq[h];
-            const int r = tl.r_lo + rq[h];
-#pragma unroll
-            for (int px = 0; px < 8; ++px) {
-                const int cc = c + px;
-                if (cc < tl.c_lo || cc >= tl.c_lo + tl.LC)
-                    continue;
-                const uint32_t sel = (px & 1) ? 0x07060302u : 0x05040100u;
-                uint4 o;
-                // channel pair (2e, 2e+1) of pixel px: dword px/2 of rows 2e, 2e+1
-                uint32_t w4[4];
-#pragma unroll
-                for (int e = 0; e < 4; ++e) {
-                    const uint32_t lo = reinterpret_cast<const uint32_t *>(&in[h][2 * e])[px >> 1];
-                    const uint32_t hi = reinterpret_cast<const uint32_t *>(&in[h][2 * e + 1])[px >> 1];
-                    w4[e] = perm(hi, lo, sel);
-                }
-                o.x = rowok[h] ? w4[0] : 0u;
-                o.y = rowok[h] ? w4[1] : 0u;
-                o.z = rowok[h] ? w4[2] : 0u;
-                o.w = rowok[h] ? w4[3] : 0u;
-                *reinterpret_cast<uint4 *>(lds + static_cast<size_t>(tl.slot(r, cc, LCP)) * CS +
-                                           cq[h] * 8) = o;
+            for (int u = 0; u < U; ++u) {
+                const int e = e0 + u * NTHR;
+                const int ic = e / run;
+                const int rest = e - ic * run;
+                const int ocl = rest / T, tn = rest - (rest / T) * T;
+                const bool ok = e < total && rest < vrun;
+                v[u] = ok ? w[(static_cast<size_t>(ic) * OC + o_lo) * T + rest] : bf16raw(0);
+                dsti[u] = e < total ? ocl * WP + (T - 1 - tn) * IC + ic : -1;
             }
+#pragma unroll
+            for (int u = 0; u < U; ++u)
+                if (dsti[u] >= 0)
+                    wl[dsti[u]] = v[u];
         }
     }
 }
 
-template <int K, int KC, bool REFLECT>
-__global__ __launch_bounds__(kThreads, 2) void conv_bf16_wide_k(
+// Input window of a pixel tile (rows r0-K .. r0+rows+K-1 of one image, all
+// IC channels), staged channel-last into LDS at slot ((r - r0 + K) * LCP +
+// c + K).  The rows inside the image are one contiguous run of each NCHW
+// plane; a work item is one 8-channel group of one 8-element chunk of that
+// run (chunks aligned to 8 elements), consecutive items take consecutive
+// channel groups.  load() reads U items of this thread (items it0 + h *
+// 256) into registers, commit() transposes them (8 x 8 bf16) into 8 pixel
+// slots; zero_halo() clears the K columns on each side and the window rows
+// outside the image.
+struct WideWindow {
+    int e_lo, e_hi, e_al, items, rbase, ra, rb, rows;
+    __device__ __forceinline__ WideWindow(int K, int H, int W, int IC, int r0, int rows_)
+    {
+        rows = rows_;
+        rbase = r0 - K;
+        ra = max(r0 - K, 0);
+        rb = min(r0 + rows_ + K, H);
+        e_lo = ra * W;
+        e_hi = rb * W;
+        e_al = e_lo & ~7;
+        items = (IC >> 3) * ((e_hi - e_al + 7) >> 3);
+    }
+};
+
+template <int K, int U, int NTHR = kThreads> struct WideTileRegs {
+    uint4 v[U][8];
+    int eb[U], cg[U];
+
+    __device__ __forceinline__ void load(const bf16raw *__restrict__ src, const WideWindow &wd,
+                                         int HW, int IC, int it0)
+    {
+        const int ncg = IC >> 3;
+#pragma unroll
+        for (int h = 0; h < U; ++h) {
+            const int it = it0 + h * NTHR;
+            const bool live = it < wd.items;
+            const int ch = live ? it / ncg : 0;
+            cg[h] = live ? it - ch * ncg : 0;
+            // e_al + 8*ch is a multiple of 8 below e_hi <= H*W (a multiple
+            // of 8): all 8 elements lie inside the plane
+            const int e0 = wd.e_al + 8 * ch;
+#pragma unroll
+            for (int j = 0; j < 8; ++j)
+                v[h][j] = *reinterpret_cast<const uint4 *>(
+                    src + static_cast<size_t>(cg[h] * 8 + j) * HW + e0);
+            eb[h] = live ? e0 : -1;
+        }
+    }
+
+    __device__ __forceinline__ void commit(bf16raw *__restrict__ tl, const WideWindow &wd, int W,
+                                           int LCP, int CS) const
+    {
+#pragma unroll
+        for (int h = 0; h < U; ++h) {
+            if (eb[h] < 0)
+                continue;
+            // the 8 pixels eb..eb+7 cross at most one row end (W >= 8); slot =
+            // window-relative element + 2K per row end crossed + K
+            const int r = eb[h] / W;
+            const int c = eb[h] - r * W;
+            const int base = (eb[h] - wd.rbase * W) + (r - wd.rbase) * 2 * K + K;
+#pragma unroll
+            for (int px = 0; px < 8; ++px) {
+                const int e = eb[h] + px;
+                const int brk = (c + px >= W) ? 1 : 0;
+                const uint32_t sel = (px & 1) ? 0x07060302u : 0x05040100u;
+                uint32_t w4[4];
+#pragma unroll
+                for (int q = 0; q < 4; ++q) {
+                    const uint32_t lo = reinterpret_cast<const uint32_t *>(&v[h][2 * q])[px >> 1];
+                    const uint32_t hi = reinterpret_cast<const uint32_t *>(&v[h][2 * q + 1])[px >> 1];
+                    w4[q] = perm(hi, lo, sel);
+                }
+                const int slot = base + px + brk * 2 * K;
+                if (e >= wd.e_lo && e < wd.e_hi)
+                    *reinterpret_cast<uint4 *>(tl + static_cast<size_t>(slot) * CS + cg[h] * 8) =
+                        make_uint4(w4[0], w4[1], w4[2], w4[3]);
+            }
+        }
+    }
+};
+
+template <int K, int NTHR = kThreads>
+__device__ __forceinline__ void zero_halo(bf16raw *__restrict__ tl, const WideWindow &wd, int W,
+                                          int IC, int LCP, int CS)
+{
+    const int LR = wd.rows + 2 * K;
+    const int v8 = IC >> 3; // 16-byte vectors per slot holding data
+    const int side = LR * 2 * K;
+    const int nlo = wd.ra - wd.rbase;                 // window rows above the image
+    const int out_rows = nlo + (wd.rbase + LR - wd.rb); // ... plus below it
+    const int total = (side + out_rows * LCP) * v8;
+    for (int e = threadIdx.x; e < total; e += NTHR) {
+        const int s = e / v8, q = e - s * v8;
+        int slot;
+        if (s < side) {
+            const int rr = s / (2 * K), j = s - rr * 2 * K;
+            slot = rr * LCP + (j < K ? j : W + j);
+        } else {
+            const int s2 = s - side;
+            const int orow = s2 / LCP, c = s2 - orow * LCP;
+            const int rr = orow < nlo ? orow : (wd.rb - wd.rbase) + (orow - nlo);
+            slot = rr * LCP + c;
+        }
+        *reinterpret_cast<uint4 *>(tl + static_cast<size_t>(slot) * CS + q * 8) = make_uint4(0, 0, 0, 0);
+    }
+}
+
+// Whole window, U items per thread per round.
+template <int K, int U>
+__device__ __forceinline__ void stage_tile(bf16raw *__restrict__ tl, const bf16raw *__restrict__ src,
+                                           int H, int W, int IC, int r0, int rows, int LCP, int CS)
+{
+    const WideWindow wd(K, H, W, IC, r0, rows);
+    for (int it0 = threadIdx.x; it0 < wd.items; it0 += U * kThreads) {
+        WideTileRegs<K, U> g;
+        g.load(src, wd, H * W, IC, it0);
+        g.commit(tl, wd, W, LCP, CS);
+    }
+    zero_halo<K>(tl, wd, W, IC, LCP, CS);
+}
+
+// Epilogue of a pixel tile, first half: bias, ReLU and bf16 rounding of
+// this wave's MT x NT accumulator tiles into LDS as [oc][pixel] with pitch
+// OP (OP = 4 mod 8: the 8-byte writes of 16 channel rows hit distinct
+// banks).  Rows of pixels past the tile's end hold garbage, never stored.
+template <int NT, int PW, int MT>
+__device__ __forceinline__ void wide_epilogue(bf16raw *__restrict__ outl, int OP,
+                                              const floatx4 (&acc)[MT][NT], const float (&bv)[NT],
+                                              int ocl0, int pg, int m, int kq, int relu)
+{
+#pragma unroll
+    for (int j = 0; j < NT; ++j) {
+        const int ocl = ocl0 + j * 16 + m;
+#pragma unroll
+        for (int i = 0; i < MT; ++i) {
+            const int q0 = (pg + PW * i) * 16 + 4 * kq;
+            float v[4];
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+                v[r] = acc[i][j][r] + bv[j];
+                if (relu)
+                    v[r] = fmaxf(v[r], 0.f);
+            }
+            *reinterpret_cast<uint2 *>(outl + ocl * OP + q0) =
+                make_uint2(pack_bf16x2(v[0], v[1]), pack_bf16x2(v[2], v[3]));
+        }
+    }
+}
+
+// Second half: 16-byte stores of noc channel rows of npix pixels (npix % 8
+// == 0) from the LDS tile (row pitch OP, rows 8-byte aligned) to y_base +
+// ocl * HW.  Every thread issues exactly NST stores (NV = 16-byte vectors per
+// full row); lanes past the end repeat a valid vector -- the same data to the
+// same address -- so the number of outstanding memory operations is known at
+// compile time and a later wait for loads does not wait for these stores.
+template <int NST, int NV, int NTHR = kThreads>
+__device__ __forceinline__ void wide_store(bf16raw *__restrict__ y_base, size_t HW,
+                                           const bf16raw *__restrict__ outl, int OP, int noc,
+                                           int npix)
+{
+    const int nvec = npix >> 3;
+#pragma unroll
+    for (int st = 0; st < NST; ++st) {
+        const int e = threadIdx.x + st * NTHR;
+        const int ocl = min(e / NV, noc - 1);
+        const int v8 = min(e - (e / NV) * NV, nvec - 1);
+        const bf16raw *src = outl + ocl * OP + v8 * 8;
+        const uint2 lo = *reinterpret_cast<const uint2 *>(src);
+        const uint2 hi = *reinterpret_cast<const uint2 *>(src + 4);
+        *reinterpret_cast<uint4 *>(y_base + static_cast<size_t>(ocl) * HW + v8 * 8) =
+            make_uint4(lo.x, lo.y, hi.x, hi.y);
+    }
+}
+
+// Scalar variant for tiles whose rows do not start on 8-element boundaries.
+template <int NTHR = kThreads>
+__device__ __forceinline__ void wide_store_scalar(bf16raw *__restrict__ y_base, size_t HW,
+                                                  const bf16raw *__restrict__ outl, int OP,
+                                                  int noc, int npix)
+{
+    for (int e = threadIdx.x; e < noc * npix; e += NTHR) {
+        const int ocl = e / npix, p = e - ocl * npix;
+        y_base[static_cast<size_t>(ocl) * HW + p] = outl[ocl * OP + p];
+    }
+}
+
+// One K-step for the wave's MT pixel tiles and NT channel tiles: the tap
+// (dq, ds) of step ks, read at each A row's centre slot plus the tap's slot
+// offset (one window row further for odd tap columns when the lane's pixel
+// column is odd).  Rows past the tile's last pixel read a clamped, valid
+// centre; their results are never stored.
+template <int K, int NT, int MT>
+__device__ __forceinline__ void wide_kstep(floatx4 (&acc)[MT][NT], const bf16x8 (&bq)[NT],
+                                           const unsigned char *__restrict__ tlb,
+                                           const int (&adr)[MT], int oddoff, int t, int icoff,
+                                           int rowb, int slotb)
+{
+    int dq = 0, ds = 0;
+    tap_axial(K, t, dq, ds);
+    const int toff = (ds + floor_half(dq)) * rowb + dq * slotb + icoff + ((dq & 1) ? oddoff : 0);
+    uint4 qa[MT];
+#pragma unroll
+    for (int i = 0; i < MT; ++i)
+        qa[i] = *reinterpret_cast<const uint4 *>(tlb + adr[i] + toff);
+#pragma unroll
+    for (int i = 0; i < MT; ++i) {
+        const bf16x8 av = __builtin_bit_cast(bf16x8, qa[i]);
+#pragma unroll
+        for (int j = 0; j < NT; ++j)
+            acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av, bq[j], acc[i][j], 0, 0, 0);
+    }
+}
+
+// KS > 0: B fragments of all KS K-steps held in registers; KS == 0: read
+// from the LDS-resident weights every K-step (a.KS K-steps).
+// Wave w: pixel group w % PW (pixel tiles w % PW + PW * i, i < MT) and
+// output-channel group w / PW (NT tiles of 16 channels).
+template <int K, int KS, int NT, int PW, int MT, bool REFLECT>
+__global__ __launch_bounds__(kThreads, KS > 0 ? 2 : 1) void conv_bf16_wide_k(
     const bf16raw *__restrict__ xin, const bf16raw *__restrict__ w, const bf16raw *__restrict__ bias,
-    bf16raw *__restrict__ y, ConvShape sh, int relu, WideTiling tg)
+    bf16raw *__restrict__ y, WideArgs a, int relu)
 {
     constexpr int T = num_taps(K);
-    extern __shared__ __align__(16) bf16raw lds[];
-    const int H = sh.H, W = sh.W;
-    const size_t HW = static_cast<size_t>(H) * W;
-    const int IC = tg.IC, OC = tg.OC;
-    const int n = blockIdx.x / tg.ntiles;
-    const int r0 = (blockIdx.x - n * tg.ntiles) * tg.TR;
-    const int rows = min(tg.TR, H - r0);
-    const int npix = rows * W;
-    const WideWindow tl{r0 - K, -K, rows + 2 * K, W + 2 * K};
-    const int oc_blk = blockIdx.y * kOCB;
-
-    stage_wide(lds, xin + static_cast<size_t>(n) * IC * HW, HW, H, W, IC, tl, tg.LCP, tg.CS);
+    constexpr bool WL = KS == 0;
+    constexpr int OG = kWaves / PW;
+    constexpr int OCB = OG * NT * 16;
+    constexpr int ICB = WL ? 1 : KS / T; // 32-channel blocks per tap (registers mode)
+    extern __shared__ __align__(16) unsigned char smem[];
+    bf16raw *wl = reinterpret_cast<bf16raw *>(smem);
+    bf16raw *tl = reinterpret_cast<bf16raw *>(smem + a.tile_off);
 
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     const int m = lane & 15, kq = lane >> 4;
-    const int ph = wave & 1;        // pixel half
-    const int oh = wave >> 1;       // output-channel half (32 channels)
-    const int ntile = (npix + 15) / 16;
+    const int pg = wave % PW, og = wave / PW;
 
-    // centre slots and column parity of this lane's A rows
-    int cen[kMT];
-    bool pv[kMT], podd[kMT];
+    // persistent work: a fixed channel chunk and strided pixel-tile slots
+    const int b = blockIdx.x;
+    const int xcd = b % kXcd, jj = b / kXcd;
+    const int occ = jj % a.nocc, sj = jj / a.nocc;
+    const int slot0 = xcd * a.spx + sj;
+    const int oc_base = occ * OCB;
+    const bool wave_live = oc_base + og * NT * 16 < a.OC;
+
+    // ---- weights
+    bf16x8 bfr[WL ? 1 : KS][NT];
+    if constexpr (WL) {
+        stage_weights<T, REFLECT>(wl, w, oc_base, OCB, a.IC, a.OC, a.WP);
+    } else {
+        // through the tile region: all channel groups at once if they fit
+        // (a.wgroups == OG), else one group at a time
+        for (int g = 0; g < OG; g += a.wgroups) {
+            __syncthreads();
+            stage_weights<T, REFLECT>(tl, w, oc_base + g * NT * 16, a.wgroups * NT * 16, a.IC,
+                                      a.OC, a.WP);
+            __syncthreads();
+            if (og >= g && og < g + a.wgroups) {
 #pragma unroll
-    for (int i = 0; i < kMT; ++i) {
-        const int mt = ph + 2 * i;
-        const int p = mt * 16 + m;
-        pv[i] = mt < ntile && p < npix;
-        const int pr = pv[i] ? p / W : 0, pc = pv[i] ? p - pr * W : 0;
-        cen[i] = tl.slot(r0 + pr, pc, tg.LCP);
-        podd[i] = (pc & 1) != 0;
+                for (int ks = 0; ks < KS; ++ks)
+#pragma unroll
+                    for (int j = 0; j < NT; ++j)
+                        bfr[ks][j] = *reinterpret_cast<const bf16x8 *>(
+                            tl + ((og - g) * NT * 16 + j * 16 + m) * a.WP + ks * 32 + 8 * kq);
+            }
+        }
     }
-    floatx4 acc[kMT][2];
-#pragma unroll
-    for (int i = 0; i < kMT; ++i)
-#pragma unroll
-        for (int j = 0; j < 2; ++j)
-            acc[i][j] = floatx4{0.f, 0.f, 0.f, 0.f};
-    __syncthreads();
 
-    const int icb = IC / 32; // K-steps per tap
-    for (int s0 = 0; s0 < tg.KS; s0 += KC) {
-        // B fragments for K-steps s0 .. s0+KC-1 and this wave's 2 channel tiles
-        bf16x8 bfr[KC][2];
+    const int H = a.H, W = a.W;
+    const int HW = H * W;
+    const int rowb = a.LCP * a.CS * 2; // bytes per window row
+    const int slotb = a.CS * 2;        // bytes per slot
+    const unsigned char *tlb = reinterpret_cast<const unsigned char *>(tl);
+    float bv[NT];
 #pragma unroll
-        for (int s = 0; s < KC; ++s) {
-            const int ks = s0 + s;
-            const int t = ks / icb;
-            const int ic0 = (ks - t * icb) * 32 + 8 * kq;
+    for (int j = 0; j < NT; ++j) {
+        const int oc = oc_base + og * NT * 16 + j * 16 + m;
+        bv[j] = (bias != nullptr && oc < a.OC) ? to_f(bias[oc]) : 0.f;
+    }
+
+    for (int pt = slot0; pt < a.ptiles; pt += a.nslots) {
+        const int n = pt / a.ntr;
+        const int r0 = (pt - n * a.ntr) * a.TR;
+        const int rows = min(a.TR, H - r0);
+        const int npix = rows * W;
+
+        __syncthreads(); // the previous tile's (or the weight copy's) LDS reads are done
+        stage_tile<K, (KS >= 14) ? 1 : 2>(tl, xin + static_cast<size_t>(n) * a.IC * HW, H, W, a.IC, r0, rows, a.LCP,
+                      a.CS);
+        __syncthreads();
+
+        // centre-slot byte address of this lane's A row in each tile (W is
+        // even and tiles start on multiples of 16 pixels, so the column
+        // parity of the lane's pixel is the parity of m)
+        int adr[MT];
 #pragma unroll
-            for (int j = 0; j < 2; ++j) {
-                const int oc = oc_blk + oh * 32 + j * 16 + m;
+        for (int i = 0; i < MT; ++i) {
+            const int p = min((pg + PW * i) * 16 + m, npix - 1);
+            const int pr = p / W, pc = p - pr * W;
+            adr[i] = ((pr + K) * a.LCP + pc + K) * slotb + kq * 16;
+        }
+        const int oddoff = (m & 1) ? rowb : 0;
+        floatx4 acc[MT][NT];
 #pragma unroll
-                for (int e = 0; e < 8; ++e) {
-                    bf16raw v = 0;
-                    if (ks < tg.KS && oc < OC) {
-                        const int ic = ic0 + e;
-                        v = REFLECT ? w[(static_cast<size_t>(ic) * OC + oc) * T + (T - 1 - t)]
-                                    : w[(static_cast<size_t>(oc) * IC + ic) * T + t];
+        for (int i = 0; i < MT; ++i)
+#pragma unroll
+            for (int j = 0; j < NT; ++j)
+                acc[i][j] = floatx4{0.f, 0.f, 0.f, 0.f};
+
+        if (wave_live) {
+            if constexpr (WL) {
+                const int icb = a.IC >> 5;
+                const bf16raw *wrow = wl + (og * NT * 16 + m) * a.WP + 8 * kq;
+                for (int ks = 0; ks < a.KS; ++ks) {
+                    const int t = ks / icb;
+                    bf16x8 bq[NT];
+#pragma unroll
+                    for (int j = 0; j < NT; ++j)
+                        bq[j] = *reinterpret_cast<const bf16x8 *>(wrow + j * 16 * a.WP + ks * 32);
+                    wide_kstep<K, NT, MT>(acc, bq, tlb, adr, oddoff, t, (ks - t * icb) * 64,
+                                          rowb, slotb);
+                }
+            } else {
+#pragma unroll
+                for (int ks = 0; ks < KS; ++ks) {
+                    // bound the scheduler's hoisting of fragment loads to one
+                    // K-step (the weights already hold most registers)
+                    __builtin_amdgcn_sched_barrier(0);
+                    wide_kstep<K, NT, MT>(acc, bfr[ks], tlb, adr, oddoff, ks / ICB,
+                                          (ks % ICB) * 64, rowb, slotb);
+                }
+            }
+        }
+
+        // epilogue: bias, ReLU, bf16 into LDS as [oc][pixel], then 16-byte stores
+        __syncthreads();
+        bf16raw *outl = tl;
+        if (wave_live)
+            wide_epilogue<NT, PW, MT>(outl, a.OP, acc, bv, og * NT * 16, pg, m, kq, relu);
+        __syncthreads();
+        const int noc = min(OCB, a.OC - oc_base);
+        bf16raw *ybase =
+            y + (static_cast<size_t>(n) * a.OC + oc_base) * HW + static_cast<size_t>(r0) * W;
+        if (a.vec_out)
+            wide_store<(OCB * PW * MT * 2 + kThreads - 1) / kThreads, PW * MT * 2>(ybase, HW, outl,
+                                                                                  a.OP, noc, npix);
+        else
+            wide_store_scalar(ybase, HW, outl, a.OP, noc, npix);
+    }
+}
+
+// ---------------------------------------------------------------------------
+// 32x32x16 kernel.  v_mfma_f32_32x32x16_bf16 (lane layout checked on the
+// device): a[i] = A[lane % 32][8 * (lane / 32) + i],
+// b[i] = B[8 * (lane / 32) + i][lane % 32],
+// d[r] = D[8 * (r / 4) + 4 * (lane / 32) + r % 4][lane % 32].
+// A = 32 pixels x 16 channels of one tap (one 16-byte LDS read per lane),
+// B = 16 channels x 32 output channels, D = 32 pixels x 32 output channels:
+// each lane ends with 4 runs of 4 consecutive pixels of one channel.
+// K-step ks covers tap ks / (IC/16) and channels 16 * (ks % (IC/16)) + 0..15.
+//
+// One block of 8 waves per CU (two waves per SIMD): wave w computes output
+// channels 32 * (w / PW) .. +31 for pixel tiles (w % PW) + PW * i, i < MT,
+// of 32 pixels each.  Block b owns the contiguous pixel tiles
+// [b * per, (b + 1) * per) -- consecutive row tiles, whose shared halo rows
+// the same CU has just read and finds in its L2 -- and loads the next tile's
+// window into registers while it computes the current one.  The weights of
+// the block's channels are held in registers (KS > 0: KS K-steps) or stay
+// resident in LDS (KS == 0, for long contractions: a.KS K-steps).
+constexpr int kThreads32 = 512;
+
+template <int K, int KS, bool WL, int OG, int PW, int MT, bool REFLECT>
+__global__ __launch_bounds__(kThreads32) void conv_bf16_wide32_k(
+    const bf16raw *__restrict__ xin, const bf16raw *__restrict__ w, const bf16raw *__restrict__ bias,
+    bf16raw *__restrict__ y, WideArgs a, int relu)
+{
+    static_assert(OG * PW == kThreads32 / 64, "8 waves");
+    constexpr int T = num_taps(K);
+    static_assert(KS % T == 0, "whole 16-channel blocks per tap");
+    constexpr int ICB = KS / T; // 16-channel blocks per tap
+    constexpr int OCB = OG * 32;
+    constexpr int PIX = PW * MT * 32;
+    extern __shared__ __align__(16) unsigned char smem[];
+    bf16raw *wl = reinterpret_cast<bf16raw *>(smem);
+    bf16raw *tl = reinterpret_cast<bf16raw *>(smem + a.tile_off);
+
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int n32 = lane & 31, kh = lane >> 5;
+    const int pg = wave % PW, og = wave / PW;
+
+    // block -> (channel chunk, run of tiles); the chunks of one run are 8
+    // blocks apart, i.e. on the same XCD, and share its L2
+    const int xcd = blockIdx.x % kXcd, jj = blockIdx.x / kXcd;
+    const int occ = jj % a.nocc;
+    const int slot = (jj / a.nocc) * kXcd + xcd;
+    const int oc_base = occ * OCB;
+    const int OCc = min(OCB, a.OC - oc_base); // channels of this chunk
+    const bool wave_live = og * 32 < OCc;
+    const int t_begin = slot * a.per_block;
+    const int t_end = min(t_begin + a.per_block, a.ptiles);
+    if (t_begin >= t_end)
+        return; // the whole block
+
+    // ---- weights
+    bf16x8 bfr[WL ? 1 : KS];
+    (void)bfr;
+    if constexpr (WL) {
+        stage_weights<T, REFLECT, kThreads32>(wl, w, oc_base, OCB, a.IC, a.OC, a.WP);
+    } else {
+        for (int g = 0; g < OG; g += a.wgroups) {
+            __syncthreads();
+            stage_weights<T, REFLECT, kThreads32>(tl, w, oc_base + g * 32, a.wgroups * 32, a.IC,
+                                                  a.OC, a.WP);
+            __syncthreads();
+            if (og >= g && og < g + a.wgroups) {
+#pragma unroll
+                for (int ks = 0; ks < KS; ++ks)
+                    bfr[ks] = *reinterpret_cast<const bf16x8 *>(
+                        tl + ((og - g) * 32 + n32) * a.WP + ks * 16 + 8 * kh);
+            }
+        }
+    }
+    float bv;
+    {
+        const int oc = oc_base + og * 32 + n32;
+        bv = (bias != nullptr && oc < a.OC) ? to_f(bias[oc]) : 0.f;
+    }
+
+    const int H = a.H, W = a.W;
+    const int HW = H * W;
+    const int rowb = a.LCP * a.CS * 2;
+    const int slotb = a.CS * 2;
+    const unsigned char *tlb = reinterpret_cast<const unsigned char *>(tl);
+    const int oddoff = (n32 & 1) ? rowb : 0; // W even, tiles on multiples of 32: parity of n32
+    const bf16raw *wrow = wl + (og * 32 + n32) * a.WP + 8 * kh;
+
+    WideTileRegs<K, 1, kThreads32> g;
+    {
+        const int n = t_begin / a.ntr;
+        const int r0 = (t_begin - n * a.ntr) * a.TR;
+        const WideWindow wd(K, H, W, a.IC, r0, min(a.TR, H - r0));
+        g.load(xin + static_cast<size_t>(n) * a.IC * HW, wd, HW, a.IC, threadIdx.x);
+    }
+    for (int pt = t_begin; pt < t_end; ++pt) {
+        const int n = pt / a.ntr;
+        const int r0 = (pt - n * a.ntr) * a.TR;
+        const int rows = min(a.TR, H - r0);
+        const int npix = rows * W;
+        const WideWindow wd(K, H, W, a.IC, r0, rows);
+
+        __syncthreads(); // the previous tile's (or the weight copy's) LDS reads are done
+        g.commit(tl, wd, W, a.LCP, a.CS);
+        zero_halo<K, kThreads32>(tl, wd, W, a.IC, a.LCP, a.CS);
+        __syncthreads();
+        if (pt + 1 < t_end) {
+            const int n2 = (pt + 1) / a.ntr;
+            const int r2 = (pt + 1 - n2 * a.ntr) * a.TR;
+            const WideWindow wd2(K, H, W, a.IC, r2, min(a.TR, H - r2));
+            g.load(xin + static_cast<size_t>(n2) * a.IC * HW, wd2, HW, a.IC, threadIdx.x);
+        }
+
+        // A-row (pixel) slot addresses; pixels past the tile read a clamped
+        // valid centre, their results are never stored
+        int adr[MT];
+#pragma unroll
+        for (int i = 0; i < MT; ++i) {
+            const int p = min((pg + PW * i) * 32 + n32, npix - 1);
+            const int pr = p / W, pc = p - pr * W;
+            adr[i] = ((pr + K) * a.LCP + pc + K) * slotb + kh * 16;
+        }
+        floatx16 acc[MT];
+#pragma unroll
+        for (int i = 0; i < MT; ++i)
+#pragma unroll
+            for (int r = 0; r < 16; ++r)
+                acc[i][r] = 0.f;
+
+        if (wave_live) {
+            // the tap and channel block of K-step ks are compile-time
+            // constants once the loop is unrolled
+            auto fetch_a = [&](uint4(&q)[MT], int ks) {
+                const int t = ks / ICB;
+                int dq = 0, ds = 0;
+                tap_axial(K, t, dq, ds);
+                const int toff = (ds + floor_half(dq)) * rowb + dq * slotb + (ks % ICB) * 32 +
+                                 ((dq & 1) ? oddoff : 0);
+#pragma unroll
+                for (int i = 0; i < MT; ++i)
+                    q[i] = *reinterpret_cast<const uint4 *>(tlb + adr[i] + toff);
+            };
+            auto fetch_b = [&](int ks) -> bf16x8 {
+                if constexpr (WL)
+                    return *reinterpret_cast<const bf16x8 *>(wrow + ks * 16);
+                else
+                    return bfr[ks];
+            };
+            // fragments of the next DEPTH - 1 K-steps in flight
+            constexpr int DEPTH = 3;
+            uint4 qa[DEPTH][MT];
+            bf16x8 qb[DEPTH];
+#pragma unroll
+            for (int d = 0; d < DEPTH - 1 && d < KS; ++d) {
+                fetch_a(qa[d], d);
+                qb[d] = fetch_b(d);
+            }
+#pragma unroll
+            for (int ks = 0; ks < KS; ++ks) {
+                if (ks + DEPTH - 1 < KS) {
+                    fetch_a(qa[(ks + DEPTH - 1) % DEPTH], ks + DEPTH - 1);
+                    qb[(ks + DEPTH - 1) % DEPTH] = fetch_b(ks + DEPTH - 1);
+                }
+                __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+                for (int i = 0; i < MT; ++i)
+                    acc[i] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+                        __builtin_bit_cast(bf16x8, qa[ks % DEPTH][i]), qb[ks % DEPTH], acc[i], 0, 0, 0);
+                __builtin_amdgcn_sched_barrier(0);
+            }
+        }
+
+        // epilogue: bias, ReLU, bf16 into LDS as [oc][pixel] (pitch OP = 4 mod
+        // 8: conflict-free 8-byte writes), then 16-byte stores
+        __syncthreads();
+        bf16raw *outl = tl;
+        if (wave_live) {
+            const int ocl = og * 32 + n32;
+#pragma unroll
+            for (int i = 0; i < MT; ++i)
+#pragma unroll
+                for (int gq = 0; gq < 4; ++gq) {
+                    const int q0 = (pg + PW * i) * 32 + 8 * gq + 4 * kh;
+                    float v[4];
+#pragma unroll
+                    for (int r = 0; r < 4; ++r) {
+                        v[r] = acc[i][4 * gq + r] + bv;
+                        if (relu)
+                            v[r] = fmaxf(v[r], 0.f);
                     }
-                    bfr[s][j][e] = __builtin_bit_cast(__bf16, v);
+                    *reinterpret_cast<uint2 *>(outl + ocl * a.OP + q0) =
+                        make_uint2(pack_bf16x2(v[0], v[1]), pack_bf16x2(v[2], v[3]));
                 }
-            }
         }
-#pragma unroll
-        for (int s = 0; s < KC; ++s) {
-            const int ks = s0 + s;
-            if (ks >= tg.KS)
-                break;
-            const int t = ks / icb;
-            const int ic0 = (ks - t * icb) * 32 + 8 * kq;
-            int dq = 0, ds = 0;
-            tap_axial(K, t, dq, ds);
-            const int off0 = tap_drow(dq, ds, 0) * tg.LCP + dq;
-            const int off1 = tap_drow(dq, ds, 1) * tg.LCP + dq;
-            uint4 qa[kMT];
-#pragma unroll
-            for (int i = 0; i < kMT; ++i) {
-                // every read issued (slot 0 for padding lanes), then masked
-                const int sl = pv[i] ? cen[i] + (podd[i] ? off1 : off0) : 0;
-                qa[i] = *reinterpret_cast<const uint4 *>(lds + static_cast<size_t>(sl) * tg.CS + ic0);
-            }
-#pragma unroll
-            for (int i = 0; i < kMT; ++i) {
-                const uint4 q = pv[i] ? qa[i] : make_uint4(0, 0, 0, 0);
-                const bf16x8 a = __builtin_bit_cast(bf16x8, q);
-#pragma unroll
-                for (int j = 0; j < 2; ++j)
-                    acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, bfr[s][j], acc[i][j], 0, 0, 0);
-            }
-        }
-    }
-
-    // epilogue: bias, ReLU, bf16 into LDS [oc][pixel], then contiguous stores
-    __syncthreads();
-    const int opitch = tg.npix_max + 8;
-    bf16raw *outl = lds;
-#pragma unroll
-    for (int j = 0; j < 2; ++j) {
-        const int ocl = oh * 32 + j * 16 + m;
-        const int oc = oc_blk + ocl;
-        const float bv = (bias != nullptr && oc < OC) ? to_f(bias[oc]) : 0.f;
-#pragma unroll
-        for (int i = 0; i < kMT; ++i) {
-            const int mt = ph + 2 * i;
-            const int q0 = mt * 16 + 4 * kq;
-            if (mt >= ntile)
-                continue;
-            uint32_t pk[2];
-#pragma unroll
-            for (int h = 0; h < 2; ++h) {
-                float v0 = acc[i][j][2 * h] + bv, v1 = acc[i][j][2 * h + 1] + bv;
-                if (relu) {
-                    v0 = fmaxf(v0, 0.f);
-                    v1 = fmaxf(v1, 0.f);
-                }
-                pk[h] = static_cast<uint32_t>(from_f<bf16raw>(v0)) |
-                        (static_cast<uint32_t>(from_f<bf16raw>(v1)) << 16);
-            }
-            *reinterpret_cast<uint2 *>(outl + ocl * opitch + q0) = make_uint2(pk[0], pk[1]);
-        }
-    }
-    __syncthreads();
-    const int nvec = (npix + 7) / 8;
-    const int noc = min(kOCB, OC - oc_blk);
-    for (int e = threadIdx.x; e < noc * nvec; e += kThreads) {
-        const int ocl = e / nvec, v8 = e - ocl * nvec;
-        const int p = v8 * 8;
-        bf16raw *dst = y + (static_cast<size_t>(n) * OC + oc_blk + ocl) * HW + static_cast<size_t>(r0) * W + p;
-        const bf16raw *srcp = outl + ocl * opitch + p;
-        if (p + 7 < npix) {
-            *reinterpret_cast<uint4 *>(dst) = *reinterpret_cast<const uint4 *>(srcp);
-        } else {
-            for (int q = 0; q < npix - p; ++q)
-                dst[q] = srcp[q];
-        }
+        __syncthreads();
+        bf16raw *ybase =
+            y + (static_cast<size_t>(n) * a.OC + oc_base) * HW + static_cast<size_t>(r0) * W;
+        if (a.vec_out)
+            wide_store<(OCB * PIX / 8 + kThreads32 - 1) / kThreads32, PIX / 8, kThreads32>(
+                ybase, HW, outl, a.OP, OCc, npix);
+        else
+            wide_store_scalar<kThreads32>(ybase, HW, outl, a.OP, OCc, npix);
     }
 }
 
 inline int cdiv(long a, long b) { return static_cast<int>((a + b - 1) / b); }
 
-constexpr int kKC = 7; // K-steps whose B fragments are held at once
+constexpr size_t kLds2 = 80 * 1024;  // two blocks per CU
+constexpr size_t kLds1 = 160 * 1024; // one block per CU
 
-WideTiling wide_tiling(const ConvShape &sh, int IC, int OC)
+// A kernel configuration.
+//   E32 = 1: 32x32x16 kernel, 8 waves, OG channel groups of 32 x PW pixel
+//            groups, MT tiles of 32 pixels per wave;
+//   E32 = 0: 16x16x32 kernel, 4 waves, NT channel tiles of 16 x PW pixel
+//            groups, MT tiles of 16 pixels per wave.
+//   KSR = K-steps held in registers (0: weights resident in LDS).
+struct WideCfg {
+    int E32, NT, PW, MT, KSR; // KSR: K-steps held in registers, 0 = weights in LDS
+    int WLK;                  // E32 with weights in LDS: instantiated K-step count
+    int waves() const { return E32 ? 8 : kWaves; }
+    int OCB() const { return E32 ? (waves() / PW) * 32 : (waves() / PW) * NT * 16; }
+    int pix() const { return PW * MT * (E32 ? 32 : 16); }
+};
+
+struct WidePlan {
+    WideCfg cfg;
+    WideArgs a;
+    size_t lds;
+    int grid;
+    bool ok;
+};
+
+// Row pitch (bf16) of LDS-resident weights whose 16-byte B fragments are
+// read by 16 (E32 = 0) or 32 (E32 = 1) consecutive rows without bank
+// conflicts: 32 mod 64 bytes, respectively an odd multiple of 16 bytes.
+int resident_pitch(int Kc, bool e32)
 {
-    WideTiling tg;
-    // rows per block: at most 2 * kMT pixel tiles of 16
-    tg.TR = std::max(1, std::min(sh.H, (2 * kMT * 16) / sh.W));
-    tg.npix_max = tg.TR * sh.W;
-    tg.LCP = sh.W + 2 * sh.k;
-    tg.CS = IC + 8; // 16-byte aligned pixel vectors, staggered banks
-    tg.ntiles = cdiv(sh.H, tg.TR);
-    tg.IC = IC;
-    tg.OC = OC;
-    tg.KS = sh.T * IC / 32;
-    return tg;
+    if (e32) {
+        int p = (Kc + 7) / 8 * 8;
+        if ((p / 8) % 2 == 0)
+            p += 8;
+        return p;
+    }
+    int p = (Kc + 15) / 16 * 16;
+    if ((p / 16) % 2 == 0)
+        p += 16;
+    return p;
 }
 
-size_t wide_lds_bytes(const ConvShape &sh, const WideTiling &tg)
+// Configurations with an instantiated kernel (see dispatch_wide).
+bool instantiated(int k, const WideCfg &c)
 {
-    const size_t in = sizeof(bf16raw) * static_cast<size_t>(tg.TR + 2 * sh.k) * tg.LCP * tg.CS;
-    const size_t out = sizeof(bf16raw) * static_cast<size_t>(kOCB) * (tg.npix_max + 8);
-    return std::max(in, out);
+    if (c.E32) {
+        if (c.NT != 1)
+            return false;
+        if (c.PW == 4 && c.MT == 2) // 64 channels
+            return (c.KSR == 0 && k == 2 && c.WLK == 38) ||
+                   (k == 1 && (c.KSR == 14 || c.KSR == 28));
+        if (c.PW == 2 && c.MT == 2) // 128 channels
+            return k == 1 && c.KSR == 28;
+        if (c.PW == 8 && c.MT == 1) // 32 channels, weights in LDS
+            return c.KSR == 0 && ((k == 2 && c.WLK == 76) || (k == 1 && c.WLK == 56));
+        return false;
+    }
+    if (c.NT == 2 && c.PW == 2 && c.MT == 4)
+        return k == 1 && (c.KSR == 7 || c.KSR == 14);
+    return c.KSR == 0 && c.NT == 2 && c.PW == 4 && c.MT == 4;
+}
+
+bool plan_cfg(const ConvShape &sh, int IC, int OC, const WideCfg &c, WidePlan &pl)
+{
+    if (sh.W > c.pix())
+        return false;
+    WideArgs a{};
+    a.N = sh.N;
+    a.H = sh.H;
+    a.W = sh.W;
+    a.IC = IC;
+    a.OC = OC;
+    a.KS = sh.T * IC / (c.E32 ? 16 : 32);
+    a.TR = std::min(sh.H, c.pix() / sh.W);
+    // 16-byte output rows need tile origins on 8-element boundaries
+    while (a.TR > 1 && (a.TR * sh.W) % 8 != 0)
+        --a.TR;
+    a.ntr = cdiv(sh.H, a.TR);
+    a.ptiles = sh.N * a.ntr;
+    a.nocc = cdiv(OC, c.OCB());
+    a.vec_out = ((a.TR * sh.W) % 8 == 0) ? 1 : 0;
+    a.LCP = sh.W + 2 * sh.k;
+    // slot pitch: odd multiple of 16 bytes for 32-row fragment reads,
+    // 32 mod 64 bytes for 16-row ones
+    a.CS = c.E32 ? IC + 8 : IC + 16;
+    a.OP = c.pix() + 4; // 8 mod 16 bytes: conflict-free 8-byte epilogue writes
+    const size_t tile_in = 2ull * (a.TR + 2 * sh.k) * a.LCP * a.CS;
+    const size_t tile_out = 2ull * c.OCB() * a.OP;
+    const size_t tiles = std::max(tile_in, tile_out);
+    const int og = c.waves() / c.PW;
+    size_t lds;
+    if (c.KSR > 0) {
+        a.WP = sh.T * IC;
+        a.tile_off = 0;
+        const size_t wgroup = 2ull * (c.OCB() / og) * a.WP; // bytes per channel group
+        a.wgroups = (wgroup * og <= tiles) ? og : 1;
+        lds = std::max(tiles, wgroup * a.wgroups);
+    } else {
+        a.WP = resident_pitch(sh.T * IC, c.E32 != 0);
+        a.tile_off = static_cast<int>((2ull * c.OCB() * a.WP + 255) / 256 * 256);
+        a.wgroups = 1;
+        lds = a.tile_off + tiles;
+    }
+    const bool two_per_cu = !c.E32 && c.KSR > 0;
+    if (lds > (two_per_cu ? kLds2 : kLds1))
+        return false;
+    if (c.E32) {
+        // staged window items of one tile: at most one per thread
+        const int slack = (sh.W % 8 == 0) ? 0 : 1;
+        const long items = static_cast<long>(IC / 8) *
+                           ((static_cast<long>(a.TR + 2 * sh.k) * sh.W + 7) / 8 + slack);
+        if (items > kThreads32)
+            return false;
+        // runs of consecutive tiles, 8 * nocc blocks per round of XCDs
+        const int runs = std::max(1, std::min(device_cus() / a.nocc, a.ptiles));
+        a.per_block = cdiv(a.ptiles, runs);
+        const int nrun = cdiv(a.ptiles, a.per_block);
+        pl.grid = cdiv(nrun, kXcd) * kXcd * a.nocc; // blocks past the last run exit at once
+    } else {
+        const int per_cu = c.KSR > 0 ? 2 : 1;
+        const int want = std::max(1, device_cus() * per_cu / (kXcd * a.nocc));
+        a.spx = std::max(1, std::min(want, cdiv(a.ptiles, kXcd)));
+        a.nslots = kXcd * a.spx;
+        pl.grid = a.nslots * a.nocc;
+    }
+    pl.cfg = c;
+    pl.a = a;
+    pl.lds = lds;
+    pl.ok = true;
+    return true;
+}
+
+WidePlan plan_wide(const ConvShape &sh, int IC, int OC)
+{
+    WidePlan pl{};
+    pl.ok = false;
+    const int KS32 = sh.T * IC / 16, KS16 = sh.T * IC / 32;
+    const WideCfg cands[] = {
+        {1, 1, 2, 2, KS32, 0}, // 32x32: 128 channels, weights in registers
+        {1, 1, 4, 2, KS32, 0}, // 32x32: 64 channels, weights in registers
+        {1, 1, 4, 2, 0, KS32}, // 32x32: 64 channels, weights in LDS
+        {1, 1, 8, 1, 0, KS32}, // 32x32: 32 channels, weights in LDS
+        {0, 2, 2, 4, KS16, 0}, // 16x16 fallbacks
+        {0, 2, 4, 4, 0, 0},
+    };
+    for (const WideCfg &c : cands) {
+        if (c.E32 && c.PW == 2 && OC <= 64)
+            continue; // 128-channel blocks only for more than 64 channels
+        if (!instantiated(sh.k, c))
+            continue;
+        if (plan_cfg(sh, IC, OC, c, pl))
+            return pl;
+    }
+    return pl;
+}
+
+template <int K, int KS, int NT, int PW, int MT, bool R>
+hipError_t launch_wide(const WidePlan &pl, const bf16raw *x, const bf16raw *w, const bf16raw *b,
+                       bf16raw *y, bool relu, hipStream_t st)
+{
+    hipLaunchKernelGGL((conv_bf16_wide_k<K, KS, NT, PW, MT, R>), dim3(pl.grid), dim3(kThreads),
+                       pl.lds, st, x, w, b, y, pl.a, relu ? 1 : 0);
+    return hipGetLastError();
+}
+
+template <int K, int KS, bool WL, int OG, int PW, int MT, bool R>
+hipError_t launch_wide32(const WidePlan &pl, const bf16raw *x, const bf16raw *w,
+                         const bf16raw *b, bf16raw *y, bool relu, hipStream_t st)
+{
+    hipLaunchKernelGGL((conv_bf16_wide32_k<K, KS, WL, OG, PW, MT, R>), dim3(pl.grid),
+                       dim3(kThreads32), pl.lds, st, x, w, b, y, pl.a, relu ? 1 : 0);
+    return hipGetLastError();
+}
+
+template <bool R>
+hipError_t dispatch_wide(const WidePlan &pl, int k, const bf16raw *x, const bf16raw *w,
+                         const bf16raw *b, bf16raw *y, bool relu, hipStream_t st)
+{
+    const WideCfg &c = pl.cfg;
+    if (c.E32) {
+        if (c.PW == 8)
+            return k == 1 ? launch_wide32<1, 56, true, 1, 8, 1, R>(pl, x, w, b, y, relu, st)
+                          : launch_wide32<2, 76, true, 1, 8, 1, R>(pl, x, w, b, y, relu, st);
+        if (c.PW == 2)
+            return launch_wide32<1, 28, false, 4, 2, 2, R>(pl, x, w, b, y, relu, st);
+        if (c.KSR == 0)
+            return launch_wide32<2, 38, true, 2, 4, 2, R>(pl, x, w, b, y, relu, st);
+        if (c.KSR == 14)
+            return launch_wide32<1, 14, false, 2, 4, 2, R>(pl, x, w, b, y, relu, st);
+        return launch_wide32<1, 28, false, 2, 4, 2, R>(pl, x, w, b, y, relu, st);
+    }
+    if (c.KSR == 0)
+        return k == 1 ? launch_wide<1, 0, 2, 4, 4, R>(pl, x, w, b, y, relu, st)
+                      : launch_wide<2, 0, 2, 4, 4, R>(pl, x, w, b, y, relu, st);
+    if (c.KSR == 7)
+        return launch_wide<1, 7, 2, 2, 4, R>(pl, x, w, b, y, relu, st);
+    return launch_wide<1, 14, 2, 2, 4, R>(pl, x, w, b, y, relu, st);
 }
 
 } // namespace
 
 bool bf16_wide_ok(const ConvShape &sh, int IC, int OC)
 {
-    if (sh.s != 1 || (sh.k != 1 && sh.k != 2) || IC % 32 != 0 || sh.W % 8 != 0 ||
-        sh.W > 2 * kMT * 16)
+    if (sh.s != 1 || (sh.k != 1 && sh.k != 2) || IC % 32 != 0 || IC > 128 || sh.W % 2 != 0 ||
+        sh.W < 8 || (static_cast<long>(sh.H) * sh.W) % 8 != 0)
         return false;
-    const WideTiling tg = wide_tiling(sh, IC, OC);
-    return wide_lds_bytes(sh, tg) <= 80 * 1024;
+    return plan_wide(sh, IC, OC).ok;
 }
 
 hipError_t bf16_wide_conv(const void *in, const void *w, const void *bias, void *out,
@@ -311,23 +925,15 @@ hipError_t bf16_wide_conv(const void *in, const void *w, const void *bias, void 
 {
     const int IC = reflect ? sh.Co : sh.Ci;
     const int OC = reflect ? sh.Ci : sh.Co;
-    const WideTiling tg = wide_tiling(sh, IC, OC);
-    dim3 grid(tg.ntiles * sh.N, cdiv(OC, kOCB));
-    const size_t lds = wide_lds_bytes(sh, tg);
+    const WidePlan pl = plan_wide(sh, IC, OC);
+    if (!pl.ok)
+        return hipErrorInvalidValue;
     const bf16raw *x = static_cast<const bf16raw *>(in);
     const bf16raw *wp = static_cast<const bf16raw *>(w);
-    const bf16raw *bp = static_cast<const bf16raw *>(bias);
     bf16raw *y = static_cast<bf16raw *>(out);
-#define HEX_WIDE(KV, RV)                                                                     \
-    hipLaunchKernelGGL((conv_bf16_wide_k<KV, kKC, RV>), grid, dim3(kThreads), lds, st, x, wp, \
-                       bp, y, sh, relu ? 1 : 0, tg)
-    if (sh.k == 1) {
-        if (reflect) HEX_WIDE(1, true); else HEX_WIDE(1, false);
-    } else {
-        if (reflect) HEX_WIDE(2, true); else HEX_WIDE(2, false);
-    }
-#undef HEX_WIDE
-    return hipGetLastError();
+    if (reflect)
+        return dispatch_wide<true>(pl, sh.k, x, wp, nullptr, y, false, st);
+    return dispatch_wide<false>(pl, sh.k, x, wp, static_cast<const bf16raw *>(bias), y, relu, st);
 }
 
 } // namespace hexk

@@ -281,6 +281,12 @@ SWEEP = [
     (1, 2, 2, 2, 9, 4, 2), (3, 3, 24, 37, 8, 2, 1), (1, 2, 70, 5, 256, 1, 1),
     (2, 48, 40, 11, 32, 2, 1), (3, 2, 20, 13, 68, 2, 1), (2, 1, 24, 9, 8, 1, 1),
     (1, 2, 16, 5, 12, 2, 1),
+    # wide bf16 matrix-core path: registers (k=1: 32 and 64 channels, k=2: 32),
+    # LDS-resident weights (long contractions), several channel chunks,
+    # partial last tiles, narrow and wide rows
+    (2, 32, 48, 10, 16, 1, 1), (1, 64, 128, 12, 12, 1, 1), (2, 64, 64, 37, 16, 1, 1),
+    (1, 96, 32, 8, 24, 1, 1), (1, 32, 32, 6, 20, 2, 1), (1, 64, 64, 30, 12, 1, 1),
+    (1, 32, 16, 6, 128, 2, 1), (1, 32, 32, 3, 256, 1, 1), (2, 128, 64, 5, 8, 2, 1),
 ]
 
 
