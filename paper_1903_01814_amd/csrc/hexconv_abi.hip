@@ -332,8 +332,10 @@ int hexpool_fwd(const void *x, void *y, uint8_t *argmax_tap, int N, int C, int H
         return HEX_OK;
     hipStream_t st = static_cast<hipStream_t>(stream);
     const Dtype d = static_cast<Dtype>(dt);
-    return launched(hexk::pool_fwd_generic(x, y, mode == HEX_POOL_MAX ? argmax_tap : nullptr, sh,
-                                           mode, d, st));
+    uint8_t *am = mode == HEX_POOL_MAX ? argmax_tap : nullptr;
+    if (!force_generic() && hexk::pool_fast_ok(sh, d))
+        return launched(hexk::pool_fwd_fast(x, y, am, sh, mode, d, st));
+    return launched(hexk::pool_fwd_generic(x, y, am, sh, mode, d, st));
 }
 
 int hexpool_bwd(const void *dy, const uint8_t *argmax_tap, const void *relu_y, void *dx, int N,
@@ -354,6 +356,8 @@ int hexpool_bwd(const void *dy, const uint8_t *argmax_tap, const void *relu_y, v
         return HEX_ERR_INVALID_ARG;
     hipStream_t st = static_cast<hipStream_t>(stream);
     const Dtype d = static_cast<Dtype>(dt);
+    if (!force_generic() && sh.Ho > 0 && hexk::pool_fast_ok(sh, d))
+        return launched(hexk::pool_bwd_fast(dy, argmax_tap, relu_y, dx, sh, mode, d, st));
     return launched(hexk::pool_bwd_generic(dy, argmax_tap, relu_y, dx, sh, mode, d, st));
 }
 

@@ -19,14 +19,11 @@ __device__ __forceinline__ float to_f(bf16raw v)
 
 template <typename T> __device__ __forceinline__ T from_f(float f);
 template <> __device__ __forceinline__ float from_f<float>(float f) { return f; }
-// float32 -> bfloat16, round to nearest even (NaN stays NaN)
+// float32 -> bfloat16, round to nearest even (gfx950 converts in hardware;
+// NaN stays NaN)
 template <> __device__ __forceinline__ bf16raw from_f<bf16raw>(float f)
 {
-    uint32_t u = __float_as_uint(f);
-    if ((u & 0x7fffffffu) > 0x7f800000u)
-        return static_cast<bf16raw>((u >> 16) | 0x40u);
-    u += 0x7fffu + ((u >> 16) & 1u);
-    return static_cast<bf16raw>(u >> 16);
+    return __builtin_bit_cast(bf16raw, static_cast<__bf16>(f));
 }
 
 // Per-block tap table in LDS: column offset, and row offset per centre

@@ -45,6 +45,18 @@ HEX_HD constexpr void tap_axial(int k, int t, int &dq, int &ds)
     ds = col_ds_lo(k, q) + rem;
 }
 
+// The taps of a size-K kernel as compile-time tables (tap_axial evaluated
+// by the compiler; index with constants so the values fold into the code).
+template <int K> struct TapTable {
+    int dq[num_taps(K)];
+    int ds[num_taps(K)];
+    constexpr TapTable() : dq(), ds()
+    {
+        for (int t = 0; t < num_taps(K); ++t)
+            tap_axial(K, t, dq[t], ds[t]);
+    }
+};
+
 // tensor row offset of axial tap (dq, ds) for a centre column of parity p
 HEX_HD constexpr int tap_drow(int dq, int ds, int p)
 {

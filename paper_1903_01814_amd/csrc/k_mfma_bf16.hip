@@ -638,8 +638,8 @@ __global__ __launch_bounds__(kThreads32) void conv_bf16_wide32_k(
             // constants once the loop is unrolled
             auto fetch_a = [&](uint4(&q)[MT], int ks) {
                 const int t = ks / ICB;
-                int dq = 0, ds = 0;
-                tap_axial(K, t, dq, ds);
+                constexpr TapTable<K> tt;
+                const int dq = tt.dq[t], ds = tt.ds[t];
                 const int toff = (ds + floor_half(dq)) * rowb + dq * slotb + (ks % ICB) * 32 +
                                  ((dq & 1) ? oddoff : 0);
 #pragma unroll

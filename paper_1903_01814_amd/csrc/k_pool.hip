@@ -1,0 +1,401 @@
+// k_pool.hip -- hexagonal max / mean pooling, forward and backward, for
+// kernel sizes k <= 2 and strides 1 and 2 (Sec. 2.4: the pool window is the
+// size-k hexagon, padded like the convolution; stride as in Sec. 2.3).
+//
+// Forward: a block stages NP whole input planes into LDS with a zero border
+// (k rows above and below, a 16-byte pad left and right of every row), so a
+// tap never needs a bounds check and padded taps read 0 (they take part in
+// the max and the mean).  Each thread then reduces the T taps of one output
+// from LDS: the strict "v > best" scan in canonical tap order keeps the
+// first maximal tap, whose index is the uint8 argmax.  With an even stride
+// every centre column is even, so the tap offsets are compile-time.
+//
+// Backward: scatter in tap phases.  dx of NP planes is accumulated in fp32
+// in LDS; in phase t every output whose argmax is t (mean pooling: every
+// output) adds its dy to the input pixel under tap t.  Two outputs with the
+// same tap never reach the same pixel, so a phase needs no atomics, and the
+// phases run in tap order -- each pixel receives its contributions in the
+// same order as a gather over taps would add them, so the result is
+// deterministic and independent of the thread layout.  Contributions through
+// taps outside the input are dropped.  Mean pooling divides the sum by T;
+// the ReLU mask [relu_in > 0] is applied last.
+#include <algorithm>
+
+#include "hexdev.h"
+#include "kernels.h"
+#include "shear.h"
+
+namespace hexk {
+namespace {
+
+using namespace hexgeom;
+
+constexpr int kPoolThreads = 256;
+
+struct PoolArgs {
+    int nplanes, H, W, Ho, Wo;
+    int NP;      // planes per block
+    int pitch;   // LDS row pitch (elements) of a staged input plane
+    int LR;      // LDS rows of a staged input plane (H + 2k)
+    FastDiv fwo; // division by Wo
+    FastDiv fho; // division by Ho * Wo
+    FastDiv fho_rows; // division by Ho
+    FastDiv fw;  // division by W
+    FastDiv fh;  // division by H
+    FastDiv fcr; // division by the 16-byte chunks of an input row
+};
+
+// centre of output (i, j) (stride S)
+template <int S> __device__ __forceinline__ int centre_r(int i, int j)
+{
+    return S * i + (j & 1) * (S / 2);
+}
+
+// ARG: write the argmax tap (max pooling).
+template <typename TT, int MODE, int K, int S, bool ARG>
+__global__ __launch_bounds__(kPoolThreads) void pool_fwd_k(const TT *__restrict__ x,
+                                                           TT *__restrict__ y,
+                                                           uint8_t *__restrict__ am, PoolArgs a)
+{
+    constexpr int T = num_taps(K);
+    constexpr int VEC = 16 / sizeof(TT); // elements per 16 bytes = left pad
+    extern __shared__ __align__(16) unsigned char smem[];
+    TT *lds = reinterpret_cast<TT *>(smem);
+    const int p0 = blockIdx.x * a.NP;
+    const int np = min(a.NP, a.nplanes - p0);
+    const int H = a.H, W = a.W;
+    const size_t HW = static_cast<size_t>(H) * W;
+    const int plane_l = a.LR * a.pitch;
+    const int cpr = W / VEC;
+
+    // zero border: whole rows above / below, one 16-byte chunk left and right
+    {
+        const int vrow = a.pitch / VEC; // 16-byte chunks per LDS row
+        const int per_plane = 2 * K * vrow + 2 * H;
+        for (int e = threadIdx.x; e < np * per_plane; e += kPoolThreads) {
+            const int pl = e / per_plane, q = e - pl * per_plane;
+            int off;
+            if (q < 2 * K * vrow) {
+                const int rr = q / vrow, v = q - rr * vrow;
+                const int row = rr < K ? rr : H + rr; // rows 0..K-1 and H+K..H+2K-1
+                off = row * a.pitch + v * VEC;
+            } else {
+                const int q2 = q - 2 * K * vrow;
+                const int row = K + (q2 >> 1);
+                off = row * a.pitch + ((q2 & 1) ? VEC + W : 0);
+            }
+            *reinterpret_cast<uint4 *>(lds + pl * plane_l + off) = make_uint4(0, 0, 0, 0);
+        }
+    }
+    // interior rows, 16-byte chunks; the planes are contiguous in x, so
+    // chunk it is x[p0 plane start + VEC * it]; U loads in flight per thread
+    {
+        constexpr int U = 4;
+        const int items = np * H * cpr;
+        const TT *src = x + static_cast<size_t>(p0) * HW;
+        for (int it0 = threadIdx.x; it0 < items; it0 += U * kPoolThreads) {
+            uint4 v[U];
+#pragma unroll
+            for (int u = 0; u < U; ++u) {
+                const int it = it0 + u * kPoolThreads;
+                v[u] = *reinterpret_cast<const uint4 *>(src + static_cast<size_t>(min(it, items - 1)) * VEC);
+            }
+#pragma unroll
+            for (int u = 0; u < U; ++u) {
+                const int it = it0 + u * kPoolThreads;
+                if (it < items) {
+                    const int rowi = static_cast<int>(fdiv(static_cast<uint32_t>(it), a.fcr));
+                    const int ch = it - rowi * cpr;
+                    const int pl = static_cast<int>(fdiv(static_cast<uint32_t>(rowi), a.fh));
+                    const int r = rowi - pl * H;
+                    *reinterpret_cast<uint4 *>(lds + pl * plane_l + (r + K) * a.pitch + VEC + ch * VEC) =
+                        v[u];
+                }
+            }
+        }
+    }
+    __syncthreads();
+
+    // thread -> output column j (fixed) and every rpp-th output row of the
+    // block's planes (rows of consecutive planes follow each other)
+    const int Wo = a.Wo, Ho = a.Ho;
+    const int HWo = Ho * Wo;
+    const int rpp = kPoolThreads / Wo; // output rows per pass (Wo <= 256)
+    const int j = threadIdx.x % Wo;
+    const int row0 = threadIdx.x / Wo;
+    if (row0 >= rpp)
+        return; // spare threads (no barrier follows)
+    const int cc = S * j;
+    const int par = (S % 2 == 0) ? 0 : (cc & 1);
+    const int halfs = (j & 1) * (S / 2);
+    TT *yb = y + static_cast<size_t>(p0) * HWo;
+    uint8_t *ab = am != nullptr ? am + static_cast<size_t>(p0) * HWo : nullptr;
+    constexpr TapTable<K> tt;
+    int pl = static_cast<int>(fdiv(static_cast<uint32_t>(row0), a.fho_rows));
+    int i = row0 - pl * Ho;
+    for (int row = row0; row < np * Ho; row += rpp) {
+        const int rc = S * i + halfs;
+        const TT *cen = lds + pl * plane_l + (rc + K) * a.pitch + VEC + cc;
+        float best = 0.f, sum = 0.f;
+        int arg = 0;
+#pragma unroll
+        for (int t = 0; t < T; ++t) {
+            const int dr = par ? tap_drow(tt.dq[t], tt.ds[t], 1) : tap_drow(tt.dq[t], tt.ds[t], 0);
+            const float v = to_f(cen[dr * a.pitch + tt.dq[t]]);
+            if (MODE == 0) {
+                if (t == 0 || v > best) {
+                    best = v;
+                    if (ARG)
+                        arg = t;
+                }
+            } else {
+                sum += v;
+            }
+        }
+        const int o = row * Wo + j; // plane-major: pl * HWo + i * Wo + j
+        if (MODE == 0) {
+            yb[o] = from_f<TT>(best);
+            if (ARG)
+                ab[o] = static_cast<uint8_t>(arg);
+        } else {
+            yb[o] = from_f<TT>(sum / static_cast<float>(T));
+        }
+        i += rpp;
+        while (i >= Ho) {
+            i -= Ho;
+            ++pl;
+        }
+    }
+}
+
+// OPT: outputs per thread held in registers across the tap phases.
+template <typename TT, int MODE, int K, int S, int OPT>
+__global__ __launch_bounds__(kPoolThreads) void pool_bwd_k(const TT *__restrict__ dy,
+                                                           const uint8_t *__restrict__ am,
+                                                           const TT *__restrict__ relu_y,
+                                                           TT *__restrict__ dx, PoolArgs a)
+{
+    constexpr int T = num_taps(K);
+    extern __shared__ __align__(16) float acc[]; // [np][H][W]
+    const int p0 = blockIdx.x * a.NP;
+    const int np = min(a.NP, a.nplanes - p0);
+    const int H = a.H, W = a.W;
+    const int HW = H * W;
+    const int HWo = a.Ho * a.Wo;
+
+    for (int e = threadIdx.x; e < np * HW; e += kPoolThreads)
+        acc[e] = 0.f;
+
+    // this thread's outputs: dy, argmax tap and centre
+    float g[OPT];
+    int tap[OPT], base[OPT], rc_[OPT], cc_[OPT];
+#pragma unroll
+    for (int u = 0; u < OPT; ++u) {
+        const int e = threadIdx.x + u * kPoolThreads;
+        g[u] = 0.f;
+        tap[u] = -1;
+        base[u] = 0;
+        rc_[u] = 0;
+        cc_[u] = 0;
+        if (e < np * HWo) {
+            const int pl = static_cast<int>(fdiv(static_cast<uint32_t>(e), a.fho));
+            const int o = e - pl * HWo;
+            const int i = static_cast<int>(fdiv(static_cast<uint32_t>(o), a.fwo));
+            const int j = o - i * a.Wo;
+            const size_t go = static_cast<size_t>(p0) * HWo + e;
+            g[u] = to_f(dy[go]);
+            tap[u] = (MODE == 0) ? static_cast<int>(am[go]) : T; // T: every tap
+            rc_[u] = centre_r<S>(i, j);
+            cc_[u] = S * j;
+            base[u] = pl * HW;
+        }
+    }
+    __syncthreads();
+
+#pragma unroll
+    for (int t = 0; t < T; ++t) {
+        constexpr TapTable<K> tt;
+        const int dq = tt.dq[t], ds = tt.ds[t];
+#pragma unroll
+        for (int u = 0; u < OPT; ++u) {
+            const bool use = (MODE == 0) ? (tap[u] == t) : (tap[u] == T);
+            if (use) {
+                const int par = (S % 2 == 0) ? 0 : (cc_[u] & 1);
+                const int r = rc_[u] + tap_drow(dq, ds, par);
+                const int c = cc_[u] + dq;
+                if (r >= 0 && r < H && c >= 0 && c < W)
+                    acc[base[u] + r * W + c] += g[u];
+            }
+        }
+        __syncthreads(); // phase t complete before phase t+1 touches the same pixels
+    }
+
+    // dx of the block's planes (contiguous in memory), VEC pixels per thread
+    // and 16-byte loads / stores when the planes hold whole 16-byte chunks
+    constexpr int VEC = 16 / sizeof(TT);
+    const size_t g0 = static_cast<size_t>(p0) * HW;
+    const int total = np * HW;
+    if (HW % VEC == 0) {
+        for (int e0 = threadIdx.x * VEC; e0 < total; e0 += kPoolThreads * VEC) {
+            TT rv[VEC], ov[VEC];
+            if (relu_y != nullptr)
+                *reinterpret_cast<uint4 *>(rv) = *reinterpret_cast<const uint4 *>(relu_y + g0 + e0);
+#pragma unroll
+            for (int q = 0; q < VEC; ++q) {
+                float v = acc[e0 + q];
+                if (MODE == 1)
+                    v = v / static_cast<float>(T);
+                if (relu_y != nullptr && !(to_f(rv[q]) > 0.f))
+                    v = 0.f;
+                ov[q] = from_f<TT>(v);
+            }
+            *reinterpret_cast<uint4 *>(dx + g0 + e0) = *reinterpret_cast<const uint4 *>(ov);
+        }
+    } else {
+        for (int e = threadIdx.x; e < total; e += kPoolThreads) {
+            float v = acc[e];
+            if (MODE == 1)
+                v = v / static_cast<float>(T);
+            if (relu_y != nullptr && !(to_f(relu_y[g0 + e]) > 0.f))
+                v = 0.f;
+            dx[g0 + e] = from_f<TT>(v);
+        }
+    }
+}
+
+inline int cdiv(long a, long b) { return static_cast<int>((a + b - 1) / b); }
+
+constexpr size_t kPoolLds = 48 * 1024;
+
+PoolArgs pool_args(const ConvShape &sh, int esz)
+{
+    PoolArgs a{};
+    a.nplanes = sh.N * sh.Ci;
+    a.H = sh.H;
+    a.W = sh.W;
+    a.Ho = sh.Ho;
+    a.Wo = sh.Wo;
+    const int vec = 16 / esz;
+    a.pitch = sh.W + 2 * vec;
+    a.LR = sh.H + 2 * sh.k;
+    a.fwo = make_fastdiv(static_cast<uint32_t>(std::max(1, sh.Wo)));
+    a.fho = make_fastdiv(static_cast<uint32_t>(std::max(1, sh.Ho * sh.Wo)));
+    a.fho_rows = make_fastdiv(static_cast<uint32_t>(std::max(1, sh.Ho)));
+    a.fw = make_fastdiv(static_cast<uint32_t>(sh.W));
+    a.fh = make_fastdiv(static_cast<uint32_t>(sh.H));
+    a.fcr = make_fastdiv(static_cast<uint32_t>(std::max(1, sh.W / vec)));
+    return a;
+}
+
+size_t fwd_plane_bytes(const PoolArgs &a, int esz) { return static_cast<size_t>(a.LR) * a.pitch * esz; }
+
+int bwd_opt(const PoolArgs &a, int np) { return cdiv(static_cast<long>(np) * a.Ho * a.Wo, kPoolThreads); }
+
+} // namespace
+
+bool pool_fast_ok(const ConvShape &sh, Dtype dt)
+{
+    const int esz = dt == F32 ? 4 : 2;
+    if (sh.k > 2 || (sh.s != 1 && sh.s != 2) || sh.W % (16 / esz) != 0 || sh.Ho == 0 ||
+        sh.Wo > kPoolThreads)
+        return false;
+    const PoolArgs a = pool_args(sh, esz);
+    // one plane must fit; the backward holds up to 16 outputs per thread
+    return fwd_plane_bytes(a, esz) <= kPoolLds &&
+           sizeof(float) * static_cast<size_t>(sh.H) * sh.W <= kPoolLds &&
+           bwd_opt(a, 1) <= 16;
+}
+
+hipError_t pool_fwd_fast(const void *x, void *y, uint8_t *am, const ConvShape &sh, int mode,
+                         Dtype dt, hipStream_t st)
+{
+    const int esz = dt == F32 ? 4 : 2;
+    PoolArgs a = pool_args(sh, esz);
+    // planes per block: LDS budget and about 8 outputs per thread
+    const int by_lds = static_cast<int>(kPoolLds / fwd_plane_bytes(a, esz));
+    const int by_work = std::max(1, (8 * kPoolThreads) / std::max(1, sh.Ho * sh.Wo));
+    a.NP = std::max(1, std::min(by_lds, by_work));
+    const int grid = cdiv(a.nplanes, a.NP);
+    const size_t lds = fwd_plane_bytes(a, esz) * a.NP;
+#define HEX_PF(TT, M, KV, SV)                                                                \
+    do {                                                                                     \
+        if (am != nullptr)                                                                   \
+            hipLaunchKernelGGL((pool_fwd_k<TT, M, KV, SV, true>), dim3(grid),                \
+                               dim3(kPoolThreads), lds, st, static_cast<const TT *>(x),      \
+                               static_cast<TT *>(y), am, a);                                 \
+        else                                                                                 \
+            hipLaunchKernelGGL((pool_fwd_k<TT, M, KV, SV, false>), dim3(grid),               \
+                               dim3(kPoolThreads), lds, st, static_cast<const TT *>(x),      \
+                               static_cast<TT *>(y), am, a);                                 \
+    } while (0)
+#define HEX_PF_KS(TT, M)                                                                     \
+    do {                                                                                     \
+        if (sh.s == 1) {                                                                     \
+            if (sh.k == 0) HEX_PF(TT, M, 0, 1);                                              \
+            else if (sh.k == 1) HEX_PF(TT, M, 1, 1);                                         \
+            else HEX_PF(TT, M, 2, 1);                                                        \
+        } else {                                                                             \
+            if (sh.k == 0) HEX_PF(TT, M, 0, 2);                                              \
+            else if (sh.k == 1) HEX_PF(TT, M, 1, 2);                                         \
+            else HEX_PF(TT, M, 2, 2);                                                        \
+        }                                                                                    \
+    } while (0)
+    if (dt == F32) {
+        if (mode == 0) HEX_PF_KS(float, 0); else HEX_PF_KS(float, 1);
+    } else {
+        if (mode == 0) HEX_PF_KS(bf16raw, 0); else HEX_PF_KS(bf16raw, 1);
+    }
+#undef HEX_PF_KS
+#undef HEX_PF
+    return hipGetLastError();
+}
+
+hipError_t pool_bwd_fast(const void *dy, const uint8_t *am, const void *relu_y, void *dx,
+                         const ConvShape &sh, int mode, Dtype dt, hipStream_t st)
+{
+    const int esz = dt == F32 ? 4 : 2;
+    PoolArgs a = pool_args(sh, esz);
+    const size_t plane = sizeof(float) * static_cast<size_t>(sh.H) * sh.W;
+    const int by_lds = static_cast<int>(kPoolLds / plane);
+    // up to 8 outputs per thread
+    const int by_opt = std::max(1, (8 * kPoolThreads) / std::max(1, sh.Ho * sh.Wo));
+    a.NP = std::max(1, std::min(by_lds, by_opt));
+    const int opt = bwd_opt(a, a.NP);
+    const int grid = cdiv(a.nplanes, a.NP);
+    const size_t lds = plane * a.NP;
+#define HEX_PB(TT, M, KV, SV, OV)                                                            \
+    hipLaunchKernelGGL((pool_bwd_k<TT, M, KV, SV, OV>), dim3(grid), dim3(kPoolThreads), lds, \
+                       st, static_cast<const TT *>(dy), am, static_cast<const TT *>(relu_y),  \
+                       static_cast<TT *>(dx), a)
+#define HEX_PB_O(TT, M, KV, SV)                                                              \
+    do {                                                                                     \
+        if (opt <= 1) HEX_PB(TT, M, KV, SV, 1);                                              \
+        else if (opt <= 2) HEX_PB(TT, M, KV, SV, 2);                                         \
+        else if (opt <= 4) HEX_PB(TT, M, KV, SV, 4);                                         \
+        else if (opt <= 8) HEX_PB(TT, M, KV, SV, 8);                                         \
+        else HEX_PB(TT, M, KV, SV, 16);                                                      \
+    } while (0)
+#define HEX_PB_KS(TT, M)                                                                     \
+    do {                                                                                     \
+        if (sh.s == 1) {                                                                     \
+            if (sh.k == 0) HEX_PB_O(TT, M, 0, 1);                                            \
+            else if (sh.k == 1) HEX_PB_O(TT, M, 1, 1);                                       \
+            else HEX_PB_O(TT, M, 2, 1);                                                      \
+        } else {                                                                             \
+            if (sh.k == 0) HEX_PB_O(TT, M, 0, 2);                                            \
+            else if (sh.k == 1) HEX_PB_O(TT, M, 1, 2);                                       \
+            else HEX_PB_O(TT, M, 2, 2);                                                      \
+        }                                                                                    \
+    } while (0)
+    if (dt == F32) {
+        if (mode == 0) HEX_PB_KS(float, 0); else HEX_PB_KS(float, 1);
+    } else {
+        if (mode == 0) HEX_PB_KS(bf16raw, 0); else HEX_PB_KS(bf16raw, 1);
+    }
+#undef HEX_PB_KS
+#undef HEX_PB_O
+#undef HEX_PB
+    return hipGetLastError();
+}
+
+} // namespace hexk

@@ -59,6 +59,13 @@ hipError_t pool_bwd_generic(const void *dy, const uint8_t *am,
                             const void *relu_y, void *dx, const ConvShape &sh,
                             int mode, Dtype dt, hipStream_t st);
 
+// ---- pooling, k <= 2, stride 1 or 2, rows of whole 16-byte chunks ------
+bool pool_fast_ok(const ConvShape &sh, Dtype dt);
+hipError_t pool_fwd_fast(const void *x, void *y, uint8_t *am, const ConvShape &sh, int mode,
+                         Dtype dt, hipStream_t st);
+hipError_t pool_bwd_fast(const void *dy, const uint8_t *am, const void *relu_y, void *dx,
+                         const ConvShape &sh, int mode, Dtype dt, hipStream_t st);
+
 // ---- float32, few input channels (C_in*T <= 64), stride 1 -------------
 bool smallc_f32_fwd_ok(const ConvShape &sh);
 hipError_t smallc_f32_fwd(const float *x, const float *w, const float *b, float *y,

@@ -313,7 +313,14 @@ def test_conv_sweep(case, dt):
 @pytest.mark.parametrize("case", [(2, 3, 9, 10, 1, 2), (1, 4, 40, 40, 1, 2),
                                   (1, 2, 11, 12, 2, 1), (2, 2, 13, 7, 2, 3),
                                   (1, 3, 1, 9, 1, 1), (1, 5, 24, 24, 1, 2),
-                                  (1, 2, 6, 6, 0, 1), (1, 1, 17, 18, 3, 4)])
+                                  (1, 2, 6, 6, 0, 1), (1, 1, 17, 18, 3, 4),
+                                  # LDS-staged kernels: k 0..2, strides 1 and 2,
+                                  # several planes per block with a partial last
+                                  # block, 16 outputs per thread
+                                  (2, 3, 16, 16, 2, 1), (1, 4, 48, 48, 1, 2),
+                                  (3, 5, 7, 8, 0, 2), (1, 2, 8, 24, 2, 2),
+                                  (1, 70, 24, 32, 1, 1), (2, 3, 5, 16, 1, 2),
+                                  (1, 2, 64, 64, 1, 1)])
 def test_pool_sweep(case, mode, dt):
     N, C, H, W, k, s = case
     rng = np.random.default_rng(sum(case) + mode)
