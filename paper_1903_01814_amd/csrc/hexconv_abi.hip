@@ -99,7 +99,7 @@ bool force_generic()
 
 // Weight-gradient kernel family for a shape; the workspace query and the
 // call must agree, so both go through this choice.
-enum class WgradPath { Generic, SmallF32, Bf16Mfma };
+enum class WgradPath { Generic, SmallF32, Bf16Mfma32, Bf16Mfma };
 
 WgradPath wgrad_path(const ConvShape &sh, Dtype d)
 {
@@ -107,6 +107,8 @@ WgradPath wgrad_path(const ConvShape &sh, Dtype d)
         return WgradPath::Generic;
     if (d == hexk::F32 && hexk::smallc_f32_wgrad_ok(sh))
         return WgradPath::SmallF32;
+    if (d == hexk::BF16 && hexk::bf16_wgrad32_ok(sh))
+        return WgradPath::Bf16Mfma32;
     if (d == hexk::BF16 && hexk::bf16_wgrad_ok(sh))
         return WgradPath::Bf16Mfma;
     return WgradPath::Generic;
@@ -123,6 +125,8 @@ size_t wgrad_workspace(const ConvShape &sh, Dtype d)
     switch (wgrad_path(sh, d)) {
     case WgradPath::SmallF32:
         return hexk::smallc_f32_wgrad_workspace(sh);
+    case WgradPath::Bf16Mfma32:
+        return hexk::bf16_wgrad32_workspace(sh);
     case WgradPath::Bf16Mfma:
         return hexk::bf16_wgrad_workspace(sh);
     default:
@@ -260,6 +264,8 @@ int hexconv_bwd_weight(const void *x, const void *dy, float *dw, float *db, void
         return launched(hexk::smallc_f32_wgrad(static_cast<const float *>(x),
                                                static_cast<const float *>(dy), dw, db, ws, sh,
                                                st));
+    case WgradPath::Bf16Mfma32:
+        return launched(hexk::bf16_wgrad32(x, dy, dw, db, ws, sh, st));
     case WgradPath::Bf16Mfma:
         return launched(hexk::bf16_wgrad(x, dy, dw, db, ws, sh, st));
     default:

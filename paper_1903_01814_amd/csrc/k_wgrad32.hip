@@ -1,0 +1,592 @@
+// k_wgrad32.hip -- bf16 weight and bias gradient on the matrix cores for
+// input and output channel counts that are multiples of 32, at stride 1:
+//   dw[co][ci][t] = sum_{n, p} dy[n][co][p] * x[n][ci][p + tap t]
+//   db[co]        = sum_{n, p} dy[n][co][p]
+// One GEMM per tap, D_t[co][ci] = sum_p dy[co][p] * x[ci][p + tap t], with
+// the pixels as the contraction index, on v_mfma_f32_32x32x16_bf16:
+//   a[i] = A[lane % 32][8 * (lane / 32) + i]: dy of channel co at 8 pixels,
+//   b[i] = B[8 * (lane / 32) + i][lane % 32]: x of channel ci at the same 8
+//          pixels moved by tap t,
+//   d[r] = D[8 * (r / 4) + 4 * (lane / 32) + r % 4][lane % 32].
+//
+// Pixel order.  A tap's row offset depends on the column parity of the
+// centre (offset-column addressing, Sec. 2.1), so the contraction runs over
+// runs of 8 pixels of one row and one column parity: the tiles of x and dy
+// are stored in LDS with every row split into its even and its odd columns
+// (split index j = column / 2, rows padded to WS, a multiple of 8).  For a
+// centre of parity p in split position j, tap (dq, ds) reads row +
+// drow(p, dq, ds), parity (p + dq) & 1, split position j + ((p + dq) >> 1):
+// the same offset for all 8 pixels of a run, and for all lanes (one tap per
+// GEMM).  The split position moves by s = (p + dq) >> 1 in {-1, 0, 1}
+// elements; s = 0 is one aligned 16-byte read, s = +-1 one aligned 16-byte
+// read plus one 4-byte read and four byte-aligns, all fixed at compile time.
+// A K-step (16 pixels) is two runs of the same parity.  Zero pads around
+// the split rows and zero rows outside the image give the padding taps.
+//
+// Work split.  One block of 8 waves per CU owns a contiguous run of pixel
+// tiles (full-width rows) and prefetches the next tile into registers while
+// it computes the current one.  Wave w owns one (ci block, co block) pair of
+// 32 x 32 channels and a group of taps (compile-time), so no two waves add
+// to the same output; the waves of the first ci block also sum dy for db.
+// Each block writes its accumulators to its own partial slot exactly as they
+// sit in the registers (one 64-lane register = 64 contiguous floats, whole
+// 256-byte lines), and a final kernel adds the slots in a fixed order and
+// scatters the sums to dw[co][ci][t] and db -- deterministic.
+#include <algorithm>
+#include <type_traits>
+
+#include "hexdev.h"
+#include "kernels.h"
+#include "shear.h"
+
+namespace hexk {
+namespace {
+
+using namespace hexgeom;
+
+typedef float floatx16 __attribute__((ext_vector_type(16)));
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+
+constexpr int kT = 512; // threads per block (8 waves)
+constexpr int kRegChunk = 64; // floats per partial chunk (one register of a wave)
+
+struct Wg32Args {
+    int N, H, W, CI, CO;
+    int co0, COT;  // this pass covers output channels co0 .. co0 + CO - 1 of COT
+    int WS;        // split row length of one parity (elements), multiple of 8
+    int XS;        // x split segment: 8 zero pad + WS + 8 zero pad
+    int TR, ntr, ptiles, per_block;
+    int dyc;       // dy LDS pitch per channel (elements)
+    int xc;        // x LDS pitch per channel (elements)
+    int x_off;     // element offset of the x region in LDS
+    int nparts;    // partial slots (= blocks)
+    int nchunk;    // partial chunks per slot: tiles * 16 + db chunks
+    int items_x, items_dy; // staging items of a full tile
+    int cpr;       // staging chunks per image row
+    FastDiv fcpr, fxr, ftr, frpr; // division by cpr, TR + 2K, TR, runs per split row
+};
+
+__device__ __forceinline__ int udiv(int n, const FastDiv &f)
+{
+    return static_cast<int>(fdiv(static_cast<uint32_t>(n), f));
+}
+
+__device__ __forceinline__ uint32_t perm(uint32_t hi, uint32_t lo, uint32_t sel)
+{
+    return __builtin_amdgcn_perm(hi, lo, sel);
+}
+__device__ __forceinline__ uint32_t align2(uint32_t hi, uint32_t lo)
+{
+    return __builtin_amdgcn_alignbyte(hi, lo, 2); // (hi:lo) >> 16
+}
+
+// Staged window of one pixel tile: rows r0 - K .. r0 + TR + K - 1 of x and
+// rows r0 .. r0 + TR - 1 of dy; rows outside the image or past the tile end
+// (dy) are zero.  Item: one CW-column chunk of one row of one channel.
+template <int K, int CW, int U> struct Wg32Regs {
+    typedef typename std::conditional<CW == 8, uint4, uint2>::type Chunk;
+    Chunk v[U];
+    uint32_t okm; // bit u: item u holds image data (else it stages zeros)
+
+    // Every load is issued unconditionally (rows outside the image read row
+    // 0 of the plane, items past the end read item 0) so that none waits for
+    // another; okm says which to keep.
+    __device__ __forceinline__ void load(const bf16raw *__restrict__ x,
+                                         const bf16raw *__restrict__ dy, const Wg32Args &a,
+                                         int n, int r0, int rows)
+    {
+        const size_t HW = static_cast<size_t>(a.H) * a.W;
+        const int XR = a.TR + 2 * K;
+        const int total = a.items_x + a.items_dy;
+        okm = 0;
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            const int it0 = threadIdx.x + u * kT;
+            const int it = it0 < total ? it0 : 0;
+            int ch, c, r;
+            bool ok;
+            const bf16raw *src;
+            if (it < a.items_x) {
+                const int rest = udiv(it, a.fcpr);
+                c = it - rest * a.cpr;
+                ch = udiv(rest, a.fxr);
+                const int rr = rest - ch * XR;
+                r = r0 - K + rr;
+                ok = r >= 0 && r < a.H;
+                src = x + (static_cast<size_t>(n) * a.CI + ch) * HW;
+            } else {
+                const int i2 = it - a.items_x;
+                const int rest = udiv(i2, a.fcpr);
+                c = i2 - rest * a.cpr;
+                ch = udiv(rest, a.ftr);
+                const int rr = rest - ch * a.TR;
+                r = r0 + rr;
+                ok = rr < rows;
+                src = dy + (static_cast<size_t>(n) * a.COT + a.co0 + ch) * HW;
+            }
+            ok = ok && it0 < total;
+            v[u] = *reinterpret_cast<const Chunk *>(src + static_cast<size_t>(ok ? r : 0) * a.W + c * CW);
+            okm |= ok ? (1u << u) : 0u;
+        }
+    }
+
+    // even columns of the chunk to parity 0, odd to parity 1
+    __device__ __forceinline__ void commit(bf16raw *__restrict__ lds, const Wg32Args &a) const
+    {
+        const int XR = a.TR + 2 * K;
+        const int total = a.items_x + a.items_dy;
+        constexpr uint32_t E = 0x05040100u, O = 0x07060302u;
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            const int it = threadIdx.x + u * kT;
+            if (it >= total)
+                continue;
+            int c, off0, off1;
+            if (it < a.items_x) {
+                const int rest = udiv(it, a.fcpr);
+                c = it - rest * a.cpr;
+                const int ch = udiv(rest, a.fxr), rr = rest - ch * XR;
+                const int b = a.x_off + ch * a.xc + (rr * 2) * a.XS + 8 + c * (CW / 2);
+                off0 = b;
+                off1 = b + a.XS;
+            } else {
+                const int i2 = it - a.items_x;
+                const int rest = udiv(i2, a.fcpr);
+                c = i2 - rest * a.cpr;
+                const int ch = udiv(rest, a.ftr), rr = rest - ch * a.TR;
+                const int b = ch * a.dyc + (rr * 2) * a.WS + c * (CW / 2);
+                off0 = b;
+                off1 = b + a.WS;
+            }
+            const bool ok = (okm >> u) & 1u;
+            if constexpr (CW == 8) {
+                const uint4 q = ok ? v[u] : make_uint4(0, 0, 0, 0);
+                *reinterpret_cast<uint2 *>(lds + off0) = make_uint2(perm(q.y, q.x, E), perm(q.w, q.z, E));
+                *reinterpret_cast<uint2 *>(lds + off1) = make_uint2(perm(q.y, q.x, O), perm(q.w, q.z, O));
+            } else {
+                const uint2 q = ok ? v[u] : make_uint2(0, 0);
+                *reinterpret_cast<uint32_t *>(lds + off0) = perm(q.y, q.x, E);
+                *reinterpret_cast<uint32_t *>(lds + off1) = perm(q.y, q.x, O);
+            }
+        }
+    }
+};
+
+// B fragment: the 8 split elements starting S (-1, 0, 1) positions after the
+// 16-byte aligned element p.
+template <int S> __device__ __forceinline__ bf16x8 load_shifted(const bf16raw *__restrict__ p)
+{
+    if constexpr (S == 0) {
+        return *reinterpret_cast<const bf16x8 *>(p);
+    } else if constexpr (S == 1) {
+        const uint4 c0 = *reinterpret_cast<const uint4 *>(p);
+        const uint32_t c1 = *reinterpret_cast<const uint32_t *>(p + 8);
+        return __builtin_bit_cast(bf16x8, make_uint4(align2(c0.y, c0.x), align2(c0.z, c0.y),
+                                                     align2(c0.w, c0.z), align2(c1, c0.w)));
+    } else {
+        const uint4 c0 = *reinterpret_cast<const uint4 *>(p);
+        const uint32_t cm = *reinterpret_cast<const uint32_t *>(p - 2);
+        return __builtin_bit_cast(bf16x8, make_uint4(align2(c0.x, cm), align2(c0.y, c0.x),
+                                                     align2(c0.z, c0.y), align2(c0.w, c0.z)));
+    }
+}
+
+// A fragment of K-step q (dy, run 2q + kh of parity P) and where its runs
+// start: window row and split position.
+template <int P> struct WgA {
+    bf16x8 a;
+    int rrow, j0;
+    __device__ __forceinline__ void fetch(const bf16raw *__restrict__ dyb, int WS, int rpr,
+                                          const FastDiv &frpr, int q, int kh)
+    {
+        const int run = 2 * q + kh;
+        rrow = udiv(run, frpr);
+        j0 = (run - rrow * rpr) * 8;
+        a = *reinterpret_cast<const bf16x8 *>(dyb + (rrow * 2 + P) * WS + j0);
+    }
+};
+
+// Products of one K-step for taps [T0, T1): every B fragment (x moved by
+// the tap) is read first, then the products run in tap order.
+template <int K, int P, int T0, int T1, int NA>
+__device__ __forceinline__ void wg_kstep(floatx16 (&acc)[NA], const WgA<P> &A, float &dbs,
+                                         bool do_db, const bf16raw *__restrict__ xb, int XS)
+{
+    constexpr TapTable<K> tt;
+    if (do_db) {
+#pragma unroll
+        for (int e = 0; e < 8; ++e)
+            dbs += static_cast<float>(A.a[e]);
+    }
+#pragma unroll
+    for (int t = T0; t < T1; ++t) {
+        const int dq = tt.dq[t], ds = tt.ds[t];
+        const int dr = tap_drow(dq, ds, P);
+        const int sh = floor_half(P + dq);
+        const bf16raw *base = xb + A.j0 + ((A.rrow + K + dr) * 2 + ((P + dq) & 1)) * XS;
+        bf16x8 b;
+        if (sh == 0)
+            b = load_shifted<0>(base);
+        else if (sh == 1)
+            b = load_shifted<1>(base);
+        else
+            b = load_shifted<-1>(base);
+        acc[t - T0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(A.a, b, acc[t - T0], 0, 0, 0);
+    }
+}
+
+// All K-steps of column parity P for taps [T0, T1); the A fragment of step
+// q + 1 is read before the products of step q (two buffers, two steps per
+// iteration so that the buffers are named at compile time).
+template <int K, int P, int T0, int T1, int NA>
+__device__ __forceinline__ void wg_parity(floatx16 (&acc)[NA], float &dbs, bool do_db,
+                                          const bf16raw *__restrict__ dyb,
+                                          const bf16raw *__restrict__ xb, int WS, int XS, int rpr,
+                                          const FastDiv &frpr, int nq, int kh)
+{
+    if (nq <= 0)
+        return;
+    for (int q = 0; q < nq; ++q) {
+        WgA<P> a0;
+        a0.fetch(dyb, WS, rpr, frpr, q, kh);
+        wg_kstep<K, P, T0, T1, NA>(acc, a0, dbs, do_db, xb, XS);
+    }
+}
+
+// Dispatch to the tap group g of this wave (wave-uniform), compile-time taps.
+template <int K, int TPG, int GI, int G>
+__device__ __forceinline__ void wg_tile(int g, floatx16 (&acc)[TPG], float &dbs, bool do_db,
+                                        const bf16raw *__restrict__ dyb,
+                                        const bf16raw *__restrict__ xb, int WS, int XS, int rpr,
+                                        const FastDiv &frpr, int nq, int kh)
+{
+    if constexpr (GI < G) {
+        constexpr int T = num_taps(K);
+        constexpr int T0 = GI * TPG;
+        constexpr int T1 = (T0 + TPG < T) ? T0 + TPG : T;
+        if (g == GI) {
+            if constexpr (T1 > T0) {
+                wg_parity<K, 0, T0, T1, TPG>(acc, dbs, do_db, dyb, xb, WS, XS, rpr, frpr, nq, kh);
+                wg_parity<K, 1, T0, T1, TPG>(acc, dbs, do_db, dyb, xb, WS, XS, rpr, frpr, nq, kh);
+            }
+        } else {
+            wg_tile<K, TPG, GI + 1, G>(g, acc, dbs, do_db, dyb, xb, WS, XS, rpr, frpr, nq, kh);
+        }
+    }
+}
+
+template <int K, int G, int CW, int U>
+__global__ __launch_bounds__(kT) void wgrad32_k(const bf16raw *__restrict__ x,
+                                                const bf16raw *__restrict__ dy,
+                                                float *__restrict__ part, Wg32Args a)
+{
+    constexpr int T = num_taps(K);
+    constexpr int TPG = (T + G - 1) / G; // taps per group
+    extern __shared__ __align__(16) bf16raw lds[];
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int n32 = lane & 31, kh = lane >> 5;
+    const int NIB = a.CI >> 5, NCB = a.CO >> 5;
+    const int C = NIB * NCB; // (ci block, co block) pairs; C * G == 8
+    const int combo = wave % C, g = wave / C;
+    const int ib = combo % NIB, cb = combo / NIB;
+    const int t0 = g * TPG;
+    const int slot = blockIdx.x;
+
+    // zero the whole LDS once: pads and unused split positions stay zero
+    {
+        const int total = (a.x_off + a.CI * a.xc) / 8;
+        for (int e = threadIdx.x; e < total; e += kT)
+            reinterpret_cast<uint4 *>(lds)[e] = make_uint4(0, 0, 0, 0);
+    }
+
+    floatx16 acc[TPG];
+#pragma unroll
+    for (int i = 0; i < TPG; ++i)
+#pragma unroll
+        for (int r = 0; r < 16; ++r)
+            acc[i][r] = 0.f;
+    float dbs = 0.f;
+    const bool do_db = (ib == 0 && g == 0);
+
+    const int t_begin = slot * a.per_block;
+    const int t_end = min(t_begin + a.per_block, a.ptiles);
+    const bf16raw *dyb = lds + (cb * 32 + n32) * a.dyc;
+    const bf16raw *xb = lds + a.x_off + (ib * 32 + n32) * a.xc + 8;
+    const int rpr = a.WS >> 3; // runs per split row
+
+    Wg32Regs<K, CW, U> regs;
+    if (t_begin < t_end) {
+        const int n = t_begin / a.ntr, r0 = (t_begin - n * a.ntr) * a.TR;
+        regs.load(x, dy, a, n, r0, min(a.TR, a.H - r0));
+    }
+    for (int pt = t_begin; pt < t_end; ++pt) {
+        __syncthreads(); // previous tile's reads done (and the LDS clear)
+        regs.commit(lds, a);
+        __syncthreads();
+        if (pt + 1 < t_end) {
+            const int n = (pt + 1) / a.ntr, r0 = (pt + 1 - n * a.ntr) * a.TR;
+            regs.load(x, dy, a, n, r0, min(a.TR, a.H - r0));
+        }
+        // K-steps: pairs of runs of one parity; run i = (row i / rpr,
+        // split position 8 * (i % rpr)); lanes kh = 0 / 1 take runs 2q / 2q+1
+        const int nq = (a.TR * rpr) >> 1;
+        wg_tile<K, TPG, 0, G>(g, acc, dbs, do_db, dyb, xb, a.WS, a.XS, rpr, a.frpr, nq, kh);
+    }
+
+    // partial slot of this block: tile (t, ib, cb) -> chunks (tile * 16 + r),
+    // one 64-float chunk per accumulator register, lanes in order
+    const int ntap = min(TPG, T - t0);
+    for (int i = 0; i < TPG; ++i) {
+        if (i >= ntap)
+            break;
+        const int tile = ((t0 + i) * NIB + ib) * NCB + cb;
+#pragma unroll
+        for (int r = 0; r < 16; ++r)
+            part[part_index(tile * 16 * kRegChunk + r * kRegChunk + lane, slot, a.nparts)] = acc[i][r];
+    }
+    if (do_db) {
+        // lanes n32 and n32 + 32 hold the same channel
+        const float s = dbs + __shfl_xor(dbs, 32, 64);
+        const int base = T * NIB * NCB * 16 * kRegChunk; // db after the tiles
+        if (kh == 0)
+            part[part_index(base + cb * 32 + n32, slot, a.nparts)] = s;
+    }
+}
+
+// Sum the slots of every partial position in a fixed order and scatter to
+// dw[co][ci][t] / db[co].
+__global__ __launch_bounds__(256) void wgrad32_reduce_k(const float *__restrict__ part, int nparts,
+                                                        int npos, int CI, int CO, int co0, int T,
+                                                        float *__restrict__ dw,
+                                                        float *__restrict__ db)
+{
+    const int pos = blockIdx.x * 64 + (threadIdx.x & 63);
+    const int sl = threadIdx.x >> 6; // 4 slices of the slots
+    __shared__ float red[4][64];
+    float s = 0.f;
+    if (pos < npos)
+        for (int p = sl; p < nparts; p += 4)
+            s += part[part_index(pos, p, nparts)];
+    red[sl][threadIdx.x & 63] = s;
+    __syncthreads();
+    if (sl != 0 || pos >= npos)
+        return;
+    const int l = threadIdx.x;
+    const float v = (red[0][l] + red[1][l]) + (red[2][l] + red[3][l]);
+    const int NIB = CI >> 5, NCB = CO >> 5;
+    const int ntile_pos = T * NIB * NCB * 16 * kRegChunk;
+    if (pos < ntile_pos) {
+        const int tile = pos / (16 * kRegChunk);
+        const int r = (pos / kRegChunk) % 16, lane = pos % kRegChunk;
+        const int cb = tile % NCB, ib = (tile / NCB) % NIB, t = tile / (NCB * NIB);
+        const int co = co0 + cb * 32 + 8 * (r / 4) + 4 * (lane / 32) + r % 4;
+        const int ci = ib * 32 + lane % 32;
+        dw[(static_cast<size_t>(co) * CI + ci) * T + t] = v;
+    } else if (db != nullptr) {
+        db[co0 + pos - ntile_pos] = v;
+    }
+}
+
+inline int cdiv(long a, long b) { return static_cast<int>((a + b - 1) / b); }
+
+constexpr size_t kLdsMax = 160 * 1024;
+
+// Most staging items per thread (prefetch registers) that each (K, tap
+// groups G, chunk width CW) variant holds without spilling next to its
+// accumulators (checked with the compiler's resource report); 0: the taps
+// per wave alone exceed the register budget.
+constexpr int max_items(int K, int G, int CW)
+{
+    if (K == 1)
+        return G == 1 ? 0 : G == 2 ? 4 : G == 4 ? (CW == 8 ? 8 : 12) : 12;
+    return G <= 2 ? 0 : G == 4 ? 4 : 8;
+}
+
+// tiling of the pass over output channels co0 .. co0 + CO - 1 for a given
+// rows-per-tile; false if it does not fit
+bool wg32_args(const ConvShape &sh, int co0, int CO, int TR, Wg32Args &a)
+{
+    a.N = sh.N;
+    a.H = sh.H;
+    a.W = sh.W;
+    a.CI = sh.Ci;
+    a.CO = CO;
+    a.co0 = co0;
+    a.COT = sh.Co;
+    a.WS = cdiv((sh.W + 1) / 2, 8) * 8;
+    a.XS = a.WS + 16;
+    a.TR = TR;
+    if ((a.TR * (a.WS / 8)) % 2 != 0)
+        return false; // K-steps pair runs of one parity
+    a.ntr = cdiv(sh.H, a.TR);
+    a.ptiles = sh.N * a.ntr;
+    // pitches: odd multiples of 16 bytes (32-row fragment reads)
+    a.dyc = a.TR * 2 * a.WS + 8;
+    if ((a.dyc / 8) % 2 == 0)
+        a.dyc += 8;
+    a.xc = (a.TR + 2 * sh.k) * 2 * a.XS + 8;
+    if ((a.xc / 8) % 2 == 0)
+        a.xc += 8;
+    a.x_off = CO * a.dyc;
+    const size_t lds = 2ull * (a.x_off + static_cast<size_t>(sh.Ci) * a.xc);
+    if (lds > kLdsMax)
+        return false;
+    const int CW = (sh.W % 8 == 0) ? 8 : 4;
+    a.cpr = sh.W / CW;
+    a.items_x = sh.Ci * (a.TR + 2 * sh.k) * a.cpr;
+    a.items_dy = CO * a.TR * a.cpr;
+    a.fcpr = make_fastdiv(static_cast<uint32_t>(a.cpr));
+    a.fxr = make_fastdiv(static_cast<uint32_t>(a.TR + 2 * sh.k));
+    a.ftr = make_fastdiv(static_cast<uint32_t>(a.TR));
+    a.frpr = make_fastdiv(static_cast<uint32_t>(a.WS / 8));
+    return true;
+}
+
+int wg32_U(const Wg32Args &a) { return cdiv(a.items_x + a.items_dy, kT); }
+
+// Most (ci block, co block) pairs one pass holds: the waves of a pass split
+// the taps into 8 / pairs groups, and a group's accumulators must fit.
+int wg32_max_pairs(int k) { return k == 1 ? 4 : 2; }
+
+// Output channels per pass: as many 32-channel blocks as the pair limit
+// allows next to all input-channel blocks (0: the input channels alone are
+// too many).
+int wg32_pass_co(const ConvShape &sh)
+{
+    const int nib = sh.Ci / 32;
+    const int lim = wg32_max_pairs(sh.k);
+    if (nib > lim)
+        return 0;
+    return 32 * std::min(sh.Co / 32, lim / nib);
+}
+
+bool wg32_plan(const ConvShape &sh, int co0, int CO, Wg32Args &a)
+{
+    const int C = (sh.Ci / 32) * (CO / 32);
+    if (C != 1 && C != 2 && C != 4 && C != 8)
+        return false;
+    const int umax = max_items(sh.k, 8 / C, (sh.W % 8 == 0) ? 8 : 4);
+    // tallest tile (at most 512 pixels) that fits LDS and the staging registers
+    for (int TR = std::min(sh.H, std::max(1, 512 / sh.W)); TR >= 1; --TR) {
+        if (wg32_args(sh, co0, CO, TR, a) && wg32_U(a) <= umax) {
+            const int blocks = std::max(1, std::min(device_cus(), a.ptiles));
+            a.per_block = cdiv(a.ptiles, blocks);
+            a.nparts = cdiv(a.ptiles, a.per_block);
+            a.nchunk = sh.T * C * 16 + cdiv(CO, kRegChunk);
+            return true;
+        }
+    }
+    return false;
+}
+
+// Calls f(co0, CO, args) for every pass; false if some pass has no plan.
+template <typename F> bool wg32_passes(const ConvShape &sh, F &&f)
+{
+    if (sh.s != 1 || (sh.k != 1 && sh.k != 2) || sh.Ci % 32 != 0 || sh.Co % 32 != 0 ||
+        sh.W % 4 != 0)
+        return false;
+    const int pco = wg32_pass_co(sh);
+    if (pco == 0)
+        return false;
+    for (int co0 = 0; co0 < sh.Co;) {
+        // a power of two of 32-channel blocks, so the tap groups split evenly
+        int nb = std::min(pco, sh.Co - co0) / 32;
+        while (nb & (nb - 1))
+            nb &= nb - 1;
+        Wg32Args a{};
+        if (!wg32_plan(sh, co0, 32 * nb, a) || !f(a))
+            return false;
+        co0 += 32 * nb;
+    }
+    return true;
+}
+
+template <int K, int G, int CW, int U>
+void launch_w32_u(const Wg32Args &a, size_t lds, hipStream_t st, const bf16raw *x,
+                  const bf16raw *dy, float *part)
+{
+    if constexpr (U <= max_items(K, G, CW))
+        hipLaunchKernelGGL((wgrad32_k<K, G, CW, U>), dim3(a.nparts), dim3(kT), lds, st, x, dy,
+                           part, a);
+}
+
+template <int K, int G, int CW>
+void launch_w32_cw(int U, const Wg32Args &a, size_t lds, hipStream_t st, const bf16raw *x,
+                   const bf16raw *dy, float *part)
+{
+    if (U <= 4)
+        launch_w32_u<K, G, CW, 4>(a, lds, st, x, dy, part);
+    else if (U <= 8)
+        launch_w32_u<K, G, CW, 8>(a, lds, st, x, dy, part);
+    else
+        launch_w32_u<K, G, CW, 12>(a, lds, st, x, dy, part);
+}
+
+template <int K>
+void launch_w32(int G, bool cw8, int U, const Wg32Args &a, size_t lds, hipStream_t st,
+                const bf16raw *x, const bf16raw *dy, float *part)
+{
+#define HEX_W32_G(GV)                                                                        \
+    do {                                                                                     \
+        if (cw8) launch_w32_cw<K, GV, 8>(U, a, lds, st, x, dy, part);                         \
+        else launch_w32_cw<K, GV, 4>(U, a, lds, st, x, dy, part);                             \
+    } while (0)
+    if (G == 1) HEX_W32_G(1);
+    else if (G == 2) HEX_W32_G(2);
+    else if (G == 4) HEX_W32_G(4);
+    else HEX_W32_G(8);
+#undef HEX_W32_G
+}
+
+} // namespace
+
+bool bf16_wgrad32_ok(const ConvShape &sh)
+{
+    return wg32_passes(sh, [](const Wg32Args &) { return true; });
+}
+
+// One partial buffer serves every pass: the passes run in stream order.
+size_t bf16_wgrad32_workspace(const ConvShape &sh)
+{
+    size_t need = 0;
+    if (!wg32_passes(sh, [&](const Wg32Args &a) {
+            need = std::max(need, sizeof(float) * static_cast<size_t>(a.nchunk) * kRegChunk *
+                                      a.nparts);
+            return true;
+        }))
+        return 0;
+    return need;
+}
+
+hipError_t bf16_wgrad32(const void *x, const void *dy, float *dw, float *db, void *ws,
+                        const ConvShape &sh, hipStream_t st)
+{
+    const bf16raw *xp = static_cast<const bf16raw *>(x);
+    const bf16raw *dp = static_cast<const bf16raw *>(dy);
+    float *part = static_cast<float *>(ws);
+    hipError_t err = hipSuccess;
+    const bool ok = wg32_passes(sh, [&](const Wg32Args &a) {
+        const int C = (sh.Ci / 32) * (a.CO / 32);
+        const int G = 8 / C;
+        const int U = wg32_U(a);
+        const bool cw8 = sh.W % 8 == 0;
+        const size_t lds = 2ull * (a.x_off + static_cast<size_t>(sh.Ci) * a.xc);
+        if (sh.k == 1)
+            launch_w32<1>(G, cw8, U, a, lds, st, xp, dp, part);
+        else
+            launch_w32<2>(G, cw8, U, a, lds, st, xp, dp, part);
+        err = hipGetLastError();
+        if (err != hipSuccess)
+            return false;
+        const int npos = sh.T * C * 16 * kRegChunk + a.CO;
+        hipLaunchKernelGGL(wgrad32_reduce_k, dim3(cdiv(npos, 64)), dim3(256), 0, st, part,
+                           a.nparts, npos, sh.Ci, a.CO, a.co0, sh.T, dw, db);
+        err = hipGetLastError();
+        return err == hipSuccess;
+    });
+    if (!ok && err == hipSuccess)
+        return hipErrorInvalidValue;
+    return err;
+}
+
+} // namespace hexk

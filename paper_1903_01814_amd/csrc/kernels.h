@@ -90,6 +90,12 @@ bool bf16_wide_ok(const ConvShape &sh, int IC, int OC);
 hipError_t bf16_wide_conv(const void *in, const void *w, const void *bias, void *out,
                           const ConvShape &sh, bool reflect, bool relu, hipStream_t st);
 
+// ---- bf16 32x32 matrix-core weight gradient (C_in, C_out multiples of 32) --
+bool bf16_wgrad32_ok(const ConvShape &sh);
+size_t bf16_wgrad32_workspace(const ConvShape &sh);
+hipError_t bf16_wgrad32(const void *x, const void *dy, float *dw, float *db, void *ws,
+                        const ConvShape &sh, hipStream_t st);
+
 // ---- bf16 matrix-core weight gradient (stride 1, k <= 2, W % 8 == 0) ----
 bool bf16_wgrad_ok(const ConvShape &sh);
 size_t bf16_wgrad_workspace(const ConvShape &sh);

@@ -287,6 +287,9 @@ SWEEP = [
     (2, 32, 48, 10, 16, 1, 1), (1, 64, 128, 12, 12, 1, 1), (2, 64, 64, 37, 16, 1, 1),
     (1, 96, 32, 8, 24, 1, 1), (1, 32, 32, 6, 20, 2, 1), (1, 64, 64, 30, 12, 1, 1),
     (1, 32, 16, 6, 128, 2, 1), (1, 32, 32, 3, 256, 1, 1), (2, 128, 64, 5, 8, 2, 1),
+    # matrix-core weight gradient in several output-channel passes (128 + 64
+    # + 32, 64 + 64 at k=2, 64 + 32 with two input-channel blocks)
+    (1, 32, 224, 6, 16, 1, 1), (2, 32, 128, 7, 12, 2, 1), (1, 64, 96, 5, 20, 1, 1),
 ]
 
 
