@@ -42,9 +42,10 @@ using namespace hexgeom;
 
 typedef float floatx4 __attribute__((ext_vector_type(4)));
 
-constexpr int kThreads = 256;
-constexpr int kWaves = kThreads / 64;
-constexpr int kTR = 8; // rows per tile
+constexpr int kThreads = 512;   // 8 waves per block, one block per compute unit
+constexpr int kDxThreads = 256; // waves 0-3: data gradient; waves 4-7: weight gradient
+constexpr int kDwWaves = 4;
+constexpr int kTR = 8;          // rows per tile
 
 template <int K> struct Geo {
     static constexpr int LR = kTR + 2 * K; // window rows
@@ -68,12 +69,11 @@ struct BwdTiling {
     FastDiv fdw4, fdlr;
 };
 
-// One tile's dy and x rows in registers: item i = tid + u * 256 is
-// (channel, window row, float4 column group).  The LDS word of an item and
-// its element offset inside the image do not depend on the tile, so they are
-// computed once (pk: LDS word | window row << 16 | dy item << 24 | live << 25).
-template <int K, int U> struct Stage {
-    float4 v[U];
+// Where the staging items of a thread go: item i = tid + u * kThreads is
+// (channel, window row, float4 column group).  Its LDS word and its element
+// offset inside the image do not depend on the tile, so they are computed
+// once (pk: LDS word | window row << 16 | dy item << 24 | live << 25).
+template <int K, int U> struct StageMap {
     int pk[U], goff[U];
 
     __device__ __forceinline__ void init(const ConvShape &sh, const BwdTiling &bt)
@@ -95,9 +95,21 @@ template <int K, int U> struct Stage {
             goff[u] = (isdy ? ch : ch - sh.Co) * HW + rr * sh.W + 4 * c4;
         }
     }
+};
 
-    __device__ __forceinline__ void load(const float *__restrict__ x, const float *__restrict__ dy,
-                                         const ConvShape &sh, int n, int r0)
+// One tile's dy and x rows in registers.  Every load is issued (items
+// outside the image read a valid address) and okm records which hold image
+// data; the others are replaced by zeros when committed.  Loads that are
+// always issued keep the count of loads in flight fixed, so a commit waits
+// only for its own buffer.
+template <int U> struct StageBuf {
+    float4 v[U];
+    uint32_t okm;
+
+    template <int K>
+    __device__ __forceinline__ void load(const StageMap<K, U> &m, const float *__restrict__ x,
+                                         const float *__restrict__ dy, const ConvShape &sh, int n,
+                                         int r0)
     {
         const size_t HW = static_cast<size_t>(sh.H) * sh.W;
         // row r0 - K of image n, channel 0: items add their offsets to it
@@ -105,40 +117,38 @@ template <int K, int U> struct Stage {
         const float *dyn = dy + static_cast<size_t>(n) * sh.Co * HW + rofs;
         const float *xn = x + static_cast<size_t>(n) * sh.Ci * HW + rofs;
         const int rlo = K - r0, rhi = sh.H - r0 + K; // window rows inside the image
+        okm = 0;
 #pragma unroll
         for (int u = 0; u < U; ++u) {
-            const int rr = (pk[u] >> 16) & 0xff;
-            const bool ok = ((pk[u] >> 25) & 1) && rr >= rlo && rr < rhi;
-            const float *b = ((pk[u] >> 24) & 1) ? dyn : xn;
-            const float4 q4 = *reinterpret_cast<const float4 *>(ok ? b + goff[u] : x);
-            v[u] = ok ? q4 : make_float4(0.f, 0.f, 0.f, 0.f);
+            const int rr = (m.pk[u] >> 16) & 0xff;
+            const bool ok = ((m.pk[u] >> 25) & 1) && rr >= rlo && rr < rhi;
+            const float *b = ((m.pk[u] >> 24) & 1) ? dyn : xn;
+            v[u] = *reinterpret_cast<const float4 *>(ok ? b + m.goff[u] : x);
+            okm |= ok ? 1u << u : 0u;
         }
     }
 
     // columns 4c4 .. 4c4+3 of a row sit at +0, +P, +2P-1, +3P-1
-    __device__ __forceinline__ void commit(float *__restrict__ lds) const
+    template <int K>
+    __device__ __forceinline__ void commit(const StageMap<K, U> &m, float *__restrict__ lds) const
     {
         using G = Geo<K>;
 #pragma unroll
         for (int u = 0; u < U; ++u) {
-            float *d = lds + (pk[u] & 0xffff);
-            d[0] = v[u].x;
-            d[G::P] = v[u].y;
-            d[2 * G::P - 1] = v[u].z;
-            d[3 * G::P - 1] = v[u].w;
+            const float4 q = ((okm >> u) & 1) ? v[u] : make_float4(0.f, 0.f, 0.f, 0.f);
+            float *d = lds + (m.pk[u] & 0xffff);
+            d[0] = q.x;
+            d[G::P] = q.y;
+            d[2 * G::P - 1] = q.z;
+            d[3 * G::P - 1] = q.w;
         }
     }
 };
 
-#ifndef HEX_BWD_WPE
-#define HEX_BWD_WPE 2
-#endif
-
 template <int K, int CI, int MT, int NT, int CG, int U>
-__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(HEX_BWD_WPE, 8)))
-void bwd_f32_k(const float *__restrict__ x, const float *__restrict__ dy, const float *__restrict__ w,
-               float *__restrict__ dx, float *__restrict__ part, ConvShape sh, BwdTiling bt,
-               int do_dx)
+__global__ __launch_bounds__(kThreads) void bwd_f32_k(
+    const float *__restrict__ x, const float *__restrict__ dy, const float *__restrict__ w,
+    float *__restrict__ dx, float *__restrict__ part, ConvShape sh, BwdTiling bt, int do_dx)
 {
     using Gm = Geo<K>;
     constexpr int T = num_taps(K);
@@ -150,9 +160,48 @@ void bwd_f32_k(const float *__restrict__ x, const float *__restrict__ dy, const 
     const int W = sh.W, Co = sh.Co;
     const int tid = threadIdx.x;
     const int lane = tid & 63, wave = tid >> 6;
-    const int m = lane & 15, kq = lane >> 4;
+    const bool dxrole = wave < kDwWaves;
 
-    // weight gradient operands of this lane (word offsets from a pixel)
+    // reflected weights (at most 3 per thread: (C_out + 1) * C_in * T <= 33 *
+    // 2 * 19 < 3 * kThreads), read before the tile loads so that waiting for
+    // them does not wait for the tiles
+    const int nwl = (Co + 1) * CI * T;
+    float wreg[3];
+#pragma unroll
+    for (int u = 0; u < 3; ++u) {
+        const int e = tid + u * kThreads;
+        const int co = e / (CI * T), rem = e - co * (CI * T);
+        const int ci = rem / T, t = rem - ci * T;
+        wreg[u] = (e < nwl && co < Co) ? w[(static_cast<size_t>(co) * CI + ci) * T + (T - 1 - t)]
+                                       : 0.f;
+    }
+
+    // the first two tiles' loads are in flight during the one-time set-up
+    StageMap<K, U> map;
+    map.init(sh, bt);
+    StageBuf<U> sa, sb;
+    const int tpi = bt.tiles_per_img, gs = gridDim.x;
+    // Every step issues the same loads (a tile past the end reloads the last
+    // one and is never committed), so the wait before a commit only covers
+    // the loads of that buffer and not the newer ones in flight.
+    auto load_tile = [&](StageBuf<U> &b, int t) {
+        t = min(t, bt.ntiles - 1);
+        const int n = t / tpi;
+        b.load(map, x, dy, sh, n, (t - n * tpi) * kTR);
+    };
+    load_tile(sa, blockIdx.x);
+    load_tile(sb, blockIdx.x + gs);
+
+    // ---- data gradient role: thread = (channel group g, column c), all TR
+    // rows of the column, CG output channels
+    const bool dxthr = dxrole && do_dx != 0 && tid < bt.G * W;
+    const int g = dxthr ? tid / W : 0;
+    const int c = dxthr ? tid - g * W : 0;
+    const int cbase = Gm::colbase(c) + K; // word of (row r0, column c)
+    // ---- weight gradient role: operands of this lane (word offsets from a
+    // pixel); lanes without a channel or a tap read a plane of zeros, the
+    // bias column a plane of ones
+    const int m = lane & 15, kq = lane >> 4;
     int abase[MT];
 #pragma unroll
     for (int i = 0; i < MT; ++i)
@@ -169,12 +218,12 @@ void bwd_f32_k(const float *__restrict__ x, const float *__restrict__ dy, const 
             bbase[j] = bt.xo + ci * bt.CS + dq * P + ds;
         }
     }
-    // K-steps of this wave: pixel quads (column c0w + 2i, rows 4 * (wave & 1) + 0..3)
-    const int c0w = wave >> 1;
-    const int p0 = Gm::colbase(c0w) + K + 4 * (wave & 1) + kq;
+    // K-steps of this wave: pixel quads (column c0w + 2i, rows 4 * (dw & 1) + 0..3)
+    const int dwv = wave - kDwWaves;
+    const int c0w = (dwv >> 1) & 1;
+    const int p0 = Gm::colbase(c0w) + K + 4 * (dwv & 1) + kq;
     constexpr int PSTEP = 2 * P - 1; // two columns further
     const int nsteps = (W - c0w + 1) / 2;
-    const int per = (nsteps + CG - 1) / CG + 1 & ~1; // steps per channel iteration, even
     floatx4 acc[2][MT][NT];
 #pragma unroll
     for (int h = 0; h < 2; ++h)
@@ -183,7 +232,6 @@ void bwd_f32_k(const float *__restrict__ x, const float *__restrict__ dy, const 
 #pragma unroll
             for (int j = 0; j < NT; ++j)
                 acc[h][i][j] = floatx4{0.f, 0.f, 0.f, 0.f};
-    // one K-step: 4 pixels of this wave's quad i into accumulator set h
     auto kstep = [&](int i, int h) {
         const int pa = p0 + i * PSTEP;
         float a[MT], b[NT];
@@ -201,23 +249,9 @@ void bwd_f32_k(const float *__restrict__ x, const float *__restrict__ dy, const 
                     __builtin_amdgcn_mfma_f32_16x16x4f32(a[ii], b[j], acc[h][ii][j], 0, 0, 0);
     };
 
-    // data gradient: this thread's column and channel group
-    const bool dxthr = do_dx != 0 && tid < bt.G * W;
-    const int g = dxthr ? tid / W : 0;
-    const int c = dxthr ? tid - g * W : 0;
-    const int cbase = Gm::colbase(c) + K; // word of (row r0, column c)
-
-    // the first tile's loads are in flight during the one-time set-up
-    Stage<K, U> stg;
-    stg.init(sh, bt);
-    int tile = blockIdx.x;
-    if (tile < bt.ntiles) {
-        const int n = tile / bt.tiles_per_img;
-        stg.load(x, dy, sh, n, (tile - n * bt.tiles_per_img) * kTR);
-    }
-
     // once per block: zero halo columns of every channel, the zeros plane,
-    // the ones plane, the reflected weights
+    // the ones plane, the reflected weights (no global load inside the tile
+    // loop: it would wait for the prefetches issued before it)
     {
         const int nch = Co + CI;
         for (int e = tid; e < nch * 2 * K * Gm::LR; e += kThreads) {
@@ -231,126 +265,146 @@ void bwd_f32_k(const float *__restrict__ x, const float *__restrict__ dy, const 
             lds[bt.zo + e] = 0.f;
             lds[bt.oo + e] = 1.f;
         }
-        for (int e = tid; e < (Co + 1) * CI * T; e += kThreads) {
-            const int co = e / (CI * T), rem = e - co * (CI * T);
-            const int ci = rem / T, t = rem - ci * T;
-            wl[e] = co < Co ? w[(static_cast<size_t>(co) * CI + ci) * T + (T - 1 - t)] : 0.f;
-        }
+#pragma unroll
+        for (int u = 0; u < 3; ++u)
+            if (tid + u * kThreads < nwl)
+                wl[tid + u * kThreads] = wreg[u];
     }
 
-    for (; tile < bt.ntiles; tile += gridDim.x) {
-        const int n = tile / bt.tiles_per_img;
-        const int r0 = (tile - n * bt.tiles_per_img) * kTR;
+    // One tile: stage it, start the loads of the tile two steps ahead into
+    // the same registers, then the two roles work on the window at the same
+    // time (VALU and matrix cores of each SIMD).  Rows past the image are
+    // zeros, so a short last tile needs no masking.
+    auto tile_step = [&](StageBuf<U> &buf, int tile) {
+        const int n = tile / tpi;
+        const int r0 = (tile - n * tpi) * kTR;
         const int rows = min(kTR, sh.H - r0);
-        stg.commit(lds);
+        buf.commit(map, lds);
         __syncthreads(); // tile staged (and, the first time, the constants)
-        const int tn = tile + gridDim.x;
-        if (tn < bt.ntiles) {
-            const int nn = tn / bt.tiles_per_img;
-            stg.load(x, dy, sh, nn, (tn - nn * bt.tiles_per_img) * kTR);
-        }
-
-        // Each channel iteration of the data gradient (VALU) is paired with
-        // a slice of the weight gradient's K-steps (matrix cores) so the two
-        // units work at the same time.  Rows past the image are zeros, so a
-        // short last tile needs no masking.
-        float gacc[CI][kTR];
-#pragma unroll
-        for (int ci = 0; ci < CI; ++ci)
-#pragma unroll
-            for (int r = 0; r < kTR; ++r)
-                gacc[ci][r] = 0.f;
-#pragma unroll 1
-        for (int cc = 0; cc < CG; ++cc) {
-            {
-                const int i1 = min(nsteps, (cc + 1) * per);
-                int i = cc * per;
-                for (; i + 1 < i1; i += 2) {
-                    kstep(i, 0);
-                    kstep(i + 1, 1);
-                }
-                if (i < i1)
-                    kstep(i, 0);
-            }
+        load_tile(buf, tile + 2 * gs);
+        if (dxrole) {
             if (dxthr) {
-                const int co = g * CG + cc;
-                const bool ok = co < Co;
-                const float *src = lds + (ok ? co : 0) * bt.CSD + cbase;
-                const float *wc = wl + (ok ? co : Co) * CI * T;
-                int t0 = 0;
+                float gacc[CI][kTR];
 #pragma unroll
-                for (int dq = -K; dq <= K; ++dq) {
-                    const int len = 2 * K + 1 - (dq < 0 ? -dq : dq);
-                    const int dslo = dq < 0 ? -K - dq : -K;
-                    const float *col = src + dq * P + dslo;
-                    float v[kTR + 2 * K];
+                for (int ci = 0; ci < CI; ++ci)
 #pragma unroll
-                    for (int j = 0; j < kTR + 2 * K; ++j)
-                        if (j < kTR + len - 1)
-                            v[j] = col[j];
+                    for (int r = 0; r < kTR; ++r)
+                        gacc[ci][r] = 0.f;
 #pragma unroll
-                    for (int u = 0; u < 2 * K + 1; ++u) {
-                        if (u < len) {
+                for (int cc = 0; cc < CG; ++cc) {
+                    const int co = g * CG + cc;
+                    const bool ok = co < Co;
+                    const float *src = lds + (ok ? co : 0) * bt.CSD + cbase;
+                    const float *wc = wl + (ok ? co : Co) * CI * T;
+                    int t0 = 0;
 #pragma unroll
-                            for (int ci = 0; ci < CI; ++ci) {
-                                const float wv = wc[ci * T + t0 + u];
+                    for (int dq = -K; dq <= K; ++dq) {
+                        const int len = 2 * K + 1 - (dq < 0 ? -dq : dq);
+                        const int dslo = dq < 0 ? -K - dq : -K;
+                        const float *col = src + dq * P + dslo;
+                        float v[kTR + 2 * K];
 #pragma unroll
-                                for (int r = 0; r < kTR; ++r)
-                                    gacc[ci][r] += wv * v[r + u];
+                        for (int j = 0; j < kTR + 2 * K; ++j)
+                            if (j < kTR + len - 1)
+                                v[j] = col[j];
+#pragma unroll
+                        for (int u = 0; u < 2 * K + 1; ++u) {
+                            if (u < len) {
+#pragma unroll
+                                for (int ci = 0; ci < CI; ++ci) {
+                                    const float wv = wc[ci * T + t0 + u];
+#pragma unroll
+                                    for (int r = 0; r < kTR; ++r)
+                                        gacc[ci][r] += wv * v[r + u];
+                                }
                             }
                         }
+                        t0 += len;
                     }
-                    t0 += len;
+                }
+#pragma unroll
+                for (int ci = 0; ci < CI; ++ci)
+#pragma unroll
+                    for (int r = 0; r < kTR; ++r)
+                        dxp[((g * CI + ci) * kTR + r) * W + c] = gacc[ci][r];
+            }
+        } else {
+            int i = 0;
+            for (; i + 1 < nsteps; i += 2) {
+                kstep(i, 0);
+                kstep(i + 1, 1);
+            }
+            if (i < nsteps)
+                kstep(i, 0);
+        }
+        __syncthreads(); // partials written; every read of the window done
+        // dx: the groups' partials added in a fixed order, 16-byte stores.
+        // Exactly CI stores per thread (CI * TR * W / 4 <= CI * kThreads for
+        // W <= 256); a thread past the end repeats the last element's store
+        // (same value, same address), so the count of stores in flight is
+        // fixed and the loads issued before them are not waited for.
+        if (do_dx != 0) {
+            const int perp4 = rows * W / 4;
+#pragma unroll
+            for (int u = 0; u < CI; ++u) {
+                const int e4 = min(tid + u * kThreads, CI * perp4 - 1);
+                {
+                    const int ci = e4 >= perp4 ? 1 : 0;
+                    const int rem = 4 * (e4 - ci * perp4);
+                    float4 s = make_float4(0.f, 0.f, 0.f, 0.f);
+                    for (int gg = 0; gg < bt.G; ++gg) {
+                        const float *q = dxp + (gg * CI + ci) * kTR * W + rem;
+                        s.x += q[0];
+                        s.y += q[1];
+                        s.z += q[2];
+                        s.w += q[3];
+                    }
+                    *reinterpret_cast<float4 *>(dx + (static_cast<size_t>(n) * CI + ci) * sh.H * W +
+                                                static_cast<size_t>(r0) * W + rem) = s;
                 }
             }
         }
-        if (dxthr) {
-#pragma unroll
-            for (int ci = 0; ci < CI; ++ci)
-#pragma unroll
-                for (int r = 0; r < kTR; ++r)
-                    dxp[((g * CI + ci) * kTR + r) * W + c] = gacc[ci][r];
-        }
-        __syncthreads(); // partials written; every read of the window done
-        if (do_dx != 0) {
-            const int perp = rows * W;
-            for (int e = tid; e < CI * perp; e += kThreads) {
-                const int ci = e / perp, rem = e - ci * perp;
-                float s = 0.f;
-                for (int gg = 0; gg < bt.G; ++gg)
-                    s += dxp[(gg * CI + ci) * kTR * W + rem];
-                dx[(static_cast<size_t>(n) * CI + ci) * sh.H * W + static_cast<size_t>(r0) * W + rem] = s;
-            }
-        }
+    };
+
+    // two register buffers, so the loop is unrolled by two
+    for (int tile = blockIdx.x; tile < bt.ntiles;) {
+        tile_step(sa, tile);
+        tile += gs;
+        if (tile >= bt.ntiles)
+            break;
+        tile_step(sb, tile);
+        tile += gs;
     }
 
-    // sum the accumulator sets and the waves in a fixed order; one partial
-    // per output element
+    // sum the accumulator sets and the weight-gradient waves in a fixed
+    // order; one partial per output element (chunked layout)
     __syncthreads();
-    float *red = lds; // [kWaves][MT * 16][NT * 16]
+    float *red = lds; // [kDwWaves][MT * 16][NT * 16]
+    if (!dxrole) {
 #pragma unroll
-    for (int i = 0; i < MT; ++i)
+        for (int i = 0; i < MT; ++i)
 #pragma unroll
-        for (int j = 0; j < NT; ++j)
+            for (int j = 0; j < NT; ++j)
 #pragma unroll
-            for (int q = 0; q < 4; ++q)
-                red[((wave * MT + i) * 16 + 4 * kq + q) * (NT * 16) + j * 16 + m] =
-                    acc[0][i][j][q] + acc[1][i][j][q];
+                for (int q = 0; q < 4; ++q)
+                    red[((dwv * MT + i) * 16 + 4 * kq + q) * (NT * 16) + j * 16 + m] =
+                        acc[0][i][j][q] + acc[1][i][j][q];
+    }
     __syncthreads();
     constexpr int Jt = J + 1;
     for (int e = tid; e < Co * Jt; e += kThreads) {
         const int row = e / Jt, col = e - row * Jt;
         float s = 0.f;
 #pragma unroll
-        for (int wv = 0; wv < kWaves; ++wv)
+        for (int wv = 0; wv < kDwWaves; ++wv)
             s += red[(wv * MT * 16 + row) * (NT * 16) + col];
-        part[(static_cast<size_t>(row) * Jt + col) * gridDim.x + blockIdx.x] = s;
+        part[part_index(e, blockIdx.x, gridDim.x)] = s;
     }
 }
 
 inline int cdiv(long a, long b) { return static_cast<int>((a + b - 1) / b); }
 
-constexpr size_t kLdsMax = 64 * 1024;
+constexpr size_t kLdsMax = 160 * 1024;
 
 int bwd_nt(const ConvShape &sh)
 {
@@ -370,7 +424,7 @@ BwdTiling bwd_tiling(const ConvShape &sh)
     bt.xo = sh.Co * bt.CSD;
     bt.zo = bt.xo + sh.Ci * bt.CS;
     bt.oo = bt.zo + bt.CS;
-    bt.G = std::max(1, std::min(sh.Co, kThreads / sh.W));
+    bt.G = std::max(1, std::min(sh.Co, kDxThreads / sh.W));
     bt.tiles_per_img = cdiv(sh.H, kTR);
     bt.ntiles = bt.tiles_per_img * sh.N;
     bt.nitems = (sh.Co + sh.Ci) * LR * bt.W4;
@@ -390,37 +444,31 @@ size_t bwd_lds(const ConvShape &sh, const BwdTiling &bt)
 {
     const int P = kTR + 2 * sh.k + 1;
     const size_t main = sizeof(float) * (static_cast<size_t>(bt.dummy) + 3 * P + 1);
-    const size_t red = sizeof(float) * kWaves * cdiv(sh.Co, 16) * 16 * bwd_nt(sh) * 16;
+    const size_t red = sizeof(float) * kDwWaves * cdiv(sh.Co, 16) * 16 * bwd_nt(sh) * 16;
     return std::max(main, red);
 }
 
-// Persistent grid: every block gets the same number of tiles, with at most
-// kBwdBlocksPerCU blocks per compute unit (the occupancy of bwd_f32_k).
-constexpr int kBwdBlocksPerCU = 3;
-
-int bwd_grid(const BwdTiling &bt)
-{
-    const int maxb = std::max(1, kBwdBlocksPerCU * device_cus());
-    const int per = cdiv(bt.ntiles, maxb);
-    return cdiv(bt.ntiles, per);
-}
+// Persistent grid: one block per compute unit, each walking a strided list
+// of tiles.
+int bwd_grid(const BwdTiling &bt) { return std::max(1, std::min(bt.ntiles, device_cus())); }
 
 } // namespace
 
 bool smallc_f32_bwd_fused_ok(const ConvShape &sh)
 {
     if (sh.s != 1 || (sh.k != 1 && sh.k != 2) || sh.Ci > 2 || sh.Co > 32 || sh.W % 4 != 0 ||
-        sh.W > kThreads || sh.Ci * sh.T + 1 > 64)
+        sh.W > kDxThreads || sh.Ci * sh.T + 1 > 64)
         return false;
     const BwdTiling bt = bwd_tiling(sh);
     const int cg = bwd_cg(sh, bt);
-    return cg <= 4 && bwd_u(bt) <= 16 && bwd_lds(sh, bt) <= kLdsMax;
+    return cg <= 4 && bwd_u(bt) <= 8 && bwd_lds(sh, bt) <= kLdsMax;
 }
 
 size_t smallc_f32_bwd_fused_workspace(const ConvShape &sh)
 {
     const BwdTiling bt = bwd_tiling(sh);
-    return sizeof(float) * static_cast<size_t>(bwd_grid(bt)) * sh.Co * (sh.Ci * sh.T + 1);
+    return sizeof(float) * static_cast<size_t>(bwd_grid(bt)) * kPartChunk *
+           part_chunks(sh.Co * (sh.Ci * sh.T + 1));
 }
 
 hipError_t smallc_f32_bwd_fused(const float *x, const float *dy, const float *w, float *dx,
@@ -441,8 +489,9 @@ hipError_t smallc_f32_bwd_fused(const float *x, const float *dy, const float *w,
                        x, dy, w, dx, part, sh, bt, do_dx)
 #define HEX_B_U(KV, CIV, MTV, NTV, CGV)                                                       \
     do {                                                                                     \
-        if (U <= 8) HEX_B(KV, CIV, MTV, NTV, CGV, 8);                                        \
-        else HEX_B(KV, CIV, MTV, NTV, CGV, 16);                                              \
+        if (U <= 2) HEX_B(KV, CIV, MTV, NTV, CGV, 2);                                        \
+        else if (U <= 4) HEX_B(KV, CIV, MTV, NTV, CGV, 4);                                   \
+        else HEX_B(KV, CIV, MTV, NTV, CGV, 8);                                               \
     } while (0)
 #define HEX_B_CG(KV, CIV, MTV, NTV)                                                           \
     do {                                                                                     \
@@ -469,7 +518,7 @@ hipError_t smallc_f32_bwd_fused(const float *x, const float *dy, const float *w,
     hipError_t e = hipGetLastError();
     if (e != hipSuccess)
         return e;
-    return reduce_partials(part, nparts, sh.Co, sh.Ci * sh.T, dw, db, st);
+    return reduce_chunked(part, nparts, sh.Co, sh.Ci * sh.T, dw, db, st);
 }
 
 } // namespace hexk

@@ -153,32 +153,11 @@ __global__ __launch_bounds__(kThreads) void fwd_f32_k(
 {
     constexpr int T = num_taps(K);
     extern __shared__ float xs[];
+    float *wt = xs + sh.Ci * tg.CS; // [16][C_in * T + 1]: this block's weights, bias last
     const size_t HW = static_cast<size_t>(sh.H) * sh.W;
+    const int J = sh.Ci * T;
 
-    // per-lane weights and tap offsets, loaded once per block
-    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-    const int m = lane & 15, kq = lane >> 4;
-    const int co = blockIdx.y * 16 + m; // B and D column of this lane
-    int off[KS]; // LDS offset of k from the centre (may be negative)
-    bool kval[KS];
-    float bw[KS];
-#pragma unroll
-    for (int s = 0; s < KS; ++s) {
-        const int kk = kq + 4 * s;
-        off[s] = 0;
-        bw[s] = 0.f;
-        kval[s] = kk < sh.Ci * T;
-        if (kval[s]) {
-            const int ci = kk / T, t = kk - ci * T;
-            int dq = 0, ds = 0;
-            tap_axial(K, t, dq, ds);
-            off[s] = ci * tg.CS + dq * tg.P + ds;
-            if (co < sh.Co)
-                bw[s] = w[(static_cast<size_t>(co) * sh.Ci + ci) * T + t];
-        }
-    }
-    const float bco = (bias != nullptr && co < sh.Co) ? bias[co] : 0.f;
-
+    // the first tile's loads are in flight while the weights are staged
     ShearPrefetch<U> pf;
     int t = blockIdx.x;
     if (t < tg.ntiles) {
@@ -186,10 +165,51 @@ __global__ __launch_bounds__(kThreads) void fwd_f32_k(
         pf.load(x + static_cast<size_t>(o.n) * sh.Ci * HW, HW, sh.Ci, sh.H, sh.W,
                 window_of(o, tg, K), tg.TR + 2 * K, tg.fdlr);
     }
+
+    // The block's weights (16 output channels) and biases: one coalesced
+    // pass into LDS.  Every block reads the same few lines, so per-lane
+    // gathers from global memory would queue on them.
+    for (int e = threadIdx.x; e < 16 * (J + 1); e += blockDim.x) {
+        const int r = e / (J + 1), col = e - r * (J + 1);
+        const int cog = blockIdx.y * 16 + r;
+        float v = 0.f;
+        if (cog < sh.Co)
+            v = col < J ? w[static_cast<size_t>(cog) * J + col] : (bias != nullptr ? bias[cog] : 0.f);
+        wt[e] = v;
+    }
+
+    // per-lane tap offsets
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int m = lane & 15, kq = lane >> 4;
+    const int co = blockIdx.y * 16 + m; // B and D column of this lane
+    int off[KS]; // LDS offset of k from the centre (may be negative)
+    bool kval[KS];
+#pragma unroll
+    for (int s = 0; s < KS; ++s) {
+        const int kk = kq + 4 * s;
+        off[s] = 0;
+        kval[s] = kk < J;
+        if (kval[s]) {
+            const int ci = kk / T, tap = kk - ci * T;
+            int dq = 0, ds = 0;
+            tap_axial(K, tap, dq, ds);
+            off[s] = ci * tg.CS + dq * tg.P + ds;
+        }
+    }
+
+    float bw[KS], bco = 0.f;
+    bool have_w = false;
     for (; t < tg.ntiles; t += gridDim.x) {
         const TileOrigin o = tile_of(t, tg, sh);
         const ShearTile tl = window_of(o, tg, K);
-        __syncthreads(); // previous tile's reads of xs are done
+        __syncthreads(); // previous tile's reads of xs are done (and the weights staged)
+        if (!have_w) {
+#pragma unroll
+            for (int s = 0; s < KS; ++s)
+                bw[s] = kval[s] ? wt[m * (J + 1) + kq + 4 * s] : 0.f;
+            bco = wt[m * (J + 1) + J];
+            have_w = true;
+        }
         pf.commit(xs);
         __syncthreads();
         const int tn = t + gridDim.x;
@@ -465,6 +485,12 @@ size_t shear_bytes(const ConvShape &sh, const Tiling &tg, int nch)
     return sizeof(float) * static_cast<size_t>(nch) * (tg.TW + 2 * sh.k) * tg.P;
 }
 
+// staged input window plus the block's weights and biases
+size_t fwd_lds(const ConvShape &sh, const Tiling &tg)
+{
+    return shear_bytes(sh, tg, sh.Ci) + sizeof(float) * 16 * (sh.Ci * sh.T + 1);
+}
+
 int wgrad_nt(const ConvShape &sh)
 {
     const int NT = cdiv(sh.Ci * sh.T + 1, 16);
@@ -542,7 +568,7 @@ bool smallc_f32_fwd_ok(const ConvShape &sh)
     if (sh.s != 1 || (sh.k != 1 && sh.k != 2) || sh.Ci * sh.T > 64 || sh.W % 4 != 0)
         return false;
     const Tiling tg = make_tiling(sh, kFwdTarget);
-    return shear_bytes(sh, tg, sh.Ci) <= kLdsLimit && shear_depth(sh, tg, sh.Ci) > 0;
+    return fwd_lds(sh, tg) <= kLdsLimit && shear_depth(sh, tg, sh.Ci) > 0;
 }
 
 hipError_t smallc_f32_fwd(const float *x, const float *w, const float *b, float *y,
@@ -552,7 +578,7 @@ hipError_t smallc_f32_fwd(const float *x, const float *w, const float *b, float 
     const int KS = cdiv(sh.Ci * sh.T, 4);
     const int U = shear_depth(sh, tg, sh.Ci);
     dim3 grid(std::min(tg.ntiles, kFwdBlocks), cdiv(sh.Co, 16));
-    const size_t lds = shear_bytes(sh, tg, sh.Ci);
+    const size_t lds = fwd_lds(sh, tg);
 #define HEX_FWD_F32(KV, KSV, UV)                                                             \
     hipLaunchKernelGGL((fwd_f32_k<KV, KSV, UV>), grid, dim3(kThreads), lds, st, x, w, b, y,  \
                        sh, relu ? 1 : 0, tg, 1)
