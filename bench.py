@@ -124,6 +124,36 @@ class GraphTimer:
         return ms                                 # ms per call
 
 
+def dominant_kernel(torch, fn, reps):
+    """The kernel with the largest GPU time over `reps` eager calls of fn,
+    timed by the library (a HIP event pair around every launch, on the
+    stream it is launched on).  Returns (name, ms per launch, launches per
+    call, {name: ms per launch})."""
+    torch.cuda.synchronize()
+    hx.hexconv_timing_begin()
+    for i in range(reps):
+        fn(i)
+    t = hx.hexconv_timing_end()
+    if not t:
+        raise RuntimeError("bench.py: no kernel launch was recorded")
+    name = max(t, key=lambda n: t[n][1])
+    cnt, tot = t[name]
+    return name, tot / cnt, cnt / reps, {n: round(ms / c, 5) for n, (c, ms) in t.items()}
+
+
+# backward kernels computing both gradients in one pass; every other
+# backward kernel computes one of them
+BOTH_GRADIENT_KERNELS = ("bwd_f32_k",)
+
+
+def products_of(kernel, op):
+    """Convolution products (of the three per layer) one launch of `kernel`
+    performs when it runs for `op`."""
+    if op.endswith("fwd"):
+        return 1
+    return 2 if kernel in BOTH_GRADIENT_KERNELS else 1
+
+
 def conv_flop(N, Ci, Co, Ho, Wo, T):
     return 2.0 * N * Ho * Wo * Ci * Co * T
 
@@ -227,20 +257,26 @@ def bench_conv(args, torch, cfg_key):
     flop_step = 3 * flop_op
     value = flop_step / (ms_step * 1e-3) / 1e9
 
+    # the dominant op of the step, and within it the kernel with the most
+    # GPU time, against its roofline: the op's algorithmic bytes (or
+    # products) per launch of that kernel over its measured duration
     dom = max(("fwd", "bwd"), key=lambda n: ops[n]["ms"])
+    fn_dom = fwd if dom == "fwd" else bwd
+    kname, kms, kper, kall = dominant_kernel(torch, fn_dom, args.steps)
     bound = "hbm" if cfg["dtype"] == gen.F32 or Ci * T < 64 else "mfma"
-    kernel_name = KERNEL_NAMES.get((cfg_key, dom), dom)
     if bound == "hbm":
-        achieved = bytes_alg[dom] / (ops[dom]["ms"] * 1e-3) / 1e9
+        units = bytes_alg[dom] / kper
+        achieved = units / (kms * 1e-3) / 1e9
         roof = dict(bound="hbm", achieved=round(achieved, 1), peak=HBM_PEAK_GBS, unit="GB/s",
                     frac=round(achieved / HBM_PEAK_GBS, 4))
     else:
-        achieved = nprod[dom] * flop_op / (ops[dom]["ms"] * 1e-3) / 1e12
+        units = products_of(kname, dom) * flop_op / kper
+        achieved = units / (kms * 1e-3) / 1e12
         roof = dict(bound="mfma", achieved=round(achieved, 2), peak=BF16_MFMA_PEAK_TFLOPS,
                     unit="TFLOP/s", frac=round(achieved / BF16_MFMA_PEAK_TFLOPS, 4))
-    roof["kernel"] = kernel_name
-    roof["op"] = dom
-    roof["traffic"] = read_counters(cfg["name"], kernel_name)
+    roof["traffic"] = read_counters(cfg["name"], kname)
+    roof.update(kernel=kname, kernel_ms=round(kms, 5), launches_per_op=kper, op=dom,
+                alg_per_launch=units, op_kernels_ms=kall)
 
     out = dict(
         metric="hex-conv effective GFLOP/s (fwd+bwd)", value=round(value, 2), unit="GFLOP/s",
@@ -323,11 +359,14 @@ def bench_pool(args, torch, cfg_key):
         ops[name] = dict(ms=ms, gbs=(in_b + out_b) / (ms * 1e-3) / 1e9)
     value = 2 * (in_b + out_b) / (ms_step * 1e-3) / 1e9
     dom = max(ops, key=lambda n: ops[n]["ms"])
-    achieved = ops[dom]["gbs"]
+    kname, kms, kper, kall = dominant_kernel(torch, pmax if dom == "max" else pavg, args.steps)
+    units = (in_b + out_b) / kper
+    achieved = units / (kms * 1e-3) / 1e9
     roof = dict(bound="hbm", achieved=round(achieved, 1), peak=HBM_PEAK_GBS, unit="GB/s",
-                frac=round(achieved / HBM_PEAK_GBS, 4),
-                kernel=KERNEL_NAMES.get((cfg_key, dom), dom), op=dom)
-    roof["traffic"] = read_counters(cfg["name"], roof["kernel"])
+                frac=round(achieved / HBM_PEAK_GBS, 4))
+    roof["traffic"] = read_counters(cfg["name"], kname)
+    roof.update(kernel=kname, kernel_ms=round(kms, 5), launches_per_op=kper, op=dom,
+                alg_per_launch=units, op_kernels_ms=kall)
     out = dict(
         metric="hex-pool HBM GB/s (max + avg, fwd)", value=round(value, 1), unit="GB/s",
         n_gpus=1, steps=args.steps, warmup=args.warmup, ms_per_step=round(ms_step, 5),
@@ -476,6 +515,7 @@ def bench_stack(args, torch, cfg_key):
     ms_step = timer.time(step, args.steps)
     # per-layer durations (each call alone, same inputs every time)
     per_layer = []
+    op_fns = {}
     for li, (kind, ci, co, k, s, relu, H, W, Ho, Wo) in enumerate(shapes):
         a_in = xs[0] if li == 0 else acts[li - 1]
         if kind == "conv":
@@ -489,6 +529,7 @@ def bench_stack(args, torch, cfg_key):
             relu_y = a_in if shapes[li - 1][0] == "conv" and shapes[li - 1][5] else None
             b = lambda i, li=li, k=k, s=s, relu_y=relu_y: hx.hexpool_bwd(
                 acts[li], ams[li], relu_y, grads[li], k, s, hx.HEX_POOL_MAX)
+        op_fns[(li, "fwd")], op_fns[(li, "bwd")] = f, b
         per_layer.append(dict(layer=li, kind=kind, C_in=ci, C_out=co, k=k, stride=s,
                               fwd_ms=round(timer.time(f, args.steps), 5),
                               bwd_ms=round(timer.time(b, args.steps), 5)))
@@ -508,9 +549,11 @@ def bench_stack(args, torch, cfg_key):
                [(pl["bwd_ms"], li, "bwd") for li, pl in enumerate(per_layer)])
     ms, li, op = best
     kind, ci, co, k, s, relu, H, W, Ho, Wo = shapes[li]
+    kname, kms, kper, kall = dominant_kernel(torch, op_fns[(li, op)], args.steps)
     if kind == "conv" and ci >= 32:
-        fl = conv_flop(N, ci, co, Ho, Wo, hx.hex_num_taps(k)) * (1 if op == "fwd" else 2)
-        ach = fl / (ms * 1e-3) / 1e12
+        # products of the op: forward 1, backward 2 (data and weight gradients)
+        units = conv_flop(N, ci, co, Ho, Wo, hx.hex_num_taps(k)) * products_of(kname, op) / kper
+        ach = units / (kms * 1e-3) / 1e12
         roof = dict(bound="mfma", achieved=round(ach, 2), peak=BF16_MFMA_PEAK_TFLOPS,
                     unit="TFLOP/s", frac=round(ach / BF16_MFMA_PEAK_TFLOPS, 4))
     else:
@@ -518,12 +561,13 @@ def bench_stack(args, torch, cfg_key):
             nb = 2 * (N * ci * H * W + N * co * Ho * Wo) * (1 if op == "fwd" else 2)
         else:
             nb = 2 * (N * ci * H * W + N * co * Ho * Wo) + N * co * Ho * Wo
-        ach = nb / (ms * 1e-3) / 1e9
+        units = nb / kper
+        ach = units / (kms * 1e-3) / 1e9
         roof = dict(bound="hbm", achieved=round(ach, 1), peak=HBM_PEAK_GBS, unit="GB/s",
                     frac=round(ach / HBM_PEAK_GBS, 4))
-    roof["op"] = "layer%d_%s" % (li, op)
-    roof["kernel"] = KERNEL_NAMES.get((cfg_key, roof["op"]), roof["op"])
-    roof["traffic"] = None
+    roof["traffic"] = read_counters(cfg["name"], kname)
+    roof.update(kernel=kname, kernel_ms=round(kms, 5), launches_per_op=kper,
+                op="layer%d_%s" % (li, op), alg_per_launch=units, op_kernels_ms=kall)
     out["roofline"] = roof
     if not args.no_cpu_baseline:
         sps, thr, reps, el = cpu_baseline_stack(cfg, dsets[0], args.cpu_seconds)
@@ -532,10 +576,6 @@ def bench_stack(args, torch, cfg_key):
             sample="2 of %d images through the whole stack, fwd+bwd, fp64, repeated %d "
                    "times in %.1f s" % (N, reps, el))
     return out
-
-
-# kernel that dominates each op (as it appears in rocprofv3 traces)
-KERNEL_NAMES = {}
 
 
 def main():
@@ -548,6 +588,9 @@ def main():
     p.add_argument("--eager", action="store_true",
                    help="launch eagerly instead of replaying a HIP graph (for counter runs)")
     p.add_argument("--cpu-seconds", type=float, default=12.0)
+    p.add_argument("--calib-copy-mib", type=int, default=0,
+                   help="after the benchmark, one device-to-device copy of this many MiB "
+                        "(counter calibration for paper_1903_01814_amd.counters)")
     args = p.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py: this library runs on a single GPU; --gpus %d is not supported "
@@ -565,6 +608,13 @@ def main():
     else:
         out = bench_conv(args, torch, args.config)
     print(json.dumps(out), flush=True)
+    if args.calib_copy_mib > 0:
+        n = args.calib_copy_mib << 18                    # float32 elements
+        src = torch.ones(n, dtype=torch.float32, device="cuda:0")
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        dst.copy_(src)
+        torch.cuda.synchronize()
 
 
 if __name__ == "__main__":

@@ -178,6 +178,29 @@ int hexpool_bwd(const void *dy, const uint8_t *argmax_tap, const void *relu_y,
 /* Static description of a hex_status value. */
 const char *hex_status_string(int status);
 
+/*
+ * Kernel timing, for profiling (not part of the paper's operations).
+ * Between hexconv_timing_begin() and hexconv_timing_end(), every kernel the
+ * library launches is bracketed by a pair of HIP events recorded on the
+ * stream it is launched on.  hexconv_timing_end() stops recording, waits
+ * for the recorded events and reports, per kernel (by the kernel's function
+ * name, template arguments dropped, in order of first launch), the number
+ * of launches and their summed GPU time in milliseconds.
+ *   names:    caller-owned, max_kernels * HEX_TIMING_NAME_LEN chars; entry i
+ *             at names + i * HEX_TIMING_NAME_LEN, NUL-terminated
+ *   counts, total_ms: caller-owned arrays of max_kernels
+ *   n_kernels: receives the number of entries filled (at most max_kernels;
+ *             further kernels are dropped)
+ * Recording allocates events on the host side of every launch: do not
+ * enable it while a HIP graph is being captured, nor from several threads
+ * at once.  Returns HEX_ERR_INVALID_ARG for NULL outputs or max_kernels < 1,
+ * HEX_ERR_LAUNCH if an event could not be waited for.
+ */
+#define HEX_TIMING_NAME_LEN 64
+int hexconv_timing_begin(void);
+int hexconv_timing_end(int max_kernels, char *names, int *counts, double *total_ms,
+                       int *n_kernels);
+
 #ifdef __cplusplus
 }
 #endif

@@ -2,7 +2,10 @@
 // argument validation (host only, before anything is enqueued), choice of
 // kernel per shape regime, and launch-status mapping.
 #include <atomic>
+#include <mutex>
 #include <stdint.h>
+#include <string>
+#include <vector>
 #include <stdlib.h>
 #include <string.h>
 
@@ -31,6 +34,57 @@ int device_cus()
     if (dev < kMaxDev)
         cache[dev].store(cus, std::memory_order_relaxed);
     return cus;
+}
+
+// ---- per-launch timing --------------------------------------------------
+
+namespace {
+
+std::atomic<bool> g_timing{false};
+std::mutex g_timing_mu;
+
+struct TimedLaunch {
+    std::string name;
+    hipEvent_t a, b;
+};
+std::vector<TimedLaunch> g_timed;
+
+// "(name<args>)" or "name<args>" -> "name"
+std::string kernel_base_name(const char *s)
+{
+    std::string n;
+    for (; *s == '(' || *s == ' '; ++s) {
+    }
+    for (; *s != '\0' && *s != '<' && *s != '(' && *s != ')' && *s != ' ' && *s != ','; ++s)
+        n.push_back(*s);
+    return n;
+}
+
+} // namespace
+
+KTimer::KTimer(const char *kernel, hipStream_t st) : name_(kernel), st_(st), a_(nullptr), b_(nullptr)
+{
+    if (!g_timing.load(std::memory_order_relaxed))
+        return;
+    if (hipEventCreate(&a_) != hipSuccess) {
+        a_ = nullptr;
+        return;
+    }
+    if (hipEventCreate(&b_) != hipSuccess) {
+        (void)hipEventDestroy(a_);
+        a_ = nullptr;
+        return;
+    }
+    (void)hipEventRecord(a_, st_);
+}
+
+KTimer::~KTimer()
+{
+    if (a_ == nullptr)
+        return;
+    (void)hipEventRecord(b_, st_);
+    std::lock_guard<std::mutex> lock(g_timing_mu);
+    g_timed.push_back(TimedLaunch{kernel_base_name(name_), a_, b_});
 }
 
 } // namespace hexk
@@ -365,6 +419,56 @@ int hexpool_bwd(const void *dy, const uint8_t *argmax_tap, const void *relu_y, v
     if (!force_generic() && sh.Ho > 0 && hexk::pool_fast_ok(sh, d))
         return launched(hexk::pool_bwd_fast(dy, argmax_tap, relu_y, dx, sh, mode, d, st));
     return launched(hexk::pool_bwd_generic(dy, argmax_tap, relu_y, dx, sh, mode, d, st));
+}
+
+int hexconv_timing_begin(void)
+{
+    std::lock_guard<std::mutex> lock(hexk::g_timing_mu);
+    for (auto &t : hexk::g_timed) {
+        (void)hipEventDestroy(t.a);
+        (void)hipEventDestroy(t.b);
+    }
+    hexk::g_timed.clear();
+    hexk::g_timing.store(true);
+    return HEX_OK;
+}
+
+int hexconv_timing_end(int max_kernels, char *names, int *counts, double *total_ms,
+                       int *n_kernels)
+{
+    hexk::g_timing.store(false);
+    if (max_kernels < 1 || names == nullptr || counts == nullptr || total_ms == nullptr ||
+        n_kernels == nullptr)
+        return HEX_ERR_INVALID_ARG;
+    std::lock_guard<std::mutex> lock(hexk::g_timing_mu);
+    std::vector<std::string> order;
+    int rc = HEX_OK;
+    *n_kernels = 0;
+    for (auto &t : hexk::g_timed) {
+        float ms = 0.f;
+        if (hipEventSynchronize(t.b) != hipSuccess || hipEventElapsedTime(&ms, t.a, t.b) != hipSuccess)
+            rc = HEX_ERR_LAUNCH;
+        (void)hipEventDestroy(t.a);
+        (void)hipEventDestroy(t.b);
+        int i = 0;
+        while (i < static_cast<int>(order.size()) && order[i] != t.name)
+            ++i;
+        if (i == static_cast<int>(order.size())) {
+            if (i >= max_kernels)
+                continue;
+            order.push_back(t.name);
+            char *dst = names + static_cast<size_t>(i) * HEX_TIMING_NAME_LEN;
+            strncpy(dst, t.name.c_str(), HEX_TIMING_NAME_LEN - 1);
+            dst[HEX_TIMING_NAME_LEN - 1] = '\0';
+            counts[i] = 0;
+            total_ms[i] = 0.0;
+        }
+        counts[i] += 1;
+        total_ms[i] += ms;
+    }
+    hexk::g_timed.clear();
+    *n_kernels = static_cast<int>(order.size());
+    return rc;
 }
 
 const char *hex_status_string(int status)

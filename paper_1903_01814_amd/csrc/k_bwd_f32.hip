@@ -62,6 +62,7 @@ struct BwdTiling {
     int xo, zo, oo;    // LDS offsets: x planes, zeros plane, ones plane
     int G;             // output-channel groups of the data gradient
     int tiles_per_img, ntiles;
+    int per;           // tiles per block: block b walks tiles [b * per, b * per + per)
     int nitems;        // float4 staging items per tile
     int dxp;           // LDS offset of the data-gradient partials
     int wl;            // LDS offset of the reflected weights
@@ -180,17 +181,22 @@ __global__ __launch_bounds__(kThreads) void bwd_f32_k(
     StageMap<K, U> map;
     map.init(sh, bt);
     StageBuf<U> sa, sb;
-    const int tpi = bt.tiles_per_img, gs = gridDim.x;
-    // Every step issues the same loads (a tile past the end reloads the last
-    // one and is never committed), so the wait before a commit only covers
-    // the loads of that buffer and not the newer ones in flight.
+    const int tpi = bt.tiles_per_img;
+    // a contiguous run of tiles (consecutive row bands of one image): the
+    // halo rows a tile shares with the previous one were fetched by this
+    // block, so they come from this XCD's L2 rather than from HBM
+    const int t_begin = blockIdx.x * bt.per;
+    const int t_end = min(t_begin + bt.per, bt.ntiles);
+    // Every step issues the same loads (a tile past this block's run reloads
+    // its last one, from L2, and is never committed), so the wait before a
+    // commit only covers the loads of that buffer and not the newer ones.
     auto load_tile = [&](StageBuf<U> &b, int t) {
-        t = min(t, bt.ntiles - 1);
+        t = min(t, t_end - 1);
         const int n = t / tpi;
         b.load(map, x, dy, sh, n, (t - n * tpi) * kTR);
     };
-    load_tile(sa, blockIdx.x);
-    load_tile(sb, blockIdx.x + gs);
+    load_tile(sa, t_begin);
+    load_tile(sb, t_begin + 1);
 
     // ---- data gradient role: thread = (channel group g, column c), all TR
     // rows of the column, CG output channels
@@ -281,7 +287,7 @@ __global__ __launch_bounds__(kThreads) void bwd_f32_k(
         const int rows = min(kTR, sh.H - r0);
         buf.commit(map, lds);
         __syncthreads(); // tile staged (and, the first time, the constants)
-        load_tile(buf, tile + 2 * gs);
+        load_tile(buf, tile + 2);
         if (dxrole) {
             if (dxthr) {
                 float gacc[CI][kTR];
@@ -367,13 +373,12 @@ __global__ __launch_bounds__(kThreads) void bwd_f32_k(
     };
 
     // two register buffers, so the loop is unrolled by two
-    for (int tile = blockIdx.x; tile < bt.ntiles;) {
+    for (int tile = t_begin; tile < t_end;) {
         tile_step(sa, tile);
-        tile += gs;
-        if (tile >= bt.ntiles)
+        if (++tile >= t_end)
             break;
         tile_step(sb, tile);
-        tile += gs;
+        ++tile;
     }
 
     // sum the accumulator sets and the weight-gradient waves in a fixed
@@ -427,6 +432,7 @@ BwdTiling bwd_tiling(const ConvShape &sh)
     bt.G = std::max(1, std::min(sh.Co, kDxThreads / sh.W));
     bt.tiles_per_img = cdiv(sh.H, kTR);
     bt.ntiles = bt.tiles_per_img * sh.N;
+    bt.per = cdiv(bt.ntiles, std::max(1, device_cus()));
     bt.nitems = (sh.Co + sh.Ci) * LR * bt.W4;
     bt.dxp = bt.oo + bt.CS;
     bt.wl = bt.dxp + bt.G * sh.Ci * kTR * sh.W;
@@ -448,9 +454,9 @@ size_t bwd_lds(const ConvShape &sh, const BwdTiling &bt)
     return std::max(main, red);
 }
 
-// Persistent grid: one block per compute unit, each walking a strided list
-// of tiles.
-int bwd_grid(const BwdTiling &bt) { return std::max(1, std::min(bt.ntiles, device_cus())); }
+// Persistent grid: at most one block per compute unit, each walking a
+// contiguous run of tiles (bt.per of them).
+int bwd_grid(const BwdTiling &bt) { return cdiv(bt.ntiles, bt.per); }
 
 } // namespace
 
@@ -485,7 +491,7 @@ hipError_t smallc_f32_bwd_fused(const float *x, const float *dy, const float *w,
     const int do_dx = dx != nullptr ? 1 : 0;
     dim3 grid(nparts);
 #define HEX_B(KV, CIV, MTV, NTV, CGV, UV)                                                     \
-    hipLaunchKernelGGL((bwd_f32_k<KV, CIV, MTV, NTV, CGV, UV>), grid, dim3(kThreads), lds, st, \
+    HEX_LAUNCH((bwd_f32_k<KV, CIV, MTV, NTV, CGV, UV>), grid, dim3(kThreads), lds, st, \
                        x, dy, w, dx, part, sh, bt, do_dx)
 #define HEX_B_U(KV, CIV, MTV, NTV, CGV)                                                       \
     do {                                                                                     \

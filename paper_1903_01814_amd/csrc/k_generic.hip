@@ -340,11 +340,11 @@ hipError_t conv_fwd_generic(const void *x, const void *w, const void *b, void *y
                        region_cols(TJ, sh.k, sh.s);
     dim3 grid(tiles_i * tiles_j, sh.N, cdiv(sh.Co, kCoBlock));
     if (dt == F32)
-        hipLaunchKernelGGL(conv_fwd_generic_k<float>, grid, dim3(kThreads), lds, st,
+        HEX_LAUNCH(conv_fwd_generic_k<float>, grid, dim3(kThreads), lds, st,
                            (const float *)x, (const float *)w, (const float *)b, (float *)y, sh,
                            relu ? 1 : 0, TI, TJ, tiles_j);
     else
-        hipLaunchKernelGGL(conv_fwd_generic_k<bf16raw>, grid, dim3(kThreads), lds, st,
+        HEX_LAUNCH(conv_fwd_generic_k<bf16raw>, grid, dim3(kThreads), lds, st,
                            (const bf16raw *)x, (const bf16raw *)w, (const bf16raw *)b,
                            (bf16raw *)y, sh, relu ? 1 : 0, TI, TJ, tiles_j);
     return hipGetLastError();
@@ -355,10 +355,10 @@ hipError_t conv_bwd_data_generic(const void *dy, const void *w, void *dx, const 
 {
     dim3 grid(cdiv(static_cast<long>(sh.H) * sh.W, kThreads), sh.N, cdiv(sh.Ci, kCiBlock));
     if (dt == F32)
-        hipLaunchKernelGGL(conv_bwd_data_generic_k<float>, grid, dim3(kThreads), 0, st,
+        HEX_LAUNCH(conv_bwd_data_generic_k<float>, grid, dim3(kThreads), 0, st,
                            (const float *)dy, (const float *)w, (float *)dx, sh);
     else
-        hipLaunchKernelGGL(conv_bwd_data_generic_k<bf16raw>, grid, dim3(kThreads), 0, st,
+        HEX_LAUNCH(conv_bwd_data_generic_k<bf16raw>, grid, dim3(kThreads), 0, st,
                            (const bf16raw *)dy, (const bf16raw *)w, (bf16raw *)dx, sh);
     return hipGetLastError();
 }
@@ -379,10 +379,10 @@ hipError_t wgrad_generic(const void *x, const void *dy, float *dw, float *db, vo
     float *part = static_cast<float *>(ws);
     dim3 grid(nchunks, sh.Co, sh.Ci);
     if (dt == F32)
-        hipLaunchKernelGGL(wgrad_partial_generic_k<float>, grid, dim3(kThreads), 0, st,
+        HEX_LAUNCH(wgrad_partial_generic_k<float>, grid, dim3(kThreads), 0, st,
                            (const float *)x, (const float *)dy, part, sh, chunk);
     else
-        hipLaunchKernelGGL(wgrad_partial_generic_k<bf16raw>, grid, dim3(kThreads), 0, st,
+        HEX_LAUNCH(wgrad_partial_generic_k<bf16raw>, grid, dim3(kThreads), 0, st,
                            (const bf16raw *)x, (const bf16raw *)dy, part, sh, chunk);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess)
@@ -393,7 +393,7 @@ hipError_t wgrad_generic(const void *x, const void *dy, float *dw, float *db, vo
 hipError_t fill_zero_f32(float *dw, float *db, const ConvShape &sh, hipStream_t st)
 {
     const long EW = static_cast<long>(sh.Co) * sh.Ci * sh.T;
-    hipLaunchKernelGGL(fill_zero_k, dim3(cdiv(EW + sh.Co, kThreads)), dim3(kThreads), 0, st, dw,
+    HEX_LAUNCH(fill_zero_k, dim3(cdiv(EW + sh.Co, kThreads)), dim3(kThreads), 0, st, dw,
                        static_cast<int>(EW), db, sh.Co);
     return hipGetLastError();
 }
@@ -404,7 +404,7 @@ hipError_t pool_fwd_generic(const void *x, void *y, uint8_t *am, const ConvShape
     const long total = static_cast<long>(sh.N) * sh.Ci * sh.Ho * sh.Wo;
     const int blocks = std::max(1, std::min(cdiv(total, kThreads), 65535 * 16));
 #define HEX_POOL_FWD(T, M)                                                                   \
-    hipLaunchKernelGGL((pool_fwd_generic_k<T, M>), dim3(blocks), dim3(kThreads), 0, st,     \
+    HEX_LAUNCH((pool_fwd_generic_k<T, M>), dim3(blocks), dim3(kThreads), 0, st,     \
                        (const T *)x, (T *)y, am, sh, total)
     if (dt == F32) {
         if (mode == 0) HEX_POOL_FWD(float, 0); else HEX_POOL_FWD(float, 1);
@@ -421,7 +421,7 @@ hipError_t pool_bwd_generic(const void *dy, const uint8_t *am, const void *relu_
     const long total = static_cast<long>(sh.N) * sh.Ci * sh.H * sh.W;
     const int blocks = std::max(1, std::min(cdiv(total, kThreads), 65535 * 16));
 #define HEX_POOL_BWD(T, M)                                                                   \
-    hipLaunchKernelGGL((pool_bwd_generic_k<T, M>), dim3(blocks), dim3(kThreads), 0, st,     \
+    HEX_LAUNCH((pool_bwd_generic_k<T, M>), dim3(blocks), dim3(kThreads), 0, st,     \
                        (const T *)dy, am, (const T *)relu_y, (T *)dx, sh, total)
     if (dt == F32) {
         if (mode == 0) HEX_POOL_BWD(float, 0); else HEX_POOL_BWD(float, 1);

@@ -871,7 +871,7 @@ template <int K, int KS, int NT, int PW, int MT, bool R>
 hipError_t launch_wide(const WidePlan &pl, const bf16raw *x, const bf16raw *w, const bf16raw *b,
                        bf16raw *y, bool relu, hipStream_t st)
 {
-    hipLaunchKernelGGL((conv_bf16_wide_k<K, KS, NT, PW, MT, R>), dim3(pl.grid), dim3(kThreads),
+    HEX_LAUNCH((conv_bf16_wide_k<K, KS, NT, PW, MT, R>), dim3(pl.grid), dim3(kThreads),
                        pl.lds, st, x, w, b, y, pl.a, relu ? 1 : 0);
     return hipGetLastError();
 }
@@ -880,7 +880,7 @@ template <int K, int KS, bool WL, int OG, int PW, int MT, bool R>
 hipError_t launch_wide32(const WidePlan &pl, const bf16raw *x, const bf16raw *w,
                          const bf16raw *b, bf16raw *y, bool relu, hipStream_t st)
 {
-    hipLaunchKernelGGL((conv_bf16_wide32_k<K, KS, WL, OG, PW, MT, R>), dim3(pl.grid),
+    HEX_LAUNCH((conv_bf16_wide32_k<K, KS, WL, OG, PW, MT, R>), dim3(pl.grid),
                        dim3(kThreads32), pl.lds, st, x, w, b, y, pl.a, relu ? 1 : 0);
     return hipGetLastError();
 }

@@ -320,11 +320,11 @@ hipError_t pool_fwd_fast(const void *x, void *y, uint8_t *am, const ConvShape &s
 #define HEX_PF(TT, M, KV, SV)                                                                \
     do {                                                                                     \
         if (am != nullptr)                                                                   \
-            hipLaunchKernelGGL((pool_fwd_k<TT, M, KV, SV, true>), dim3(grid),                \
+            HEX_LAUNCH((pool_fwd_k<TT, M, KV, SV, true>), dim3(grid),                \
                                dim3(kPoolThreads), lds, st, static_cast<const TT *>(x),      \
                                static_cast<TT *>(y), am, a);                                 \
         else                                                                                 \
-            hipLaunchKernelGGL((pool_fwd_k<TT, M, KV, SV, false>), dim3(grid),               \
+            HEX_LAUNCH((pool_fwd_k<TT, M, KV, SV, false>), dim3(grid),               \
                                dim3(kPoolThreads), lds, st, static_cast<const TT *>(x),      \
                                static_cast<TT *>(y), am, a);                                 \
     } while (0)
@@ -364,7 +364,7 @@ hipError_t pool_bwd_fast(const void *dy, const uint8_t *am, const void *relu_y, 
     const int grid = cdiv(a.nplanes, a.NP);
     const size_t lds = plane * a.NP;
 #define HEX_PB(TT, M, KV, SV, OV)                                                            \
-    hipLaunchKernelGGL((pool_bwd_k<TT, M, KV, SV, OV>), dim3(grid), dim3(kPoolThreads), lds, \
+    HEX_LAUNCH((pool_bwd_k<TT, M, KV, SV, OV>), dim3(grid), dim3(kPoolThreads), lds, \
                        st, static_cast<const TT *>(dy), am, static_cast<const TT *>(relu_y),  \
                        static_cast<TT *>(dx), a)
 #define HEX_PB_O(TT, M, KV, SV)                                                              \

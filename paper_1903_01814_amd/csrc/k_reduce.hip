@@ -90,7 +90,7 @@ hipError_t reduce_chunked(const float *part, int nparts, int Co, int J, float *d
                           hipStream_t st)
 {
     const int E = Co * (J + 1);
-    hipLaunchKernelGGL(reduce_chunked_k, dim3((E + kPartChunk - 1) / kPartChunk),
+    HEX_LAUNCH(reduce_chunked_k, dim3((E + kPartChunk - 1) / kPartChunk),
                        dim3(kPartChunk * kRedSlices), 0, st, part, nparts, E, J, dw, db);
     return hipGetLastError();
 }
@@ -99,7 +99,7 @@ hipError_t reduce_partials(const float *part, int nparts, int Co, int J, float *
                            hipStream_t st)
 {
     const int E = Co * (J + 1);
-    hipLaunchKernelGGL(reduce_partials_k, dim3(E), dim3(64), 0, st, part, nparts, J, dw, db);
+    HEX_LAUNCH(reduce_partials_k, dim3(E), dim3(64), 0, st, part, nparts, J, dw, db);
     return hipGetLastError();
 }
 

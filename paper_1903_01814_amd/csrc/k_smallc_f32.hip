@@ -580,7 +580,7 @@ hipError_t smallc_f32_fwd(const float *x, const float *w, const float *b, float 
     dim3 grid(std::min(tg.ntiles, kFwdBlocks), cdiv(sh.Co, 16));
     const size_t lds = fwd_lds(sh, tg);
 #define HEX_FWD_F32(KV, KSV, UV)                                                             \
-    hipLaunchKernelGGL((fwd_f32_k<KV, KSV, UV>), grid, dim3(kThreads), lds, st, x, w, b, y,  \
+    HEX_LAUNCH((fwd_f32_k<KV, KSV, UV>), grid, dim3(kThreads), lds, st, x, w, b, y,  \
                        sh, relu ? 1 : 0, tg, 1)
 #define HEX_FWD_F32_U(KV, KSV)                                                               \
     do {                                                                                     \
@@ -619,10 +619,10 @@ hipError_t smallc_f32_bwd_data(const float *dy, const float *w, float *dx, const
     const int vec4 = (sh.W % 4 == 0) ? 1 : 0;
     dim3 grid(tg.ntiles, sh.Ci);
     if (sh.k == 1)
-        hipLaunchKernelGGL((bwd_data_f32_k<1, kBwdR>), grid, dim3(kThreads), lds, st, dy, w, dx,
+        HEX_LAUNCH((bwd_data_f32_k<1, kBwdR>), grid, dim3(kThreads), lds, st, dy, w, dx,
                            sh, tg, ic_chunk, vec4);
     else
-        hipLaunchKernelGGL((bwd_data_f32_k<2, kBwdR>), grid, dim3(kThreads), lds, st, dy, w, dx,
+        HEX_LAUNCH((bwd_data_f32_k<2, kBwdR>), grid, dim3(kThreads), lds, st, dy, w, dx,
                            sh, tg, ic_chunk, vec4);
     return hipGetLastError();
 }
@@ -659,7 +659,7 @@ hipError_t smallc_f32_wgrad(const float *x, const float *dy, float *dw, float *d
     dim3 grid(nparts, cdiv(sh.Co, 16));
     const size_t lds = wgrad_lds(sh, tg);
 #define HEX_WG(KV, NTV, UXV, UDV)                                                            \
-    hipLaunchKernelGGL((wgrad_f32_k<KV, NTV, UXV, UDV>), grid, dim3(kThreads), lds, st, x, dy, \
+    HEX_LAUNCH((wgrad_f32_k<KV, NTV, UXV, UDV>), grid, dim3(kThreads), lds, st, x, dy, \
                        part, sh, tg, dstride)
 #define HEX_WG_UD(KV, NTV, UXV)                                                              \
     do {                                                                                     \

@@ -506,7 +506,7 @@ void launch_w32_u(const Wg32Args &a, size_t lds, hipStream_t st, const bf16raw *
                   const bf16raw *dy, float *part)
 {
     if constexpr (U <= max_items(K, G, CW))
-        hipLaunchKernelGGL((wgrad32_k<K, G, CW, U>), dim3(a.nparts), dim3(kT), lds, st, x, dy,
+        HEX_LAUNCH((wgrad32_k<K, G, CW, U>), dim3(a.nparts), dim3(kT), lds, st, x, dy,
                            part, a);
 }
 
@@ -579,7 +579,7 @@ hipError_t bf16_wgrad32(const void *x, const void *dy, float *dw, float *db, voi
         if (err != hipSuccess)
             return false;
         const int npos = sh.T * C * 16 * kRegChunk + a.CO;
-        hipLaunchKernelGGL(wgrad32_reduce_k, dim3(cdiv(npos, 64)), dim3(256), 0, st, part,
+        HEX_LAUNCH(wgrad32_reduce_k, dim3(cdiv(npos, 64)), dim3(256), 0, st, part,
                            a.nparts, npos, sh.Ci, a.CO, a.co0, sh.T, dw, db);
         err = hipGetLastError();
         return err == hipSuccess;

@@ -316,7 +316,7 @@ hipError_t bf16_wgrad(const void *x, const void *dy, float *dw, float *db, void 
     const bf16raw *dp = static_cast<const bf16raw *>(dy);
     float *part = static_cast<float *>(ws);
 #define HEX_WG(KV, NV)                                                                       \
-    hipLaunchKernelGGL((wgrad_bf16_k<KV, NV>), grid, dim3(kThreads), lds, st, xp, dp, part, sh, tg)
+    HEX_LAUNCH((wgrad_bf16_k<KV, NV>), grid, dim3(kThreads), lds, st, xp, dp, part, sh, tg)
 #define HEX_WG_N(KV)                                                                         \
     do {                                                                                     \
         switch (nbw) {                                                                       \

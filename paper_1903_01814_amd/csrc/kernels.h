@@ -12,6 +12,27 @@
 
 namespace hexk {
 
+// Optional per-launch timing (hexconv_timing_begin / hexconv_timing_end):
+// when enabled, a HIP event pair brackets each launch made through
+// HEX_LAUNCH; otherwise the cost is one relaxed atomic load.
+struct KTimer {
+    KTimer(const char *kernel, hipStream_t st);
+    ~KTimer();
+    KTimer(const KTimer &) = delete;
+    KTimer &operator=(const KTimer &) = delete;
+
+  private:
+    const char *name_;
+    hipStream_t st_;
+    hipEvent_t a_, b_;
+};
+
+#define HEX_LAUNCH(kern, grid, block, shm, st, ...)                                          \
+    do {                                                                                     \
+        ::hexk::KTimer hex_kt_(#kern, st);                                                   \
+        hipLaunchKernelGGL(kern, grid, block, shm, st, __VA_ARGS__);                         \
+    } while (0)
+
 enum Dtype { F32 = 0, BF16 = 1 };
 
 struct ConvShape {

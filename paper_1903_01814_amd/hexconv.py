@@ -45,7 +45,12 @@ SIGNATURES = {
     "hexpool_fwd": ([_P, _P, _P, _I, _I, _I, _I, _I, _I, _I, _I, _P], _I),
     "hexpool_bwd": ([_P, _P, _P, _P, _I, _I, _I, _I, _I, _I, _I, _I, _P], _I),
     "hex_status_string": ([_I], ctypes.c_char_p),
+    "hexconv_timing_begin": ([], _I),
+    "hexconv_timing_end": ([_I, ctypes.c_char_p, _IP, ctypes.POINTER(ctypes.c_double), _IP],
+                           _I),
 }
+
+HEX_TIMING_NAME_LEN = 64
 
 _lib = None
 
@@ -96,6 +101,28 @@ def hex_out_shape(H: int, W: int, stride: int):
     _ok("hex_out_shape", load().hex_out_shape(H, W, stride, ctypes.byref(ho),
                                               ctypes.byref(wo)))
     return ho.value, wo.value
+
+
+def hexconv_timing_begin():
+    """Start bracketing every kernel launch with HIP events (eager use only,
+    not while a HIP graph is being captured)."""
+    _ok("hexconv_timing_begin", load().hexconv_timing_begin())
+
+
+def hexconv_timing_end(max_kernels: int = 32):
+    """Stop recording; {kernel name: (launches, summed GPU ms)} in order of
+    first launch."""
+    names = ctypes.create_string_buffer(max_kernels * HEX_TIMING_NAME_LEN)
+    counts = (ctypes.c_int * max_kernels)()
+    total = (ctypes.c_double * max_kernels)()
+    n = ctypes.c_int()
+    _ok("hexconv_timing_end", load().hexconv_timing_end(max_kernels, names, counts, total,
+                                                        ctypes.byref(n)))
+    out = {}
+    for i in range(n.value):
+        raw = names.raw[i * HEX_TIMING_NAME_LEN:(i + 1) * HEX_TIMING_NAME_LEN]
+        out[raw.split(b"\0", 1)[0].decode()] = (counts[i], total[i])
+    return out
 
 
 def hex_tap_table(k: int, parity: int):

@@ -191,3 +191,17 @@ def test_host_helper_errors():
     buf = (ctypes.c_int * 7)()
     assert lib.hex_tap_table(1, 2, buf, buf) == -1
     assert lib.hex_tap_table(1, 0, None, buf) == -1
+
+
+def test_timing_host_paths():
+    """Kernel timing with nothing launched reports nothing; bad output
+    arguments are rejected."""
+    hx.hexconv_timing_begin()
+    assert hx.hexconv_timing_end() == {}
+    lib = hx.load()
+    n = ctypes.c_int()
+    counts = (ctypes.c_int * 1)()
+    total = (ctypes.c_double * 1)()
+    names = ctypes.create_string_buffer(hx.HEX_TIMING_NAME_LEN)
+    assert lib.hexconv_timing_end(0, names, counts, total, ctypes.byref(n)) == hx.HEX_ERR_INVALID_ARG
+    assert lib.hexconv_timing_end(1, None, counts, total, ctypes.byref(n)) == hx.HEX_ERR_INVALID_ARG

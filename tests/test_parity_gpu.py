@@ -467,3 +467,22 @@ def test_graph_replay_matches_eager(dt):
             torch.cuda.synchronize()
             for o, r in zip(outs, ref):
                 assert torch.equal(o, r), "replay %d differs" % rep
+
+
+def test_kernel_timing_reports_launches():
+    """hexconv_timing_* brackets each launch with events: one forward call of
+    the camera shape reports its kernel once, with a positive duration, and
+    the combined backward reports its main kernel and its reduction."""
+    cfg = CFG["c2"]
+    d = _conv_inputs(cfg, N=8)
+    run_fwd(d["x"], d["w"], d["b"], cfg["k"], 1, "f32")  # warm (module load)
+    hx.hexconv_timing_begin()
+    run_fwd(d["x"], d["w"], d["b"], cfg["k"], 1, "f32")
+    t = hx.hexconv_timing_end()
+    assert list(t) == ["fwd_f32_k"], t
+    assert t["fwd_f32_k"][0] == 1 and t["fwd_f32_k"][1] > 0
+    hx.hexconv_timing_begin()
+    run_bwd(d["x"], d["dy"], d["w"], cfg["k"], 1, "f32")
+    t = hx.hexconv_timing_end()
+    assert list(t) == ["bwd_f32_k", "reduce_chunked_k"], t
+    assert all(c == 1 and ms > 0 for c, ms in t.values()), t
