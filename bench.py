@@ -143,7 +143,7 @@ def dominant_kernel(torch, fn, reps):
 
 # backward kernels computing both gradients in one pass; every other
 # backward kernel computes one of them
-BOTH_GRADIENT_KERNELS = ("bwd_f32_k",)
+BOTH_GRADIENT_KERNELS = ("bwd_smallc_k",)
 
 
 def products_of(kernel, op):

@@ -171,7 +171,7 @@ WgradPath wgrad_path(const ConvShape &sh, Dtype d)
 // Fused data + weight gradient (hexconv_bwd) for this shape?
 bool bwd_fused(const ConvShape &sh, Dtype d)
 {
-    return !force_generic() && d == hexk::F32 && hexk::smallc_f32_bwd_fused_ok(sh);
+    return !force_generic() && hexk::smallc_bwd_fused_ok(sh, d);
 }
 
 size_t wgrad_workspace(const ConvShape &sh, Dtype d)
@@ -245,11 +245,8 @@ int hexconv_fwd(const void *x, const void *w, const void *bias, void *y, int N, 
     const bool relu = (flags & HEX_FLAG_RELU) != 0;
     const Dtype d = static_cast<Dtype>(dt);
     if (!force_generic()) {
-        if (d == hexk::F32 && hexk::smallc_f32_fwd_ok(sh))
-            return launched(hexk::smallc_f32_fwd(static_cast<const float *>(x),
-                                                 static_cast<const float *>(w),
-                                                 static_cast<const float *>(bias),
-                                                 static_cast<float *>(y), sh, relu, st));
+        if (hexk::smallc_fwd_ok(sh))
+            return launched(hexk::smallc_fwd(x, w, bias, y, sh, d, relu, st));
         if (d == hexk::BF16 && hexk::bf16_wide_ok(sh, sh.Ci, sh.Co))
             return launched(hexk::bf16_wide_conv(x, w, bias, y, sh, false, relu, st));
     }
@@ -336,7 +333,7 @@ size_t hexconv_bwd_workspace(int N, int C_in, int C_out, int H, int W, int k, in
     if (N == 0 || sh.Ho == 0)
         return 0;
     const Dtype d = static_cast<Dtype>(dt);
-    return bwd_fused(sh, d) ? hexk::smallc_f32_bwd_fused_workspace(sh) : wgrad_workspace(sh, d);
+    return bwd_fused(sh, d) ? hexk::smallc_bwd_fused_workspace(sh) : wgrad_workspace(sh, d);
 }
 
 int hexconv_bwd(const void *x, const void *dy, const void *w, void *dx, float *dw, float *db,
@@ -358,14 +355,12 @@ int hexconv_bwd(const void *x, const void *dy, const void *w, void *dx, float *d
     const Dtype d = static_cast<Dtype>(dt);
     const bool fused = !empty && bwd_fused(sh, d);
     const size_t need =
-        empty ? 0 : (fused ? hexk::smallc_f32_bwd_fused_workspace(sh) : wgrad_workspace(sh, d));
+        empty ? 0 : (fused ? hexk::smallc_bwd_fused_workspace(sh) : wgrad_workspace(sh, d));
     if (need > 0 && (ws == nullptr || ws_bytes < need))
         return HEX_ERR_INVALID_ARG;
     hipStream_t st = static_cast<hipStream_t>(stream);
     if (fused)
-        return launched(hexk::smallc_f32_bwd_fused(
-            static_cast<const float *>(x), static_cast<const float *>(dy),
-            static_cast<const float *>(w), static_cast<float *>(dx), dw, db, ws, sh, st));
+        return launched(hexk::smallc_bwd_fused(x, dy, w, dx, dw, db, ws, sh, d, st));
     if (dx != nullptr && N > 0) {
         rc = hexconv_bwd_data(dy, w, dx, N, C_in, C_out, H, W, k, stride, dt, stream);
         if (rc != HEX_OK)

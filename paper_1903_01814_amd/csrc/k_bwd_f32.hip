@@ -30,6 +30,7 @@
 // consecutive words, loaded once per channel and reused by all its taps.  The
 // channel groups' partial sums are added in LDS in a fixed order.
 #include <algorithm>
+#include <type_traits>
 
 #include "hexdev.h"
 #include "kernels.h"
@@ -61,6 +62,7 @@ struct BwdTiling {
     int CSD;           // LDS words per dy channel
     int xo, zo, oo;    // LDS offsets: x planes, zeros plane, ones plane
     int G;             // output-channel groups of the data gradient
+    int CG;            // output channels per group (G * CG >= C_out)
     int tiles_per_img, ntiles;
     int per;           // tiles per block: block b walks tiles [b * per, b * per + per)
     int nitems;        // float4 staging items per tile
@@ -98,33 +100,42 @@ template <int K, int U> struct StageMap {
     }
 };
 
-// One tile's dy and x rows in registers.  Every load is issued (items
-// outside the image read a valid address) and okm records which hold image
-// data; the others are replaced by zeros when committed.  Loads that are
-// always issued keep the count of loads in flight fixed, so a commit waits
-// only for its own buffer.
-template <int U> struct StageBuf {
-    float4 v[U];
+// One tile's dy and x rows in registers, as loaded (4 elements per item:
+// a float4, or 8 bytes of bf16).  Every load is issued (items outside the
+// image read a valid address) and okm records which hold image data; the
+// others are replaced by zeros when committed.  Loads that are always
+// issued keep the count of loads in flight fixed, so a commit waits only
+// for its own buffer.
+template <typename TT, int U> struct StageBuf {
+    typedef typename std::conditional<sizeof(TT) == 4, float4, uint2>::type Raw;
+    Raw v[U];
     uint32_t okm;
 
+    __device__ __forceinline__ static float4 widen(const float4 &q) { return q; }
+    __device__ __forceinline__ static float4 widen(const uint2 &q)
+    {
+        return make_float4(__uint_as_float(q.x << 16), __uint_as_float(q.x & 0xffff0000u),
+                           __uint_as_float(q.y << 16), __uint_as_float(q.y & 0xffff0000u));
+    }
+
     template <int K>
-    __device__ __forceinline__ void load(const StageMap<K, U> &m, const float *__restrict__ x,
-                                         const float *__restrict__ dy, const ConvShape &sh, int n,
+    __device__ __forceinline__ void load(const StageMap<K, U> &m, const TT *__restrict__ x,
+                                         const TT *__restrict__ dy, const ConvShape &sh, int n,
                                          int r0)
     {
         const size_t HW = static_cast<size_t>(sh.H) * sh.W;
         // row r0 - K of image n, channel 0: items add their offsets to it
         const long rofs = static_cast<long>(r0 - K) * sh.W;
-        const float *dyn = dy + static_cast<size_t>(n) * sh.Co * HW + rofs;
-        const float *xn = x + static_cast<size_t>(n) * sh.Ci * HW + rofs;
+        const TT *dyn = dy + static_cast<size_t>(n) * sh.Co * HW + rofs;
+        const TT *xn = x + static_cast<size_t>(n) * sh.Ci * HW + rofs;
         const int rlo = K - r0, rhi = sh.H - r0 + K; // window rows inside the image
         okm = 0;
 #pragma unroll
         for (int u = 0; u < U; ++u) {
             const int rr = (m.pk[u] >> 16) & 0xff;
             const bool ok = ((m.pk[u] >> 25) & 1) && rr >= rlo && rr < rhi;
-            const float *b = ((m.pk[u] >> 24) & 1) ? dyn : xn;
-            v[u] = *reinterpret_cast<const float4 *>(ok ? b + m.goff[u] : x);
+            const TT *b = ((m.pk[u] >> 24) & 1) ? dyn : xn;
+            v[u] = *reinterpret_cast<const Raw *>(ok ? b + m.goff[u] : x);
             okm |= ok ? 1u << u : 0u;
         }
     }
@@ -136,7 +147,7 @@ template <int U> struct StageBuf {
         using G = Geo<K>;
 #pragma unroll
         for (int u = 0; u < U; ++u) {
-            const float4 q = ((okm >> u) & 1) ? v[u] : make_float4(0.f, 0.f, 0.f, 0.f);
+            const float4 q = ((okm >> u) & 1) ? widen(v[u]) : make_float4(0.f, 0.f, 0.f, 0.f);
             float *d = lds + (m.pk[u] & 0xffff);
             d[0] = q.x;
             d[G::P] = q.y;
@@ -146,10 +157,12 @@ template <int U> struct StageBuf {
     }
 };
 
-template <int K, int CI, int MT, int NT, int CG, int U>
-__global__ __launch_bounds__(kThreads) void bwd_f32_k(
-    const float *__restrict__ x, const float *__restrict__ dy, const float *__restrict__ w,
-    float *__restrict__ dx, float *__restrict__ part, ConvShape sh, BwdTiling bt, int do_dx)
+// CGT: output channels per data-gradient group when fixed at compile time
+// (the channel loop is then unrolled), 0 for a loop over bt.CG.
+template <typename TT, int K, int CI, int MT, int NT, int CGT, int U>
+__global__ __launch_bounds__(kThreads) void bwd_smallc_k(
+    const TT *__restrict__ x, const TT *__restrict__ dy, const TT *__restrict__ w,
+    TT *__restrict__ dx, float *__restrict__ part, ConvShape sh, BwdTiling bt, int do_dx)
 {
     using Gm = Geo<K>;
     constexpr int T = num_taps(K);
@@ -173,14 +186,15 @@ __global__ __launch_bounds__(kThreads) void bwd_f32_k(
         const int e = tid + u * kThreads;
         const int co = e / (CI * T), rem = e - co * (CI * T);
         const int ci = rem / T, t = rem - ci * T;
-        wreg[u] = (e < nwl && co < Co) ? w[(static_cast<size_t>(co) * CI + ci) * T + (T - 1 - t)]
-                                       : 0.f;
+        wreg[u] = (e < nwl && co < Co)
+                      ? to_f(w[(static_cast<size_t>(co) * CI + ci) * T + (T - 1 - t)])
+                      : 0.f;
     }
 
     // the first two tiles' loads are in flight during the one-time set-up
     StageMap<K, U> map;
     map.init(sh, bt);
-    StageBuf<U> sa, sb;
+    StageBuf<TT, U> sa, sb;
     const int tpi = bt.tiles_per_img;
     // a contiguous run of tiles (consecutive row bands of one image): the
     // halo rows a tile shares with the previous one were fetched by this
@@ -190,7 +204,7 @@ __global__ __launch_bounds__(kThreads) void bwd_f32_k(
     // Every step issues the same loads (a tile past this block's run reloads
     // its last one, from L2, and is never committed), so the wait before a
     // commit only covers the loads of that buffer and not the newer ones.
-    auto load_tile = [&](StageBuf<U> &b, int t) {
+    auto load_tile = [&](StageBuf<TT, U> &b, int t) {
         t = min(t, t_end - 1);
         const int n = t / tpi;
         b.load(map, x, dy, sh, n, (t - n * tpi) * kTR);
@@ -281,7 +295,7 @@ __global__ __launch_bounds__(kThreads) void bwd_f32_k(
     // the same registers, then the two roles work on the window at the same
     // time (VALU and matrix cores of each SIMD).  Rows past the image are
     // zeros, so a short last tile needs no masking.
-    auto tile_step = [&](StageBuf<U> &buf, int tile) {
+    auto tile_step = [&](StageBuf<TT, U> &buf, int tile) {
         const int n = tile / tpi;
         const int r0 = (tile - n * tpi) * kTR;
         const int rows = min(kTR, sh.H - r0);
@@ -296,9 +310,10 @@ __global__ __launch_bounds__(kThreads) void bwd_f32_k(
 #pragma unroll
                     for (int r = 0; r < kTR; ++r)
                         gacc[ci][r] = 0.f;
-#pragma unroll
-                for (int cc = 0; cc < CG; ++cc) {
-                    const int co = g * CG + cc;
+                // one output channel's contribution (all taps, all CI)
+                auto chan = [&](int cc) {
+                    // CGT >= bt.CG: groups of CGT still cover every channel once
+                    const int co = g * (CGT > 0 ? CGT : bt.CG) + cc;
                     const bool ok = co < Co;
                     const float *src = lds + (ok ? co : 0) * bt.CSD + cbase;
                     const float *wc = wl + (ok ? co : Co) * CI * T;
@@ -327,6 +342,15 @@ __global__ __launch_bounds__(kThreads) void bwd_f32_k(
                         }
                         t0 += len;
                     }
+                };
+                if constexpr (CGT > 0) {
+#pragma unroll
+                    for (int cc = 0; cc < CGT; ++cc)
+                        chan(cc);
+                } else {
+#pragma unroll 1
+                    for (int cc = 0; cc < bt.CG; ++cc)
+                        chan(cc);
                 }
 #pragma unroll
                 for (int ci = 0; ci < CI; ++ci)
@@ -365,8 +389,15 @@ __global__ __launch_bounds__(kThreads) void bwd_f32_k(
                         s.z += q[2];
                         s.w += q[3];
                     }
-                    *reinterpret_cast<float4 *>(dx + (static_cast<size_t>(n) * CI + ci) * sh.H * W +
-                                                static_cast<size_t>(r0) * W + rem) = s;
+                    TT *dst = dx + (static_cast<size_t>(n) * CI + ci) * sh.H * W +
+                              static_cast<size_t>(r0) * W + rem;
+                    if constexpr (sizeof(TT) == 4) {
+                        *reinterpret_cast<float4 *>(dst) = s;
+                    } else {
+                        *reinterpret_cast<uint2 *>(dst) = make_uint2(
+                            from_f<bf16raw>(s.x) | (uint32_t(from_f<bf16raw>(s.y)) << 16),
+                            from_f<bf16raw>(s.z) | (uint32_t(from_f<bf16raw>(s.w)) << 16));
+                    }
                 }
             }
         }
@@ -430,6 +461,7 @@ BwdTiling bwd_tiling(const ConvShape &sh)
     bt.zo = bt.xo + sh.Ci * bt.CS;
     bt.oo = bt.zo + bt.CS;
     bt.G = std::max(1, std::min(sh.Co, kDxThreads / sh.W));
+    bt.CG = cdiv(sh.Co, bt.G);
     bt.tiles_per_img = cdiv(sh.H, kTR);
     bt.ntiles = bt.tiles_per_img * sh.N;
     bt.per = cdiv(bt.ntiles, std::max(1, device_cus()));
@@ -442,9 +474,10 @@ BwdTiling bwd_tiling(const ConvShape &sh)
     return bt;
 }
 
-int bwd_cg(const ConvShape &sh, const BwdTiling &bt) { return cdiv(sh.Co, bt.G); }
-
 int bwd_u(const BwdTiling &bt) { return cdiv(bt.nitems, kThreads); }
+
+// register buffers per dtype: fp32 items are 16 bytes, bf16 items 8
+int bwd_umax(Dtype d) { return d == F32 ? 8 : 12; }
 
 size_t bwd_lds(const ConvShape &sh, const BwdTiling &bt)
 {
@@ -458,73 +491,103 @@ size_t bwd_lds(const ConvShape &sh, const BwdTiling &bt)
 // contiguous run of tiles (bt.per of them).
 int bwd_grid(const BwdTiling &bt) { return cdiv(bt.ntiles, bt.per); }
 
+template <typename TT, int K, int CI, int NT>
+void launch_bwd(int MT, int U, const BwdTiling &bt, const ConvShape &sh, size_t lds,
+                hipStream_t st, const TT *x, const TT *dy, const TT *w, TT *dx, float *part,
+                int do_dx)
+{
+    const dim3 grid(bwd_grid(bt));
+#define HEX_B2(MTV, CGV, UV)                                                                  \
+    HEX_LAUNCH((bwd_smallc_k<TT, K, CI, MTV, NT, CGV, UV>), grid, dim3(kThreads), lds, st, x, dy, \
+               w, dx, part, sh, bt, do_dx)
+    // fp32 (the camera layers) unrolls channel groups of 2, 3 or 4
+#define HEX_B(MTV, UV)                                                                        \
+    do {                                                                                     \
+        if constexpr (sizeof(TT) == 4) {                                                     \
+            if (bt.CG <= 2) HEX_B2(MTV, 2, UV);                                              \
+            else if (bt.CG == 3) HEX_B2(MTV, 3, UV);                                         \
+            else if (bt.CG == 4) HEX_B2(MTV, 4, UV);                                         \
+            else HEX_B2(MTV, 0, UV);                                                         \
+        } else {                                                                             \
+            HEX_B2(MTV, 0, UV);                                                              \
+        }                                                                                    \
+    } while (0)
+#define HEX_B_U(MTV)                                                                          \
+    do {                                                                                     \
+        if (U <= 4) {                                                                        \
+            HEX_B(MTV, 4);                                                                   \
+        } else if (U <= 8) {                                                                 \
+            HEX_B(MTV, 8);                                                                   \
+        } else {                                                                             \
+            if constexpr (sizeof(TT) == 2)                                                   \
+                HEX_B(MTV, 12);                                                              \
+        }                                                                                    \
+    } while (0)
+    if (MT == 1)
+        HEX_B_U(1);
+    else
+        HEX_B_U(2);
+#undef HEX_B_U
+#undef HEX_B
+#undef HEX_B2
+}
+
+template <typename TT>
+hipError_t bwd_fused_t(const TT *x, const TT *dy, const TT *w, TT *dx, float *dw, float *db,
+                       void *ws, const ConvShape &sh, hipStream_t st)
+{
+    const BwdTiling bt = bwd_tiling(sh);
+    const int nparts = bwd_grid(bt);
+    const int MT = cdiv(sh.Co, 16);
+    const int U = bwd_u(bt);
+    float *part = static_cast<float *>(ws);
+    const size_t lds = bwd_lds(sh, bt);
+    const int do_dx = dx != nullptr ? 1 : 0;
+    if (sh.k == 1) {
+        if (sh.Ci == 1)
+            launch_bwd<TT, 1, 1, 1>(MT, U, bt, sh, lds, st, x, dy, w, dx, part, do_dx); // J + 1 = 8
+        else
+            launch_bwd<TT, 1, 2, 1>(MT, U, bt, sh, lds, st, x, dy, w, dx, part, do_dx); // 15
+    } else {
+        if (sh.Ci == 1)
+            launch_bwd<TT, 2, 1, 2>(MT, U, bt, sh, lds, st, x, dy, w, dx, part, do_dx); // 20
+        else
+            launch_bwd<TT, 2, 2, 4>(MT, U, bt, sh, lds, st, x, dy, w, dx, part, do_dx); // 39
+    }
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess)
+        return e;
+    return reduce_chunked(part, nparts, sh.Co, sh.Ci * sh.T, dw, db, st);
+}
+
 } // namespace
 
-bool smallc_f32_bwd_fused_ok(const ConvShape &sh)
+bool smallc_bwd_fused_ok(const ConvShape &sh, Dtype d)
 {
     if (sh.s != 1 || (sh.k != 1 && sh.k != 2) || sh.Ci > 2 || sh.Co > 32 || sh.W % 4 != 0 ||
         sh.W > kDxThreads || sh.Ci * sh.T + 1 > 64)
         return false;
     const BwdTiling bt = bwd_tiling(sh);
-    const int cg = bwd_cg(sh, bt);
-    return cg <= 4 && bwd_u(bt) <= 8 && bwd_lds(sh, bt) <= kLdsMax;
+    return bt.CG <= 8 && bwd_u(bt) <= bwd_umax(d) && bwd_lds(sh, bt) <= kLdsMax;
 }
 
-size_t smallc_f32_bwd_fused_workspace(const ConvShape &sh)
+size_t smallc_bwd_fused_workspace(const ConvShape &sh)
 {
     const BwdTiling bt = bwd_tiling(sh);
     return sizeof(float) * static_cast<size_t>(bwd_grid(bt)) * kPartChunk *
            part_chunks(sh.Co * (sh.Ci * sh.T + 1));
 }
 
-hipError_t smallc_f32_bwd_fused(const float *x, const float *dy, const float *w, float *dx,
-                                float *dw, float *db, void *ws, const ConvShape &sh,
-                                hipStream_t st)
+hipError_t smallc_bwd_fused(const void *x, const void *dy, const void *w, void *dx, float *dw,
+                            float *db, void *ws, const ConvShape &sh, Dtype d, hipStream_t st)
 {
-    const BwdTiling bt = bwd_tiling(sh);
-    const int nparts = bwd_grid(bt);
-    const int MT = cdiv(sh.Co, 16);
-    const int CG = std::max(2, bwd_cg(sh, bt));
-    const int U = bwd_u(bt);
-    float *part = static_cast<float *>(ws);
-    const size_t lds = bwd_lds(sh, bt);
-    const int do_dx = dx != nullptr ? 1 : 0;
-    dim3 grid(nparts);
-#define HEX_B(KV, CIV, MTV, NTV, CGV, UV)                                                     \
-    HEX_LAUNCH((bwd_f32_k<KV, CIV, MTV, NTV, CGV, UV>), grid, dim3(kThreads), lds, st, \
-                       x, dy, w, dx, part, sh, bt, do_dx)
-#define HEX_B_U(KV, CIV, MTV, NTV, CGV)                                                       \
-    do {                                                                                     \
-        if (U <= 2) HEX_B(KV, CIV, MTV, NTV, CGV, 2);                                        \
-        else if (U <= 4) HEX_B(KV, CIV, MTV, NTV, CGV, 4);                                   \
-        else HEX_B(KV, CIV, MTV, NTV, CGV, 8);                                               \
-    } while (0)
-#define HEX_B_CG(KV, CIV, MTV, NTV)                                                           \
-    do {                                                                                     \
-        if (CG == 2) HEX_B_U(KV, CIV, MTV, NTV, 2);                                          \
-        else if (CG == 3) HEX_B_U(KV, CIV, MTV, NTV, 3);                                     \
-        else HEX_B_U(KV, CIV, MTV, NTV, 4);                                                  \
-    } while (0)
-#define HEX_B_MT(KV, CIV, NTV)                                                                \
-    do {                                                                                     \
-        if (MT == 1) HEX_B_CG(KV, CIV, 1, NTV);                                              \
-        else HEX_B_CG(KV, CIV, 2, NTV);                                                      \
-    } while (0)
-    if (sh.k == 1) {
-        if (sh.Ci == 1) HEX_B_MT(1, 1, 1);     // J + 1 = 8
-        else HEX_B_MT(1, 2, 1);                // J + 1 = 15
-    } else {
-        if (sh.Ci == 1) HEX_B_MT(2, 1, 2);     // J + 1 = 20
-        else HEX_B_MT(2, 2, 4);                // J + 1 = 39
-    }
-#undef HEX_B_MT
-#undef HEX_B_CG
-#undef HEX_B_U
-#undef HEX_B
-    hipError_t e = hipGetLastError();
-    if (e != hipSuccess)
-        return e;
-    return reduce_chunked(part, nparts, sh.Co, sh.Ci * sh.T, dw, db, st);
+    if (d == F32)
+        return bwd_fused_t(static_cast<const float *>(x), static_cast<const float *>(dy),
+                           static_cast<const float *>(w), static_cast<float *>(dx), dw, db, ws,
+                           sh, st);
+    return bwd_fused_t(static_cast<const bf16raw *>(x), static_cast<const bf16raw *>(dy),
+                       static_cast<const bf16raw *>(w), static_cast<bf16raw *>(dx), dw, db, ws, sh,
+                       st);
 }
 
 } // namespace hexk

@@ -146,10 +146,10 @@ template <int U> struct PlainPrefetch {
 
 // --------------------------------------------------------------- forward
 
-template <int K, int KS, int U>
-__global__ __launch_bounds__(kThreads) void fwd_f32_k(
-    const float *__restrict__ x, const float *__restrict__ w, const float *__restrict__ bias,
-    float *__restrict__ y, ConvShape sh, int relu, Tiling tg, int vec4)
+template <typename TT, int K, int KS, int U>
+__global__ __launch_bounds__(kThreads) void fwd_smallc_k(
+    const TT *__restrict__ x, const TT *__restrict__ w, const TT *__restrict__ bias,
+    TT *__restrict__ y, ConvShape sh, int relu, Tiling tg, int vec4)
 {
     constexpr int T = num_taps(K);
     extern __shared__ float xs[];
@@ -174,7 +174,8 @@ __global__ __launch_bounds__(kThreads) void fwd_f32_k(
         const int cog = blockIdx.y * 16 + r;
         float v = 0.f;
         if (cog < sh.Co)
-            v = col < J ? w[static_cast<size_t>(cog) * J + col] : (bias != nullptr ? bias[cog] : 0.f);
+            v = col < J ? to_f(w[static_cast<size_t>(cog) * J + col])
+                        : (bias != nullptr ? to_f(bias[cog]) : 0.f);
         wt[e] = v;
     }
 
@@ -221,7 +222,7 @@ __global__ __launch_bounds__(kThreads) void fwd_f32_k(
 
         const int nslot = o.rows * tg.TW;
         const int ntile = (nslot + 15) / 16;
-        float *yb = y + (static_cast<size_t>(o.n) * sh.Co + co) * HW;
+        TT *yb = y + (static_cast<size_t>(o.n) * sh.Co + co) * HW;
         for (int mt = wave; mt < ntile; mt += kWaves) {
             // A row of this lane: pixel slot p of the tile
             const int p = mt * 16 + m;
@@ -255,14 +256,20 @@ __global__ __launch_bounds__(kThreads) void fwd_f32_k(
                 if (relu)
                     v[j] = fmaxf(v[j], 0.f);
             }
-            float *dst = yb + static_cast<size_t>(o.r0 + qr) * sh.W + o.c0 + qc;
+            TT *dst = yb + static_cast<size_t>(o.r0 + qr) * sh.W + o.c0 + qc;
             if (vec4 && qc + 3 < o.cols) {
-                *reinterpret_cast<float4 *>(dst) = make_float4(v[0], v[1], v[2], v[3]);
+                if constexpr (sizeof(TT) == 4) {
+                    *reinterpret_cast<float4 *>(dst) = make_float4(v[0], v[1], v[2], v[3]);
+                } else {
+                    const uint32_t lo = from_f<bf16raw>(v[0]) | (uint32_t(from_f<bf16raw>(v[1])) << 16);
+                    const uint32_t hi = from_f<bf16raw>(v[2]) | (uint32_t(from_f<bf16raw>(v[3])) << 16);
+                    *reinterpret_cast<uint2 *>(dst) = make_uint2(lo, hi);
+                }
             } else {
 #pragma unroll
                 for (int j = 0; j < 4; ++j)
                     if (qc + j < o.cols)
-                        dst[j] = v[j];
+                        dst[j] = from_f<TT>(v[j]);
             }
         }
     }
@@ -563,7 +570,7 @@ int bwd_ic_chunk(const ConvShape &sh, const Tiling &tg)
 
 // ------------------------------------------------------------- launchers
 
-bool smallc_f32_fwd_ok(const ConvShape &sh)
+bool smallc_fwd_ok(const ConvShape &sh)
 {
     if (sh.s != 1 || (sh.k != 1 && sh.k != 2) || sh.Ci * sh.T > 64 || sh.W % 4 != 0)
         return false;
@@ -571,37 +578,50 @@ bool smallc_f32_fwd_ok(const ConvShape &sh)
     return fwd_lds(sh, tg) <= kLdsLimit && shear_depth(sh, tg, sh.Ci) > 0;
 }
 
-hipError_t smallc_f32_fwd(const float *x, const float *w, const float *b, float *y,
-                          const ConvShape &sh, bool relu, hipStream_t st)
+namespace {
+template <typename TT>
+hipError_t smallc_fwd_t(const TT *x, const TT *w, const TT *b, TT *y, const ConvShape &sh,
+                        bool relu, hipStream_t st)
 {
     const Tiling tg = make_tiling(sh, kFwdTarget);
     const int KS = cdiv(sh.Ci * sh.T, 4);
     const int U = shear_depth(sh, tg, sh.Ci);
     dim3 grid(std::min(tg.ntiles, kFwdBlocks), cdiv(sh.Co, 16));
     const size_t lds = fwd_lds(sh, tg);
-#define HEX_FWD_F32(KV, KSV, UV)                                                             \
-    HEX_LAUNCH((fwd_f32_k<KV, KSV, UV>), grid, dim3(kThreads), lds, st, x, w, b, y,  \
-                       sh, relu ? 1 : 0, tg, 1)
-#define HEX_FWD_F32_U(KV, KSV)                                                               \
+#define HEX_FWD_SC(KV, KSV, UV)                                                              \
+    HEX_LAUNCH((fwd_smallc_k<TT, KV, KSV, UV>), grid, dim3(kThreads), lds, st, x, w, b, y,   \
+               sh, relu ? 1 : 0, tg, 1)
+#define HEX_FWD_SC_U(KV, KSV)                                                                \
     do {                                                                                     \
-        if (U == 1) HEX_FWD_F32(KV, KSV, 1);                                                 \
-        else if (U == 2) HEX_FWD_F32(KV, KSV, 2);                                            \
-        else if (U == 4) HEX_FWD_F32(KV, KSV, 4);                                            \
-        else HEX_FWD_F32(KV, KSV, 8);                                                        \
+        if (U == 1) HEX_FWD_SC(KV, KSV, 1);                                                  \
+        else if (U == 2) HEX_FWD_SC(KV, KSV, 2);                                             \
+        else if (U == 4) HEX_FWD_SC(KV, KSV, 4);                                             \
+        else HEX_FWD_SC(KV, KSV, 8);                                                         \
     } while (0)
     if (sh.k == 1) {
-        if (KS <= 2) HEX_FWD_F32_U(1, 2);
-        else if (KS <= 4) HEX_FWD_F32_U(1, 4);
-        else if (KS <= 8) HEX_FWD_F32_U(1, 8);
-        else HEX_FWD_F32_U(1, 16);
+        if (KS <= 2) HEX_FWD_SC_U(1, 2);
+        else if (KS <= 4) HEX_FWD_SC_U(1, 4);
+        else if (KS <= 8) HEX_FWD_SC_U(1, 8);
+        else HEX_FWD_SC_U(1, 16);
     } else {
-        if (KS <= 5) HEX_FWD_F32_U(2, 5);
-        else if (KS <= 10) HEX_FWD_F32_U(2, 10);
-        else HEX_FWD_F32_U(2, 16);
+        if (KS <= 5) HEX_FWD_SC_U(2, 5);
+        else if (KS <= 10) HEX_FWD_SC_U(2, 10);
+        else HEX_FWD_SC_U(2, 16);
     }
-#undef HEX_FWD_F32_U
-#undef HEX_FWD_F32
+#undef HEX_FWD_SC_U
+#undef HEX_FWD_SC
     return hipGetLastError();
+}
+} // namespace
+
+hipError_t smallc_fwd(const void *x, const void *w, const void *b, void *y, const ConvShape &sh,
+                      Dtype d, bool relu, hipStream_t st)
+{
+    if (d == F32)
+        return smallc_fwd_t(static_cast<const float *>(x), static_cast<const float *>(w),
+                            static_cast<const float *>(b), static_cast<float *>(y), sh, relu, st);
+    return smallc_fwd_t(static_cast<const bf16raw *>(x), static_cast<const bf16raw *>(w),
+                        static_cast<const bf16raw *>(b), static_cast<bf16raw *>(y), sh, relu, st);
 }
 
 bool smallc_f32_bwd_data_ok(const ConvShape &sh)

@@ -354,25 +354,38 @@ __global__ __launch_bounds__(kT) void wgrad32_k(const bf16raw *__restrict__ x,
 }
 
 // Sum the slots of every partial position in a fixed order and scatter to
-// dw[co][ci][t] / db[co].
-__global__ __launch_bounds__(256) void wgrad32_reduce_k(const float *__restrict__ part, int nparts,
-                                                        int npos, int CI, int CO, int co0, int T,
-                                                        float *__restrict__ dw,
-                                                        float *__restrict__ db)
+// dw[co][ci][t] / db[co].  Block = 64 positions x kRedSlices slot slices;
+// each thread adds every kRedSlices-th slot with four loads in flight, then
+// the slices are added by a fixed tree in LDS.
+constexpr int kRedSlices = 16;
+
+__global__ __launch_bounds__(kRegChunk * kRedSlices) void wgrad32_reduce_k(
+    const float *__restrict__ part, int nparts, int npos, int CI, int CO, int co0, int T,
+    float *__restrict__ dw, float *__restrict__ db)
 {
-    const int pos = blockIdx.x * 64 + (threadIdx.x & 63);
-    const int sl = threadIdx.x >> 6; // 4 slices of the slots
-    __shared__ float red[4][64];
-    float s = 0.f;
-    if (pos < npos)
-        for (int p = sl; p < nparts; p += 4)
-            s += part[part_index(pos, p, nparts)];
-    red[sl][threadIdx.x & 63] = s;
-    __syncthreads();
+    __shared__ float red[kRedSlices][kRegChunk];
+    const int el = threadIdx.x % kRegChunk, sl = threadIdx.x / kRegChunk;
+    const int pos = blockIdx.x * kRegChunk + el;
+    float s4[4] = {0.f, 0.f, 0.f, 0.f};
+    if (pos < npos) {
+        int p = sl;
+        for (; p + 3 * kRedSlices < nparts; p += 4 * kRedSlices) {
+#pragma unroll
+            for (int u = 0; u < 4; ++u)
+                s4[u] += part[part_index(pos, p + u * kRedSlices, nparts)];
+        }
+        for (; p < nparts; p += kRedSlices)
+            s4[0] += part[part_index(pos, p, nparts)];
+    }
+    red[sl][el] = (s4[0] + s4[1]) + (s4[2] + s4[3]);
+    for (int half = kRedSlices / 2; half > 0; half >>= 1) {
+        __syncthreads();
+        if (sl < half)
+            red[sl][el] += red[sl + half][el];
+    }
     if (sl != 0 || pos >= npos)
         return;
-    const int l = threadIdx.x;
-    const float v = (red[0][l] + red[1][l]) + (red[2][l] + red[3][l]);
+    const float v = red[0][el];
     const int NIB = CI >> 5, NCB = CO >> 5;
     const int ntile_pos = T * NIB * NCB * 16 * kRegChunk;
     if (pos < ntile_pos) {
@@ -579,7 +592,7 @@ hipError_t bf16_wgrad32(const void *x, const void *dy, float *dw, float *db, voi
         if (err != hipSuccess)
             return false;
         const int npos = sh.T * C * 16 * kRegChunk + a.CO;
-        HEX_LAUNCH(wgrad32_reduce_k, dim3(cdiv(npos, 64)), dim3(256), 0, st, part,
+        HEX_LAUNCH(wgrad32_reduce_k, dim3(cdiv(npos, kRegChunk)), dim3(kRegChunk * kRedSlices), 0, st, part,
                            a.nparts, npos, sh.Ci, a.CO, a.co0, sh.T, dw, db);
         err = hipGetLastError();
         return err == hipSuccess;

@@ -88,9 +88,9 @@ hipError_t pool_bwd_fast(const void *dy, const uint8_t *am, const void *relu_y, 
                          const ConvShape &sh, int mode, Dtype dt, hipStream_t st);
 
 // ---- float32, few input channels (C_in*T <= 64), stride 1 -------------
-bool smallc_f32_fwd_ok(const ConvShape &sh);
-hipError_t smallc_f32_fwd(const float *x, const float *w, const float *b, float *y,
-                          const ConvShape &sh, bool relu, hipStream_t st);
+bool smallc_fwd_ok(const ConvShape &sh);
+hipError_t smallc_fwd(const void *x, const void *w, const void *b, void *y, const ConvShape &sh,
+                      Dtype d, bool relu, hipStream_t st);
 bool smallc_f32_bwd_data_ok(const ConvShape &sh);
 hipError_t smallc_f32_bwd_data(const float *dy, const float *w, float *dx, const ConvShape &sh,
                                hipStream_t st);
@@ -98,11 +98,11 @@ bool smallc_f32_wgrad_ok(const ConvShape &sh);
 size_t smallc_f32_wgrad_workspace(const ConvShape &sh);
 hipError_t smallc_f32_wgrad(const float *x, const float *dy, float *dw, float *db, void *ws,
                             const ConvShape &sh, hipStream_t st);
-bool smallc_f32_bwd_fused_ok(const ConvShape &sh);
-size_t smallc_f32_bwd_fused_workspace(const ConvShape &sh);
-hipError_t smallc_f32_bwd_fused(const float *x, const float *dy, const float *w, float *dx,
-                                float *dw, float *db, void *ws, const ConvShape &sh,
-                                hipStream_t st);
+// both gradients in one pass over dy (C_in <= 2, C_out <= 32), fp32 or bf16
+bool smallc_bwd_fused_ok(const ConvShape &sh, Dtype d);
+size_t smallc_bwd_fused_workspace(const ConvShape &sh);
+hipError_t smallc_bwd_fused(const void *x, const void *dy, const void *w, void *dx, float *dw,
+                            float *db, void *ws, const ConvShape &sh, Dtype d, hipStream_t st);
 
 // ---- bf16 matrix-core convolution, input channels a multiple of 32 -----
 // forward (reflect = false: IC = C_in, OC = C_out) or stride-1 data

@@ -479,10 +479,10 @@ def test_kernel_timing_reports_launches():
     hx.hexconv_timing_begin()
     run_fwd(d["x"], d["w"], d["b"], cfg["k"], 1, "f32")
     t = hx.hexconv_timing_end()
-    assert list(t) == ["fwd_f32_k"], t
-    assert t["fwd_f32_k"][0] == 1 and t["fwd_f32_k"][1] > 0
+    assert list(t) == ["fwd_smallc_k"], t
+    assert t["fwd_smallc_k"][0] == 1 and t["fwd_smallc_k"][1] > 0
     hx.hexconv_timing_begin()
     run_bwd(d["x"], d["dy"], d["w"], cfg["k"], 1, "f32")
     t = hx.hexconv_timing_end()
-    assert list(t) == ["bwd_f32_k", "reduce_chunked_k"], t
+    assert list(t) == ["bwd_smallc_k", "reduce_chunked_k"], t
     assert all(c == 1 and ms > 0 for c, ms in t.values()), t
