@@ -48,7 +48,13 @@ __global__ __launch_bounds__(64) void reduce_partials_k(const float *__restrict_
 }
 
 constexpr int kRedSlices = 16; // slot slices per chunk block (1024 threads)
+constexpr int kRedBatch = 16;  // slots per thread whose loads are in flight together
 
+// Chunked layout: one block per chunk of 64 elements; thread (slice sl,
+// element el) adds slots sl, sl + 16, sl + 32, ... of its element, issuing
+// the loads of 16 slots before adding any (one memory latency per 256
+// slots), then the 16 slices are added by a fixed tree.  The order of the
+// additions depends only on nparts, so results are reproducible.
 __global__ __launch_bounds__(kPartChunk * kRedSlices) void reduce_chunked_k(
     const float *__restrict__ part, int nparts, int E, int J, float *__restrict__ dw,
     float *__restrict__ db)
@@ -57,16 +63,19 @@ __global__ __launch_bounds__(kPartChunk * kRedSlices) void reduce_chunked_k(
     const int chunk = blockIdx.x;
     const int el = threadIdx.x % kPartChunk, sl = threadIdx.x / kPartChunk;
     const float *src = part + static_cast<size_t>(chunk) * nparts * kPartChunk + el;
-    float s[4] = {0.f, 0.f, 0.f, 0.f};
-    int p = sl;
-    for (; p + 3 * kRedSlices < nparts; p += 4 * kRedSlices) {
+    float acc = 0.f;
+    for (int p0 = 0; p0 < nparts; p0 += kRedSlices * kRedBatch) {
+        float v[kRedBatch];
 #pragma unroll
-        for (int u = 0; u < 4; ++u)
-            s[u] += src[static_cast<size_t>(p + u * kRedSlices) * kPartChunk];
+        for (int u = 0; u < kRedBatch; ++u) {
+            const int p = p0 + sl + u * kRedSlices;
+            v[u] = p < nparts ? src[static_cast<size_t>(p) * kPartChunk] : 0.f;
+        }
+#pragma unroll
+        for (int u = 0; u < kRedBatch; ++u)
+            acc += v[u];
     }
-    for (; p < nparts; p += kRedSlices)
-        s[0] += src[static_cast<size_t>(p) * kPartChunk];
-    red[sl][el] = (s[0] + s[1]) + (s[2] + s[3]);
+    red[sl][el] = acc;
     for (int half = kRedSlices / 2; half > 0; half >>= 1) {
         __syncthreads();
         if (sl < half)

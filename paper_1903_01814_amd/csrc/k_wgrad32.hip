@@ -355,9 +355,10 @@ __global__ __launch_bounds__(kT) void wgrad32_k(const bf16raw *__restrict__ x,
 
 // Sum the slots of every partial position in a fixed order and scatter to
 // dw[co][ci][t] / db[co].  Block = 64 positions x kRedSlices slot slices;
-// each thread adds every kRedSlices-th slot with four loads in flight, then
-// the slices are added by a fixed tree in LDS.
+// each thread adds every kRedSlices-th slot, issuing kRedBatch loads before
+// adding any, then the slices are added by a fixed tree in LDS.
 constexpr int kRedSlices = 16;
+constexpr int kRedBatch = 16; // slots per thread whose loads are in flight together
 
 __global__ __launch_bounds__(kRegChunk * kRedSlices) void wgrad32_reduce_k(
     const float *__restrict__ part, int nparts, int npos, int CI, int CO, int co0, int T,
@@ -366,18 +367,21 @@ __global__ __launch_bounds__(kRegChunk * kRedSlices) void wgrad32_reduce_k(
     __shared__ float red[kRedSlices][kRegChunk];
     const int el = threadIdx.x % kRegChunk, sl = threadIdx.x / kRegChunk;
     const int pos = blockIdx.x * kRegChunk + el;
-    float s4[4] = {0.f, 0.f, 0.f, 0.f};
+    float acc = 0.f;
     if (pos < npos) {
-        int p = sl;
-        for (; p + 3 * kRedSlices < nparts; p += 4 * kRedSlices) {
+        for (int p0 = 0; p0 < nparts; p0 += kRedSlices * kRedBatch) {
+            float v[kRedBatch];
 #pragma unroll
-            for (int u = 0; u < 4; ++u)
-                s4[u] += part[part_index(pos, p + u * kRedSlices, nparts)];
+            for (int u = 0; u < kRedBatch; ++u) {
+                const int p = p0 + sl + u * kRedSlices;
+                v[u] = p < nparts ? part[part_index(pos, p, nparts)] : 0.f;
+            }
+#pragma unroll
+            for (int u = 0; u < kRedBatch; ++u)
+                acc += v[u];
         }
-        for (; p < nparts; p += kRedSlices)
-            s4[0] += part[part_index(pos, p, nparts)];
     }
-    red[sl][el] = (s4[0] + s4[1]) + (s4[2] + s4[3]);
+    red[sl][el] = acc;
     for (int half = kRedSlices / 2; half > 0; half >>= 1) {
         __syncthreads();
         if (sl < half)
