@@ -161,8 +161,13 @@ WgradPath wgrad_path(const ConvShape &sh, Dtype d)
         return WgradPath::Generic;
     if (d == hexk::F32 && hexk::smallc_f32_wgrad_ok(sh))
         return WgradPath::SmallF32;
-    if (d == hexk::BF16 && hexk::bf16_wgrad32_ok(sh))
-        return WgradPath::Bf16Mfma32;
+    if (d == hexk::BF16) {
+        // several passes re-read x once per pass: then the single-pass
+        // kernel, where it applies, is the faster one
+        const int passes = hexk::bf16_wgrad32_passes(sh);
+        if (passes == 1 || (passes > 1 && !hexk::bf16_wgrad_ok(sh)))
+            return WgradPath::Bf16Mfma32;
+    }
     if (d == hexk::BF16 && hexk::bf16_wgrad_ok(sh))
         return WgradPath::Bf16Mfma;
     return WgradPath::Generic;

@@ -23,11 +23,16 @@
 // A K-step (16 pixels) is two runs of the same parity.  Zero pads around
 // the split rows and zero rows outside the image give the padding taps.
 //
-// Work split.  One block of 8 waves per CU owns a contiguous run of pixel
-// tiles (full-width rows) and prefetches the next tile into registers while
-// it computes the current one.  Wave w owns one (ci block, co block) pair of
-// 32 x 32 channels and a group of taps (compile-time), so no two waves add
-// to the same output; the waves of the first ci block also sum dy for db.
+// Work split.  One block of 4 waves per CU (one wave per SIMD, so a wave
+// may hold up to 512 registers and the accumulators sit beside the
+// prefetch buffers) owns a contiguous run of pixel tiles (full-width rows)
+// and prefetches the next tile into registers while it computes the
+// current one.  Wave w owns one 32-channel block of ci, a group of taps
+// (compile-time) and every 32-channel block of co in the pass (at most
+// two), so each B fragment feeds one product per co block and no two waves
+// add to the same output; the waves of the first ci block and tap group
+// also sum dy for db.  Within a K-step the B fragment of the next tap, and
+// the A fragments of the next K-step, are read before the current products.
 // Each block writes its accumulators to its own partial slot exactly as they
 // sit in the registers (one 64-lane register = 64 contiguous floats, whole
 // 256-byte lines), and a final kernel adds the slots in a fixed order and
@@ -47,7 +52,8 @@ using namespace hexgeom;
 typedef float floatx16 __attribute__((ext_vector_type(16)));
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 
-constexpr int kT = 512; // threads per block (8 waves)
+constexpr int kT = 256; // threads per block (4 waves, one per SIMD)
+constexpr int kWaves = kT / 64;
 constexpr int kRegChunk = 64; // floats per partial chunk (one register of a wave)
 
 struct Wg32Args {
@@ -191,72 +197,85 @@ template <int S> __device__ __forceinline__ bf16x8 load_shifted(const bf16raw *_
     }
 }
 
-// A fragment of K-step q (dy, run 2q + kh of parity P) and where its runs
-// start: window row and split position.
-template <int P> struct WgA {
-    bf16x8 a;
+// A fragments of K-step q (dy of each co block, run 2q + kh of parity P)
+// and where the runs start: window row and split position.
+template <int P, int NCB> struct WgA {
+    bf16x8 a[NCB];
     int rrow, j0;
-    __device__ __forceinline__ void fetch(const bf16raw *__restrict__ dyb, int WS, int rpr,
-                                          const FastDiv &frpr, int q, int kh)
+    __device__ __forceinline__ void fetch(const bf16raw *__restrict__ dyb, int dyblk, int WS,
+                                          int rpr, const FastDiv &frpr, int q, int kh)
     {
         const int run = 2 * q + kh;
         rrow = udiv(run, frpr);
         j0 = (run - rrow * rpr) * 8;
-        a = *reinterpret_cast<const bf16x8 *>(dyb + (rrow * 2 + P) * WS + j0);
+        const bf16raw *p = dyb + (rrow * 2 + P) * WS + j0;
+#pragma unroll
+        for (int c = 0; c < NCB; ++c)
+            a[c] = *reinterpret_cast<const bf16x8 *>(p + c * dyblk);
     }
 };
 
-// Products of one K-step for taps [T0, T1): every B fragment (x moved by
-// the tap) is read first, then the products run in tap order.
-template <int K, int P, int T0, int T1, int NA>
-__device__ __forceinline__ void wg_kstep(floatx16 (&acc)[NA], const WgA<P> &A, float &dbs,
-                                         bool do_db, const bf16raw *__restrict__ xb, int XS)
+// B fragment of tap t for the runs of A (x moved by the tap).
+template <int K, int P>
+__device__ __forceinline__ bf16x8 wg_loadB(int t, const bf16raw *__restrict__ xb, int XS,
+                                           int rrow, int j0)
 {
     constexpr TapTable<K> tt;
-    if (do_db) {
-#pragma unroll
-        for (int e = 0; e < 8; ++e)
-            dbs += static_cast<float>(A.a[e]);
-    }
-#pragma unroll
-    for (int t = T0; t < T1; ++t) {
-        const int dq = tt.dq[t], ds = tt.ds[t];
-        const int dr = tap_drow(dq, ds, P);
-        const int sh = floor_half(P + dq);
-        const bf16raw *base = xb + A.j0 + ((A.rrow + K + dr) * 2 + ((P + dq) & 1)) * XS;
-        bf16x8 b;
-        if (sh == 0)
-            b = load_shifted<0>(base);
-        else if (sh == 1)
-            b = load_shifted<1>(base);
-        else
-            b = load_shifted<-1>(base);
-        acc[t - T0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(A.a, b, acc[t - T0], 0, 0, 0);
-    }
+    const int dq = tt.dq[t], ds = tt.ds[t];
+    const int dr = tap_drow(dq, ds, P);
+    const int sh = floor_half(P + dq); // split-position shift: -1, 0 or 1
+    // aligned run start in window row (rrow + K + dr), parity (P + dq) & 1
+    const bf16raw *base = xb + j0 + ((rrow + K + dr) * 2 + ((P + dq) & 1)) * XS;
+    if (sh == 0)
+        return load_shifted<0>(base);
+    if (sh == 1)
+        return load_shifted<1>(base);
+    return load_shifted<-1>(base);
 }
 
-// All K-steps of column parity P for taps [T0, T1); the A fragment of step
-// q + 1 is read before the products of step q (two buffers, two steps per
-// iteration so that the buffers are named at compile time).
-template <int K, int P, int T0, int T1, int NA>
-__device__ __forceinline__ void wg_parity(floatx16 (&acc)[NA], float &dbs, bool do_db,
-                                          const bf16raw *__restrict__ dyb,
+// All K-steps of column parity P for taps [T0, T1): per K-step the products
+// tap by tap with the next tap's B fragment already requested, and the next
+// K-step's A fragments requested before the first product.
+template <int K, int P, int T0, int T1, int NCB, int TPG>
+__device__ __forceinline__ void wg_parity(floatx16 (&acc)[NCB][TPG], float (&dbs)[NCB],
+                                          bool do_db, const bf16raw *__restrict__ dyb, int dyblk,
                                           const bf16raw *__restrict__ xb, int WS, int XS, int rpr,
                                           const FastDiv &frpr, int nq, int kh)
 {
     if (nq <= 0)
         return;
+    WgA<P, NCB> cur;
+    cur.fetch(dyb, dyblk, WS, rpr, frpr, 0, kh);
     for (int q = 0; q < nq; ++q) {
-        WgA<P> a0;
-        a0.fetch(dyb, WS, rpr, frpr, q, kh);
-        wg_kstep<K, P, T0, T1, NA>(acc, a0, dbs, do_db, xb, XS);
+        WgA<P, NCB> nxt;
+        nxt.fetch(dyb, dyblk, WS, rpr, frpr, q + 1 < nq ? q + 1 : q, kh);
+        if (do_db) {
+#pragma unroll
+            for (int c = 0; c < NCB; ++c)
+#pragma unroll
+                for (int e = 0; e < 8; ++e)
+                    dbs[c] += static_cast<float>(cur.a[c][e]);
+        }
+        bf16x8 b = wg_loadB<K, P>(T0, xb, XS, cur.rrow, cur.j0);
+#pragma unroll
+        for (int t = T0; t < T1; ++t) {
+            bf16x8 bn = b;
+            if (t + 1 < T1)
+                bn = wg_loadB<K, P>(t + 1, xb, XS, cur.rrow, cur.j0);
+#pragma unroll
+            for (int c = 0; c < NCB; ++c)
+                acc[c][t - T0] =
+                    __builtin_amdgcn_mfma_f32_32x32x16_bf16(cur.a[c], b, acc[c][t - T0], 0, 0, 0);
+            b = bn;
+        }
+        cur = nxt;
     }
 }
 
 // Dispatch to the tap group g of this wave (wave-uniform), compile-time taps.
-template <int K, int TPG, int GI, int G>
-__device__ __forceinline__ void wg_tile(int g, floatx16 (&acc)[TPG], float &dbs, bool do_db,
-                                        const bf16raw *__restrict__ dyb,
+template <int K, int TPG, int NCB, int GI, int G>
+__device__ __forceinline__ void wg_tile(int g, floatx16 (&acc)[NCB][TPG], float (&dbs)[NCB],
+                                        bool do_db, const bf16raw *__restrict__ dyb, int dyblk,
                                         const bf16raw *__restrict__ xb, int WS, int XS, int rpr,
                                         const FastDiv &frpr, int nq, int kh)
 {
@@ -266,29 +285,31 @@ __device__ __forceinline__ void wg_tile(int g, floatx16 (&acc)[TPG], float &dbs,
         constexpr int T1 = (T0 + TPG < T) ? T0 + TPG : T;
         if (g == GI) {
             if constexpr (T1 > T0) {
-                wg_parity<K, 0, T0, T1, TPG>(acc, dbs, do_db, dyb, xb, WS, XS, rpr, frpr, nq, kh);
-                wg_parity<K, 1, T0, T1, TPG>(acc, dbs, do_db, dyb, xb, WS, XS, rpr, frpr, nq, kh);
+                wg_parity<K, 0, T0, T1, NCB, TPG>(acc, dbs, do_db, dyb, dyblk, xb, WS, XS, rpr,
+                                                  frpr, nq, kh);
+                wg_parity<K, 1, T0, T1, NCB, TPG>(acc, dbs, do_db, dyb, dyblk, xb, WS, XS, rpr,
+                                                  frpr, nq, kh);
             }
         } else {
-            wg_tile<K, TPG, GI + 1, G>(g, acc, dbs, do_db, dyb, xb, WS, XS, rpr, frpr, nq, kh);
+            wg_tile<K, TPG, NCB, GI + 1, G>(g, acc, dbs, do_db, dyb, dyblk, xb, WS, XS, rpr,
+                                            frpr, nq, kh);
         }
     }
 }
 
-template <int K, int G, int CW, int U>
-__global__ __launch_bounds__(kT) void wgrad32_k(const bf16raw *__restrict__ x,
-                                                const bf16raw *__restrict__ dy,
-                                                float *__restrict__ part, Wg32Args a)
+// Waves: NIB ci blocks x G = 4 / NIB tap groups; NCB co blocks per wave.
+template <int K, int NIB, int NCB, int CW, int U>
+__global__ __launch_bounds__(kT) __attribute__((amdgpu_waves_per_eu(1, 1))) void wgrad32_k(
+    const bf16raw *__restrict__ x, const bf16raw *__restrict__ dy, float *__restrict__ part,
+    Wg32Args a)
 {
     constexpr int T = num_taps(K);
+    constexpr int G = kWaves / NIB;
     constexpr int TPG = (T + G - 1) / G; // taps per group
     extern __shared__ __align__(16) bf16raw lds[];
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     const int n32 = lane & 31, kh = lane >> 5;
-    const int NIB = a.CI >> 5, NCB = a.CO >> 5;
-    const int C = NIB * NCB; // (ci block, co block) pairs; C * G == 8
-    const int combo = wave % C, g = wave / C;
-    const int ib = combo % NIB, cb = combo / NIB;
+    const int ib = wave % NIB, g = wave / NIB;
     const int t0 = g * TPG;
     const int slot = blockIdx.x;
 
@@ -299,18 +320,24 @@ __global__ __launch_bounds__(kT) void wgrad32_k(const bf16raw *__restrict__ x,
             reinterpret_cast<uint4 *>(lds)[e] = make_uint4(0, 0, 0, 0);
     }
 
-    floatx16 acc[TPG];
+    floatx16 acc[NCB][TPG];
 #pragma unroll
-    for (int i = 0; i < TPG; ++i)
+    for (int c = 0; c < NCB; ++c)
 #pragma unroll
-        for (int r = 0; r < 16; ++r)
-            acc[i][r] = 0.f;
-    float dbs = 0.f;
+        for (int i = 0; i < TPG; ++i)
+#pragma unroll
+            for (int r = 0; r < 16; ++r)
+                acc[c][i][r] = 0.f;
+    float dbs[NCB];
+#pragma unroll
+    for (int c = 0; c < NCB; ++c)
+        dbs[c] = 0.f;
     const bool do_db = (ib == 0 && g == 0);
 
     const int t_begin = slot * a.per_block;
     const int t_end = min(t_begin + a.per_block, a.ptiles);
-    const bf16raw *dyb = lds + (cb * 32 + n32) * a.dyc;
+    const bf16raw *dyb = lds + n32 * a.dyc;
+    const int dyblk = 32 * a.dyc; // next co block
     const bf16raw *xb = lds + a.x_off + (ib * 32 + n32) * a.xc + 8;
     const int rpr = a.WS >> 3; // runs per split row
 
@@ -330,26 +357,35 @@ __global__ __launch_bounds__(kT) void wgrad32_k(const bf16raw *__restrict__ x,
         // K-steps: pairs of runs of one parity; run i = (row i / rpr,
         // split position 8 * (i % rpr)); lanes kh = 0 / 1 take runs 2q / 2q+1
         const int nq = (a.TR * rpr) >> 1;
-        wg_tile<K, TPG, 0, G>(g, acc, dbs, do_db, dyb, xb, a.WS, a.XS, rpr, a.frpr, nq, kh);
+        wg_tile<K, TPG, NCB, 0, G>(g, acc, dbs, do_db, dyb, dyblk, xb, a.WS, a.XS, rpr, a.frpr,
+                                   nq, kh);
     }
 
     // partial slot of this block: tile (t, ib, cb) -> chunks (tile * 16 + r),
     // one 64-float chunk per accumulator register, lanes in order
     const int ntap = min(TPG, T - t0);
-    for (int i = 0; i < TPG; ++i) {
-        if (i >= ntap)
-            break;
-        const int tile = ((t0 + i) * NIB + ib) * NCB + cb;
 #pragma unroll
-        for (int r = 0; r < 16; ++r)
-            part[part_index(tile * 16 * kRegChunk + r * kRegChunk + lane, slot, a.nparts)] = acc[i][r];
+    for (int c = 0; c < NCB; ++c) {
+#pragma unroll
+        for (int i = 0; i < TPG; ++i) {
+            if (i < ntap) {
+                const int tile = ((t0 + i) * NIB + ib) * NCB + c;
+#pragma unroll
+                for (int r = 0; r < 16; ++r)
+                    part[part_index(tile * 16 * kRegChunk + r * kRegChunk + lane, slot,
+                                    a.nparts)] = acc[c][i][r];
+            }
+        }
     }
     if (do_db) {
-        // lanes n32 and n32 + 32 hold the same channel
-        const float s = dbs + __shfl_xor(dbs, 32, 64);
         const int base = T * NIB * NCB * 16 * kRegChunk; // db after the tiles
-        if (kh == 0)
-            part[part_index(base + cb * 32 + n32, slot, a.nparts)] = s;
+#pragma unroll
+        for (int c = 0; c < NCB; ++c) {
+            // lanes n32 and n32 + 32 hold the same channel
+            const float s = dbs[c] + __shfl_xor(dbs[c], 32, 64);
+            if (kh == 0)
+                part[part_index(base + c * 32 + n32, slot, a.nparts)] = s;
+        }
     }
 }
 
@@ -408,15 +444,29 @@ inline int cdiv(long a, long b) { return static_cast<int>((a + b - 1) / b); }
 
 constexpr size_t kLdsMax = 160 * 1024;
 
-// Most staging items per thread (prefetch registers) that each (K, tap
-// groups G, chunk width CW) variant holds without spilling next to its
-// accumulators (checked with the compiler's resource report); 0: the taps
-// per wave alone exceed the register budget.
-constexpr int max_items(int K, int G, int CW)
+// Most staging items per thread (prefetch registers: 16 or 8 bytes each)
+// that each (K, ci blocks, co blocks, chunk width) variant holds without
+// spilling next to its accumulators (the compiler's resource report).
+constexpr int max_items(int K, int NIB, int NCB, int CW)
 {
-    if (K == 1)
-        return G == 1 ? 0 : G == 2 ? 4 : G == 4 ? (CW == 8 ? 8 : 12) : 12;
-    return G <= 2 ? 0 : G == 4 ? 4 : 8;
+    if (K == 1) {
+        if (NIB == 1)
+            return NCB == 1 ? (CW == 8 ? 16 : 24) : 24;
+        if (NIB == 2)
+            return NCB == 1 ? 24 : (CW == 8 ? 8 : 16);
+        return 16;
+    }
+    if (NIB == 1)
+        return NCB == 1 ? (CW == 8 ? 16 : 24) : 8;
+    return 8;
+}
+
+// Most 32-channel co blocks per wave next to its taps' accumulators (each
+// block and tap one 16-register tile, at most 192 registers): k = 1 splits
+// 7 taps over 4 / NIB groups, k = 2 splits 19.  0: not supported.
+constexpr int max_ncb(int K, int NIB)
+{
+    return K == 1 ? (NIB <= 2 ? 2 : 1) : (NIB == 1 ? 2 : NIB == 2 ? 1 : 0);
 }
 
 // tiling of the pass over output channels co0 .. co0 + CO - 1 for a given
@@ -461,28 +511,13 @@ bool wg32_args(const ConvShape &sh, int co0, int CO, int TR, Wg32Args &a)
 
 int wg32_U(const Wg32Args &a) { return cdiv(a.items_x + a.items_dy, kT); }
 
-// Most (ci block, co block) pairs one pass holds: the waves of a pass split
-// the taps into 8 / pairs groups, and a group's accumulators must fit.
-int wg32_max_pairs(int k) { return k == 1 ? 4 : 2; }
-
-// Output channels per pass: as many 32-channel blocks as the pair limit
-// allows next to all input-channel blocks (0: the input channels alone are
-// too many).
-int wg32_pass_co(const ConvShape &sh)
-{
-    const int nib = sh.Ci / 32;
-    const int lim = wg32_max_pairs(sh.k);
-    if (nib > lim)
-        return 0;
-    return 32 * std::min(sh.Co / 32, lim / nib);
-}
-
 bool wg32_plan(const ConvShape &sh, int co0, int CO, Wg32Args &a)
 {
-    const int C = (sh.Ci / 32) * (CO / 32);
-    if (C != 1 && C != 2 && C != 4 && C != 8)
+    const int NIB = sh.Ci / 32, NCB = CO / 32;
+    const int C = NIB * NCB;
+    if (NCB > max_ncb(sh.k, NIB))
         return false;
-    const int umax = max_items(sh.k, 8 / C, (sh.W % 8 == 0) ? 8 : 4);
+    const int umax = max_items(sh.k, NIB, NCB, sh.W % 8 == 0 ? 8 : 4);
     // tallest tile (at most 512 pixels) that fits LDS and the staging registers
     for (int TR = std::min(sh.H, std::max(1, 512 / sh.W)); TR >= 1; --TR) {
         if (wg32_args(sh, co0, CO, TR, a) && wg32_U(a) <= umax) {
@@ -502,64 +537,80 @@ template <typename F> bool wg32_passes(const ConvShape &sh, F &&f)
     if (sh.s != 1 || (sh.k != 1 && sh.k != 2) || sh.Ci % 32 != 0 || sh.Co % 32 != 0 ||
         sh.W % 4 != 0)
         return false;
-    const int pco = wg32_pass_co(sh);
-    if (pco == 0)
+    const int nib = sh.Ci / 32;
+    if (nib != 1 && nib != 2 && nib != 4)
         return false;
     for (int co0 = 0; co0 < sh.Co;) {
-        // a power of two of 32-channel blocks, so the tap groups split evenly
-        int nb = std::min(pco, sh.Co - co0) / 32;
-        while (nb & (nb - 1))
-            nb &= nb - 1;
+        // two 32-channel co blocks per pass where a tile fits, else one
         Wg32Args a{};
-        if (!wg32_plan(sh, co0, 32 * nb, a) || !f(a))
+        int nb = std::min(max_ncb(sh.k, nib), (sh.Co - co0) / 32);
+        while (nb > 0 && !wg32_plan(sh, co0, 32 * nb, a))
+            --nb;
+        if (nb == 0 || !f(a))
             return false;
         co0 += 32 * nb;
     }
     return true;
 }
 
-template <int K, int G, int CW, int U>
-void launch_w32_u(const Wg32Args &a, size_t lds, hipStream_t st, const bf16raw *x,
-                  const bf16raw *dy, float *part)
-{
-    if constexpr (U <= max_items(K, G, CW))
-        HEX_LAUNCH((wgrad32_k<K, G, CW, U>), dim3(a.nparts), dim3(kT), lds, st, x, dy,
-                           part, a);
-}
-
-template <int K, int G, int CW>
+template <int K, int NIB, int NCB, int CW>
 void launch_w32_cw(int U, const Wg32Args &a, size_t lds, hipStream_t st, const bf16raw *x,
                    const bf16raw *dy, float *part)
 {
-    if (U <= 4)
-        launch_w32_u<K, G, CW, 4>(a, lds, st, x, dy, part);
-    else if (U <= 8)
-        launch_w32_u<K, G, CW, 8>(a, lds, st, x, dy, part);
-    else
-        launch_w32_u<K, G, CW, 12>(a, lds, st, x, dy, part);
+    if constexpr (NCB <= max_ncb(K, NIB)) {
+#define HEX_W32(UV)                                                                          \
+    HEX_LAUNCH((wgrad32_k<K, NIB, NCB, CW, UV>), dim3(a.nparts), dim3(kT), lds, st, x, dy,     \
+               part, a)
+        constexpr int UM = max_items(K, NIB, NCB, CW);
+        if (U <= 8) {
+            HEX_W32(8);
+        } else if (U <= 16) {
+            if constexpr (UM >= 16)
+                HEX_W32(16);
+        } else {
+            if constexpr (UM >= 24)
+                HEX_W32(24);
+        }
+#undef HEX_W32
+    }
+}
+
+template <int K, int NIB>
+void launch_w32_nib(int NCB, bool cw8, int U, const Wg32Args &a, size_t lds, hipStream_t st,
+                    const bf16raw *x, const bf16raw *dy, float *part)
+{
+    if (NCB == 1) {
+        if (cw8) launch_w32_cw<K, NIB, 1, 8>(U, a, lds, st, x, dy, part);
+        else launch_w32_cw<K, NIB, 1, 4>(U, a, lds, st, x, dy, part);
+    } else {
+        if (cw8) launch_w32_cw<K, NIB, 2, 8>(U, a, lds, st, x, dy, part);
+        else launch_w32_cw<K, NIB, 2, 4>(U, a, lds, st, x, dy, part);
+    }
 }
 
 template <int K>
-void launch_w32(int G, bool cw8, int U, const Wg32Args &a, size_t lds, hipStream_t st,
-                const bf16raw *x, const bf16raw *dy, float *part)
+void launch_w32(int NIB, int NCB, bool cw8, int U, const Wg32Args &a, size_t lds,
+                hipStream_t st, const bf16raw *x, const bf16raw *dy, float *part)
 {
-#define HEX_W32_G(GV)                                                                        \
-    do {                                                                                     \
-        if (cw8) launch_w32_cw<K, GV, 8>(U, a, lds, st, x, dy, part);                         \
-        else launch_w32_cw<K, GV, 4>(U, a, lds, st, x, dy, part);                             \
-    } while (0)
-    if (G == 1) HEX_W32_G(1);
-    else if (G == 2) HEX_W32_G(2);
-    else if (G == 4) HEX_W32_G(4);
-    else HEX_W32_G(8);
-#undef HEX_W32_G
+    if (NIB == 1)
+        launch_w32_nib<K, 1>(NCB, cw8, U, a, lds, st, x, dy, part);
+    else if (NIB == 2)
+        launch_w32_nib<K, 2>(NCB, cw8, U, a, lds, st, x, dy, part);
+    else
+        launch_w32_nib<K, 4>(NCB, cw8, U, a, lds, st, x, dy, part);
 }
 
 } // namespace
 
-bool bf16_wgrad32_ok(const ConvShape &sh)
+int bf16_wgrad32_passes(const ConvShape &sh)
 {
-    return wg32_passes(sh, [](const Wg32Args &) { return true; });
+    int n = 0;
+    if (!wg32_passes(sh, [&](const Wg32Args &) {
+            ++n;
+            return true;
+        }))
+        return 0;
+    return n;
 }
 
 // One partial buffer serves every pass: the passes run in stream order.
@@ -583,15 +634,15 @@ hipError_t bf16_wgrad32(const void *x, const void *dy, float *dw, float *db, voi
     float *part = static_cast<float *>(ws);
     hipError_t err = hipSuccess;
     const bool ok = wg32_passes(sh, [&](const Wg32Args &a) {
-        const int C = (sh.Ci / 32) * (a.CO / 32);
-        const int G = 8 / C;
+        const int NIB = sh.Ci / 32, NCB = a.CO / 32;
+        const int C = NIB * NCB;
         const int U = wg32_U(a);
         const bool cw8 = sh.W % 8 == 0;
         const size_t lds = 2ull * (a.x_off + static_cast<size_t>(sh.Ci) * a.xc);
         if (sh.k == 1)
-            launch_w32<1>(G, cw8, U, a, lds, st, xp, dp, part);
+            launch_w32<1>(NIB, NCB, cw8, U, a, lds, st, xp, dp, part);
         else
-            launch_w32<2>(G, cw8, U, a, lds, st, xp, dp, part);
+            launch_w32<2>(NIB, NCB, cw8, U, a, lds, st, xp, dp, part);
         err = hipGetLastError();
         if (err != hipSuccess)
             return false;

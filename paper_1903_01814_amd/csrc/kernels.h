@@ -112,7 +112,8 @@ hipError_t bf16_wide_conv(const void *in, const void *w, const void *bias, void 
                           const ConvShape &sh, bool reflect, bool relu, hipStream_t st);
 
 // ---- bf16 32x32 matrix-core weight gradient (C_in, C_out multiples of 32) --
-bool bf16_wgrad32_ok(const ConvShape &sh);
+// output-channel passes the kernel needs for this shape (0: not supported)
+int bf16_wgrad32_passes(const ConvShape &sh);
 size_t bf16_wgrad32_workspace(const ConvShape &sh);
 hipError_t bf16_wgrad32(const void *x, const void *dy, float *dw, float *db, void *ws,
                         const ConvShape &sh, hipStream_t st);

@@ -290,6 +290,8 @@ SWEEP = [
     # matrix-core weight gradient in several output-channel passes (128 + 64
     # + 32, 64 + 64 at k=2, 64 + 32 with two input-channel blocks)
     (1, 32, 224, 6, 16, 1, 1), (2, 32, 128, 7, 12, 2, 1), (1, 64, 96, 5, 20, 1, 1),
+    # four input-channel blocks per wave group at k = 1
+    (1, 128, 32, 6, 16, 1, 1),
 ]
 
 
