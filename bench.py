@@ -15,7 +15,9 @@ one untimed replay), so the time is GPU execution, not Python launch cost.  Each
 different batch from a rotating set whose total size exceeds the 256 MB
 Infinity Cache, so reads and writes go to HBM rather than staying cached.
 
-Other workloads print their own line on request: --config c3 (hex max and
+Other workloads print their own line on request: --config c1 (the tiny
+fp32 forward, N=4, 1 -> 4 channels, 16x16, k=1: launch-latency bound,
+reported in microseconds per call as us_per_step), c3 (hex max and
 average pooling, bf16, GB/s), c4 (wide-channel bf16 convolution, GFLOP/s)
 and c5 (the five-layer bf16 stack, forward and backward, samples/s).
 
@@ -169,13 +171,15 @@ def cpu_baseline_conv(cfg, d, k, s, seconds):
     H, W = cfg["H"], cfg["W"]
     Ho, Wo = oracle.out_shape(H, W, s)
     T = oracle.num_taps(k)
-    flop = 3 * conv_flop(cfg["N"], cfg["C_in"], cfg["C_out"], Ho, Wo, T)
+    has_bwd = "dy" in d
+    flop = (3 if has_bwd else 1) * conv_flop(cfg["N"], cfg["C_in"], cfg["C_out"], Ho, Wo, T)
     reps = 0
     t0 = time.perf_counter()
     while True:
         oracle.conv_fwd(d["x"], d["w"], d["b"], k, s)
-        oracle.conv_bwd_data(d["dy"], d["w"], k, s, H, W)
-        oracle.conv_bwd_weight(d["x"], d["dy"], k, s)
+        if has_bwd:
+            oracle.conv_bwd_data(d["dy"], d["w"], k, s, H, W)
+            oracle.conv_bwd_weight(d["x"], d["dy"], k, s)
         reps += 1
         el = time.perf_counter() - t0
         if el >= seconds:
@@ -191,12 +195,15 @@ def bench_conv(args, torch, cfg_key):
     dt = torch.float32 if cfg["dtype"] == gen.F32 else torch.bfloat16
     esz = 4 if dt == torch.float32 else 2
     per_set = esz * (N * Ci * H * W * 2 + N * Co * Ho * Wo * 2)
-    nsets = max(1, -(-ROTATE_MIN_BYTES // per_set))
+    # enough batches to exceed the Infinity Cache (a tiny launch-bound
+    # workload stops at 256)
+    nsets = min(256, max(1, -(-ROTATE_MIN_BYTES // per_set)))
     d0 = gen.conv_inputs(cfg, T, (Ho, Wo), seed=0)
     sets = []
     for b in range(nsets):
         d = d0 if b == 0 else gen.conv_inputs(cfg, T, (Ho, Wo), seed=b)
-        sets.append(dict(x=dev(torch, d["x"], dt), dy=dev(torch, d["dy"], dt),
+        sets.append(dict(x=dev(torch, d["x"], dt),
+                         dy=dev(torch, d["dy"], dt) if "dy" in d else None,
                          y=torch.empty((N, Co, Ho, Wo), dtype=dt, device="cuda:0"),
                          dx=torch.empty((N, Ci, H, W), dtype=dt, device="cuda:0")))
         if b == 0:
@@ -226,9 +233,12 @@ def bench_conv(args, torch, cfg_key):
         z = sets[i % nsets]
         hx.hexconv_bwd_weight(z["x"], z["dy"], dw, db, ws, k, s)
 
+    has_bwd = bool(cfg.get("bwd"))
+
     def step(i):
         fwd(i)
-        bwd(i)
+        if has_bwd:
+            bwd(i)
 
     timer = EagerTimer(torch) if args.eager else GraphTimer(torch)
     for i in range(args.warmup):
@@ -238,7 +248,7 @@ def bench_conv(args, torch, cfg_key):
 
     # per-op durations, each op alone over the same rotation (HIP events on
     # the launch stream); the step uses fwd and bwd, the separate gradient
-    # entry points are timed for reference
+    # entry points are timed for reference (forward-only workloads: fwd)
     ops = {}
     x_b, y_b = esz * N * Ci * H * W, esz * N * Co * Ho * Wo
     w_b, b_b, g_b = esz * Co * Ci * T, esz * Co, 4 * (Co * Ci * T + Co)
@@ -249,18 +259,19 @@ def bench_conv(args, torch, cfg_key):
         "bwd_weight": x_b + y_b + g_b,
     }
     nprod = {"fwd": 1, "bwd": 2, "bwd_data": 1, "bwd_weight": 1}
-    for name, fn in (("fwd", fwd), ("bwd", bwd), ("bwd_data", bwd_data),
-                     ("bwd_weight", bwd_weight)):
+    op_list = (("fwd", fwd), ("bwd", bwd), ("bwd_data", bwd_data),
+               ("bwd_weight", bwd_weight)) if has_bwd else (("fwd", fwd),)
+    for name, fn in op_list:
         ms = timer.time(fn, args.steps)
         ops[name] = dict(ms=ms, gbs=bytes_alg[name] / (ms * 1e-3) / 1e9)
     flop_op = conv_flop(N, Ci, Co, Ho, Wo, T)
-    flop_step = 3 * flop_op
+    flop_step = (3 if has_bwd else 1) * flop_op
     value = flop_step / (ms_step * 1e-3) / 1e9
 
     # the dominant op of the step, and within it the kernel with the most
     # GPU time, against its roofline: the op's algorithmic bytes (or
     # products) per launch of that kernel over its measured duration
-    dom = max(("fwd", "bwd"), key=lambda n: ops[n]["ms"])
+    dom = max(("fwd", "bwd") if has_bwd else ("fwd",), key=lambda n: ops[n]["ms"])
     fn_dom = fwd if dom == "fwd" else bwd
     kname, kms, kper, kall = dominant_kernel(torch, fn_dom, args.steps)
     bound = "hbm" if cfg["dtype"] == gen.F32 or Ci * T < 64 else "mfma"
@@ -279,13 +290,15 @@ def bench_conv(args, torch, cfg_key):
                 alg_per_launch=units, op_kernels_ms=kall)
 
     out = dict(
-        metric="hex-conv effective GFLOP/s (fwd+bwd)", value=round(value, 2), unit="GFLOP/s",
+        metric="hex-conv effective GFLOP/s (%s)" % ("fwd+bwd" if has_bwd else "fwd"),
+        value=round(value, 2), unit="GFLOP/s",
         n_gpus=1, steps=args.steps, warmup=args.warmup, ms_per_step=round(ms_step, 5),
         higher_is_better=True, scaling="weak", vs_baseline=None,
         dtype="f32" if esz == 4 else "bf16", data="synthetic",
         config=dict(workload=cfg["name"], N=N, C_in=Ci, C_out=Co, H=H, W=W, k=k, stride=s,
                     taps=T, H_out=Ho, W_out=Wo, rotating_batches=nsets),
         samples_per_s=round(N / (ms_step * 1e-3), 1),
+        us_per_step=round(ms_step * 1e3, 3),
         per_op={n: dict(ms=round(v["ms"], 5), alg_GBps=round(v["gbs"], 1),
                         GFLOPs=round(nprod[n] * flop_op / (v["ms"] * 1e-3) / 1e9, 1))
                 for n, v in ops.items()},
@@ -296,8 +309,8 @@ def bench_conv(args, torch, cfg_key):
         gfs, thr, reps, el = cpu_baseline_conv(cfg, d, k, s, args.cpu_seconds)
         out["cpu_baseline"] = dict(
             value=round(gfs, 3), unit="GFLOP/s", cores=thr, kind="oracle",
-            sample="full batch (N=%d) fwd+bwd_data+bwd_weight, fp64, repeated %d times in %.1f s"
-                   % (N, reps, el))
+            sample="full batch (N=%d) %s, fp64, repeated %d times in %.1f s"
+                   % (N, "fwd+bwd_data+bwd_weight" if has_bwd else "fwd", reps, el))
     return out
 
 
@@ -583,7 +596,7 @@ def main():
     p.add_argument("--gpus", type=int, default=1)
     p.add_argument("--steps", type=int, default=500)
     p.add_argument("--warmup", type=int, default=20)
-    p.add_argument("--config", default="c2", choices=["c2", "c3", "c4", "c5"])
+    p.add_argument("--config", default="c2", choices=["c1", "c2", "c3", "c4", "c5"])
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--eager", action="store_true",
                    help="launch eagerly instead of replaying a HIP graph (for counter runs)")
