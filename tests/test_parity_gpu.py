@@ -249,6 +249,12 @@ def test_c5_stack_teacher_forced():
             check_bf16(db, g.sum(axis=(0, 2, 3)), np.abs(g).sum(axis=(0, 2, 3)),
                        "c5 L%d db" % li)
             if li == 0:
+                # the first layer as a network runs it: the combined entry
+                # point without dx (fused small-channel kernel in bf16)
+                _, dw2, db2 = run_bwd(a, g, p["w"], k, s, "bf16", want_dx=False)
+                check_bf16(dw2.reshape(-1)[widx], ref, mag, "c5 L0 combined dw")
+                check_bf16(db2, g.sum(axis=(0, 2, 3)), np.abs(g).sum(axis=(0, 2, 3)),
+                           "c5 L0 combined db")
                 break                    # no gradient for the input image
             dx = run_bwd_data(g, p["w"], k, s, Hin, Win, "bf16")
             idx = sample_indices(dx.shape, 2000, rng)
@@ -349,14 +355,18 @@ def test_pool_sweep(case, mode, dt):
         check(dt, dx, rdx, mag, "pool bwd")
 
 
-def test_bwd_without_dx():
+@pytest.mark.parametrize("dt", ["f32", "bf16"])
+def test_bwd_without_dx(dt):
     """hexconv_bwd with dx = NULL (a first layer) still gives dw and db."""
     cfg = CFG["c2"]
     d = _conv_inputs(cfg, N=24)
-    _, dw, db = run_bwd(d["x"], d["dy"], d["w"], cfg["k"], 1, "f32", want_dx=False)
-    rw, rb = oracle.conv_bwd_weight(d["x"], d["dy"], cfg["k"], 1)
-    check_f32(dw, rw, "dw")
-    check_f32(db, rb, "db")
+    x, dy = gen.round_to(d["x"], dt), gen.round_to(d["dy"], dt)
+    w = gen.round_to(d["w"], dt)
+    _, dw, db = run_bwd(x, dy, w, cfg["k"], 1, dt, want_dx=False)
+    rw, rb = oracle.conv_bwd_weight(x, dy, cfg["k"], 1)
+    mw, mb = oracle.conv_bwd_weight(np.abs(x), np.abs(dy), cfg["k"], 1)
+    check(dt, dw, rw, mw, "dw")
+    check(dt, db, rb, mb, "db")
 
 
 def test_debug_mode_golden():
