@@ -52,8 +52,9 @@ using namespace hexgeom;
 typedef float floatx16 __attribute__((ext_vector_type(16)));
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 
-constexpr int kT = 256; // threads per block (4 waves, one per SIMD)
-constexpr int kWaves = kT / 64;
+constexpr int kP = 256;      // producer threads: waves 4..7 stage the next tile
+constexpr int kT = 2 * kP;   // threads per block: waves 0..3 compute, 4..7 stage
+constexpr int kWaves = 4;    // computing waves, one per SIMD
 constexpr int kRegChunk = 64; // floats per partial chunk (one register of a wave)
 
 struct Wg32Args {
@@ -86,6 +87,16 @@ __device__ __forceinline__ uint32_t align2(uint32_t hi, uint32_t lo)
     return __builtin_amdgcn_alignbyte(hi, lo, 2); // (hi:lo) >> 16
 }
 
+// The thread index behind an empty asm: an item's address arithmetic is
+// then redone at every tile instead of being hoisted out of the tile loop,
+// where it would hold about eight registers per item for the whole kernel.
+__device__ __forceinline__ int opaque_tid()
+{
+    int t = threadIdx.x;
+    asm volatile("" : "+v"(t));
+    return t;
+}
+
 // Staged window of one pixel tile: rows r0 - K .. r0 + TR + K - 1 of x and
 // rows r0 .. r0 + TR - 1 of dy; rows outside the image or past the tile end
 // (dy) are zero.  Item: one CW-column chunk of one row of one channel.
@@ -104,10 +115,11 @@ template <int K, int CW, int U> struct Wg32Regs {
         const size_t HW = static_cast<size_t>(a.H) * a.W;
         const int XR = a.TR + 2 * K;
         const int total = a.items_x + a.items_dy;
+        const int tid = opaque_tid() - kP;
         okm = 0;
 #pragma unroll
         for (int u = 0; u < U; ++u) {
-            const int it0 = threadIdx.x + u * kT;
+            const int it0 = tid + u * kP;
             const int it = it0 < total ? it0 : 0;
             int ch, c, r;
             bool ok;
@@ -142,9 +154,10 @@ template <int K, int CW, int U> struct Wg32Regs {
         const int XR = a.TR + 2 * K;
         const int total = a.items_x + a.items_dy;
         constexpr uint32_t E = 0x05040100u, O = 0x07060302u;
+        const int tid = opaque_tid() - kP;
 #pragma unroll
         for (int u = 0; u < U; ++u) {
-            const int it = threadIdx.x + u * kT;
+            const int it = tid + u * kP;
             if (it >= total)
                 continue;
             int c, off0, off1;
@@ -233,20 +246,26 @@ __device__ __forceinline__ bf16x8 wg_loadB(int t, const bf16raw *__restrict__ xb
     return load_shifted<-1>(base);
 }
 
-// All K-steps of column parity P for taps [T0, T1): per K-step the products
-// tap by tap with the next tap's B fragment already requested, and the next
-// K-step's A fragments requested before the first product.
+// All K-steps of column parity P for taps [T0, T1).  The A fragments of
+// the next K-step are requested first; then, tap by tap, the products of
+// this K-step and the request for that tap's B fragment of the next
+// K-step, so each fragment has the rest of a K-step's products to arrive.
 template <int K, int P, int T0, int T1, int NCB, int TPG>
 __device__ __forceinline__ void wg_parity(floatx16 (&acc)[NCB][TPG], float (&dbs)[NCB],
                                           bool do_db, const bf16raw *__restrict__ dyb, int dyblk,
                                           const bf16raw *__restrict__ xb, int WS, int XS, int rpr,
                                           const FastDiv &frpr, int nq, int kh)
 {
-    if (nq <= 0)
-        return;
+    // nq >= 1: a tile holds at least one K-step (the planner pairs runs)
+    constexpr int NT = T1 - T0;
     WgA<P, NCB> cur;
     cur.fetch(dyb, dyblk, WS, rpr, frpr, 0, kh);
-    for (int q = 0; q < nq; ++q) {
+    bf16x8 b[NT];
+#pragma unroll
+    for (int t = 0; t < NT; ++t)
+        b[t] = wg_loadB<K, P>(T0 + t, xb, XS, cur.rrow, cur.j0);
+    int q = 0;
+    do {
         WgA<P, NCB> nxt;
         nxt.fetch(dyb, dyblk, WS, rpr, frpr, q + 1 < nq ? q + 1 : q, kh);
         if (do_db) {
@@ -256,69 +275,31 @@ __device__ __forceinline__ void wg_parity(floatx16 (&acc)[NCB][TPG], float (&dbs
                 for (int e = 0; e < 8; ++e)
                     dbs[c] += static_cast<float>(cur.a[c][e]);
         }
-        bf16x8 b = wg_loadB<K, P>(T0, xb, XS, cur.rrow, cur.j0);
 #pragma unroll
-        for (int t = T0; t < T1; ++t) {
-            bf16x8 bn = b;
-            if (t + 1 < T1)
-                bn = wg_loadB<K, P>(t + 1, xb, XS, cur.rrow, cur.j0);
+        for (int t = 0; t < NT; ++t) {
 #pragma unroll
             for (int c = 0; c < NCB; ++c)
-                acc[c][t - T0] =
-                    __builtin_amdgcn_mfma_f32_32x32x16_bf16(cur.a[c], b, acc[c][t - T0], 0, 0, 0);
-            b = bn;
+                acc[c][t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(cur.a[c], b[t], acc[c][t], 0, 0, 0);
+            b[t] = wg_loadB<K, P>(T0 + t, xb, XS, nxt.rrow, nxt.j0);
         }
         cur = nxt;
-    }
+    } while (++q < nq);
 }
 
-// Dispatch to the tap group g of this wave (wave-uniform), compile-time taps.
-template <int K, int TPG, int NCB, int GI, int G>
-__device__ __forceinline__ void wg_tile(int g, floatx16 (&acc)[NCB][TPG], float (&dbs)[NCB],
-                                        bool do_db, const bf16raw *__restrict__ dyb, int dyblk,
-                                        const bf16raw *__restrict__ xb, int WS, int XS, int rpr,
-                                        const FastDiv &frpr, int nq, int kh)
-{
-    if constexpr (GI < G) {
-        constexpr int T = num_taps(K);
-        constexpr int T0 = GI * TPG;
-        constexpr int T1 = (T0 + TPG < T) ? T0 + TPG : T;
-        if (g == GI) {
-            if constexpr (T1 > T0) {
-                wg_parity<K, 0, T0, T1, NCB, TPG>(acc, dbs, do_db, dyb, dyblk, xb, WS, XS, rpr,
-                                                  frpr, nq, kh);
-                wg_parity<K, 1, T0, T1, NCB, TPG>(acc, dbs, do_db, dyb, dyblk, xb, WS, XS, rpr,
-                                                  frpr, nq, kh);
-            }
-        } else {
-            wg_tile<K, TPG, NCB, GI + 1, G>(g, acc, dbs, do_db, dyb, dyblk, xb, WS, XS, rpr,
-                                            frpr, nq, kh);
-        }
-    }
-}
-
-// Waves: NIB ci blocks x G = 4 / NIB tap groups; NCB co blocks per wave.
-template <int K, int NIB, int NCB, int CW, int U>
-__global__ __launch_bounds__(kT) __attribute__((amdgpu_waves_per_eu(1, 1))) void wgrad32_k(
-    const bf16raw *__restrict__ x, const bf16raw *__restrict__ dy, float *__restrict__ part,
-    Wg32Args a)
+// A computing wave of ci block ib and tap group GI (taps T0 .. T1 - 1) over
+// the block's run of tiles: both barriers of every tile, the products of
+// both column parities, then its accumulators to the block's partial slot.
+// One instantiation per group keeps each group's registers its own.
+template <int K, int NIB, int NCB, int TPG, int GI>
+__device__ __forceinline__ void wg_consume(const bf16raw *__restrict__ lds, float *__restrict__ part,
+                                           const Wg32Args &a, int ib, int t_begin, int t_end)
 {
     constexpr int T = num_taps(K);
-    constexpr int G = kWaves / NIB;
-    constexpr int TPG = (T + G - 1) / G; // taps per group
-    extern __shared__ __align__(16) bf16raw lds[];
-    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-    const int n32 = lane & 31, kh = lane >> 5;
-    const int ib = wave % NIB, g = wave / NIB;
-    const int t0 = g * TPG;
+    constexpr int T0 = GI * TPG;
+    constexpr int T1 = (T0 + TPG < T) ? T0 + TPG : T;
+    constexpr int NT = T1 > T0 ? T1 - T0 : 0;
+    const int lane = threadIdx.x & 63, n32 = lane & 31, kh = lane >> 5;
     const int slot = blockIdx.x;
-
-    // zero the whole LDS once: pads and unused split positions stay zero
-    {
-        const int total = (a.x_off + a.CI * a.xc) / 8;
-        for (int e = threadIdx.x; e < total; e += kT)
-            reinterpret_cast<uint4 *>(lds)[e] = make_uint4(0, 0, 0, 0);
-    }
 
     floatx16 acc[NCB][TPG];
 #pragma unroll
@@ -332,49 +313,36 @@ __global__ __launch_bounds__(kT) __attribute__((amdgpu_waves_per_eu(1, 1))) void
 #pragma unroll
     for (int c = 0; c < NCB; ++c)
         dbs[c] = 0.f;
-    const bool do_db = (ib == 0 && g == 0);
-
-    const int t_begin = slot * a.per_block;
-    const int t_end = min(t_begin + a.per_block, a.ptiles);
+    const bool do_db = ib == 0 && GI == 0;
     const bf16raw *dyb = lds + n32 * a.dyc;
     const int dyblk = 32 * a.dyc; // next co block
     const bf16raw *xb = lds + a.x_off + (ib * 32 + n32) * a.xc + 8;
     const int rpr = a.WS >> 3; // runs per split row
-
-    Wg32Regs<K, CW, U> regs;
-    if (t_begin < t_end) {
-        const int n = t_begin / a.ntr, r0 = (t_begin - n * a.ntr) * a.TR;
-        regs.load(x, dy, a, n, r0, min(a.TR, a.H - r0));
-    }
+    // K-steps: pairs of runs of one parity; run i = (row i / rpr, split
+    // position 8 * (i % rpr)); lanes kh = 0 / 1 take runs 2q / 2q + 1
+    const int nq = (a.TR * rpr) >> 1;
     for (int pt = t_begin; pt < t_end; ++pt) {
-        __syncthreads(); // previous tile's reads done (and the LDS clear)
-        regs.commit(lds, a);
         __syncthreads();
-        if (pt + 1 < t_end) {
-            const int n = (pt + 1) / a.ntr, r0 = (pt + 1 - n * a.ntr) * a.TR;
-            regs.load(x, dy, a, n, r0, min(a.TR, a.H - r0));
+        __syncthreads(); // tile pt is in LDS
+        if constexpr (NT > 0) {
+            wg_parity<K, 0, T0, T1, NCB, TPG>(acc, dbs, do_db, dyb, dyblk, xb, a.WS, a.XS, rpr,
+                                              a.frpr, nq, kh);
+            wg_parity<K, 1, T0, T1, NCB, TPG>(acc, dbs, do_db, dyb, dyblk, xb, a.WS, a.XS, rpr,
+                                              a.frpr, nq, kh);
         }
-        // K-steps: pairs of runs of one parity; run i = (row i / rpr,
-        // split position 8 * (i % rpr)); lanes kh = 0 / 1 take runs 2q / 2q+1
-        const int nq = (a.TR * rpr) >> 1;
-        wg_tile<K, TPG, NCB, 0, G>(g, acc, dbs, do_db, dyb, dyblk, xb, a.WS, a.XS, rpr, a.frpr,
-                                   nq, kh);
     }
 
     // partial slot of this block: tile (t, ib, cb) -> chunks (tile * 16 + r),
     // one 64-float chunk per accumulator register, lanes in order
-    const int ntap = min(TPG, T - t0);
 #pragma unroll
     for (int c = 0; c < NCB; ++c) {
 #pragma unroll
-        for (int i = 0; i < TPG; ++i) {
-            if (i < ntap) {
-                const int tile = ((t0 + i) * NIB + ib) * NCB + c;
+        for (int i = 0; i < NT; ++i) {
+            const int tile = ((T0 + i) * NIB + ib) * NCB + c;
 #pragma unroll
-                for (int r = 0; r < 16; ++r)
-                    part[part_index(tile * 16 * kRegChunk + r * kRegChunk + lane, slot,
-                                    a.nparts)] = acc[c][i][r];
-            }
+            for (int r = 0; r < 16; ++r)
+                part[part_index(tile * 16 * kRegChunk + r * kRegChunk + lane, slot, a.nparts)] =
+                    acc[c][i][r];
         }
     }
     if (do_db) {
@@ -387,6 +355,70 @@ __global__ __launch_bounds__(kT) __attribute__((amdgpu_waves_per_eu(1, 1))) void
                 part[part_index(base + c * 32 + n32, slot, a.nparts)] = s;
         }
     }
+}
+
+template <int K, int NIB, int NCB, int TPG, int GI, int G>
+__device__ __forceinline__ void wg_consume_group(int g, const bf16raw *__restrict__ lds,
+                                                 float *__restrict__ part, const Wg32Args &a,
+                                                 int ib, int t_begin, int t_end)
+{
+    if constexpr (GI < G) {
+        if (g == GI)
+            wg_consume<K, NIB, NCB, TPG, GI>(lds, part, a, ib, t_begin, t_end);
+        else
+            wg_consume_group<K, NIB, NCB, TPG, GI + 1, G>(g, lds, part, a, ib, t_begin, t_end);
+    }
+}
+
+// Waves: NIB ci blocks x G = 4 / NIB tap groups; NCB co blocks per wave.
+template <int K, int NIB, int NCB, int CW, int U>
+__global__ __launch_bounds__(kT) __attribute__((amdgpu_waves_per_eu(2, 2))) void wgrad32_k(
+    const bf16raw *__restrict__ x, const bf16raw *__restrict__ dy, float *__restrict__ part,
+    Wg32Args a)
+{
+    constexpr int T = num_taps(K);
+    constexpr int G = kWaves / NIB;
+    constexpr int TPG = (T + G - 1) / G; // taps per group
+    extern __shared__ __align__(16) bf16raw lds[];
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const bool producer = wave >= kWaves;
+    const int ib = wave % NIB, g = wave / NIB;
+    const int slot = blockIdx.x;
+
+    // zero the whole LDS once: pads and unused split positions stay zero
+    {
+        const int total = (a.x_off + a.CI * a.xc) / 8;
+        for (int e = threadIdx.x; e < total; e += kT)
+            reinterpret_cast<uint4 *>(lds)[e] = make_uint4(0, 0, 0, 0);
+    }
+
+    const int t_begin = slot * a.per_block;
+    const int t_end = min(t_begin + a.per_block, a.ptiles);
+
+    // Staging waves: hold the next tile in registers while the computing
+    // waves work on the current one from LDS, and write it to LDS between
+    // the two barriers of every tile.  Both kinds of wave pass the same
+    // barriers; the two loops keep the staging registers and the
+    // accumulators out of each other's way.
+    if (producer) {
+        Wg32Regs<K, CW, U> regs;
+        if (t_begin < t_end) {
+            const int n = t_begin / a.ntr, r0 = (t_begin - n * a.ntr) * a.TR;
+            regs.load(x, dy, a, n, r0, min(a.TR, a.H - r0));
+        }
+        for (int pt = t_begin; pt < t_end; ++pt) {
+            __syncthreads(); // previous tile's reads done (and the LDS clear)
+            regs.commit(lds, a);
+            __syncthreads();
+            if (pt + 1 < t_end) {
+                const int n = (pt + 1) / a.ntr, r0 = (pt + 1 - n * a.ntr) * a.TR;
+                regs.load(x, dy, a, n, r0, min(a.TR, a.H - r0));
+            }
+        }
+        return;
+    }
+
+    wg_consume_group<K, NIB, NCB, TPG, 0, G>(g, lds, part, a, ib, t_begin, t_end);
 }
 
 // Sum the slots of every partial position in a fixed order and scatter to
@@ -444,22 +476,10 @@ inline int cdiv(long a, long b) { return static_cast<int>((a + b - 1) / b); }
 
 constexpr size_t kLdsMax = 160 * 1024;
 
-// Most staging items per thread (prefetch registers: 16 or 8 bytes each)
-// that each (K, ci blocks, co blocks, chunk width) variant holds without
-// spilling next to its accumulators (the compiler's resource report).
-constexpr int max_items(int K, int NIB, int NCB, int CW)
-{
-    if (K == 1) {
-        if (NIB == 1)
-            return NCB == 1 ? (CW == 8 ? 16 : 24) : 24;
-        if (NIB == 2)
-            return NCB == 1 ? 24 : (CW == 8 ? 8 : 16);
-        return 16;
-    }
-    if (NIB == 1)
-        return NCB == 1 ? (CW == 8 ? 16 : 24) : 8;
-    return 8;
-}
+// Most staging items per thread (prefetch registers: 16 or 8 bytes each);
+// every variant holds 32 next to its accumulators without scratch spills
+// (the compiler's resource report).
+constexpr int kMaxItems = 32;
 
 // Most 32-channel co blocks per wave next to its taps' accumulators (each
 // block and tap one 16-register tile, at most 192 registers): k = 1 splits
@@ -509,7 +529,7 @@ bool wg32_args(const ConvShape &sh, int co0, int CO, int TR, Wg32Args &a)
     return true;
 }
 
-int wg32_U(const Wg32Args &a) { return cdiv(a.items_x + a.items_dy, kT); }
+int wg32_U(const Wg32Args &a) { return cdiv(a.items_x + a.items_dy, kP); }
 
 bool wg32_plan(const ConvShape &sh, int co0, int CO, Wg32Args &a)
 {
@@ -517,18 +537,30 @@ bool wg32_plan(const ConvShape &sh, int co0, int CO, Wg32Args &a)
     const int C = NIB * NCB;
     if (NCB > max_ncb(sh.k, NIB))
         return false;
-    const int umax = max_items(sh.k, NIB, NCB, sh.W % 8 == 0 ? 8 : 4);
-    // tallest tile (at most 512 pixels) that fits LDS and the staging registers
+    // Tile height (at most 512 pixels a tile) that fits LDS and the staging
+    // registers and stages the fewest rows per image: x rows with their
+    // halo plus dy rows, over all tiles of the image (rows past the image
+    // are computed but not real, so a ragged last tile costs a whole one);
+    // ties go to the taller tile.
+    int best = 0;
+    long best_rows = 0;
     for (int TR = std::min(sh.H, std::max(1, 512 / sh.W)); TR >= 1; --TR) {
-        if (wg32_args(sh, co0, CO, TR, a) && wg32_U(a) <= umax) {
-            const int blocks = std::max(1, std::min(device_cus(), a.ptiles));
-            a.per_block = cdiv(a.ptiles, blocks);
-            a.nparts = cdiv(a.ptiles, a.per_block);
-            a.nchunk = sh.T * C * 16 + cdiv(CO, kRegChunk);
-            return true;
+        if (!wg32_args(sh, co0, CO, TR, a) || wg32_U(a) > kMaxItems)
+            continue;
+        const long rows = static_cast<long>(a.ntr) *
+                          (static_cast<long>(TR + 2 * sh.k) * sh.Ci + static_cast<long>(TR) * CO);
+        if (best == 0 || rows < best_rows) {
+            best = TR;
+            best_rows = rows;
         }
     }
-    return false;
+    if (best == 0 || !wg32_args(sh, co0, CO, best, a))
+        return false;
+    const int blocks = std::max(1, std::min(device_cus(), a.ptiles));
+    a.per_block = cdiv(a.ptiles, blocks);
+    a.nparts = cdiv(a.ptiles, a.per_block);
+    a.nchunk = sh.T * C * 16 + cdiv(CO, kRegChunk);
+    return true;
 }
 
 // Calls f(co0, CO, args) for every pass; false if some pass has no plan.
@@ -561,16 +593,15 @@ void launch_w32_cw(int U, const Wg32Args &a, size_t lds, hipStream_t st, const b
 #define HEX_W32(UV)                                                                          \
     HEX_LAUNCH((wgrad32_k<K, NIB, NCB, CW, UV>), dim3(a.nparts), dim3(kT), lds, st, x, dy,     \
                part, a)
-        constexpr int UM = max_items(K, NIB, NCB, CW);
-        if (U <= 8) {
+        static_assert(kMaxItems == 32, "staging variants: 8, 16, 24, 32 items");
+        if (U <= 8)
             HEX_W32(8);
-        } else if (U <= 16) {
-            if constexpr (UM >= 16)
-                HEX_W32(16);
-        } else {
-            if constexpr (UM >= 24)
-                HEX_W32(24);
-        }
+        else if (U <= 16)
+            HEX_W32(16);
+        else if (U <= 24)
+            HEX_W32(24);
+        else
+            HEX_W32(32);
 #undef HEX_W32
     }
 }
