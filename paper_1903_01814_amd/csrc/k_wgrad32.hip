@@ -56,6 +56,7 @@ constexpr int kP = 256;      // producer threads: waves 4..7 stage the next tile
 constexpr int kT = 2 * kP;   // threads per block: waves 0..3 compute, 4..7 stage
 constexpr int kWaves = 4;    // computing waves, one per SIMD
 constexpr int kRegChunk = 64; // floats per partial chunk (one register of a wave)
+constexpr int kMaxRounds = 32; // staging items per thread at most
 
 struct Wg32Args {
     int N, H, W, CI, CO;
@@ -71,6 +72,9 @@ struct Wg32Args {
     int items_x, items_dy; // staging items of a full tile
     int cpr;       // staging chunks per image row
     FastDiv fcpr, fxr, ftr, frpr; // division by cpr, TR + 2K, TR, runs per split row
+    // regular staging (Wg32RegsR): channel blocks per row (0: general
+    // staging), channels per round, log2 of the chunks per row
+    int rg, rpu, lcpr;
 };
 
 __device__ __forceinline__ int udiv(int n, const FastDiv &f)
@@ -191,23 +195,122 @@ template <int K, int CW, int U> struct Wg32Regs {
     }
 };
 
-// B fragment: the 8 split elements starting S (-1, 0, 1) positions after the
-// 16-byte aligned element p.
-template <int S> __device__ __forceinline__ bf16x8 load_shifted(const bf16raw *__restrict__ p)
-{
-    if constexpr (S == 0) {
-        return *reinterpret_cast<const bf16x8 *>(p);
-    } else if constexpr (S == 1) {
-        const uint4 c0 = *reinterpret_cast<const uint4 *>(p);
-        const uint32_t c1 = *reinterpret_cast<const uint32_t *>(p + 8);
-        return __builtin_bit_cast(bf16x8, make_uint4(align2(c0.y, c0.x), align2(c0.z, c0.y),
-                                                     align2(c0.w, c0.z), align2(c1, c0.w)));
-    } else {
-        const uint4 c0 = *reinterpret_cast<const uint4 *>(p);
-        const uint32_t cm = *reinterpret_cast<const uint32_t *>(p - 2);
-        return __builtin_bit_cast(bf16x8, make_uint4(align2(c0.x, cm), align2(c0.y, c0.x),
-                                                     align2(c0.z, c0.y), align2(c0.w, c0.z)));
+// Regular staging, for 16-byte chunks where the chunks per row (cpr, a
+// power of two) divide the staging threads and both channel counts (x and
+// this pass's dy) are G times rpu = kP / cpr.  Thread tid stages chunk
+// tid % cpr of channel tid / cpr (relative) in every round; round u covers
+// rpu channels of one row: x window row u / G, channels (u % G) * rpu, for
+// u < rx = (TR + 2K) G, then dy row u / G - (TR + 2K).  Where a round reads
+// and writes is then the same for the whole block and a compile-time
+// multiple of a few strides: per item one load, and at the commit one
+// address add, four permutes and two LDS writes.
+template <int K, int U, int G> struct Wg32RegsR {
+    uint4 v[U];
+    uint32_t okm; // bit u: round u holds image data (the same for all threads)
+
+    __device__ __forceinline__ void load(const bf16raw *__restrict__ x,
+                                         const bf16raw *__restrict__ dy, const Wg32Args &a,
+                                         int n, int r0, int rows)
+    {
+        const size_t HW = static_cast<size_t>(a.H) * a.W;
+        const int tid = static_cast<int>(threadIdx.x) - kP;
+        const uint32_t voff = static_cast<uint32_t>((tid >> a.lcpr) * HW +
+                                                    (tid & ((1 << a.lcpr) - 1)) * 8);
+        const int XR = a.TR + 2 * K, rx = XR * G, rt = rx + a.TR * G;
+        const int RH = a.rpu * a.H * a.W; // elements between the channel blocks of a row
+        const bf16raw *xn = x + static_cast<size_t>(n) * a.CI * HW;
+        const bf16raw *xw = xn + static_cast<ptrdiff_t>(r0 - K) * a.W;
+        // dy round u reads row u / G - XR: the base takes XR rows off
+        const bf16raw *yw = dy + (static_cast<size_t>(n) * a.COT + a.co0) * HW +
+                            static_cast<ptrdiff_t>(r0 - XR) * a.W;
+        // rounds in the image: x rows lo .. hi - 1 of the window, dy rows
+        // below the tile's end
+        const int lo = max(0, K - r0), hi = min(XR, a.H - r0 + K);
+        uint32_t m = 0;
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            const int rr = u / G;
+            const bool ok = u < rx ? (rr >= lo && rr < hi) : (u < rt && rr - XR < rows);
+            m |= ok ? (1u << u) : 0u;
+        }
+        okm = __builtin_amdgcn_readfirstlane(m);
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            const int ro = (u / G) * a.W + (u % G) * RH; // offset from the base
+            const bf16raw *src = ((okm >> u) & 1u) ? (u < rx ? xw : yw) + ro : xn;
+            v[u] = *reinterpret_cast<const uint4 *>(src + voff);
+        }
     }
+
+    // even columns of the chunk to parity 0, odd to parity 1
+    __device__ __forceinline__ void commit(bf16raw *__restrict__ lds, const Wg32Args &a) const
+    {
+        constexpr uint32_t E = 0x05040100u, O = 0x07060302u;
+        const int tid = static_cast<int>(threadIdx.x) - kP;
+        const int j = tid >> a.lcpr, c4 = (tid & ((1 << a.lcpr) - 1)) * 4;
+        const int XR = a.TR + 2 * K, rx = XR * G, rt = rx + a.TR * G;
+        const int bx = a.x_off + j * a.xc + 8 + c4;
+        const int by = j * a.dyc + c4 - XR * 2 * a.WS; // dy round u: row u / G - XR
+        const int sx = a.rpu * a.xc, sy = a.rpu * a.dyc;
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            if (u < rt) {
+                const bool isx = u < rx;
+                const int rr = u / G, cb = u % G;
+                const int off0 = isx ? bx + rr * 2 * a.XS + cb * sx : by + rr * 2 * a.WS + cb * sy;
+                const int off1 = off0 + (isx ? a.XS : a.WS);
+                if ((okm >> u) & 1u) {
+                    const uint4 q = v[u];
+                    *reinterpret_cast<uint2 *>(lds + off0) =
+                        make_uint2(perm(q.y, q.x, E), perm(q.w, q.z, E));
+                    *reinterpret_cast<uint2 *>(lds + off1) =
+                        make_uint2(perm(q.y, q.x, O), perm(q.w, q.z, O));
+                } else {
+                    *reinterpret_cast<uint2 *>(lds + off0) = make_uint2(0, 0);
+                    *reinterpret_cast<uint2 *>(lds + off1) = make_uint2(0, 0);
+                }
+            }
+        }
+    }
+};
+
+// B fragment as read from LDS: the 16-byte aligned chunk holding the run
+// and, for a run shifted by one split position, the neighbouring 4 bytes.
+// The byte-aligns that form the fragment are left to the product that uses
+// it, so waiting for the read does not come right after issuing it.
+struct BRaw {
+    uint4 c;
+    uint32_t e;
+};
+
+template <int S> __device__ __forceinline__ BRaw read_shifted(const bf16raw *__restrict__ p)
+{
+    BRaw r;
+    r.c = *reinterpret_cast<const uint4 *>(p);
+    if constexpr (S == 0) {
+        r.e = 0;
+    } else {
+        // the offset behind an empty asm: merged with the chunk into one
+        // 4-byte aligned 20-byte load, the read would become three
+        int off = S == 1 ? 8 : -2;
+        asm("" : "+v"(off));
+        r.e = *reinterpret_cast<const uint32_t *>(p + off);
+    }
+    return r;
+}
+
+// the 8 split elements starting S (-1, 0, 1) positions after the chunk
+template <int S> __device__ __forceinline__ bf16x8 frag_shifted(const BRaw &r)
+{
+    const uint4 c0 = r.c;
+    if constexpr (S == 0)
+        return __builtin_bit_cast(bf16x8, c0);
+    else if constexpr (S == 1)
+        return __builtin_bit_cast(bf16x8, make_uint4(align2(c0.y, c0.x), align2(c0.z, c0.y),
+                                                     align2(c0.w, c0.z), align2(r.e, c0.w)));
+    else
+        return __builtin_bit_cast(bf16x8, make_uint4(align2(c0.x, r.e), align2(c0.y, c0.x),
+                                                     align2(c0.z, c0.y), align2(c0.w, c0.z)));
 }
 
 // A fragments of K-step q (dy of each co block, run 2q + kh of parity P)
@@ -228,22 +331,39 @@ template <int P, int NCB> struct WgA {
     }
 };
 
-// B fragment of tap t for the runs of A (x moved by the tap).
+// Split-position shift of tap t for centres of parity P: -1, 0 or 1.
+template <int K, int P> __device__ __forceinline__ constexpr int tap_shift(int t)
+{
+    constexpr TapTable<K> tt;
+    return floor_half(P + tt.dq[t]);
+}
+
+// B fragment of tap t for the runs of A (x moved by the tap), as read.
 template <int K, int P>
-__device__ __forceinline__ bf16x8 wg_loadB(int t, const bf16raw *__restrict__ xb, int XS,
-                                           int rrow, int j0)
+__device__ __forceinline__ BRaw wg_readB(int t, const bf16raw *__restrict__ xb, int XS, int rrow,
+                                         int j0)
 {
     constexpr TapTable<K> tt;
     const int dq = tt.dq[t], ds = tt.ds[t];
     const int dr = tap_drow(dq, ds, P);
-    const int sh = floor_half(P + dq); // split-position shift: -1, 0 or 1
+    const int sh = tap_shift<K, P>(t);
     // aligned run start in window row (rrow + K + dr), parity (P + dq) & 1
     const bf16raw *base = xb + j0 + ((rrow + K + dr) * 2 + ((P + dq) & 1)) * XS;
     if (sh == 0)
-        return load_shifted<0>(base);
+        return read_shifted<0>(base);
     if (sh == 1)
-        return load_shifted<1>(base);
-    return load_shifted<-1>(base);
+        return read_shifted<1>(base);
+    return read_shifted<-1>(base);
+}
+
+template <int K, int P> __device__ __forceinline__ bf16x8 wg_fragB(int t, const BRaw &r)
+{
+    const int sh = tap_shift<K, P>(t);
+    if (sh == 0)
+        return frag_shifted<0>(r);
+    if (sh == 1)
+        return frag_shifted<1>(r);
+    return frag_shifted<-1>(r);
 }
 
 // All K-steps of column parity P for taps [T0, T1).  The A fragments of
@@ -260,10 +380,10 @@ __device__ __forceinline__ void wg_parity(floatx16 (&acc)[NCB][TPG], float (&dbs
     constexpr int NT = T1 - T0;
     WgA<P, NCB> cur;
     cur.fetch(dyb, dyblk, WS, rpr, frpr, 0, kh);
-    bf16x8 b[NT];
+    BRaw b[NT];
 #pragma unroll
     for (int t = 0; t < NT; ++t)
-        b[t] = wg_loadB<K, P>(T0 + t, xb, XS, cur.rrow, cur.j0);
+        b[t] = wg_readB<K, P>(T0 + t, xb, XS, cur.rrow, cur.j0);
     int q = 0;
     do {
         WgA<P, NCB> nxt;
@@ -277,10 +397,13 @@ __device__ __forceinline__ void wg_parity(floatx16 (&acc)[NCB][TPG], float (&dbs
         }
 #pragma unroll
         for (int t = 0; t < NT; ++t) {
+            const bf16x8 bf = wg_fragB<K, P>(T0 + t, b[t]);
 #pragma unroll
             for (int c = 0; c < NCB; ++c)
-                acc[c][t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(cur.a[c], b[t], acc[c][t], 0, 0, 0);
-            b[t] = wg_loadB<K, P>(T0 + t, xb, XS, nxt.rrow, nxt.j0);
+                acc[c][t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(cur.a[c], bf, acc[c][t], 0, 0, 0);
+            b[t] = wg_readB<K, P>(T0 + t, xb, XS, nxt.rrow, nxt.j0);
+            // keep the read here, a tap's products ahead of its use
+            __builtin_amdgcn_sched_barrier(0);
         }
         cur = nxt;
     } while (++q < nq);
@@ -371,7 +494,7 @@ __device__ __forceinline__ void wg_consume_group(int g, const bf16raw *__restric
 }
 
 // Waves: NIB ci blocks x G = 4 / NIB tap groups; NCB co blocks per wave.
-template <int K, int NIB, int NCB, int CW, int U>
+template <int K, int NIB, int NCB, int CW, int U, int RG>
 __global__ __launch_bounds__(kT) __attribute__((amdgpu_waves_per_eu(2, 2))) void wgrad32_k(
     const bf16raw *__restrict__ x, const bf16raw *__restrict__ dy, float *__restrict__ part,
     Wg32Args a)
@@ -401,7 +524,7 @@ __global__ __launch_bounds__(kT) __attribute__((amdgpu_waves_per_eu(2, 2))) void
     // barriers; the two loops keep the staging registers and the
     // accumulators out of each other's way.
     if (producer) {
-        Wg32Regs<K, CW, U> regs;
+        typename std::conditional<(RG > 0), Wg32RegsR<K, U, RG>, Wg32Regs<K, CW, U>>::type regs;
         if (t_begin < t_end) {
             const int n = t_begin / a.ntr, r0 = (t_begin - n * a.ntr) * a.TR;
             regs.load(x, dy, a, n, r0, min(a.TR, a.H - r0));
@@ -479,7 +602,7 @@ constexpr size_t kLdsMax = 160 * 1024;
 // Most staging items per thread (prefetch registers: 16 or 8 bytes each);
 // every variant holds 32 next to its accumulators without scratch spills
 // (the compiler's resource report).
-constexpr int kMaxItems = 32;
+constexpr int kMaxItems = kMaxRounds;
 
 // Most 32-channel co blocks per wave next to its taps' accumulators (each
 // block and tap one 16-register tile, at most 192 registers): k = 1 splits
@@ -487,6 +610,12 @@ constexpr int kMaxItems = 32;
 constexpr int max_ncb(int K, int NIB)
 {
     return K == 1 ? (NIB <= 2 ? 2 : 1) : (NIB == 1 ? 2 : NIB == 2 ? 1 : 0);
+}
+
+// LDS bytes: dy, then x
+size_t wg32_lds(const Wg32Args &a)
+{
+    return 2ull * (a.x_off + static_cast<size_t>(a.CI) * a.xc);
 }
 
 // tiling of the pass over output channels co0 .. co0 + CO - 1 for a given
@@ -515,8 +644,7 @@ bool wg32_args(const ConvShape &sh, int co0, int CO, int TR, Wg32Args &a)
     if ((a.xc / 8) % 2 == 0)
         a.xc += 8;
     a.x_off = CO * a.dyc;
-    const size_t lds = 2ull * (a.x_off + static_cast<size_t>(sh.Ci) * a.xc);
-    if (lds > kLdsMax)
+    if (wg32_lds(a) > kLdsMax)
         return false;
     const int CW = (sh.W % 8 == 0) ? 8 : 4;
     a.cpr = sh.W / CW;
@@ -526,6 +654,21 @@ bool wg32_args(const ConvShape &sh, int co0, int CO, int TR, Wg32Args &a)
     a.fxr = make_fastdiv(static_cast<uint32_t>(a.TR + 2 * sh.k));
     a.ftr = make_fastdiv(static_cast<uint32_t>(a.TR));
     a.frpr = make_fastdiv(static_cast<uint32_t>(a.WS / 8));
+    // regular staging: 16-byte chunks, a power-of-two chunk count per row
+    // dividing the staging threads, x and dy each G = 2 or 4 rounds of
+    // channels per row, offsets within 31 bits
+    a.rg = a.rpu = a.lcpr = 0;
+    if (CW == 8 && a.cpr <= kP && (a.cpr & (a.cpr - 1)) == 0) {
+        const int rpu = kP / a.cpr;
+        const int g = sh.Ci / rpu;
+        if (sh.Ci == CO && sh.Ci % rpu == 0 && (g == 2 || g == 4) &&
+            static_cast<long>(sh.Ci) * sh.H * sh.W < (1L << 31)) {
+            a.rg = g;
+            a.rpu = rpu;
+            while ((1 << a.lcpr) < a.cpr)
+                ++a.lcpr;
+        }
+    }
     return true;
 }
 
@@ -585,14 +728,14 @@ template <typename F> bool wg32_passes(const ConvShape &sh, F &&f)
     return true;
 }
 
-template <int K, int NIB, int NCB, int CW>
+template <int K, int NIB, int NCB, int CW, int RG>
 void launch_w32_cw(int U, const Wg32Args &a, size_t lds, hipStream_t st, const bf16raw *x,
                    const bf16raw *dy, float *part)
 {
     if constexpr (NCB <= max_ncb(K, NIB)) {
 #define HEX_W32(UV)                                                                          \
-    HEX_LAUNCH((wgrad32_k<K, NIB, NCB, CW, UV>), dim3(a.nparts), dim3(kT), lds, st, x, dy,     \
-               part, a)
+    HEX_LAUNCH((wgrad32_k<K, NIB, NCB, CW, UV, RG>), dim3(a.nparts), dim3(kT), lds, st, x,   \
+               dy, part, a)
         static_assert(kMaxItems == 32, "staging variants: 8, 16, 24, 32 items");
         if (U <= 8)
             HEX_W32(8);
@@ -610,12 +753,18 @@ template <int K, int NIB>
 void launch_w32_nib(int NCB, bool cw8, int U, const Wg32Args &a, size_t lds, hipStream_t st,
                     const bf16raw *x, const bf16raw *dy, float *part)
 {
+    // regular staging needs C_in == this pass's C_out: one co block with one
+    // ci block, two with two
     if (NCB == 1) {
-        if (cw8) launch_w32_cw<K, NIB, 1, 8>(U, a, lds, st, x, dy, part);
-        else launch_w32_cw<K, NIB, 1, 4>(U, a, lds, st, x, dy, part);
+        if (NIB == 1 && a.rg == 2) launch_w32_cw<K, NIB, 1, 8, 2>(U, a, lds, st, x, dy, part);
+        else if (NIB == 1 && a.rg == 4) launch_w32_cw<K, NIB, 1, 8, 4>(U, a, lds, st, x, dy, part);
+        else if (cw8) launch_w32_cw<K, NIB, 1, 8, 0>(U, a, lds, st, x, dy, part);
+        else launch_w32_cw<K, NIB, 1, 4, 0>(U, a, lds, st, x, dy, part);
     } else {
-        if (cw8) launch_w32_cw<K, NIB, 2, 8>(U, a, lds, st, x, dy, part);
-        else launch_w32_cw<K, NIB, 2, 4>(U, a, lds, st, x, dy, part);
+        if (NIB == 2 && a.rg == 2) launch_w32_cw<K, NIB, 2, 8, 2>(U, a, lds, st, x, dy, part);
+        else if (NIB == 2 && a.rg == 4) launch_w32_cw<K, NIB, 2, 8, 4>(U, a, lds, st, x, dy, part);
+        else if (cw8) launch_w32_cw<K, NIB, 2, 8, 0>(U, a, lds, st, x, dy, part);
+        else launch_w32_cw<K, NIB, 2, 4, 0>(U, a, lds, st, x, dy, part);
     }
 }
 
@@ -669,7 +818,7 @@ hipError_t bf16_wgrad32(const void *x, const void *dy, float *dw, float *db, voi
         const int C = NIB * NCB;
         const int U = wg32_U(a);
         const bool cw8 = sh.W % 8 == 0;
-        const size_t lds = 2ull * (a.x_off + static_cast<size_t>(sh.Ci) * a.xc);
+        const size_t lds = wg32_lds(a);
         if (sh.k == 1)
             launch_w32<1>(NIB, NCB, cw8, U, a, lds, st, xp, dp, part);
         else

@@ -298,6 +298,11 @@ SWEEP = [
     (1, 32, 224, 6, 16, 1, 1), (2, 32, 128, 7, 12, 2, 1), (1, 64, 96, 5, 20, 1, 1),
     # four input-channel blocks per wave group at k = 1
     (1, 128, 32, 6, 16, 1, 1),
+    # matrix-core weight gradient with regular staging (rows of whole 16-byte
+    # chunks, as many input as output channels in the pass): 2 and 4 channel
+    # blocks per row, ragged last tiles
+    (2, 64, 64, 37, 128, 1, 1), (1, 32, 32, 19, 128, 2, 1), (3, 64, 64, 9, 64, 1, 1),
+    (1, 32, 32, 10, 256, 2, 1),
 ]
 
 
