@@ -71,7 +71,7 @@ struct Wg32Args {
     int nchunk;    // partial chunks per slot: tiles * 16 + db chunks
     int items_x, items_dy; // staging items of a full tile
     int cpr;       // staging chunks per image row
-    FastDiv fcpr, fxr, ftr, frpr; // division by cpr, TR + 2K, TR, runs per split row
+    FastDiv fcpr, fxr, ftr; // division by cpr, TR + 2K, TR
     // regular staging (Wg32RegsR): channel blocks per row (0: general
     // staging), channels per round, log2 of the chunks per row
     int rg, rpu, lcpr;
@@ -313,23 +313,49 @@ template <int S> __device__ __forceinline__ bf16x8 frag_shifted(const BRaw &r)
                                                      align2(c0.z, c0.y), align2(c0.w, c0.z)));
 }
 
-// A fragments of K-step q (dy of each co block, run 2q + kh of parity P)
-// and where the runs start: window row and split position.
-template <int P, int NCB> struct WgA {
-    bf16x8 a[NCB];
-    int rrow, j0;
-    __device__ __forceinline__ void fetch(const bf16raw *__restrict__ dyb, int dyblk, int WS,
-                                          int rpr, const FastDiv &frpr, int q, int kh)
+// Where the runs of a K-step start.  Lanes kh = 0 / 1 take runs 2q and
+// 2q + 1 of K-step q; run i lies in window row i / rpr at split position
+// 8 * (i % rpr).  Kept as element offsets of the run in a dy channel
+// (rows of 2 * WS) and in an x channel (rows of 2 * XS), advanced one
+// K-step (16 split positions) at a time.
+struct WgRun {
+    int j0, ao, xo;
+    __device__ __forceinline__ void init(int kh, int WS, int XS)
     {
-        const int run = 2 * q + kh;
-        rrow = udiv(run, frpr);
-        j0 = (run - rrow * rpr) * 8;
-        const bf16raw *p = dyb + (rrow * 2 + P) * WS + j0;
+        j0 = ao = xo = 8 * kh;
+        wrap(WS, XS);
+    }
+    __device__ __forceinline__ void wrap(int WS, int XS)
+    {
+        // a split row holds at least one run, so two steps suffice
 #pragma unroll
-        for (int c = 0; c < NCB; ++c)
-            a[c] = *reinterpret_cast<const bf16x8 *>(p + c * dyblk);
+        for (int i = 0; i < 2; ++i) {
+            if (j0 >= WS) {
+                j0 -= WS;
+                ao += WS;          // + 2 WS - WS
+                xo += 2 * XS - WS;
+            }
+        }
+    }
+    __device__ __forceinline__ void next(int WS, int XS)
+    {
+        j0 += 16;
+        ao += 16;
+        xo += 16;
+        wrap(WS, XS);
     }
 };
+
+// A fragments (dy of each co block) of the runs at r, column parity P.
+template <int P, int NCB>
+__device__ __forceinline__ void wg_fetchA(bf16x8 (&a)[NCB], const bf16raw *__restrict__ dyb,
+                                          int dyblk, int WS, const WgRun &r)
+{
+    const bf16raw *p = dyb + P * WS + r.ao;
+#pragma unroll
+    for (int c = 0; c < NCB; ++c)
+        a[c] = *reinterpret_cast<const bf16x8 *>(p + c * dyblk);
+}
 
 // Split-position shift of tap t for centres of parity P: -1, 0 or 1.
 template <int K, int P> __device__ __forceinline__ constexpr int tap_shift(int t)
@@ -338,17 +364,21 @@ template <int K, int P> __device__ __forceinline__ constexpr int tap_shift(int t
     return floor_half(P + tt.dq[t]);
 }
 
-// B fragment of tap t for the runs of A (x moved by the tap), as read.
-template <int K, int P>
-__device__ __forceinline__ BRaw wg_readB(int t, const bf16raw *__restrict__ xb, int XS, int rrow,
-                                         int j0)
+// Offset of tap t's B runs from the runs of A in an x channel: window row
+// K + drow, column parity (P + dq) & 1 (the same for the whole block).
+template <int K, int P> __device__ __forceinline__ int tap_xoff(int t, int XS)
 {
     constexpr TapTable<K> tt;
     const int dq = tt.dq[t], ds = tt.ds[t];
-    const int dr = tap_drow(dq, ds, P);
+    return ((K + tap_drow(dq, ds, P)) * 2 + ((P + dq) & 1)) * XS;
+}
+
+// B fragment of tap t for the runs at xr (x moved by the tap), as read.
+template <int K, int P>
+__device__ __forceinline__ BRaw wg_readB(int t, const bf16raw *__restrict__ xr, int toff)
+{
     const int sh = tap_shift<K, P>(t);
-    // aligned run start in window row (rrow + K + dr), parity (P + dq) & 1
-    const bf16raw *base = xb + j0 + ((rrow + K + dr) * 2 + ((P + dq) & 1)) * XS;
+    const bf16raw *base = xr + toff;
     if (sh == 0)
         return read_shifted<0>(base);
     if (sh == 1)
@@ -366,47 +396,75 @@ template <int K, int P> __device__ __forceinline__ bf16x8 wg_fragB(int t, const 
     return frag_shifted<-1>(r);
 }
 
-// All K-steps of column parity P for taps [T0, T1).  The A fragments of
-// the next K-step are requested first; then, tap by tap, the products of
-// this K-step and the request for that tap's B fragment of the next
-// K-step, so each fragment has the rest of a K-step's products to arrive.
+// One K-step: the products of every tap with the A fragments a, each
+// followed by the request for that tap's B fragment at the runs xr of the
+// next K-step, so a fragment has the rest of a K-step's products to arrive.
+template <int K, int P, int T0, int NT, int NCB, int TPG>
+__device__ __forceinline__ void wg_kstep(floatx16 (&acc)[NCB][TPG], float (&dbs)[NCB],
+                                         bool do_db, const bf16x8 (&a)[NCB], BRaw (&b)[NT],
+                                         const bf16raw *__restrict__ xr, const int (&toff)[NT])
+{
+    if (do_db) {
+#pragma unroll
+        for (int c = 0; c < NCB; ++c)
+#pragma unroll
+            for (int e = 0; e < 8; ++e)
+                dbs[c] += static_cast<float>(a[c][e]);
+    }
+#pragma unroll
+    for (int t = 0; t < NT; ++t) {
+        const bf16x8 bf = wg_fragB<K, P>(T0 + t, b[t]);
+#pragma unroll
+        for (int c = 0; c < NCB; ++c)
+            acc[c][t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[c], bf, acc[c][t], 0, 0, 0);
+        b[t] = wg_readB<K, P>(T0 + t, xr, toff[t]);
+        // keep the read here, a tap's products ahead of its use
+        __builtin_amdgcn_sched_barrier(0);
+    }
+}
+
+// All K-steps of column parity P for taps [T0, T1), two per loop turn so
+// that the A fragments alternate between two register sets; the next
+// K-step's A fragments are requested before this one's products.
 template <int K, int P, int T0, int T1, int NCB, int TPG>
 __device__ __forceinline__ void wg_parity(floatx16 (&acc)[NCB][TPG], float (&dbs)[NCB],
                                           bool do_db, const bf16raw *__restrict__ dyb, int dyblk,
-                                          const bf16raw *__restrict__ xb, int WS, int XS, int rpr,
-                                          const FastDiv &frpr, int nq, int kh)
+                                          const bf16raw *__restrict__ xb, int WS, int XS, int nq,
+                                          int kh)
 {
     // nq >= 1: a tile holds at least one K-step (the planner pairs runs)
     constexpr int NT = T1 - T0;
-    WgA<P, NCB> cur;
-    cur.fetch(dyb, dyblk, WS, rpr, frpr, 0, kh);
+    int toff[NT];
+#pragma unroll
+    for (int t = 0; t < NT; ++t)
+        toff[t] = tap_xoff<K, P>(T0 + t, XS);
+    WgRun r;
+    r.init(kh, WS, XS);
+    bf16x8 a0[NCB], a1[NCB];
+    wg_fetchA<P, NCB>(a0, dyb, dyblk, WS, r);
     BRaw b[NT];
 #pragma unroll
     for (int t = 0; t < NT; ++t)
-        b[t] = wg_readB<K, P>(T0 + t, xb, XS, cur.rrow, cur.j0);
+        b[t] = wg_readB<K, P>(T0 + t, xb + r.xo, toff[t]);
+    // pairs of K-steps with no exit between them (an exit there would let
+    // the compiler sink the B requests below the products); the last
+    // K-step requests its own runs again
     int q = 0;
-    do {
-        WgA<P, NCB> nxt;
-        nxt.fetch(dyb, dyblk, WS, rpr, frpr, q + 1 < nq ? q + 1 : q, kh);
-        if (do_db) {
-#pragma unroll
-            for (int c = 0; c < NCB; ++c)
-#pragma unroll
-                for (int e = 0; e < 8; ++e)
-                    dbs[c] += static_cast<float>(cur.a[c][e]);
-        }
-#pragma unroll
-        for (int t = 0; t < NT; ++t) {
-            const bf16x8 bf = wg_fragB<K, P>(T0 + t, b[t]);
-#pragma unroll
-            for (int c = 0; c < NCB; ++c)
-                acc[c][t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(cur.a[c], bf, acc[c][t], 0, 0, 0);
-            b[t] = wg_readB<K, P>(T0 + t, xb, XS, nxt.rrow, nxt.j0);
-            // keep the read here, a tap's products ahead of its use
-            __builtin_amdgcn_sched_barrier(0);
-        }
-        cur = nxt;
-    } while (++q < nq);
+    for (; q + 2 <= nq; q += 2) {
+        r.next(WS, XS);
+        wg_fetchA<P, NCB>(a1, dyb, dyblk, WS, r);
+        wg_kstep<K, P, T0, NT, NCB, TPG>(acc, dbs, do_db, a0, b, xb + r.xo, toff);
+        WgRun rn = r;
+        rn.next(WS, XS);
+        const bool more = q + 2 < nq;
+        r.j0 = more ? rn.j0 : r.j0;
+        r.ao = more ? rn.ao : r.ao;
+        r.xo = more ? rn.xo : r.xo;
+        wg_fetchA<P, NCB>(a0, dyb, dyblk, WS, r);
+        wg_kstep<K, P, T0, NT, NCB, TPG>(acc, dbs, do_db, a1, b, xb + r.xo, toff);
+    }
+    if (q < nq)
+        wg_kstep<K, P, T0, NT, NCB, TPG>(acc, dbs, do_db, a0, b, xb + r.xo, toff);
 }
 
 // A computing wave of ci block ib and tap group GI (taps T0 .. T1 - 1) over
@@ -436,7 +494,9 @@ __device__ __forceinline__ void wg_consume(const bf16raw *__restrict__ lds, floa
 #pragma unroll
     for (int c = 0; c < NCB; ++c)
         dbs[c] = 0.f;
-    const bool do_db = ib == 0 && GI == 0;
+    // the db sums go to the last tap group, which has the fewest taps
+    constexpr int G = (T + TPG - 1) / TPG;
+    const bool do_db = ib == 0 && GI == G - 1;
     const bf16raw *dyb = lds + n32 * a.dyc;
     const int dyblk = 32 * a.dyc; // next co block
     const bf16raw *xb = lds + a.x_off + (ib * 32 + n32) * a.xc + 8;
@@ -448,10 +508,10 @@ __device__ __forceinline__ void wg_consume(const bf16raw *__restrict__ lds, floa
         __syncthreads();
         __syncthreads(); // tile pt is in LDS
         if constexpr (NT > 0) {
-            wg_parity<K, 0, T0, T1, NCB, TPG>(acc, dbs, do_db, dyb, dyblk, xb, a.WS, a.XS, rpr,
-                                              a.frpr, nq, kh);
-            wg_parity<K, 1, T0, T1, NCB, TPG>(acc, dbs, do_db, dyb, dyblk, xb, a.WS, a.XS, rpr,
-                                              a.frpr, nq, kh);
+            wg_parity<K, 0, T0, T1, NCB, TPG>(acc, dbs, do_db, dyb, dyblk, xb, a.WS, a.XS, nq,
+                                              kh);
+            wg_parity<K, 1, T0, T1, NCB, TPG>(acc, dbs, do_db, dyb, dyblk, xb, a.WS, a.XS, nq,
+                                              kh);
         }
     }
 
@@ -653,7 +713,6 @@ bool wg32_args(const ConvShape &sh, int co0, int CO, int TR, Wg32Args &a)
     a.fcpr = make_fastdiv(static_cast<uint32_t>(a.cpr));
     a.fxr = make_fastdiv(static_cast<uint32_t>(a.TR + 2 * sh.k));
     a.ftr = make_fastdiv(static_cast<uint32_t>(a.TR));
-    a.frpr = make_fastdiv(static_cast<uint32_t>(a.WS / 8));
     // regular staging: 16-byte chunks, a power-of-two chunk count per row
     // dividing the staging threads, x and dy each G = 2 or 4 rounds of
     // channels per row, offsets within 31 bits
@@ -755,15 +814,23 @@ void launch_w32_nib(int NCB, bool cw8, int U, const Wg32Args &a, size_t lds, hip
 {
     // regular staging needs C_in == this pass's C_out: one co block with one
     // ci block, two with two
+    bool done = false;
+    if constexpr (NIB <= 2) {
+        if (NCB == NIB && a.rg == 2) {
+            launch_w32_cw<K, NIB, NIB, 8, 2>(U, a, lds, st, x, dy, part);
+            done = true;
+        } else if (NCB == NIB && a.rg == 4) {
+            launch_w32_cw<K, NIB, NIB, 8, 4>(U, a, lds, st, x, dy, part);
+            done = true;
+        }
+    }
+    if (done)
+        return;
     if (NCB == 1) {
-        if (NIB == 1 && a.rg == 2) launch_w32_cw<K, NIB, 1, 8, 2>(U, a, lds, st, x, dy, part);
-        else if (NIB == 1 && a.rg == 4) launch_w32_cw<K, NIB, 1, 8, 4>(U, a, lds, st, x, dy, part);
-        else if (cw8) launch_w32_cw<K, NIB, 1, 8, 0>(U, a, lds, st, x, dy, part);
+        if (cw8) launch_w32_cw<K, NIB, 1, 8, 0>(U, a, lds, st, x, dy, part);
         else launch_w32_cw<K, NIB, 1, 4, 0>(U, a, lds, st, x, dy, part);
     } else {
-        if (NIB == 2 && a.rg == 2) launch_w32_cw<K, NIB, 2, 8, 2>(U, a, lds, st, x, dy, part);
-        else if (NIB == 2 && a.rg == 4) launch_w32_cw<K, NIB, 2, 8, 4>(U, a, lds, st, x, dy, part);
-        else if (cw8) launch_w32_cw<K, NIB, 2, 8, 0>(U, a, lds, st, x, dy, part);
+        if (cw8) launch_w32_cw<K, NIB, 2, 8, 0>(U, a, lds, st, x, dy, part);
         else launch_w32_cw<K, NIB, 2, 4, 0>(U, a, lds, st, x, dy, part);
     }
 }
