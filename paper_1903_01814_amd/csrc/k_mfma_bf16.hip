@@ -67,6 +67,8 @@ struct WideArgs {
     int vec_out;        // 16-byte output stores allowed
     int wgroups;        // channel groups whose weights are copied per pass (registers mode)
     int per_block;      // pixel tiles per block (prefetching kernel)
+    int ring;           // 32x32 kernel: window rows kept from tile to tile of an image
+    int out_off;        // 32x32 kernel: byte offset of the output staging in LDS
 };
 
 __device__ __forceinline__ uint32_t perm(uint32_t hi, uint32_t lo, uint32_t sel)
@@ -277,6 +279,102 @@ __device__ __forceinline__ void stage_tile(bf16raw *__restrict__ tl, const bf16r
         g.commit(tl, wd, W, LCP, CS);
     }
     zero_halo<K>(tl, wd, W, IC, LCP, CS);
+}
+
+// Ring window of the 32x32 kernel.  The window of a tile (rows r0 - K ..
+// r0 + TR + K - 1) lives in R = TR + 2K ring rows of LCP slots, image row r
+// in ring row (r + K) mod R, so the next tile of the same image finds its
+// first 2K rows already there and stages only its TR new ones; the first
+// tile of an image (or of a block) stages the whole window.  Staged rows
+// inside the image [rlo, rhi) are items of one 8-channel group of one
+// 8-element chunk (chunks aligned to 8 elements, as for the full window),
+// one per thread.
+struct RingRows {
+    int e_lo, e_hi, e_al, items;
+    __device__ __forceinline__ RingRows(int W, int IC, int rlo, int rhi)
+    {
+        e_lo = rlo * W;
+        e_hi = max(rhi, rlo) * W;
+        e_al = e_lo & ~7;
+        items = e_hi > e_lo ? (IC >> 3) * ((e_hi - e_al + 7) >> 3) : 0;
+    }
+};
+
+template <int NTHR> struct RingRegs {
+    uint4 v[8];
+    int eb, cg;
+
+    __device__ __forceinline__ void load(const bf16raw *__restrict__ src, const RingRows &rw,
+                                         int HW, int IC)
+    {
+        const int ncg = IC >> 3;
+        const int it = threadIdx.x;
+        const bool live = it < rw.items;
+        const int ch = live ? it / ncg : 0;
+        cg = live ? it - ch * ncg : 0;
+        // e_al + 8*ch is a multiple of 8 below H*W: all 8 elements lie in
+        // the plane (and item 0 of an empty range reads chunk 0)
+        const int e0 = live ? rw.e_al + 8 * ch : 0;
+#pragma unroll
+        for (int j = 0; j < 8; ++j)
+            v[j] = *reinterpret_cast<const uint4 *>(src + static_cast<size_t>(cg * 8 + j) * HW + e0);
+        eb = live ? e0 : -1;
+    }
+
+    __device__ __forceinline__ void commit(bf16raw *__restrict__ tl, const RingRows &rw, int K,
+                                           int W, int R, int LCP, int CS) const
+    {
+        if (eb < 0)
+            return;
+        // the 8 pixels eb..eb+7 cross at most one row end (W >= 8)
+        const int r = eb / W, c = eb - r * W;
+        int rr = (r + K) % R;
+        const int rr1 = rr + 1 == R ? 0 : rr + 1;
+#pragma unroll
+        for (int px = 0; px < 8; ++px) {
+            const int e = eb + px;
+            const bool brk = c + px >= W;
+            const uint32_t sel = (px & 1) ? 0x07060302u : 0x05040100u;
+            uint32_t w4[4];
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+                const uint32_t lo = reinterpret_cast<const uint32_t *>(&v[2 * q])[px >> 1];
+                const uint32_t hi = reinterpret_cast<const uint32_t *>(&v[2 * q + 1])[px >> 1];
+                w4[q] = perm(hi, lo, sel);
+            }
+            const int slot = (brk ? rr1 * LCP + c + px - W : rr * LCP + c + px) + K;
+            if (e >= rw.e_lo && e < rw.e_hi)
+                *reinterpret_cast<uint4 *>(tl + static_cast<size_t>(slot) * CS + cg * 8) =
+                    make_uint4(w4[0], w4[1], w4[2], w4[3]);
+        }
+    }
+};
+
+// Zeros for the ring window: with cols, the K side columns of all R ring
+// rows; and the ring rows of image rows [slo, shi) outside the image.
+template <int NTHR>
+__device__ __forceinline__ void ring_zero(bf16raw *__restrict__ tl, bool cols, int slo, int shi,
+                                          int K, int H, int W, int IC, int R, int LCP, int CS)
+{
+    const int v8 = IC >> 3;
+    const int side = cols ? R * 2 * K : 0;
+    const int nlo = max(0, min(shi, 0) - slo);     // rows above the image
+    const int nhi = max(0, shi - max(slo, H));     // rows below it
+    const int total = (side + (nlo + nhi) * LCP) * v8;
+    for (int e = threadIdx.x; e < total; e += NTHR) {
+        const int s = e / v8, q = e - s * v8;
+        int slot;
+        if (s < side) {
+            const int rr = s / (2 * K), j = s - rr * 2 * K;
+            slot = rr * LCP + (j < K ? j : W + j);
+        } else {
+            const int s2 = s - side;
+            const int o = s2 / LCP, c = s2 - o * LCP;
+            const int r = o < nlo ? slo + o : max(slo, H) + (o - nlo);
+            slot = ((r + K) % R) * LCP + c;
+        }
+        *reinterpret_cast<uint4 *>(tl + static_cast<size_t>(slot) * CS + q * 8) = make_uint4(0, 0, 0, 0);
+    }
 }
 
 // Epilogue of a pixel tile, first half: bias, ReLU and bf16 rounding of
@@ -589,42 +687,69 @@ __global__ __launch_bounds__(kThreads32) void conv_bf16_wide32_k(
     const int rowb = a.LCP * a.CS * 2;
     const int slotb = a.CS * 2;
     const unsigned char *tlb = reinterpret_cast<const unsigned char *>(tl);
-    const int oddoff = (n32 & 1) ? rowb : 0; // W even, tiles on multiples of 32: parity of n32
+    // W even, tiles on multiples of 32: a lane's pixel column has the parity of n32
+    const int podd = n32 & 1;
     const bf16raw *wrow = wl + (og * 32 + n32) * a.WP + 8 * kh;
+    const int R = a.TR + 2 * K; // ring rows
 
-    WideTileRegs<K, 1, kThreads32> g;
+    // tile pt stages image rows [slo, shi): the whole window for the first
+    // tile of an image or of the block (every tile without the ring), else
+    // the TR rows after the previous window
+    auto staged = [&](int pt, int &slo, int &shi) {
+        const int n = pt / a.ntr, r0 = (pt - n * a.ntr) * a.TR;
+        const bool whole = !a.ring || pt == t_begin || r0 == 0;
+        slo = whole ? r0 - K : r0 + K;
+        shi = r0 + a.TR + K;
+    };
+    RingRegs<kThreads32> g;
     {
+        int slo, shi;
+        staged(t_begin, slo, shi);
         const int n = t_begin / a.ntr;
-        const int r0 = (t_begin - n * a.ntr) * a.TR;
-        const WideWindow wd(K, H, W, a.IC, r0, min(a.TR, H - r0));
-        g.load(xin + static_cast<size_t>(n) * a.IC * HW, wd, HW, a.IC, threadIdx.x);
+        g.load(xin + static_cast<size_t>(n) * a.IC * HW,
+               RingRows(W, a.IC, max(slo, 0), min(shi, H)), HW, a.IC);
     }
     for (int pt = t_begin; pt < t_end; ++pt) {
         const int n = pt / a.ntr;
         const int r0 = (pt - n * a.ntr) * a.TR;
         const int rows = min(a.TR, H - r0);
         const int npix = rows * W;
-        const WideWindow wd(K, H, W, a.IC, r0, rows);
+        int slo, shi;
+        staged(pt, slo, shi);
 
         __syncthreads(); // the previous tile's (or the weight copy's) LDS reads are done
-        g.commit(tl, wd, W, a.LCP, a.CS);
-        zero_halo<K, kThreads32>(tl, wd, W, a.IC, a.LCP, a.CS);
+        g.commit(tl, RingRows(W, a.IC, max(slo, 0), min(shi, H)), K, W, R, a.LCP, a.CS);
+        ring_zero<kThreads32>(tl, slo == r0 - K, slo, shi, K, H, W, a.IC, R, a.LCP, a.CS);
         __syncthreads();
         if (pt + 1 < t_end) {
+            int slo2, shi2;
+            staged(pt + 1, slo2, shi2);
             const int n2 = (pt + 1) / a.ntr;
-            const int r2 = (pt + 1 - n2 * a.ntr) * a.TR;
-            const WideWindow wd2(K, H, W, a.IC, r2, min(a.TR, H - r2));
-            g.load(xin + static_cast<size_t>(n2) * a.IC * HW, wd2, HW, a.IC, threadIdx.x);
+            g.load(xin + static_cast<size_t>(n2) * a.IC * HW,
+                   RingRows(W, a.IC, max(slo2, 0), min(shi2, H)), HW, a.IC);
         }
 
-        // A-row (pixel) slot addresses; pixels past the tile read a clamped
-        // valid centre, their results are never stored
-        int adr[MT];
+        // A rows (pixels): column part of the slot address, and the ring row
+        // offsets of the image rows d - K from the pixel's row (d = 0 .. 2K),
+        // plain and one row further for odd pixel columns (taps with odd dq);
+        // pixels past the tile read a clamped valid centre, their results
+        // are never stored
+        int colb[MT], ro[MT][2 * K + 1], rop[MT][2 * K + 1];
 #pragma unroll
         for (int i = 0; i < MT; ++i) {
             const int p = min((pg + PW * i) * 32 + n32, npix - 1);
             const int pr = p / W, pc = p - pr * W;
-            adr[i] = ((pr + K) * a.LCP + pc + K) * slotb + kh * 16;
+            colb[i] = (pc + K) * slotb + kh * 16;
+            // image row pr + d - K of the tile is ring row (rb + d) mod R
+            const int rb = (r0 + pr) % R;
+            // (rb + d + 1 < 2R: R = TR + 2K > 2K); computed, not selected
+            // from ro, which would put ro in scratch memory
+#pragma unroll
+            for (int d = 0; d <= 2 * K; ++d) {
+                const int rr = rb + d, rq = rr + podd;
+                ro[i][d] = (rr >= R ? rr - R : rr) * rowb;
+                rop[i][d] = (rq >= R ? rq - R : rq) * rowb;
+            }
         }
         floatx16 acc[MT];
 #pragma unroll
@@ -640,11 +765,12 @@ __global__ __launch_bounds__(kThreads32) void conv_bf16_wide32_k(
                 const int t = ks / ICB;
                 constexpr TapTable<K> tt;
                 const int dq = tt.dq[t], ds = tt.ds[t];
-                const int toff = (ds + floor_half(dq)) * rowb + dq * slotb + (ks % ICB) * 32 +
-                                 ((dq & 1) ? oddoff : 0);
+                const int d = K + ds + floor_half(dq); // row of even columns, + K
+                const int toff = dq * slotb + (ks % ICB) * 32;
 #pragma unroll
                 for (int i = 0; i < MT; ++i)
-                    q[i] = *reinterpret_cast<const uint4 *>(tlb + adr[i] + toff);
+                    q[i] = *reinterpret_cast<const uint4 *>(
+                        tlb + ((dq & 1) ? rop[i][d] : ro[i][d]) + colb[i] + toff);
             };
             auto fetch_b = [&](int ks) -> bf16x8 {
                 if constexpr (WL)
@@ -677,9 +803,11 @@ __global__ __launch_bounds__(kThreads32) void conv_bf16_wide32_k(
         }
 
         // epilogue: bias, ReLU, bf16 into LDS as [oc][pixel] (pitch OP = 4 mod
-        // 8: conflict-free 8-byte writes), then 16-byte stores
-        __syncthreads();
-        bf16raw *outl = tl;
+        // 8: conflict-free 8-byte writes), then 16-byte stores.  Without the
+        // ring the staging overlays the window.
+        if (!a.ring)
+            __syncthreads();
+        bf16raw *outl = reinterpret_cast<bf16raw *>(smem + a.out_off);
         if (wave_live) {
             const int ocl = og * 32 + n32;
 #pragma unroll
@@ -799,23 +927,33 @@ bool plan_cfg(const ConvShape &sh, int IC, int OC, const WideCfg &c, WidePlan &p
     a.OP = c.pix() + 4; // 8 mod 16 bytes: conflict-free 8-byte epilogue writes
     const size_t tile_in = 2ull * (a.TR + 2 * sh.k) * a.LCP * a.CS;
     const size_t tile_out = 2ull * c.OCB() * a.OP;
-    const size_t tiles = std::max(tile_in, tile_out);
     const int og = c.waves() / c.PW;
-    size_t lds;
-    if (c.KSR > 0) {
-        a.WP = sh.T * IC;
-        a.tile_off = 0;
-        const size_t wgroup = 2ull * (c.OCB() / og) * a.WP; // bytes per channel group
-        a.wgroups = (wgroup * og <= tiles) ? og : 1;
-        lds = std::max(tiles, wgroup * a.wgroups);
-    } else {
-        a.WP = resident_pitch(sh.T * IC, c.E32 != 0);
-        a.tile_off = static_cast<int>((2ull * c.OCB() * a.WP + 255) / 256 * 256);
-        a.wgroups = 1;
-        lds = a.tile_off + tiles;
-    }
     const bool two_per_cu = !c.E32 && c.KSR > 0;
-    if (lds > (two_per_cu ? kLds2 : kLds1))
+    const size_t limit = two_per_cu ? kLds2 : kLds1;
+    // 32x32 kernel: the input window and the output staging side by side
+    // (the window rows carry over from tile to tile) if LDS holds both,
+    // else the staging overlays the window
+    auto layout = [&](bool ring, size_t &lds) {
+        const size_t in_r = (tile_in + 255) / 256 * 256;
+        const size_t tiles = ring ? in_r + tile_out : std::max(tile_in, tile_out);
+        if (c.KSR > 0) {
+            a.WP = sh.T * IC;
+            a.tile_off = 0;
+            const size_t wgroup = 2ull * (c.OCB() / og) * a.WP; // bytes per channel group
+            a.wgroups = (wgroup * og <= tiles) ? og : 1;
+            lds = std::max(tiles, wgroup * a.wgroups);
+        } else {
+            a.WP = resident_pitch(sh.T * IC, c.E32 != 0);
+            a.tile_off = static_cast<int>((2ull * c.OCB() * a.WP + 255) / 256 * 256);
+            a.wgroups = 1;
+            lds = a.tile_off + tiles;
+        }
+        a.ring = ring ? 1 : 0;
+        a.out_off = a.tile_off + (ring ? static_cast<int>(in_r) : 0);
+        return lds <= limit;
+    };
+    size_t lds = 0;
+    if (!(c.E32 && layout(true, lds)) && !layout(false, lds))
         return false;
     if (c.E32) {
         // staged window items of one tile: at most one per thread
