@@ -51,8 +51,55 @@ template <int S> __device__ __forceinline__ int centre_r(int i, int j)
     return S * i + (j & 1) * (S / 2);
 }
 
-// ARG: write the argmax tap (max pooling).
-template <typename TT, int MODE, int K, int S, bool ARG>
+// Interior rows of a group of NP planes in 16-byte chunks, U per thread; the
+// planes are contiguous in x, so chunk it is x[group start + VEC * it].
+// Every load is issued (the index clamped) so that their count is fixed.
+// (a native vector type: copies of the uint4 struct become memcpys that keep
+// the array in scratch memory)
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+template <typename TT, int K, int U> struct PoolStage {
+    static constexpr int VEC = 16 / sizeof(TT);
+    u32x4 v[U];
+
+    __device__ __forceinline__ void load(const TT *__restrict__ x, const PoolArgs &a, int g)
+    {
+        const int np = min(a.NP, a.nplanes - g * a.NP);
+        const int items = np * a.H * (a.W / VEC);
+        const TT *src = x + static_cast<size_t>(g) * a.NP * a.H * a.W;
+#pragma clang loop unroll(full)
+        for (int u = 0; u < U; ++u) {
+            const int it = threadIdx.x + u * kPoolThreads;
+            v[u] = *reinterpret_cast<const u32x4 *>(src + static_cast<size_t>(min(it, items - 1)) * VEC);
+        }
+    }
+
+    // into LDS rows K .. K + H - 1 of each plane, after the 16-byte left pad
+    __device__ __forceinline__ void commit(TT *__restrict__ lds, const PoolArgs &a, int g) const
+    {
+        const int np = min(a.NP, a.nplanes - g * a.NP);
+        const int cpr = a.W / VEC;
+        const int items = np * a.H * cpr;
+        const int plane_l = a.LR * a.pitch;
+#pragma clang loop unroll(full)
+        for (int u = 0; u < U; ++u) {
+            const int it = threadIdx.x + u * kPoolThreads;
+            if (it < items) {
+                const int rowi = static_cast<int>(fdiv(static_cast<uint32_t>(it), a.fcr));
+                const int ch = it - rowi * cpr;
+                const int pl = static_cast<int>(fdiv(static_cast<uint32_t>(rowi), a.fh));
+                const int r = rowi - pl * a.H;
+                *reinterpret_cast<u32x4 *>(lds + pl * plane_l + (r + K) * a.pitch + VEC + ch * VEC) = v[u];
+            }
+        }
+    }
+};
+
+// ARG: write the argmax tap (max pooling).  U: 16-byte chunks per thread of
+// a group of NP planes.  Persistent blocks walk the plane groups g =
+// blockIdx.x, + gridDim.x, ...; the next group's chunks are loaded into
+// registers right after the current group is written to LDS, so every block
+// has a load in flight while it reduces and stores.
+template <typename TT, int MODE, int K, int S, bool ARG, int U>
 __global__ __launch_bounds__(kPoolThreads) void pool_fwd_k(const TT *__restrict__ x,
                                                            TT *__restrict__ y,
                                                            uint8_t *__restrict__ am, PoolArgs a)
@@ -61,18 +108,16 @@ __global__ __launch_bounds__(kPoolThreads) void pool_fwd_k(const TT *__restrict_
     constexpr int VEC = 16 / sizeof(TT); // elements per 16 bytes = left pad
     extern __shared__ __align__(16) unsigned char smem[];
     TT *lds = reinterpret_cast<TT *>(smem);
-    const int p0 = blockIdx.x * a.NP;
-    const int np = min(a.NP, a.nplanes - p0);
     const int H = a.H, W = a.W;
-    const size_t HW = static_cast<size_t>(H) * W;
     const int plane_l = a.LR * a.pitch;
-    const int cpr = W / VEC;
+    const int ngroups = (a.nplanes + a.NP - 1) / a.NP;
 
-    // zero border: whole rows above / below, one 16-byte chunk left and right
+    // zero border, once: whole rows above / below, one 16-byte chunk left
+    // and right; the group's rows never overwrite it
     {
         const int vrow = a.pitch / VEC; // 16-byte chunks per LDS row
         const int per_plane = 2 * K * vrow + 2 * H;
-        for (int e = threadIdx.x; e < np * per_plane; e += kPoolThreads) {
+        for (int e = threadIdx.x; e < a.NP * per_plane; e += kPoolThreads) {
             const int pl = e / per_plane, q = e - pl * per_plane;
             int off;
             if (q < 2 * K * vrow) {
@@ -87,83 +132,69 @@ __global__ __launch_bounds__(kPoolThreads) void pool_fwd_k(const TT *__restrict_
             *reinterpret_cast<uint4 *>(lds + pl * plane_l + off) = make_uint4(0, 0, 0, 0);
         }
     }
-    // interior rows, 16-byte chunks; the planes are contiguous in x, so
-    // chunk it is x[p0 plane start + VEC * it]; U loads in flight per thread
-    {
-        constexpr int U = 4;
-        const int items = np * H * cpr;
-        const TT *src = x + static_cast<size_t>(p0) * HW;
-        for (int it0 = threadIdx.x; it0 < items; it0 += U * kPoolThreads) {
-            uint4 v[U];
-#pragma unroll
-            for (int u = 0; u < U; ++u) {
-                const int it = it0 + u * kPoolThreads;
-                v[u] = *reinterpret_cast<const uint4 *>(src + static_cast<size_t>(min(it, items - 1)) * VEC);
-            }
-#pragma unroll
-            for (int u = 0; u < U; ++u) {
-                const int it = it0 + u * kPoolThreads;
-                if (it < items) {
-                    const int rowi = static_cast<int>(fdiv(static_cast<uint32_t>(it), a.fcr));
-                    const int ch = it - rowi * cpr;
-                    const int pl = static_cast<int>(fdiv(static_cast<uint32_t>(rowi), a.fh));
-                    const int r = rowi - pl * H;
-                    *reinterpret_cast<uint4 *>(lds + pl * plane_l + (r + K) * a.pitch + VEC + ch * VEC) =
-                        v[u];
-                }
-            }
-        }
-    }
-    __syncthreads();
+
+    PoolStage<TT, K, U> stg;
 
     // thread -> output column j (fixed) and every rpp-th output row of the
-    // block's planes (rows of consecutive planes follow each other)
+    // group's planes (rows of consecutive planes follow each other)
     const int Wo = a.Wo, Ho = a.Ho;
     const int HWo = Ho * Wo;
     const int rpp = kPoolThreads / Wo; // output rows per pass (Wo <= 256)
     const int j = threadIdx.x % Wo;
     const int row0 = threadIdx.x / Wo;
-    if (row0 >= rpp)
-        return; // spare threads (no barrier follows)
     const int cc = S * j;
     const int par = (S % 2 == 0) ? 0 : (cc & 1);
     const int halfs = (j & 1) * (S / 2);
-    TT *yb = y + static_cast<size_t>(p0) * HWo;
-    uint8_t *ab = am != nullptr ? am + static_cast<size_t>(p0) * HWo : nullptr;
     constexpr TapTable<K> tt;
-    int pl = static_cast<int>(fdiv(static_cast<uint32_t>(row0), a.fho_rows));
-    int i = row0 - pl * Ho;
-    for (int row = row0; row < np * Ho; row += rpp) {
-        const int rc = S * i + halfs;
-        const TT *cen = lds + pl * plane_l + (rc + K) * a.pitch + VEC + cc;
-        float best = 0.f, sum = 0.f;
-        int arg = 0;
-#pragma unroll
-        for (int t = 0; t < T; ++t) {
-            const int dr = par ? tap_drow(tt.dq[t], tt.ds[t], 1) : tap_drow(tt.dq[t], tt.ds[t], 0);
-            const float v = to_f(cen[dr * a.pitch + tt.dq[t]]);
-            if (MODE == 0) {
-                if (t == 0 || v > best) {
-                    best = v;
-                    if (ARG)
-                        arg = t;
+
+    if (blockIdx.x < ngroups)
+        stg.load(x, a, blockIdx.x);
+    for (int g = blockIdx.x; g < ngroups; g += gridDim.x) {
+        __syncthreads(); // the previous group's LDS reads are done (and the border)
+        stg.commit(lds, a, g);
+        __syncthreads();
+        if (g + static_cast<int>(gridDim.x) < ngroups)
+            stg.load(x, a, g + gridDim.x);
+        if (row0 < rpp) { // spare threads: only the staging and the barriers
+            const int p0 = g * a.NP;
+            const int np = min(a.NP, a.nplanes - p0);
+            TT *yb = y + static_cast<size_t>(p0) * HWo;
+            uint8_t *ab = am != nullptr ? am + static_cast<size_t>(p0) * HWo : nullptr;
+            int pl = static_cast<int>(fdiv(static_cast<uint32_t>(row0), a.fho_rows));
+            int i = row0 - pl * Ho;
+            for (int row = row0; row < np * Ho; row += rpp) {
+                const int rc = S * i + halfs;
+                const TT *cen = lds + pl * plane_l + (rc + K) * a.pitch + VEC + cc;
+                float best = 0.f, sum = 0.f;
+                int arg = 0;
+    #pragma unroll
+                for (int t = 0; t < T; ++t) {
+                    const int dr = par ? tap_drow(tt.dq[t], tt.ds[t], 1) : tap_drow(tt.dq[t], tt.ds[t], 0);
+                    const float val = to_f(cen[dr * a.pitch + tt.dq[t]]);
+                    if (MODE == 0) {
+                        if (t == 0 || val > best) {
+                            best = val;
+                            if (ARG)
+                                arg = t;
+                        }
+                    } else {
+                        sum += val;
+                    }
                 }
-            } else {
-                sum += v;
+                const int o = row * Wo + j; // plane-major: pl * HWo + i * Wo + j
+                if (MODE == 0) {
+                    yb[o] = from_f<TT>(best);
+                    if (ARG)
+                        ab[o] = static_cast<uint8_t>(arg);
+                } else {
+                    yb[o] = from_f<TT>(sum / static_cast<float>(T));
+                }
+                i += rpp;
+                while (i >= Ho) {
+                    i -= Ho;
+                    ++pl;
+                }
             }
-        }
-        const int o = row * Wo + j; // plane-major: pl * HWo + i * Wo + j
-        if (MODE == 0) {
-            yb[o] = from_f<TT>(best);
-            if (ARG)
-                ab[o] = static_cast<uint8_t>(arg);
-        } else {
-            yb[o] = from_f<TT>(sum / static_cast<float>(T));
-        }
-        i += rpp;
-        while (i >= Ho) {
-            i -= Ho;
-            ++pl;
         }
     }
 }
@@ -266,6 +297,8 @@ __global__ __launch_bounds__(kPoolThreads) void pool_bwd_k(const TT *__restrict_
 inline int cdiv(long a, long b) { return static_cast<int>((a + b - 1) / b); }
 
 constexpr size_t kPoolLds = 48 * 1024;
+constexpr size_t kLdsPerCu = 160 * 1024;
+constexpr int kPoolMaxU = 12; // staged 16-byte chunks per thread at most (forward)
 
 PoolArgs pool_args(const ConvShape &sh, int esz)
 {
@@ -311,23 +344,42 @@ hipError_t pool_fwd_fast(const void *x, void *y, uint8_t *am, const ConvShape &s
 {
     const int esz = dt == F32 ? 4 : 2;
     PoolArgs a = pool_args(sh, esz);
-    // planes per block: LDS budget and about 4 outputs per thread (measured
-    // on the 40x40 -> 20x20 pools: 2 planes per block beat 1, 5 and 10)
+    // planes per group: LDS budget and about 4 outputs per thread (measured
+    // on the 40x40 -> 20x20 pools: 2 planes per group beat 1, 5 and 10);
+    // chunks per thread within the instantiated staging depths
     const int by_lds = static_cast<int>(kPoolLds / fwd_plane_bytes(a, esz));
     const int by_work = std::max(1, (4 * kPoolThreads) / std::max(1, sh.Ho * sh.Wo));
     a.NP = std::max(1, std::min(by_lds, by_work));
-    const int grid = cdiv(a.nplanes, a.NP);
+    const int cpr = sh.W / (16 / esz);
+    while (a.NP > 1 && a.NP * sh.H * cpr > kPoolMaxU * kPoolThreads)
+        --a.NP;
+    const int U = cdiv(static_cast<long>(a.NP) * sh.H * cpr, kPoolThreads);
     const size_t lds = fwd_plane_bytes(a, esz) * a.NP;
+    // persistent blocks: as many as fit on a CU (threads and LDS), or one per group
+    const int groups = cdiv(a.nplanes, a.NP);
+    const int per_cu = std::max(1, std::min(8, static_cast<int>(kLdsPerCu / std::max<size_t>(lds, 1))));
+    const int grid = std::max(1, std::min(groups, device_cus() * per_cu));
+#define HEX_PF_U(TT, M, KV, SV, ARGV)                                                        \
+    do {                                                                                     \
+        if (U <= 1) HEX_LAUNCH((pool_fwd_k<TT, M, KV, SV, ARGV, 1>), dim3(grid),             \
+                               dim3(kPoolThreads), lds, st, static_cast<const TT *>(x),      \
+                               static_cast<TT *>(y), am, a);                                 \
+        else if (U <= 2) HEX_LAUNCH((pool_fwd_k<TT, M, KV, SV, ARGV, 2>), dim3(grid),        \
+                                    dim3(kPoolThreads), lds, st, static_cast<const TT *>(x), \
+                                    static_cast<TT *>(y), am, a);                            \
+        else if (U <= 4) HEX_LAUNCH((pool_fwd_k<TT, M, KV, SV, ARGV, 4>), dim3(grid),        \
+                                    dim3(kPoolThreads), lds, st, static_cast<const TT *>(x), \
+                                    static_cast<TT *>(y), am, a);                            \
+        else HEX_LAUNCH((pool_fwd_k<TT, M, KV, SV, ARGV, kPoolMaxU>), dim3(grid),            \
+                        dim3(kPoolThreads), lds, st, static_cast<const TT *>(x),             \
+                        static_cast<TT *>(y), am, a);                                        \
+    } while (0)
 #define HEX_PF(TT, M, KV, SV)                                                                \
     do {                                                                                     \
         if (am != nullptr)                                                                   \
-            HEX_LAUNCH((pool_fwd_k<TT, M, KV, SV, true>), dim3(grid),                \
-                               dim3(kPoolThreads), lds, st, static_cast<const TT *>(x),      \
-                               static_cast<TT *>(y), am, a);                                 \
+            HEX_PF_U(TT, M, KV, SV, true);                                                   \
         else                                                                                 \
-            HEX_LAUNCH((pool_fwd_k<TT, M, KV, SV, false>), dim3(grid),               \
-                               dim3(kPoolThreads), lds, st, static_cast<const TT *>(x),      \
-                               static_cast<TT *>(y), am, a);                                 \
+            HEX_PF_U(TT, M, KV, SV, false);                                                  \
     } while (0)
 #define HEX_PF_KS(TT, M)                                                                     \
     do {                                                                                     \
@@ -348,6 +400,7 @@ hipError_t pool_fwd_fast(const void *x, void *y, uint8_t *am, const ConvShape &s
     }
 #undef HEX_PF_KS
 #undef HEX_PF
+#undef HEX_PF_U
     return hipGetLastError();
 }
 
