@@ -26,10 +26,13 @@
 //
 // conv_bf16_wide32_k (preferred): v_mfma_f32_32x32x16_bf16, one block of 8
 // waves per CU, each block a contiguous run of row tiles, the next tile's
-// window prefetched into registers while the current one is computed, the A
-// fragments of the next two K-steps in flight.  The 32x32 instruction keeps
-// the matrix cores at about 2 PFLOP/s with one or two waves per SIMD, where
-// the 16x16 one needs more waves than the registers allow.
+// rows prefetched into registers while the current one is computed, the A
+// fragments of the next two K-steps in flight.  Where LDS holds it, the
+// window is a ring of TR + 2K rows kept from tile to tile of an image (a
+// tile after the first stages only its TR new rows) and the results are
+// staged in a region of their own.  The 32x32 instruction keeps the matrix
+// cores at about 2 PFLOP/s with one or two waves per SIMD, where the 16x16
+// one needs more waves than the registers allow.
 // conv_bf16_wide_k (fallback for other channel counts): 16x16x32, 4 waves,
 // two blocks per CU, pixel tiles handed out so that the blocks of one XCD
 // work on neighbouring tiles at the same time.

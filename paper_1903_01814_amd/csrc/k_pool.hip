@@ -2,7 +2,9 @@
 // kernel sizes k <= 2 and strides 1 and 2 (Sec. 2.4: the pool window is the
 // size-k hexagon, padded like the convolution; stride as in Sec. 2.3).
 //
-// Forward: a block stages NP whole input planes into LDS with a zero border
+// Forward: persistent blocks walk groups of NP planes, loading the next
+// group into registers while the current one is reduced and stored.  A
+// group's NP whole input planes are staged into LDS with a zero border
 // (k rows above and below, a 16-byte pad left and right of every row), so a
 // tap never needs a bounds check and padded taps read 0 (they take part in
 // the max and the mean).  Each thread then reduces the T taps of one output

@@ -23,20 +23,25 @@
 // A K-step (16 pixels) is two runs of the same parity.  Zero pads around
 // the split rows and zero rows outside the image give the padding taps.
 //
-// Work split.  One block of 4 waves per CU (one wave per SIMD, so a wave
-// may hold up to 512 registers and the accumulators sit beside the
-// prefetch buffers) owns a contiguous run of pixel tiles (full-width rows)
-// and prefetches the next tile into registers while it computes the
-// current one.  Wave w owns one 32-channel block of ci, a group of taps
-// (compile-time) and every 32-channel block of co in the pass (at most
-// two), so each B fragment feeds one product per co block and no two waves
-// add to the same output; the waves of the first ci block and tap group
-// also sum dy for db.  Within a K-step the B fragment of the next tap, and
-// the A fragments of the next K-step, are read before the current products.
-// Each block writes its accumulators to its own partial slot exactly as they
-// sit in the registers (one 64-lane register = 64 contiguous floats, whole
-// 256-byte lines), and a final kernel adds the slots in a fixed order and
-// scatters the sums to dw[co][ci][t] and db -- deterministic.
+// Work split.  One block of 8 waves per CU (two per SIMD) owns a contiguous
+// run of pixel tiles (full-width rows) and has two kinds of wave that meet
+// at the two barriers of every tile: waves 4-7 stage the next tile in
+// registers while the others compute and write it to LDS between the
+// barriers; waves 0-3 compute.  They run separate loops, so the staging
+// registers and the accumulators are never live in the same wave (each of
+// the two may use 256).  Computing wave w owns one 32-channel block of ci,
+// a group of taps (compile-time; one loop per group, so each group's
+// accumulators keep their registers) and every 32-channel block of co in
+// the pass (at most two), so each B fragment feeds one product per co block
+// and no two waves add to the same output; the wave of the first ci block
+// and the last (smallest) tap group also sums dy for db.  K-steps go in
+// pairs with the A fragments alternating between two register sets, and
+// every tap's B fragment of the next K-step is requested right after that
+// tap's products.  Each block writes its accumulators to its own partial
+// slot exactly as they sit in the registers (one 64-lane register = 64
+// contiguous floats, whole 256-byte lines), and a final kernel adds the
+// slots in a fixed order and scatters the sums to dw[co][ci][t] and db --
+// deterministic.
 #include <algorithm>
 #include <type_traits>
 
