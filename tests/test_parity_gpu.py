@@ -274,6 +274,23 @@ def test_c5_stack_teacher_forced():
             g = dx
 
 
+@pytest.mark.parametrize("ci,co,k", [(32, 32, 1), (64, 64, 1), (32, 32, 2)])
+def test_wide_runs_across_images(ci, co, k):
+    """bf16 matrix-core convolution with blocks that walk several row tiles:
+    100 images of 48x16 in 3 tiles each (300 tiles), so runs of 2 consecutive
+    tiles continue an image's window (only the new rows are staged) and some
+    cross into the next image (whole window again); every output compared."""
+    rng = np.random.default_rng(1000 * ci + 10 * co + k)
+    N, H, W = 100, 48, 16
+    T = oracle.num_taps(k)
+    x = gen.round_to(rng.normal(size=(N, ci, H, W)), "bf16")
+    w = gen.round_to(rng.normal(size=(co, ci, T)) / np.sqrt(ci * T), "bf16")
+    b = gen.round_to(rng.normal(size=co) * 0.1, "bf16")
+    check_fwd_full(x, w, b, k, 1, "bf16", what="fwd")
+    dy = gen.round_to(rng.normal(size=(N, co, H, W)), "bf16")
+    check_bwd_full(x, w, dy, k, 1, "bf16", what="bwd")
+
+
 # --------------------------------------------------------------- sweeps
 
 SWEEP = [
