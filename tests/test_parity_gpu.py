@@ -291,6 +291,24 @@ def test_wide_runs_across_images(ci, co, k):
     check_bwd_full(x, w, dy, k, 1, "bf16", what="bwd")
 
 
+@pytest.mark.parametrize("N,ci,co,H,k", [(10, 64, 64, 91, 1), (20, 32, 32, 57, 2)])
+def test_wgrad32_regular_runs(N, ci, co, H, k):
+    """bf16 matrix-core weight gradient with regular staging (rows of 128
+    elements, as many input as output channels) over more tiles than blocks:
+    block runs of several tiles, ragged last tiles (H not a multiple of the
+    tile height) and runs crossing into the next image; dw and db compared
+    in full."""
+    rng = np.random.default_rng(N * 1000 + ci + H + k)
+    W = 128
+    x = gen.round_to(rng.normal(size=(N, ci, H, W)), "bf16")
+    dy = gen.round_to(rng.normal(size=(N, co, H, W)), "bf16")
+    dw, db = run_bwd_weight(x, dy, k, 1, "bf16")
+    rw, rb = oracle.conv_bwd_weight(x, dy, k, 1)
+    mw, mb = oracle.conv_bwd_weight(np.abs(x), np.abs(dy), k, 1)
+    check("bf16", dw, rw, mw, "dw")
+    check("bf16", db, rb, mb, "db")
+
+
 # --------------------------------------------------------------- sweeps
 
 SWEEP = [
