@@ -1,5 +1,5 @@
 // k_pool.hip -- hexagonal max / mean pooling, forward and backward, for
-// kernel sizes k <= 2 and strides 1 and 2 (Sec. 2.4: the pool window is the
+// kernel sizes k <= 3 and strides 1 and 2 (Sec. 2.4: the pool window is the
 // size-k hexagon, padded like the convolution; stride as in Sec. 2.3).
 //
 // Forward: persistent blocks walk groups of NP planes, loading the next
@@ -331,8 +331,9 @@ int bwd_opt(const PoolArgs &a, int np) { return cdiv(static_cast<long>(np) * a.H
 bool pool_fast_ok(const ConvShape &sh, Dtype dt)
 {
     const int esz = dt == F32 ? 4 : 2;
-    if (sh.k > 2 || (sh.s != 1 && sh.s != 2) || sh.W % (16 / esz) != 0 || sh.Ho == 0 ||
-        sh.Wo > kPoolThreads)
+    // the 16-byte pad left and right of a staged row holds the k-column halo
+    if (sh.k > 3 || sh.k > 16 / esz || (sh.s != 1 && sh.s != 2) || sh.W % (16 / esz) != 0 ||
+        sh.Ho == 0 || sh.Wo > kPoolThreads)
         return false;
     const PoolArgs a = pool_args(sh, esz);
     // one plane must fit; the backward holds up to 16 outputs per thread
@@ -388,11 +389,13 @@ hipError_t pool_fwd_fast(const void *x, void *y, uint8_t *am, const ConvShape &s
         if (sh.s == 1) {                                                                     \
             if (sh.k == 0) HEX_PF(TT, M, 0, 1);                                              \
             else if (sh.k == 1) HEX_PF(TT, M, 1, 1);                                         \
-            else HEX_PF(TT, M, 2, 1);                                                        \
+            else if (sh.k == 2) HEX_PF(TT, M, 2, 1);                                         \
+            else HEX_PF(TT, M, 3, 1);                                                        \
         } else {                                                                             \
             if (sh.k == 0) HEX_PF(TT, M, 0, 2);                                              \
             else if (sh.k == 1) HEX_PF(TT, M, 1, 2);                                         \
-            else HEX_PF(TT, M, 2, 2);                                                        \
+            else if (sh.k == 2) HEX_PF(TT, M, 2, 2);                                         \
+            else HEX_PF(TT, M, 3, 2);                                                        \
         }                                                                                    \
     } while (0)
     if (dt == F32) {
@@ -420,8 +423,8 @@ hipError_t pool_bwd_fast(const void *dy, const uint8_t *am, const void *relu_y, 
     const int grid = cdiv(a.nplanes, a.NP);
     const size_t lds = plane * a.NP;
 #define HEX_PB(TT, M, KV, SV, OV)                                                            \
-    HEX_LAUNCH((pool_bwd_k<TT, M, KV, SV, OV>), dim3(grid), dim3(kPoolThreads), lds, \
-                       st, static_cast<const TT *>(dy), am, static_cast<const TT *>(relu_y),  \
+    HEX_LAUNCH((pool_bwd_k<TT, M, KV, SV, OV>), dim3(grid), dim3(kPoolThreads), lds,         \
+                       st, static_cast<const TT *>(dy), am, static_cast<const TT *>(relu_y), \
                        static_cast<TT *>(dx), a)
 #define HEX_PB_O(TT, M, KV, SV)                                                              \
     do {                                                                                     \
@@ -436,11 +439,13 @@ hipError_t pool_bwd_fast(const void *dy, const uint8_t *am, const void *relu_y, 
         if (sh.s == 1) {                                                                     \
             if (sh.k == 0) HEX_PB_O(TT, M, 0, 1);                                            \
             else if (sh.k == 1) HEX_PB_O(TT, M, 1, 1);                                       \
-            else HEX_PB_O(TT, M, 2, 1);                                                      \
+            else if (sh.k == 2) HEX_PB_O(TT, M, 2, 1);                                       \
+            else HEX_PB_O(TT, M, 3, 1);                                                      \
         } else {                                                                             \
             if (sh.k == 0) HEX_PB_O(TT, M, 0, 2);                                            \
             else if (sh.k == 1) HEX_PB_O(TT, M, 1, 2);                                       \
-            else HEX_PB_O(TT, M, 2, 2);                                                      \
+            else if (sh.k == 2) HEX_PB_O(TT, M, 2, 2);                                       \
+            else HEX_PB_O(TT, M, 3, 2);                                                      \
         }                                                                                    \
     } while (0)
     if (dt == F32) {

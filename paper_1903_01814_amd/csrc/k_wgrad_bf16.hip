@@ -292,7 +292,7 @@ size_t wg_lds(const ConvShape &sh, const WgTiling &tg) { return wg_lds_bytes(sh,
 
 bool bf16_wgrad_ok(const ConvShape &sh)
 {
-    if (sh.s != 1 || (sh.k != 1 && sh.k != 2) || sh.W % 8 != 0 || sh.W > 256)
+    if (sh.s != 1 || sh.k < 1 || sh.k > 3 || sh.W % 8 != 0 || sh.W > 256)
         return false;
     return wg_lds(sh, wg_tiling(sh, wg_nbw(sh))) <= kWgLdsMax;
 }
@@ -331,8 +331,10 @@ hipError_t bf16_wgrad(const void *x, const void *dy, float *dw, float *db, void 
     } while (0)
     if (sh.k == 1)
         HEX_WG_N(1);
-    else
+    else if (sh.k == 2)
         HEX_WG_N(2);
+    else
+        HEX_WG_N(3);
 #undef HEX_WG_N
 #undef HEX_WG
     hipError_t e = hipGetLastError();

@@ -80,7 +80,7 @@ hipError_t pool_bwd_generic(const void *dy, const uint8_t *am,
                             const void *relu_y, void *dx, const ConvShape &sh,
                             int mode, Dtype dt, hipStream_t st);
 
-// ---- pooling, k <= 2, stride 1 or 2, rows of whole 16-byte chunks ------
+// ---- pooling, k <= 3, stride 1 or 2, rows of whole 16-byte chunks ------
 bool pool_fast_ok(const ConvShape &sh, Dtype dt);
 hipError_t pool_fwd_fast(const void *x, void *y, uint8_t *am, const ConvShape &sh, int mode,
                          Dtype dt, hipStream_t st);
@@ -118,7 +118,7 @@ size_t bf16_wgrad32_workspace(const ConvShape &sh);
 hipError_t bf16_wgrad32(const void *x, const void *dy, float *dw, float *db, void *ws,
                         const ConvShape &sh, hipStream_t st);
 
-// ---- bf16 matrix-core weight gradient (stride 1, k <= 2, W % 8 == 0) ----
+// ---- bf16 matrix-core weight gradient (stride 1, k <= 3, W % 8 == 0) ----
 bool bf16_wgrad_ok(const ConvShape &sh);
 size_t bf16_wgrad_workspace(const ConvShape &sh);
 hipError_t bf16_wgrad(const void *x, const void *dy, float *dw, float *db, void *ws,

@@ -134,7 +134,8 @@ def test_hexconv2d_grad_subsets():
 @pytest.mark.parametrize("dt", ["f32", "bf16"])
 @pytest.mark.parametrize("mode", [hx.HEX_POOL_MAX, hx.HEX_POOL_AVG])
 @pytest.mark.parametrize("case", [(2, 3, 11, 12, 1, 2), (1, 4, 16, 16, 2, 1),
-                                  (2, 5, 24, 24, 1, 2), (1, 2, 9, 7, 0, 1)])
+                                  (2, 5, 24, 24, 1, 2), (1, 2, 9, 7, 0, 1),
+                                  (2, 3, 24, 32, 3, 2)])
 def test_hexpool2d_autograd(case, mode, dt):
     torch = torch_mod()
     hn = pytest.importorskip("paper_1903_01814_amd.nn")

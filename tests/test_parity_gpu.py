@@ -338,6 +338,9 @@ SWEEP = [
     # blocks per row, ragged last tiles
     (2, 64, 64, 37, 128, 1, 1), (1, 32, 32, 19, 128, 2, 1), (3, 64, 64, 9, 64, 1, 1),
     (1, 32, 32, 10, 256, 2, 1),
+    # k = 3 (37 taps): matrix-core weight gradient (forward and data gradient
+    # on the generic kernels)
+    (2, 32, 32, 12, 16, 3, 1), (1, 64, 32, 9, 24, 3, 1), (1, 32, 64, 7, 40, 3, 1),
 ]
 
 
@@ -371,7 +374,10 @@ def test_conv_sweep(case, dt):
                                   (2, 3, 16, 16, 2, 1), (1, 4, 48, 48, 1, 2),
                                   (3, 5, 7, 8, 0, 2), (1, 2, 8, 24, 2, 2),
                                   (1, 70, 24, 32, 1, 1), (2, 3, 5, 16, 1, 2),
-                                  (1, 2, 64, 64, 1, 1)])
+                                  (1, 2, 64, 64, 1, 1),
+                                  # k = 3 (37 taps) on the LDS-staged kernels
+                                  (2, 3, 16, 16, 3, 1), (1, 4, 40, 40, 3, 2),
+                                  (3, 2, 11, 24, 3, 2), (1, 70, 8, 16, 3, 1)])
 def test_pool_sweep(case, mode, dt):
     N, C, H, W, k, s = case
     rng = np.random.default_rng(sum(case) + mode)
