@@ -4,7 +4,8 @@
 //
 // Conv forward: one output pixel per thread, a 2-D output tile per block,
 // the input region of the tile (with its k-wide halo, zero outside the
-// tensor) staged channel by channel in LDS as float.
+// tensor) and the block's weights staged in LDS as float, a few input
+// channels per pair of barriers.
 // Conv backward-data: gather form -- each input pixel looks up, per tap, the
 // output whose window reads it (a lattice test for strides > 1).
 // Weight gradient: per-chunk partial sums in a fixed tree order, then the
@@ -22,31 +23,46 @@ namespace {
 using namespace hexgeom;
 
 constexpr int kThreads = 256;
-constexpr int kCoBlock = 8; // output channels per block (forward)
-constexpr int kCiBlock = 8; // input channels per block (backward-data)
+// Channels per block: output channels (forward) or input channels (data
+// gradient), 8 or 32 by the layer's channel count: every staged input
+// element (forward) or loaded dy element (data gradient) feeds that many
+// accumulators, and the input is staged once per block of channels.
+constexpr int kMaxChanBlock = 32;
 constexpr int kTapGroup = 8; // taps accumulated per pass (weight gradient)
 
 __host__ __device__ inline int region_rows(int TI, int k, int s) { return s * (TI - 1) + (s >> 1) + 2 * k + 1; }
 __host__ __device__ inline int region_cols(int TJ, int k, int s) { return s * (TJ - 1) + 2 * k + 1; }
 
-template <typename T>
+// LDS per channel of a stage: the input region (rounded up to 16 bytes) and
+// the block's weights of that channel as float [T][CB].
+__host__ __device__ inline int fwd_region_floats(int TI, int TJ, int k, int s)
+{
+    return (region_rows(TI, k, s) * region_cols(TJ, k, s) + 3) & ~3;
+}
+
+// G input channels per stage: their regions and weights are staged between
+// one pair of barriers, and each tap's CB weights are read as broadcast
+// 16-byte LDS vectors.
+template <typename T, int CB>
 __global__ __launch_bounds__(kThreads) void conv_fwd_generic_k(
     const T *__restrict__ x, const T *__restrict__ w, const T *__restrict__ b,
-    T *__restrict__ y, ConvShape sh, int relu, int TI, int TJ, int tiles_j)
+    T *__restrict__ y, ConvShape sh, int relu, int TI, int TJ, int tiles_j, int G)
 {
-    extern __shared__ float region[];
+    extern __shared__ __align__(16) float region[];
     __shared__ TapLds tl;
     fill_taps(tl, sh.k);
 
     const int tile = blockIdx.x;
     const int n = blockIdx.y;
-    const int co0 = blockIdx.z * kCoBlock;
+    const int co0 = blockIdx.z * CB;
     const int ti0 = (tile / tiles_j) * TI;
     const int tj0 = (tile % tiles_j) * TJ;
     const int r_lo = sh.s * ti0 - sh.k;
     const int c_lo = sh.s * tj0 - sh.k;
     const int RH = region_rows(TI, sh.k, sh.s);
     const int RW = region_cols(TJ, sh.k, sh.s);
+    const int RF = fwd_region_floats(TI, TJ, sh.k, sh.s);
+    float *wl = region + static_cast<size_t>(G) * RF; // [G][T][CB]
 
     const int li = threadIdx.x / TJ, lj = threadIdx.x % TJ;
     const int i = ti0 + li, j = tj0 + lj;
@@ -58,24 +74,44 @@ __global__ __launch_bounds__(kThreads) void conv_fwd_generic_k(
         par = centre_col(j, sh.s) & 1;
     }
 
-    float acc[kCoBlock];
+    float acc[CB];
 #pragma unroll
-    for (int cb = 0; cb < kCoBlock; ++cb)
+    for (int cb = 0; cb < CB; ++cb)
         acc[cb] = (b != nullptr && co0 + cb < sh.Co) ? to_f(b[co0 + cb]) : 0.f;
 
     const size_t HW = static_cast<size_t>(sh.H) * sh.W;
-    for (int ci = 0; ci < sh.Ci; ++ci) {
+    const int TCB = sh.T * CB;
+    for (int ci0 = 0; ci0 < sh.Ci; ci0 += G) {
+        const int ng = min(G, sh.Ci - ci0);
         __syncthreads();
-        stage_window<8>(region, x + (static_cast<size_t>(n) * sh.Ci + ci) * HW, sh.H, sh.W, r_lo,
-                        c_lo, RH, RW);
+        for (int g = 0; g < ng; ++g)
+            stage_window<8>(region + static_cast<size_t>(g) * RF,
+                            x + (static_cast<size_t>(n) * sh.Ci + ci0 + g) * HW, sh.H, sh.W, r_lo,
+                            c_lo, RH, RW);
+        // weights of output channels co0 .. co0 + CB - 1 (clamped to the
+        // last one; those accumulators are never stored)
+        for (int e = threadIdx.x; e < ng * TCB; e += kThreads) {
+            const int cb = e % CB, rest = e / CB;
+            const int g = rest / sh.T, t = rest - g * sh.T;
+            const int co = min(co0 + cb, sh.Co - 1);
+            wl[e] = to_f(w[(static_cast<size_t>(co) * sh.Ci + ci0 + g) * sh.T + t]);
+        }
         __syncthreads();
         if (active) {
-            for (int t = 0; t < sh.T; ++t) {
-                const float v = region[(rr + tl.drow[par][t]) * RW + cc + tl.dq[t]];
+            for (int g = 0; g < ng; ++g) {
+                const float *rg = region + static_cast<size_t>(g) * RF;
+                const float *wg = wl + g * TCB;
+                for (int t = 0; t < sh.T; ++t) {
+                    const float v = rg[(rr + tl.drow[par][t]) * RW + cc + tl.dq[t]];
+                    const float4 *w4 = reinterpret_cast<const float4 *>(wg + t * CB);
 #pragma unroll
-                for (int cb = 0; cb < kCoBlock; ++cb) {
-                    const int co = min(co0 + cb, sh.Co - 1);
-                    acc[cb] += to_f(w[(static_cast<size_t>(co) * sh.Ci + ci) * sh.T + t]) * v;
+                    for (int q = 0; q < CB / 4; ++q) {
+                        const float4 ww = w4[q];
+                        acc[4 * q] += ww.x * v;
+                        acc[4 * q + 1] += ww.y * v;
+                        acc[4 * q + 2] += ww.z * v;
+                        acc[4 * q + 3] += ww.w * v;
+                    }
                 }
             }
         }
@@ -84,7 +120,7 @@ __global__ __launch_bounds__(kThreads) void conv_fwd_generic_k(
         return;
     const size_t HWo = static_cast<size_t>(sh.Ho) * sh.Wo;
 #pragma unroll
-    for (int cb = 0; cb < kCoBlock; ++cb) {
+    for (int cb = 0; cb < CB; ++cb) {
         const int co = co0 + cb;
         if (co >= sh.Co)
             break;
@@ -95,7 +131,7 @@ __global__ __launch_bounds__(kThreads) void conv_fwd_generic_k(
     }
 }
 
-template <typename T>
+template <typename T, int CB>
 __global__ __launch_bounds__(kThreads) void conv_bwd_data_generic_k(
     const T *__restrict__ dy, const T *__restrict__ w, T *__restrict__ dx, ConvShape sh)
 {
@@ -105,15 +141,15 @@ __global__ __launch_bounds__(kThreads) void conv_bwd_data_generic_k(
 
     const int p = blockIdx.x * kThreads + threadIdx.x;
     const int n = blockIdx.y;
-    const int ci0 = blockIdx.z * kCiBlock;
+    const int ci0 = blockIdx.z * CB;
     if (p >= sh.H * sh.W)
         return;
     const int r = p / sh.W, c = p % sh.W;
     const size_t HWo = static_cast<size_t>(sh.Ho) * sh.Wo;
 
-    float acc[kCiBlock];
+    float acc[CB];
 #pragma unroll
-    for (int cb = 0; cb < kCiBlock; ++cb)
+    for (int cb = 0; cb < CB; ++cb)
         acc[cb] = 0.f;
 
     for (int t = 0; t < sh.T; ++t) {
@@ -124,7 +160,7 @@ __global__ __launch_bounds__(kThreads) void conv_bwd_data_generic_k(
         for (int co = 0; co < sh.Co; ++co) {
             const float g = to_f(dy[(static_cast<size_t>(n) * sh.Co + co) * HWo + o]);
 #pragma unroll
-            for (int cb = 0; cb < kCiBlock; ++cb) {
+            for (int cb = 0; cb < CB; ++cb) {
                 const int ci = min(ci0 + cb, sh.Ci - 1);
                 acc[cb] += to_f(w[(static_cast<size_t>(co) * sh.Ci + ci) * sh.T + t]) * g;
             }
@@ -132,7 +168,7 @@ __global__ __launch_bounds__(kThreads) void conv_bwd_data_generic_k(
     }
     const size_t HW = static_cast<size_t>(sh.H) * sh.W;
 #pragma unroll
-    for (int cb = 0; cb < kCiBlock; ++cb) {
+    for (int cb = 0; cb < CB; ++cb) {
         const int ci = ci0 + cb;
         if (ci >= sh.Ci)
             break;
@@ -298,6 +334,7 @@ __global__ __launch_bounds__(kThreads) void pool_bwd_generic_k(
 inline int cdiv(long a, long b) { return static_cast<int>((a + b - 1) / b); }
 
 constexpr size_t kGenericLdsLimit = 64 * 1024;
+constexpr size_t kGenericStageLds = 40 * 1024; // forward: several channels per stage up to this
 
 void pick_fwd_tile(const ConvShape &sh, int &TI, int &TJ)
 {
@@ -314,6 +351,10 @@ void pick_fwd_tile(const ConvShape &sh, int &TI, int &TJ)
         }
     }
 }
+
+// channels per block for a layer of C channels (see kMaxChanBlock): 32 for
+// wide layers, else 8 (more blocks for the narrow ones)
+int chan_block(int C) { return C >= kMaxChanBlock ? kMaxChanBlock : 8; }
 
 int wgrad_generic_chunks(const ConvShape &sh, int &chunk)
 {
@@ -336,30 +377,50 @@ hipError_t conv_fwd_generic(const void *x, const void *w, const void *b, void *y
     int TI, TJ;
     pick_fwd_tile(sh, TI, TJ);
     const int tiles_i = cdiv(sh.Ho, TI), tiles_j = cdiv(sh.Wo, TJ);
-    const size_t lds = sizeof(float) * static_cast<size_t>(region_rows(TI, sh.k, sh.s)) *
-                       region_cols(TJ, sh.k, sh.s);
-    dim3 grid(tiles_i * tiles_j, sh.N, cdiv(sh.Co, kCoBlock));
+    const int cb = chan_block(sh.Co);
+    // input channels per stage: within kGenericStageLds where more than one fit
+    const size_t per_ch = sizeof(float) * (static_cast<size_t>(fwd_region_floats(TI, TJ, sh.k, sh.s)) +
+                                           static_cast<size_t>(sh.T) * cb);
+    const int G = static_cast<int>(std::max<size_t>(
+        1, std::min<size_t>({kGenericStageLds / per_ch, 8, static_cast<size_t>(sh.Ci)})));
+    const size_t lds = per_ch * G;
+    dim3 grid(tiles_i * tiles_j, sh.N, cdiv(sh.Co, cb));
+#define HEX_FWD_G(TT, CBV)                                                                   \
+    HEX_LAUNCH((conv_fwd_generic_k<TT, CBV>), grid, dim3(kThreads), lds, st, (const TT *)x, \
+               (const TT *)w, (const TT *)b, (TT *)y, sh, relu ? 1 : 0, TI, TJ, tiles_j, G)
+#define HEX_FWD_CB(TT)                                                                       \
+    do {                                                                                     \
+        if (cb == 8) HEX_FWD_G(TT, 8);                                                       \
+        else HEX_FWD_G(TT, kMaxChanBlock);                                                   \
+    } while (0)
     if (dt == F32)
-        HEX_LAUNCH(conv_fwd_generic_k<float>, grid, dim3(kThreads), lds, st,
-                           (const float *)x, (const float *)w, (const float *)b, (float *)y, sh,
-                           relu ? 1 : 0, TI, TJ, tiles_j);
+        HEX_FWD_CB(float);
     else
-        HEX_LAUNCH(conv_fwd_generic_k<bf16raw>, grid, dim3(kThreads), lds, st,
-                           (const bf16raw *)x, (const bf16raw *)w, (const bf16raw *)b,
-                           (bf16raw *)y, sh, relu ? 1 : 0, TI, TJ, tiles_j);
+        HEX_FWD_CB(bf16raw);
+#undef HEX_FWD_CB
+#undef HEX_FWD_G
     return hipGetLastError();
 }
 
 hipError_t conv_bwd_data_generic(const void *dy, const void *w, void *dx, const ConvShape &sh,
                                  Dtype dt, hipStream_t st)
 {
-    dim3 grid(cdiv(static_cast<long>(sh.H) * sh.W, kThreads), sh.N, cdiv(sh.Ci, kCiBlock));
+    const int cb = chan_block(sh.Ci);
+    dim3 grid(cdiv(static_cast<long>(sh.H) * sh.W, kThreads), sh.N, cdiv(sh.Ci, cb));
+#define HEX_BD_G(TT, CBV)                                                                    \
+    HEX_LAUNCH((conv_bwd_data_generic_k<TT, CBV>), grid, dim3(kThreads), 0, st,              \
+               (const TT *)dy, (const TT *)w, (TT *)dx, sh)
+#define HEX_BD_CB(TT)                                                                        \
+    do {                                                                                     \
+        if (cb == 8) HEX_BD_G(TT, 8);                                                        \
+        else HEX_BD_G(TT, kMaxChanBlock);                                                    \
+    } while (0)
     if (dt == F32)
-        HEX_LAUNCH(conv_bwd_data_generic_k<float>, grid, dim3(kThreads), 0, st,
-                           (const float *)dy, (const float *)w, (float *)dx, sh);
+        HEX_BD_CB(float);
     else
-        HEX_LAUNCH(conv_bwd_data_generic_k<bf16raw>, grid, dim3(kThreads), 0, st,
-                           (const bf16raw *)dy, (const bf16raw *)w, (bf16raw *)dx, sh);
+        HEX_BD_CB(bf16raw);
+#undef HEX_BD_CB
+#undef HEX_BD_G
     return hipGetLastError();
 }
 

@@ -98,8 +98,6 @@ class HexPool2dFunction(torch.autograd.Function):
         hx.hexpool_fwd(x, y, am, k, stride, mode)
         ctx.save_for_backward(am)
         ctx.k, ctx.stride, ctx.mode, ctx.in_shape = k, stride, mode, x.shape
-        if am is not None:
-            ctx.mark_non_differentiable(am)
         return y
 
     @staticmethod
