@@ -7,7 +7,8 @@
 // tensor) and the block's weights staged in LDS as float, a few input
 // channels per pair of barriers.
 // Conv backward-data: gather form -- each input pixel looks up, per tap, the
-// output whose window reads it (a lattice test for strides > 1).
+// output whose window reads it (a lattice test for strides > 1); the weights
+// of a few output channels at a time are staged in LDS as float.
 // Weight gradient: per-chunk partial sums in a fixed tree order, then the
 // fixed-order reduction over chunks of k_reduce.hip (deterministic).
 // Pool forward / backward: one output (input) element per thread.
@@ -131,20 +132,22 @@ __global__ __launch_bounds__(kThreads) void conv_fwd_generic_k(
     }
 }
 
+// CC output channels per stage: their weights for the block's CB input
+// channels are staged in LDS as float [CC][T][CB] between one pair of
+// barriers and read as broadcast 16-byte vectors.
 template <typename T, int CB>
 __global__ __launch_bounds__(kThreads) void conv_bwd_data_generic_k(
-    const T *__restrict__ dy, const T *__restrict__ w, T *__restrict__ dx, ConvShape sh)
+    const T *__restrict__ dy, const T *__restrict__ w, T *__restrict__ dx, ConvShape sh, int CC)
 {
+    extern __shared__ __align__(16) float wl[];
     __shared__ TapLds tl;
     fill_taps(tl, sh.k);
-    __syncthreads();
 
     const int p = blockIdx.x * kThreads + threadIdx.x;
     const int n = blockIdx.y;
     const int ci0 = blockIdx.z * CB;
-    if (p >= sh.H * sh.W)
-        return;
-    const int r = p / sh.W, c = p % sh.W;
+    const bool active = p < sh.H * sh.W;
+    const int r = active ? p / sh.W : 0, c = active ? p % sh.W : 0;
     const size_t HWo = static_cast<size_t>(sh.Ho) * sh.Wo;
 
     float acc[CB];
@@ -152,20 +155,41 @@ __global__ __launch_bounds__(kThreads) void conv_bwd_data_generic_k(
     for (int cb = 0; cb < CB; ++cb)
         acc[cb] = 0.f;
 
-    for (int t = 0; t < sh.T; ++t) {
-        int i = 0, j = 0;
-        if (!source_output(r, c, tl.dq[t], tl.ds[t], sh.s, sh.Ho, sh.Wo, i, j))
+    const int TCB = sh.T * CB;
+    for (int co0 = 0; co0 < sh.Co; co0 += CC) {
+        const int nc = min(CC, sh.Co - co0);
+        __syncthreads(); // previous stage read (and the tap table written)
+        for (int e = threadIdx.x; e < nc * TCB; e += kThreads) {
+            const int cb = e % CB, rest = e / CB;
+            const int q = rest / sh.T, t = rest - q * sh.T;
+            const int ci = min(ci0 + cb, sh.Ci - 1); // clamped: never stored
+            wl[e] = to_f(w[(static_cast<size_t>(co0 + q) * sh.Ci + ci) * sh.T + t]);
+        }
+        __syncthreads();
+        if (!active)
             continue;
-        const size_t o = static_cast<size_t>(i) * sh.Wo + j;
-        for (int co = 0; co < sh.Co; ++co) {
-            const float g = to_f(dy[(static_cast<size_t>(n) * sh.Co + co) * HWo + o]);
+        for (int t = 0; t < sh.T; ++t) {
+            int i = 0, j = 0;
+            if (!source_output(r, c, tl.dq[t], tl.ds[t], sh.s, sh.Ho, sh.Wo, i, j))
+                continue;
+            const T *dyo = dy + (static_cast<size_t>(n) * sh.Co + co0) * HWo +
+                           static_cast<size_t>(i) * sh.Wo + j;
+            for (int q = 0; q < nc; ++q) {
+                const float g = to_f(dyo[static_cast<size_t>(q) * HWo]);
+                const float4 *w4 = reinterpret_cast<const float4 *>(wl + (q * sh.T + t) * CB);
 #pragma unroll
-            for (int cb = 0; cb < CB; ++cb) {
-                const int ci = min(ci0 + cb, sh.Ci - 1);
-                acc[cb] += to_f(w[(static_cast<size_t>(co) * sh.Ci + ci) * sh.T + t]) * g;
+                for (int v = 0; v < CB / 4; ++v) {
+                    const float4 ww = w4[v];
+                    acc[4 * v] += ww.x * g;
+                    acc[4 * v + 1] += ww.y * g;
+                    acc[4 * v + 2] += ww.z * g;
+                    acc[4 * v + 3] += ww.w * g;
+                }
             }
         }
     }
+    if (!active)
+        return;
     const size_t HW = static_cast<size_t>(sh.H) * sh.W;
 #pragma unroll
     for (int cb = 0; cb < CB; ++cb) {
@@ -406,10 +430,15 @@ hipError_t conv_bwd_data_generic(const void *dy, const void *w, void *dx, const 
                                  Dtype dt, hipStream_t st)
 {
     const int cb = chan_block(sh.Ci);
+    // output channels per weight stage, within kGenericStageLds
+    const size_t per_co = sizeof(float) * static_cast<size_t>(sh.T) * cb;
+    const int CC = static_cast<int>(std::max<size_t>(
+        1, std::min<size_t>(kGenericStageLds / per_co, static_cast<size_t>(sh.Co))));
+    const size_t lds = per_co * CC;
     dim3 grid(cdiv(static_cast<long>(sh.H) * sh.W, kThreads), sh.N, cdiv(sh.Ci, cb));
 #define HEX_BD_G(TT, CBV)                                                                    \
-    HEX_LAUNCH((conv_bwd_data_generic_k<TT, CBV>), grid, dim3(kThreads), 0, st,              \
-               (const TT *)dy, (const TT *)w, (TT *)dx, sh)
+    HEX_LAUNCH((conv_bwd_data_generic_k<TT, CBV>), grid, dim3(kThreads), lds, st,            \
+               (const TT *)dy, (const TT *)w, (TT *)dx, sh, CC)
 #define HEX_BD_CB(TT)                                                                        \
     do {                                                                                     \
         if (cb == 8) HEX_BD_G(TT, 8);                                                        \
