@@ -29,7 +29,8 @@ constexpr int kThreads = 256;
 // element (forward) or loaded dy element (data gradient) feeds that many
 // accumulators, and the input is staged once per block of channels.
 constexpr int kMaxChanBlock = 32;
-constexpr int kTapGroup = 8; // taps accumulated per pass (weight gradient)
+constexpr int kTapGroup = 8;  // taps accumulated per pass (weight gradient)
+constexpr int kWgCoBlock = 8; // output channels per block (weight gradient)
 
 __host__ __device__ inline int region_rows(int TI, int k, int s) { return s * (TI - 1) + (s >> 1) + 2 * k + 1; }
 __host__ __device__ inline int region_cols(int TJ, int k, int s) { return s * (TJ - 1) + 2 * k + 1; }
@@ -200,70 +201,105 @@ __global__ __launch_bounds__(kThreads) void conv_bwd_data_generic_k(
     }
 }
 
+// Block = (pixel chunk, kWgCoBlock output channels, one input channel): per
+// pixel the dy of the block's output channels and the x under one group of
+// taps feed kWgCoBlock x kTapGroup accumulators.  Sums over the block's
+// threads: a fixed xor-shuffle tree per wave, then the waves in order.
 template <typename T>
 __global__ __launch_bounds__(kThreads) void wgrad_partial_generic_k(
     const T *__restrict__ x, const T *__restrict__ dy, float *__restrict__ part, ConvShape sh,
     int chunk)
 {
+    constexpr int NV = kWgCoBlock * kTapGroup + kWgCoBlock; // tap sums, then bias sums
+    constexpr int kWavesG = kThreads / 64;
     __shared__ TapLds tl;
-    __shared__ float red[kTapGroup + 1][kThreads];
+    __shared__ float red[kWavesG][NV];
     fill_taps(tl, sh.k);
     __syncthreads();
 
-    const int co = blockIdx.y, ci = blockIdx.z;
+    const int co0 = blockIdx.y * kWgCoBlock, ci = blockIdx.z;
     const long HWo = static_cast<long>(sh.Ho) * sh.Wo;
     const long total = HWo * sh.N;
     const long begin = static_cast<long>(blockIdx.x) * chunk;
     const long end = min(begin + chunk, total);
     const size_t HW = static_cast<size_t>(sh.H) * sh.W;
     const bool do_bias = (ci == 0);
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const size_t Jt = static_cast<size_t>(sh.Ci) * sh.T + 1;
 
     for (int tg = 0; tg < sh.T; tg += kTapGroup) {
-        float acc[kTapGroup];
+        float acc[kWgCoBlock][kTapGroup];
+        float accb[kWgCoBlock];
 #pragma unroll
-        for (int u = 0; u < kTapGroup; ++u)
-            acc[u] = 0.f;
-        float accb = 0.f;
+        for (int q = 0; q < kWgCoBlock; ++q) {
+            accb[q] = 0.f;
+#pragma unroll
+            for (int u = 0; u < kTapGroup; ++u)
+                acc[q][u] = 0.f;
+        }
         for (long e = begin + threadIdx.x; e < end; e += kThreads) {
             const int n = static_cast<int>(e / HWo);
             const int o = static_cast<int>(e % HWo);
             const int i = o / sh.Wo, j = o % sh.Wo;
-            const float g = to_f(dy[(static_cast<size_t>(n) * sh.Co + co) * HWo + o]);
+            float g[kWgCoBlock];
+#pragma unroll
+            for (int q = 0; q < kWgCoBlock; ++q)
+                g[q] = co0 + q < sh.Co
+                           ? to_f(dy[(static_cast<size_t>(n) * sh.Co + co0 + q) * HWo + o])
+                           : 0.f;
             const int rc = centre_row(i, j, sh.s), cc = centre_col(j, sh.s);
             const int par = cc & 1;
             const T *plane = x + (static_cast<size_t>(n) * sh.Ci + ci) * HW;
 #pragma unroll
             for (int u = 0; u < kTapGroup; ++u) {
                 const int t = tg + u;
+                float v = 0.f;
                 if (t < sh.T) {
                     const int r = rc + tl.drow[par][t], c = cc + tl.dq[t];
                     if (r >= 0 && r < sh.H && c >= 0 && c < sh.W)
-                        acc[u] += g * to_f(plane[static_cast<size_t>(r) * sh.W + c]);
+                        v = to_f(plane[static_cast<size_t>(r) * sh.W + c]);
                 }
+#pragma unroll
+                for (int q = 0; q < kWgCoBlock; ++q)
+                    acc[q][u] += g[q] * v;
             }
-            if (tg == 0)
-                accb += g;
+            if (tg == 0) {
+#pragma unroll
+                for (int q = 0; q < kWgCoBlock; ++q)
+                    accb[q] += g[q];
+            }
         }
+        // wave sums (fixed xor tree), lane 0 to LDS
 #pragma unroll
-        for (int u = 0; u < kTapGroup; ++u)
-            red[u][threadIdx.x] = acc[u];
-        red[kTapGroup][threadIdx.x] = accb;
-        for (int half = kThreads / 2; half > 0; half >>= 1) {
-            __syncthreads();
-            if (threadIdx.x < half) {
+        for (int q = 0; q < kWgCoBlock; ++q) {
 #pragma unroll
-                for (int u = 0; u <= kTapGroup; ++u)
-                    red[u][threadIdx.x] += red[u][threadIdx.x + half];
+            for (int u = 0; u <= kTapGroup; ++u) {
+                float v = u < kTapGroup ? acc[q][u] : accb[q];
+#pragma unroll
+                for (int m = 32; m > 0; m >>= 1)
+                    v += __shfl_xor(v, m, 64);
+                if (lane == 0)
+                    red[wave][u < kTapGroup ? q * kTapGroup + u : kWgCoBlock * kTapGroup + q] = v;
             }
         }
         __syncthreads();
         // partial layout [e][chunk], e = co * (Ci*T + 1) + col
-        const size_t Jt = static_cast<size_t>(sh.Ci) * sh.T + 1;
-        if (threadIdx.x < kTapGroup && tg + threadIdx.x < sh.T)
-            part[(co * Jt + static_cast<size_t>(ci) * sh.T + tg + threadIdx.x) * gridDim.x +
-                 blockIdx.x] = red[threadIdx.x][0];
-        if (tg == 0 && do_bias && threadIdx.x == 0)
-            part[(co * Jt + Jt - 1) * gridDim.x + blockIdx.x] = red[kTapGroup][0];
+        for (int idx = threadIdx.x; idx < NV; idx += kThreads) {
+            float v = red[0][idx];
+#pragma unroll
+            for (int wv = 1; wv < kWavesG; ++wv)
+                v += red[wv][idx];
+            if (idx < kWgCoBlock * kTapGroup) {
+                const int q = idx / kTapGroup, t = tg + idx % kTapGroup;
+                if (co0 + q < sh.Co && t < sh.T)
+                    part[((co0 + q) * Jt + static_cast<size_t>(ci) * sh.T + t) * gridDim.x +
+                         blockIdx.x] = v;
+            } else {
+                const int q = idx - kWgCoBlock * kTapGroup;
+                if (tg == 0 && do_bias && co0 + q < sh.Co)
+                    part[((co0 + q) * Jt + Jt - 1) * gridDim.x + blockIdx.x] = v;
+            }
+        }
         __syncthreads();
     }
 }
@@ -383,7 +419,7 @@ int chan_block(int C) { return C >= kMaxChanBlock ? kMaxChanBlock : 8; }
 int wgrad_generic_chunks(const ConvShape &sh, int &chunk)
 {
     const long total = static_cast<long>(sh.N) * sh.Ho * sh.Wo;
-    const long pairs = static_cast<long>(sh.Co) * sh.Ci;
+    const long pairs = static_cast<long>(cdiv(sh.Co, kWgCoBlock)) * sh.Ci;
     long nchunks = (2048 + pairs - 1) / pairs;
     nchunks = std::max(1L, std::min(nchunks, (total + 255) / 256));
     nchunks = std::min(nchunks, 65535L);
@@ -467,7 +503,7 @@ hipError_t wgrad_generic(const void *x, const void *dy, float *dw, float *db, vo
     int chunk;
     const int nchunks = wgrad_generic_chunks(sh, chunk);
     float *part = static_cast<float *>(ws);
-    dim3 grid(nchunks, sh.Co, sh.Ci);
+    dim3 grid(nchunks, cdiv(sh.Co, kWgCoBlock), sh.Ci);
     if (dt == F32)
         HEX_LAUNCH(wgrad_partial_generic_k<float>, grid, dim3(kThreads), 0, st,
                            (const float *)x, (const float *)dy, part, sh, chunk);
