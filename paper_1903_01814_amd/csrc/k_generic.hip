@@ -30,7 +30,7 @@ constexpr int kThreads = 256;
 // accumulators, and the input is staged once per block of channels.
 constexpr int kMaxChanBlock = 32;
 constexpr int kTapGroup = 8;  // taps accumulated per pass (weight gradient)
-constexpr int kWgCoBlock = 8; // output channels per block (weight gradient)
+constexpr int kWgCoBlock = 8; // output channels per block (weight gradient, >= 32 channels)
 
 __host__ __device__ inline int region_rows(int TI, int k, int s) { return s * (TI - 1) + (s >> 1) + 2 * k + 1; }
 __host__ __device__ inline int region_cols(int TJ, int k, int s) { return s * (TJ - 1) + 2 * k + 1; }
@@ -201,23 +201,23 @@ __global__ __launch_bounds__(kThreads) void conv_bwd_data_generic_k(
     }
 }
 
-// Block = (pixel chunk, kWgCoBlock output channels, one input channel): per
-// pixel the dy of the block's output channels and the x under one group of
-// taps feed kWgCoBlock x kTapGroup accumulators.  Sums over the block's
+// Block = (pixel chunk, CO output channels, one input channel): per pixel
+// the dy of the block's output channels and the x under one group of taps
+// feed CO x kTapGroup accumulators.  Sums over the block's
 // threads: a fixed xor-shuffle tree per wave, then the waves in order.
-template <typename T>
+template <typename T, int CO>
 __global__ __launch_bounds__(kThreads) void wgrad_partial_generic_k(
     const T *__restrict__ x, const T *__restrict__ dy, float *__restrict__ part, ConvShape sh,
     int chunk)
 {
-    constexpr int NV = kWgCoBlock * kTapGroup + kWgCoBlock; // tap sums, then bias sums
+    constexpr int NV = CO * kTapGroup + CO; // tap sums, then bias sums
     constexpr int kWavesG = kThreads / 64;
     __shared__ TapLds tl;
     __shared__ float red[kWavesG][NV];
     fill_taps(tl, sh.k);
     __syncthreads();
 
-    const int co0 = blockIdx.y * kWgCoBlock, ci = blockIdx.z;
+    const int co0 = blockIdx.y * CO, ci = blockIdx.z;
     const long HWo = static_cast<long>(sh.Ho) * sh.Wo;
     const long total = HWo * sh.N;
     const long begin = static_cast<long>(blockIdx.x) * chunk;
@@ -228,10 +228,10 @@ __global__ __launch_bounds__(kThreads) void wgrad_partial_generic_k(
     const size_t Jt = static_cast<size_t>(sh.Ci) * sh.T + 1;
 
     for (int tg = 0; tg < sh.T; tg += kTapGroup) {
-        float acc[kWgCoBlock][kTapGroup];
-        float accb[kWgCoBlock];
+        float acc[CO][kTapGroup];
+        float accb[CO];
 #pragma unroll
-        for (int q = 0; q < kWgCoBlock; ++q) {
+        for (int q = 0; q < CO; ++q) {
             accb[q] = 0.f;
 #pragma unroll
             for (int u = 0; u < kTapGroup; ++u)
@@ -241,9 +241,9 @@ __global__ __launch_bounds__(kThreads) void wgrad_partial_generic_k(
             const int n = static_cast<int>(e / HWo);
             const int o = static_cast<int>(e % HWo);
             const int i = o / sh.Wo, j = o % sh.Wo;
-            float g[kWgCoBlock];
+            float g[CO];
 #pragma unroll
-            for (int q = 0; q < kWgCoBlock; ++q)
+            for (int q = 0; q < CO; ++q)
                 g[q] = co0 + q < sh.Co
                            ? to_f(dy[(static_cast<size_t>(n) * sh.Co + co0 + q) * HWo + o])
                            : 0.f;
@@ -260,18 +260,18 @@ __global__ __launch_bounds__(kThreads) void wgrad_partial_generic_k(
                         v = to_f(plane[static_cast<size_t>(r) * sh.W + c]);
                 }
 #pragma unroll
-                for (int q = 0; q < kWgCoBlock; ++q)
+                for (int q = 0; q < CO; ++q)
                     acc[q][u] += g[q] * v;
             }
             if (tg == 0) {
 #pragma unroll
-                for (int q = 0; q < kWgCoBlock; ++q)
+                for (int q = 0; q < CO; ++q)
                     accb[q] += g[q];
             }
         }
         // wave sums (fixed xor tree), lane 0 to LDS
 #pragma unroll
-        for (int q = 0; q < kWgCoBlock; ++q) {
+        for (int q = 0; q < CO; ++q) {
 #pragma unroll
             for (int u = 0; u <= kTapGroup; ++u) {
                 float v = u < kTapGroup ? acc[q][u] : accb[q];
@@ -279,7 +279,7 @@ __global__ __launch_bounds__(kThreads) void wgrad_partial_generic_k(
                 for (int m = 32; m > 0; m >>= 1)
                     v += __shfl_xor(v, m, 64);
                 if (lane == 0)
-                    red[wave][u < kTapGroup ? q * kTapGroup + u : kWgCoBlock * kTapGroup + q] = v;
+                    red[wave][u < kTapGroup ? q * kTapGroup + u : CO * kTapGroup + q] = v;
             }
         }
         __syncthreads();
@@ -289,13 +289,13 @@ __global__ __launch_bounds__(kThreads) void wgrad_partial_generic_k(
 #pragma unroll
             for (int wv = 1; wv < kWavesG; ++wv)
                 v += red[wv][idx];
-            if (idx < kWgCoBlock * kTapGroup) {
+            if (idx < CO * kTapGroup) {
                 const int q = idx / kTapGroup, t = tg + idx % kTapGroup;
                 if (co0 + q < sh.Co && t < sh.T)
                     part[((co0 + q) * Jt + static_cast<size_t>(ci) * sh.T + t) * gridDim.x +
                          blockIdx.x] = v;
             } else {
-                const int q = idx - kWgCoBlock * kTapGroup;
+                const int q = idx - CO * kTapGroup;
                 if (tg == 0 && do_bias && co0 + q < sh.Co)
                     part[((co0 + q) * Jt + Jt - 1) * gridDim.x + blockIdx.x] = v;
             }
@@ -416,10 +416,14 @@ void pick_fwd_tile(const ConvShape &sh, int &TI, int &TJ)
 // wide layers, else 8 (more blocks for the narrow ones)
 int chan_block(int C) { return C >= kMaxChanBlock ? kMaxChanBlock : 8; }
 
+// output channels per weight-gradient block: narrow layers keep one channel
+// per block (more blocks, a cheaper block-wide sum)
+int wgrad_co_block(int Co) { return Co >= 32 ? kWgCoBlock : 1; }
+
 int wgrad_generic_chunks(const ConvShape &sh, int &chunk)
 {
     const long total = static_cast<long>(sh.N) * sh.Ho * sh.Wo;
-    const long pairs = static_cast<long>(cdiv(sh.Co, kWgCoBlock)) * sh.Ci;
+    const long pairs = static_cast<long>(cdiv(sh.Co, wgrad_co_block(sh.Co))) * sh.Ci;
     long nchunks = (2048 + pairs - 1) / pairs;
     nchunks = std::max(1L, std::min(nchunks, (total + 255) / 256));
     nchunks = std::min(nchunks, 65535L);
@@ -503,13 +507,17 @@ hipError_t wgrad_generic(const void *x, const void *dy, float *dw, float *db, vo
     int chunk;
     const int nchunks = wgrad_generic_chunks(sh, chunk);
     float *part = static_cast<float *>(ws);
-    dim3 grid(nchunks, cdiv(sh.Co, kWgCoBlock), sh.Ci);
-    if (dt == F32)
-        HEX_LAUNCH(wgrad_partial_generic_k<float>, grid, dim3(kThreads), 0, st,
-                           (const float *)x, (const float *)dy, part, sh, chunk);
-    else
-        HEX_LAUNCH(wgrad_partial_generic_k<bf16raw>, grid, dim3(kThreads), 0, st,
-                           (const bf16raw *)x, (const bf16raw *)dy, part, sh, chunk);
+    const int cob = wgrad_co_block(sh.Co);
+    dim3 grid(nchunks, cdiv(sh.Co, cob), sh.Ci);
+#define HEX_WGG(TT, COV)                                                                     \
+    HEX_LAUNCH((wgrad_partial_generic_k<TT, COV>), grid, dim3(kThreads), 0, st,              \
+               (const TT *)x, (const TT *)dy, part, sh, chunk)
+    if (dt == F32) {
+        if (cob == 1) HEX_WGG(float, 1); else HEX_WGG(float, kWgCoBlock);
+    } else {
+        if (cob == 1) HEX_WGG(bf16raw, 1); else HEX_WGG(bf16raw, kWgCoBlock);
+    }
+#undef HEX_WGG
     hipError_t e = hipGetLastError();
     if (e != hipSuccess)
         return e;
