@@ -49,7 +49,12 @@ struct WgTiling {
     int nparts;             // partial slots (= grid.x)
 };
 
-template <int K, int NBW>
+// SV: the stride when it is 1 (compile-time), else 0 (the stride of sh).
+// At stride s output pixel (i, j) is centred on input row s i + (j & 1)
+// floor(s / 2), column s j: the x window of a tile of TR output rows spans
+// s (TR - 1) + floor(s / 2) + 2K + 1 input rows, and element e of a run of 8
+// pixels sits s e columns after the first (odd pixels floor(s / 2) rows down).
+template <int K, int NBW, int SV>
 __global__ __launch_bounds__(kThreads) void wgrad_bf16_k(
     const bf16raw *__restrict__ x, const bf16raw *__restrict__ dy, float *__restrict__ part,
     ConvShape sh, WgTiling tg)
@@ -59,8 +64,10 @@ __global__ __launch_bounds__(kThreads) void wgrad_bf16_k(
     bf16raw *xs = lds;                                       // [Ci][XCS]
     bf16raw *ds_ = lds + static_cast<size_t>(sh.Ci) * tg.XCS; // [64][DP]
 
-    const int H = sh.H, W = sh.W;
+    const int H = sh.H, W = sh.W, Wo = sh.Wo;
+    const int S = SV ? SV : sh.s, SH = S >> 1;
     const size_t HW = static_cast<size_t>(H) * W;
+    const size_t HWo = static_cast<size_t>(sh.Ho) * Wo;
     const int mg = blockIdx.y % tg.mgroups, ngp = blockIdx.y / tg.mgroups;
     const int co_blk = mg * kMB * 16;
     const int nco = min(kMB * 16, sh.Co - co_blk);
@@ -80,7 +87,7 @@ __global__ __launch_bounds__(kThreads) void wgrad_bf16_k(
         tap_axial(K, t, dq, ds);
         bch[j] = ci;
         boff0[j] = tap_drow(dq, ds, 0) * tg.LCP + dq;
-        boff1[j] = tap_drow(dq, ds, 1) * tg.LCP + dq;
+        boff1[j] = (tap_drow(dq, ds, S & 1) + SH) * tg.LCP + dq;
     }
     floatx4 acc[kMB][NBW];
 #pragma unroll
@@ -92,15 +99,15 @@ __global__ __launch_bounds__(kThreads) void wgrad_bf16_k(
 
     for (int tile = blockIdx.x; tile < tg.ntiles; tile += gridDim.x) {
         const int n = tile / tg.tiles_per_img;
-        const int r0 = (tile - n * tg.tiles_per_img) * tg.TR;
-        const int rows = min(tg.TR, H - r0);
-        const int npix = rows * W;
+        const int r0 = (tile - n * tg.tiles_per_img) * tg.TR; // first output row
+        const int rows = min(tg.TR, sh.Ho - r0);
+        const int npix = rows * Wo;
         __syncthreads(); // previous tile's LDS reads are done
-        // x window rows r0-K .. r0+rows+K-1; plane column c sits at slot
-        // column c + kXO (16-byte aligned), the K halo columns on each side
-        // hold zeros
+        // x window input rows S r0 - K .. S (r0 + rows - 1) + SH + K; plane
+        // column c sits at slot column c + kXO (16-byte aligned), the K halo
+        // columns on each side hold zeros
         {
-            const int LR = rows + 2 * K;
+            const int LR = S * (rows - 1) + SH + 2 * K + 1;
             const int cols8 = W / 8;          // 16-byte column groups of a row
             const int items = sh.Ci * LR * cols8;
             for (int it0 = threadIdx.x; it0 < items; it0 += 4 * kThreads) {
@@ -113,7 +120,7 @@ __global__ __launch_bounds__(kThreads) void wgrad_bf16_k(
                     const int g = live ? it % cols8 : 0;
                     const int rest = live ? it / cols8 : 0;
                     const int rr = rest % LR, ci = rest / LR;
-                    const int r = r0 - K + rr;
+                    const int r = S * r0 - K + rr;
                     const bool ok = live && r >= 0 && r < H;
                     dst[u] = live ? ci * tg.XCS + rr * tg.LCP + kXO + 8 * g : -1;
                     const uint4 q = *reinterpret_cast<const uint4 *>(
@@ -135,7 +142,7 @@ __global__ __launch_bounds__(kThreads) void wgrad_bf16_k(
                 xs[ci * tg.XCS + rr * tg.LCP + cc] = 0;
             }
         }
-        // dy tile: channels co_blk .. co_blk+nco-1, pixels r0*W .. r0*W+npix-1
+        // dy tile: channels co_blk .. co_blk+nco-1, pixels r0*Wo .. r0*Wo+npix-1
         {
             const int n8 = npix / 8;
             const int items = nco * n8;
@@ -149,8 +156,8 @@ __global__ __launch_bounds__(kThreads) void wgrad_bf16_k(
                     const int c = live ? it / n8 : 0, g = live ? it - c * n8 : 0;
                     dst[u] = live ? c * tg.DP + 8 * g : -1;
                     v[u] = *reinterpret_cast<const uint4 *>(
-                        dy + (live ? (static_cast<size_t>(n) * sh.Co + co_blk + c) * HW +
-                                         static_cast<size_t>(r0) * W + 8 * g
+                        dy + (live ? (static_cast<size_t>(n) * sh.Co + co_blk + c) * HWo +
+                                         static_cast<size_t>(r0) * Wo + 8 * g
                                    : 0));
                 }
 #pragma unroll
@@ -164,10 +171,11 @@ __global__ __launch_bounds__(kThreads) void wgrad_bf16_k(
         const int nks = (npix + 31) / 32;
         for (int ks = 0; ks < nks; ++ks) {
             const int p = ks * 32 + 8 * kq; // first pixel of this lane's group of 8
-            const bool pv = p < npix;       // groups never straddle rows (W % 8 == 0)
-            const int pr = pv ? p / W : 0, pc = pv ? p - pr * W : 0;
-            // slot of pixel (pr, pc) in the x window (window row = pr + K)
-            const int s0 = (pr + K) * tg.LCP + pc + kXO;
+            const bool pv = p < npix;       // groups never straddle rows (Wo % 8 == 0)
+            const int pr = pv ? p / Wo : 0, pc = pv ? p - pr * Wo : 0;
+            // slot of the centre of pixel (pr, pc) in the x window (window
+            // row S pr + K, column S pc; pc is even)
+            const int s0 = (S * pr + K) * tg.LCP + S * pc + kXO;
             bf16x8 a[kMB];
 #pragma unroll
             for (int i = 0; i < kMB; ++i) {
@@ -185,13 +193,13 @@ __global__ __launch_bounds__(kThreads) void wgrad_bf16_k(
             }
 #pragma unroll
             for (int j = 0; j < NBW; ++j) {
-                // pixel pc + e has parity (pc + e) & 1 = e & 1 (pc is even)
+                // pixel pc + e is odd for odd e (pc is even)
                 const bf16raw *b0 = xs + bch[j] * tg.XCS + s0 + boff0[j];
                 const bf16raw *b1 = xs + bch[j] * tg.XCS + s0 + boff1[j];
                 shortx8 bs;
 #pragma unroll
                 for (int e = 0; e < 8; ++e)
-                    bs[e] = static_cast<short>((e & 1) ? b1[e] : b0[e]);
+                    bs[e] = static_cast<short>((e & 1) ? b1[S * e] : b0[S * e]);
                 const bool ok = pv && bval[j];
                 const bf16x8 b = __builtin_bit_cast(bf16x8, ok ? bs : shortx8{0, 0, 0, 0, 0, 0, 0, 0});
 #pragma unroll
@@ -242,11 +250,14 @@ inline int cdiv(long a, long b) { return static_cast<int>((a + b - 1) / b); }
 
 constexpr int kWgBlocks = 512; // persistent blocks (x grid.y groups)
 
+// x window rows of a tile of TR output rows
+int wg_win_rows(const ConvShape &sh, int TR) { return sh.s * (TR - 1) + sh.s / 2 + 2 * sh.k + 1; }
+
 size_t wg_lds_bytes(const ConvShape &sh, int TR)
 {
     const long LCP = sh.W + 2 * kXO;
-    const long XCS = (TR + 2 * sh.k) * LCP + 8;
-    const long DP = static_cast<long>(TR) * sh.W + 8;
+    const long XCS = static_cast<long>(wg_win_rows(sh, TR)) * LCP + 8;
+    const long DP = static_cast<long>(TR) * sh.Wo + 8;
     return sizeof(bf16raw) * static_cast<size_t>(sh.Ci * XCS + kMB * 16 * DP);
 }
 
@@ -257,15 +268,15 @@ WgTiling wg_tiling(const ConvShape &sh, int NBW)
 {
     WgTiling tg;
     // tallest full-width tile of at most 256 pixels within the LDS target
-    int TR = std::max(1, std::min(sh.H, 256 / sh.W));
+    int TR = std::max(1, std::min(sh.Ho, 256 / std::max(1, sh.Wo)));
     while (TR > 1 && wg_lds_bytes(sh, TR) > kWgLdsTarget)
         --TR;
     tg.TR = TR;
-    tg.npix_max = tg.TR * sh.W;
-    tg.tiles_per_img = cdiv(sh.H, tg.TR);
+    tg.npix_max = tg.TR * sh.Wo;
+    tg.tiles_per_img = cdiv(sh.Ho, tg.TR);
     tg.ntiles = tg.tiles_per_img * sh.N;
     tg.LCP = sh.W + 2 * kXO;
-    tg.XCS = (tg.TR + 2 * sh.k) * tg.LCP + 8;
+    tg.XCS = wg_win_rows(sh, tg.TR) * tg.LCP + 8;
     tg.DP = tg.npix_max + 8;
     tg.J = sh.Ci * sh.T;
     tg.Jt = tg.J + 1;
@@ -292,7 +303,8 @@ size_t wg_lds(const ConvShape &sh, const WgTiling &tg) { return wg_lds_bytes(sh,
 
 bool bf16_wgrad_ok(const ConvShape &sh)
 {
-    if (sh.s != 1 || sh.k < 1 || sh.k > 3 || sh.W % 8 != 0 || sh.W > 256)
+    if (sh.s < 1 || sh.k < 1 || sh.k > 3 || sh.W % 8 != 0 || sh.W > 256 || sh.Ho < 1 ||
+        sh.Wo % 8 != 0)
         return false;
     return wg_lds(sh, wg_tiling(sh, wg_nbw(sh))) <= kWgLdsMax;
 }
@@ -315,8 +327,12 @@ hipError_t bf16_wgrad(const void *x, const void *dy, float *dw, float *db, void 
     const bf16raw *xp = static_cast<const bf16raw *>(x);
     const bf16raw *dp = static_cast<const bf16raw *>(dy);
     float *part = static_cast<float *>(ws);
+#define HEX_WG_S(KV, NV, SV)                                                                 \
+    HEX_LAUNCH((wgrad_bf16_k<KV, NV, SV>), grid, dim3(kThreads), lds, st, xp, dp, part, sh, tg)
 #define HEX_WG(KV, NV)                                                                       \
-    HEX_LAUNCH((wgrad_bf16_k<KV, NV>), grid, dim3(kThreads), lds, st, xp, dp, part, sh, tg)
+    do {                                                                                     \
+        if (sh.s == 1) HEX_WG_S(KV, NV, 1); else HEX_WG_S(KV, NV, 0);                        \
+    } while (0)
 #define HEX_WG_N(KV)                                                                         \
     do {                                                                                     \
         switch (nbw) {                                                                       \
@@ -337,6 +353,7 @@ hipError_t bf16_wgrad(const void *x, const void *dy, float *dw, float *db, void 
         HEX_WG_N(3);
 #undef HEX_WG_N
 #undef HEX_WG
+#undef HEX_WG_S
     hipError_t e = hipGetLastError();
     if (e != hipSuccess)
         return e;

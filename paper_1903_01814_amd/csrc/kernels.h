@@ -118,7 +118,7 @@ size_t bf16_wgrad32_workspace(const ConvShape &sh);
 hipError_t bf16_wgrad32(const void *x, const void *dy, float *dw, float *db, void *ws,
                         const ConvShape &sh, hipStream_t st);
 
-// ---- bf16 matrix-core weight gradient (stride 1, k <= 3, W % 8 == 0) ----
+// ---- bf16 matrix-core weight gradient (k <= 3, W and W_out % 8 == 0) ---
 bool bf16_wgrad_ok(const ConvShape &sh);
 size_t bf16_wgrad_workspace(const ConvShape &sh);
 hipError_t bf16_wgrad(const void *x, const void *dy, float *dw, float *db, void *ws,

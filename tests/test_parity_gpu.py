@@ -341,6 +341,10 @@ SWEEP = [
     # k = 3 (37 taps): matrix-core weight gradient (forward and data gradient
     # on the generic kernels)
     (2, 32, 32, 12, 16, 3, 1), (1, 64, 32, 9, 24, 3, 1), (1, 32, 64, 7, 40, 3, 1),
+    # strided matrix-core weight gradient (W and W_out multiples of 8):
+    # strides 2 and 3, k 1-3, ragged last tiles
+    (2, 32, 32, 20, 32, 1, 2), (1, 64, 32, 17, 48, 2, 2), (1, 16, 24, 13, 48, 1, 3),
+    (1, 32, 32, 14, 64, 3, 2), (3, 32, 64, 9, 16, 2, 2),
 ]
 
 
