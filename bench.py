@@ -21,7 +21,7 @@ reported in microseconds per call as us_per_step), c3 (hex max and
 average pooling, bf16, GB/s), c4 (wide-channel bf16 convolution, GFLOP/s)
 and c5 (the five-layer bf16 stack, forward and backward, samples/s).
 
-Prints one JSON line.  With --gpus > 1 it exits: this build runs on one GPU.
+Prints one JSON line.  With --gpus > 1 it exits: the library runs on one GPU.
 """
 from __future__ import annotations
 

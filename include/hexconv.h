@@ -66,7 +66,7 @@ extern "C" {
 typedef enum {
     HEX_OK = 0,
     HEX_ERR_INVALID_ARG = -1, /* null pointer, bad size, k, stride, dtype */
-    HEX_ERR_UNSUPPORTED = -2, /* valid request this build cannot run */
+    HEX_ERR_UNSUPPORTED = -2, /* valid request the library does not implement */
     HEX_ERR_LAUNCH = -3       /* a kernel launch reported an error */
 } hex_status;
 

@@ -479,7 +479,7 @@ const char *hex_status_string(int status)
     case HEX_ERR_INVALID_ARG:
         return "HEX_ERR_INVALID_ARG: invalid argument";
     case HEX_ERR_UNSUPPORTED:
-        return "HEX_ERR_UNSUPPORTED: valid request not supported by this build";
+        return "HEX_ERR_UNSUPPORTED: valid request not implemented by the library";
     case HEX_ERR_LAUNCH:
         return "HEX_ERR_LAUNCH: kernel launch failed";
     default:
