@@ -1,5 +1,5 @@
 // k_pool.hip -- hexagonal max / mean pooling, forward and backward, for
-// kernel sizes k <= 3 and strides 1 and 2 (Sec. 2.4: the pool window is the
+// kernel sizes k <= 3 and strides 1 to 4 (Sec. 2.4: the pool window is the
 // size-k hexagon, padded like the convolution; stride as in Sec. 2.3).
 //
 // Forward: persistent blocks walk groups of NP planes, loading the next
@@ -332,7 +332,7 @@ bool pool_fast_ok(const ConvShape &sh, Dtype dt)
 {
     const int esz = dt == F32 ? 4 : 2;
     // the 16-byte pad left and right of a staged row holds the k-column halo
-    if (sh.k > 3 || sh.k > 16 / esz || (sh.s != 1 && sh.s != 2) || sh.W % (16 / esz) != 0 ||
+    if (sh.k > 3 || sh.k > 16 / esz || sh.s < 1 || sh.s > 4 || sh.W % (16 / esz) != 0 ||
         sh.Ho == 0 || sh.Wo > kPoolThreads)
         return false;
     const PoolArgs a = pool_args(sh, esz);
@@ -391,11 +391,24 @@ hipError_t pool_fwd_fast(const void *x, void *y, uint8_t *am, const ConvShape &s
             else if (sh.k == 1) HEX_PF(TT, M, 1, 1);                                         \
             else if (sh.k == 2) HEX_PF(TT, M, 2, 1);                                         \
             else HEX_PF(TT, M, 3, 1);                                                        \
-        } else {                                                                             \
+        }                                                                                    \
+        else if (sh.s == 2) {                                                                \
             if (sh.k == 0) HEX_PF(TT, M, 0, 2);                                              \
             else if (sh.k == 1) HEX_PF(TT, M, 1, 2);                                         \
             else if (sh.k == 2) HEX_PF(TT, M, 2, 2);                                         \
             else HEX_PF(TT, M, 3, 2);                                                        \
+        }                                                                                    \
+        else if (sh.s == 3) {                                                                \
+            if (sh.k == 0) HEX_PF(TT, M, 0, 3);                                              \
+            else if (sh.k == 1) HEX_PF(TT, M, 1, 3);                                         \
+            else if (sh.k == 2) HEX_PF(TT, M, 2, 3);                                         \
+            else HEX_PF(TT, M, 3, 3);                                                        \
+        }                                                                                    \
+        else {                                                                               \
+            if (sh.k == 0) HEX_PF(TT, M, 0, 4);                                              \
+            else if (sh.k == 1) HEX_PF(TT, M, 1, 4);                                         \
+            else if (sh.k == 2) HEX_PF(TT, M, 2, 4);                                         \
+            else HEX_PF(TT, M, 3, 4);                                                        \
         }                                                                                    \
     } while (0)
     if (dt == F32) {
@@ -441,11 +454,24 @@ hipError_t pool_bwd_fast(const void *dy, const uint8_t *am, const void *relu_y, 
             else if (sh.k == 1) HEX_PB_O(TT, M, 1, 1);                                       \
             else if (sh.k == 2) HEX_PB_O(TT, M, 2, 1);                                       \
             else HEX_PB_O(TT, M, 3, 1);                                                      \
-        } else {                                                                             \
+        }                                                                                    \
+        else if (sh.s == 2) {                                                                \
             if (sh.k == 0) HEX_PB_O(TT, M, 0, 2);                                            \
             else if (sh.k == 1) HEX_PB_O(TT, M, 1, 2);                                       \
             else if (sh.k == 2) HEX_PB_O(TT, M, 2, 2);                                       \
             else HEX_PB_O(TT, M, 3, 2);                                                      \
+        }                                                                                    \
+        else if (sh.s == 3) {                                                                \
+            if (sh.k == 0) HEX_PB_O(TT, M, 0, 3);                                            \
+            else if (sh.k == 1) HEX_PB_O(TT, M, 1, 3);                                       \
+            else if (sh.k == 2) HEX_PB_O(TT, M, 2, 3);                                       \
+            else HEX_PB_O(TT, M, 3, 3);                                                      \
+        }                                                                                    \
+        else {                                                                               \
+            if (sh.k == 0) HEX_PB_O(TT, M, 0, 4);                                            \
+            else if (sh.k == 1) HEX_PB_O(TT, M, 1, 4);                                       \
+            else if (sh.k == 2) HEX_PB_O(TT, M, 2, 4);                                       \
+            else HEX_PB_O(TT, M, 3, 4);                                                      \
         }                                                                                    \
     } while (0)
     if (dt == F32) {

@@ -80,7 +80,7 @@ hipError_t pool_bwd_generic(const void *dy, const uint8_t *am,
                             const void *relu_y, void *dx, const ConvShape &sh,
                             int mode, Dtype dt, hipStream_t st);
 
-// ---- pooling, k <= 3, stride 1 or 2, rows of whole 16-byte chunks ------
+// ---- pooling, k <= 3, stride 1 to 4, rows of whole 16-byte chunks -----
 bool pool_fast_ok(const ConvShape &sh, Dtype dt);
 hipError_t pool_fwd_fast(const void *x, void *y, uint8_t *am, const ConvShape &sh, int mode,
                          Dtype dt, hipStream_t st);

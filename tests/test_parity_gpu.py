@@ -381,7 +381,10 @@ def test_conv_sweep(case, dt):
                                   (1, 2, 64, 64, 1, 1),
                                   # k = 3 (37 taps) on the LDS-staged kernels
                                   (2, 3, 16, 16, 3, 1), (1, 4, 40, 40, 3, 2),
-                                  (3, 2, 11, 24, 3, 2), (1, 70, 8, 16, 3, 1)])
+                                  (3, 2, 11, 24, 3, 2), (1, 70, 8, 16, 3, 1),
+                                  # strides 3 and 4 on the LDS-staged kernels
+                                  (1, 3, 20, 24, 1, 3), (2, 2, 17, 32, 2, 4),
+                                  (1, 4, 30, 48, 3, 3), (2, 3, 9, 16, 0, 4)])
 def test_pool_sweep(case, mode, dt):
     N, C, H, W, k, s = case
     rng = np.random.default_rng(sum(case) + mode)
