@@ -24,10 +24,10 @@ namespace {
 using namespace hexgeom;
 
 constexpr int kThreads = 256;
-// Channels per block: output channels (forward) or input channels (data
-// gradient), 8 or 32 by the layer's channel count: every staged input
-// element (forward) or loaded dy element (data gradient) feeds that many
-// accumulators, and the input is staged once per block of channels.
+// Channels per block: output channels (forward: 8, 32 or 64) or input
+// channels (data gradient: 8 or 32) by the layer's channel count: every
+// staged input element (forward) or loaded dy element (data gradient) feeds
+// that many accumulators, and the input is staged once per block of channels.
 constexpr int kMaxChanBlock = 32;
 constexpr int kTapGroup = 8;  // taps accumulated per pass (weight gradient)
 constexpr int kWgCoBlock = 8; // output channels per block (weight gradient, >= 32 channels)
@@ -441,7 +441,7 @@ hipError_t conv_fwd_generic(const void *x, const void *w, const void *b, void *y
     int TI, TJ;
     pick_fwd_tile(sh, TI, TJ);
     const int tiles_i = cdiv(sh.Ho, TI), tiles_j = cdiv(sh.Wo, TJ);
-    const int cb = chan_block(sh.Co);
+    const int cb = sh.Co >= 64 ? 2 * kMaxChanBlock : chan_block(sh.Co);
     // input channels per stage: within kGenericStageLds where more than one fit
     const size_t per_ch = sizeof(float) * (static_cast<size_t>(fwd_region_floats(TI, TJ, sh.k, sh.s)) +
                                            static_cast<size_t>(sh.T) * cb);
@@ -455,7 +455,8 @@ hipError_t conv_fwd_generic(const void *x, const void *w, const void *b, void *y
 #define HEX_FWD_CB(TT)                                                                       \
     do {                                                                                     \
         if (cb == 8) HEX_FWD_G(TT, 8);                                                       \
-        else HEX_FWD_G(TT, kMaxChanBlock);                                                   \
+        else if (cb == 32) HEX_FWD_G(TT, 32);                                                \
+        else HEX_FWD_G(TT, 2 * kMaxChanBlock);                                               \
     } while (0)
     if (dt == F32)
         HEX_FWD_CB(float);
