@@ -24,10 +24,10 @@ namespace {
 using namespace hexgeom;
 
 constexpr int kThreads = 256;
-// Channels per block: output channels (forward: 8, 32 or 64) or input
-// channels (data gradient: 8 or 32) by the layer's channel count: every
-// staged input element (forward) or loaded dy element (data gradient) feeds
-// that many accumulators, and the input is staged once per block of channels.
+// Channels per block: output channels (forward) or input channels (data
+// gradient), 8, 32 or 64 by the layer's channel count: every staged input
+// element (forward) or loaded dy element (data gradient) feeds that many
+// accumulators, and the input is staged once per block of channels.
 constexpr int kMaxChanBlock = 32;
 constexpr int kTapGroup = 8;  // taps accumulated per pass (weight gradient)
 constexpr int kWgCoBlock = 8; // output channels per block (weight gradient, >= 32 channels)
@@ -470,7 +470,7 @@ hipError_t conv_fwd_generic(const void *x, const void *w, const void *b, void *y
 hipError_t conv_bwd_data_generic(const void *dy, const void *w, void *dx, const ConvShape &sh,
                                  Dtype dt, hipStream_t st)
 {
-    const int cb = chan_block(sh.Ci);
+    const int cb = sh.Ci >= 64 ? 2 * kMaxChanBlock : chan_block(sh.Ci);
     // output channels per weight stage, within kGenericStageLds
     const size_t per_co = sizeof(float) * static_cast<size_t>(sh.T) * cb;
     const int CC = static_cast<int>(std::max<size_t>(
@@ -483,7 +483,8 @@ hipError_t conv_bwd_data_generic(const void *dy, const void *w, void *dx, const 
 #define HEX_BD_CB(TT)                                                                        \
     do {                                                                                     \
         if (cb == 8) HEX_BD_G(TT, 8);                                                        \
-        else HEX_BD_G(TT, kMaxChanBlock);                                                    \
+        else if (cb == kMaxChanBlock) HEX_BD_G(TT, kMaxChanBlock);                           \
+        else HEX_BD_G(TT, 2 * kMaxChanBlock);                                                \
     } while (0)
     if (dt == F32)
         HEX_BD_CB(float);
