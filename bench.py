@@ -191,7 +191,7 @@ def bench_conv(args, torch, cfg_key):
     cfg = gen.CONFIGS[cfg_key]
     N, Ci, Co, H, W, k, s = (cfg[n] for n in ("N", "C_in", "C_out", "H", "W", "k", "stride"))
     T = hx.hex_num_taps(k)
-    Ho, Wo = hx.hex_out_shape(H, W, s)
+    Ho, Wo = hx.hex_out_shape(H, W, k, s)
     dt = torch.float32 if cfg["dtype"] == gen.F32 else torch.bfloat16
     esz = 4 if dt == torch.float32 else 2
     per_set = esz * (N * Ci * H * W * 2 + N * Co * Ho * Wo * 2)
@@ -336,7 +336,7 @@ def cpu_baseline_pool(cfg, x, seconds):
 def bench_pool(args, torch, cfg_key):
     cfg = gen.CONFIGS[cfg_key]
     N, C, H, W, k, s = (cfg[n] for n in ("N", "C", "H", "W", "k", "stride"))
-    Ho, Wo = hx.hex_out_shape(H, W, s)
+    Ho, Wo = hx.hex_out_shape(H, W, k, s)
     dt = torch.bfloat16
     esz = 2
     in_b, out_b = esz * N * C * H * W, esz * N * C * Ho * Wo
@@ -410,7 +410,7 @@ def stack_shapes(cfg):
         else:
             _, ci, k, s = layer
             co, relu = ci, False
-        Ho, Wo = hx.hex_out_shape(H, W, s)
+        Ho, Wo = hx.hex_out_shape(H, W, k, s)
         out.append((layer[0], ci, co, k, s, relu, H, W, Ho, Wo))
         H, W = Ho, Wo
     return out

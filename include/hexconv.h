@@ -83,9 +83,13 @@ enum { HEX_FLAG_RELU = 1 };
  * hex_status for k outside [0, HEX_MAX_K]. */
 int hex_num_taps(int k);
 
-/* Output size of an H x W input under stride s (Sec. 2.3).  H_out may be 0
- * when H is too small for the odd output columns.  Returns a hex_status. */
-int hex_out_shape(int H, int W, int stride, int *H_out, int *W_out);
+/* Output size of an H x W input under a size-k kernel and stride s
+ * (Sec. 2.3).  Every window is centred on a tensor element and padding
+ * supplies the taps that fall outside, so the size depends on the stride
+ * only: k is validated (0 .. HEX_MAX_K) and otherwise does not change the
+ * result.  H_out may be 0 when H is too small for the odd output columns.
+ * H_out and W_out are host pointers.  Returns a hex_status. */
+int hex_out_shape(int H, int W, int k, int stride, int *H_out, int *W_out);
 
 /* Tap offsets of a size-k kernel for a centre element in a column of the
  * given parity (0 even, 1 odd): tap t reads element (r + drow[t],
@@ -105,7 +109,9 @@ int hexconv_fwd(const void *x, const void *w, const void *bias, void *y,
 
 /*
  * Gradient of the forward map with respect to x (adjoint of hexconv_fwd
- * without bias):
+ * without bias).  The paper's layers are meant to sit inside CNN models
+ * that are trained by gradient descent (Sec. 2.4, and the networks trained
+ * in Sec. 4); this is the data half of that backward pass:
  *   dx[n][ci][p] = sum over (co, i, j, t) with p_t(i, j) = p of
  *                  w[co][ci][t] * dy[n][co][i][j].
  * dy is [N][C_out][H_out][W_out]; dx is [N][C_in][H][W] in dtype dt.
@@ -120,7 +126,9 @@ size_t hexconv_bwd_weight_workspace(int N, int C_in, int C_out, int H, int W,
                                     int k, int stride, hex_dtype dt);
 
 /*
- * Gradient with respect to the weights and bias:
+ * Gradient with respect to the weights and bias, the parameter half of the
+ * backward pass of a hexagonal convolution layer trained inside a CNN
+ * (Sec. 2.4; the trained networks of Sec. 4):
  *   dw[co][ci][t] = sum_n sum_(i,j) dy[n][co][i][j] * x[n][ci][p_t(i, j)]
  *   db[co]        = sum_n sum_(i,j) dy[n][co][i][j]          (db nullable)
  * dw and db are float32 device buffers.  ws is a device workspace of at
@@ -165,8 +173,9 @@ int hexpool_fwd(const void *x, void *y, uint8_t *argmax_tap, int N, int C,
                 hex_dtype dt, void *stream);
 
 /*
- * Pooling gradient: max routes dy[o] to the element its argmax tap points
- * at (dropped when that tap is padding; argmax_tap required); avg shares
+ * Pooling gradient, the backward pass of the pooling layer of Sec. 2.4 as
+ * used in the trained networks of Sec. 4: max routes dy[o] to the element
+ * its argmax tap points at (dropped when that tap is padding; argmax_tap required); avg shares
  * dy[o] / T over the in-tensor taps.  When relu_y is not NULL (the ReLU
  * output that fed the pool, [N][C][H][W], dtype dt) the result is
  * multiplied by [relu_y > 0].  dx is [N][C][H][W].

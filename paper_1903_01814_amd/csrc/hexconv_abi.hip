@@ -204,10 +204,10 @@ int hex_num_taps(int k)
     return hexgeom::num_taps(k);
 }
 
-int hex_out_shape(int H, int W, int stride, int *H_out, int *W_out)
+int hex_out_shape(int H, int W, int k, int stride, int *H_out, int *W_out)
 {
-    if (H < 1 || W < 1 || stride < 1 || stride > HEX_MAX_STRIDE || H_out == nullptr ||
-        W_out == nullptr)
+    if (H < 1 || W < 1 || k < 0 || k > HEX_MAX_K || stride < 1 || stride > HEX_MAX_STRIDE ||
+        H_out == nullptr || W_out == nullptr)
         return HEX_ERR_INVALID_ARG;
     int ho = 0, wo = 0;
     hexgeom::out_shape(H, W, stride, ho, wo);
@@ -255,6 +255,8 @@ int hexconv_fwd(const void *x, const void *w, const void *bias, void *y, int N, 
         if (d == hexk::BF16 && hexk::bf16_wide_ok(sh, sh.Ci, sh.Co))
             return launched(hexk::bf16_wide_conv(x, w, bias, y, sh, false, relu, st));
     }
+    if (!hexk::conv_fwd_generic_ok(sh))
+        return HEX_ERR_UNSUPPORTED;
     return launched(hexk::conv_fwd_generic(x, w, bias, y, sh, d, relu, st));
 }
 
@@ -281,6 +283,8 @@ int hexconv_bwd_data(const void *dy, const void *w, void *dx, int N, int C_in, i
         if (d == hexk::BF16 && hexk::bf16_wide_ok(sh, sh.Co, sh.Ci))
             return launched(hexk::bf16_wide_conv(dy, w, nullptr, dx, sh, true, false, st));
     }
+    if (!hexk::conv_bwd_data_generic_ok(sh))
+        return HEX_ERR_UNSUPPORTED;
     return launched(hexk::conv_bwd_data_generic(dy, w, dx, sh, d, st));
 }
 

@@ -14,6 +14,7 @@
 // Pool forward / backward: one output (input) element per thread.
 #include <algorithm>
 
+#include "generic_plan.h"
 #include "hexdev.h"
 #include "kernels.h"
 #include "stage.h"
@@ -23,24 +24,13 @@ namespace {
 
 using namespace hexgeom;
 
-constexpr int kThreads = 256;
-// Channels per block: output channels (forward) or input channels (data
-// gradient), 8, 32 or 64 by the layer's channel count: every staged input
-// element (forward) or loaded dy element (data gradient) feeds that many
-// accumulators, and the input is staged once per block of channels.
-constexpr int kMaxChanBlock = 32;
+using plan::kThreads;
+using plan::region_cols;
+using plan::region_rows;
+// Channels per block (plan::chan_block): output channels (forward) or input
+// channels (data gradient), 8, 32 or 64.
 constexpr int kTapGroup = 8;  // taps accumulated per pass (weight gradient)
 constexpr int kWgCoBlock = 8; // output channels per block (weight gradient, >= 32 channels)
-
-__host__ __device__ inline int region_rows(int TI, int k, int s) { return s * (TI - 1) + (s >> 1) + 2 * k + 1; }
-__host__ __device__ inline int region_cols(int TJ, int k, int s) { return s * (TJ - 1) + 2 * k + 1; }
-
-// LDS per channel of a stage: the input region (rounded up to 16 bytes) and
-// the block's weights of that channel as float [T][CB].
-__host__ __device__ inline int fwd_region_floats(int TI, int TJ, int k, int s)
-{
-    return (region_rows(TI, k, s) * region_cols(TJ, k, s) + 3) & ~3;
-}
 
 // G input channels per stage: their regions and weights are staged between
 // one pair of barriers, and each tap's CB weights are read as broadcast
@@ -63,7 +53,7 @@ __global__ __launch_bounds__(kThreads) void conv_fwd_generic_k(
     const int c_lo = sh.s * tj0 - sh.k;
     const int RH = region_rows(TI, sh.k, sh.s);
     const int RW = region_cols(TJ, sh.k, sh.s);
-    const int RF = fwd_region_floats(TI, TJ, sh.k, sh.s);
+    const int RF = plan::region_floats(TI, TJ, sh.k, sh.s);
     float *wl = region + static_cast<size_t>(G) * RF; // [G][T][CB]
 
     const int li = threadIdx.x / TJ, lj = threadIdx.x % TJ;
@@ -393,29 +383,6 @@ __global__ __launch_bounds__(kThreads) void pool_bwd_generic_k(
 
 inline int cdiv(long a, long b) { return static_cast<int>((a + b - 1) / b); }
 
-constexpr size_t kGenericLdsLimit = 64 * 1024;
-constexpr size_t kGenericStageLds = 40 * 1024; // forward: several channels per stage up to this
-
-void pick_fwd_tile(const ConvShape &sh, int &TI, int &TJ)
-{
-    static const int cand[][2] = {{8, 32}, {16, 16}, {4, 64}, {8, 16}, {4, 32}, {4, 16}, {2, 16}, {1, 16}, {1, 8}};
-    TI = 1;
-    TJ = 8;
-    for (auto &c : cand) {
-        const size_t bytes = sizeof(float) * static_cast<size_t>(region_rows(c[0], sh.k, sh.s)) *
-                             region_cols(c[1], sh.k, sh.s);
-        if (bytes <= kGenericLdsLimit) {
-            TI = c[0];
-            TJ = c[1];
-            return;
-        }
-    }
-}
-
-// channels per block for a layer of C channels (see kMaxChanBlock): 32 for
-// wide layers, else 8 (more blocks for the narrow ones)
-int chan_block(int C) { return C >= kMaxChanBlock ? kMaxChanBlock : 8; }
-
 // output channels per weight-gradient block: narrow layers keep one channel
 // per block (more blocks, a cheaper block-wide sum)
 int wgrad_co_block(int Co) { return Co >= 32 ? kWgCoBlock : 1; }
@@ -435,19 +402,25 @@ int wgrad_generic_chunks(const ConvShape &sh, int &chunk)
 
 } // namespace
 
+bool conv_fwd_generic_ok(const ConvShape &sh)
+{
+    return plan::plan_fwd(sh.Ci, sh.Co, sh.k, sh.s).ok;
+}
+
+bool conv_bwd_data_generic_ok(const ConvShape &sh)
+{
+    return plan::plan_bwd_data(sh.Ci, sh.Co, sh.k).ok;
+}
+
 hipError_t conv_fwd_generic(const void *x, const void *w, const void *b, void *y,
                             const ConvShape &sh, Dtype dt, bool relu, hipStream_t st)
 {
-    int TI, TJ;
-    pick_fwd_tile(sh, TI, TJ);
+    const plan::FwdPlan p = plan::plan_fwd(sh.Ci, sh.Co, sh.k, sh.s);
+    if (!p.ok)
+        return hipErrorInvalidConfiguration; // the ABI checks the plan first
+    const int TI = p.TI, TJ = p.TJ, cb = p.cb, G = p.G;
+    const size_t lds = p.lds;
     const int tiles_i = cdiv(sh.Ho, TI), tiles_j = cdiv(sh.Wo, TJ);
-    const int cb = sh.Co >= 64 ? 2 * kMaxChanBlock : chan_block(sh.Co);
-    // input channels per stage: within kGenericStageLds where more than one fit
-    const size_t per_ch = sizeof(float) * (static_cast<size_t>(fwd_region_floats(TI, TJ, sh.k, sh.s)) +
-                                           static_cast<size_t>(sh.T) * cb);
-    const int G = static_cast<int>(std::max<size_t>(
-        1, std::min<size_t>({kGenericStageLds / per_ch, 8, static_cast<size_t>(sh.Ci)})));
-    const size_t lds = per_ch * G;
     dim3 grid(tiles_i * tiles_j, sh.N, cdiv(sh.Co, cb));
 #define HEX_FWD_G(TT, CBV)                                                                   \
     HEX_LAUNCH((conv_fwd_generic_k<TT, CBV>), grid, dim3(kThreads), lds, st, (const TT *)x, \
@@ -456,7 +429,7 @@ hipError_t conv_fwd_generic(const void *x, const void *w, const void *b, void *y
     do {                                                                                     \
         if (cb == 8) HEX_FWD_G(TT, 8);                                                       \
         else if (cb == 32) HEX_FWD_G(TT, 32);                                                \
-        else HEX_FWD_G(TT, 2 * kMaxChanBlock);                                               \
+        else HEX_FWD_G(TT, 64);                                                              \
     } while (0)
     if (dt == F32)
         HEX_FWD_CB(float);
@@ -470,12 +443,11 @@ hipError_t conv_fwd_generic(const void *x, const void *w, const void *b, void *y
 hipError_t conv_bwd_data_generic(const void *dy, const void *w, void *dx, const ConvShape &sh,
                                  Dtype dt, hipStream_t st)
 {
-    const int cb = sh.Ci >= 64 ? 2 * kMaxChanBlock : chan_block(sh.Ci);
-    // output channels per weight stage, within kGenericStageLds
-    const size_t per_co = sizeof(float) * static_cast<size_t>(sh.T) * cb;
-    const int CC = static_cast<int>(std::max<size_t>(
-        1, std::min<size_t>(kGenericStageLds / per_co, static_cast<size_t>(sh.Co))));
-    const size_t lds = per_co * CC;
+    const plan::BwdDataPlan p = plan::plan_bwd_data(sh.Ci, sh.Co, sh.k);
+    if (!p.ok)
+        return hipErrorInvalidConfiguration; // the ABI checks the plan first
+    const int cb = p.cb, CC = p.CC;
+    const size_t lds = p.lds;
     dim3 grid(cdiv(static_cast<long>(sh.H) * sh.W, kThreads), sh.N, cdiv(sh.Ci, cb));
 #define HEX_BD_G(TT, CBV)                                                                    \
     HEX_LAUNCH((conv_bwd_data_generic_k<TT, CBV>), grid, dim3(kThreads), lds, st,            \
@@ -483,8 +455,8 @@ hipError_t conv_bwd_data_generic(const void *dy, const void *w, void *dx, const 
 #define HEX_BD_CB(TT)                                                                        \
     do {                                                                                     \
         if (cb == 8) HEX_BD_G(TT, 8);                                                        \
-        else if (cb == kMaxChanBlock) HEX_BD_G(TT, kMaxChanBlock);                           \
-        else HEX_BD_G(TT, 2 * kMaxChanBlock);                                                \
+        else if (cb == 32) HEX_BD_G(TT, 32);                                                 \
+        else HEX_BD_G(TT, 64);                                                               \
     } while (0)
     if (dt == F32)
         HEX_BD_CB(float);

@@ -61,6 +61,10 @@ hipError_t reduce_chunked(const float *part, int nparts, int Co, int J, float *d
                           hipStream_t st);
 
 // ---- generic kernels: any k, stride, channel count and dtype -----------
+// whether the launch plan of the generic forward / data gradient fits the
+// LDS of a block (checked by the ABI before anything is enqueued)
+bool conv_fwd_generic_ok(const ConvShape &sh);
+bool conv_bwd_data_generic_ok(const ConvShape &sh);
 hipError_t conv_fwd_generic(const void *x, const void *w, const void *b,
                             void *y, const ConvShape &sh, Dtype dt, bool relu,
                             hipStream_t st);

@@ -32,7 +32,7 @@ _IP = ctypes.POINTER(ctypes.c_int)
 _S = ctypes.c_size_t
 SIGNATURES = {
     "hex_num_taps": ([_I], _I),
-    "hex_out_shape": ([_I, _I, _I, _IP, _IP], _I),
+    "hex_out_shape": ([_I, _I, _I, _I, _IP, _IP], _I),
     "hex_tap_table": ([_I, _I, _IP, _IP], _I),
     "hexconv_fwd": ([_P, _P, _P, _P, _I, _I, _I, _I, _I, _I, _I, _I, _I, _P], _I),
     "hexconv_bwd_data": ([_P, _P, _P, _I, _I, _I, _I, _I, _I, _I, _I, _P], _I),
@@ -96,9 +96,9 @@ def hex_num_taps(k: int) -> int:
     return rc
 
 
-def hex_out_shape(H: int, W: int, stride: int):
+def hex_out_shape(H: int, W: int, k: int, stride: int):
     ho, wo = ctypes.c_int(), ctypes.c_int()
-    _ok("hex_out_shape", load().hex_out_shape(H, W, stride, ctypes.byref(ho),
+    _ok("hex_out_shape", load().hex_out_shape(H, W, k, stride, ctypes.byref(ho),
                                               ctypes.byref(wo)))
     return ho.value, wo.value
 
@@ -181,7 +181,7 @@ def hexconv_fwd(x, w, bias, y, k: int, stride: int = 1, relu: bool = False,
     Co = w.shape[0]
     dt = _dtype_code(x)
     T = hex_num_taps(k)
-    Ho, Wo = hex_out_shape(H, W, stride)
+    Ho, Wo = hex_out_shape(H, W, k, stride)
     rc = load().hexconv_fwd(
         _dev(x, "x", dt), _dev(w, "w", dt, (Co, Ci, T)),
         _dev(bias, "bias", dt, (Co,)), _dev(y, "y", dt, (N, Co, Ho, Wo)),
@@ -197,7 +197,7 @@ def hexconv_bwd_data(dy, w, dx, k: int, stride: int = 1, stream=None):
     Co = w.shape[0]
     dt = _dtype_code(dx)
     T = hex_num_taps(k)
-    Ho, Wo = hex_out_shape(H, W, stride)
+    Ho, Wo = hex_out_shape(H, W, k, stride)
     rc = load().hexconv_bwd_data(
         _dev(dy, "dy", dt, (N, Co, Ho, Wo)), _dev(w, "w", dt, (Co, Ci, T)),
         _dev(dx, "dx", dt), N, Ci, Co, H, W, k, stride, dt, _stream(stream))
@@ -220,7 +220,7 @@ def hexconv_bwd_weight(x, dy, dw, db, ws, k: int, stride: int = 1,
     Co = dw.shape[0]
     dt = _dtype_code(x)
     T = hex_num_taps(k)
-    Ho, Wo = hex_out_shape(H, W, stride)
+    Ho, Wo = hex_out_shape(H, W, k, stride)
     if dw.dtype != torch.float32 or (db is not None and db.dtype != torch.float32):
         raise TypeError("hexconv: dw and db must be float32")
     ws_ptr = _dev(ws, "ws")
@@ -247,7 +247,7 @@ def hexconv_bwd(x, dy, w, dx, dw, db, ws, k: int, stride: int = 1,
     Co = dw.shape[0]
     dt = _dtype_code(x)
     T = hex_num_taps(k)
-    Ho, Wo = hex_out_shape(H, W, stride)
+    Ho, Wo = hex_out_shape(H, W, k, stride)
     if dw.dtype != torch.float32 or (db is not None and db.dtype != torch.float32):
         raise TypeError("hexconv: dw and db must be float32")
     ws_ptr = _dev(ws, "ws")
@@ -267,7 +267,7 @@ def hexpool_fwd(x, y, argmax_tap, k: int, stride: int, mode: int,
     torch = _torch()
     N, C, H, W = x.shape
     dt = _dtype_code(x)
-    Ho, Wo = hex_out_shape(H, W, stride)
+    Ho, Wo = hex_out_shape(H, W, k, stride)
     if argmax_tap is not None and argmax_tap.dtype != torch.uint8:
         raise TypeError("hexconv: argmax_tap must be uint8")
     rc = load().hexpool_fwd(
@@ -284,7 +284,7 @@ def hexpool_bwd(dy, argmax_tap, relu_y, dx, k: int, stride: int, mode: int,
     torch = _torch()
     N, C, H, W = dx.shape
     dt = _dtype_code(dx)
-    Ho, Wo = hex_out_shape(H, W, stride)
+    Ho, Wo = hex_out_shape(H, W, k, stride)
     if argmax_tap is not None and argmax_tap.dtype != torch.uint8:
         raise TypeError("hexconv: argmax_tap must be uint8")
     rc = load().hexpool_bwd(

@@ -46,7 +46,7 @@ class HexConv2dFunction(torch.autograd.Function):
         if w.dtype != x.dtype or (b is not None and b.dtype != x.dtype):
             raise TypeError("hex_conv2d: x, weight and bias must share a dtype")
         N, _, H, W = x.shape
-        Ho, Wo = hx.hex_out_shape(H, W, stride)
+        Ho, Wo = hx.hex_out_shape(H, W, k, stride)
         y = _empty((N, w.shape[0], Ho, Wo), x)
         hx.hexconv_fwd(x, w, b, y, k, stride, relu=relu)
         ctx.save_for_backward(x, w, y if relu else None)
@@ -92,7 +92,7 @@ class HexPool2dFunction(torch.autograd.Function):
     def forward(ctx, x, k, stride, mode):
         x = x.contiguous()
         N, C, H, W = x.shape
-        Ho, Wo = hx.hex_out_shape(H, W, stride)
+        Ho, Wo = hx.hex_out_shape(H, W, k, stride)
         y = _empty((N, C, Ho, Wo), x)
         am = _empty(y.shape, x, torch.uint8) if mode == hx.HEX_POOL_MAX else None
         hx.hexpool_fwd(x, y, am, k, stride, mode)

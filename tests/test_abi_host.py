@@ -53,10 +53,14 @@ def test_tap_table_matches_oracle(k, parity):
 
 
 def test_out_shape_matches_oracle():
+    # the output lattice does not depend on the kernel size (centres sit on
+    # tensor elements, Sec. 2.3): every k gives the same shape
     for s in range(1, 9):
         for H in list(range(1, 20)) + [40, 48, 128, 257]:
             for W in list(range(1, 14)) + [40, 48, 128, 255]:
-                assert hx.hex_out_shape(H, W, s) == oracle.out_shape(H, W, s), (H, W, s)
+                want = oracle.out_shape(H, W, s)
+                for k in (0, 1, 5, 8):
+                    assert hx.hex_out_shape(H, W, k, s) == want, (H, W, k, s)
 
 
 def test_status_strings():
@@ -186,8 +190,11 @@ def test_host_helper_errors():
     assert lib.hex_num_taps(-1) == hx.HEX_ERR_INVALID_ARG
     assert lib.hex_num_taps(9) == hx.HEX_ERR_INVALID_ARG
     a, b = ctypes.c_int(), ctypes.c_int()
-    assert lib.hex_out_shape(0, 5, 1, ctypes.byref(a), ctypes.byref(b)) == -1
-    assert lib.hex_out_shape(5, 5, 1, None, ctypes.byref(b)) == -1
+    assert lib.hex_out_shape(0, 5, 1, 1, ctypes.byref(a), ctypes.byref(b)) == -1
+    assert lib.hex_out_shape(5, 5, 1, 1, None, ctypes.byref(b)) == -1
+    assert lib.hex_out_shape(5, 5, -1, 1, ctypes.byref(a), ctypes.byref(b)) == -1
+    assert lib.hex_out_shape(5, 5, 9, 1, ctypes.byref(a), ctypes.byref(b)) == -1
+    assert lib.hex_out_shape(5, 5, 1, 0, ctypes.byref(a), ctypes.byref(b)) == -1
     buf = (ctypes.c_int * 7)()
     assert lib.hex_tap_table(1, 2, buf, buf) == -1
     assert lib.hex_tap_table(1, 0, None, buf) == -1

@@ -37,7 +37,7 @@ def _conv_inputs(cfg, N=None, seed=0):
 def run_fwd(x, w, b, k, s, dt, relu=False):
     torch = torch_mod()
     N, Ci, H, W = x.shape
-    Ho, Wo = hx.hex_out_shape(H, W, s)
+    Ho, Wo = hx.hex_out_shape(H, W, k, s)
     xd, wd = to_dev(x, dt), to_dev(w, dt)
     bd = None if b is None else to_dev(b, dt)
     y = empty((N, w.shape[0], Ho, Wo), dt)
@@ -92,7 +92,7 @@ def run_bwd(x, dy, w, k, s, dt, want_dx=True):
 def run_pool_fwd(x, k, s, mode, dt, want_argmax=True):
     torch = torch_mod()
     N, C, H, W = x.shape
-    Ho, Wo = hx.hex_out_shape(H, W, s)
+    Ho, Wo = hx.hex_out_shape(H, W, k, s)
     y = empty((N, C, Ho, Wo), dt)
     am = torch.full((N, C, Ho, Wo), 255, dtype=torch.uint8,
                     device="cuda:0") if want_argmax else None
@@ -205,8 +205,8 @@ def test_c5_stack_teacher_forced():
     shapes = []
     H, W = cfg["H"], cfg["W"]
     for layer in cfg["layers"]:
-        s = layer[4] if layer[0] == "conv" else layer[3]
-        H, W = hx.hex_out_shape(H, W, s)
+        k, s = (layer[3], layer[4]) if layer[0] == "conv" else (layer[2], layer[3])
+        H, W = hx.hex_out_shape(H, W, k, s)
     d = gen.stack_inputs(cfg, oracle.num_taps, (H, W))
     rng = np.random.default_rng(5)
     acts = [d["x"]]                  # float64 copies of GPU activations
@@ -366,6 +366,65 @@ def test_conv_sweep(case, dt):
         check_bwd_full(x, w, dy, k, s, dt, what="bwd")
 
 
+# Kernel sizes and strides up to the largest the ABI accepts (HEX_MAX_K = 8,
+# HEX_MAX_STRIDE = 8): generic kernels for every op, including a block of
+# 64 output channels at k = 5 and the k = 8 / stride 8 plan with 64 output
+# channels (region plus staged weights within the block's LDS), and the
+# bf16 matrix-core weight gradient at strides 4 and 8 (W and W_out
+# multiples of 8).
+LARGE_K_S = [
+    # N, Ci, Co, H, W, k, s
+    (1, 2, 3, 20, 22, 5, 1), (1, 3, 2, 25, 27, 8, 1), (1, 2, 2, 30, 33, 1, 5),
+    (1, 2, 3, 41, 40, 2, 8), (1, 3, 3, 40, 41, 8, 8), (1, 4, 64, 40, 40, 8, 8),
+    (1, 64, 64, 24, 24, 5, 1), (2, 5, 7, 37, 29, 5, 5), (1, 8, 40, 26, 26, 8, 5),
+    (1, 32, 32, 30, 32, 2, 4), (2, 32, 32, 40, 64, 3, 8), (1, 32, 64, 24, 32, 1, 4),
+]
+
+
+@pytest.mark.parametrize("dt", ["f32", "bf16"])
+@pytest.mark.parametrize("case", LARGE_K_S, ids=lambda c: "N%d_ci%d_co%d_%dx%d_k%d_s%d" % c)
+def test_conv_large_k_and_stride(case, dt):
+    N, Ci, Co, H, W, k, s = case
+    rng = np.random.default_rng(7000 + sum(case))
+    T = oracle.num_taps(k)
+    x = gen.round_to(rng.normal(size=(N, Ci, H, W)), dt)
+    w = gen.round_to(rng.normal(size=(Co, Ci, T)) / np.sqrt(Ci * T), dt)
+    b = gen.round_to(rng.normal(size=Co) * 0.1, dt)
+    Ho, Wo = oracle.out_shape(H, W, s)
+    assert Ho > 0
+    check_fwd_full(x, w, b, k, s, dt, what="fwd")
+    dy = gen.round_to(rng.normal(size=(N, Co, Ho, Wo)), dt)
+    check_bwd_full(x, w, dy, k, s, dt, what="bwd")
+
+
+@pytest.mark.parametrize("dt", ["f32", "bf16"])
+@pytest.mark.parametrize("mode", [hx.HEX_POOL_MAX, hx.HEX_POOL_AVG])
+@pytest.mark.parametrize("case", [(1, 2, 20, 24, 5, 1), (1, 2, 25, 26, 8, 1),
+                                  (2, 2, 30, 32, 1, 5), (1, 3, 40, 41, 2, 8),
+                                  (1, 2, 33, 35, 8, 8), (1, 2, 30, 32, 5, 5)])
+def test_pool_large_k_and_stride(case, mode, dt):
+    N, C, H, W, k, s = case
+    rng = np.random.default_rng(9000 + sum(case) + mode)
+    x = gen.round_to(rng.normal(size=(N, C, H, W)), dt)
+    x[0, 0, : H // 2, : W // 2] = 0.5            # plateaus: exercise ties
+    y, am = run_pool_fwd(x, k, s, mode, dt)
+    ref, ram = oracle.pool_fwd(x, k, s, mode)
+    if mode == hx.HEX_POOL_MAX:
+        np.testing.assert_array_equal(y, ref)
+        np.testing.assert_array_equal(am, ram)
+    elif dt == "bf16":
+        want = round_bf16_f64(ref)
+        assert np.all(np.abs(y - want) <= bf16_ulp(want))
+    else:
+        check_f32(y, ref, "avg pool")
+    dy = gen.round_to(rng.normal(size=ref.shape), dt)
+    for relu_y in (None, np.maximum(x, 0.0)):
+        dx = run_pool_bwd(dy, ram if mode == 0 else None, relu_y, k, s, mode, H, W, dt)
+        rdx = oracle.pool_bwd(dy, ram if mode == 0 else None, relu_y, k, s, mode, H, W)
+        mag = oracle.pool_bwd(np.abs(dy), ram if mode == 0 else None, relu_y, k, s, mode, H, W)
+        check(dt, dx, rdx, mag, "pool bwd")
+
+
 @pytest.mark.parametrize("dt", ["f32", "bf16"])
 @pytest.mark.parametrize("mode", [hx.HEX_POOL_MAX, hx.HEX_POOL_AVG])
 @pytest.mark.parametrize("case", [(2, 3, 9, 10, 1, 2), (1, 4, 40, 40, 1, 2),
@@ -443,7 +502,7 @@ def test_empty_batch_and_empty_output():
     hx.hexconv_fwd(x, w, None, y, 1, 1)
     # H too small for the odd output columns: empty output; gradients are 0
     H, W, k, s = 1, 5, 1, 2
-    assert hx.hex_out_shape(H, W, s) == (0, 3)
+    assert hx.hex_out_shape(H, W, k, s) == (0, 3)
     dy = np.zeros((1, 2, 0, 3))
     dx = run_bwd_data(dy, np.ones((2, 1, 7)), k, s, H, W, "f32")
     assert np.all(dx == 0)
@@ -492,7 +551,7 @@ def test_graph_replay_matches_eager(dt):
     cases = [(8, 1, 16, 40, 40, 2), (2, 32, 64, 24, 24, 2)]
     for (N, Ci, Co, H, W, k) in cases:
         T = hx.hex_num_taps(k)
-        Ho, Wo = hx.hex_out_shape(H, W, 1)
+        Ho, Wo = hx.hex_out_shape(H, W, k, 1)
         x = to_dev(gen.round_to(rng.normal(size=(N, Ci, H, W)), dt), dt)
         w = to_dev(gen.round_to(rng.normal(size=(Co, Ci, T)) * 0.1, dt), dt)
         b = to_dev(gen.round_to(rng.normal(size=Co) * 0.1, dt), dt)
@@ -501,7 +560,7 @@ def test_graph_replay_matches_eager(dt):
         dx = empty((N, Ci, H, W), dt)
         dw = torch.empty((Co, Ci, T), dtype=torch.float32, device="cuda:0")
         db = torch.empty((Co,), dtype=torch.float32, device="cuda:0")
-        yp = empty((N, Co, *hx.hex_out_shape(Ho, Wo, 2)), dt)
+        yp = empty((N, Co, *hx.hex_out_shape(Ho, Wo, 1, 2)), dt)
         am = torch.empty(yp.shape, dtype=torch.uint8, device="cuda:0")
         dxp = empty((N, Co, Ho, Wo), dt)
         nws = hx.hexconv_bwd_weight_workspace(N, Ci, Co, H, W, k, 1,
