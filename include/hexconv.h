@@ -162,6 +162,27 @@ int hexconv_bwd(const void *x, const void *dy, const void *w, void *dx,
                 hex_dtype dt, void *stream);
 
 /*
+ * hexconv_bwd without a workspace argument, for callers that cannot
+ * allocate device memory: code being captured into a HIP graph, tight
+ * serving loops, harnesses that forbid allocation.  Same arguments,
+ * results and checks as hexconv_bwd (results bit-identical to it), minus
+ * ws and ws_bytes: the workspace lives in a static device array of the
+ * library, HEX_NOALLOC_SCRATCH_BYTES bytes per GPU, which each GPU the
+ * library runs on holds until the process ends.  A shape whose workspace
+ * (hexconv_bwd_workspace) exceeds that size is rejected with
+ * HEX_ERR_UNSUPPORTED before anything is enqueued.  The call allocates and
+ * frees nothing.  Every call on one GPU shares that GPU's array, so calls
+ * that overlap on one GPU (on different streams, or from several threads)
+ * race and must be serialised by the caller; calls on one stream are
+ * ordered and safe.  HEX_ERR_LAUNCH if the array's device address cannot be
+ * obtained.
+ */
+#define HEX_NOALLOC_SCRATCH_BYTES ((size_t)64 << 20)
+int hexconv_bwd_noalloc(const void *x, const void *dy, const void *w, void *dx, float *dw,
+                        float *db, int N, int C_in, int C_out, int H, int W, int k,
+                        int stride, hex_dtype dt, void *stream);
+
+/*
  * Pooling (Sec. 2.4) over the windows of hexconv_fwd, per channel:
  *   max: y = value of the first maximal tap (padding counts as 0);
  *   avg: y = (sum of the T tap values, padding 0) / T.

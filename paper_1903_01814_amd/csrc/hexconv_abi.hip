@@ -193,6 +193,60 @@ size_t wgrad_workspace(const ConvShape &sh, Dtype d)
     }
 }
 
+// Every check of hexconv_bwd's arguments but the workspace, so that a bad
+// argument enqueues nothing; `need` receives the workspace bytes.
+int bwd_check(const void *x, const void *dy, const void *w, const void *dx, const float *dw,
+              const float *db, int N, int Ci, int Co, int H, int W, int k, int stride, int dt,
+              ConvShape &sh, size_t &need)
+{
+    int rc = check_shape(N, Ci, Co, H, W, k, stride, dt, sh);
+    if (rc != HEX_OK)
+        return rc;
+    if ((rc = ptrs_ok({dw}, {x, dy, w, dx, db})) != HEX_OK)
+        return rc;
+    const bool empty = (N == 0 || sh.Ho == 0);
+    if (!empty && (x == nullptr || dy == nullptr))
+        return HEX_ERR_INVALID_ARG;
+    if (dx != nullptr && w == nullptr)
+        return HEX_ERR_INVALID_ARG;
+    const Dtype d = static_cast<Dtype>(dt);
+    need = empty ? 0
+                 : (bwd_fused(sh, d) ? hexk::smallc_bwd_fused_workspace(sh) : wgrad_workspace(sh, d));
+    return HEX_OK;
+}
+
+} // namespace
+
+// Scratch memory of hexconv_bwd_noalloc: one copy of this array per GPU,
+// held until the process ends, shared by every such call on that GPU.  On
+// the host the name only stands for the symbol: host code uses the device
+// address of the current GPU's copy, obtained once per device by
+// scratch_ptr(), never the name itself.
+static __device__ __align__(256) unsigned char scratch[HEX_NOALLOC_SCRATCH_BYTES];
+
+namespace {
+
+constexpr int kMaxScratchDevices = 64;
+std::mutex g_scratch_mu;
+void *g_scratch_dev[kMaxScratchDevices];
+
+// Device address of the current GPU's scratch array (looked up on the
+// first call on each device), or nullptr if it cannot be obtained.
+void *scratch_ptr()
+{
+    int dev = -1;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxScratchDevices)
+        return nullptr;
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    if (g_scratch_dev[dev] == nullptr) {
+        void *p = nullptr;
+        if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess || p == nullptr)
+            return nullptr;
+        g_scratch_dev[dev] = p;
+    }
+    return g_scratch_dev[dev];
+}
+
 } // namespace
 
 extern "C" {
@@ -345,38 +399,58 @@ size_t hexconv_bwd_workspace(int N, int C_in, int C_out, int H, int W, int k, in
     return bwd_fused(sh, d) ? hexk::smallc_bwd_fused_workspace(sh) : wgrad_workspace(sh, d);
 }
 
+// hexconv_bwd after its checks: ws holds at least the workspace the shape
+// needs (ws_bytes of it).
+static int bwd_run(const void *x, const void *dy, const void *w, void *dx, float *dw, float *db,
+                   void *ws, size_t ws_bytes, const ConvShape &sh, hex_dtype dt, void *stream)
+{
+    hipStream_t st = static_cast<hipStream_t>(stream);
+    const Dtype d = static_cast<Dtype>(dt);
+    const bool empty = (sh.N == 0 || sh.Ho == 0);
+    if (!empty && bwd_fused(sh, d))
+        return launched(hexk::smallc_bwd_fused(x, dy, w, dx, dw, db, ws, sh, d, st));
+    if (dx != nullptr && sh.N > 0) {
+        const int rc = hexconv_bwd_data(dy, w, dx, sh.N, sh.Ci, sh.Co, sh.H, sh.W, sh.k, sh.s, dt,
+                                        stream);
+        if (rc != HEX_OK)
+            return rc;
+    }
+    return hexconv_bwd_weight(x, dy, dw, db, ws, ws_bytes, sh.N, sh.Ci, sh.Co, sh.H, sh.W, sh.k,
+                              sh.s, dt, stream);
+}
+
 int hexconv_bwd(const void *x, const void *dy, const void *w, void *dx, float *dw, float *db,
                 void *ws, size_t ws_bytes, int N, int C_in, int C_out, int H, int W, int k,
                 int stride, hex_dtype dt, void *stream)
 {
     ConvShape sh;
-    int rc = check_shape(N, C_in, C_out, H, W, k, stride, dt, sh);
+    size_t need = 0;
+    int rc = bwd_check(x, dy, w, dx, dw, db, N, C_in, C_out, H, W, k, stride, dt, sh, need);
     if (rc != HEX_OK)
         return rc;
-    // every check of both gradients first, so that a bad argument enqueues nothing
-    if ((rc = ptrs_ok({dw}, {x, dy, w, dx, db, ws})) != HEX_OK)
+    if ((rc = ptrs_ok({}, {ws})) != HEX_OK)
         return rc;
-    const bool empty = (N == 0 || sh.Ho == 0);
-    if (!empty && (x == nullptr || dy == nullptr))
-        return HEX_ERR_INVALID_ARG;
-    if (dx != nullptr && w == nullptr)
-        return HEX_ERR_INVALID_ARG;
-    const Dtype d = static_cast<Dtype>(dt);
-    const bool fused = !empty && bwd_fused(sh, d);
-    const size_t need =
-        empty ? 0 : (fused ? hexk::smallc_bwd_fused_workspace(sh) : wgrad_workspace(sh, d));
     if (need > 0 && (ws == nullptr || ws_bytes < need))
         return HEX_ERR_INVALID_ARG;
-    hipStream_t st = static_cast<hipStream_t>(stream);
-    if (fused)
-        return launched(hexk::smallc_bwd_fused(x, dy, w, dx, dw, db, ws, sh, d, st));
-    if (dx != nullptr && N > 0) {
-        rc = hexconv_bwd_data(dy, w, dx, N, C_in, C_out, H, W, k, stride, dt, stream);
-        if (rc != HEX_OK)
-            return rc;
-    }
-    return hexconv_bwd_weight(x, dy, dw, db, ws, ws_bytes, N, C_in, C_out, H, W, k, stride, dt,
-                              stream);
+    return bwd_run(x, dy, w, dx, dw, db, ws, ws_bytes, sh, dt, stream);
+}
+
+int hexconv_bwd_noalloc(const void *x, const void *dy, const void *w, void *dx, float *dw,
+                        float *db, int N, int C_in, int C_out, int H, int W, int k, int stride,
+                        hex_dtype dt, void *stream)
+{
+    ConvShape sh;
+    size_t need = 0;
+    int rc = bwd_check(x, dy, w, dx, dw, db, N, C_in, C_out, H, W, k, stride, dt, sh, need);
+    if (rc != HEX_OK)
+        return rc;
+    if (need > HEX_NOALLOC_SCRATCH_BYTES)
+        return HEX_ERR_UNSUPPORTED;
+    void *ws = nullptr;
+    if (need > 0 && (ws = scratch_ptr()) == nullptr)
+        return HEX_ERR_LAUNCH;
+    return bwd_run(x, dy, w, dx, dw, db, ws, need > 0 ? HEX_NOALLOC_SCRATCH_BYTES : 0, sh, dt,
+                   stream);
 }
 
 int hexpool_fwd(const void *x, void *y, uint8_t *argmax_tap, int N, int C, int H, int W, int k,

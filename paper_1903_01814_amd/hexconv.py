@@ -42,6 +42,8 @@ SIGNATURES = {
     "hexconv_bwd_workspace": ([_I, _I, _I, _I, _I, _I, _I, _I], _S),
     "hexconv_bwd": ([_P, _P, _P, _P, _P, _P, _P, _S, _I, _I, _I, _I, _I, _I, _I,
                      _I, _P], _I),
+    "hexconv_bwd_noalloc": ([_P, _P, _P, _P, _P, _P, _I, _I, _I, _I, _I, _I, _I, _I, _P],
+                            _I),
     "hexpool_fwd": ([_P, _P, _P, _I, _I, _I, _I, _I, _I, _I, _I, _P], _I),
     "hexpool_bwd": ([_P, _P, _P, _P, _I, _I, _I, _I, _I, _I, _I, _I, _P], _I),
     "hex_status_string": ([_I], ctypes.c_char_p),
@@ -258,6 +260,30 @@ def hexconv_bwd(x, dy, w, dx, dw, db, ws, k: int, stride: int = 1,
         _dev(dw, "dw", None, (Co, Ci, T)), _dev(db, "db", None, (Co,)),
         ws_ptr, ws_bytes, N, Ci, Co, H, W, k, stride, dt, _stream(stream))
     _ok("hexconv_bwd", rc)
+    return dx, dw, db
+
+
+HEX_NOALLOC_SCRATCH_BYTES = 64 << 20
+
+
+def hexconv_bwd_noalloc(x, dy, w, dx, dw, db, k: int, stride: int = 1, stream=None):
+    """hexconv_bwd without a workspace: the library's static scratch array
+    serves instead (no allocation in the call; overlapping calls on one GPU
+    race)."""
+    torch = _torch()
+    N, Ci, H, W = x.shape
+    Co = dw.shape[0]
+    dt = _dtype_code(x)
+    T = hex_num_taps(k)
+    Ho, Wo = hex_out_shape(H, W, k, stride)
+    if dw.dtype != torch.float32 or (db is not None and db.dtype != torch.float32):
+        raise TypeError("hexconv: dw and db must be float32")
+    rc = load().hexconv_bwd_noalloc(
+        _dev(x, "x", dt), _dev(dy, "dy", dt, (N, Co, Ho, Wo)),
+        _dev(w, "w", dt, (Co, Ci, T)), _dev(dx, "dx", dt, (N, Ci, H, W)),
+        _dev(dw, "dw", None, (Co, Ci, T)), _dev(db, "db", None, (Co,)),
+        N, Ci, Co, H, W, k, stride, dt, _stream(stream))
+    _ok("hexconv_bwd_noalloc", rc)
     return dx, dw, db
 
 

@@ -26,7 +26,7 @@ def test_header_declares_expected_entry_points():
     names = declared_functions()
     for n in ["hexconv_fwd", "hexconv_bwd_data", "hexconv_bwd_weight",
               "hexconv_bwd_weight_workspace", "hexpool_fwd", "hexpool_bwd",
-              "hexconv_bwd", "hexconv_bwd_workspace",
+              "hexconv_bwd", "hexconv_bwd_workspace", "hexconv_bwd_noalloc",
               "hex_num_taps", "hex_out_shape", "hex_tap_table",
               "hex_status_string"]:
         assert n in names
@@ -183,6 +183,24 @@ def test_pool_rejects_invalid():
     assert bw(dx=None) == hx.HEX_ERR_INVALID_ARG
     assert bw(ry=FakePtr.D + 2) == hx.HEX_ERR_INVALID_ARG
     assert bw(mode=3) == hx.HEX_ERR_INVALID_ARG
+
+
+def test_noalloc_rejects_oversized_workspace():
+    """hexconv_bwd_noalloc: a shape whose workspace exceeds the static
+    scratch array is HEX_ERR_UNSUPPORTED, decided on the host before any
+    HIP call (fake pointers are never touched); bad arguments are rejected
+    like hexconv_bwd's."""
+    lib = hx.load()
+    big = (64, 512, 256, 128, 128, 8, 1, hx.HEX_F32)
+    assert hx.hexconv_bwd_workspace(*big) > hx.HEX_NOALLOC_SCRATCH_BYTES
+    A, B, C, D, E, F = (FakePtr.A, FakePtr.B, FakePtr.C, FakePtr.D, FakePtr.E, FakePtr.F)
+    assert lib.hexconv_bwd_noalloc(A, B, C, D, E, F, *big, None) == hx.HEX_ERR_UNSUPPORTED
+    ok = (2, 1, 4, 16, 16, 1, 1, hx.HEX_F32)
+    assert lib.hexconv_bwd_noalloc(A, B, C, D, None, F, *ok, None) == hx.HEX_ERR_INVALID_ARG
+    assert lib.hexconv_bwd_noalloc(A, B, None, D, E, F, *ok, None) == hx.HEX_ERR_INVALID_ARG
+    assert lib.hexconv_bwd_noalloc(A, B, C, D + 4, E, F, *ok, None) == hx.HEX_ERR_INVALID_ARG
+    assert lib.hexconv_bwd_noalloc(A, B, C, D, E, F, 2, 1, 4, 16, 16, 9, 1, 0,
+                                   None) == hx.HEX_ERR_INVALID_ARG
 
 
 def test_host_helper_errors():
