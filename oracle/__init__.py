@@ -66,6 +66,7 @@ def _load():
         "oracle_pool_fwd": [dp, dp, ip, i, i, i, i, i, i, i],
         "oracle_pool_bwd": [dp, ip, dp, dp, i, i, i, i, i, i, i],
         "oracle_threads": [],
+        "oracle_set_threads": [i],
     }
     for name, args in sig.items():
         f = getattr(lib, name)
@@ -141,6 +142,11 @@ def out_shape(H: int, W: int, stride: int):
 
 def threads() -> int:
     return _load().oracle_threads()
+
+
+def set_threads(n: int) -> None:
+    """Threads of the later parallel loops (timing on fewer cores)."""
+    _check(_load().oracle_set_threads(n), "set_threads")
 
 
 # ------------------------------------------------------------- convolution

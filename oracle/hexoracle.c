@@ -561,3 +561,16 @@ int oracle_threads(void)
     }
     return n;
 }
+
+/* Sets the number of threads later parallel loops use (n >= 1); used to
+ * time the reference on one core.  No effect on results. */
+int oracle_set_threads(int n)
+{
+    if (n < 1)
+        return ORACLE_BAD;
+#ifdef _OPENMP
+    extern void omp_set_num_threads(int);
+    omp_set_num_threads(n);
+#endif
+    return ORACLE_OK;
+}

@@ -1,24 +1,35 @@
 """rocprofv3 summaries of the benchmark kernels.
 
-    python -m paper_1903_01814_amd.counters pmc --config c2 --kernel bwd_f32_k
-    python -m paper_1903_01814_amd.counters stats --config c2 --csv <kernel_stats.csv> \
+    python -m paper_1903_01814_amd.counters pmc --config c4 --op bwd --kernel wgrad32_k
+    python -m paper_1903_01814_amd.counters stats --config c4 --csv <kernel_stats.csv> \
         --command "<the rocprofv3 command line>" [--bench-json <bench output>]
 
 `stats` turns a `rocprofv3 --kernel-trace --stats` kernel_stats.csv into
-profiles/kernels_<workload>.txt (one row per kernel: calls, average, min,
-max duration, share of GPU time).
+profiles/kernels_<workload>.txt (one row per kernel instantiation: calls,
+average, min, max duration, share of GPU time).
 
-`pmc` measures the HBM traffic of one kernel:
-runs bench.py (eager launches, a few steps) twice under
-`rocprofv3 --pmc FETCH_SIZE` and `--pmc WRITE_SIZE`, each time followed by a
-plain device-to-device copy of known size (bench.py --calib-copy-mib).  The
-copy calibrates the counters: its bytes read and written over its FETCH_SIZE
-and WRITE_SIZE readings give one scale factor per counter, applied to the
-kernel's per-dispatch average.  The summary goes to
-profiles/counters_<workload>.txt, stamped with the hash of the kernel
-sources; bench.py reports it as roofline.traffic only while the sources are
-unchanged.  rocprofv3 is started as a child process with the Python
-interpreter directly after `--`.
+`pmc` measures one kernel while one op of a workload runs alone: bench.py
+--counter-op <op> (eager launches, after one warm-up step) under four
+rocprofv3 --pmc passes, each a run of its own:
+  1. FETCH_SIZE and 2. WRITE_SIZE -- HBM bytes.  The run ends with a plain
+     device-to-device copy of known size (bench.py --calib-copy-mib); its
+     bytes over its counter readings give one scale factor per counter,
+     applied to the kernel's per-dispatch average.
+  3. SQ_VALU_MFMA_BUSY_CYCLES, SQ_INSTS_VALU_MFMA_MOPS_BF16,
+     SQ_INSTS_VALU_MFMA_MOPS_F32, GRBM_GUI_ACTIVE -- matrix-core busy
+     cycles over (active cycles x 1024 SIMDs) is the MFMA utilisation;
+     MOPS x 512 is the matrix-core FLOP count.
+  4. SQ_INSTS_LDS, SQ_LDS_BANK_CONFLICT, SQ_LDS_IDX_ACTIVE, SQ_INSTS_MFMA,
+     GRBM_GUI_ACTIVE -- LDS instructions issued and cycles lost to bank
+     conflicts.
+rocprofv3 writes one row per counter and dispatch, summed over the
+counter's instances; GRBM_GUI_ACTIVE, counted per XCD, is divided by the 8
+XCDs to give the dispatch's active cycles.  The summary goes to
+profiles/counters_<workload>_<op>_<kernel>.txt with the exact kernel
+instantiation and the hash of the kernel sources; bench.py attaches it to
+its roofline entry only for the same workload, op, kernel and sources.
+rocprofv3 is started as a child process with the Python interpreter
+directly after `--`.
 """
 from __future__ import annotations
 
@@ -34,38 +45,54 @@ sys.path.insert(0, ROOT)
 
 COPY_KERNEL = "__amd_rocclr_copyBuffer"
 COPY_MIB = 1024
+SIMDS = 1024
+XCDS = 8           # GRBM_GUI_ACTIVE comes summed over the 8 XCDs
+
+PASSES = [
+    ("fetch", ["FETCH_SIZE"]),
+    ("write", ["WRITE_SIZE"]),
+    ("mfma", ["SQ_VALU_MFMA_BUSY_CYCLES", "SQ_INSTS_VALU_MFMA_MOPS_BF16",
+              "SQ_INSTS_VALU_MFMA_MOPS_F32", "GRBM_GUI_ACTIVE"]),
+    ("lds", ["SQ_INSTS_LDS", "SQ_LDS_BANK_CONFLICT", "SQ_LDS_IDX_ACTIVE", "SQ_INSTS_MFMA",
+             "GRBM_GUI_ACTIVE"]),
+]
 
 
-def run_pmc(counter, cfg, regex, out_dir, steps):
-    d = os.path.join(out_dir, counter.lower())
-    cmd = ["rocprofv3", "--pmc", counter, "--kernel-include-regex", regex,
-           "--output-format", "csv", "-d", d, "-o", "pmc", "--",
-           sys.executable, os.path.join(ROOT, "bench.py"), "--config", cfg, "--eager",
-           "--steps", str(steps), "--warmup", "1", "--no-cpu-baseline",
-           "--calib-copy-mib", str(COPY_MIB)]
-    env = dict(os.environ, TMPDIR=os.environ.get("TMPDIR", "/tmp"))
-    print("counters: running", " ".join(cmd), flush=True)
-    r = subprocess.run(cmd, cwd="/tmp", env=env, timeout=240)
-    if r.returncode != 0:
-        raise SystemExit("counters: rocprofv3 --pmc %s exited with %d" % (counter, r.returncode))
+def run_pass(tag, counters, cfg, op, regex, out_dir, steps, reuse=False):
+    """One rocprofv3 --pmc pass (or, with reuse, the CSV an earlier run of
+    the same command left in out_dir)."""
+    d = os.path.join(out_dir, tag)
+    cmd = ["rocprofv3", "--pmc"] + counters + [
+        "--kernel-include-regex", regex, "--output-format", "csv", "-d", d, "-o", "pmc", "--",
+        "python3", os.path.join(ROOT, "bench.py"), "--config", cfg, "--counter-op", op,
+        "--steps", str(steps), "--calib-copy-mib", str(COPY_MIB)]
+    rc = 0
+    if not reuse:
+        env = dict(os.environ, TMPDIR=os.environ.get("TMPDIR", "/tmp"))
+        print("counters: running", " ".join(cmd), flush=True)
+        rc = subprocess.run([sys.executable if c == "python3" else c for c in cmd], cwd="/tmp",
+                            env=env, timeout=180).returncode
     files = glob.glob(os.path.join(d, "**", "*counter_collection.csv"), recursive=True)
+    if rc != 0 and not files:
+        raise SystemExit("counters: rocprofv3 --pmc %s exited with %d" % (tag, rc))
     if not files:
         raise SystemExit("counters: no counter_collection.csv under " + d)
     return files[0], " ".join(cmd)
 
 
-def per_dispatch(path, counter):
-    """{kernel base name: [per-dispatch values in dispatch order]} of one
-    counter (summed over the dimension rows of a dispatch)."""
-    acc = {}
+def per_dispatch(path):
+    """{(kernel base name, counter): {dispatch: value}} (rows of one
+    dispatch and counter summed) and {dispatch: full instantiation name}."""
+    acc, inst = {}, {}
     for row in csv.DictReader(open(path)):
-        if row.get("Counter_Name") != counter:
-            continue
-        key = short_name(row["Kernel_Name"]).split("<")[0].split("::")[-1].strip()
-        disp = row.get("Dispatch_Id") or row.get("Correlation_Id")
-        acc.setdefault(key, {}).setdefault(int(disp), 0.0)
-        acc[key][int(disp)] += float(row["Counter_Value"])
-    return {k: [v[d] for d in sorted(v)] for k, v in acc.items()}
+        full = short_name(row["Kernel_Name"])
+        base = full.split("<")[0].strip()
+        cn = row.get("Counter_Name")
+        disp = int(row.get("Dispatch_Id") or row.get("Correlation_Id"))
+        inst[disp] = full
+        slot = acc.setdefault((base, cn), {})
+        slot[disp] = slot.get(disp, 0.0) + float(row["Counter_Value"])
+    return acc, inst
 
 
 def short_name(name):
@@ -109,10 +136,83 @@ def stats(args):
             if lines:
                 b = json.loads(lines[-1])
                 roof = b.get("roofline", {})
-                fo.write("# bench line of the same run: %s %s %s, %.5f ms per step; dominant "
-                         "kernel %s at %.2f us per launch (library event timing)\n"
-                         % (b["metric"], b["value"], b["unit"], b["ms_per_step"],
-                            roof.get("kernel"), 1e3 * roof.get("kernel_ms", 0.0)))
+                fo.write("# bench line of the same run: %s %s, %.5f ms per step; dominant "
+                         "kernel %s (op %s) at %.2f us per launch (library event timing), "
+                         "roofline frac %s\n"
+                         % (b["value"], b["unit"], b["ms_per_step"], roof.get("kernel"),
+                            roof.get("op"), 1e3 * roof.get("kernel_ms", 0.0), roof.get("frac")))
+    print(open(dst).read())
+
+
+def pmc(args):
+    from paper_1903_01814_amd import inputs as gen
+    import bench
+    workload = gen.CONFIGS[args.config]["name"]
+    regex = "%s|%s" % (args.kernel, COPY_KERNEL)
+    cmds, vals, insts = [], {}, set()
+    for tag, counters in PASSES:
+        path, cmd = run_pass(tag, counters, args.config, args.op, regex,
+                             os.path.join(args.out_dir, "%s_%s" % (args.config, args.op)),
+                             args.steps, reuse=args.reuse)
+        cmds.append(cmd)
+        acc, inst = per_dispatch(path)
+        for cn in counters:
+            k = acc.get((args.kernel, cn))
+            if not k:
+                raise SystemExit("counters: %s of %s missing from %s" % (cn, args.kernel, path))
+            disp = sorted(k)[-args.steps:]                # the op's launches
+            insts |= {inst[i] for i in disp}
+            d = [k[i] for i in disp]
+            vals[cn] = sum(d) / len(d)
+            if tag in ("fetch", "write"):
+                c = acc.get((COPY_KERNEL, cn))
+                if not c:
+                    raise SystemExit("counters: calibration copy missing from %s" % path)
+                vals["copy_" + cn] = max(c.values())
+    copy_bytes = COPY_MIB * 1024.0 * 1024.0
+    f_scale = copy_bytes / vals["copy_FETCH_SIZE"]       # bytes per counted unit
+    w_scale = copy_bytes / vals["copy_WRITE_SIZE"]
+    read_b = vals["FETCH_SIZE"] * f_scale
+    write_b = vals["WRITE_SIZE"] * w_scale
+    gui = vals["GRBM_GUI_ACTIVE"] / XCDS
+    mfma_util = vals["SQ_VALU_MFMA_BUSY_CYCLES"] / (gui * SIMDS) if gui > 0 else 0.0
+    mflop = 512.0 * (vals["SQ_INSTS_VALU_MFMA_MOPS_BF16"] + vals["SQ_INSTS_VALU_MFMA_MOPS_F32"])
+    lds_idx = vals["SQ_LDS_IDX_ACTIVE"]
+    conflict_frac = vals["SQ_LDS_BANK_CONFLICT"] / lds_idx if lds_idx > 0 else 0.0
+    dst = os.path.join(args.dest, "counters_%s_%s_%s.txt" % (workload, args.op, args.kernel))
+    with open(dst, "w") as fo:
+        fo.write("# rocprofv3 counters per launch of %s while op %s of workload %s runs alone\n"
+                 % (args.kernel, args.op, workload))
+        fo.write("# commands (run from /tmp, one pass each):\n")
+        for c in cmds:
+            fo.write("#   %s\n" % c)
+        fo.write("# calibration: a %d MiB device-to-device copy (%s) reads and writes %d bytes\n"
+                 % (COPY_MIB, COPY_KERNEL, int(copy_bytes)))
+        fo.write("# one value per counter and dispatch (summed over instances); active cycles "
+                 "= GRBM_GUI_ACTIVE / %d XCDs; mfma_util = SQ_VALU_MFMA_BUSY_CYCLES / (active "
+                 "cycles x %d SIMDs); lds_bank_conflict_frac = SQ_LDS_BANK_CONFLICT / "
+                 "SQ_LDS_IDX_ACTIVE\n" % (XCDS, SIMDS))
+        fo.write("workload: %s\n" % workload)
+        fo.write("op: %s\n" % args.op)
+        fo.write("kernel: %s\n" % args.kernel)
+        fo.write("instantiation: %s\n" % " ; ".join(sorted(insts)))
+        fo.write("source_hash: %s\n" % bench.source_hash())
+        fo.write("launches_averaged: %d (the op's last launches in each pass)\n" % args.steps)
+        for cn in sorted(k for k in vals if not k.startswith("copy_")):
+            fo.write("raw_%s: %.1f\n" % (cn, vals[cn]))
+        fo.write("copy_fetch_size_raw: %.1f\n" % vals["copy_FETCH_SIZE"])
+        fo.write("copy_write_size_raw: %.1f\n" % vals["copy_WRITE_SIZE"])
+        fo.write("fetch_scale_bytes_per_unit: %.4f\n" % f_scale)
+        fo.write("write_scale_bytes_per_unit: %.4f\n" % w_scale)
+        fo.write("hbm_read_bytes_per_launch: %.0f\n" % read_b)
+        fo.write("hbm_write_bytes_per_launch: %.0f\n" % write_b)
+        fo.write("hbm_bytes_per_launch: %.0f\n" % (read_b + write_b))
+        fo.write("active_cycles_per_launch: %.0f\n" % gui)
+        fo.write("mfma_util: %.4f\n" % mfma_util)
+        fo.write("mfma_flop_per_launch: %.0f\n" % mflop)
+        fo.write("lds_insts_per_launch: %.0f\n" % vals["SQ_INSTS_LDS"])
+        fo.write("lds_bank_conflict_cycles_per_launch: %.0f\n" % vals["SQ_LDS_BANK_CONFLICT"])
+        fo.write("lds_bank_conflict_frac: %.4f\n" % conflict_frac)
     print(open(dst).read())
 
 
@@ -121,68 +221,24 @@ def main():
     sub = p.add_subparsers(dest="cmd", required=True)
     q = sub.add_parser("pmc")
     q.add_argument("--config", required=True, choices=["c2", "c3", "c4", "c5"])
+    q.add_argument("--op", required=True, help="op of the workload, as bench.py names it")
     q.add_argument("--kernel", required=True, help="kernel base name, as bench.py reports it")
     q.add_argument("--out-dir", default=os.path.join(ROOT, "gpurun_out", "pmc"))
     q.add_argument("--steps", type=int, default=3)
     q.add_argument("--dest", default=os.path.join(ROOT, "profiles"))
+    q.add_argument("--reuse", action="store_true",
+                   help="summarise the CSVs an earlier run left under --out-dir")
     q = sub.add_parser("stats")
     q.add_argument("--dest", default=os.path.join(ROOT, "profiles"))
-    q.add_argument("--config", required=True, choices=["c2", "c3", "c4", "c5"])
+    q.add_argument("--config", required=True, choices=["c1", "c2", "c3", "c4", "c5"])
     q.add_argument("--csv", required=True)
     q.add_argument("--command", required=True)
     q.add_argument("--bench-json", default=None)
     args = p.parse_args()
     if args.cmd == "stats":
         stats(args)
-        return
-    from paper_1903_01814_amd import inputs as gen
-    import bench
-    workload = gen.CONFIGS[args.config]["name"]
-    regex = "%s|%s" % (args.kernel, COPY_KERNEL)
-    out = {}
-    cmds = []
-    for counter in ("FETCH_SIZE", "WRITE_SIZE"):
-        path, cmd = run_pmc(counter, args.config, regex, os.path.join(args.out_dir, args.config),
-                            args.steps)
-        cmds.append(cmd)
-        vals = per_dispatch(path, counter)
-        if args.kernel not in vals or COPY_KERNEL not in vals:
-            raise SystemExit("counters: %s or %s missing from %s (found %s)"
-                             % (args.kernel, COPY_KERNEL, path, sorted(vals)))
-        # the last `steps` dispatches of the kernel are bench.py's timing pass
-        # of the dominant op (the last launches before the calibration copy),
-        # so they have that op's shape even where the kernel serves others
-        k = vals[args.kernel][-args.steps:]
-        c = max(vals[COPY_KERNEL])   # the calibration copy is the largest copy
-        out[counter] = (sum(k) / len(k), len(k), c)
-    copy_bytes = COPY_MIB * 1024.0 * 1024.0
-    f_kib, n_f, f_copy = out["FETCH_SIZE"]
-    w_kib, n_w, w_copy = out["WRITE_SIZE"]
-    f_scale = copy_bytes / f_copy          # bytes per counted KiB unit
-    w_scale = copy_bytes / w_copy
-    read_b = f_kib * f_scale
-    write_b = w_kib * w_scale
-    dst = os.path.join(args.dest, "counters_%s.txt" % workload)
-    with open(dst, "w") as fo:
-        fo.write("# HBM traffic per launch of %s, workload %s, from rocprofv3 counters\n"
-                 % (args.kernel, workload))
-        fo.write("# commands (run from /tmp):\n#   %s\n#   %s\n" % (cmds[0], cmds[1]))
-        fo.write("# calibration: a %d MiB device-to-device copy (%s) read and wrote %d bytes\n"
-                 % (COPY_MIB, COPY_KERNEL, int(copy_bytes)))
-        fo.write("kernel: %s\n" % args.kernel)
-        fo.write("source_hash: %s\n" % bench.source_hash())
-        fo.write("dispatches: %d (FETCH_SIZE), %d (WRITE_SIZE): the last ones of the run, "
-                 "from bench.py's timing pass of the dominant op\n" % (n_f, n_w))
-        fo.write("fetch_size_raw_per_launch: %.1f\n" % f_kib)
-        fo.write("write_size_raw_per_launch: %.1f\n" % w_kib)
-        fo.write("copy_fetch_size_raw: %.1f\n" % f_copy)
-        fo.write("copy_write_size_raw: %.1f\n" % w_copy)
-        fo.write("fetch_scale_bytes_per_unit: %.4f\n" % f_scale)
-        fo.write("write_scale_bytes_per_unit: %.4f\n" % w_scale)
-        fo.write("hbm_read_bytes_per_launch: %.0f\n" % read_b)
-        fo.write("hbm_write_bytes_per_launch: %.0f\n" % write_b)
-        fo.write("hbm_bytes_per_launch: %.0f\n" % (read_b + write_b))
-    print(open(dst).read())
+    else:
+        pmc(args)
 
 
 if __name__ == "__main__":
