@@ -67,6 +67,12 @@ def _load():
         "oracle_pool_bwd": [dp, ip, dp, dp, i, i, i, i, i, i, i],
         "oracle_threads": [],
         "oracle_set_threads": [i],
+        "oracle_out_shape3d": [i, i, i, i, i, ip, ip, ip],
+        "oracle_conv3d_fwd": [dp, dp, dp, dp] + [i] * 10,
+        "oracle_conv3d_bwd_data": [dp, dp, dp] + [i] * 10,
+        "oracle_conv3d_bwd_weight": [dp, dp, dp, dp] + [i] * 10,
+        "oracle_pool3d_fwd": [dp, dp, ip] + [i] * 10,
+        "oracle_pool3d_bwd": [dp, ip, dp, dp] + [i] * 10,
     }
     for name, args in sig.items():
         f = getattr(lib, name)
@@ -248,4 +254,73 @@ def pool_bwd(dy, argmax, relu_y, k, stride, mode, H, W):
     dx = np.empty((N, C, H, W), np.float64)
     _check(_load().oracle_pool_bwd(_d(dy), _i(am), _d(relu_y), _d(dx), N, C,
                                    H, W, k, stride, mode), "pool_bwd")
+    return dx
+
+
+# -------------------------------------------------------- three dimensions
+# x[N][C][D][H][W]; kernel of size (k, kz): the size-k hexagonal window in
+# the plane times the planes dz = -kz .. kz; w[C_out][C_in][2kz+1][T];
+# plane stride stride_z (hexoracle.c, "three dimensions").
+
+def out_shape3d(D: int, H: int, W: int, stride: int, stride_z: int):
+    do, ho, wo = ctypes.c_int(), ctypes.c_int(), ctypes.c_int()
+    _check(_load().oracle_out_shape3d(D, H, W, stride, stride_z, ctypes.byref(do),
+                                      ctypes.byref(ho), ctypes.byref(wo)), "out_shape3d")
+    return do.value, ho.value, wo.value
+
+
+def conv3d_fwd(x, w, b, k, kz, stride=1, stride_z=1):
+    x, w, b = _f64(x), _f64(w), _f64(b)
+    N, Ci, D, H, W = x.shape
+    Co = w.shape[0]
+    assert w.shape == (Co, Ci, 2 * kz + 1, num_taps(k))
+    Do, Ho, Wo = out_shape3d(D, H, W, stride, stride_z)
+    y = np.empty((N, Co, Do, Ho, Wo), np.float64)
+    _check(_load().oracle_conv3d_fwd(_d(x), _d(w), _d(b), _d(y), N, Ci, Co, D, H, W, k, kz,
+                                     stride, stride_z), "conv3d_fwd")
+    return y
+
+
+def conv3d_bwd_data(dy, w, k, kz, stride, stride_z, D, H, W):
+    dy, w = _f64(dy), _f64(w)
+    N, Co = dy.shape[:2]
+    Ci = w.shape[1]
+    assert dy.shape[2:] == out_shape3d(D, H, W, stride, stride_z)
+    dx = np.empty((N, Ci, D, H, W), np.float64)
+    _check(_load().oracle_conv3d_bwd_data(_d(dy), _d(w), _d(dx), N, Ci, Co, D, H, W, k, kz,
+                                          stride, stride_z), "conv3d_bwd_data")
+    return dx
+
+
+def conv3d_bwd_weight(x, dy, k, kz, stride=1, stride_z=1):
+    x, dy = _f64(x), _f64(dy)
+    N, Ci, D, H, W = x.shape
+    Co = dy.shape[1]
+    dw = np.empty((Co, Ci, 2 * kz + 1, num_taps(k)), np.float64)
+    db = np.empty(Co, np.float64)
+    _check(_load().oracle_conv3d_bwd_weight(_d(x), _d(dy), _d(dw), _d(db), N, Ci, Co, D, H,
+                                            W, k, kz, stride, stride_z), "conv3d_bwd_weight")
+    return dw, db
+
+
+def pool3d_fwd(x, k, kz, stride, stride_z, mode):
+    """Returns (y, argmax int32: (dz + kz) * T + t of the first maximal tap)."""
+    x = _f64(x)
+    N, C, D, H, W = x.shape
+    Do, Ho, Wo = out_shape3d(D, H, W, stride, stride_z)
+    y = np.empty((N, C, Do, Ho, Wo), np.float64)
+    am = np.empty((N, C, Do, Ho, Wo), np.int32)
+    _check(_load().oracle_pool3d_fwd(_d(x), _d(y), _i(am), N, C, D, H, W, k, kz, stride,
+                                     stride_z, mode), "pool3d_fwd")
+    return y, am
+
+
+def pool3d_bwd(dy, argmax, relu_y, k, kz, stride, stride_z, mode, D, H, W):
+    dy = _f64(dy)
+    relu_y = _f64(relu_y)
+    N, C = dy.shape[:2]
+    am = None if argmax is None else np.ascontiguousarray(argmax, np.int32)
+    dx = np.empty((N, C, D, H, W), np.float64)
+    _check(_load().oracle_pool3d_bwd(_d(dy), _i(am), _d(relu_y), _d(dx), N, C, D, H, W, k, kz,
+                                     stride, stride_z, mode), "pool3d_bwd")
     return dx

@@ -224,3 +224,71 @@ def parity_tables(k):
             tab.append((r - r0, c - c0))
         out[par] = tab
     return out
+
+
+# ------------------------------------------------------------ three dimensions
+# Sec. 2.4: hexagonal x-y planes, equidistant samples along z.  Here the z
+# axis is modelled as its own equidistant lattice: plane d sits at height d;
+# the window of a centre plane z0 holds the planes at heights z0 - kz ..
+# z0 + kz that exist (others read zero), and the centres are reached by
+# steps of stride_z from the first plane.
+
+def z_centres(D: int, stride_z: int):
+    out, z = [], 0
+    while z < D:
+        out.append(z)
+        z += stride_z
+    return out
+
+
+def conv3d_fwd(x, w, b, k, kz, stride=1, stride_z=1):
+    x = np.asarray(x, np.float64)
+    N, Ci, D, H, W = x.shape
+    Co = w.shape[0]
+    win, Ho, Wo, T = _windows(H, W, k, stride)
+    zc = z_centres(D, stride_z)
+    assert w.shape == (Co, Ci, 2 * kz + 1, T)
+    y = np.zeros((N, Co, len(zc), Ho, Wo))
+    for n in range(N):
+        for co in range(Co):
+            for l, z0 in enumerate(zc):
+                for i in range(Ho):
+                    for j in range(Wo):
+                        acc = 0.0 if b is None else float(b[co])
+                        for ci in range(Ci):
+                            for h in range(-kz, kz + 1):
+                                if not 0 <= z0 + h < D:
+                                    continue
+                                for t, e in enumerate(win[i][j]):
+                                    if e is not None:
+                                        acc += w[co, ci, h + kz, t] * x[n, ci, z0 + h, e[0], e[1]]
+                        y[n, co, l, i, j] = acc
+    return y
+
+
+def pool3d_fwd(x, k, kz, stride, stride_z, mode):
+    """mode 0 = max (value of the first maximal tap, planes in ascending
+    height, padding counts as 0), 1 = average over all (2kz+1) T taps."""
+    x = np.asarray(x, np.float64)
+    N, C, D, H, W = x.shape
+    win, Ho, Wo, T = _windows(H, W, k, stride)
+    zc = z_centres(D, stride_z)
+    y = np.zeros((N, C, len(zc), Ho, Wo))
+    am = np.zeros(y.shape, np.int32)
+    for n in range(N):
+        for ch in range(C):
+            for l, z0 in enumerate(zc):
+                for i in range(Ho):
+                    for j in range(Wo):
+                        vals = []
+                        for h in range(-kz, kz + 1):
+                            for e in win[i][j]:
+                                inside = e is not None and 0 <= z0 + h < D
+                                vals.append(x[n, ch, z0 + h, e[0], e[1]] if inside else 0.0)
+                        if mode == 0:
+                            best = max(vals)
+                            am[n, ch, l, i, j] = vals.index(best)
+                            y[n, ch, l, i, j] = best
+                        else:
+                            y[n, ch, l, i, j] = sum(vals) / len(vals)
+    return y, am

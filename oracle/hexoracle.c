@@ -545,6 +545,317 @@ int oracle_pool_bwd(const double *dy, const int *argmax, const double *relu_y,
     return bad ? ORACLE_BAD : ORACLE_OK;
 }
 
+/* ------------------------------------------------------ three dimensions */
+
+/*
+ * Three-dimensional operations (Sec. 2.4, "Software Functionalities"): the
+ * x-y planes are hexagonal, in the addressing above, and the samples along
+ * z are equidistant (e.g. the time slices of a hexagonal camera).  The paper
+ * gives no further detail; readings adopted:
+ *  - tensors x[N][C][D][H][W]: D planes along z, each an H x W hexagonal
+ *    plane;
+ *  - a kernel of size (k, kz) is the size-k hexagonal window in the plane
+ *    times the 2kz+1 planes dz = -kz .. kz around the centre plane; taps are
+ *    numbered dz-major (dz ascending), the hexagonal taps in canonical order
+ *    inside; weights w[C_out][C_in][2kz+1][T];
+ *  - padding and stride follow the 2-D rule along z as well: windows are
+ *    centred on real planes only and planes outside the tensor read zero;
+ *    the centres are the planes sz*l, l = 0, 1, ... while sz*l < D, so
+ *    D_out = floor((D-1)/sz) + 1 (equal steps from the first plane);
+ *  - pooling: maximum or average over the (2kz+1)*T taps, padded taps
+ *    counting as zeros; the average divides by (2kz+1)*T; the maximum keeps
+ *    the first maximal tap in the order above, its index (dz+kz)*T + t.
+ */
+
+int oracle_out_shape3d(int D, int H, int W, int stride, int stride_z, int *Do,
+                       int *Ho, int *Wo)
+{
+    if (D < 1 || stride_z < 1 || oracle_out_shape(H, W, stride, Ho, Wo))
+        return ORACLE_BAD;
+    long l = 0;
+    while ((long)stride_z * l < D)
+        l++;
+    *Do = (int)l;
+    return ORACLE_OK;
+}
+
+typedef struct {
+    int N, Ci, Co, D, H, W, Do, Ho, Wo, kz, Z, stride, stride_z;
+    taps_t tp;
+} shape3d_t;
+
+static int shape3d_make(int N, int Ci, int Co, int D, int H, int W, int k,
+                        int kz, int stride, int stride_z, shape3d_t *sh)
+{
+    if (N < 0 || Ci < 1 || Co < 1 || kz < 0 ||
+        oracle_out_shape3d(D, H, W, stride, stride_z, &sh->Do, &sh->Ho, &sh->Wo)
+        || taps_make(k, &sh->tp))
+        return ORACLE_BAD;
+    sh->N = N;
+    sh->Ci = Ci;
+    sh->Co = Co;
+    sh->D = D;
+    sh->H = H;
+    sh->W = W;
+    sh->kz = kz;
+    sh->Z = 2 * kz + 1;
+    sh->stride = stride;
+    sh->stride_z = stride_z;
+    return ORACLE_OK;
+}
+
+/* plane z of channel ch of image n in x[N][C][D][H][W] */
+static const double *plane3d(const double *x, const shape3d_t *sh, long n,
+                             long ch, long C, long z)
+{
+    return x + ((n * C + ch) * sh->D + z) * (long)sh->H * sh->W;
+}
+
+/* y[n][co][l][i][j] = b[co] + sum_ci sum_dz sum_t w[co][ci][dz][t] * x[n][ci][sz*l+dz][centre + tap t] */
+static double conv3d_fwd_one(const double *x, const double *w, const double *b,
+                             const shape3d_t *sh, long n, long co, long l,
+                             long i, long j)
+{
+    long q0, s0;
+    centre_axial(i, j, sh->stride, &q0, &s0);
+    const long z0 = (long)sh->stride_z * l;
+    const int T = sh->tp.T;
+    double acc = b ? b[co] : 0.0;
+    for (long ci = 0; ci < sh->Ci; ci++)
+        for (long dz = -sh->kz; dz <= sh->kz; dz++) {
+            const long z = z0 + dz;
+            if (z < 0 || z >= sh->D)
+                continue;
+            const double *plane = plane3d(x, sh, n, ci, sh->Ci, z);
+            for (int t = 0; t < T; t++) {
+                int inside;
+                double v = tap_value(plane, sh->H, sh->W, q0 + sh->tp.dq[t],
+                                     s0 + sh->tp.ds[t], &inside);
+                if (inside)
+                    acc += w[((co * sh->Ci + ci) * sh->Z + (dz + sh->kz)) * T + t] * v;
+            }
+        }
+    return acc;
+}
+
+int oracle_conv3d_fwd(const double *x, const double *w, const double *b,
+                      double *y, int N, int Ci, int Co, int D, int H, int W,
+                      int k, int kz, int stride, int stride_z)
+{
+    shape3d_t sh;
+    if (shape3d_make(N, Ci, Co, D, H, W, k, kz, stride, stride_z, &sh))
+        return ORACLE_BAD;
+    const long Do = sh.Do, Ho = sh.Ho, Wo = sh.Wo;
+#pragma omp parallel for collapse(3) schedule(static)
+    for (long n = 0; n < N; n++)
+        for (long co = 0; co < Co; co++)
+            for (long l = 0; l < Do; l++)
+                for (long i = 0; i < Ho; i++)
+                    for (long j = 0; j < Wo; j++)
+                        y[(((n * Co + co) * Do + l) * Ho + i) * Wo + j] =
+                            conv3d_fwd_one(x, w, b, &sh, n, co, l, i, j);
+    taps_free(&sh.tp);
+    return ORACLE_OK;
+}
+
+/*
+ * Gradient with respect to x: the adjoint of the forward sum -- every
+ * product w[co][ci][dz][t] * x[n][ci][sz*l+dz][centre(i,j) + tap t] sends
+ * dy[n][co][l][i][j] * w[co][ci][dz][t] back to that input element.
+ */
+int oracle_conv3d_bwd_data(const double *dy, const double *w, double *dx,
+                           int N, int Ci, int Co, int D, int H, int W, int k,
+                           int kz, int stride, int stride_z)
+{
+    shape3d_t sh;
+    if (shape3d_make(N, Ci, Co, D, H, W, k, kz, stride, stride_z, &sh))
+        return ORACLE_BAD;
+    const long Do = sh.Do, Ho = sh.Ho, Wo = sh.Wo;
+    const int T = sh.tp.T;
+    memset(dx, 0, sizeof(double) * (size_t)N * Ci * D * H * W);
+#pragma omp parallel for schedule(static)
+    for (long n = 0; n < N; n++)
+        for (long co = 0; co < Co; co++)
+            for (long l = 0; l < Do; l++)
+                for (long i = 0; i < Ho; i++)
+                    for (long j = 0; j < Wo; j++) {
+                        const double g = dy[(((n * Co + co) * Do + l) * Ho + i) * Wo + j];
+                        long q0, s0;
+                        centre_axial(i, j, stride, &q0, &s0);
+                        for (long ci = 0; ci < Ci; ci++)
+                            for (long dz = -kz; dz <= kz; dz++) {
+                                const long z = (long)stride_z * l + dz;
+                                if (z < 0 || z >= D)
+                                    continue;
+                                for (int t = 0; t < T; t++) {
+                                    long r, c;
+                                    to_offset(q0 + sh.tp.dq[t], s0 + sh.tp.ds[t], &r, &c);
+                                    if (r < 0 || r >= H || c < 0 || c >= W)
+                                        continue;
+                                    dx[(((n * Ci + ci) * D + z) * H + r) * W + c] +=
+                                        g * w[((co * Ci + ci) * sh.Z + (dz + kz)) * T + t];
+                                }
+                            }
+                    }
+    taps_free(&sh.tp);
+    return ORACLE_OK;
+}
+
+/* dw[co][ci][dz][t] = sum_n sum_(l,i,j) dy[n][co][l][i][j] * x[n][ci][sz*l+dz][centre + tap t];
+ * db[co] = sum_n sum_(l,i,j) dy[n][co][l][i][j] */
+int oracle_conv3d_bwd_weight(const double *x, const double *dy, double *dw,
+                             double *db, int N, int Ci, int Co, int D, int H,
+                             int W, int k, int kz, int stride, int stride_z)
+{
+    shape3d_t sh;
+    if (shape3d_make(N, Ci, Co, D, H, W, k, kz, stride, stride_z, &sh))
+        return ORACLE_BAD;
+    const long Do = sh.Do, Ho = sh.Ho, Wo = sh.Wo;
+    const int T = sh.tp.T, Z = sh.Z;
+#pragma omp parallel for collapse(3) schedule(dynamic, 1)
+    for (long co = 0; co < Co; co++)
+        for (long ci = 0; ci < Ci; ci++)
+            for (long zt = 0; zt < (long)Z * T; zt++) {
+                const long dz = zt / T - kz;
+                const int t = (int)(zt % T);
+                double acc = 0.0;
+                for (long n = 0; n < N; n++)
+                    for (long l = 0; l < Do; l++) {
+                        const long z = (long)stride_z * l + dz;
+                        if (z < 0 || z >= D)
+                            continue;
+                        const double *plane = plane3d(x, &sh, n, ci, Ci, z);
+                        for (long i = 0; i < Ho; i++)
+                            for (long j = 0; j < Wo; j++) {
+                                long q0, s0;
+                                int inside;
+                                centre_axial(i, j, stride, &q0, &s0);
+                                double v = tap_value(plane, H, W, q0 + sh.tp.dq[t],
+                                                     s0 + sh.tp.ds[t], &inside);
+                                if (inside)
+                                    acc += dy[(((n * Co + co) * Do + l) * Ho + i) * Wo + j] * v;
+                            }
+                    }
+                dw[(co * Ci + ci) * (long)Z * T + zt] = acc;
+            }
+    if (db) {
+        for (long co = 0; co < Co; co++) {
+            double acc = 0.0;
+            for (long n = 0; n < N; n++)
+                for (long e = 0; e < Do * Ho * Wo; e++)
+                    acc += dy[(n * Co + co) * Do * Ho * Wo + e];
+            db[co] = acc;
+        }
+    }
+    taps_free(&sh.tp);
+    return ORACLE_OK;
+}
+
+int oracle_pool3d_fwd(const double *x, double *y, int *argmax, int N, int C,
+                      int D, int H, int W, int k, int kz, int stride,
+                      int stride_z, int mode)
+{
+    shape3d_t sh;
+    if ((mode != ORACLE_POOL_MAX && mode != ORACLE_POOL_AVG) ||
+        shape3d_make(N, C, C, D, H, W, k, kz, stride, stride_z, &sh))
+        return ORACLE_BAD;
+    const long Do = sh.Do, Ho = sh.Ho, Wo = sh.Wo;
+    const int T = sh.tp.T;
+#pragma omp parallel for collapse(3) schedule(static)
+    for (long n = 0; n < N; n++)
+        for (long ch = 0; ch < C; ch++)
+            for (long l = 0; l < Do; l++)
+                for (long i = 0; i < Ho; i++)
+                    for (long j = 0; j < Wo; j++) {
+                        long q0, s0;
+                        centre_axial(i, j, stride, &q0, &s0);
+                        double best = 0.0, sum = 0.0;
+                        int arg = 0, first = 1;
+                        for (long dz = -kz; dz <= kz; dz++) {
+                            const long z = (long)stride_z * l + dz;
+                            for (int t = 0; t < T; t++) {
+                                double v = 0.0;
+                                if (z >= 0 && z < D) {
+                                    int inside;
+                                    v = tap_value(plane3d(x, &sh, n, ch, C, z), H, W,
+                                                  q0 + sh.tp.dq[t], s0 + sh.tp.ds[t], &inside);
+                                }
+                                sum += v;
+                                if (first || v > best) {
+                                    best = v;
+                                    arg = (int)((dz + kz) * T + t);
+                                    first = 0;
+                                }
+                            }
+                        }
+                        const long o = (((n * C + ch) * Do + l) * Ho + i) * Wo + j;
+                        y[o] = mode == ORACLE_POOL_MAX ? best : sum / ((double)sh.Z * T);
+                        if (argmax)
+                            argmax[o] = arg;
+                    }
+    taps_free(&sh.tp);
+    return ORACLE_OK;
+}
+
+/*
+ * 3-D pool gradient.  Max: each output's gradient goes to the element its
+ * argmax tap points at (dropped when that tap is padding).  Average: dy /
+ * ((2kz+1) T) to every in-tensor tap.  relu_y (nullable) masks the result
+ * by [relu_y > 0].
+ */
+int oracle_pool3d_bwd(const double *dy, const int *argmax, const double *relu_y,
+                      double *dx, int N, int C, int D, int H, int W, int k,
+                      int kz, int stride, int stride_z, int mode)
+{
+    shape3d_t sh;
+    if ((mode != ORACLE_POOL_MAX && mode != ORACLE_POOL_AVG) ||
+        (mode == ORACLE_POOL_MAX && !argmax) ||
+        shape3d_make(N, C, C, D, H, W, k, kz, stride, stride_z, &sh))
+        return ORACLE_BAD;
+    const long Do = sh.Do, Ho = sh.Ho, Wo = sh.Wo;
+    const int T = sh.tp.T;
+    const long ZT = (long)sh.Z * T;
+    memset(dx, 0, sizeof(double) * (size_t)N * C * D * H * W);
+    int bad = 0;
+#pragma omp parallel for collapse(2) schedule(static) reduction(| : bad)
+    for (long n = 0; n < N; n++)
+        for (long ch = 0; ch < C; ch++)
+            for (long l = 0; l < Do; l++)
+                for (long i = 0; i < Ho; i++)
+                    for (long j = 0; j < Wo; j++) {
+                        const long o = (((n * C + ch) * Do + l) * Ho + i) * Wo + j;
+                        long q0, s0;
+                        centre_axial(i, j, stride, &q0, &s0);
+                        if (mode == ORACLE_POOL_MAX && (argmax[o] < 0 || argmax[o] >= ZT))
+                            bad = 1;
+                        for (long zt = 0; zt < ZT; zt++) {
+                            double g;
+                            if (mode == ORACLE_POOL_MAX) {
+                                if (zt != argmax[o])
+                                    continue;
+                                g = dy[o];
+                            } else {
+                                g = dy[o] / (double)ZT;
+                            }
+                            const long z = (long)stride_z * l + zt / T - kz;
+                            const int t = (int)(zt % T);
+                            long r, c;
+                            to_offset(q0 + sh.tp.dq[t], s0 + sh.tp.ds[t], &r, &c);
+                            if (z < 0 || z >= D || r < 0 || r >= H || c < 0 || c >= W)
+                                continue;
+                            dx[(((n * C + ch) * D + z) * H + r) * W + c] += g;
+                        }
+                    }
+    if (relu_y) {
+        const long total = (long)N * C * D * H * W;
+        for (long e = 0; e < total; e++)
+            if (!(relu_y[e] > 0.0))
+                dx[e] = 0.0;
+    }
+    taps_free(&sh.tp);
+    return bad ? ORACLE_BAD : ORACLE_OK;
+}
+
 /* Threads the OpenMP runtime will use for the parallel loops above. */
 int oracle_threads(void)
 {
