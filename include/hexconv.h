@@ -77,7 +77,8 @@ typedef enum { HEX_POOL_MAX = 0, HEX_POOL_AVG = 1 } hex_pool_mode;
 enum { HEX_FLAG_RELU = 1 };
 
 #define HEX_MAX_K 8      /* largest kernel size accepted */
-#define HEX_MAX_STRIDE 8 /* largest stride accepted */
+#define HEX_MAX_STRIDE 8 /* largest stride accepted (in the plane and along z) */
+#define HEX_MAX_KZ 4     /* largest half-depth of a 3-D window (2*4+1 planes) */
 
 /* Number of taps of a size-k kernel, 1 + 3k(k+1) (Sec. 2.2); negative
  * hex_status for k outside [0, HEX_MAX_K]. */
@@ -204,6 +205,86 @@ int hexpool_fwd(const void *x, void *y, uint8_t *argmax_tap, int N, int C,
 int hexpool_bwd(const void *dy, const uint8_t *argmax_tap, const void *relu_y,
                 void *dx, int N, int C, int H, int W, int k, int stride,
                 hex_pool_mode mode, hex_dtype dt, void *stream);
+
+/*
+ * Three-dimensional operations (Sec. 2.4: hexagonal layout in the x-y plane,
+ * equidistant samples along z, e.g. the time slices of a hexagonal camera).
+ * Conventions fixed here (the paper gives no further detail):
+ *  - tensors are dense NCDHW: x[N][C_in][D][H][W], D planes along z, each
+ *    an H x W plane in the addressing above;
+ *  - a window of size (k, kz) is the size-k hexagon in the plane times the
+ *    2kz+1 planes dz = -kz .. kz around the centre plane (0 <= kz <=
+ *    HEX_MAX_KZ); taps are numbered dz-major (dz ascending), the hexagonal
+ *    taps in hex_tap_table order inside; w[C_out][C_in][2kz+1][T];
+ *  - padding and stride follow the 2-D rule along z too: windows are
+ *    centred on real planes only, planes outside the tensor read zero, and
+ *    output plane l is centred on input plane stride_z * l, so
+ *    D_out = (D - 1) / stride_z + 1 (1 <= stride_z <= HEX_MAX_STRIDE);
+ *  - pooling takes the maximum or the average over the (2kz+1) * T taps,
+ *    padded taps counting as zeros; the average divides by (2kz+1) * T; the
+ *    maximum keeps the first maximal tap, whose index (dz + kz) * T + t is
+ *    written to a uint16 argmax.
+ * Every other convention (ownership, alignment, asynchrony, validation,
+ * empty batches, bf16 rounding, fp32 weight gradients, the ReLU flag) is
+ * that of the 2-D entry points.  H, W and D are input sizes.
+ */
+
+/* Output size of a D x H x W input (Sec. 2.3 in the plane, the same rule
+ * along z): D_out = (D - 1) / stride_z + 1; H_out, W_out as
+ * hex_out_shape.  Host pointers.  Returns a hex_status. */
+int hex_out_shape3d(int D, int H, int W, int k, int kz, int stride, int stride_z, int *D_out,
+                    int *H_out, int *W_out);
+
+/*
+ * 3-D forward convolution (Sec. 2.4):
+ *   y[n][co][l][i][j] = bias[co] + sum_ci sum_dz sum_t
+ *       w[co][ci][dz+kz][t] * x[n][ci][stride_z*l + dz][p_t(i, j)]
+ * x reads 0 outside the tensor.  y is [N][C_out][D_out][H_out][W_out].
+ * bias may be NULL; flags: HEX_FLAG_RELU.
+ */
+int hexconv3d_fwd(const void *x, const void *w, const void *bias, void *y, int N, int C_in,
+                  int C_out, int D, int H, int W, int k, int kz, int stride, int stride_z,
+                  hex_dtype dt, int flags, void *stream);
+
+/* Gradient of hexconv3d_fwd with respect to x (its adjoint without bias;
+ * the data half of the backward pass of a 3-D layer inside a trained CNN,
+ * Sec. 2.4).  dy is [N][C_out][D_out][H_out][W_out], dx [N][C_in][D][H][W]. */
+int hexconv3d_bwd_data(const void *dy, const void *w, void *dx, int N, int C_in, int C_out, int D,
+                       int H, int W, int k, int kz, int stride, int stride_z, hex_dtype dt,
+                       void *stream);
+
+/* Bytes of device workspace hexconv3d_bwd_weight needs (0 for invalid
+ * arguments). */
+size_t hexconv3d_bwd_weight_workspace(int N, int C_in, int C_out, int D, int H, int W, int k,
+                                      int kz, int stride, int stride_z, hex_dtype dt);
+
+/* Gradient with respect to the weights and bias (Sec. 2.4, the parameter
+ * half of a 3-D layer's backward pass):
+ *   dw[co][ci][dz+kz][t] = sum over (n, l, i, j) of
+ *       dy[n][co][l][i][j] * x[n][ci][stride_z*l + dz][p_t(i, j)]
+ *   db[co] = sum of dy[n][co] (nullable)
+ * float32 dw [C_out][C_in][2kz+1][T] and db; deterministic; ws as for
+ * hexconv_bwd_weight. */
+int hexconv3d_bwd_weight(const void *x, const void *dy, float *dw, float *db, void *ws,
+                         size_t ws_bytes, int N, int C_in, int C_out, int D, int H, int W, int k,
+                         int kz, int stride, int stride_z, hex_dtype dt, void *stream);
+
+/* 3-D pooling (Sec. 2.4: pooling built like the convolutions, same
+ * padding and striding) per channel over the (k, kz) windows: max or
+ * average as stated above.  argmax (nullable, uint16
+ * [N][C][D_out][H_out][W_out]) receives (dz + kz) * T + t of the winning
+ * tap for HEX_POOL_MAX. */
+int hexpool3d_fwd(const void *x, void *y, uint16_t *argmax, int N, int C, int D, int H, int W,
+                  int k, int kz, int stride, int stride_z, hex_pool_mode mode, hex_dtype dt,
+                  void *stream);
+
+/* Gradient of hexpool3d_fwd: max routes dy to the element of its argmax tap
+ * (dropped when that tap is padding; argmax required), average shares dy /
+ * ((2kz+1) T) over the in-tensor taps; times [relu_y > 0] when relu_y
+ * ([N][C][D][H][W]) is given.  dx is [N][C][D][H][W]. */
+int hexpool3d_bwd(const void *dy, const uint16_t *argmax, const void *relu_y, void *dx, int N,
+                  int C, int D, int H, int W, int k, int kz, int stride, int stride_z,
+                  hex_pool_mode mode, hex_dtype dt, void *stream);
 
 /* Static description of a hex_status value. */
 const char *hex_status_string(int status);

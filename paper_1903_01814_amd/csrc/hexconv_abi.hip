@@ -127,6 +127,33 @@ int check_shape(int N, int Ci, int Co, int H, int W, int k, int stride, int dt, 
     sh.s = stride;
     sh.T = hexgeom::num_taps(k);
     hexgeom::out_shape(H, W, stride, sh.Ho, sh.Wo);
+    sh.D = sh.Do = sh.Z = sh.sz = 1;
+    sh.kz = 0;
+    return HEX_OK;
+}
+
+// Shape checks of the three-dimensional entry points: the 2-D checks of the
+// plane, then the planes (D), the window depth (kz) and the plane stride.
+int check_shape3d(int N, int Ci, int Co, int D, int H, int W, int k, int kz, int stride,
+                  int stride_z, int dt, ConvShape &sh)
+{
+    if (D < 1 || kz < 0 || kz > HEX_MAX_KZ || stride_z < 1 || stride_z > HEX_MAX_STRIDE)
+        return HEX_ERR_INVALID_ARG;
+    int rc = check_shape(N, Ci, Co, H, W, k, stride, dt, sh);
+    if (rc != HEX_OK)
+        return rc;
+    if (D > 65535)
+        return HEX_ERR_UNSUPPORTED;
+    const long dhw = static_cast<long>(D) * H * W;
+    if (dhw * N > kMaxElems / Ci || dhw * N > kMaxElems / Co)
+        return HEX_ERR_UNSUPPORTED;
+    if (static_cast<long>(Co) * Ci * (2 * kz + 1) * sh.T > kMaxElems)
+        return HEX_ERR_UNSUPPORTED;
+    sh.D = D;
+    sh.kz = kz;
+    sh.Z = 2 * kz + 1;
+    sh.sz = stride_z;
+    sh.Do = (D - 1) / stride_z + 1;
     return HEX_OK;
 }
 
@@ -473,7 +500,7 @@ int hexpool_fwd(const void *x, void *y, uint8_t *argmax_tap, int N, int C, int H
     uint8_t *am = mode == HEX_POOL_MAX ? argmax_tap : nullptr;
     if (!force_generic() && hexk::pool_fast_ok(sh, d))
         return launched(hexk::pool_fwd_fast(x, y, am, sh, mode, d, st));
-    return launched(hexk::pool_fwd_generic(x, y, am, sh, mode, d, st));
+    return launched(hexk::pool_fwd_generic(x, y, am, sh, mode, d, false, st));
 }
 
 int hexpool_bwd(const void *dy, const uint8_t *argmax_tap, const void *relu_y, void *dx, int N,
@@ -496,7 +523,140 @@ int hexpool_bwd(const void *dy, const uint8_t *argmax_tap, const void *relu_y, v
     const Dtype d = static_cast<Dtype>(dt);
     if (!force_generic() && sh.Ho > 0 && hexk::pool_fast_ok(sh, d))
         return launched(hexk::pool_bwd_fast(dy, argmax_tap, relu_y, dx, sh, mode, d, st));
-    return launched(hexk::pool_bwd_generic(dy, argmax_tap, relu_y, dx, sh, mode, d, st));
+    return launched(hexk::pool_bwd_generic(dy, argmax_tap, relu_y, dx, sh, mode, d, false, st));
+}
+
+// ------------------------------------------------------- three dimensions
+
+int hex_out_shape3d(int D, int H, int W, int k, int kz, int stride, int stride_z, int *D_out,
+                    int *H_out, int *W_out)
+{
+    if (D < 1 || kz < 0 || kz > HEX_MAX_KZ || stride_z < 1 || stride_z > HEX_MAX_STRIDE ||
+        D_out == nullptr)
+        return HEX_ERR_INVALID_ARG;
+    const int rc = hex_out_shape(H, W, k, stride, H_out, W_out);
+    if (rc != HEX_OK)
+        return rc;
+    *D_out = (D - 1) / stride_z + 1;
+    return HEX_OK;
+}
+
+int hexconv3d_fwd(const void *x, const void *w, const void *bias, void *y, int N, int C_in,
+                  int C_out, int D, int H, int W, int k, int kz, int stride, int stride_z,
+                  hex_dtype dt, int flags, void *stream)
+{
+    ConvShape sh;
+    int rc = check_shape3d(N, C_in, C_out, D, H, W, k, kz, stride, stride_z, dt, sh);
+    if (rc != HEX_OK)
+        return rc;
+    if ((flags & ~HEX_FLAG_RELU) != 0)
+        return HEX_ERR_INVALID_ARG;
+    if (N == 0)
+        return HEX_OK;
+    if ((rc = ptrs_ok({x, w, y}, {bias})) != HEX_OK)
+        return rc;
+    if (sh.Ho == 0)
+        return HEX_OK;
+    if (!hexk::conv_fwd_generic_ok(sh))
+        return HEX_ERR_UNSUPPORTED;
+    return launched(hexk::conv_fwd_generic(x, w, bias, y, sh, static_cast<Dtype>(dt),
+                                           (flags & HEX_FLAG_RELU) != 0,
+                                           static_cast<hipStream_t>(stream)));
+}
+
+int hexconv3d_bwd_data(const void *dy, const void *w, void *dx, int N, int C_in, int C_out, int D,
+                       int H, int W, int k, int kz, int stride, int stride_z, hex_dtype dt,
+                       void *stream)
+{
+    ConvShape sh;
+    int rc = check_shape3d(N, C_in, C_out, D, H, W, k, kz, stride, stride_z, dt, sh);
+    if (rc != HEX_OK)
+        return rc;
+    if (N == 0)
+        return HEX_OK;
+    if ((rc = ptrs_ok({w, dx}, {dy})) != HEX_OK)
+        return rc;
+    if (dy == nullptr && sh.Ho > 0)
+        return HEX_ERR_INVALID_ARG;
+    if (!hexk::conv_bwd_data_generic_ok(sh))
+        return HEX_ERR_UNSUPPORTED;
+    return launched(hexk::conv_bwd_data_generic(dy, w, dx, sh, static_cast<Dtype>(dt),
+                                                static_cast<hipStream_t>(stream)));
+}
+
+size_t hexconv3d_bwd_weight_workspace(int N, int C_in, int C_out, int D, int H, int W, int k,
+                                      int kz, int stride, int stride_z, hex_dtype dt)
+{
+    ConvShape sh;
+    if (check_shape3d(N, C_in, C_out, D, H, W, k, kz, stride, stride_z, dt, sh) != HEX_OK)
+        return 0;
+    if (N == 0 || sh.Ho == 0)
+        return 0;
+    return hexk::wgrad_generic_workspace(sh);
+}
+
+int hexconv3d_bwd_weight(const void *x, const void *dy, float *dw, float *db, void *ws,
+                         size_t ws_bytes, int N, int C_in, int C_out, int D, int H, int W, int k,
+                         int kz, int stride, int stride_z, hex_dtype dt, void *stream)
+{
+    ConvShape sh;
+    int rc = check_shape3d(N, C_in, C_out, D, H, W, k, kz, stride, stride_z, dt, sh);
+    if (rc != HEX_OK)
+        return rc;
+    if ((rc = ptrs_ok({dw}, {x, dy, db, ws})) != HEX_OK)
+        return rc;
+    const bool empty = (N == 0 || sh.Ho == 0);
+    if (!empty && (x == nullptr || dy == nullptr))
+        return HEX_ERR_INVALID_ARG;
+    const size_t need = empty ? 0 : hexk::wgrad_generic_workspace(sh);
+    if (need > 0 && (ws == nullptr || ws_bytes < need))
+        return HEX_ERR_INVALID_ARG;
+    hipStream_t st = static_cast<hipStream_t>(stream);
+    if (empty)
+        return launched(hexk::fill_zero_f32(dw, db, sh, st));
+    return launched(hexk::wgrad_generic(x, dy, dw, db, ws, sh, static_cast<Dtype>(dt), st));
+}
+
+int hexpool3d_fwd(const void *x, void *y, uint16_t *argmax, int N, int C, int D, int H, int W,
+                  int k, int kz, int stride, int stride_z, hex_pool_mode mode, hex_dtype dt,
+                  void *stream)
+{
+    ConvShape sh;
+    int rc = check_shape3d(N, C, C, D, H, W, k, kz, stride, stride_z, dt, sh);
+    if (rc != HEX_OK)
+        return rc;
+    if (mode != HEX_POOL_MAX && mode != HEX_POOL_AVG)
+        return HEX_ERR_INVALID_ARG;
+    if (N == 0)
+        return HEX_OK;
+    if ((rc = ptrs_ok({x, y}, {argmax})) != HEX_OK)
+        return rc;
+    if (sh.Ho == 0)
+        return HEX_OK;
+    return launched(hexk::pool_fwd_generic(x, y, mode == HEX_POOL_MAX ? argmax : nullptr, sh,
+                                           mode, static_cast<Dtype>(dt), true,
+                                           static_cast<hipStream_t>(stream)));
+}
+
+int hexpool3d_bwd(const void *dy, const uint16_t *argmax, const void *relu_y, void *dx, int N,
+                  int C, int D, int H, int W, int k, int kz, int stride, int stride_z,
+                  hex_pool_mode mode, hex_dtype dt, void *stream)
+{
+    ConvShape sh;
+    int rc = check_shape3d(N, C, C, D, H, W, k, kz, stride, stride_z, dt, sh);
+    if (rc != HEX_OK)
+        return rc;
+    if (mode != HEX_POOL_MAX && mode != HEX_POOL_AVG)
+        return HEX_ERR_INVALID_ARG;
+    if (N == 0)
+        return HEX_OK;
+    if ((rc = ptrs_ok({dx}, {dy, argmax, relu_y})) != HEX_OK)
+        return rc;
+    if (sh.Ho > 0 && (dy == nullptr || (mode == HEX_POOL_MAX && argmax == nullptr)))
+        return HEX_ERR_INVALID_ARG;
+    return launched(hexk::pool_bwd_generic(dy, argmax, relu_y, dx, sh, mode,
+                                           static_cast<Dtype>(dt), true,
+                                           static_cast<hipStream_t>(stream)));
 }
 
 int hexconv_timing_begin(void)

@@ -32,9 +32,27 @@ using plan::region_rows;
 constexpr int kTapGroup = 8;  // taps accumulated per pass (weight gradient)
 constexpr int kWgCoBlock = 8; // output channels per block (weight gradient, >= 32 channels)
 
-// G input channels per stage: their regions and weights are staged between
-// one pair of barriers, and each tap's CB weights are read as broadcast
-// 16-byte LDS vectors.
+// Depth: every kernel here also serves the three-dimensional operations
+// (x[N][C][D][H][W], a window of 2kz+1 planes around the centre plane
+// sz*l, planes outside the tensor reading zero); a 2-D call is the case
+// D = D_out = 1, kz = 0.  An input channel ci and a plane offset dz form one
+// "pair" p = ci*Z + dz_index (Z = 2kz+1), so the weights w[C_out][C_in][Z][T]
+// are w[C_out][pairs][T] and each pair is staged like one 2-D input channel.
+
+// Plane of pair p for output plane l of image n (nullptr: a padding plane).
+template <typename T>
+__device__ __forceinline__ const T *pair_plane(const T *x, const ConvShape &sh, int n, int p, int l)
+{
+    const int ci = p / sh.Z, dzi = p - ci * sh.Z;
+    const int z = sh.sz * l + dzi - sh.kz;
+    if (z < 0 || z >= sh.D)
+        return nullptr;
+    return x + ((static_cast<size_t>(n) * sh.Ci + ci) * sh.D + z) * (static_cast<size_t>(sh.H) * sh.W);
+}
+
+// G pairs per stage: their regions and weights are staged between one pair
+// of barriers, and each tap's CB weights are read as broadcast 16-byte LDS
+// vectors.  blockIdx.x = output plane l * tiles + tile.
 template <typename T, int CB>
 __global__ __launch_bounds__(kThreads) void conv_fwd_generic_k(
     const T *__restrict__ x, const T *__restrict__ w, const T *__restrict__ b,
@@ -44,7 +62,9 @@ __global__ __launch_bounds__(kThreads) void conv_fwd_generic_k(
     __shared__ TapLds tl;
     fill_taps(tl, sh.k);
 
-    const int tile = blockIdx.x;
+    const int tiles = gridDim.x / sh.Do;
+    const int l = blockIdx.x / tiles;
+    const int tile = blockIdx.x - l * tiles;
     const int n = blockIdx.y;
     const int co0 = blockIdx.z * CB;
     const int ti0 = (tile / tiles_j) * TI;
@@ -71,22 +91,24 @@ __global__ __launch_bounds__(kThreads) void conv_fwd_generic_k(
     for (int cb = 0; cb < CB; ++cb)
         acc[cb] = (b != nullptr && co0 + cb < sh.Co) ? to_f(b[co0 + cb]) : 0.f;
 
-    const size_t HW = static_cast<size_t>(sh.H) * sh.W;
+    const int P = sh.Ci * sh.Z;
     const int TCB = sh.T * CB;
-    for (int ci0 = 0; ci0 < sh.Ci; ci0 += G) {
-        const int ng = min(G, sh.Ci - ci0);
+    for (int p0 = 0; p0 < P; p0 += G) {
+        const int ng = min(G, P - p0);
         __syncthreads();
-        for (int g = 0; g < ng; ++g)
-            stage_window<8>(region + static_cast<size_t>(g) * RF,
-                            x + (static_cast<size_t>(n) * sh.Ci + ci0 + g) * HW, sh.H, sh.W, r_lo,
-                            c_lo, RH, RW);
+        for (int g = 0; g < ng; ++g) {
+            const T *plane = pair_plane(x, sh, n, p0 + g, l);
+            // a padding plane stages zeros (no row is inside)
+            stage_window<8>(region + static_cast<size_t>(g) * RF, plane != nullptr ? plane : x,
+                            plane != nullptr ? sh.H : 0, sh.W, r_lo, c_lo, RH, RW);
+        }
         // weights of output channels co0 .. co0 + CB - 1 (clamped to the
         // last one; those accumulators are never stored)
         for (int e = threadIdx.x; e < ng * TCB; e += kThreads) {
             const int cb = e % CB, rest = e / CB;
             const int g = rest / sh.T, t = rest - g * sh.T;
             const int co = min(co0 + cb, sh.Co - 1);
-            wl[e] = to_f(w[(static_cast<size_t>(co) * sh.Ci + ci0 + g) * sh.T + t]);
+            wl[e] = to_f(w[(static_cast<size_t>(co) * P + p0 + g) * sh.T + t]);
         }
         __syncthreads();
         if (active) {
@@ -119,13 +141,15 @@ __global__ __launch_bounds__(kThreads) void conv_fwd_generic_k(
         float v = acc[cb];
         if (relu)
             v = fmaxf(v, 0.f);
-        y[(static_cast<size_t>(n) * sh.Co + co) * HWo + static_cast<size_t>(i) * sh.Wo + j] = from_f<T>(v);
+        y[((static_cast<size_t>(n) * sh.Co + co) * sh.Do + l) * HWo + static_cast<size_t>(i) * sh.Wo + j] =
+            from_f<T>(v);
     }
 }
 
-// CC output channels per stage: their weights for the block's CB input
-// channels are staged in LDS as float [CC][T][CB] between one pair of
-// barriers and read as broadcast 16-byte vectors.
+// CC output channels per stage: their weights (one plane offset) for the
+// block's CB input channels are staged in LDS as float [CC][T][CB] between
+// one pair of barriers and read as broadcast 16-byte vectors.
+// blockIdx.x = input plane z * pixel blocks + pixel block.
 template <typename T, int CB>
 __global__ __launch_bounds__(kThreads) void conv_bwd_data_generic_k(
     const T *__restrict__ dy, const T *__restrict__ w, T *__restrict__ dx, ConvShape sh, int CC)
@@ -134,12 +158,15 @@ __global__ __launch_bounds__(kThreads) void conv_bwd_data_generic_k(
     __shared__ TapLds tl;
     fill_taps(tl, sh.k);
 
-    const int p = blockIdx.x * kThreads + threadIdx.x;
+    const int pblocks = gridDim.x / sh.D;
+    const int z = blockIdx.x / pblocks;
+    const int p = (blockIdx.x - z * pblocks) * kThreads + threadIdx.x;
     const int n = blockIdx.y;
     const int ci0 = blockIdx.z * CB;
     const bool active = p < sh.H * sh.W;
     const int r = active ? p / sh.W : 0, c = active ? p % sh.W : 0;
     const size_t HWo = static_cast<size_t>(sh.Ho) * sh.Wo;
+    const int P = sh.Ci * sh.Z;
 
     float acc[CB];
 #pragma unroll
@@ -147,34 +174,41 @@ __global__ __launch_bounds__(kThreads) void conv_bwd_data_generic_k(
         acc[cb] = 0.f;
 
     const int TCB = sh.T * CB;
-    for (int co0 = 0; co0 < sh.Co; co0 += CC) {
-        const int nc = min(CC, sh.Co - co0);
-        __syncthreads(); // previous stage read (and the tap table written)
-        for (int e = threadIdx.x; e < nc * TCB; e += kThreads) {
-            const int cb = e % CB, rest = e / CB;
-            const int q = rest / sh.T, t = rest - q * sh.T;
-            const int ci = min(ci0 + cb, sh.Ci - 1); // clamped: never stored
-            wl[e] = to_f(w[(static_cast<size_t>(co0 + q) * sh.Ci + ci) * sh.T + t]);
-        }
-        __syncthreads();
-        if (!active)
+    for (int dzi = 0; dzi < sh.Z; ++dzi) {
+        // the output plane whose window reads plane z at offset dz (block-uniform)
+        const int zc = z - (dzi - sh.kz);
+        if (zc < 0 || zc % sh.sz != 0 || zc / sh.sz >= sh.Do)
             continue;
-        for (int t = 0; t < sh.T; ++t) {
-            int i = 0, j = 0;
-            if (!source_output(r, c, tl.dq[t], tl.ds[t], sh.s, sh.Ho, sh.Wo, i, j))
+        const int l = zc / sh.sz;
+        for (int co0 = 0; co0 < sh.Co; co0 += CC) {
+            const int nc = min(CC, sh.Co - co0);
+            __syncthreads(); // previous stage read (and the tap table written)
+            for (int e = threadIdx.x; e < nc * TCB; e += kThreads) {
+                const int cb = e % CB, rest = e / CB;
+                const int q = rest / sh.T, t = rest - q * sh.T;
+                const int ci = min(ci0 + cb, sh.Ci - 1); // clamped: never stored
+                wl[e] = to_f(w[(static_cast<size_t>(co0 + q) * P + ci * sh.Z + dzi) * sh.T + t]);
+            }
+            __syncthreads();
+            if (!active)
                 continue;
-            const T *dyo = dy + (static_cast<size_t>(n) * sh.Co + co0) * HWo +
-                           static_cast<size_t>(i) * sh.Wo + j;
-            for (int q = 0; q < nc; ++q) {
-                const float g = to_f(dyo[static_cast<size_t>(q) * HWo]);
-                const float4 *w4 = reinterpret_cast<const float4 *>(wl + (q * sh.T + t) * CB);
+            for (int t = 0; t < sh.T; ++t) {
+                int i = 0, j = 0;
+                if (!source_output(r, c, tl.dq[t], tl.ds[t], sh.s, sh.Ho, sh.Wo, i, j))
+                    continue;
+                const T *dyo = dy + ((static_cast<size_t>(n) * sh.Co + co0) * sh.Do + l) * HWo +
+                               static_cast<size_t>(i) * sh.Wo + j;
+                for (int q = 0; q < nc; ++q) {
+                    const float g = to_f(dyo[static_cast<size_t>(q) * sh.Do * HWo]);
+                    const float4 *w4 = reinterpret_cast<const float4 *>(wl + (q * sh.T + t) * CB);
 #pragma unroll
-                for (int v = 0; v < CB / 4; ++v) {
-                    const float4 ww = w4[v];
-                    acc[4 * v] += ww.x * g;
-                    acc[4 * v + 1] += ww.y * g;
-                    acc[4 * v + 2] += ww.z * g;
-                    acc[4 * v + 3] += ww.w * g;
+                    for (int v = 0; v < CB / 4; ++v) {
+                        const float4 ww = w4[v];
+                        acc[4 * v] += ww.x * g;
+                        acc[4 * v + 1] += ww.y * g;
+                        acc[4 * v + 2] += ww.z * g;
+                        acc[4 * v + 3] += ww.w * g;
+                    }
                 }
             }
         }
@@ -187,14 +221,15 @@ __global__ __launch_bounds__(kThreads) void conv_bwd_data_generic_k(
         const int ci = ci0 + cb;
         if (ci >= sh.Ci)
             break;
-        dx[(static_cast<size_t>(n) * sh.Ci + ci) * HW + p] = from_f<T>(acc[cb]);
+        dx[((static_cast<size_t>(n) * sh.Ci + ci) * sh.D + z) * HW + p] = from_f<T>(acc[cb]);
     }
 }
 
-// Block = (pixel chunk, CO output channels, one input channel): per pixel
-// the dy of the block's output channels and the x under one group of taps
-// feed CO x kTapGroup accumulators.  Sums over the block's
-// threads: a fixed xor-shuffle tree per wave, then the waves in order.
+// Block = (pixel chunk, CO output channels, one input channel): per output
+// pixel the dy of the block's output channels and the x under one group of
+// (plane offset, tap) pairs feed CO x kTapGroup accumulators.  Sums over
+// the block's threads: a fixed xor-shuffle tree per wave, then the waves in
+// order.  Pixels run over (n, l, i, j); taps tt = dz_index * T + t.
 template <typename T, int CO>
 __global__ __launch_bounds__(kThreads) void wgrad_partial_generic_k(
     const T *__restrict__ x, const T *__restrict__ dy, float *__restrict__ part, ConvShape sh,
@@ -209,15 +244,17 @@ __global__ __launch_bounds__(kThreads) void wgrad_partial_generic_k(
 
     const int co0 = blockIdx.y * CO, ci = blockIdx.z;
     const long HWo = static_cast<long>(sh.Ho) * sh.Wo;
-    const long total = HWo * sh.N;
+    const long DHWo = HWo * sh.Do;
+    const long total = DHWo * sh.N;
     const long begin = static_cast<long>(blockIdx.x) * chunk;
     const long end = min(begin + chunk, total);
     const size_t HW = static_cast<size_t>(sh.H) * sh.W;
     const bool do_bias = (ci == 0);
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-    const size_t Jt = static_cast<size_t>(sh.Ci) * sh.T + 1;
+    const int TT = sh.Z * sh.T;
+    const size_t Jt = static_cast<size_t>(sh.Ci) * TT + 1;
 
-    for (int tg = 0; tg < sh.T; tg += kTapGroup) {
+    for (int tg = 0; tg < TT; tg += kTapGroup) {
         float acc[CO][kTapGroup];
         float accb[CO];
 #pragma unroll
@@ -228,26 +265,30 @@ __global__ __launch_bounds__(kThreads) void wgrad_partial_generic_k(
                 acc[q][u] = 0.f;
         }
         for (long e = begin + threadIdx.x; e < end; e += kThreads) {
-            const int n = static_cast<int>(e / HWo);
-            const int o = static_cast<int>(e % HWo);
+            const int n = static_cast<int>(e / DHWo);
+            const long rem = e - static_cast<long>(n) * DHWo;
+            const int l = static_cast<int>(rem / HWo);
+            const int o = static_cast<int>(rem - static_cast<long>(l) * HWo);
             const int i = o / sh.Wo, j = o % sh.Wo;
             float g[CO];
 #pragma unroll
             for (int q = 0; q < CO; ++q)
                 g[q] = co0 + q < sh.Co
-                           ? to_f(dy[(static_cast<size_t>(n) * sh.Co + co0 + q) * HWo + o])
+                           ? to_f(dy[(static_cast<size_t>(n) * sh.Co + co0 + q) * DHWo + rem])
                            : 0.f;
             const int rc = centre_row(i, j, sh.s), cc = centre_col(j, sh.s);
             const int par = cc & 1;
-            const T *plane = x + (static_cast<size_t>(n) * sh.Ci + ci) * HW;
+            const T *img = x + static_cast<size_t>(n * sh.Ci + ci) * sh.D * HW;
 #pragma unroll
             for (int u = 0; u < kTapGroup; ++u) {
-                const int t = tg + u;
+                const int tt = tg + u;
                 float v = 0.f;
-                if (t < sh.T) {
+                if (tt < TT) {
+                    const int dzi = tt / sh.T, t = tt - dzi * sh.T;
+                    const int z = sh.sz * l + dzi - sh.kz;
                     const int r = rc + tl.drow[par][t], c = cc + tl.dq[t];
-                    if (r >= 0 && r < sh.H && c >= 0 && c < sh.W)
-                        v = to_f(plane[static_cast<size_t>(r) * sh.W + c]);
+                    if (z >= 0 && z < sh.D && r >= 0 && r < sh.H && c >= 0 && c < sh.W)
+                        v = to_f(img[z * HW + static_cast<size_t>(r) * sh.W + c]);
                 }
 #pragma unroll
                 for (int q = 0; q < CO; ++q)
@@ -273,16 +314,16 @@ __global__ __launch_bounds__(kThreads) void wgrad_partial_generic_k(
             }
         }
         __syncthreads();
-        // partial layout [e][chunk], e = co * (Ci*T + 1) + col
+        // partial layout [e][chunk], e = co * (Ci*Z*T + 1) + col
         for (int idx = threadIdx.x; idx < NV; idx += kThreads) {
             float v = red[0][idx];
 #pragma unroll
             for (int wv = 1; wv < kWavesG; ++wv)
                 v += red[wv][idx];
             if (idx < CO * kTapGroup) {
-                const int q = idx / kTapGroup, t = tg + idx % kTapGroup;
-                if (co0 + q < sh.Co && t < sh.T)
-                    part[((co0 + q) * Jt + static_cast<size_t>(ci) * sh.T + t) * gridDim.x +
+                const int q = idx / kTapGroup, tt = tg + idx % kTapGroup;
+                if (co0 + q < sh.Co && tt < TT)
+                    part[((co0 + q) * Jt + static_cast<size_t>(ci) * TT + tt) * gridDim.x +
                          blockIdx.x] = v;
             } else {
                 const int q = idx - CO * kTapGroup;
@@ -304,77 +345,97 @@ __global__ __launch_bounds__(kThreads) void fill_zero_k(float *__restrict__ a, i
         b[e - na] = 0.f;
 }
 
-template <typename T, int MODE>
+// One output element per thread; argmax index dz_index * T + t (AM: uint8_t
+// for 2-D calls, uint16_t for 3-D ones).
+template <typename T, int MODE, typename AM>
 __global__ __launch_bounds__(kThreads) void pool_fwd_generic_k(
-    const T *__restrict__ x, T *__restrict__ y, uint8_t *__restrict__ am,
+    const T *__restrict__ x, T *__restrict__ y, AM *__restrict__ am,
     ConvShape sh, long total)
 {
     __shared__ TapLds tl;
     fill_taps(tl, sh.k);
     __syncthreads();
     const long HWo = static_cast<long>(sh.Ho) * sh.Wo;
+    const long DHWo = HWo * sh.Do;
     const size_t HW = static_cast<size_t>(sh.H) * sh.W;
     for (long e = static_cast<long>(blockIdx.x) * kThreads + threadIdx.x; e < total;
          e += static_cast<long>(gridDim.x) * kThreads) {
-        const long plane = e / HWo;
-        const int o = static_cast<int>(e % HWo);
+        const long plane = e / DHWo;
+        const long rem = e - plane * DHWo;
+        const int l = static_cast<int>(rem / HWo);
+        const int o = static_cast<int>(rem - static_cast<long>(l) * HWo);
         const int i = o / sh.Wo, j = o % sh.Wo;
         const int rc = centre_row(i, j, sh.s), cc = centre_col(j, sh.s);
         const int par = cc & 1;
-        const T *src = x + plane * HW;
         float best = 0.f, sum = 0.f;
         int arg = 0;
-        for (int t = 0; t < sh.T; ++t) {
-            const int r = rc + tl.drow[par][t], c = cc + tl.dq[t];
-            const float v = (r >= 0 && r < sh.H && c >= 0 && c < sh.W)
-                                ? to_f(src[static_cast<size_t>(r) * sh.W + c])
-                                : 0.f;
-            sum += v;
-            if (t == 0 || v > best) {
-                best = v;
-                arg = t;
+        for (int dzi = 0; dzi < sh.Z; ++dzi) {
+            const int z = sh.sz * l + dzi - sh.kz;
+            const bool zin = z >= 0 && z < sh.D;
+            const T *src = x + (plane * sh.D + (zin ? z : 0)) * HW;
+            for (int t = 0; t < sh.T; ++t) {
+                const int r = rc + tl.drow[par][t], c = cc + tl.dq[t];
+                const float v = (zin && r >= 0 && r < sh.H && c >= 0 && c < sh.W)
+                                    ? to_f(src[static_cast<size_t>(r) * sh.W + c])
+                                    : 0.f;
+                sum += v;
+                if ((dzi == 0 && t == 0) || v > best) {
+                    best = v;
+                    arg = dzi * sh.T + t;
+                }
             }
         }
         if (MODE == 0) {
             y[e] = from_f<T>(best);
             if (am != nullptr)
-                am[e] = static_cast<uint8_t>(arg);
+                am[e] = static_cast<AM>(arg);
         } else {
-            y[e] = from_f<T>(sum / static_cast<float>(sh.T));
+            y[e] = from_f<T>(sum / static_cast<float>(sh.Z * sh.T));
         }
     }
 }
 
-template <typename T, int MODE>
+// One input element per thread: gathers from every output whose window
+// holds it (plane lattice, then the hexagonal lattice test).
+template <typename T, int MODE, typename AM>
 __global__ __launch_bounds__(kThreads) void pool_bwd_generic_k(
-    const T *__restrict__ dy, const uint8_t *__restrict__ am,
+    const T *__restrict__ dy, const AM *__restrict__ am,
     const T *__restrict__ relu_y, T *__restrict__ dx, ConvShape sh, long total)
 {
     __shared__ TapLds tl;
     fill_taps(tl, sh.k);
     __syncthreads();
     const long HW = static_cast<long>(sh.H) * sh.W;
+    const long DHW = HW * sh.D;
     const size_t HWo = static_cast<size_t>(sh.Ho) * sh.Wo;
     for (long e = static_cast<long>(blockIdx.x) * kThreads + threadIdx.x; e < total;
          e += static_cast<long>(gridDim.x) * kThreads) {
-        const long plane = e / HW;
-        const int p = static_cast<int>(e % HW);
+        const long plane = e / DHW;
+        const long rem = e - plane * DHW;
+        const int z = static_cast<int>(rem / HW);
+        const int p = static_cast<int>(rem - static_cast<long>(z) * HW);
         const int r = p / sh.W, c = p % sh.W;
         float acc = 0.f;
-        for (int t = 0; t < sh.T; ++t) {
-            int i = 0, j = 0;
-            if (!source_output(r, c, tl.dq[t], tl.ds[t], sh.s, sh.Ho, sh.Wo, i, j))
+        for (int dzi = 0; dzi < sh.Z; ++dzi) {
+            const int zc = z - (dzi - sh.kz);
+            if (zc < 0 || zc % sh.sz != 0 || zc / sh.sz >= sh.Do)
                 continue;
-            const size_t o = plane * HWo + static_cast<size_t>(i) * sh.Wo + j;
-            if (MODE == 0) {
-                if (am[o] == t)
+            const int l = zc / sh.sz;
+            for (int t = 0; t < sh.T; ++t) {
+                int i = 0, j = 0;
+                if (!source_output(r, c, tl.dq[t], tl.ds[t], sh.s, sh.Ho, sh.Wo, i, j))
+                    continue;
+                const size_t o = (plane * sh.Do + l) * HWo + static_cast<size_t>(i) * sh.Wo + j;
+                if (MODE == 0) {
+                    if (static_cast<int>(am[o]) == dzi * sh.T + t)
+                        acc += to_f(dy[o]);
+                } else {
                     acc += to_f(dy[o]);
-            } else {
-                acc += to_f(dy[o]);
+                }
             }
         }
         if (MODE == 1)
-            acc = acc / static_cast<float>(sh.T);
+            acc = acc / static_cast<float>(sh.Z * sh.T);
         if (relu_y != nullptr && !(to_f(relu_y[e]) > 0.f))
             acc = 0.f;
         dx[e] = from_f<T>(acc);
@@ -389,7 +450,7 @@ int wgrad_co_block(int Co) { return Co >= 32 ? kWgCoBlock : 1; }
 
 int wgrad_generic_chunks(const ConvShape &sh, int &chunk)
 {
-    const long total = static_cast<long>(sh.N) * sh.Ho * sh.Wo;
+    const long total = static_cast<long>(sh.N) * sh.Do * sh.Ho * sh.Wo;
     const long pairs = static_cast<long>(cdiv(sh.Co, wgrad_co_block(sh.Co))) * sh.Ci;
     long nchunks = (2048 + pairs - 1) / pairs;
     nchunks = std::max(1L, std::min(nchunks, (total + 255) / 256));
@@ -404,7 +465,7 @@ int wgrad_generic_chunks(const ConvShape &sh, int &chunk)
 
 bool conv_fwd_generic_ok(const ConvShape &sh)
 {
-    return plan::plan_fwd(sh.Ci, sh.Co, sh.k, sh.s).ok;
+    return plan::plan_fwd(sh.Ci * sh.Z, sh.Co, sh.k, sh.s).ok;
 }
 
 bool conv_bwd_data_generic_ok(const ConvShape &sh)
@@ -415,13 +476,14 @@ bool conv_bwd_data_generic_ok(const ConvShape &sh)
 hipError_t conv_fwd_generic(const void *x, const void *w, const void *b, void *y,
                             const ConvShape &sh, Dtype dt, bool relu, hipStream_t st)
 {
-    const plan::FwdPlan p = plan::plan_fwd(sh.Ci, sh.Co, sh.k, sh.s);
+    // (input channel, plane offset) pairs are staged like 2-D input channels
+    const plan::FwdPlan p = plan::plan_fwd(sh.Ci * sh.Z, sh.Co, sh.k, sh.s);
     if (!p.ok)
         return hipErrorInvalidConfiguration; // the ABI checks the plan first
     const int TI = p.TI, TJ = p.TJ, cb = p.cb, G = p.G;
     const size_t lds = p.lds;
     const int tiles_i = cdiv(sh.Ho, TI), tiles_j = cdiv(sh.Wo, TJ);
-    dim3 grid(tiles_i * tiles_j, sh.N, cdiv(sh.Co, cb));
+    dim3 grid(tiles_i * tiles_j * sh.Do, sh.N, cdiv(sh.Co, cb));
 #define HEX_FWD_G(TT, CBV)                                                                   \
     HEX_LAUNCH((conv_fwd_generic_k<TT, CBV>), grid, dim3(kThreads), lds, st, (const TT *)x, \
                (const TT *)w, (const TT *)b, (TT *)y, sh, relu ? 1 : 0, TI, TJ, tiles_j, G)
@@ -448,7 +510,7 @@ hipError_t conv_bwd_data_generic(const void *dy, const void *w, void *dx, const 
         return hipErrorInvalidConfiguration; // the ABI checks the plan first
     const int cb = p.cb, CC = p.CC;
     const size_t lds = p.lds;
-    dim3 grid(cdiv(static_cast<long>(sh.H) * sh.W, kThreads), sh.N, cdiv(sh.Ci, cb));
+    dim3 grid(cdiv(static_cast<long>(sh.H) * sh.W, kThreads) * sh.D, sh.N, cdiv(sh.Ci, cb));
 #define HEX_BD_G(TT, CBV)                                                                    \
     HEX_LAUNCH((conv_bwd_data_generic_k<TT, CBV>), grid, dim3(kThreads), lds, st,            \
                (const TT *)dy, (const TT *)w, (TT *)dx, sh, CC)
@@ -472,7 +534,7 @@ size_t wgrad_generic_workspace(const ConvShape &sh)
     int chunk;
     const int nchunks = wgrad_generic_chunks(sh, chunk);
     return sizeof(float) * static_cast<size_t>(nchunks) *
-           (static_cast<size_t>(sh.Co) * sh.Ci * sh.T + sh.Co);
+           (static_cast<size_t>(sh.Co) * sh.Ci * sh.Z * sh.T + sh.Co);
 }
 
 hipError_t wgrad_generic(const void *x, const void *dy, float *dw, float *db, void *ws,
@@ -495,47 +557,57 @@ hipError_t wgrad_generic(const void *x, const void *dy, float *dw, float *db, vo
     hipError_t e = hipGetLastError();
     if (e != hipSuccess)
         return e;
-    return reduce_partials(part, nchunks, sh.Co, sh.Ci * sh.T, dw, db, st);
+    return reduce_partials(part, nchunks, sh.Co, sh.Ci * sh.Z * sh.T, dw, db, st);
 }
 
 hipError_t fill_zero_f32(float *dw, float *db, const ConvShape &sh, hipStream_t st)
 {
-    const long EW = static_cast<long>(sh.Co) * sh.Ci * sh.T;
+    const long EW = static_cast<long>(sh.Co) * sh.Ci * sh.Z * sh.T;
     HEX_LAUNCH(fill_zero_k, dim3(cdiv(EW + sh.Co, kThreads)), dim3(kThreads), 0, st, dw,
                        static_cast<int>(EW), db, sh.Co);
     return hipGetLastError();
 }
 
-hipError_t pool_fwd_generic(const void *x, void *y, uint8_t *am, const ConvShape &sh, int mode,
-                            Dtype dt, hipStream_t st)
+hipError_t pool_fwd_generic(const void *x, void *y, void *am, const ConvShape &sh, int mode,
+                            Dtype dt, bool am16, hipStream_t st)
 {
-    const long total = static_cast<long>(sh.N) * sh.Ci * sh.Ho * sh.Wo;
+    const long total = static_cast<long>(sh.N) * sh.Ci * sh.Do * sh.Ho * sh.Wo;
     const int blocks = std::max(1, std::min(cdiv(total, kThreads), 65535 * 16));
-#define HEX_POOL_FWD(T, M)                                                                   \
-    HEX_LAUNCH((pool_fwd_generic_k<T, M>), dim3(blocks), dim3(kThreads), 0, st,     \
-                       (const T *)x, (T *)y, am, sh, total)
+#define HEX_POOL_FWD(T, M, A)                                                                \
+    HEX_LAUNCH((pool_fwd_generic_k<T, M, A>), dim3(blocks), dim3(kThreads), 0, st,           \
+               (const T *)x, (T *)y, (A *)am, sh, total)
+#define HEX_POOL_FWD_A(T, M)                                                                 \
+    do {                                                                                     \
+        if (am16) HEX_POOL_FWD(T, M, uint16_t); else HEX_POOL_FWD(T, M, uint8_t);            \
+    } while (0)
     if (dt == F32) {
-        if (mode == 0) HEX_POOL_FWD(float, 0); else HEX_POOL_FWD(float, 1);
+        if (mode == 0) HEX_POOL_FWD_A(float, 0); else HEX_POOL_FWD(float, 1, uint8_t);
     } else {
-        if (mode == 0) HEX_POOL_FWD(bf16raw, 0); else HEX_POOL_FWD(bf16raw, 1);
+        if (mode == 0) HEX_POOL_FWD_A(bf16raw, 0); else HEX_POOL_FWD(bf16raw, 1, uint8_t);
     }
+#undef HEX_POOL_FWD_A
 #undef HEX_POOL_FWD
     return hipGetLastError();
 }
 
-hipError_t pool_bwd_generic(const void *dy, const uint8_t *am, const void *relu_y, void *dx,
-                            const ConvShape &sh, int mode, Dtype dt, hipStream_t st)
+hipError_t pool_bwd_generic(const void *dy, const void *am, const void *relu_y, void *dx,
+                            const ConvShape &sh, int mode, Dtype dt, bool am16, hipStream_t st)
 {
-    const long total = static_cast<long>(sh.N) * sh.Ci * sh.H * sh.W;
+    const long total = static_cast<long>(sh.N) * sh.Ci * sh.D * sh.H * sh.W;
     const int blocks = std::max(1, std::min(cdiv(total, kThreads), 65535 * 16));
-#define HEX_POOL_BWD(T, M)                                                                   \
-    HEX_LAUNCH((pool_bwd_generic_k<T, M>), dim3(blocks), dim3(kThreads), 0, st,     \
-                       (const T *)dy, am, (const T *)relu_y, (T *)dx, sh, total)
+#define HEX_POOL_BWD(T, M, A)                                                                \
+    HEX_LAUNCH((pool_bwd_generic_k<T, M, A>), dim3(blocks), dim3(kThreads), 0, st,           \
+               (const T *)dy, (const A *)am, (const T *)relu_y, (T *)dx, sh, total)
+#define HEX_POOL_BWD_A(T, M)                                                                 \
+    do {                                                                                     \
+        if (am16) HEX_POOL_BWD(T, M, uint16_t); else HEX_POOL_BWD(T, M, uint8_t);            \
+    } while (0)
     if (dt == F32) {
-        if (mode == 0) HEX_POOL_BWD(float, 0); else HEX_POOL_BWD(float, 1);
+        if (mode == 0) HEX_POOL_BWD_A(float, 0); else HEX_POOL_BWD(float, 1, uint8_t);
     } else {
-        if (mode == 0) HEX_POOL_BWD(bf16raw, 0); else HEX_POOL_BWD(bf16raw, 1);
+        if (mode == 0) HEX_POOL_BWD_A(bf16raw, 0); else HEX_POOL_BWD(bf16raw, 1, uint8_t);
     }
+#undef HEX_POOL_BWD_A
 #undef HEX_POOL_BWD
     return hipGetLastError();
 }

@@ -35,8 +35,14 @@ struct KTimer {
 
 enum Dtype { F32 = 0, BF16 = 1 };
 
+// Sizes of one call.  Three-dimensional calls add D planes along z, a
+// window of Z = 2kz+1 planes and a plane stride sz (D_out output planes);
+// 2-D calls have D = Do = Z = sz = 1, kz = 0.  Only the generic kernels
+// read the depth fields; the specialised kernels are chosen for 2-D calls
+// only.
 struct ConvShape {
     int N, Ci, Co, H, W, k, s, Ho, Wo, T;
+    int D, Do, kz, Z, sz;
 };
 
 // Sum weight-gradient partials laid out [e][slot], e = co*(J+1) + col
@@ -77,12 +83,14 @@ hipError_t wgrad_generic(const void *x, const void *dy, float *dw, float *db,
                          hipStream_t st);
 // dw (and db if not null) := 0
 hipError_t fill_zero_f32(float *dw, float *db, const ConvShape &sh, hipStream_t st);
-hipError_t pool_fwd_generic(const void *x, void *y, uint8_t *am,
-                            const ConvShape &sh, int mode, Dtype dt,
+// argmax: uint8_t per output (am16 false) or uint16_t (am16 true, the 3-D
+// entry points), index dz_index * T + t
+hipError_t pool_fwd_generic(const void *x, void *y, void *am,
+                            const ConvShape &sh, int mode, Dtype dt, bool am16,
                             hipStream_t st);
-hipError_t pool_bwd_generic(const void *dy, const uint8_t *am,
+hipError_t pool_bwd_generic(const void *dy, const void *am,
                             const void *relu_y, void *dx, const ConvShape &sh,
-                            int mode, Dtype dt, hipStream_t st);
+                            int mode, Dtype dt, bool am16, hipStream_t st);
 
 // ---- pooling, k <= 3, stride 1 to 4, rows of whole 16-byte chunks -----
 bool pool_fast_ok(const ConvShape &sh, Dtype dt);

@@ -24,6 +24,9 @@ HEX_BF16 = 1
 HEX_POOL_MAX = 0
 HEX_POOL_AVG = 1
 HEX_FLAG_RELU = 1
+HEX_MAX_K = 8
+HEX_MAX_STRIDE = 8
+HEX_MAX_KZ = 4
 
 # (name, argtypes, restype) of every exported symbol
 _P = ctypes.c_void_p
@@ -47,6 +50,13 @@ SIGNATURES = {
     "hexpool_fwd": ([_P, _P, _P, _I, _I, _I, _I, _I, _I, _I, _I, _P], _I),
     "hexpool_bwd": ([_P, _P, _P, _P, _I, _I, _I, _I, _I, _I, _I, _I, _P], _I),
     "hex_status_string": ([_I], ctypes.c_char_p),
+    "hex_out_shape3d": ([_I] * 7 + [_IP, _IP, _IP], _I),
+    "hexconv3d_fwd": ([_P, _P, _P, _P] + [_I] * 12 + [_P], _I),
+    "hexconv3d_bwd_data": ([_P, _P, _P] + [_I] * 11 + [_P], _I),
+    "hexconv3d_bwd_weight_workspace": ([_I] * 11, _S),
+    "hexconv3d_bwd_weight": ([_P, _P, _P, _P, _P, _S] + [_I] * 11 + [_P], _I),
+    "hexpool3d_fwd": ([_P, _P, _P] + [_I] * 11 + [_P], _I),
+    "hexpool3d_bwd": ([_P, _P, _P, _P] + [_I] * 11 + [_P], _I),
     "hexconv_timing_begin": ([], _I),
     "hexconv_timing_end": ([_I, ctypes.c_char_p, _IP, ctypes.POINTER(ctypes.c_double), _IP],
                            _I),
@@ -319,4 +329,107 @@ def hexpool_bwd(dy, argmax_tap, relu_y, dx, k: int, stride: int, mode: int,
         _dev(relu_y, "relu_y", dt, (N, C, H, W)), _dev(dx, "dx", dt),
         N, C, H, W, k, stride, mode, dt, _stream(stream))
     _ok("hexpool_bwd", rc)
+    return dx
+
+
+# ------------------------------------------------------- three dimensions
+# x[N][C][D][H][W]; window of size (k, kz): the size-k hexagon times the
+# planes dz = -kz .. kz; w[C_out][C_in][2kz+1][T]; plane stride stride_z.
+
+def hex_out_shape3d(D: int, H: int, W: int, k: int, kz: int, stride: int, stride_z: int):
+    do, ho, wo = ctypes.c_int(), ctypes.c_int(), ctypes.c_int()
+    _ok("hex_out_shape3d", load().hex_out_shape3d(D, H, W, k, kz, stride, stride_z,
+                                                  ctypes.byref(do), ctypes.byref(ho),
+                                                  ctypes.byref(wo)))
+    return do.value, ho.value, wo.value
+
+
+def hexconv3d_fwd(x, w, bias, y, k: int, kz: int, stride: int = 1, stride_z: int = 1,
+                  relu: bool = False, stream=None):
+    """y <- 3-D hexagonal convolution of x with w (+ bias) (Sec. 2.4)."""
+    N, Ci, D, H, W = x.shape
+    Co = w.shape[0]
+    dt = _dtype_code(x)
+    T = hex_num_taps(k)
+    Do, Ho, Wo = hex_out_shape3d(D, H, W, k, kz, stride, stride_z)
+    rc = load().hexconv3d_fwd(
+        _dev(x, "x", dt), _dev(w, "w", dt, (Co, Ci, 2 * kz + 1, T)),
+        _dev(bias, "bias", dt, (Co,)), _dev(y, "y", dt, (N, Co, Do, Ho, Wo)),
+        N, Ci, Co, D, H, W, k, kz, stride, stride_z, dt, HEX_FLAG_RELU if relu else 0,
+        _stream(stream))
+    _ok("hexconv3d_fwd", rc)
+    return y
+
+
+def hexconv3d_bwd_data(dy, w, dx, k: int, kz: int, stride: int = 1, stride_z: int = 1,
+                       stream=None):
+    N, Ci, D, H, W = dx.shape
+    Co = w.shape[0]
+    dt = _dtype_code(dx)
+    T = hex_num_taps(k)
+    Do, Ho, Wo = hex_out_shape3d(D, H, W, k, kz, stride, stride_z)
+    rc = load().hexconv3d_bwd_data(
+        _dev(dy, "dy", dt, (N, Co, Do, Ho, Wo)), _dev(w, "w", dt, (Co, Ci, 2 * kz + 1, T)),
+        _dev(dx, "dx", dt), N, Ci, Co, D, H, W, k, kz, stride, stride_z, dt, _stream(stream))
+    _ok("hexconv3d_bwd_data", rc)
+    return dx
+
+
+def hexconv3d_bwd_weight_workspace(N, C_in, C_out, D, H, W, k, kz, stride, stride_z, dt):
+    return load().hexconv3d_bwd_weight_workspace(N, C_in, C_out, D, H, W, k, kz, stride,
+                                                 stride_z, dt)
+
+
+def hexconv3d_bwd_weight(x, dy, dw, db, ws, k: int, kz: int, stride: int = 1,
+                         stride_z: int = 1, stream=None):
+    torch = _torch()
+    N, Ci, D, H, W = x.shape
+    Co = dw.shape[0]
+    dt = _dtype_code(x)
+    T = hex_num_taps(k)
+    Do, Ho, Wo = hex_out_shape3d(D, H, W, k, kz, stride, stride_z)
+    if dw.dtype != torch.float32 or (db is not None and db.dtype != torch.float32):
+        raise TypeError("hexconv: dw and db must be float32")
+    ws_bytes = 0 if ws is None else ws.numel() * ws.element_size()
+    rc = load().hexconv3d_bwd_weight(
+        _dev(x, "x", dt), _dev(dy, "dy", dt, (N, Co, Do, Ho, Wo)),
+        _dev(dw, "dw", None, (Co, Ci, 2 * kz + 1, T)), _dev(db, "db", None, (Co,)),
+        _dev(ws, "ws"), ws_bytes, N, Ci, Co, D, H, W, k, kz, stride, stride_z, dt,
+        _stream(stream))
+    _ok("hexconv3d_bwd_weight", rc)
+    return dw, db
+
+
+def hexpool3d_fwd(x, y, argmax, k: int, kz: int, stride: int, stride_z: int, mode: int,
+                  stream=None):
+    """y <- 3-D max (mode 0) or average (mode 1) pooling; argmax: int16
+    tensor (the uint16 tap indices, bit for bit) or None."""
+    torch = _torch()
+    N, C, D, H, W = x.shape
+    dt = _dtype_code(x)
+    Do, Ho, Wo = hex_out_shape3d(D, H, W, k, kz, stride, stride_z)
+    if argmax is not None and argmax.dtype not in (torch.int16, torch.uint16):
+        raise TypeError("hexconv: 3-D argmax must be a 16-bit tensor")
+    rc = load().hexpool3d_fwd(
+        _dev(x, "x", dt), _dev(y, "y", dt, (N, C, Do, Ho, Wo)),
+        _dev(argmax, "argmax", None, (N, C, Do, Ho, Wo)),
+        N, C, D, H, W, k, kz, stride, stride_z, mode, dt, _stream(stream))
+    _ok("hexpool3d_fwd", rc)
+    return y
+
+
+def hexpool3d_bwd(dy, argmax, relu_y, dx, k: int, kz: int, stride: int, stride_z: int,
+                  mode: int, stream=None):
+    torch = _torch()
+    N, C, D, H, W = dx.shape
+    dt = _dtype_code(dx)
+    Do, Ho, Wo = hex_out_shape3d(D, H, W, k, kz, stride, stride_z)
+    if argmax is not None and argmax.dtype not in (torch.int16, torch.uint16):
+        raise TypeError("hexconv: 3-D argmax must be a 16-bit tensor")
+    rc = load().hexpool3d_bwd(
+        _dev(dy, "dy", dt, (N, C, Do, Ho, Wo)),
+        _dev(argmax, "argmax", None, (N, C, Do, Ho, Wo)),
+        _dev(relu_y, "relu_y", dt, (N, C, D, H, W)), _dev(dx, "dx", dt),
+        N, C, D, H, W, k, kz, stride, stride_z, mode, dt, _stream(stream))
+    _ok("hexpool3d_bwd", rc)
     return dx

@@ -230,3 +230,49 @@ def test_timing_host_paths():
     names = ctypes.create_string_buffer(hx.HEX_TIMING_NAME_LEN)
     assert lib.hexconv_timing_end(0, names, counts, total, ctypes.byref(n)) == hx.HEX_ERR_INVALID_ARG
     assert lib.hexconv_timing_end(1, None, counts, total, ctypes.byref(n)) == hx.HEX_ERR_INVALID_ARG
+
+
+def test_out_shape3d_matches_oracle():
+    for sz in range(1, 9):
+        for D in range(1, 12):
+            for (H, W, s) in [(5, 5, 2), (40, 40, 1), (9, 12, 3), (1, 5, 2)]:
+                want = oracle.out_shape3d(D, H, W, s, sz)
+                for k, kz in ((0, 0), (1, 4), (8, 2)):
+                    assert hx.hex_out_shape3d(D, H, W, k, kz, s, sz) == want
+
+
+def test_3d_argument_errors():
+    """3-D entry points reject bad sizes, window depths, plane strides,
+    modes and pointers on the host (fake pointers are never touched)."""
+    lib = hx.load()
+    A, B, C, D_, E = FakePtr.A, FakePtr.B, FakePtr.C, FakePtr.D, FakePtr.E
+    a, b, c = ctypes.c_int(), ctypes.c_int(), ctypes.c_int()
+    shp = lambda D=4, kz=1, sz=1: lib.hex_out_shape3d(D, 8, 8, 1, kz, 1, sz, ctypes.byref(a),
+                                                      ctypes.byref(b), ctypes.byref(c))
+    assert shp() == 0 and (a.value, b.value, c.value) == (4, 8, 8)
+    assert shp(D=0) == hx.HEX_ERR_INVALID_ARG
+    assert shp(kz=hx.HEX_MAX_KZ + 1) == hx.HEX_ERR_INVALID_ARG
+    assert shp(kz=-1) == hx.HEX_ERR_INVALID_ARG
+    assert shp(sz=0) == hx.HEX_ERR_INVALID_ARG
+    assert shp(sz=9) == hx.HEX_ERR_INVALID_ARG
+
+    def fwd(x=A, w=B, y=C, N=2, D=4, kz=1, sz=1, flags=0, dt=0):
+        return lib.hexconv3d_fwd(x, w, None, y, N, 2, 3, D, 8, 8, 1, kz, 1, sz, dt, flags, None)
+    assert fwd(kz=5) == hx.HEX_ERR_INVALID_ARG
+    assert fwd(sz=0) == hx.HEX_ERR_INVALID_ARG
+    assert fwd(D=0) == hx.HEX_ERR_INVALID_ARG
+    assert fwd(x=None) == hx.HEX_ERR_INVALID_ARG
+    assert fwd(y=C + 8) == hx.HEX_ERR_INVALID_ARG
+    assert fwd(flags=2) == hx.HEX_ERR_INVALID_ARG
+    assert fwd(dt=5) == hx.HEX_ERR_INVALID_ARG
+    assert fwd(N=0) == hx.HEX_OK                       # empty batch: nothing enqueued
+    assert fwd(D=70000) == hx.HEX_ERR_UNSUPPORTED
+    assert lib.hexconv3d_bwd_data(A, B, None, 2, 2, 3, 4, 8, 8, 1, 1, 1, 1, 0,
+                                  None) == hx.HEX_ERR_INVALID_ARG
+    assert lib.hexconv3d_bwd_weight(A, B, C, None, None, 0, 2, 2, 3, 4, 8, 8, 1, 1, 1, 1, 0,
+                                    None) == hx.HEX_ERR_INVALID_ARG   # workspace missing
+    assert hx.hexconv3d_bwd_weight_workspace(2, 2, 3, 4, 8, 8, 1, 9, 1, 1, 0) == 0
+    assert lib.hexpool3d_fwd(A, B, C, 2, 3, 4, 8, 8, 1, 1, 1, 1, 2, 0,
+                             None) == hx.HEX_ERR_INVALID_ARG          # mode
+    assert lib.hexpool3d_bwd(A, None, None, D_, 2, 3, 4, 8, 8, 1, 1, 1, 1, 0, 0,
+                             None) == hx.HEX_ERR_INVALID_ARG          # max needs argmax

@@ -1,0 +1,192 @@
+"""GPU parity of the three-dimensional operations (hexagonal x-y planes,
+equidistant planes along z; Sec. 2.4) through the C ABI against the fp64
+oracle, on the same seeded inputs.
+
+Tolerances as for 2-D: float32 rel-L2 <= 1e-5 per output tensor; bfloat16
+|err| <= 1e-2 * (sum of |terms|) per element; max pooling and its argmax
+bit-exact; average pooling within one bf16 ulp of the rounded fp64 value.
+"""
+import numpy as np
+import pytest
+
+import oracle
+from paper_1903_01814_amd import hexconv as hx
+from paper_1903_01814_amd import inputs as gen
+
+from gpu_helpers import (bf16_ulp, check, check_f32, empty, from_dev, round_bf16_f64,
+                         to_dev, torch_mod)
+
+pytestmark = pytest.mark.gpu
+
+
+def _sync():
+    torch_mod().cuda.synchronize()
+
+
+def run_fwd3(x, w, b, k, kz, s, sz, dt, relu=False):
+    N, Ci, D, H, W = x.shape
+    Do, Ho, Wo = hx.hex_out_shape3d(D, H, W, k, kz, s, sz)
+    y = empty((N, w.shape[0], Do, Ho, Wo), dt)
+    hx.hexconv3d_fwd(to_dev(x, dt), to_dev(w, dt), None if b is None else to_dev(b, dt), y,
+                     k, kz, s, sz, relu=relu)
+    _sync()
+    return from_dev(y)
+
+
+def run_bwd_data3(dy, w, k, kz, s, sz, D, H, W, dt):
+    dx = empty((dy.shape[0], w.shape[1], D, H, W), dt)
+    hx.hexconv3d_bwd_data(to_dev(dy, dt), to_dev(w, dt), dx, k, kz, s, sz)
+    _sync()
+    return from_dev(dx)
+
+
+def run_bwd_weight3(x, dy, k, kz, s, sz, dt):
+    torch = torch_mod()
+    N, Ci, D, H, W = x.shape
+    Co = dy.shape[1]
+    T = hx.hex_num_taps(k)
+    dw = torch.full((Co, Ci, 2 * kz + 1, T), float("nan"), dtype=torch.float32, device="cuda:0")
+    db = torch.full((Co,), float("nan"), dtype=torch.float32, device="cuda:0")
+    nws = hx.hexconv3d_bwd_weight_workspace(N, Ci, Co, D, H, W, k, kz, s, sz,
+                                            hx.HEX_F32 if dt == "f32" else hx.HEX_BF16)
+    ws = torch.empty(nws, dtype=torch.uint8, device="cuda:0") if nws else None
+    hx.hexconv3d_bwd_weight(to_dev(x, dt), to_dev(dy, dt), dw, db, ws, k, kz, s, sz)
+    _sync()
+    return from_dev(dw), from_dev(db)
+
+
+def run_pool_fwd3(x, k, kz, s, sz, mode, dt):
+    torch = torch_mod()
+    N, C, D, H, W = x.shape
+    Do, Ho, Wo = hx.hex_out_shape3d(D, H, W, k, kz, s, sz)
+    y = empty((N, C, Do, Ho, Wo), dt)
+    am = torch.full((N, C, Do, Ho, Wo), -1, dtype=torch.int16, device="cuda:0")
+    hx.hexpool3d_fwd(to_dev(x, dt), y, am, k, kz, s, sz, mode)
+    _sync()
+    return from_dev(y), am.cpu().numpy().view(np.uint16).astype(np.int32)
+
+
+def run_pool_bwd3(dy, am, relu_y, k, kz, s, sz, mode, D, H, W, dt):
+    torch = torch_mod()
+    N, C = dy.shape[:2]
+    dx = empty((N, C, D, H, W), dt)
+    amd = None if am is None else torch.from_numpy(
+        np.ascontiguousarray(am.astype(np.uint16).view(np.int16))).to("cuda:0")
+    ry = None if relu_y is None else to_dev(relu_y, dt)
+    hx.hexpool3d_bwd(to_dev(dy, dt), amd, ry, dx, k, kz, s, sz, mode)
+    _sync()
+    return from_dev(dx)
+
+
+CASES = [
+    # N, Ci, Co, D, H, W, k, kz, s, sz
+    (2, 1, 4, 5, 16, 16, 1, 1, 1, 1), (1, 2, 3, 7, 11, 12, 2, 1, 1, 2),
+    (2, 3, 5, 6, 9, 10, 1, 2, 2, 1), (1, 1, 2, 1, 13, 11, 2, 2, 1, 1),
+    (1, 4, 6, 9, 8, 9, 0, 4, 1, 3), (1, 2, 2, 4, 10, 12, 3, 0, 2, 2),
+    (1, 8, 40, 5, 12, 12, 1, 1, 1, 1), (1, 33, 17, 4, 10, 14, 1, 1, 1, 2),
+    (1, 64, 64, 3, 12, 12, 1, 1, 1, 1), (2, 3, 70, 6, 7, 9, 2, 2, 3, 2),
+    (1, 1, 16, 32, 40, 40, 1, 1, 1, 1), (1, 2, 3, 11, 20, 22, 5, 1, 5, 4),
+]
+
+
+@pytest.mark.parametrize("dt", ["f32", "bf16"])
+@pytest.mark.parametrize("case", CASES, ids=lambda c: "N%d_ci%d_co%d_%dx%dx%d_k%d_kz%d_s%d_sz%d" % c)
+def test_conv3d(case, dt):
+    N, Ci, Co, D, H, W, k, kz, s, sz = case
+    rng = np.random.default_rng(sum(case) * 7 + (dt == "bf16"))
+    T = oracle.num_taps(k)
+    Z = 2 * kz + 1
+    x = gen.round_to(rng.normal(size=(N, Ci, D, H, W)), dt)
+    w = gen.round_to(rng.normal(size=(Co, Ci, Z, T)) / np.sqrt(Ci * Z * T), dt)
+    b = gen.round_to(rng.normal(size=Co) * 0.1, dt)
+    y = run_fwd3(x, w, b, k, kz, s, sz, dt)
+    ref = oracle.conv3d_fwd(x, w, b, k, kz, s, sz)
+    mag = oracle.conv3d_fwd(np.abs(x), np.abs(w), np.abs(b), k, kz, s, sz)
+    check(dt, y, ref, mag, "fwd3d")
+    yr = run_fwd3(x, w, None, k, kz, s, sz, dt, relu=True)
+    check(dt, yr, np.maximum(oracle.conv3d_fwd(x, w, None, k, kz, s, sz), 0.0),
+          oracle.conv3d_fwd(np.abs(x), np.abs(w), None, k, kz, s, sz), "fwd3d relu")
+    dy = gen.round_to(rng.normal(size=ref.shape), dt)
+    dx = run_bwd_data3(dy, w, k, kz, s, sz, D, H, W, dt)
+    check(dt, dx, oracle.conv3d_bwd_data(dy, w, k, kz, s, sz, D, H, W),
+          oracle.conv3d_bwd_data(np.abs(dy), np.abs(w), k, kz, s, sz, D, H, W), "dx3d")
+    dw, db = run_bwd_weight3(x, dy, k, kz, s, sz, dt)
+    rw, rb = oracle.conv3d_bwd_weight(x, dy, k, kz, s, sz)
+    mw, mb = oracle.conv3d_bwd_weight(np.abs(x), np.abs(dy), k, kz, s, sz)
+    check(dt, dw, rw, mw, "dw3d")
+    check(dt, db, rb, mb, "db3d")
+
+
+@pytest.mark.parametrize("dt", ["f32", "bf16"])
+def test_conv3d_single_plane_matches_2d(dt):
+    """D = 1, kz = 0: the 3-D entry points compute the 2-D convolution (the
+    2-D call may run another kernel; both are held to the parity bar)."""
+    rng = np.random.default_rng(31)
+    N, Ci, Co, H, W, k = 2, 3, 8, 14, 16, 2
+    T = oracle.num_taps(k)
+    x = gen.round_to(rng.normal(size=(N, Ci, 1, H, W)), dt)
+    w = gen.round_to(rng.normal(size=(Co, Ci, 1, T)) * 0.2, dt)
+    y3 = run_fwd3(x, w, None, k, 0, 1, 1, dt)[:, :, 0]
+    torch = torch_mod()
+    y2 = empty((N, Co, H, W), dt)
+    hx.hexconv_fwd(to_dev(x[:, :, 0], dt), to_dev(w[:, :, 0], dt), None, y2, k, 1)
+    torch.cuda.synchronize()
+    mag = oracle.conv_fwd(np.abs(x[:, :, 0]), np.abs(w[:, :, 0]), None, k, 1)
+    check(dt, y3, from_dev(y2), mag, "3-D vs 2-D")
+
+
+@pytest.mark.parametrize("dt", ["f32", "bf16"])
+@pytest.mark.parametrize("mode", [hx.HEX_POOL_MAX, hx.HEX_POOL_AVG])
+@pytest.mark.parametrize("case", [(2, 3, 5, 9, 10, 1, 1, 2, 1), (1, 2, 7, 12, 12, 1, 1, 1, 2),
+                                  (1, 4, 4, 11, 12, 2, 2, 2, 2), (2, 2, 1, 8, 9, 1, 3, 1, 1),
+                                  (1, 3, 9, 10, 11, 0, 4, 1, 3), (1, 2, 6, 20, 24, 5, 1, 5, 2),
+                                  (1, 2, 5, 33, 35, 8, 2, 8, 1)])
+def test_pool3d(case, mode, dt):
+    N, C, D, H, W, k, kz, s, sz = case
+    rng = np.random.default_rng(sum(case) + 13 * mode)
+    x = gen.round_to(rng.normal(size=(N, C, D, H, W)), dt)
+    x[0, 0, : D // 2 + 1, : H // 2, : W // 2] = 0.5        # plateaus: ties
+    y, am = run_pool_fwd3(x, k, kz, s, sz, mode, dt)
+    ref, ram = oracle.pool3d_fwd(x, k, kz, s, sz, mode)
+    if mode == hx.HEX_POOL_MAX:
+        np.testing.assert_array_equal(y, ref)
+        np.testing.assert_array_equal(am, ram)
+    elif dt == "bf16":
+        want = round_bf16_f64(ref)
+        assert np.all(np.abs(y - want) <= bf16_ulp(want))
+    else:
+        check_f32(y, ref, "avg pool3d")
+    dy = gen.round_to(rng.normal(size=ref.shape), dt)
+    for relu_y in (None, np.maximum(x, 0.0)):
+        amx = ram if mode == hx.HEX_POOL_MAX else None
+        dx = run_pool_bwd3(dy, amx, relu_y, k, kz, s, sz, mode, D, H, W, dt)
+        rdx = oracle.pool3d_bwd(dy, amx, relu_y, k, kz, s, sz, mode, D, H, W)
+        mag = oracle.pool3d_bwd(np.abs(dy), amx, relu_y, k, kz, s, sz, mode, D, H, W)
+        check(dt, dx, rdx, mag, "pool3d bwd")
+
+
+def test_conv3d_empty_batch_and_output():
+    torch = torch_mod()
+    x = torch.empty((0, 1, 3, 8, 8), dtype=torch.float32, device="cuda:0")
+    w = to_dev(np.ones((2, 1, 3, 7)), "f32")
+    y = torch.empty((0, 2, 3, 8, 8), dtype=torch.float32, device="cuda:0")
+    hx.hexconv3d_fwd(x, w, None, y, 1, 1)
+    # H too small for the odd output columns: empty output, zero gradients
+    D, H, W, k, kz, s, sz = 3, 1, 5, 1, 1, 2, 1
+    assert hx.hex_out_shape3d(D, H, W, k, kz, s, sz) == (3, 0, 3)
+    dy = np.zeros((1, 2, 3, 0, 3))
+    dx = run_bwd_data3(dy, np.ones((2, 1, 3, 7)), k, kz, s, sz, D, H, W, "f32")
+    assert np.all(dx == 0)
+    dw, db = run_bwd_weight3(np.ones((1, 1, D, H, W)), dy, k, kz, s, sz, "f32")
+    assert np.all(dw == 0) and np.all(db == 0)
+
+
+def test_conv3d_weight_gradient_deterministic():
+    """Fixed-order partial sums: the same inputs give the same bits."""
+    rng = np.random.default_rng(77)
+    x = rng.normal(size=(2, 4, 6, 20, 20))
+    dy = rng.normal(size=(2, 16, 6, 20, 20))
+    a = run_bwd_weight3(x, dy, 1, 1, 1, 1, "f32")
+    b = run_bwd_weight3(x, dy, 1, 1, 1, 1, "f32")
+    np.testing.assert_array_equal(a[0], b[0])
+    np.testing.assert_array_equal(a[1], b[1])
