@@ -19,8 +19,10 @@ at least 50 steps, each replayed and timed on its own, is reported.
 
 The other workloads are carried as extra keys of the same line ("others"):
 c2 (camera-shaped fp32 layer, 1 -> 16 channels, k=2, GFLOP/s), c3 (bf16
-max and average pooling, GB/s) and c5 (the five-layer bf16 stack, forward
-and backward, samples/s).  --config picks another headline (c1: the tiny
+max and average pooling, GB/s), c5 (the five-layer bf16 stack, forward
+and backward, samples/s) and c6 (3-D convolution of time-resolved camera
+data, 32 time slices, 1 -> 16 channels, k=1 over 3 slices, fp32, forward
+and backward, GFLOP/s).  --config picks another headline (c1: the tiny
 launch-bound forward, reported in microseconds per call).
 
 Prints one JSON line.  With --gpus > 1 it exits: the library runs on one GPU.
@@ -523,6 +525,111 @@ def bench_pool(args, torch, cfg_key, headline=True):
     return out
 
 
+def bench_conv3d(args, torch, cfg_key, headline=True):
+    """3-D hexagonal convolution (time-resolved camera): one step = forward,
+    then the data and weight gradients, over one batch; GFLOP/s."""
+    cfg = gen.CONFIGS[cfg_key]
+    N, Ci, Co, D, H, W, k, kz, s, sz = (cfg[n] for n in ("N", "C_in", "C_out", "D", "H", "W",
+                                                         "k", "kz", "stride", "stride_z"))
+    T = hx.hex_num_taps(k)
+    Z = 2 * kz + 1
+    Do, Ho, Wo = hx.hex_out_shape3d(D, H, W, k, kz, s, sz)
+    dt = torch.float32 if cfg["dtype"] == gen.F32 else torch.bfloat16
+    esz = 4 if dt == torch.float32 else 2
+    x_b, y_b = esz * N * Ci * D * H * W, esz * N * Co * Do * Ho * Wo
+    nsets = max(2, -(-ROTATE_MIN_BYTES // (2 * x_b + 2 * y_b)))
+    d0 = gen.conv3d_inputs(cfg, T, (Do, Ho, Wo), seed=0)
+    sets = []
+    for b in range(nsets):
+        d = d0 if b == 0 else gen.conv3d_inputs(cfg, T, (Do, Ho, Wo), seed=b)
+        sets.append(dict(x=dev(torch, d["x"], dt), dy=dev(torch, d["dy"], dt),
+                         y=torch.empty((N, Co, Do, Ho, Wo), dtype=dt, device="cuda:0"),
+                         dx=torch.empty((N, Ci, D, H, W), dtype=dt, device="cuda:0")))
+    w = dev(torch, d0["w"], dt)
+    bias = dev(torch, d0["b"], dt)
+    dw = torch.empty((Co, Ci, Z, T), dtype=torch.float32, device="cuda:0")
+    db = torch.empty((Co,), dtype=torch.float32, device="cuda:0")
+    nws = hx.hexconv3d_bwd_weight_workspace(N, Ci, Co, D, H, W, k, kz, s, sz,
+                                            hx.HEX_F32 if esz == 4 else hx.HEX_BF16)
+    ws = torch.empty(max(nws, 1), dtype=torch.uint8, device="cuda:0")
+
+    def fwd(i):
+        z = sets[i % nsets]
+        hx.hexconv3d_fwd(z["x"], w, bias, z["y"], k, kz, s, sz)
+
+    def bwd_data(i):
+        z = sets[i % nsets]
+        hx.hexconv3d_bwd_data(z["dy"], w, z["dx"], k, kz, s, sz)
+
+    def bwd_weight(i):
+        z = sets[i % nsets]
+        hx.hexconv3d_bwd_weight(z["x"], z["dy"], dw, db, ws, k, kz, s, sz)
+
+    def step(i):
+        fwd(i)
+        bwd_data(i)
+        bwd_weight(i)
+
+    op_fns = dict(fwd=fwd, bwd_data=bwd_data, bwd_weight=bwd_weight)
+    if args.counter_op:
+        return run_counter_op(args, torch, step, op_fns)
+    timer = EagerTimer(torch) if args.eager else GraphTimer(torch)
+    for i in range(args.warmup):
+        step(i)
+    torch.cuda.synchronize()
+    ms_step = timer.time(step, args.steps)
+    dist = step_distribution(torch, step, nsets)
+    log("%s: %.5f ms per step (%d steps), median %.5f" % (cfg["name"], ms_step, args.steps,
+                                                          dist["median"]))
+    g_b = 4 * (Co * Ci * Z * T + Co)
+    bytes_alg = {"fwd": x_b + y_b + esz * (Co * Ci * Z * T + Co),
+                 "bwd_data": y_b + x_b + esz * Co * Ci * Z * T,
+                 "bwd_weight": x_b + y_b + g_b}
+    flop_op = 2.0 * N * Do * Ho * Wo * Ci * Co * Z * T
+    reps_op = max(20, min(args.steps, 200))
+    ops = {}
+    for name, fn in op_fns.items():
+        ms = timer.time(fn, reps_op)
+        ops[name] = dict(ms=ms, gbs=bytes_alg[name] / (ms * 1e-3) / 1e9)
+    dom = max(ops, key=lambda n: ops[n]["ms"])
+    kname, kms, kper, kall = dominant_kernel(torch, op_fns[dom], reps_op)
+    roof = roofline_entry("hbm", bytes_alg[dom] / kper, kname, kms, kper, dom, kall, cfg["name"])
+    out = dict(
+        metric=METRIC, value=round(3 * flop_op / (ms_step * 1e-3) / 1e9, 2), unit="GFLOP/s",
+        n_gpus=1, steps=args.steps, warmup=args.warmup, ms_per_step=round(ms_step, 5),
+        higher_is_better=True, scaling="weak", vs_baseline=None,
+        dtype="f32" if esz == 4 else "bf16", data="synthetic",
+        config=dict(workload=cfg["name"], N=N, C_in=Ci, C_out=Co, D=D, H=H, W=W, k=k, kz=kz,
+                    stride=s, stride_z=sz, taps=Z * T, D_out=Do, H_out=Ho, W_out=Wo,
+                    rotating_batches=nsets, step="fwd, then dx, then dw+db"),
+        hbm_GBps=round(sum(bytes_alg.values()) / (ms_step * 1e-3) / 1e9, 1),
+        samples_per_s=round(N / (ms_step * 1e-3), 1),
+        step_ms=dist,
+        per_op={n: dict(ms=round(v["ms"], 5), alg_GBps=round(v["gbs"], 1),
+                        GFLOPs=round(flop_op / (v["ms"] * 1e-3) / 1e9, 1))
+                for n, v in ops.items()},
+        roofline=roof,
+    )
+    if headline and not args.no_cpu_baseline:
+        import oracle
+        n_slice = 8
+        xs, dys = d0["x"][:n_slice], d0["dy"][:n_slice]
+
+        def body():
+            oracle.conv3d_fwd(xs, d0["w"], d0["b"], k, kz, s, sz)
+            oracle.conv3d_bwd_data(dys, d0["w"], k, kz, s, sz, D, H, W)
+            oracle.conv3d_bwd_weight(xs, dys, k, kz, s, sz)
+
+        log("cpu baseline")
+        reps, el = repeat_for(args.cpu_seconds, body)
+        out["cpu_baseline"] = dict(
+            value=round(3 * flop_op * n_slice / N * reps / el / 1e9, 3), unit="GFLOP/s",
+            cores=oracle.threads(), kind="oracle", cpu_model=cpu_model(), host_cores=host_cores(),
+            sample="%d of %d events, fwd+bwd_data+bwd_weight, fp64, repeated %d times in %.1f s"
+                   % (n_slice, N, reps, el))
+    return out
+
+
 def stack_shapes(cfg):
     """Per layer: (kind, C_in, C_out, k, stride, relu, H_in, W_in, H_out, W_out)."""
     H, W = cfg["H"], cfg["W"]
@@ -776,7 +883,7 @@ def calibration_copy(torch, mib):
 
 
 BENCHES = {"c1": bench_conv, "c2": bench_conv, "c3": bench_pool, "c4": bench_conv,
-           "c5": bench_stack}
+           "c5": bench_stack, "c6": bench_conv3d}
 
 
 def compact(line):
@@ -793,7 +900,7 @@ def main():
     p.add_argument("--steps", type=int, default=200)
     p.add_argument("--warmup", type=int, default=20)
     p.add_argument("--config", default="c4", choices=sorted(BENCHES))
-    p.add_argument("--also", default="c2,c3,c5",
+    p.add_argument("--also", default="c2,c3,c5,c6",
                    help="comma-separated workloads carried as extra keys ('' for none)")
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--eager", action="store_true",

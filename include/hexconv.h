@@ -289,6 +289,11 @@ int hexpool3d_bwd(const void *dy, const uint16_t *argmax, const void *relu_y, vo
 /* Static description of a hex_status value. */
 const char *hex_status_string(int status);
 
+/* For diagnosis: the HIP runtime's description of the error behind the last
+ * HEX_ERR_LAUNCH returned on the calling thread ("" if there was none).
+ * Static string, never NULL. */
+const char *hex_last_launch_error(void);
+
 /*
  * Kernel timing, for profiling (not part of the paper's operations).
  * Between hexconv_timing_begin() and hexconv_timing_end(), every kernel the

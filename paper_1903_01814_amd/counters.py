@@ -220,7 +220,7 @@ def main():
     p = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     sub = p.add_subparsers(dest="cmd", required=True)
     q = sub.add_parser("pmc")
-    q.add_argument("--config", required=True, choices=["c2", "c3", "c4", "c5"])
+    q.add_argument("--config", required=True, choices=["c2", "c3", "c4", "c5", "c6"])
     q.add_argument("--op", required=True, help="op of the workload, as bench.py names it")
     q.add_argument("--kernel", required=True, help="kernel base name, as bench.py reports it")
     q.add_argument("--out-dir", default=os.path.join(ROOT, "gpurun_out", "pmc"))
@@ -230,7 +230,7 @@ def main():
                    help="summarise the CSVs an earlier run left under --out-dir")
     q = sub.add_parser("stats")
     q.add_argument("--dest", default=os.path.join(ROOT, "profiles"))
-    q.add_argument("--config", required=True, choices=["c1", "c2", "c3", "c4", "c5"])
+    q.add_argument("--config", required=True, choices=["c1", "c2", "c3", "c4", "c5", "c6"])
     q.add_argument("--csv", required=True)
     q.add_argument("--command", required=True)
     q.add_argument("--bench-json", default=None)

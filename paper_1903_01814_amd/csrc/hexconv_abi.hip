@@ -168,7 +168,16 @@ int ptrs_ok(std::initializer_list<const void *> required, std::initializer_list<
     return HEX_OK;
 }
 
-int launched(hipError_t e) { return e == hipSuccess ? HEX_OK : HEX_ERR_LAUNCH; }
+// HIP status of the last failed launch on this thread (hex_last_launch_error)
+thread_local hipError_t g_last_launch_error = hipSuccess;
+
+int launched(hipError_t e)
+{
+    if (e == hipSuccess)
+        return HEX_OK;
+    g_last_launch_error = e;
+    return HEX_ERR_LAUNCH;
+}
 
 // HEXCONV_PATH=generic forces the generic kernels (used by tests to compare
 // the specialised kernels against them).
@@ -707,6 +716,11 @@ int hexconv_timing_end(int max_kernels, char *names, int *counts, double *total_
     hexk::g_timed.clear();
     *n_kernels = static_cast<int>(order.size());
     return rc;
+}
+
+const char *hex_last_launch_error(void)
+{
+    return g_last_launch_error == hipSuccess ? "" : hipGetErrorString(g_last_launch_error);
 }
 
 const char *hex_status_string(int status)

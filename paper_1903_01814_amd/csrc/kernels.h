@@ -27,8 +27,13 @@ struct KTimer {
     hipEvent_t a_, b_;
 };
 
+// The launchers report hipGetLastError() after their launches; the
+// thread's error state is cleared first, so that a status left by an
+// earlier runtime call of the caller (or of another library on the same
+// thread) is not taken for a failure of this launch.
 #define HEX_LAUNCH(kern, grid, block, shm, st, ...)                                          \
     do {                                                                                     \
+        (void)hipGetLastError();                                                             \
         ::hexk::KTimer hex_kt_(#kern, st);                                                   \
         hipLaunchKernelGGL(kern, grid, block, shm, st, __VA_ARGS__);                         \
     } while (0)

@@ -50,6 +50,7 @@ SIGNATURES = {
     "hexpool_fwd": ([_P, _P, _P, _I, _I, _I, _I, _I, _I, _I, _I, _P], _I),
     "hexpool_bwd": ([_P, _P, _P, _P, _I, _I, _I, _I, _I, _I, _I, _I, _P], _I),
     "hex_status_string": ([_I], ctypes.c_char_p),
+    "hex_last_launch_error": ([], ctypes.c_char_p),
     "hex_out_shape3d": ([_I] * 7 + [_IP, _IP, _IP], _I),
     "hexconv3d_fwd": ([_P, _P, _P, _P] + [_I] * 12 + [_P], _I),
     "hexconv3d_bwd_data": ([_P, _P, _P] + [_I] * 11 + [_P], _I),
@@ -70,13 +71,25 @@ _lib = None
 class HexError(RuntimeError):
     def __init__(self, fn, status):
         self.status = status
-        super().__init__("%s: %s" % (fn, status_string(status)))
+        msg = "%s: %s" % (fn, status_string(status))
+        if status == HEX_ERR_LAUNCH:
+            msg += " (%s)" % load().hex_last_launch_error().decode()
+        super().__init__(msg)
 
 
 def load():
-    """Load libhexconv.so (must have been built, e.g. by build.build())."""
+    """Load libhexconv.so (must have been built, e.g. by build.build()).
+
+    torch is imported first.  torch ships its own HIP runtime (needed under
+    the name libamdhip64.so), while libhexconv links the system one
+    (libamdhip64.so.7); both then share the HSA runtime that was loaded
+    first.  With libhexconv loaded before torch, torch's HIP runtime ends up
+    on the system HSA runtime and the system HIP runtime, initialised after
+    it, finds no device.  Loading torch's libraries first keeps the one
+    order that works."""
     global _lib
     if _lib is None:
+        import torch  # noqa: F401  (load order of the HIP runtimes, above)
         if not os.path.exists(LIB_PATH):
             raise RuntimeError(
                 "libhexconv.so not found at %s: build it first "

@@ -45,6 +45,11 @@ CONFIGS = {
                layers=[("conv", 1, 32, 2, 1, True), ("pool", 32, 1, 2),
                        ("conv", 32, 64, 2, 1, False), ("pool", 64, 1, 2),
                        ("conv", 64, 128, 1, 1, False)]),
+    # time-resolved camera (hexagonal planes, equidistant time samples):
+    # 3-D convolution over a window of 3 time slices, forward and backward
+    "c6": dict(name="c6_time_resolved_3d_fp32", kind="conv3d", N=64, C_in=1,
+               C_out=16, D=32, H=40, W=40, k=1, kz=1, stride=1, stride_z=1,
+               dtype=F32, bias=True, bwd=True, x_dist="camera_footprint"),
 }
 
 # Hexagonal camera footprint of config 2: every pixel within 18 neighbour
@@ -171,3 +176,22 @@ def stack_inputs(cfg: dict, taps_of, out_hw, seed: int = 0,
             params.append(None)
     dy = rng.standard_normal(size=(n, C) + tuple(out_hw))
     return dict(x=round_to(x, dt), params=params, dy=round_to(dy, dt))
+
+
+def conv3d_inputs(cfg: dict, T: int, out_dhw, seed: int = 0, N: int | None = None):
+    """x [N][C_in][D][H][W], w [C_out][C_in][2kz+1][T] (He-normal over the
+    (2kz+1) T C_in fan-in), b, dy for a 3-D convolution workload, rounded to
+    dtype.  Every plane of x follows the camera recipe of `x_dist`."""
+    rng = np.random.default_rng(seed)
+    n = cfg["N"] if N is None else N
+    dt = cfg["dtype"]
+    Z = 2 * cfg["kz"] + 1
+    x = _draw_x(rng, (n, cfg["C_in"], cfg["D"], cfg["H"], cfg["W"]), cfg["x_dist"])
+    w = _draw_w(rng, cfg["C_out"], cfg["C_in"] * Z, T, "he").reshape(cfg["C_out"], cfg["C_in"],
+                                                                    Z, T)
+    b = rng.normal(0.0, 0.1, size=cfg["C_out"]) if cfg.get("bias") else None
+    out = dict(x=round_to(x, dt), w=round_to(w, dt), b=None if b is None else round_to(b, dt))
+    if cfg.get("bwd"):
+        dy = rng.standard_normal(size=(n, cfg["C_out"]) + tuple(out_dhw))
+        out["dy"] = round_to(dy, dt)
+    return out

@@ -190,3 +190,21 @@ def test_conv3d_weight_gradient_deterministic():
     b = run_bwd_weight3(x, dy, 1, 1, 1, 1, "f32")
     np.testing.assert_array_equal(a[0], b[0])
     np.testing.assert_array_equal(a[1], b[1])
+
+
+def test_c6_time_resolved_full():
+    """The benchmark's 3-D workload at full size (64 events x 32 time
+    slices of the 40x40 camera footprint, 1 -> 16 channels, k = 1, kz = 1,
+    float32), forward and both gradients compared with the oracle in full."""
+    cfg = gen.CONFIGS["c6"]
+    k, kz, s, sz = cfg["k"], cfg["kz"], cfg["stride"], cfg["stride_z"]
+    D, H, W = cfg["D"], cfg["H"], cfg["W"]
+    d = gen.conv3d_inputs(cfg, oracle.num_taps(k), oracle.out_shape3d(D, H, W, s, sz))
+    y = run_fwd3(d["x"], d["w"], d["b"], k, kz, s, sz, "f32")
+    check_f32(y, oracle.conv3d_fwd(d["x"], d["w"], d["b"], k, kz, s, sz), "c6 fwd")
+    dx = run_bwd_data3(d["dy"], d["w"], k, kz, s, sz, D, H, W, "f32")
+    check_f32(dx, oracle.conv3d_bwd_data(d["dy"], d["w"], k, kz, s, sz, D, H, W), "c6 dx")
+    dw, db = run_bwd_weight3(d["x"], d["dy"], k, kz, s, sz, "f32")
+    rw, rb = oracle.conv3d_bwd_weight(d["x"], d["dy"], k, kz, s, sz)
+    check_f32(dw, rw, "c6 dw")
+    check_f32(db, rb, "c6 db")
