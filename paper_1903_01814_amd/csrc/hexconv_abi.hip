@@ -344,6 +344,8 @@ int hexconv_fwd(const void *x, const void *w, const void *bias, void *y, int N, 
             return launched(hexk::smallc_fwd(x, w, bias, y, sh, d, relu, st));
         if (d == hexk::BF16 && hexk::bf16_wide_ok(sh, sh.Ci, sh.Co))
             return launched(hexk::bf16_wide_conv(x, w, bias, y, sh, false, relu, st));
+        if (d == hexk::BF16 && hexk::bf16_gen_fwd_ok(sh))
+            return launched(hexk::bf16_gen_fwd(x, w, bias, y, sh, relu, st));
     }
     if (!hexk::conv_fwd_generic_ok(sh))
         return HEX_ERR_UNSUPPORTED;
@@ -372,6 +374,8 @@ int hexconv_bwd_data(const void *dy, const void *w, void *dx, int N, int C_in, i
                                                       static_cast<float *>(dx), sh, st));
         if (d == hexk::BF16 && hexk::bf16_wide_ok(sh, sh.Co, sh.Ci))
             return launched(hexk::bf16_wide_conv(dy, w, nullptr, dx, sh, true, false, st));
+        if (d == hexk::BF16 && hexk::bf16_gen_dgrad_ok(sh))
+            return launched(hexk::bf16_gen_dgrad(dy, w, dx, sh, st));
     }
     if (!hexk::conv_bwd_data_generic_ok(sh))
         return HEX_ERR_UNSUPPORTED;

@@ -128,6 +128,17 @@ bool bf16_wide_ok(const ConvShape &sh, int IC, int OC);
 hipError_t bf16_wide_conv(const void *in, const void *w, const void *bias, void *out,
                           const ConvShape &sh, bool reflect, bool relu, hipStream_t st);
 
+// ---- bf16 matrix-core convolution at any stride, k <= 3 ------------------
+// forward: C_in % 32 == 0, W % 8 == 0, W_out <= 256; data gradient (the
+// transposed lattice gather): C_out % 32 == 0, W and W_out % 8 == 0,
+// W <= 256, H a multiple of the stride
+bool bf16_gen_fwd_ok(const ConvShape &sh);
+hipError_t bf16_gen_fwd(const void *x, const void *w, const void *bias, void *y,
+                        const ConvShape &sh, bool relu, hipStream_t st);
+bool bf16_gen_dgrad_ok(const ConvShape &sh);
+hipError_t bf16_gen_dgrad(const void *dy, const void *w, void *dx, const ConvShape &sh,
+                          hipStream_t st);
+
 // ---- bf16 32x32 matrix-core weight gradient (C_in, C_out multiples of 32) --
 // output-channel passes the kernel needs for this shape (0: not supported)
 int bf16_wgrad32_passes(const ConvShape &sh);

@@ -425,6 +425,41 @@ def test_pool_large_k_and_stride(case, mode, dt):
         check(dt, dx, rdx, mag, "pool bwd")
 
 
+# bf16 matrix-core convolution at any stride and k <= 3 (k_mfma_gen.hip):
+# forward for C_in % 32 == 0, W % 8 == 0; data gradient (transposed lattice
+# gather) for C_out % 32 == 0, W and W_out % 8 == 0, H a multiple of the
+# stride.  Strides 1 (k = 3) to 8, several 32-channel chunks, 64-channel
+# blocks cut short, ragged row tiles, output widths that are not a multiple
+# of 8 (scalar stores), data-gradient tiles in several rounds of pixel
+# groups (strides 3 and 4 over wide rows).
+GEN_CASES = [
+    # N, Ci, Co, H, W, k, s
+    (2, 32, 32, 12, 16, 3, 1), (1, 64, 96, 9, 24, 3, 1), (1, 96, 32, 8, 40, 3, 1),
+    (2, 32, 64, 20, 32, 1, 2), (1, 64, 64, 34, 48, 2, 2), (1, 32, 32, 14, 64, 3, 2),
+    (1, 32, 32, 30, 48, 1, 3), (2, 64, 32, 24, 96, 2, 3), (1, 32, 64, 24, 32, 1, 4),
+    (1, 32, 32, 32, 128, 3, 4), (1, 32, 32, 40, 40, 2, 5), (2, 32, 32, 40, 64, 3, 8),
+    (1, 32, 32, 21, 40, 1, 2), (1, 32, 48, 10, 24, 2, 1), (3, 64, 64, 16, 128, 1, 2),
+    (1, 32, 32, 24, 256, 2, 3),
+]
+
+
+@pytest.mark.parametrize("case", GEN_CASES, ids=lambda c: "N%d_ci%d_co%d_%dx%d_k%d_s%d" % c)
+def test_conv_matrix_core_any_stride(case):
+    N, Ci, Co, H, W, k, s = case
+    rng = np.random.default_rng(5000 + sum(case))
+    T = oracle.num_taps(k)
+    x = gen.round_to(rng.normal(size=(N, Ci, H, W)), "bf16")
+    w = gen.round_to(rng.normal(size=(Co, Ci, T)) / np.sqrt(Ci * T), "bf16")
+    b = gen.round_to(rng.normal(size=Co) * 0.1, "bf16")
+    check_fwd_full(x, w, b, k, s, "bf16", what="fwd")
+    check_fwd_full(x, w, None, k, s, "bf16", relu=True, what="fwd relu")
+    Ho, Wo = oracle.out_shape(H, W, s)
+    dy = gen.round_to(rng.normal(size=(N, Co, Ho, Wo)), "bf16")
+    dx = run_bwd_data(dy, w, k, s, H, W, "bf16")
+    check("bf16", dx, oracle.conv_bwd_data(dy, w, k, s, H, W),
+          oracle.conv_bwd_data(np.abs(dy), np.abs(w), k, s, H, W), "dx")
+
+
 @pytest.mark.parametrize("dt", ["f32", "bf16"])
 @pytest.mark.parametrize("mode", [hx.HEX_POOL_MAX, hx.HEX_POOL_AVG])
 @pytest.mark.parametrize("case", [(2, 3, 9, 10, 1, 2), (1, 4, 40, 40, 1, 2),
