@@ -61,7 +61,7 @@ struct GenArgs {
     int tiles;        // tiles per image
     int WR, WC;       // window rows and slots per row
     int coff;         // slot column of source column 0
-    int TG;           // taps per weight stage
+    int TG;           // taps per weight stage (kTG)
     int win_off;      // byte offsets in LDS: window, weights, output staging
     int wgt_off;
     int out_off;
@@ -83,35 +83,45 @@ __device__ __forceinline__ void stage_window(bf16raw *__restrict__ win,
                                              int Hsrc, int Wsrc, int g_r0, int nrows, int WC,
                                              int coff)
 {
+    constexpr int U = 2; // items per thread per round, all loads issued first
     const int ncol8 = Wsrc >> 3;
     const int items = nrows * ncol8 * 4;
-    for (int it = threadIdx.x; it < items; it += kGThreads) {
-        const int g = it & 3, rest = it >> 2;
-        const int ch = rest % ncol8, rr = rest / ncol8;
-        const int r = g_r0 + rr, col0 = 8 * ch;
-        if (col0 + coff >= WC)
-            continue;
-        uint4 v[8];
-        const bool rin = r >= 0 && r < Hsrc;
+    for (int it0 = threadIdx.x; it0 < items; it0 += U * kGThreads) {
+        uint4 v[U][8];
+        int slot0[U], ncopy[U], grp[U];
 #pragma unroll
-        for (int e = 0; e < 8; ++e)
-            v[e] = rin ? *reinterpret_cast<const uint4 *>(src + (8 * g + e) * HW +
-                                                          static_cast<size_t>(r) * Wsrc + col0)
-                       : make_uint4(0, 0, 0, 0);
-        const int slot0 = rr * WC + col0 + coff;
+        for (int h = 0; h < U; ++h) {
+            const int it = it0 + h * kGThreads;
+            const int g = it & 3, rest = it >> 2;
+            const int ch = rest % ncol8, rr = rest / ncol8;
+            const int r = g_r0 + rr, col0 = 8 * ch;
+            const bool live = it < items && col0 + coff < WC;
+            const bool rin = live && r >= 0 && r < Hsrc;
 #pragma unroll
-        for (int px = 0; px < 8; ++px) {
-            if (col0 + coff + px >= WC)
-                break;
-            uint32_t q[4];
+            for (int e = 0; e < 8; ++e)
+                v[h][e] = rin ? *reinterpret_cast<const uint4 *>(src + (8 * g + e) * HW +
+                                                                 static_cast<size_t>(r) * Wsrc + col0)
+                              : make_uint4(0, 0, 0, 0);
+            slot0[h] = rr * WC + col0 + coff;
+            ncopy[h] = live ? min(8, WC - col0 - coff) : 0;
+            grp[h] = g;
+        }
 #pragma unroll
-            for (int h = 0; h < 4; ++h) {
-                const uint32_t a = reinterpret_cast<const uint32_t *>(&v[2 * h])[px >> 1];
-                const uint32_t b = reinterpret_cast<const uint32_t *>(&v[2 * h + 1])[px >> 1];
-                q[h] = (px & 1) ? (hi16(a) | (b & 0xffff0000u)) : (lo16(a) | (b << 16));
+        for (int h = 0; h < U; ++h) {
+#pragma unroll
+            for (int px = 0; px < 8; ++px) {
+                if (px >= ncopy[h])
+                    break;
+                uint32_t q[4];
+#pragma unroll
+                for (int j = 0; j < 4; ++j) {
+                    const uint32_t a = reinterpret_cast<const uint32_t *>(&v[h][2 * j])[px >> 1];
+                    const uint32_t b = reinterpret_cast<const uint32_t *>(&v[h][2 * j + 1])[px >> 1];
+                    q[j] = (px & 1) ? (hi16(a) | (b & 0xffff0000u)) : (lo16(a) | (b << 16));
+                }
+                *reinterpret_cast<uint4 *>(win + (slot0[h] + px) * kCP + 8 * grp[h]) =
+                    make_uint4(q[0], q[1], q[2], q[3]);
             }
-            *reinterpret_cast<uint4 *>(win + (slot0 + px) * kCP + 8 * g) =
-                make_uint4(q[0], q[1], q[2], q[3]);
         }
     }
     // slot columns without a source column: [0, coff) and [Wsrc + coff, WC)
@@ -126,31 +136,53 @@ __device__ __forceinline__ void stage_window(bf16raw *__restrict__ win,
     }
 }
 
-// Weights of taps [t0, t0 + ntap) into LDS as wl[(tt * kNB + n) * kCP + kc]:
+// Weights of one stage -- taps [t0, t0 + kTG) of one 32-channel chunk of
+// the contraction, for the block's 64 destination channels -- as
+// wl[(tt * kNB + n) * kCP + kc]:
 //   forward (DG = false): n = output channel d0 + n, kc = input channel c0 + kc,
 //     value w[d0 + n][c0 + kc][t0 + tt];
 //   data gradient (DG = true): n = input channel d0 + n, kc = output channel
 //     c0 + kc, value w[c0 + kc][d0 + n][t0 + tt].
-// Zero for destination channels past Cd.  w is [Cout][Cin][T].
-template <bool DG>
-__device__ __forceinline__ void stage_wgt(bf16raw *__restrict__ wl, const bf16raw *__restrict__ w,
-                                          int T, int Cs, int Cd, int d0, int c0, int t0, int ntap)
-{
-    const int total = ntap * kNB * kCK;
-    for (int e = threadIdx.x; e < total; e += kGThreads) {
-        const int tt = e % ntap, rest = e / ntap;
-        const int kc = rest % kCK, n = rest / kCK;
-        const int d = d0 + n;
-        bf16raw v = 0;
-        if (d < Cd) {
-            // forward: w[d][c0 + kc][t]; data gradient: w[c0 + kc][d][t]
-            const size_t idx = DG ? (static_cast<size_t>(c0 + kc) * Cd + d) * T + t0 + tt
-                                  : (static_cast<size_t>(d) * Cs + c0 + kc) * T + t0 + tt;
-            v = w[idx];
+// Zero for destination channels past Cd and taps past T.  w is
+// [Cout][Cin][T]: the kTG taps of one (n, kc) are consecutive in memory, and
+// element e of the stage is (tt, kc, n) = (e % 8, (e / 8) % 32, e / 256), so
+// eight consecutive lanes read one 16-byte run.  load() issues all of a
+// thread's loads (into registers, while the previous stage computes);
+// store() writes them to LDS.
+constexpr int kTG = 8;                                // taps per stage
+constexpr int kWPer = kTG * kNB * kCK / kGThreads;    // elements per thread
+
+template <bool DG> struct WgtRegs {
+    bf16raw v[kWPer];
+
+    __device__ __forceinline__ void load(const bf16raw *__restrict__ w, int T, int Cs, int Cd,
+                                         int d0, int c0, int t0)
+    {
+#pragma unroll
+        for (int u = 0; u < kWPer; ++u) {
+            const int e = threadIdx.x + u * kGThreads;
+            const int tt = e & 7, kc = (e >> 3) & 31, n = e >> 8;
+            const int d = d0 + n, t = t0 + tt;
+            bf16raw x = 0;
+            if (d < Cd && t < T) {
+                const size_t idx = DG ? (static_cast<size_t>(c0 + kc) * Cd + d) * T + t
+                                      : (static_cast<size_t>(d) * Cs + c0 + kc) * T + t;
+                x = w[idx];
+            }
+            v[u] = x;
         }
-        wl[(tt * kNB + n) * kCP + kc] = v;
     }
-}
+
+    __device__ __forceinline__ void store(bf16raw *__restrict__ wl) const
+    {
+#pragma unroll
+        for (int u = 0; u < kWPer; ++u) {
+            const int e = threadIdx.x + u * kGThreads;
+            const int tt = e & 7, kc = (e >> 3) & 31, n = e >> 8;
+            wl[(tt * kNB + n) * kCP + kc] = v[u];
+        }
+    }
+};
 
 // Slot offset of axial tap (dq, ds) from a forward centre: row ds + dq/2
 // (floor), plus one more row for odd dq when the centre column is odd.
@@ -230,29 +262,36 @@ __global__ __launch_bounds__(kGThreads) void conv_gen_fwd_k(const bf16raw *__res
         acc[m][0] = acc[m][1] = floatx16{};
 
     const size_t HWs = static_cast<size_t>(a.Hs) * a.Ws;
-    for (int c0 = 0; c0 < a.Cs; c0 += kCK) {
-        for (int t0 = 0; t0 < T; t0 += a.TG) {
-            const int ntap = min(a.TG, T - t0);
-            __syncthreads(); // the previous stage's readers are done
-            if (t0 == 0)
-                stage_window(win, x + (static_cast<size_t>(n) * a.Cs + c0) * HWs, HWs, a.Hs,
-                             a.Ws, r_lo, a.WR, a.WC, a.coff);
-            stage_wgt<false>(wl, w, T, a.Cs, a.Cd, d0, c0, t0, ntap);
-            __syncthreads();
-            if (ng == 0)
-                continue;
-            for (int tt = 0; tt < ntap; ++tt) {
-                const int t = t0 + tt;
-                const int dq = tab.dq[t], ds = tab.ds[t];
-                const int off = fwd_tap_off(dq, ds, a.WC);
-                int slot[kMG];
+    // stages: (chunk c0, taps t0 .. t0 + 7); the next stage's weights are
+    // loaded into registers while the current stage computes
+    constexpr int NTG = (T + kTG - 1) / kTG;
+    const int nst = (a.Cs / kCK) * NTG;
+    WgtRegs<false> wr;
+    wr.load(w, T, a.Cs, a.Cd, d0, 0, 0);
+    for (int st = 0; st < nst; ++st) {
+        const int c0 = (st / NTG) * kCK, t0 = (st % NTG) * kTG;
+        __syncthreads(); // the previous stage's readers are done
+        if (t0 == 0)
+            stage_window(win, x + (static_cast<size_t>(n) * a.Cs + c0) * HWs, HWs, a.Hs, a.Ws,
+                         r_lo, a.WR, a.WC, a.coff);
+        wr.store(wl);
+        __syncthreads();
+        if (st + 1 < nst)
+            wr.load(w, T, a.Cs, a.Cd, d0, ((st + 1) / NTG) * kCK, ((st + 1) % NTG) * kTG);
+        if (ng == 0)
+            continue;
+        const int ntap = min(kTG, T - t0);
+        for (int tt = 0; tt < ntap; ++tt) {
+            const int t = t0 + tt;
+            const int dq = tab.dq[t], ds = tab.ds[t];
+            const int off = fwd_tap_off(dq, ds, a.WC);
+            int slot[kMG];
 #pragma unroll
-                for (int m = 0; m < kMG; ++m)
-                    slot[m] = slot0[m] + off + ((dq & 1) ? podd[m] : 0);
-                const bf16raw *wrow = wl + (tt * kNB + n32) * kCP + 8 * kh;
-                kstep<kMG>(acc, win, wrow, slot, ng, 0, kh);
-                kstep<kMG>(acc, win, wrow, slot, ng, 1, kh);
-            }
+            for (int m = 0; m < kMG; ++m)
+                slot[m] = slot0[m] + off + ((dq & 1) ? podd[m] : 0);
+            const bf16raw *wrow = wl + (tt * kNB + n32) * kCP + 8 * kh;
+            kstep<kMG>(acc, win, wrow, slot, ng, 0, kh);
+            kstep<kMG>(acc, win, wrow, slot, ng, 1, kh);
         }
     }
 
@@ -404,45 +443,49 @@ __global__ __launch_bounds__(kGThreads) void conv_gen_dgrad_k(const bf16raw *__r
         for (int m = 0; m < kMG; ++m)
             acc[m][0] = acc[m][1] = floatx16{};
 
-        for (int c0 = 0; c0 < a.Cs; c0 += kCK) {
-            for (int t0 = 0; t0 < T; t0 += a.TG) {
-                const int ntap = min(a.TG, T - t0);
-                __syncthreads();
-                if (t0 == 0)
-                    stage_window(win, dy + (static_cast<size_t>(n) * a.Cs + c0) * HWs, HWs, a.Hs,
-                                 a.Ws, i_lo, a.WR, a.WC, a.coff);
-                stage_wgt<true>(wl, w, T, a.Cs, a.Cd, d0, c0, t0, ntap);
-                __syncthreads();
-                if (ng == 0)
-                    continue;
-                for (int tt = 0; tt < ntap; ++tt) {
-                    const int t = t0 + tt;
-                    const int dq = tab.dq[t], ds = tab.ds[t];
-                    const bf16raw *wrow = wl + (tt * kNB + n32) * kCP + 8 * kh;
+        constexpr int NTG = (T + kTG - 1) / kTG;
+        const int nst = (a.Cs / kCK) * NTG;
+        WgtRegs<true> wr;
+        wr.load(w, T, a.Cs, a.Cd, d0, 0, 0);
+        for (int st = 0; st < nst; ++st) {
+            const int c0 = (st / NTG) * kCK, t0 = (st % NTG) * kTG;
+            __syncthreads();
+            if (t0 == 0)
+                stage_window(win, dy + (static_cast<size_t>(n) * a.Cs + c0) * HWs, HWs, a.Hs,
+                             a.Ws, i_lo, a.WR, a.WC, a.coff);
+            wr.store(wl);
+            __syncthreads();
+            if (st + 1 < nst)
+                wr.load(w, T, a.Cs, a.Cd, d0, ((st + 1) / NTG) * kCK, ((st + 1) % NTG) * kTG);
+            if (ng == 0)
+                continue;
+            const int ntap = min(kTG, T - t0);
+            for (int tt = 0; tt < ntap; ++tt) {
+                const int t = t0 + tt;
+                const int dq = tab.dq[t], ds = tab.ds[t];
+                const bf16raw *wrow = wl + (tt * kNB + n32) * kCP + 8 * kh;
 #pragma unroll
-                    for (int m = 0; m < kMG; ++m) {
-                        if (m >= ng)
-                            break;
-                        // live iff (dq, ds) = (a, b) mod s (wave-uniform)
-                        const int ra = dq - cls[m].a, rb = ds - cls[m].b;
-                        if (floordiv(ra, s) * s != ra || floordiv(rb, s) * s != rb)
-                            continue;
-                        const int dQ = ra / s, dS = rb / s;
-                        const int slot = slot0[m] - (dS + floor_half(dQ)) * a.WC - dQ -
-                                         ((dQ & 1) ? peven[m] : 0);
-                        const bf16x8 b0 = *reinterpret_cast<const bf16x8 *>(wrow);
-                        const bf16x8 b1 = *reinterpret_cast<const bf16x8 *>(wrow + 32 * kCP);
-                        const bf16x8 b2 = *reinterpret_cast<const bf16x8 *>(wrow + 16);
-                        const bf16x8 b3 = *reinterpret_cast<const bf16x8 *>(wrow + 32 * kCP + 16);
-                        const bf16x8 x0 =
-                            *reinterpret_cast<const bf16x8 *>(win + slot * kCP + 8 * kh);
-                        const bf16x8 x1 =
-                            *reinterpret_cast<const bf16x8 *>(win + slot * kCP + 16 + 8 * kh);
-                        acc[m][0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(x0, b0, acc[m][0], 0, 0, 0);
-                        acc[m][1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(x0, b1, acc[m][1], 0, 0, 0);
-                        acc[m][0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(x1, b2, acc[m][0], 0, 0, 0);
-                        acc[m][1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(x1, b3, acc[m][1], 0, 0, 0);
-                    }
+                for (int m = 0; m < kMG; ++m) {
+                    if (m >= ng)
+                        break;
+                    // live iff (dq, ds) = (a, b) mod s (wave-uniform)
+                    const int ra = dq - cls[m].a, rb = ds - cls[m].b;
+                    if (floordiv(ra, s) * s != ra || floordiv(rb, s) * s != rb)
+                        continue;
+                    const int dQ = ra / s, dS = rb / s;
+                    const int slot = slot0[m] - (dS + floor_half(dQ)) * a.WC - dQ -
+                                     ((dQ & 1) ? peven[m] : 0);
+                    const bf16x8 b0 = *reinterpret_cast<const bf16x8 *>(wrow);
+                    const bf16x8 b1 = *reinterpret_cast<const bf16x8 *>(wrow + 32 * kCP);
+                    const bf16x8 b2 = *reinterpret_cast<const bf16x8 *>(wrow + 16);
+                    const bf16x8 b3 = *reinterpret_cast<const bf16x8 *>(wrow + 32 * kCP + 16);
+                    const bf16x8 x0 = *reinterpret_cast<const bf16x8 *>(win + slot * kCP + 8 * kh);
+                    const bf16x8 x1 =
+                        *reinterpret_cast<const bf16x8 *>(win + slot * kCP + 16 + 8 * kh);
+                    acc[m][0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(x0, b0, acc[m][0], 0, 0, 0);
+                    acc[m][1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(x0, b1, acc[m][1], 0, 0, 0);
+                    acc[m][0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(x1, b2, acc[m][0], 0, 0, 0);
+                    acc[m][1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(x1, b3, acc[m][1], 0, 0, 0);
                 }
             }
         }
@@ -505,28 +548,22 @@ size_t gen_lds(const GenArgs &a, int TG, bool alias, int M)
     return alias ? std::max(win, out) + wgt : win + wgt + out;
 }
 
-// The most taps per stage (of 8, 4, 2, 1) whose LDS fits `limit`.
-bool finish_plan(GenArgs &a, int T, int M, bool alias, size_t limit, size_t &lds)
+// LDS offsets of a plan (window, one stage of weights, output staging
+// aliasing the window when `alias`), if they fit `limit`.
+bool finish_plan(GenArgs &a, int M, bool alias, size_t limit, size_t &lds)
 {
-    {
-        for (int TG : {8, 4, 2, 1}) {
-            if (TG > T && TG > 1)
-                continue;
-            const size_t need = gen_lds(a, TG, alias, M);
-            if (need <= limit) {
-                a.TG = TG;
-                const size_t win = align256(sizeof(bf16raw) * static_cast<size_t>(a.WR) * a.WC * kCP);
-                const size_t out = align256(sizeof(bf16raw) * static_cast<size_t>(kNB) * out_pitch(M));
-                a.win_off = 0;
-                a.out_off = alias ? 0 : static_cast<int>(win);
-                a.wgt_off = static_cast<int>(alias ? std::max(win, out) : win + out);
-                a.OP = out_pitch(M);
-                lds = need;
-                return true;
-            }
-        }
-    }
-    return false;
+    const size_t need = gen_lds(a, kTG, alias, M);
+    if (need > limit)
+        return false;
+    const size_t win = align256(sizeof(bf16raw) * static_cast<size_t>(a.WR) * a.WC * kCP);
+    const size_t out = align256(sizeof(bf16raw) * static_cast<size_t>(kNB) * out_pitch(M));
+    a.TG = kTG;
+    a.win_off = 0;
+    a.out_off = alias ? 0 : static_cast<int>(win);
+    a.wgt_off = static_cast<int>(alias ? std::max(win, out) : win + out);
+    a.OP = out_pitch(M);
+    lds = need;
+    return true;
 }
 
 bool plan_fwd(const ConvShape &sh, GenArgs &a, size_t &lds)
@@ -553,7 +590,7 @@ bool plan_fwd(const ConvShape &sh, GenArgs &a, size_t &lds)
             a.TR = TR;
             a.WR = sh.s * (TR - 1) + (sh.s >> 1) + 2 * sh.k + 1;
             a.tiles = cdiv(sh.Ho, TR);
-            if (finish_plan(a, sh.T, TR * sh.Wo, true, limit, lds))
+            if (finish_plan(a, TR * sh.Wo, true, limit, lds))
                 return true;
         }
     }
@@ -602,7 +639,7 @@ bool plan_dgrad(const ConvShape &sh, GenArgs &a, size_t &lds, int &ngroups)
             a.tiles = sh.H / TR;
             ngroups = dg_groups(sh.s, sh.W, TR);
             const bool single = ngroups <= 4 * kMG;
-            if (finish_plan(a, sh.T, TR * sh.W, single, limit, lds))
+            if (finish_plan(a, TR * sh.W, single, limit, lds))
                 return true;
         }
     }
