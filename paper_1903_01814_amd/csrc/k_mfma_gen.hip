@@ -68,31 +68,37 @@ struct GenArgs {
     int OP;           // output staging pitch (bf16 per destination channel)
     int nblk;         // destination-channel blocks of 64
     int relu;
+    int CW;           // contraction channels held by the window (32, 64 or 128)
+    int SP;           // bf16 per window slot (CW + 8)
+    int resident;     // every stage's weights held in LDS for the block's life
+    int ntot;         // tiles in the batch (N * tiles)
 };
 
 __device__ __forceinline__ uint32_t lo16(uint32_t v) { return v & 0xffffu; }
 __device__ __forceinline__ uint32_t hi16(uint32_t v) { return v >> 16; }
 
-// Rows [g_r0, g_r0 + nrows) of a 32-channel chunk of one image (src points
-// at the chunk's first plane; planes HW apart, rows of Wsrc elements, Wsrc a
-// multiple of 8) into window rows 0 .. nrows-1: source column c goes to slot
-// column c + coff (if below WC), 8 channels per 16-byte vector.  Rows
-// outside [0, Hsrc) and the slot columns holding no source column are zero.
+// Rows [g_r0, g_r0 + nrows) of CW channels of one image (src points at the
+// first plane; planes HW apart, rows of Wsrc elements, Wsrc a multiple of 8)
+// into window rows 0 .. nrows-1: source column c goes to slot column c +
+// coff (if below WC), slots of SP bf16, 8 channels per 16-byte vector.
+// Rows outside [0, Hsrc) and the slot columns holding no source column are
+// zero.  Two items per thread per round, all their loads issued first.
 __device__ __forceinline__ void stage_window(bf16raw *__restrict__ win,
                                              const bf16raw *__restrict__ src, size_t HW,
                                              int Hsrc, int Wsrc, int g_r0, int nrows, int WC,
-                                             int coff)
+                                             int coff, int CW, int SP)
 {
-    constexpr int U = 2; // items per thread per round, all loads issued first
+    constexpr int U = 2;
+    const int ngl = __builtin_ctz(CW >> 3); // log2 of the 8-channel groups
     const int ncol8 = Wsrc >> 3;
-    const int items = nrows * ncol8 * 4;
+    const int items = (nrows * ncol8) << ngl;
     for (int it0 = threadIdx.x; it0 < items; it0 += U * kGThreads) {
         uint4 v[U][8];
         int slot0[U], ncopy[U], grp[U];
 #pragma unroll
         for (int h = 0; h < U; ++h) {
             const int it = it0 + h * kGThreads;
-            const int g = it & 3, rest = it >> 2;
+            const int g = it & ((1 << ngl) - 1), rest = it >> ngl;
             const int ch = rest % ncol8, rr = rest / ncol8;
             const int r = g_r0 + rr, col0 = 8 * ch;
             const bool live = it < items && col0 + coff < WC;
@@ -119,7 +125,7 @@ __device__ __forceinline__ void stage_window(bf16raw *__restrict__ win,
                     const uint32_t b = reinterpret_cast<const uint32_t *>(&v[h][2 * j + 1])[px >> 1];
                     q[j] = (px & 1) ? (hi16(a) | (b & 0xffff0000u)) : (lo16(a) | (b << 16));
                 }
-                *reinterpret_cast<uint4 *>(win + (slot0[h] + px) * kCP + 8 * grp[h]) =
+                *reinterpret_cast<uint4 *>(win + (slot0[h] + px) * SP + 8 * grp[h]) =
                     make_uint4(q[0], q[1], q[2], q[3]);
             }
         }
@@ -127,60 +133,70 @@ __device__ __forceinline__ void stage_window(bf16raw *__restrict__ win,
     // slot columns without a source column: [0, coff) and [Wsrc + coff, WC)
     const int right = max(0, WC - Wsrc - coff);
     const int side = coff + right;
-    const int zitems = nrows * side * 4;
+    const int zitems = (nrows * side) << ngl;
     for (int it = threadIdx.x; it < zitems; it += kGThreads) {
-        const int g = it & 3, rest = it >> 2;
+        const int g = it & ((1 << ngl) - 1), rest = it >> ngl;
         const int sc = rest % side, rr = rest / side;
         const int col = sc < coff ? sc : Wsrc + coff + (sc - coff);
-        *reinterpret_cast<uint4 *>(win + (rr * WC + col) * kCP + 8 * g) = make_uint4(0, 0, 0, 0);
+        *reinterpret_cast<uint4 *>(win + (rr * WC + col) * SP + 8 * g) = make_uint4(0, 0, 0, 0);
     }
 }
 
 // Weights of one stage -- taps [t0, t0 + kTG) of one 32-channel chunk of
-// the contraction, for the block's 64 destination channels -- as
-// wl[(tt * kNB + n) * kCP + kc]:
+// the contraction, for the block's 64 destination channels -- in LDS as
+// wl[tt * kTB + n * kCP + kc] (kTB = 64 rows of kCP plus a pad of 8, so the
+// tap blocks start on different banks):
 //   forward (DG = false): n = output channel d0 + n, kc = input channel c0 + kc,
 //     value w[d0 + n][c0 + kc][t0 + tt];
 //   data gradient (DG = true): n = input channel d0 + n, kc = output channel
 //     c0 + kc, value w[c0 + kc][d0 + n][t0 + tt].
 // Zero for destination channels past Cd and taps past T.  w is
-// [Cout][Cin][T]: the kTG taps of one (n, kc) are consecutive in memory, and
-// element e of the stage is (tt, kc, n) = (e % 8, (e / 8) % 32, e / 256), so
-// eight consecutive lanes read one 16-byte run.  load() issues all of a
-// thread's loads (into registers, while the previous stage computes);
-// store() writes them to LDS.
-constexpr int kTG = 8;                                // taps per stage
-constexpr int kWPer = kTG * kNB * kCK / kGThreads;    // elements per thread
+// [Cout][Cin][T].  Thread mapping: tap tt = tid % 8, channel octet kc0 =
+// 8 ((tid / 8) % 4), rows n = tid / 32 + 8 j (j < 8); a thread gathers the
+// eight channels kc0 .. kc0 + 7 of each of its rows (loads one stride apart:
+// T elements in the forward, C_in T in the data gradient), packs them into
+// 16 bytes and writes them with one LDS store.  Eight consecutive lanes read
+// eight consecutive taps, one 16-byte run.  load() issues every load of the
+// thread (while the previous stage computes); store() writes them.
+constexpr int kTG = 8;                      // taps per stage
+constexpr int kTB = kNB * kCP + 8;          // bf16 per tap block in LDS
 
 template <bool DG> struct WgtRegs {
-    bf16raw v[kWPer];
+    uint4 v[8]; // row j: channels kc0 .. kc0 + 7
 
     __device__ __forceinline__ void load(const bf16raw *__restrict__ w, int T, int Cs, int Cd,
                                          int d0, int c0, int t0)
     {
+        const int tt = threadIdx.x & 7, kc0 = 8 * ((threadIdx.x >> 3) & 3);
+        const int nb = threadIdx.x >> 5;
+        const bool tv = t0 + tt < T;
+        const int t = tv ? t0 + tt : T - 1;            // clamped: valid address, value dropped
+        const size_t cstride = DG ? static_cast<size_t>(Cd) * T : static_cast<size_t>(T);
 #pragma unroll
-        for (int u = 0; u < kWPer; ++u) {
-            const int e = threadIdx.x + u * kGThreads;
-            const int tt = e & 7, kc = (e >> 3) & 31, n = e >> 8;
-            const int d = d0 + n, t = t0 + tt;
-            bf16raw x = 0;
-            if (d < Cd && t < T) {
-                const size_t idx = DG ? (static_cast<size_t>(c0 + kc) * Cd + d) * T + t
-                                      : (static_cast<size_t>(d) * Cs + c0 + kc) * T + t;
-                x = w[idx];
+        for (int j = 0; j < 8; ++j) {
+            const int n = nb + 8 * j;
+            const bool nv = tv && d0 + n < Cd;
+            const int d = nv ? d0 + n : Cd - 1;
+            const bf16raw *p = DG ? w + (static_cast<size_t>(c0 + kc0) * Cd + d) * T + t
+                                  : w + (static_cast<size_t>(d) * Cs + c0 + kc0) * T + t;
+            uint32_t q[4];
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                const uint32_t lo = p[(2 * i) * cstride];
+                const uint32_t hi = p[(2 * i + 1) * cstride];
+                q[i] = nv ? (lo | (hi << 16)) : 0u;
             }
-            v[u] = x;
+            v[j] = make_uint4(q[0], q[1], q[2], q[3]);
         }
     }
 
     __device__ __forceinline__ void store(bf16raw *__restrict__ wl) const
     {
+        const int tt = threadIdx.x & 7, kc0 = 8 * ((threadIdx.x >> 3) & 3);
+        const int nb = threadIdx.x >> 5;
 #pragma unroll
-        for (int u = 0; u < kWPer; ++u) {
-            const int e = threadIdx.x + u * kGThreads;
-            const int tt = e & 7, kc = (e >> 3) & 31, n = e >> 8;
-            wl[(tt * kNB + n) * kCP + kc] = v[u];
-        }
+        for (int j = 0; j < 8; ++j)
+            *reinterpret_cast<uint4 *>(wl + tt * kTB + (nb + 8 * j) * kCP + kc0) = v[j];
     }
 };
 
@@ -191,13 +207,13 @@ __device__ __forceinline__ int fwd_tap_off(int dq, int ds, int WC)
     return (ds + floor_half(dq)) * WC + dq;
 }
 
-// Accumulate one K-step (16 channels at half h of the chunk) for the wave's
-// groups: A at slot adr[m] (+ the odd offset), B for both 32-channel halves
-// of the block.
+// Accumulate one K-step (16 channels at window channel cl + 16 h) for the
+// wave's groups: A at window slot slot[m], B for both 32-channel halves of
+// the block.
 template <int MG>
 __device__ __forceinline__ void kstep(floatx16 (&acc)[MG][2], const bf16raw *__restrict__ win,
                                       const bf16raw *__restrict__ wrow, const int (&slot)[MG],
-                                      int ng, int h, int kh)
+                                      int ng, int h, int kh, int SP, int cl)
 {
     const bf16x8 b0 = *reinterpret_cast<const bf16x8 *>(wrow + h * 16);
     const bf16x8 b1 = *reinterpret_cast<const bf16x8 *>(wrow + 32 * kCP + h * 16);
@@ -205,17 +221,39 @@ __device__ __forceinline__ void kstep(floatx16 (&acc)[MG][2], const bf16raw *__r
     for (int m = 0; m < MG; ++m) {
         if (m >= ng)
             break;
-        const bf16x8 a = *reinterpret_cast<const bf16x8 *>(win + slot[m] * kCP + h * 16 + 8 * kh);
+        const bf16x8 a =
+            *reinterpret_cast<const bf16x8 *>(win + slot[m] * SP + cl + h * 16 + 8 * kh);
         acc[m][0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b0, acc[m][0], 0, 0, 0);
         acc[m][1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b1, acc[m][1], 0, 0, 0);
     }
 }
 
+// Stage weights: every stage at once (resident, once per block) or one
+// stage into the single buffer.  Stage st = (chunk st / NTG, taps
+// (st % NTG) * kTG ..).
+constexpr int kStageElems = kTG * kTB; // bf16 per stage in LDS
+
+template <bool DG>
+__device__ __forceinline__ void stage_all_weights(bf16raw *__restrict__ wl,
+                                                  const bf16raw *__restrict__ w, int T, int NTG,
+                                                  int nst, int Cs, int Cd, int d0)
+{
+    for (int st = 0; st < nst; ++st) {
+        WgtRegs<DG> r;
+        r.load(w, T, Cs, Cd, d0, (st / NTG) * kCK, (st % NTG) * kTG);
+        r.store(wl + st * kStageElems);
+    }
+}
+
 // ---------------------------------------------------------------- forward
-// Block: tile (image n, output rows i0 .. i0 + rows - 1, all W_out columns)
-// x destination block db (output channels 64 db ..).  Pixel p of the tile
-// (row-major) is in group p / 32; wave w owns groups w, w + 4 (one round:
-// tiles hold at most 256 pixels).
+// Persistent blocks: block b keeps destination block db = b % nblk (output
+// channels 64 db ..) and walks the tiles b / nblk, + gridDim / nblk, ...; a
+// tile is (image n, output rows i0 .. i0 + rows - 1, all W_out columns).
+// Pixel p of the tile (row-major) is in group p / 32; wave w owns groups w,
+// w + 4 (tiles hold at most 256 pixels).  Per tile the stages run over
+// (32-channel chunk, 8 taps); the window holds CW channels and is staged
+// when a stage starts a new window's worth of channels; streamed weights of
+// the next stage (of this tile or the next) load during the current one.
 template <int K>
 __global__ __launch_bounds__(kGThreads) void conv_gen_fwd_k(const bf16raw *__restrict__ x,
                                                             const bf16raw *__restrict__ w,
@@ -224,6 +262,7 @@ __global__ __launch_bounds__(kGThreads) void conv_gen_fwd_k(const bf16raw *__res
 {
     constexpr int T = num_taps(K);
     constexpr TapTable<K> tab{};
+    constexpr int NTG = (T + kTG - 1) / kTG;
     extern __shared__ __align__(16) unsigned char smem[];
     bf16raw *win = reinterpret_cast<bf16raw *>(smem + a.win_off);
     bf16raw *wl = reinterpret_cast<bf16raw *>(smem + a.wgt_off);
@@ -231,123 +270,133 @@ __global__ __launch_bounds__(kGThreads) void conv_gen_fwd_k(const bf16raw *__res
 
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     const int n32 = lane & 31, kh = lane >> 5;
-    const int db = blockIdx.x % a.nblk, tb = blockIdx.x / a.nblk;
-    const int n = tb / a.tiles, i0 = (tb - n * a.tiles) * a.TR;
-    const int rows = min(a.TR, a.Hd - i0);
-    const int M = rows * a.Wd;
-    const int ngroups = (M + 31) >> 5;
+    const int db = blockIdx.x % a.nblk, tstep = gridDim.x / a.nblk;
     const int d0 = db * kNB;
     const int s = a.s;
-    const int r_lo = s * i0 - K; // window row 0
-
-    // this lane's pixel (A row) per group: window slot of its centre and the
-    // extra row of odd tap columns when the centre column is odd
-    int slot0[kMG], podd[kMG];
-    int ng = 0;
-#pragma unroll
-    for (int m = 0; m < kMG; ++m) {
-        const int g = wave + 4 * m;
-        if (g < ngroups)
-            ng = m + 1;
-        const int p = min(g * 32 + n32, M - 1); // clamped: valid, never stored
-        const int i = i0 + p / a.Wd, j = p % a.Wd;
-        const int rc = s * i + (j & 1) * (s >> 1), cc = s * j;
-        slot0[m] = (rc - r_lo) * a.WC + cc + a.coff;
-        podd[m] = (cc & 1) ? a.WC : 0;
-    }
-
-    floatx16 acc[kMG][2];
-#pragma unroll
-    for (int m = 0; m < kMG; ++m)
-        acc[m][0] = acc[m][1] = floatx16{};
-
-    const size_t HWs = static_cast<size_t>(a.Hs) * a.Ws;
-    // stages: (chunk c0, taps t0 .. t0 + 7); the next stage's weights are
-    // loaded into registers while the current stage computes
-    constexpr int NTG = (T + kTG - 1) / kTG;
     const int nst = (a.Cs / kCK) * NTG;
-    WgtRegs<false> wr;
-    wr.load(w, T, a.Cs, a.Cd, d0, 0, 0);
-    for (int st = 0; st < nst; ++st) {
-        const int c0 = (st / NTG) * kCK, t0 = (st % NTG) * kTG;
-        __syncthreads(); // the previous stage's readers are done
-        if (t0 == 0)
-            stage_window(win, x + (static_cast<size_t>(n) * a.Cs + c0) * HWs, HWs, a.Hs, a.Ws,
-                         r_lo, a.WR, a.WC, a.coff);
-        wr.store(wl);
-        __syncthreads();
-        if (st + 1 < nst)
-            wr.load(w, T, a.Cs, a.Cd, d0, ((st + 1) / NTG) * kCK, ((st + 1) % NTG) * kTG);
-        if (ng == 0)
-            continue;
-        const int ntap = min(kTG, T - t0);
-        for (int tt = 0; tt < ntap; ++tt) {
-            const int t = t0 + tt;
-            const int dq = tab.dq[t], ds = tab.ds[t];
-            const int off = fwd_tap_off(dq, ds, a.WC);
-            int slot[kMG];
-#pragma unroll
-            for (int m = 0; m < kMG; ++m)
-                slot[m] = slot0[m] + off + ((dq & 1) ? podd[m] : 0);
-            const bf16raw *wrow = wl + (tt * kNB + n32) * kCP + 8 * kh;
-            kstep<kMG>(acc, win, wrow, slot, ng, 0, kh);
-            kstep<kMG>(acc, win, wrow, slot, ng, 1, kh);
-        }
-    }
-
-    // epilogue: bias, ReLU, bf16 into LDS [channel][pixel], then whole rows
-    __syncthreads();
+    const size_t HWs = static_cast<size_t>(a.Hs) * a.Ws;
+    const size_t HWd = static_cast<size_t>(a.Hd) * a.Wd;
+    const int nd = min(kNB, a.Cd - d0);
     float bv[2];
 #pragma unroll
     for (int j = 0; j < 2; ++j) {
         const int d = d0 + j * 32 + n32;
         bv[j] = (bias != nullptr && d < a.Cd) ? to_f(bias[d]) : 0.f;
     }
+
+    WgtRegs<false> wr;
+    if (a.resident)
+        stage_all_weights<false>(wl, w, T, NTG, nst, a.Cs, a.Cd, d0);
+    else
+        wr.load(w, T, a.Cs, a.Cd, d0, 0, 0);
+
+    for (int tb = blockIdx.x / a.nblk; tb < a.ntot; tb += tstep) {
+        const int n = tb / a.tiles, i0 = (tb - n * a.tiles) * a.TR;
+        const int rows = min(a.TR, a.Hd - i0);
+        const int M = rows * a.Wd;
+        const int ngroups = (M + 31) >> 5;
+        const int r_lo = s * i0 - K; // window row 0
+
+        // this lane's pixel (A row) per group: window slot of its centre and
+        // the extra row of odd tap columns when the centre column is odd
+        int slot0[kMG], podd[kMG];
+        int ng = 0;
 #pragma unroll
-    for (int m = 0; m < kMG; ++m) {
-        if (m >= ng)
-            break;
-        const int g = wave + 4 * m;
+        for (int m = 0; m < kMG; ++m) {
+            const int g = wave + 4 * m;
+            if (g < ngroups)
+                ng = m + 1;
+            const int p = min(g * 32 + n32, M - 1); // clamped: valid, never stored
+            const int i = i0 + p / a.Wd, j = p % a.Wd;
+            const int rc = s * i + (j & 1) * (s >> 1), cc = s * j;
+            slot0[m] = (rc - r_lo) * a.WC + cc + a.coff;
+            podd[m] = (cc & 1) ? a.WC : 0;
+        }
+        floatx16 acc[kMG][2];
 #pragma unroll
-        for (int j = 0; j < 2; ++j) {
-            bf16raw *orow = outl + (j * 32 + n32) * a.OP + g * 32 + 4 * kh;
+        for (int m = 0; m < kMG; ++m)
+            acc[m][0] = acc[m][1] = floatx16{};
+
+        for (int st = 0; st < nst; ++st) {
+            const int c0 = (st / NTG) * kCK, t0 = (st % NTG) * kTG;
+            const int cw0 = c0 - c0 % a.CW; // first channel of the window
+            __syncthreads(); // the previous stage's (or tile's) readers are done
+            if (c0 == cw0 && t0 == 0)
+                stage_window(win, x + (static_cast<size_t>(n) * a.Cs + cw0) * HWs, HWs, a.Hs,
+                             a.Ws, r_lo, a.WR, a.WC, a.coff, a.CW, a.SP);
+            if (!a.resident)
+                wr.store(wl);
+            __syncthreads();
+            if (!a.resident && (st + 1 < nst || tb + tstep < a.ntot)) {
+                const int sn = st + 1 < nst ? st + 1 : 0; // next stage, maybe the next tile's
+                wr.load(w, T, a.Cs, a.Cd, d0, (sn / NTG) * kCK, (sn % NTG) * kTG);
+            }
+            if (ng == 0)
+                continue;
+            const bf16raw *wst = a.resident ? wl + st * kStageElems : wl;
+            const int ntap = min(kTG, T - t0);
+            for (int tt = 0; tt < ntap; ++tt) {
+                const int t = t0 + tt;
+                const int dq = tab.dq[t], ds = tab.ds[t];
+                const int off = fwd_tap_off(dq, ds, a.WC);
+                int slot[kMG];
 #pragma unroll
-            for (int q = 0; q < 4; ++q) {
-                float v[4];
-#pragma unroll
-                for (int r = 0; r < 4; ++r) {
-                    v[r] = acc[m][j][4 * q + r] + bv[j];
-                    if (a.relu)
-                        v[r] = fmaxf(v[r], 0.f);
-                }
-                bf16raw o[4];
-#pragma unroll
-                for (int r = 0; r < 4; ++r)
-                    o[r] = from_f<bf16raw>(v[r]);
-                // pixels g*32 + 8q + 4kh + 0..3 (the row is padded to 32-pixel groups)
-                *reinterpret_cast<uint2 *>(orow + 8 * q) =
-                    make_uint2(o[0] | (static_cast<uint32_t>(o[1]) << 16),
-                               o[2] | (static_cast<uint32_t>(o[3]) << 16));
+                for (int m = 0; m < kMG; ++m)
+                    slot[m] = slot0[m] + off + ((dq & 1) ? podd[m] : 0);
+                const bf16raw *wrow = wst + tt * kTB + n32 * kCP + 8 * kh;
+                kstep<kMG>(acc, win, wrow, slot, ng, 0, kh, a.SP, c0 - cw0);
+                kstep<kMG>(acc, win, wrow, slot, ng, 1, kh, a.SP, c0 - cw0);
             }
         }
-    }
-    __syncthreads();
-    const size_t HWd = static_cast<size_t>(a.Hd) * a.Wd;
-    const int nd = min(kNB, a.Cd - d0);
-    bf16raw *ybase = y + (static_cast<size_t>(n) * a.Cd + d0) * HWd + static_cast<size_t>(i0) * a.Wd;
-    if ((a.Wd & 7) == 0) { // then every row of the tile starts on 16 bytes
-        const int nv = M >> 3;
-        for (int e = threadIdx.x; e < nd * nv; e += kGThreads) {
-            const int d = e / nv, v = e - d * nv;
-            const bf16raw *src = outl + d * a.OP + 8 * v;
-            const uint2 lo = *reinterpret_cast<const uint2 *>(src);
-            const uint2 hi = *reinterpret_cast<const uint2 *>(src + 4);
-            *reinterpret_cast<uint4 *>(ybase + d * HWd + 8 * v) = make_uint4(lo.x, lo.y, hi.x, hi.y);
+
+        // epilogue: bias, ReLU, bf16 into LDS [channel][pixel], then whole rows
+        __syncthreads();
+#pragma unroll
+        for (int m = 0; m < kMG; ++m) {
+            if (m >= ng)
+                break;
+            const int g = wave + 4 * m;
+#pragma unroll
+            for (int j = 0; j < 2; ++j) {
+                bf16raw *orow = outl + (j * 32 + n32) * a.OP + g * 32 + 4 * kh;
+#pragma unroll
+                for (int q = 0; q < 4; ++q) {
+                    float v[4];
+#pragma unroll
+                    for (int r = 0; r < 4; ++r) {
+                        v[r] = acc[m][j][4 * q + r] + bv[j];
+                        if (a.relu)
+                            v[r] = fmaxf(v[r], 0.f);
+                    }
+                    bf16raw o[4];
+#pragma unroll
+                    for (int r = 0; r < 4; ++r)
+                        o[r] = from_f<bf16raw>(v[r]);
+                    // pixels g*32 + 8q + 4kh + 0..3 (rows padded to 32-pixel groups)
+                    *reinterpret_cast<uint2 *>(orow + 8 * q) =
+                        make_uint2(o[0] | (static_cast<uint32_t>(o[1]) << 16),
+                                   o[2] | (static_cast<uint32_t>(o[3]) << 16));
+                }
+            }
         }
-    } else {
-        for (int e = threadIdx.x; e < nd * M; e += kGThreads) {
-            const int d = e / M, p = e - d * M;
-            ybase[d * HWd + p] = outl[d * a.OP + p];
+        __syncthreads();
+        bf16raw *ybase =
+            y + (static_cast<size_t>(n) * a.Cd + d0) * HWd + static_cast<size_t>(i0) * a.Wd;
+        if ((a.Wd & 7) == 0) { // then every row of the tile starts on 16 bytes
+            const int nv = M >> 3;
+            for (int e = threadIdx.x; e < nd * nv; e += kGThreads) {
+                const int d = e / nv, v = e - d * nv;
+                const bf16raw *src = outl + d * a.OP + 8 * v;
+                const uint2 lo = *reinterpret_cast<const uint2 *>(src);
+                const uint2 hi = *reinterpret_cast<const uint2 *>(src + 4);
+                *reinterpret_cast<uint4 *>(ybase + d * HWd + 8 * v) =
+                    make_uint4(lo.x, lo.y, hi.x, hi.y);
+            }
+        } else {
+            for (int e = threadIdx.x; e < nd * M; e += kGThreads) {
+                const int d = e / M, p = e - d * M;
+                ybase[d * HWd + p] = outl[d * a.OP + p];
+            }
         }
     }
 }
@@ -392,10 +441,11 @@ template <int K>
 __global__ __launch_bounds__(kGThreads) void conv_gen_dgrad_k(const bf16raw *__restrict__ dy,
                                                               const bf16raw *__restrict__ w,
                                                               bf16raw *__restrict__ dx, GenArgs a,
-                                                              int ngroups_total, int i_lo_rel)
+                                                              int ngroups_total)
 {
     constexpr int T = num_taps(K);
     constexpr TapTable<K> tab{};
+    constexpr int NTG = (T + kTG - 1) / kTG;
     extern __shared__ __align__(16) unsigned char smem[];
     bf16raw *win = reinterpret_cast<bf16raw *>(smem + a.win_off);
     bf16raw *wl = reinterpret_cast<bf16raw *>(smem + a.wgt_off);
@@ -403,134 +453,145 @@ __global__ __launch_bounds__(kGThreads) void conv_gen_dgrad_k(const bf16raw *__r
 
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     const int n32 = lane & 31, kh = lane >> 5;
-    const int db = blockIdx.x % a.nblk, tb = blockIdx.x / a.nblk;
-    const int n = tb / a.tiles, r0 = (tb - n * a.tiles) * a.TR;
+    const int db = blockIdx.x % a.nblk, tstep = gridDim.x / a.nblk;
     const int d0 = db * kNB;
     const int s = a.s;
-    // window row 0 = output row i_lo: floor((r0 - K - s/2) / s)
-    const int i_lo = floordiv(r0 - K - (s >> 1), s);
-    (void)i_lo_rel;
+    const int nst = (a.Cs / kCK) * NTG;
     const size_t HWs = static_cast<size_t>(a.Hs) * a.Ws;
-    const int TRW = a.TR * a.Wd;
+    const size_t HWd = static_cast<size_t>(a.Hd) * a.Wd;
+    const int nd = min(kNB, a.Cd - d0);
     const int nrounds = (ngroups_total + 4 * kMG - 1) / (4 * kMG);
+    const bool alias = a.out_off == a.win_off; // single round only
+    const bool whole = a.CW == a.Cs;            // the window holds every channel
 
-    for (int rd = 0; rd < nrounds; ++rd) {
-        // this wave's groups in this round: one class each
-        DgClass cls[kMG];
-        int slot0[kMG], peven[kMG], e0[kMG];
-        int ng = 0;
-#pragma unroll
-        for (int m = 0; m < kMG; ++m) {
-            const int g = rd * 4 * kMG + wave + 4 * m;
-            cls[m] = dg_class_of_group(g, s, a.Wd, a.TR);
-            e0[m] = (g - cls[m].g0) * 32;
-            const bool live = g < ngroups_total;
-            if (live)
-                ng = m + 1;
-            int r = r0, c = 0;
-            if (live)
-                dg_pixel(cls[m], min(e0[m] + n32, cls[m].size - 1), s, r0, r, c);
-            // axial (q, sa) = (c, r - floor(c/2)); class residues (a, b):
-            // c_s = (c - a) / s, sa_s = (sa - b) / s (exact)
-            const int cs = (c - cls[m].a) / s;
-            const int sas = floordiv(r - floor_half(c) - cls[m].b, s);
-            // source output (i, j) of a live tap: j = c_s - dQ, i = sa_s - dS + floor(j/2)
-            slot0[m] = (sas + floor_half(cs) - i_lo) * a.WC + cs + a.coff;
-            peven[m] = (cs & 1) ? 0 : a.WC; // one row less for odd dQ at even c_s
-        }
-        floatx16 acc[kMG][2];
-#pragma unroll
-        for (int m = 0; m < kMG; ++m)
-            acc[m][0] = acc[m][1] = floatx16{};
-
-        constexpr int NTG = (T + kTG - 1) / kTG;
-        const int nst = (a.Cs / kCK) * NTG;
-        WgtRegs<true> wr;
+    WgtRegs<true> wr;
+    if (a.resident)
+        stage_all_weights<true>(wl, w, T, NTG, nst, a.Cs, a.Cd, d0);
+    else
         wr.load(w, T, a.Cs, a.Cd, d0, 0, 0);
-        for (int st = 0; st < nst; ++st) {
-            const int c0 = (st / NTG) * kCK, t0 = (st % NTG) * kTG;
-            __syncthreads();
-            if (t0 == 0)
-                stage_window(win, dy + (static_cast<size_t>(n) * a.Cs + c0) * HWs, HWs, a.Hs,
-                             a.Ws, i_lo, a.WR, a.WC, a.coff);
-            wr.store(wl);
-            __syncthreads();
-            if (st + 1 < nst)
-                wr.load(w, T, a.Cs, a.Cd, d0, ((st + 1) / NTG) * kCK, ((st + 1) % NTG) * kTG);
-            if (ng == 0)
-                continue;
-            const int ntap = min(kTG, T - t0);
-            for (int tt = 0; tt < ntap; ++tt) {
-                const int t = t0 + tt;
-                const int dq = tab.dq[t], ds = tab.ds[t];
-                const bf16raw *wrow = wl + (tt * kNB + n32) * kCP + 8 * kh;
+
+    for (int tb = blockIdx.x / a.nblk; tb < a.ntot; tb += tstep) {
+        const int n = tb / a.tiles, r0 = (tb - n * a.tiles) * a.TR;
+        // window row 0 = output row i_lo = floor((r0 - K - s/2) / s)
+        const int i_lo = floordiv(r0 - K - (s >> 1), s);
+
+        for (int rd = 0; rd < nrounds; ++rd) {
+            // this wave's groups in this round: one class each
+            DgClass cls[kMG];
+            int slot0[kMG], peven[kMG], pix[kMG];
+            int ng = 0;
 #pragma unroll
-                for (int m = 0; m < kMG; ++m) {
-                    if (m >= ng)
-                        break;
-                    // live iff (dq, ds) = (a, b) mod s (wave-uniform)
-                    const int ra = dq - cls[m].a, rb = ds - cls[m].b;
-                    if (floordiv(ra, s) * s != ra || floordiv(rb, s) * s != rb)
+            for (int m = 0; m < kMG; ++m) {
+                const int g = rd * 4 * kMG + wave + 4 * m;
+                cls[m] = dg_class_of_group(g, s, a.Wd, a.TR);
+                const int e0 = (g - cls[m].g0) * 32;
+                const bool live = g < ngroups_total;
+                if (live)
+                    ng = m + 1;
+                int r = r0, c = 0;
+                if (live)
+                    dg_pixel(cls[m], min(e0 + n32, cls[m].size - 1), s, r0, r, c);
+                // tile position of this lane's A row (-1 past the class's end)
+                pix[m] = (live && e0 + n32 < cls[m].size) ? (r - r0) * a.Wd + c : -1;
+                // axial (q, sa) = (c, r - floor(c/2)); class residues (a, b):
+                // c_s = (c - a) / s, sa_s = (sa - b) / s (exact)
+                const int cs = (c - cls[m].a) / s;
+                const int sas = floordiv(r - floor_half(c) - cls[m].b, s);
+                // source output (i, j) of a live tap: j = c_s - dQ, i = sa_s - dS + floor(j/2)
+                slot0[m] = (sas + floor_half(cs) - i_lo) * a.WC + cs + a.coff;
+                peven[m] = (cs & 1) ? 0 : a.WC; // one row less for odd dQ at even c_s
+            }
+            floatx16 acc[kMG][2];
+#pragma unroll
+            for (int m = 0; m < kMG; ++m)
+                acc[m][0] = acc[m][1] = floatx16{};
+
+            for (int st = 0; st < nst; ++st) {
+                const int c0 = (st / NTG) * kCK, t0 = (st % NTG) * kTG;
+                const int cw0 = c0 - c0 % a.CW;
+                __syncthreads();
+                if (c0 == cw0 && t0 == 0 && (!whole || rd == 0))
+                    stage_window(win, dy + (static_cast<size_t>(n) * a.Cs + cw0) * HWs, HWs,
+                                 a.Hs, a.Ws, i_lo, a.WR, a.WC, a.coff, a.CW, a.SP);
+                if (!a.resident)
+                    wr.store(wl);
+                __syncthreads();
+                if (!a.resident &&
+                    (st + 1 < nst || rd + 1 < nrounds || tb + tstep < a.ntot)) {
+                    const int sn = st + 1 < nst ? st + 1 : 0;
+                    wr.load(w, T, a.Cs, a.Cd, d0, (sn / NTG) * kCK, (sn % NTG) * kTG);
+                }
+                if (ng == 0)
+                    continue;
+                const bf16raw *wst = a.resident ? wl + st * kStageElems : wl;
+                const int ntap = min(kTG, T - t0);
+                const int cl = c0 - cw0;
+                for (int tt = 0; tt < ntap; ++tt) {
+                    const int t = t0 + tt;
+                    const int dq = tab.dq[t], ds = tab.ds[t];
+                    const bf16raw *wrow = wst + tt * kTB + n32 * kCP + 8 * kh;
+#pragma unroll
+                    for (int m = 0; m < kMG; ++m) {
+                        if (m >= ng)
+                            break;
+                        // live iff (dq, ds) = (a, b) mod s (wave-uniform)
+                        const int ra = dq - cls[m].a, rb = ds - cls[m].b;
+                        if (floordiv(ra, s) * s != ra || floordiv(rb, s) * s != rb)
+                            continue;
+                        const int dQ = ra / s, dS = rb / s;
+                        const int slot = slot0[m] - (dS + floor_half(dQ)) * a.WC - dQ -
+                                         ((dQ & 1) ? peven[m] : 0);
+                        const bf16x8 b0 = *reinterpret_cast<const bf16x8 *>(wrow);
+                        const bf16x8 b1 = *reinterpret_cast<const bf16x8 *>(wrow + 32 * kCP);
+                        const bf16x8 b2 = *reinterpret_cast<const bf16x8 *>(wrow + 16);
+                        const bf16x8 b3 = *reinterpret_cast<const bf16x8 *>(wrow + 32 * kCP + 16);
+                        const bf16raw *ap = win + slot * a.SP + cl + 8 * kh;
+                        const bf16x8 x0 = *reinterpret_cast<const bf16x8 *>(ap);
+                        const bf16x8 x1 = *reinterpret_cast<const bf16x8 *>(ap + 16);
+                        acc[m][0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(x0, b0, acc[m][0], 0, 0, 0);
+                        acc[m][1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(x0, b1, acc[m][1], 0, 0, 0);
+                        acc[m][0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(x1, b2, acc[m][0], 0, 0, 0);
+                        acc[m][1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(x1, b3, acc[m][1], 0, 0, 0);
+                    }
+                }
+            }
+            // this round's results into the LDS tile [channel][row-major pixel]
+            if (alias)
+                __syncthreads(); // the tile overlays the window (single round)
+#pragma unroll
+            for (int m = 0; m < kMG; ++m) {
+                if (m >= ng)
+                    break;
+#pragma unroll
+                for (int r = 0; r < 16; ++r) {
+                    // D row 8 (r / 4) + 4 kh + r % 4 is the A row of that lane
+                    const int p = __shfl(pix[m], 8 * (r >> 2) + 4 * kh + (r & 3), 64);
+                    if (p < 0)
                         continue;
-                    const int dQ = ra / s, dS = rb / s;
-                    const int slot = slot0[m] - (dS + floor_half(dQ)) * a.WC - dQ -
-                                     ((dQ & 1) ? peven[m] : 0);
-                    const bf16x8 b0 = *reinterpret_cast<const bf16x8 *>(wrow);
-                    const bf16x8 b1 = *reinterpret_cast<const bf16x8 *>(wrow + 32 * kCP);
-                    const bf16x8 b2 = *reinterpret_cast<const bf16x8 *>(wrow + 16);
-                    const bf16x8 b3 = *reinterpret_cast<const bf16x8 *>(wrow + 32 * kCP + 16);
-                    const bf16x8 x0 = *reinterpret_cast<const bf16x8 *>(win + slot * kCP + 8 * kh);
-                    const bf16x8 x1 =
-                        *reinterpret_cast<const bf16x8 *>(win + slot * kCP + 16 + 8 * kh);
-                    acc[m][0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(x0, b0, acc[m][0], 0, 0, 0);
-                    acc[m][1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(x0, b1, acc[m][1], 0, 0, 0);
-                    acc[m][0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(x1, b2, acc[m][0], 0, 0, 0);
-                    acc[m][1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(x1, b3, acc[m][1], 0, 0, 0);
+#pragma unroll
+                    for (int j = 0; j < 2; ++j)
+                        outl[(j * 32 + n32) * a.OP + p] = from_f<bf16raw>(acc[m][j][r]);
                 }
             }
         }
-        // this round's results into the LDS tile [channel][row-major pixel]
-        if (rd == 0 && a.out_off == a.win_off)
-            __syncthreads(); // the tile aliases the window (single round only)
-#pragma unroll
-        for (int m = 0; m < kMG; ++m) {
-            if (m >= ng)
-                break;
-#pragma unroll
-            for (int r = 0; r < 16; ++r) {
-                const int e = e0[m] + 8 * (r >> 2) + 4 * kh + (r & 3);
-                if (e >= cls[m].size)
-                    continue;
-                int pr = 0, pc = 0;
-                dg_pixel(cls[m], e, s, r0, pr, pc);
-                const int p = (pr - r0) * a.Wd + pc;
-#pragma unroll
-                for (int j = 0; j < 2; ++j)
-                    outl[(j * 32 + n32) * a.OP + p] = from_f<bf16raw>(acc[m][j][r]);
-            }
+        __syncthreads();
+        const int M = a.TR * a.Wd; // TR divides H: whole tiles
+        bf16raw *xbase =
+            dx + (static_cast<size_t>(n) * a.Cd + d0) * HWd + static_cast<size_t>(r0) * a.Wd;
+        const int nv = M >> 3; // W % 8 == 0
+        for (int e = threadIdx.x; e < nd * nv; e += kGThreads) {
+            const int d = e / nv, v = e - d * nv;
+            const bf16raw *src = outl + d * a.OP + 8 * v;
+            const uint2 lo = *reinterpret_cast<const uint2 *>(src);
+            const uint2 hi = *reinterpret_cast<const uint2 *>(src + 4);
+            *reinterpret_cast<uint4 *>(xbase + d * HWd + 8 * v) = make_uint4(lo.x, lo.y, hi.x, hi.y);
         }
-    }
-    __syncthreads();
-    const size_t HWd = static_cast<size_t>(a.Hd) * a.Wd;
-    const int nd = min(kNB, a.Cd - d0);
-    const int rows = min(a.TR, a.Hd - r0);
-    const int M = rows * a.Wd;
-    (void)TRW;
-    bf16raw *xbase = dx + (static_cast<size_t>(n) * a.Cd + d0) * HWd + static_cast<size_t>(r0) * a.Wd;
-    const int nv = M >> 3; // W % 8 == 0
-    for (int e = threadIdx.x; e < nd * nv; e += kGThreads) {
-        const int d = e / nv, v = e - d * nv;
-        const bf16raw *src = outl + d * a.OP + 8 * v;
-        const uint2 lo = *reinterpret_cast<const uint2 *>(src);
-        const uint2 hi = *reinterpret_cast<const uint2 *>(src + 4);
-        *reinterpret_cast<uint4 *>(xbase + d * HWd + 8 * v) = make_uint4(lo.x, lo.y, hi.x, hi.y);
     }
 }
 
 inline int cdiv(long a, long b) { return static_cast<int>((a + b - 1) / b); }
 
-constexpr size_t kGenLdsTwo = 80 * 1024;  // two blocks per CU
-constexpr size_t kGenLdsOne = 160 * 1024; // one block per CU
+constexpr size_t kGenLds = 160 * 1024; // one block per CU (registers allow no more)
 
 size_t align256(size_t v) { return (v + 255) & ~static_cast<size_t>(255); }
 
@@ -538,32 +599,46 @@ size_t align256(size_t v) { return (v + 255) & ~static_cast<size_t>(255); }
 // plus 4 (rows 8 mod 16 bytes apart for the 8-byte writes).
 int out_pitch(int M) { return ((M + 31) & ~31) + 4; }
 
-// LDS layout of a plan: window, weights (TG taps), output staging (aliasing
-// the window when `alias`).
-size_t gen_lds(const GenArgs &a, int TG, bool alias, int M)
+// LDS offsets of a plan -- window (WR x WC slots of SP bf16), output
+// staging (overlaying the window when `alias`), weights (every stage when
+// resident, else one) -- if they fit.
+bool finish_plan(GenArgs &a, int M, bool alias, int nst, size_t &lds)
 {
-    const size_t win = align256(sizeof(bf16raw) * static_cast<size_t>(a.WR) * a.WC * kCP);
-    const size_t wgt = align256(sizeof(bf16raw) * static_cast<size_t>(TG) * kNB * kCP);
+    const size_t win = align256(sizeof(bf16raw) * static_cast<size_t>(a.WR) * a.WC * a.SP);
     const size_t out = align256(sizeof(bf16raw) * static_cast<size_t>(kNB) * out_pitch(M));
-    return alias ? std::max(win, out) + wgt : win + wgt + out;
-}
-
-// LDS offsets of a plan (window, one stage of weights, output staging
-// aliasing the window when `alias`), if they fit `limit`.
-bool finish_plan(GenArgs &a, int M, bool alias, size_t limit, size_t &lds)
-{
-    const size_t need = gen_lds(a, kTG, alias, M);
-    if (need > limit)
+    const size_t wgt = sizeof(bf16raw) * static_cast<size_t>(a.resident ? nst : 1) * kStageElems;
+    const size_t base = alias ? std::max(win, out) : win + out;
+    if (base + wgt > kGenLds)
         return false;
-    const size_t win = align256(sizeof(bf16raw) * static_cast<size_t>(a.WR) * a.WC * kCP);
-    const size_t out = align256(sizeof(bf16raw) * static_cast<size_t>(kNB) * out_pitch(M));
     a.TG = kTG;
     a.win_off = 0;
     a.out_off = alias ? 0 : static_cast<int>(win);
-    a.wgt_off = static_cast<int>(alias ? std::max(win, out) : win + out);
+    a.wgt_off = static_cast<int>(base);
     a.OP = out_pitch(M);
-    lds = need;
+    lds = base + wgt;
     return true;
+}
+
+// Window channel counts to try, widest first: divisors of Cs among 128, 64, 32.
+int window_channels(int Cs, int idx)
+{
+    static const int cand[3] = {128, 64, 32};
+    int found = 0;
+    for (int c : cand)
+        if (c <= Cs && Cs % c == 0) {
+            if (found == idx)
+                return c;
+            ++found;
+        }
+    return 0;
+}
+
+// Persistent grid: as many blocks per destination block as CUs, at most one
+// per tile.
+int persistent_blocks(const GenArgs &a)
+{
+    const int per_db = std::max(1, std::min(a.ntot, device_cus() / std::max(1, a.nblk)));
+    return per_db * a.nblk;
 }
 
 bool plan_fwd(const ConvShape &sh, GenArgs &a, size_t &lds)
@@ -583,15 +658,22 @@ bool plan_fwd(const ConvShape &sh, GenArgs &a, size_t &lds)
     a.coff = sh.k;
     a.WC = sh.s * (sh.Wo - 1) + 2 * sh.k + 1;
     a.nblk = cdiv(sh.Co, kNB);
-    // the tallest tile of at most 256 pixels whose plan keeps two blocks per
-    // CU, else one block per CU
-    for (size_t limit : {kGenLdsTwo, kGenLdsOne}) {
-        for (int TR = std::max(1, std::min(sh.Ho, 256 / sh.Wo)); TR >= 1; --TR) {
-            a.TR = TR;
-            a.WR = sh.s * (TR - 1) + (sh.s >> 1) + 2 * sh.k + 1;
-            a.tiles = cdiv(sh.Ho, TR);
-            if (finish_plan(a, TR * sh.Wo, true, limit, lds))
-                return true;
+    const int nst = (sh.Ci / kCK) * cdiv(sh.T, kTG);
+    // the tallest tile of at most 256 pixels, then the widest window, then
+    // resident weights
+    for (int TR = std::max(1, std::min(sh.Ho, 256 / sh.Wo)); TR >= 1; --TR) {
+        a.TR = TR;
+        a.WR = sh.s * (TR - 1) + (sh.s >> 1) + 2 * sh.k + 1;
+        a.tiles = cdiv(sh.Ho, TR);
+        a.ntot = sh.N * a.tiles;
+        for (int ci = 0; window_channels(sh.Ci, ci) > 0; ++ci) {
+            a.CW = window_channels(sh.Ci, ci);
+            a.SP = a.CW + 8;
+            for (int res = 1; res >= 0; --res) {
+                a.resident = res;
+                if (finish_plan(a, TR * sh.Wo, true, nst, lds))
+                    return true;
+            }
         }
     }
     return false;
@@ -626,21 +708,28 @@ bool plan_dgrad(const ConvShape &sh, GenArgs &a, size_t &lds, int &ngroups)
     a.coff = sh.k;
     a.WC = sh.Wo + 2 * sh.k;
     a.nblk = cdiv(sh.Ci, kNB);
+    const int nst = (sh.Co / kCK) * cdiv(sh.T, kTG);
     // tiles of TR input rows, a multiple of s dividing H, at most 256 pixels
-    // where possible; two blocks per CU where possible
-    for (size_t limit : {kGenLdsTwo, kGenLdsOne}) {
-        for (int TR = sh.s * std::max(1, 256 / (sh.s * sh.W)); TR >= sh.s; TR -= sh.s) {
-            if (sh.H % TR != 0)
-                continue;
-            a.TR = TR;
-            const int i_lo = -((sh.k + (sh.s >> 1) + sh.s - 1) / sh.s); // floor((-k - s/2) / s)
-            const int i_hi = (TR - 1 + sh.k) / sh.s;                     // floor((TR - 1 + k) / s)
-            a.WR = i_hi - i_lo + 1;
-            a.tiles = sh.H / TR;
-            ngroups = dg_groups(sh.s, sh.W, TR);
-            const bool single = ngroups <= 4 * kMG;
-            if (finish_plan(a, TR * sh.W, single, limit, lds))
-                return true;
+    // where possible; then the widest window, then resident weights
+    for (int TR = sh.s * std::max(1, 256 / (sh.s * sh.W)); TR >= sh.s; TR -= sh.s) {
+        if (sh.H % TR != 0)
+            continue;
+        a.TR = TR;
+        const int i_lo = -((sh.k + (sh.s >> 1) + sh.s - 1) / sh.s); // floor((-k - s/2) / s)
+        const int i_hi = (TR - 1 + sh.k) / sh.s;                     // floor((TR - 1 + k) / s)
+        a.WR = i_hi - i_lo + 1;
+        a.tiles = sh.H / TR;
+        a.ntot = sh.N * a.tiles;
+        ngroups = dg_groups(sh.s, sh.W, TR);
+        const bool single = ngroups <= 4 * kMG;
+        for (int ci = 0; window_channels(sh.Co, ci) > 0; ++ci) {
+            a.CW = window_channels(sh.Co, ci);
+            a.SP = a.CW + 8;
+            for (int res = 1; res >= 0; --res) {
+                a.resident = res;
+                if (finish_plan(a, TR * sh.W, single, nst, lds))
+                    return true;
+            }
         }
     }
     return false;
@@ -671,7 +760,7 @@ hipError_t bf16_gen_fwd(const void *x, const void *w, const void *bias, void *y,
     if (!plan_fwd(sh, a, lds))
         return hipErrorInvalidConfiguration;
     a.relu = relu ? 1 : 0;
-    dim3 grid(a.N * a.tiles * a.nblk);
+    dim3 grid(persistent_blocks(a));
 #define HEX_GF(KV)                                                                           \
     HEX_LAUNCH((conv_gen_fwd_k<KV>), grid, dim3(kGThreads), lds, st,                        \
                static_cast<const bf16raw *>(x), static_cast<const bf16raw *>(w),             \
@@ -694,11 +783,11 @@ hipError_t bf16_gen_dgrad(const void *dy, const void *w, void *dx, const ConvSha
     int ngroups = 0;
     if (!plan_dgrad(sh, a, lds, ngroups))
         return hipErrorInvalidConfiguration;
-    dim3 grid(a.N * a.tiles * a.nblk);
+    dim3 grid(persistent_blocks(a));
 #define HEX_GD(KV)                                                                           \
     HEX_LAUNCH((conv_gen_dgrad_k<KV>), grid, dim3(kGThreads), lds, st,                      \
                static_cast<const bf16raw *>(dy), static_cast<const bf16raw *>(w),            \
-               static_cast<bf16raw *>(dx), a, ngroups, 0)
+               static_cast<bf16raw *>(dx), a, ngroups)
     if (sh.k == 1)
         HEX_GD(1);
     else if (sh.k == 2)
