@@ -60,7 +60,10 @@ struct GenArgs {
     int TR;           // destination rows per tile
     int tiles;        // tiles per image
     int WR, WC;       // window rows and slots per row
-    int coff;         // slot column of source column 0
+    int coff;         // window column of source column 0
+    int split;        // window columns stored by residue mod split (the forward's stride)
+    int WCs;          // slots per residue class; a window row holds RP = split * WCs slots
+    int RP;
     int TG;           // taps per weight stage (kTG)
     int win_off;      // byte offsets in LDS: window, weights, output staging
     int wgt_off;
@@ -86,7 +89,8 @@ __device__ __forceinline__ uint32_t hi16(uint32_t v) { return v >> 16; }
 __device__ __forceinline__ void stage_window(bf16raw *__restrict__ win,
                                              const bf16raw *__restrict__ src, size_t HW,
                                              int Hsrc, int Wsrc, int g_r0, int nrows, int WC,
-                                             int coff, int CW, int SP)
+                                             int coff, int CW, int SP, int split, int WCs,
+                                             int RP)
 {
     constexpr int U = 2;
     const int ngl = __builtin_ctz(CW >> 3); // log2 of the 8-channel groups
@@ -108,16 +112,24 @@ __device__ __forceinline__ void stage_window(bf16raw *__restrict__ win,
                 v[h][e] = rin ? *reinterpret_cast<const uint4 *>(src + (8 * g + e) * HW +
                                                                  static_cast<size_t>(r) * Wsrc + col0)
                               : make_uint4(0, 0, 0, 0);
-            slot0[h] = rr * WC + col0 + coff;
+            slot0[h] = rr * RP;                // + column map of col0 + coff + px
             ncopy[h] = live ? min(8, WC - col0 - coff) : 0;
-            grp[h] = g;
+            grp[h] = (col0 + coff) | (g << 20); // window column of px 0, channel group
         }
 #pragma unroll
         for (int h = 0; h < U; ++h) {
+            const int g = grp[h] >> 20, c0w = grp[h] & 0xfffff;
+            // window column c lives at slot column (c % split) WCs + c / split
+            int cq = c0w / split, cr = c0w - (c0w / split) * split;
 #pragma unroll
             for (int px = 0; px < 8; ++px) {
                 if (px >= ncopy[h])
                     break;
+                const int scol = cr * WCs + cq;
+                if (++cr == split) {
+                    cr = 0;
+                    ++cq;
+                }
                 uint32_t q[4];
 #pragma unroll
                 for (int j = 0; j < 4; ++j) {
@@ -125,7 +137,7 @@ __device__ __forceinline__ void stage_window(bf16raw *__restrict__ win,
                     const uint32_t b = reinterpret_cast<const uint32_t *>(&v[h][2 * j + 1])[px >> 1];
                     q[j] = (px & 1) ? (hi16(a) | (b & 0xffff0000u)) : (lo16(a) | (b << 16));
                 }
-                *reinterpret_cast<uint4 *>(win + (slot0[h] + px) * SP + 8 * grp[h]) =
+                *reinterpret_cast<uint4 *>(win + (slot0[h] + scol) * SP + 8 * g) =
                     make_uint4(q[0], q[1], q[2], q[3]);
             }
         }
@@ -138,7 +150,8 @@ __device__ __forceinline__ void stage_window(bf16raw *__restrict__ win,
         const int g = it & ((1 << ngl) - 1), rest = it >> ngl;
         const int sc = rest % side, rr = rest / side;
         const int col = sc < coff ? sc : Wsrc + coff + (sc - coff);
-        *reinterpret_cast<uint4 *>(win + (rr * WC + col) * SP + 8 * g) = make_uint4(0, 0, 0, 0);
+        const int scol = (col % split) * WCs + col / split;
+        *reinterpret_cast<uint4 *>(win + (rr * RP + scol) * SP + 8 * g) = make_uint4(0, 0, 0, 0);
     }
 }
 
@@ -206,6 +219,10 @@ __device__ __forceinline__ int fwd_tap_off(int dq, int ds, int WC)
 {
     return (ds + floor_half(dq)) * WC + dq;
 }
+
+// Slot column offset of window column c (>= 0) in a window split by column
+// residue mod s: (c % s) WCs + c / s.
+__device__ __forceinline__ int tap_col(int c, int s, int WCs) { return (c % s) * WCs + c / s; }
 
 // Accumulate one K-step (16 channels at window channel cl + 16 h) for the
 // wave's groups: A at window slot slot[m], B for both 32-channel halves of
@@ -309,8 +326,10 @@ __global__ __launch_bounds__(kGThreads) void conv_gen_fwd_k(const bf16raw *__res
             const int p = min(g * 32 + n32, M - 1); // clamped: valid, never stored
             const int i = i0 + p / a.Wd, j = p % a.Wd;
             const int rc = s * i + (j & 1) * (s >> 1), cc = s * j;
-            slot0[m] = (rc - r_lo) * a.WC + cc + a.coff;
-            podd[m] = (cc & 1) ? a.WC : 0;
+            // window column cc + coff + dq = s j + coff + dq sits at slot
+            // column j + tap_col(dq) (the window is split by column mod s)
+            slot0[m] = (rc - r_lo) * a.RP + j;
+            podd[m] = (cc & 1) ? a.RP : 0;
         }
         floatx16 acc[kMG][2];
 #pragma unroll
@@ -323,7 +342,7 @@ __global__ __launch_bounds__(kGThreads) void conv_gen_fwd_k(const bf16raw *__res
             __syncthreads(); // the previous stage's (or tile's) readers are done
             if (c0 == cw0 && t0 == 0)
                 stage_window(win, x + (static_cast<size_t>(n) * a.Cs + cw0) * HWs, HWs, a.Hs,
-                             a.Ws, r_lo, a.WR, a.WC, a.coff, a.CW, a.SP);
+                             a.Ws, r_lo, a.WR, a.WC, a.coff, a.CW, a.SP, a.split, a.WCs, a.RP);
             if (!a.resident)
                 wr.store(wl);
             __syncthreads();
@@ -338,7 +357,7 @@ __global__ __launch_bounds__(kGThreads) void conv_gen_fwd_k(const bf16raw *__res
             for (int tt = 0; tt < ntap; ++tt) {
                 const int t = t0 + tt;
                 const int dq = tab.dq[t], ds = tab.ds[t];
-                const int off = fwd_tap_off(dq, ds, a.WC);
+                const int off = fwd_tap_off(dq, ds, a.RP) - dq + tap_col(dq + a.coff, s, a.WCs);
                 int slot[kMG];
 #pragma unroll
                 for (int m = 0; m < kMG; ++m)
@@ -413,6 +432,22 @@ struct DgClass {
     int a, b, nv, size, g0; // residues, columns, elements, first group
 };
 
+// v mod s and v / s for the small offsets of a tap against a class residue
+// (|v| < 2 s + 4): a few subtractions instead of a division
+__device__ __forceinline__ void small_divmod(int v, int s, int &q, int &r)
+{
+    q = 0;
+    while (v < 0) {
+        v += s;
+        --q;
+    }
+    while (v >= s) {
+        v -= s;
+        ++q;
+    }
+    r = v;
+}
+
 __device__ __forceinline__ DgClass dg_class_of_group(int g, int s, int W, int TR)
 {
     int g0 = 0;
@@ -484,6 +519,12 @@ __global__ __launch_bounds__(kGThreads) void conv_gen_dgrad_k(const bf16raw *__r
             for (int m = 0; m < kMG; ++m) {
                 const int g = rd * 4 * kMG + wave + 4 * m;
                 cls[m] = dg_class_of_group(g, s, a.Wd, a.TR);
+                // the class is the wave's: keep it in scalar registers
+                cls[m].a = __builtin_amdgcn_readfirstlane(cls[m].a);
+                cls[m].b = __builtin_amdgcn_readfirstlane(cls[m].b);
+                cls[m].nv = __builtin_amdgcn_readfirstlane(cls[m].nv);
+                cls[m].size = __builtin_amdgcn_readfirstlane(cls[m].size);
+                cls[m].g0 = __builtin_amdgcn_readfirstlane(cls[m].g0);
                 const int e0 = (g - cls[m].g0) * 32;
                 const bool live = g < ngroups_total;
                 if (live)
@@ -498,8 +539,8 @@ __global__ __launch_bounds__(kGThreads) void conv_gen_dgrad_k(const bf16raw *__r
                 const int cs = (c - cls[m].a) / s;
                 const int sas = floordiv(r - floor_half(c) - cls[m].b, s);
                 // source output (i, j) of a live tap: j = c_s - dQ, i = sa_s - dS + floor(j/2)
-                slot0[m] = (sas + floor_half(cs) - i_lo) * a.WC + cs + a.coff;
-                peven[m] = (cs & 1) ? 0 : a.WC; // one row less for odd dQ at even c_s
+                slot0[m] = (sas + floor_half(cs) - i_lo) * a.RP + cs + a.coff;
+                peven[m] = (cs & 1) ? 0 : a.RP; // one row less for odd dQ at even c_s
             }
             floatx16 acc[kMG][2];
 #pragma unroll
@@ -512,7 +553,8 @@ __global__ __launch_bounds__(kGThreads) void conv_gen_dgrad_k(const bf16raw *__r
                 __syncthreads();
                 if (c0 == cw0 && t0 == 0 && (!whole || rd == 0))
                     stage_window(win, dy + (static_cast<size_t>(n) * a.Cs + cw0) * HWs, HWs,
-                                 a.Hs, a.Ws, i_lo, a.WR, a.WC, a.coff, a.CW, a.SP);
+                                 a.Hs, a.Ws, i_lo, a.WR, a.WC, a.coff, a.CW, a.SP, a.split,
+                                 a.WCs, a.RP);
                 if (!a.resident)
                     wr.store(wl);
                 __syncthreads();
@@ -535,11 +577,12 @@ __global__ __launch_bounds__(kGThreads) void conv_gen_dgrad_k(const bf16raw *__r
                         if (m >= ng)
                             break;
                         // live iff (dq, ds) = (a, b) mod s (wave-uniform)
-                        const int ra = dq - cls[m].a, rb = ds - cls[m].b;
-                        if (floordiv(ra, s) * s != ra || floordiv(rb, s) * s != rb)
+                        int dQ, dS, rq, rs;
+                        small_divmod(dq - cls[m].a, s, dQ, rq);
+                        small_divmod(ds - cls[m].b, s, dS, rs);
+                        if (rq != 0 || rs != 0)
                             continue;
-                        const int dQ = ra / s, dS = rb / s;
-                        const int slot = slot0[m] - (dS + floor_half(dQ)) * a.WC - dQ -
+                        const int slot = slot0[m] - (dS + floor_half(dQ)) * a.RP - dQ -
                                          ((dQ & 1) ? peven[m] : 0);
                         const bf16x8 b0 = *reinterpret_cast<const bf16x8 *>(wrow);
                         const bf16x8 b1 = *reinterpret_cast<const bf16x8 *>(wrow + 32 * kCP);
@@ -604,7 +647,7 @@ int out_pitch(int M) { return ((M + 31) & ~31) + 4; }
 // resident, else one) -- if they fit.
 bool finish_plan(GenArgs &a, int M, bool alias, int nst, size_t &lds)
 {
-    const size_t win = align256(sizeof(bf16raw) * static_cast<size_t>(a.WR) * a.WC * a.SP);
+    const size_t win = align256(sizeof(bf16raw) * static_cast<size_t>(a.WR) * a.RP * a.SP);
     const size_t out = align256(sizeof(bf16raw) * static_cast<size_t>(kNB) * out_pitch(M));
     const size_t wgt = sizeof(bf16raw) * static_cast<size_t>(a.resident ? nst : 1) * kStageElems;
     const size_t base = alias ? std::max(win, out) : win + out;
@@ -657,6 +700,9 @@ bool plan_fwd(const ConvShape &sh, GenArgs &a, size_t &lds)
     a.s = sh.s;
     a.coff = sh.k;
     a.WC = sh.s * (sh.Wo - 1) + 2 * sh.k + 1;
+    a.split = sh.s;
+    a.WCs = cdiv(a.WC, sh.s);
+    a.RP = a.split * a.WCs;
     a.nblk = cdiv(sh.Co, kNB);
     const int nst = (sh.Ci / kCK) * cdiv(sh.T, kTG);
     // the tallest tile of at most 256 pixels, then the widest window, then
@@ -707,6 +753,9 @@ bool plan_dgrad(const ConvShape &sh, GenArgs &a, size_t &lds, int &ngroups)
     a.s = sh.s;
     a.coff = sh.k;
     a.WC = sh.Wo + 2 * sh.k;
+    a.split = 1;
+    a.WCs = a.WC;
+    a.RP = a.WC;
     a.nblk = cdiv(sh.Ci, kNB);
     const int nst = (sh.Co / kCK) * cdiv(sh.T, kTG);
     // tiles of TR input rows, a multiple of s dividing H, at most 256 pixels
