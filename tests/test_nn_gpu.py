@@ -216,3 +216,60 @@ def test_sequential_stack(dt):
     G1 = from_dev(a1.grad) * (A1 > 0)
     _check_conv_grads(x, w1, b1, G1, 2, 1, dt, xd.grad, c1.weight.grad, c1.bias.grad,
                       "stack conv1")
+
+
+@pytest.mark.parametrize("dt", ["f32", "bf16"])
+@pytest.mark.parametrize("case", [
+    # N, C_in, C_out, D, H, W, k, kz, s, sz, bias, relu
+    (2, 1, 4, 5, 11, 12, 1, 1, 1, 1, True, False),
+    (1, 3, 5, 6, 9, 10, 2, 1, 2, 2, True, True),
+    (2, 2, 3, 4, 8, 8, 1, 2, 1, 3, False, True),
+])
+def test_hexconv3d_autograd(case, dt):
+    """HexConv3d forward and every gradient against the 3-D oracle."""
+    torch = torch_mod()
+    hn = pytest.importorskip("paper_1903_01814_amd.nn")
+    N, Ci, Co, D, H, W, k, kz, s, sz, bias, relu = case
+    rng = np.random.default_rng(sum(case[:10]))
+    T = oracle.num_taps(k)
+    x = _draw(rng, (N, Ci, D, H, W), dt)
+    layer = hn.HexConv3d(Ci, Co, (k, kz), (s, sz), bias=bias, relu=relu,
+                         device="cuda:0", dtype=torch.float32 if dt == "f32" else torch.bfloat16)
+    w = from_dev(layer.weight)
+    b = from_dev(layer.bias) if bias else None
+    xt = _leaf(x, dt)
+    y = layer(xt)
+    ref = oracle.conv3d_fwd(x, w, b, k, kz, s, sz)
+    mag = oracle.conv3d_fwd(np.abs(x), np.abs(w), None if b is None else np.abs(b), k, kz, s, sz)
+    if relu:
+        ref = np.maximum(ref, 0.0)
+    check(dt, from_dev(y), ref, mag, "3d fwd")
+    g = _draw(rng, y.shape, dt)
+    y.backward(to_dev(g, dt))
+    gm = np.where(from_dev(y) > 0, g, 0.0) if relu else g
+    check(dt, from_dev(xt.grad), oracle.conv3d_bwd_data(gm, w, k, kz, s, sz, D, H, W),
+          oracle.conv3d_bwd_data(np.abs(gm), np.abs(w), k, kz, s, sz, D, H, W), "3d dx")
+    rw, rb = oracle.conv3d_bwd_weight(x, gm, k, kz, s, sz)
+    mw, mb = oracle.conv3d_bwd_weight(np.abs(x), np.abs(gm), k, kz, s, sz)
+    check(dt, from_dev(layer.weight.grad), rw, mw, "3d dw")
+    if bias:
+        check(dt, from_dev(layer.bias.grad), rb, mb, "3d db")
+
+
+@pytest.mark.parametrize("mode", ["max", "avg"])
+def test_hexpool3d_autograd(mode):
+    torch = torch_mod()
+    hn = pytest.importorskip("paper_1903_01814_amd.nn")
+    rng = np.random.default_rng(3 + (mode == "max"))
+    N, C, D, H, W, k, kz, s, sz = 2, 3, 6, 10, 12, 1, 1, 2, 2
+    x = _draw(rng, (N, C, D, H, W), "f32")
+    pool = (hn.HexMaxPool3d if mode == "max" else hn.HexAvgPool3d)((k, kz), (s, sz))
+    xt = _leaf(x, "f32")
+    y = pool(xt)
+    m = oracle.POOL_MAX if mode == "max" else oracle.POOL_AVG
+    ref, am = oracle.pool3d_fwd(x, k, kz, s, sz, m)
+    check("f32", from_dev(y), ref, None, "pool3d fwd")
+    g = _draw(rng, y.shape, "f32")
+    y.backward(to_dev(g, "f32"))
+    rdx = oracle.pool3d_bwd(g, am if mode == "max" else None, None, k, kz, s, sz, m, D, H, W)
+    check("f32", from_dev(xt.grad), rdx, None, "pool3d dx")
