@@ -289,6 +289,31 @@ def test_wide_runs_across_images(ci, co, k):
     check_bwd_full(x, w, dy, k, 1, "bf16", what="bwd")
 
 
+@pytest.mark.parametrize("N,ci,co,H,W,relu", [
+    (3, 32, 48, 9, 96, True),     # 32 channels in, 48 out, rows of 96 pixels
+    (300, 32, 32, 3, 72, False),  # more runs than blocks: blocks walk two runs
+    (5, 64, 16, 130, 120, True),  # runs of 3 rows, the last run a single row
+    (128, 64, 64, 4, 128, False), # runs of 2 rows
+    (2, 64, 64, 37, 128, False),  # one image split into many runs
+])
+def test_wide_pipelined_rows(N, ci, co, H, W, relu):
+    """bf16 matrix-core convolution with one-row tiles and split roles (k = 1,
+    32 or 64 channels in, at most 64 out, rows of 64 < W <= 128 pixels):
+    ring window of four rows, rows staged two tiles ahead, results stored
+    one tile behind; runs of several rows per block, runs that end after one
+    or two rows, blocks that take several runs; every output compared, and
+    the data gradient where the output channels qualify as its input."""
+    rng = np.random.default_rng(7 * N + ci + co + H + W)
+    k = 1
+    T = oracle.num_taps(k)
+    x = gen.round_to(rng.normal(size=(N, ci, H, W)), "bf16")
+    w = gen.round_to(rng.normal(size=(co, ci, T)) / np.sqrt(ci * T), "bf16")
+    b = gen.round_to(rng.normal(size=co) * 0.1, "bf16")
+    check_fwd_full(x, w, b, k, 1, "bf16", relu=relu, what="fwd")
+    dy = gen.round_to(rng.normal(size=(N, co, H, W)), "bf16")
+    check_bwd_full(x, w, dy, k, 1, "bf16", what="bwd")
+
+
 @pytest.mark.parametrize("N,ci,co,H,k", [(10, 64, 64, 91, 1), (20, 32, 32, 57, 2)])
 def test_wgrad32_regular_runs(N, ci, co, H, k):
     """bf16 matrix-core weight gradient with regular staging (rows of 128
