@@ -570,6 +570,12 @@ int hexconv3d_fwd(const void *x, const void *w, const void *bias, void *y, int N
         return rc;
     if (sh.Ho == 0)
         return HEX_OK;
+    // few input channels: the small-channel forward with the 2kz + 1 planes
+    // around each output plane staged as extra input channels
+    if (!force_generic() && hexk::smallc_fwd_ok(sh))
+        return launched(hexk::smallc_fwd(x, w, bias, y, sh, static_cast<Dtype>(dt),
+                                         (flags & HEX_FLAG_RELU) != 0,
+                                         static_cast<hipStream_t>(stream)));
     if (!hexk::conv_fwd_generic_ok(sh))
         return HEX_ERR_UNSUPPORTED;
     return launched(hexk::conv_fwd_generic(x, w, bias, y, sh, static_cast<Dtype>(dt),

@@ -209,8 +209,13 @@ __global__ __launch_bounds__(kThreads) void bwd_smallc_k(
         const int n = t / tpi;
         b.load(map, x, dy, sh, n, (t - n * tpi) * kTR);
     };
+    // issued in this order (the scheduler may not swap them): the steady
+    // state has the older buffer's loads first as well, so the waits before
+    // a commit are the same on the loop's entry and back edge
     load_tile(sa, t_begin);
+    __builtin_amdgcn_sched_barrier(0);
     load_tile(sb, t_begin + 1);
+    __builtin_amdgcn_sched_barrier(0);
 
     // ---- data gradient role: thread = (channel group g, column c), all TR
     // rows of the column, CG output channels
@@ -403,14 +408,16 @@ __global__ __launch_bounds__(kThreads) void bwd_smallc_k(
         }
     };
 
-    // two register buffers, so the loop is unrolled by two
-    for (int tile = t_begin; tile < t_end;) {
+    // two register buffers, so the loop is unrolled by two; no exit between
+    // the two halves (a path from the first half back to the loop head would
+    // make the waits before its commit cover the other buffer's loads)
+    int tile = t_begin;
+    for (; tile + 1 < t_end; tile += 2) {
         tile_step(sa, tile);
-        if (++tile >= t_end)
-            break;
-        tile_step(sb, tile);
-        ++tile;
+        tile_step(sb, tile + 1);
     }
+    if (tile < t_end)
+        tile_step(sa, tile);
 
     // sum the accumulator sets and the weight-gradient waves in a fixed
     // order; one partial per output element (chunked layout)

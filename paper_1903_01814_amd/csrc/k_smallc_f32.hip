@@ -146,25 +146,53 @@ template <int U> struct PlainPrefetch {
 
 // --------------------------------------------------------------- forward
 
-template <typename TT, int K, int KS, int U>
+// D3: three-dimensional layer.  A tile's "image" index then runs over
+// (sample, output plane) pairs (sh.N = samples x output planes here), and
+// the staged channels are the 2 kz + 1 planes around the centre plane of
+// every input channel (ch = ci * Z + dz), so the contraction runs over
+// (ci, dz, t) -- exactly the order of w[C_out][C_in][2kz+1][T].
+template <typename TT, int K, int KS, int U, bool D3>
 __global__ __launch_bounds__(kThreads) void fwd_smallc_k(
     const TT *__restrict__ x, const TT *__restrict__ w, const TT *__restrict__ bias,
     TT *__restrict__ y, ConvShape sh, int relu, Tiling tg, int vec4)
 {
     constexpr int T = num_taps(K);
     extern __shared__ float xs[];
-    float *wt = xs + sh.Ci * tg.CS; // [16][C_in * T + 1]: this block's weights, bias last
+    const int NCH = D3 ? sh.Ci * sh.Z : sh.Ci; // staged channels
+    float *wt = xs + NCH * tg.CS; // [16][NCH * T + 1]: this block's weights, bias last
     const size_t HW = static_cast<size_t>(sh.H) * sh.W;
-    const int J = sh.Ci * T;
+    const int J = NCH * T;
+
+    // input channel 0 of the tile's sample, the output plane's index, and the
+    // staging of a tile's window (all planes around the output plane)
+    auto stage = [&](ShearPrefetch<U> &p, const TileOrigin &o) {
+        if constexpr (D3) {
+            const int n = o.n / sh.Do, dd = o.n - n * sh.Do;
+            const int d0 = dd * sh.sz - sh.kz; // plane of dz = 0
+            p.load3(x + static_cast<size_t>(n) * sh.Ci * sh.D * HW, sh.D * HW, HW,
+                    static_cast<long>(d0) * static_cast<long>(HW), sh.Z, max(0, -d0),
+                    min(sh.Z, sh.D - d0), NCH, sh.H, sh.W, window_of(o, tg, K), tg.TR + 2 * K,
+                    tg.fdlr);
+        } else {
+            p.load(x + static_cast<size_t>(o.n) * sh.Ci * HW, HW, sh.Ci, sh.H, sh.W,
+                   window_of(o, tg, K), tg.TR + 2 * K, tg.fdlr);
+        }
+    };
+    // first element of output plane (sample, channel co, plane) of a tile
+    auto out_plane = [&](const TileOrigin &o, int co) -> size_t {
+        if constexpr (D3) {
+            const int n = o.n / sh.Do, dd = o.n - n * sh.Do;
+            return ((static_cast<size_t>(n) * sh.Co + co) * sh.Do + dd) * HW;
+        } else {
+            return (static_cast<size_t>(o.n) * sh.Co + co) * HW;
+        }
+    };
 
     // the first tile's loads are in flight while the weights are staged
     ShearPrefetch<U> pf;
     int t = blockIdx.x;
-    if (t < tg.ntiles) {
-        const TileOrigin o = tile_of(t, tg, sh);
-        pf.load(x + static_cast<size_t>(o.n) * sh.Ci * HW, HW, sh.Ci, sh.H, sh.W,
-                window_of(o, tg, K), tg.TR + 2 * K, tg.fdlr);
-    }
+    if (t < tg.ntiles)
+        stage(pf, tile_of(t, tg, sh));
 
     // The block's weights (16 output channels) and biases: one coalesced
     // pass into LDS.  Every block reads the same few lines, so per-lane
@@ -214,15 +242,12 @@ __global__ __launch_bounds__(kThreads) void fwd_smallc_k(
         pf.commit(xs);
         __syncthreads();
         const int tn = t + gridDim.x;
-        if (tn < tg.ntiles) {
-            const TileOrigin on = tile_of(tn, tg, sh);
-            pf.load(x + static_cast<size_t>(on.n) * sh.Ci * HW, HW, sh.Ci, sh.H, sh.W,
-                    window_of(on, tg, K), tg.TR + 2 * K, tg.fdlr);
-        }
+        if (tn < tg.ntiles)
+            stage(pf, tile_of(tn, tg, sh));
 
         const int nslot = o.rows * tg.TW;
         const int ntile = (nslot + 15) / 16;
-        TT *yb = y + (static_cast<size_t>(o.n) * sh.Co + co) * HW;
+        TT *yb = y + out_plane(o, co);
         for (int mt = wave; mt < ntile; mt += kWaves) {
             // A row of this lane: pixel slot p of the tile
             const int p = mt * 16 + m;
@@ -495,7 +520,17 @@ size_t shear_bytes(const ConvShape &sh, const Tiling &tg, int nch)
 // staged input window plus the block's weights and biases
 size_t fwd_lds(const ConvShape &sh, const Tiling &tg)
 {
-    return shear_bytes(sh, tg, sh.Ci) + sizeof(float) * 16 * (sh.Ci * sh.T + 1);
+    const int nch = sh.Ci * sh.Z; // staged channels (planes around the centre in 3-D)
+    return shear_bytes(sh, tg, nch) + sizeof(float) * 16 * (nch * sh.T + 1);
+}
+
+// The forward tiles (sample, output plane) pairs as images: a 2-D layer has
+// one plane per sample.
+ConvShape fwd_view(const ConvShape &sh)
+{
+    ConvShape e = sh;
+    e.N = sh.N * sh.Do;
+    return e;
 }
 
 int wgrad_nt(const ConvShape &sh)
@@ -572,25 +607,36 @@ int bwd_ic_chunk(const ConvShape &sh, const Tiling &tg)
 
 bool smallc_fwd_ok(const ConvShape &sh)
 {
-    if (sh.s != 1 || (sh.k != 1 && sh.k != 2) || sh.Ci * sh.T > 64 || sh.W % 4 != 0)
+    const int nch = sh.Ci * sh.Z;
+    if (sh.s != 1 || (sh.k != 1 && sh.k != 2) || nch * sh.T > 64 || sh.W % 4 != 0)
         return false;
-    const Tiling tg = make_tiling(sh, kFwdTarget);
-    return fwd_lds(sh, tg) <= kLdsLimit && shear_depth(sh, tg, sh.Ci) > 0;
+    const ConvShape e = fwd_view(sh);
+    const Tiling tg = make_tiling(e, kFwdTarget);
+    return fwd_lds(e, tg) <= kLdsLimit && shear_depth(e, tg, nch) > 0;
 }
 
 namespace {
 template <typename TT>
-hipError_t smallc_fwd_t(const TT *x, const TT *w, const TT *b, TT *y, const ConvShape &sh,
+hipError_t smallc_fwd_t(const TT *x, const TT *w, const TT *b, TT *y, const ConvShape &sh0,
                         bool relu, hipStream_t st)
 {
+    const ConvShape sh = fwd_view(sh0);
+    const int nch = sh.Ci * sh.Z;
+    const bool d3 = sh.D != 1 || sh.Z != 1;
     const Tiling tg = make_tiling(sh, kFwdTarget);
-    const int KS = cdiv(sh.Ci * sh.T, 4);
-    const int U = shear_depth(sh, tg, sh.Ci);
+    const int KS = cdiv(nch * sh.T, 4);
+    const int U = shear_depth(sh, tg, nch);
     dim3 grid(std::min(tg.ntiles, kFwdBlocks), cdiv(sh.Co, 16));
     const size_t lds = fwd_lds(sh, tg);
 #define HEX_FWD_SC(KV, KSV, UV)                                                              \
-    HEX_LAUNCH((fwd_smallc_k<TT, KV, KSV, UV>), grid, dim3(kThreads), lds, st, x, w, b, y,   \
-               sh, relu ? 1 : 0, tg, 1)
+    do {                                                                                     \
+        if (d3)                                                                              \
+            HEX_LAUNCH((fwd_smallc_k<TT, KV, KSV, UV, true>), grid, dim3(kThreads), lds, st, \
+                       x, w, b, y, sh, relu ? 1 : 0, tg, 1);                                 \
+        else                                                                                 \
+            HEX_LAUNCH((fwd_smallc_k<TT, KV, KSV, UV, false>), grid, dim3(kThreads), lds,    \
+                       st, x, w, b, y, sh, relu ? 1 : 0, tg, 1);                             \
+    } while (0)
 #define HEX_FWD_SC_U(KV, KSV)                                                                \
     do {                                                                                     \
         if (U == 1) HEX_FWD_SC(KV, KSV, 1);                                                  \

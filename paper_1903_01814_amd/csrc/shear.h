@@ -309,6 +309,49 @@ template <int U> struct ShearPrefetch {
         }
     }
 
+    // Three-dimensional variant: staged channel ch = ci * Z + dz is plane
+    // d0 + dz of input channel ci (channel stride chan_plane, plane stride
+    // plane); planes dz outside [dz_lo, dz_hi) lie outside the volume and
+    // are staged as zeros.  img is channel 0, plane 0 of the sample (a valid
+    // address; z_off = d0 * plane is added only for loaded rows).
+    template <typename T>
+    __device__ __forceinline__ void load3(const T *__restrict__ img, size_t chan_plane,
+                                          size_t plane, long z_off, int Z, int dz_lo, int dz_hi,
+                                          int nch, int H, int W, const ShearTile &tl, int LRmax,
+                                          const FastDiv &fdlr)
+    {
+        const int nt = blockDim.x;
+        const int a4 = (tl.c_lo >= 0 ? tl.c_lo : tl.c_lo - 3) / 4 * 4;
+        const int ng = (tl.c_lo + tl.LC - a4 + 3) / 4;
+        const int rstep = nt / ng;
+        const int g = threadIdx.x % ng;
+        const int fr0 = threadIdx.x / ng;
+        const int cs = tl.chan_stride();
+        const int total = nch * LRmax;
+        P = tl.P;
+        c = a4 + 4 * g;
+        base_c = (c - tl.c_lo) * P - ((c >> 1) - (tl.c_lo >> 1));
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+            wcol[j] = (c + j >= tl.c_lo) && (c + j < tl.c_lo + tl.LC);
+        const bool inside = c >= 0 && c + 3 < W;
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            const int fr = fr0 + u * rstep;
+            live[u] = fr0 < rstep && fr < total;
+            const int ch = static_cast<int>(fdiv(static_cast<uint32_t>(fr), fdlr));
+            const int rr = fr - ch * LRmax;
+            const int r = tl.r_lo + rr;
+            const int ci = ch / Z, dz = ch - ci * Z;
+            okr[u] = live[u] && inside && r >= 0 && r < H && dz >= dz_lo && dz < dz_hi;
+            da[u] = ch * cs + base_c + rr;
+            Vec4Load<T>::load(img + (okr[u] ? static_cast<long>(ci * chan_plane + dz * plane) +
+                                                  z_off + static_cast<long>(r) * W + c
+                                            : 0),
+                              v[u]);
+        }
+    }
+
     __device__ __forceinline__ void commit(float *__restrict__ dst) const
     {
         const int o1 = P, o2 = 2 * P - 1, o3 = 3 * P - 1;

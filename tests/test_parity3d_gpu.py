@@ -86,6 +86,13 @@ CASES = [
     (1, 8, 40, 5, 12, 12, 1, 1, 1, 1), (1, 33, 17, 4, 10, 14, 1, 1, 1, 2),
     (1, 64, 64, 3, 12, 12, 1, 1, 1, 1), (2, 3, 70, 6, 7, 9, 2, 2, 3, 2),
     (1, 1, 16, 32, 40, 40, 1, 1, 1, 1), (1, 2, 3, 11, 20, 22, 5, 1, 5, 4),
+    # few input channels (C_in (2kz+1) T <= 64, k <= 2, W % 4 == 0): the
+    # planes around an output plane staged as extra input channels; plane
+    # strides 2 and 3, nine planes over a six-plane volume, one plane, two
+    # input channels, several 16-channel output blocks
+    (2, 1, 5, 9, 12, 16, 1, 1, 1, 2), (1, 1, 3, 10, 8, 8, 1, 1, 1, 3),
+    (1, 1, 7, 6, 12, 12, 1, 4, 1, 1), (1, 3, 20, 4, 12, 16, 2, 0, 1, 1),
+    (3, 2, 17, 5, 10, 20, 1, 1, 1, 2), (2, 1, 4, 1, 12, 8, 1, 2, 1, 1),
 ]
 
 
