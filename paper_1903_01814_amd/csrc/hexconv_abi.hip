@@ -603,6 +603,21 @@ int hexconv3d_bwd_data(const void *dy, const void *w, void *dx, int N, int C_in,
                                                 static_cast<hipStream_t>(stream)));
 }
 
+namespace {
+// 3-D weight gradient: the small-channel fp32 kernel with the planes around
+// each output plane staged as channels where it applies, else the generic one
+bool wgrad3d_smallc(const ConvShape &sh, hex_dtype dt)
+{
+    return !force_generic() && dt == HEX_F32 && hexk::smallc_f32_wgrad_ok(sh);
+}
+
+size_t wgrad3d_workspace(const ConvShape &sh, hex_dtype dt)
+{
+    return wgrad3d_smallc(sh, dt) ? hexk::smallc_f32_wgrad_workspace(sh)
+                                  : hexk::wgrad_generic_workspace(sh);
+}
+} // namespace
+
 size_t hexconv3d_bwd_weight_workspace(int N, int C_in, int C_out, int D, int H, int W, int k,
                                       int kz, int stride, int stride_z, hex_dtype dt)
 {
@@ -611,7 +626,7 @@ size_t hexconv3d_bwd_weight_workspace(int N, int C_in, int C_out, int D, int H, 
         return 0;
     if (N == 0 || sh.Ho == 0)
         return 0;
-    return hexk::wgrad_generic_workspace(sh);
+    return wgrad3d_workspace(sh, dt);
 }
 
 int hexconv3d_bwd_weight(const void *x, const void *dy, float *dw, float *db, void *ws,
@@ -627,12 +642,15 @@ int hexconv3d_bwd_weight(const void *x, const void *dy, float *dw, float *db, vo
     const bool empty = (N == 0 || sh.Ho == 0);
     if (!empty && (x == nullptr || dy == nullptr))
         return HEX_ERR_INVALID_ARG;
-    const size_t need = empty ? 0 : hexk::wgrad_generic_workspace(sh);
+    const size_t need = empty ? 0 : wgrad3d_workspace(sh, dt);
     if (need > 0 && (ws == nullptr || ws_bytes < need))
         return HEX_ERR_INVALID_ARG;
     hipStream_t st = static_cast<hipStream_t>(stream);
     if (empty)
         return launched(hexk::fill_zero_f32(dw, db, sh, st));
+    if (wgrad3d_smallc(sh, dt))
+        return launched(hexk::smallc_f32_wgrad(static_cast<const float *>(x),
+                                               static_cast<const float *>(dy), dw, db, ws, sh, st));
     return launched(hexk::wgrad_generic(x, dy, dw, db, ws, sh, static_cast<Dtype>(dt), st));
 }
 

@@ -380,7 +380,10 @@ __global__ __launch_bounds__(kThreads) void bwd_data_f32_k(
 
 // -------------------------------------------------------- weight gradient
 
-template <int K, int NT, int UX, int UD>
+// D3: three-dimensional layer, tiles over (sample, output plane) pairs with
+// the 2kz + 1 input planes around each output plane staged as channels
+// (ch = ci * Z + dz), so that column (ch, t) is dw[co][ci][dz][t].
+template <int K, int NT, int UX, int UD, bool D3>
 __global__ __launch_bounds__(kThreads) void wgrad_f32_k(
     const float *__restrict__ x, const float *__restrict__ dy, float *__restrict__ part,
     ConvShape sh, Tiling tg, int dstride)
@@ -388,8 +391,9 @@ __global__ __launch_bounds__(kThreads) void wgrad_f32_k(
     constexpr int T = num_taps(K);
     extern __shared__ float lds[];
     const int b = blockIdx.x; // partial slot
-    float *xs = lds;                      // [Ci][CS]
-    float *dys = xs + sh.Ci * tg.CS;      // [16][dstride], pitch TW
+    const int NCH = D3 ? sh.Ci * sh.Z : sh.Ci; // staged x channels
+    float *xs = lds;                      // [NCH][CS]
+    float *dys = xs + NCH * tg.CS;        // [16][dstride], pitch TW
     float *red = dys + 16 * dstride;      // [kWaves][16][NT * 16]
     const int mt = blockIdx.y;            // 16 output channels
     const int nco = min(16, sh.Co - mt * 16);
@@ -397,7 +401,7 @@ __global__ __launch_bounds__(kThreads) void wgrad_f32_k(
 
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     const int m = lane & 15, kq = lane >> 4;
-    const int J = sh.Ci * T; // tap columns; column J is the bias column
+    const int J = NCH * T; // tap columns; column J is the bias column
     int off[NT];  // LDS offset of the tap from the centre (may be negative)
     int kind[NT]; // 0: tap column, 1: ones (bias column), 2: unused
 #pragma unroll
@@ -421,14 +425,27 @@ __global__ __launch_bounds__(kThreads) void wgrad_f32_k(
 
     ShearPrefetch<UX> px;
     PlainPrefetch<UD> pd;
+    // a tile's x window (every plane around its output plane) and dy rows
+    auto stage = [&](const TileOrigin &o) {
+        if constexpr (D3) {
+            const int n = o.n / sh.Do, dd = o.n - n * sh.Do;
+            const int d0 = dd * sh.sz - sh.kz;
+            px.load3(x + static_cast<size_t>(n) * sh.Ci * sh.D * HW, sh.D * HW, HW,
+                     static_cast<long>(d0) * static_cast<long>(HW), sh.Z, max(0, -d0),
+                     min(sh.Z, sh.D - d0), NCH, sh.H, sh.W, window_of(o, tg, K), tg.TR + 2 * K,
+                     tg.fdlr);
+            pd.load(dy + ((static_cast<size_t>(n) * sh.Co + mt * 16) * sh.Do + dd) * HW,
+                    sh.Do * HW, nco, sh.W, o, tg.TW, dstride, tg.fdtr, tg.TR);
+        } else {
+            px.load(x + static_cast<size_t>(o.n) * sh.Ci * HW, HW, sh.Ci, sh.H, sh.W,
+                    window_of(o, tg, K), tg.TR + 2 * K, tg.fdlr);
+            pd.load(dy + (static_cast<size_t>(o.n) * sh.Co + mt * 16) * HW, HW, nco, sh.W, o,
+                    tg.TW, dstride, tg.fdtr, tg.TR);
+        }
+    };
     int t = b;
-    if (t < tg.ntiles) {
-        const TileOrigin o = tile_of(t, tg, sh);
-        px.load(x + static_cast<size_t>(o.n) * sh.Ci * HW, HW, sh.Ci, sh.H, sh.W,
-                window_of(o, tg, K), tg.TR + 2 * K, tg.fdlr);
-        pd.load(dy + (static_cast<size_t>(o.n) * sh.Co + mt * 16) * HW, HW, nco, sh.W, o, tg.TW,
-                dstride, tg.fdtr, tg.TR);
-    }
+    if (t < tg.ntiles)
+        stage(tile_of(t, tg, sh));
     for (; t < tg.ntiles; t += gridDim.x) {
         const TileOrigin o = tile_of(t, tg, sh);
         const ShearTile tl = window_of(o, tg, K);
@@ -437,13 +454,8 @@ __global__ __launch_bounds__(kThreads) void wgrad_f32_k(
         pd.commit(dys);
         __syncthreads();
         const int tn = t + gridDim.x;
-        if (tn < tg.ntiles) {
-            const TileOrigin on = tile_of(tn, tg, sh);
-            px.load(x + static_cast<size_t>(on.n) * sh.Ci * HW, HW, sh.Ci, sh.H, sh.W,
-                    window_of(on, tg, K), tg.TR + 2 * K, tg.fdlr);
-            pd.load(dy + (static_cast<size_t>(on.n) * sh.Co + mt * 16) * HW, HW, nco, sh.W, on,
-                    tg.TW, dstride, tg.fdtr, tg.TR);
-        }
+        if (tn < tg.ntiles)
+            stage(tile_of(tn, tg, sh));
         const int nslot = o.rows * tg.TW;
         const int nks = (nslot + 3) / 4;
         for (int ks = wave; ks < nks; ks += kWaves) {
@@ -535,7 +547,7 @@ ConvShape fwd_view(const ConvShape &sh)
 
 int wgrad_nt(const ConvShape &sh)
 {
-    const int NT = cdiv(sh.Ci * sh.T + 1, 16);
+    const int NT = cdiv(sh.Ci * sh.Z * sh.T + 1, 16);
     return NT <= 1 ? 1 : (NT <= 2 ? 2 : 4);
 }
 
@@ -548,7 +560,7 @@ int wgrad_dstride(const Tiling &tg)
 
 size_t wgrad_lds(const ConvShape &sh, const Tiling &tg)
 {
-    return shear_bytes(sh, tg, sh.Ci) +
+    return shear_bytes(sh, tg, sh.Ci * sh.Z) +
            sizeof(float) * (16 * static_cast<size_t>(wgrad_dstride(tg)) +
                             kWaves * 16 * wgrad_nt(sh) * 16);
 }
@@ -697,36 +709,51 @@ namespace {
 int wgrad_grid(const Tiling &tg) { return std::min(tg.ntiles, kWgradBlocks); }
 } // namespace
 
-bool smallc_f32_wgrad_ok(const ConvShape &sh)
+// (2-D shapes have Z = 1 and one plane per sample; the tiles of a 3-D
+// shape are (sample, output plane) pairs: fwd_view)
+bool smallc_f32_wgrad_ok(const ConvShape &sh0)
 {
-    if (sh.s != 1 || (sh.k != 1 && sh.k != 2) || sh.Ci * sh.T + 1 > 64 || sh.W % 4 != 0)
+    const ConvShape sh = fwd_view(sh0);
+    const int nch = sh.Ci * sh.Z;
+    if (sh.s != 1 || (sh.k != 1 && sh.k != 2) || nch * sh.T + 1 > 64 || sh.W % 4 != 0)
         return false;
     const Tiling tg = make_tiling(sh, kWgradTarget);
-    return wgrad_lds(sh, tg) <= kLdsLimit && shear_depth(sh, tg, sh.Ci) > 0 &&
+    return wgrad_lds(sh, tg) <= kLdsLimit && shear_depth(sh, tg, nch) > 0 &&
            plain_depth(tg, 16) > 0;
 }
 
-size_t smallc_f32_wgrad_workspace(const ConvShape &sh)
+size_t smallc_f32_wgrad_workspace(const ConvShape &sh0)
 {
+    const ConvShape sh = fwd_view(sh0);
     const Tiling tg = make_tiling(sh, kWgradTarget);
-    return sizeof(float) * static_cast<size_t>(wgrad_grid(tg)) * sh.Co * (sh.Ci * sh.T + 1);
+    return sizeof(float) * static_cast<size_t>(wgrad_grid(tg)) * sh.Co *
+           (sh.Ci * sh.Z * sh.T + 1);
 }
 
 hipError_t smallc_f32_wgrad(const float *x, const float *dy, float *dw, float *db, void *ws,
-                            const ConvShape &sh, hipStream_t st)
+                            const ConvShape &sh0, hipStream_t st)
 {
+    const ConvShape sh = fwd_view(sh0);
+    const int nch = sh.Ci * sh.Z;
+    const bool d3 = sh.D != 1 || sh.Z != 1;
     const Tiling tg = make_tiling(sh, kWgradTarget);
     const int nparts = wgrad_grid(tg);
     const int NT = wgrad_nt(sh);
-    const int UX = shear_depth(sh, tg, sh.Ci);
+    const int UX = shear_depth(sh, tg, nch);
     const int UD = plain_depth(tg, 16);
     const int dstride = wgrad_dstride(tg);
     float *part = static_cast<float *>(ws);
     dim3 grid(nparts, cdiv(sh.Co, 16));
     const size_t lds = wgrad_lds(sh, tg);
 #define HEX_WG(KV, NTV, UXV, UDV)                                                            \
-    HEX_LAUNCH((wgrad_f32_k<KV, NTV, UXV, UDV>), grid, dim3(kThreads), lds, st, x, dy, \
-                       part, sh, tg, dstride)
+    do {                                                                                     \
+        if (d3)                                                                              \
+            HEX_LAUNCH((wgrad_f32_k<KV, NTV, UXV, UDV, true>), grid, dim3(kThreads), lds,    \
+                       st, x, dy, part, sh, tg, dstride);                                    \
+        else                                                                                 \
+            HEX_LAUNCH((wgrad_f32_k<KV, NTV, UXV, UDV, false>), grid, dim3(kThreads), lds,   \
+                       st, x, dy, part, sh, tg, dstride);                                    \
+    } while (0)
 #define HEX_WG_UD(KV, NTV, UXV)                                                              \
     do {                                                                                     \
         if (UD <= 4) HEX_WG(KV, NTV, UXV, 4);                                                \
@@ -754,7 +781,7 @@ hipError_t smallc_f32_wgrad(const float *x, const float *dy, float *dw, float *d
     hipError_t e = hipGetLastError();
     if (e != hipSuccess)
         return e;
-    return reduce_partials(part, nparts, sh.Co, sh.Ci * sh.T, dw, db, st);
+    return reduce_partials(part, nparts, sh.Co, nch * sh.T, dw, db, st);
 }
 
 } // namespace hexk
