@@ -597,6 +597,11 @@ int hexconv3d_bwd_data(const void *dy, const void *w, void *dx, int N, int C_in,
         return rc;
     if (dy == nullptr && sh.Ho > 0)
         return HEX_ERR_INVALID_ARG;
+    if (!force_generic() && sh.Ho > 0 && dt == HEX_F32 && hexk::smallc3d_f32_bwd_data_ok(sh))
+        return launched(hexk::smallc3d_f32_bwd_data(static_cast<const float *>(dy),
+                                                    static_cast<const float *>(w),
+                                                    static_cast<float *>(dx), sh,
+                                                    static_cast<hipStream_t>(stream)));
     if (!hexk::conv_bwd_data_generic_ok(sh))
         return HEX_ERR_UNSUPPORTED;
     return launched(hexk::conv_bwd_data_generic(dy, w, dx, sh, static_cast<Dtype>(dt),

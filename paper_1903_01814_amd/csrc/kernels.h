@@ -111,6 +111,11 @@ hipError_t smallc_fwd(const void *x, const void *w, const void *b, void *y, cons
 bool smallc_f32_bwd_data_ok(const ConvShape &sh);
 hipError_t smallc_f32_bwd_data(const float *dy, const float *w, float *dx, const ConvShape &sh,
                                hipStream_t st);
+// Data gradient of a 3-D layer with 1 or 2 input channels, float32, plane
+// and in-plane stride 1, k <= 2, kz <= 2, W % 4 == 0 (k_bwd3d.hip).
+bool smallc3d_f32_bwd_data_ok(const ConvShape &sh);
+hipError_t smallc3d_f32_bwd_data(const float *dy, const float *w, float *dx, const ConvShape &sh,
+                                 hipStream_t st);
 bool smallc_f32_wgrad_ok(const ConvShape &sh);
 size_t smallc_f32_wgrad_workspace(const ConvShape &sh);
 hipError_t smallc_f32_wgrad(const float *x, const float *dy, float *dw, float *db, void *ws,
