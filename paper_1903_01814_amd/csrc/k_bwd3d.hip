@@ -17,10 +17,10 @@
 // ring shifts by one.  Every dy element is read from HBM once per plane
 // chunk (plus the 2kz planes a chunk shares with its neighbours).
 //
-// Thread = (column, strip of R rows) of the band; the weights are read with
-// wave-uniform indices (scalar loads).  The next two planes are loaded into
-// registers while the current one is computed; the loop body holds two
-// planes, so the register buffers have fixed names.
+// Thread = (column, strip of R = 2 rows) of the band; the weights sit in
+// LDS and are read with wave-uniform addresses.  The next two planes are
+// loaded into registers while the current one is computed; the loop body
+// holds two planes, so the register buffers have fixed names.
 #include <algorithm>
 
 #include "hexdev.h"
@@ -51,6 +51,12 @@ __global__ __launch_bounds__(kMaxThreads3) void bwd_data3d_smallc_k(
     constexpr int T = num_taps(K);
     constexpr int Z = 2 * KZ + 1;
     extern __shared__ float ds3[];
+    // weights staged once per block, [co][ci][s][t'] with t' the reflected
+    // tap, each (co, ci) row padded to WROW floats (16-byte aligned rows,
+    // read as wave-uniform 16-byte LDS reads: LDS reads complete in order,
+    // so the waits in the channel loop count them exactly, where scalar
+    // loads -- which may complete out of order -- would force a full wait)
+    constexpr int WROW = (Z * T + 3) / 4 * 4;
     const int W = sh.W, H = sh.H, D = sh.D, Co = sh.Co;
     const size_t HW = static_cast<size_t>(H) * W;
 
@@ -64,6 +70,12 @@ __global__ __launch_bounds__(kMaxThreads3) void bwd_data3d_smallc_k(
     const int e_lo = chunk * a.EC, e_hi = min(D, e_lo + a.EC);
     const int dlo = max(0, e_lo - KZ), dhi = min(D, e_hi + KZ);
 
+    float *wl = ds3 + Co * a.CS;
+    for (int e = threadIdx.x; e < Co * CI * WROW; e += blockDim.x) {
+        const int row = e / WROW, q = e - row * WROW; // row = co * CI + ci
+        const int s = q / T, tr = q - s * T;
+        wl[e] = q < Z * T ? w[(static_cast<size_t>(row) * Z + s) * T + (T - 1 - tr)] : 0.f;
+    }
     const ShearTile tl{r0 - K, -K, a.TR + 2 * K, W + 2 * K, a.P, a.CS};
     const int c = threadIdx.x % W, strip = threadIdx.x / W;
     const bool active = strip * R < rows; // threadIdx.x < W * ceil(TR / R)
@@ -138,10 +150,10 @@ __global__ __launch_bounds__(kMaxThreads3) void bwd_data3d_smallc_k(
 #pragma unroll
                     for (int u = 0; u < 2 * K + 1; ++u) {
                         if (u < len) {
-                            const int tr = T - 1 - (t0 + u); // reflected tap
+                            const int tr = t0 + u; // position in the reflected row
 #pragma unroll
                             for (int ci = 0; ci < CI; ++ci) {
-                                const float *wc = w + (static_cast<size_t>(co) * CI + ci) * Z * T;
+                                const float *wc = wl + (co * CI + ci) * WROW;
 #pragma unroll
                                 for (int s = 0; s < Z; ++s) {
                                     const float wv = wc[s * T + tr];
@@ -203,7 +215,7 @@ Bwd3Plan plan_bwd3(const ConvShape &sh)
     Bwd3Args &a = pl.a;
     // rows per band and per thread: about 2 blocks' worth of threads per band
     a.TR = 8;
-    pl.R = (sh.W * a.TR <= kMaxThreads3) ? 1 : 2;
+    pl.R = 2; // two rows per thread: each weight read serves two outputs
     if (sh.W * cdiv(a.TR, pl.R) > kMaxThreads3)
         return pl;
     pl.threads = cdiv(sh.W * cdiv(a.TR, pl.R), 64) * 64;
@@ -211,7 +223,10 @@ Bwd3Plan plan_bwd3(const ConvShape &sh)
     a.P = a.TR + 2 * K + 1;
     a.CS = (sh.W + 2 * K) * a.P;
     a.fdlr = make_fastdiv(static_cast<uint32_t>(a.TR + 2 * K));
-    pl.lds = sizeof(float) * static_cast<size_t>(sh.Co) * a.CS;
+    const int Z = 2 * sh.kz + 1;
+    const int wrow = (Z * sh.T + 3) / 4 * 4;
+    pl.lds = sizeof(float) * (static_cast<size_t>(sh.Co) * a.CS +
+                              static_cast<size_t>(sh.Co) * sh.Ci * wrow);
     if (pl.lds > kLds3)
         return pl;
     // staging rows per thread (ShearPrefetch): one 4-column group per thread
