@@ -479,7 +479,6 @@ __global__ __launch_bounds__(kGThreads) void conv_gen_dgrad_k(const bf16raw *__r
                                                               int ngroups_total)
 {
     constexpr int T = num_taps(K);
-    constexpr TapTable<K> tab{};
     constexpr int NTG = (T + kTG - 1) / kTG;
     extern __shared__ __align__(16) unsigned char smem[];
     bf16raw *win = reinterpret_cast<bf16raw *>(smem + a.win_off);
@@ -542,6 +541,26 @@ __global__ __launch_bounds__(kGThreads) void conv_gen_dgrad_k(const bf16raw *__r
                 slot0[m] = (sas + floor_half(cs) - i_lo) * a.RP + cs + a.coff;
                 peven[m] = (cs & 1) ? 0 : a.RP; // one row less for odd dQ at even c_s
             }
+            // taps that reach each group's class, once per round: lane t
+            // (t < T) tests tap t against the class residues; the ballot is
+            // the group's tap mask (wave-uniform), and the lane keeps the
+            // tap's slot offset for the K-steps to read back
+            uint64_t tmask[kMG];
+            int tdel[kMG], todd[kMG];
+            {
+                int dq = 0, ds = 0;
+                if (lane < T)
+                    tap_axial(K, lane, dq, ds);
+#pragma unroll
+                for (int m = 0; m < kMG; ++m) {
+                    const int vq = dq - cls[m].a, vs = ds - cls[m].b;
+                    const int dQ = floordiv(vq, s), dS = floordiv(vs, s);
+                    const bool match = lane < T && m < ng && vq == dQ * s && vs == dS * s;
+                    tmask[m] = __ballot(match);
+                    tdel[m] = -(dS + floor_half(dQ)) * a.RP - dQ;
+                    todd[m] = dQ & 1;
+                }
+            }
             floatx16 acc[kMG][2];
 #pragma unroll
             for (int m = 0; m < kMG; ++m)
@@ -568,22 +587,18 @@ __global__ __launch_bounds__(kGThreads) void conv_gen_dgrad_k(const bf16raw *__r
                 const bf16raw *wst = a.resident ? wl + st * kStageElems : wl;
                 const int ntap = min(kTG, T - t0);
                 const int cl = c0 - cw0;
-                for (int tt = 0; tt < ntap; ++tt) {
-                    const int t = t0 + tt;
-                    const int dq = tab.dq[t], ds = tab.ds[t];
-                    const bf16raw *wrow = wst + tt * kTB + n32 * kCP + 8 * kh;
+                const uint64_t smask = ((uint64_t(1) << ntap) - 1) << t0; // ntap <= 8
 #pragma unroll
-                    for (int m = 0; m < kMG; ++m) {
-                        if (m >= ng)
-                            break;
-                        // live iff (dq, ds) = (a, b) mod s (wave-uniform)
-                        int dQ, dS, rq, rs;
-                        small_divmod(dq - cls[m].a, s, dQ, rq);
-                        small_divmod(ds - cls[m].b, s, dS, rs);
-                        if (rq != 0 || rs != 0)
-                            continue;
-                        const int slot = slot0[m] - (dS + floor_half(dQ)) * a.RP - dQ -
-                                         ((dQ & 1) ? peven[m] : 0);
+                for (int m = 0; m < kMG; ++m) {
+                    // this stage's taps of the group's class, one at a time
+                    uint64_t bits = tmask[m] & smask;
+                    while (bits != 0) {
+                        const int t = static_cast<int>(__builtin_ctzll(bits));
+                        bits &= bits - 1;
+                        const int del = __builtin_amdgcn_readlane(tdel[m], t);
+                        const int odd = __builtin_amdgcn_readlane(todd[m], t);
+                        const int slot = slot0[m] + del - (odd ? peven[m] : 0);
+                        const bf16raw *wrow = wst + (t - t0) * kTB + n32 * kCP + 8 * kh;
                         const bf16x8 b0 = *reinterpret_cast<const bf16x8 *>(wrow);
                         const bf16x8 b1 = *reinterpret_cast<const bf16x8 *>(wrow + 32 * kCP);
                         const bf16x8 b2 = *reinterpret_cast<const bf16x8 *>(wrow + 16);
