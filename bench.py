@@ -54,6 +54,7 @@ from paper_1903_01814_amd import inputs as gen         # noqa: E402
 METRIC = "hex-conv effective GFLOP/s (fwd+bwd) and HBM GB/s vs roofline; samples/s"
 HBM_PEAK_GBS = 8000.0
 BF16_MFMA_PEAK_TFLOPS = 2500.0
+FP32_PEAK_TFLOPS = 157.3 # fp32 matrix cores and fp32 vector units alike
 SIMDS = 1024                      # 256 CUs x 4 SIMDs (MFMA utilisation denominator)
 CACHE_BYTES = 256 << 20
 ROTATE_MIN_BYTES = 3 * CACHE_BYTES
@@ -228,6 +229,18 @@ def products_of(kernel, op):
     return 2 if kernel in BOTH_GRADIENT_KERNELS else 1
 
 
+def part_of(kernel, op):
+    """The part of a convolution op one launch of `kernel` performs: "fwd",
+    "bwd" (both gradients), "bwd_data" or "bwd_weight"."""
+    if op.endswith("fwd"):
+        return "fwd"
+    if op in ("bwd_data", "bwd_weight"):
+        return op
+    if kernel in BOTH_GRADIENT_KERNELS:
+        return "bwd"
+    return "bwd_weight" if "wgrad" in kernel else "bwd_data"
+
+
 def conv_flop(N, Ci, Co, Ho, Wo, T):
     return 2.0 * N * Ho * Wo * Ci * Co * T
 
@@ -236,18 +249,29 @@ def dev(torch, a, dtype):
     return torch.from_numpy(np.ascontiguousarray(a)).to(dtype).to("cuda:0")
 
 
-def roofline_entry(bound, units, kname, kms, kper, op, kall, workload):
-    """Roofline of the dominant kernel: `units` (algorithmic bytes or FLOP
-    of the op) per launch over its measured duration; counters attached
-    when the committed summary matches."""
-    if bound == "hbm":
-        achieved = units / (kms * 1e-3) / 1e9
-        roof = dict(bound="hbm", achieved=round(achieved, 1), peak=HBM_PEAK_GBS, unit="GB/s",
-                    frac=round(achieved / HBM_PEAK_GBS, 4))
-    else:
-        achieved = units / (kms * 1e-3) / 1e12
-        roof = dict(bound="mfma", achieved=round(achieved, 2), peak=BF16_MFMA_PEAK_TFLOPS,
-                    unit="TFLOP/s", frac=round(achieved / BF16_MFMA_PEAK_TFLOPS, 4))
+def roofline_entry(bytes_pl, flop_pl, cpeak, kname, kms, kper, op, kall, workload):
+    """Roofline of the dominant kernel: its algorithmic bytes and FLOP per
+    launch (the part of the op that kernel performs) over its measured
+    duration, against HBM and against the matrix-core peak `cpeak` (TFLOP/s,
+    for the kernel's dtype).  The roof that binds is the one the kernel is
+    closer to (the larger fraction: at its peak it would take longer); the
+    other fraction is reported beside it.  Counters are attached when the
+    committed summary matches."""
+    t = kms * 1e-3
+    roofs = {}
+    if bytes_pl:
+        a = bytes_pl / t / 1e9
+        roofs["hbm"] = dict(bound="hbm", achieved=round(a, 1), peak=HBM_PEAK_GBS, unit="GB/s",
+                            frac=round(a / HBM_PEAK_GBS, 4), units=bytes_pl)
+    if flop_pl:
+        a = flop_pl / t / 1e12
+        roofs["mfma"] = dict(bound="mfma", achieved=round(a, 2), peak=cpeak, unit="TFLOP/s",
+                             frac=round(a / cpeak, 4), units=flop_pl)
+    bound = max(roofs, key=lambda b: roofs[b]["frac"])
+    roof = dict(roofs[bound])
+    units = roof.pop("units")
+    for b, r in roofs.items():
+        roof["frac_" + b] = r["frac"]
     cnt = read_counters(workload, op, kname)
     roof["traffic"] = None if cnt is None else cnt.get("hbm_bytes_per_launch")
     roof.update(kernel=kname, kernel_ms=round(kms, 5), launches_per_op=kper, op=op,
@@ -401,12 +425,10 @@ def bench_conv(args, torch, cfg_key, headline=True):
     # products) per launch of that kernel over its measured duration
     dom = max(("fwd", "bwd") if has_bwd else ("fwd",), key=lambda n: ops[n]["ms"])
     kname, kms, kper, kall = dominant_kernel(torch, op_fns[dom], reps_op)
-    bound = "hbm" if cfg["dtype"] == gen.F32 or Ci * T < 64 else "mfma"
-    if bound == "hbm":
-        units = bytes_alg[dom] / kper
-    else:
-        units = products_of(kname, dom) * flop_op / kper
-    roof = roofline_entry(bound, units, kname, kms, kper, dom, kall, cfg["name"])
+    cpeak = FP32_PEAK_TFLOPS if esz == 4 else BF16_MFMA_PEAK_TFLOPS
+    roof = roofline_entry(bytes_alg[part_of(kname, dom)] / kper,
+                          products_of(kname, dom) * flop_op / kper, cpeak, kname, kms, kper, dom,
+                          kall, cfg["name"])
 
     out = dict(
         metric=METRIC, value=round(value, 2), unit="GFLOP/s",
@@ -505,7 +527,8 @@ def bench_pool(args, torch, cfg_key, headline=True):
     value = 2 * (in_b + out_b) / (ms_step * 1e-3) / 1e9
     dom = max(ops, key=lambda n: ops[n]["ms"])
     kname, kms, kper, kall = dominant_kernel(torch, op_fns[dom], reps_op)
-    roof = roofline_entry("hbm", (in_b + out_b) / kper, kname, kms, kper, dom, kall, cfg["name"])
+    roof = roofline_entry((in_b + out_b) / kper, None, None, kname, kms, kper, dom, kall,
+                          cfg["name"])
     out = dict(
         metric=METRIC, value=round(value, 1), unit="GB/s",
         n_gpus=1, steps=args.steps, warmup=args.warmup, ms_per_step=round(ms_step, 5),
@@ -593,7 +616,9 @@ def bench_conv3d(args, torch, cfg_key, headline=True):
         ops[name] = dict(ms=ms, gbs=bytes_alg[name] / (ms * 1e-3) / 1e9)
     dom = max(ops, key=lambda n: ops[n]["ms"])
     kname, kms, kper, kall = dominant_kernel(torch, op_fns[dom], reps_op)
-    roof = roofline_entry("hbm", bytes_alg[dom] / kper, kname, kms, kper, dom, kall, cfg["name"])
+    roof = roofline_entry(bytes_alg[part_of(kname, dom)] / kper,
+                          flop_op / kper, FP32_PEAK_TFLOPS if esz == 4 else BF16_MFMA_PEAK_TFLOPS,
+                          kname, kms, kper, dom, kall, cfg["name"])
     out = dict(
         metric=METRIC, value=round(3 * flop_op / (ms_step * 1e-3) / 1e9, 2), unit="GFLOP/s",
         n_gpus=1, steps=args.steps, warmup=args.warmup, ms_per_step=round(ms_step, 5),
@@ -798,11 +823,12 @@ def bench_stack(args, torch, cfg_key, headline=True):
                 a_in[i % len(a_in)], g_in[i % len(g_in)], p["w"], dxs[i % len(dxs)],
                 wgr[li][0], wgr[li][1], ws, k, s)
             flop = conv_flop(N, ci, co, Ho, Wo, hx.hex_num_taps(k))
-            op_units["layer%d_fwd" % li] = ("mfma" if ci >= 32 else "hbm",
-                                            flop if ci >= 32 else in_b + out_b)
-            op_units["layer%d_bwd" % li] = ("mfma" if ci >= 32 else "hbm",
-                                            flop if ci >= 32 else
-                                            in_b + out_b + (in_b if li > 0 else 0))
+            dx_b = in_b if li > 0 else 0 # layer 0 has no data gradient
+            op_units["layer%d_fwd" % li] = (
+                {"fwd": in_b + out_b}, flop)
+            op_units["layer%d_bwd" % li] = (
+                {"bwd": in_b + out_b + dx_b, "bwd_weight": in_b + out_b,
+                 "bwd_data": out_b + dx_b}, flop)
         else:
             am_out = [ams[0][li].clone() for _ in range(R)]
             ry = [a.clone() for a in a_in] if relu_before(li) else None
@@ -814,9 +840,9 @@ def bench_stack(args, torch, cfg_key, headline=True):
                 None if ry is None else ry[i % len(ry)], dxs[i % len(dxs)], k, s,
                 hx.HEX_POOL_MAX)
             am_b = N * co * Ho * Wo
-            op_units["layer%d_fwd" % li] = ("hbm", in_b + out_b + am_b)
-            op_units["layer%d_bwd" % li] = ("hbm", out_b + am_b + in_b +
-                                            (in_b if ry is not None else 0))
+            op_units["layer%d_fwd" % li] = ({"fwd": in_b + out_b + am_b}, None)
+            op_units["layer%d_bwd" % li] = (
+                {"bwd": out_b + am_b + in_b + (in_b if ry is not None else 0)}, None)
         rot_fns["layer%d_fwd" % li], rot_fns["layer%d_bwd" % li] = f, bw
         per_layer.append(dict(layer=li, kind=kind, C_in=ci, C_out=co, k=k, stride=s,
                               rotating_copies=R,
@@ -826,11 +852,13 @@ def bench_stack(args, torch, cfg_key, headline=True):
     layer_roof = {}
     for op, fn in rot_fns.items():
         kname, kms, kper, kall = dominant_kernel(torch, fn, reps_op)
-        bound, alg = op_units[op]
-        # an MFMA-bound op's units are the products its dominant kernel does
-        units = (alg * products_of(kname, op) if bound == "mfma" else alg) / kper
-        r = roofline_entry(bound, units, kname, kms, kper, op, kall, cfg["name"])
-        layer_roof[op] = dict(kernel=kname, kernel_ms=r["kernel_ms"], bound=bound,
+        byts, flop = op_units[op]
+        # the bytes and products of the part of the op its dominant kernel does
+        part = part_of(kname, op) if flop is not None else op.rsplit("_", 1)[1]
+        b = byts.get(part, byts.get("bwd", byts.get("fwd")))
+        r = roofline_entry(b / kper, None if flop is None else flop * products_of(kname, op) / kper,
+                           BF16_MFMA_PEAK_TFLOPS, kname, kms, kper, op, kall, cfg["name"])
+        layer_roof[op] = dict(kernel=kname, kernel_ms=r["kernel_ms"], bound=r["bound"],
                               frac=r["frac"], achieved=r["achieved"], unit=r["unit"],
                               traffic=r["traffic"], full=r)
     flop = stack_flop(cfg, N)
