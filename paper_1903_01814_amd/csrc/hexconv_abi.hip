@@ -75,14 +75,13 @@ KTimer::KTimer(const char *kernel, hipStream_t st) : name_(kernel), st_(st), a_(
         a_ = nullptr;
         return;
     }
-    (void)hipEventRecord(a_, st_);
+    // the launch itself records the pair (see HEX_LAUNCH)
 }
 
 KTimer::~KTimer()
 {
     if (a_ == nullptr)
         return;
-    (void)hipEventRecord(b_, st_);
     std::lock_guard<std::mutex> lock(g_timing_mu);
     g_timed.push_back(TimedLaunch{kernel_base_name(name_), a_, b_});
 }

@@ -6,6 +6,7 @@
 // given stream and return the launch status.
 #pragma once
 
+#include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 #include <stddef.h>
 #include <stdint.h>
@@ -13,13 +14,19 @@
 namespace hexk {
 
 // Optional per-launch timing (hexconv_timing_begin / hexconv_timing_end):
-// when enabled, a HIP event pair brackets each launch made through
-// HEX_LAUNCH; otherwise the cost is one relaxed atomic load.
+// when enabled, each launch made through HEX_LAUNCH carries a HIP event pair
+// that the runtime records at the start and at the end of that kernel's own
+// execution (hipExtLaunchKernelGGL), so the dispatch of the launch is not
+// counted; otherwise the launch is a plain one and the cost is one relaxed
+// atomic load.
 struct KTimer {
     KTimer(const char *kernel, hipStream_t st);
     ~KTimer();
     KTimer(const KTimer &) = delete;
     KTimer &operator=(const KTimer &) = delete;
+    bool active() const { return a_ != nullptr; }
+    hipEvent_t start() const { return a_; }
+    hipEvent_t stop() const { return b_; }
 
   private:
     const char *name_;
@@ -35,7 +42,11 @@ struct KTimer {
     do {                                                                                     \
         (void)hipGetLastError();                                                             \
         ::hexk::KTimer hex_kt_(#kern, st);                                                   \
-        hipLaunchKernelGGL(kern, grid, block, shm, st, __VA_ARGS__);                         \
+        if (hex_kt_.active())                                                                \
+            hipExtLaunchKernelGGL(kern, grid, block, shm, st, hex_kt_.start(), hex_kt_.stop(), \
+                                  0, __VA_ARGS__);                                           \
+        else                                                                                 \
+            hipLaunchKernelGGL(kern, grid, block, shm, st, __VA_ARGS__);                     \
     } while (0)
 
 enum Dtype { F32 = 0, BF16 = 1 };
