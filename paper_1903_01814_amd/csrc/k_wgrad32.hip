@@ -247,7 +247,12 @@ template <int K, int U, int G> struct Wg32RegsR {
         }
     }
 
-    // even columns of the chunk to parity 0, odd to parity 1
+    // even columns of the chunk to parity 0, odd to parity 1.  Without
+    // branches: rounds outside the image write zeros (a select), rounds past
+    // the tile's last one write to this lane's 16 bytes of the sink region at
+    // the end of LDS.  (With a branch per round the staging waves issued
+    // about 600 scalar instructions and 150 branches per tile, and the
+    // commit took about 3 us of every tile while the computing waves waited.)
     __device__ __forceinline__ void commit(bf16raw *__restrict__ lds, const Wg32Args &a) const
     {
         constexpr uint32_t E = 0x05040100u, O = 0x07060302u;
@@ -257,24 +262,22 @@ template <int K, int U, int G> struct Wg32RegsR {
         const int bx = a.x_off + j * a.xc + 8 + c4;
         const int by = j * a.dyc + c4 - XR * 2 * a.WS; // dy round u: row u / G - XR
         const int sx = a.rpu * a.xc, sy = a.rpu * a.dyc;
+        const int sink = a.x_off + a.CI * a.xc + (threadIdx.x & 63) * 8;
 #pragma unroll
         for (int u = 0; u < U; ++u) {
-            if (u < rt) {
-                const bool isx = u < rx;
-                const int rr = u / G, cb = u % G;
-                const int off0 = isx ? bx + rr * 2 * a.XS + cb * sx : by + rr * 2 * a.WS + cb * sy;
-                const int off1 = off0 + (isx ? a.XS : a.WS);
-                if ((okm >> u) & 1u) {
-                    const uint4 q = v[u];
-                    *reinterpret_cast<uint2 *>(lds + off0) =
-                        make_uint2(perm(q.y, q.x, E), perm(q.w, q.z, E));
-                    *reinterpret_cast<uint2 *>(lds + off1) =
-                        make_uint2(perm(q.y, q.x, O), perm(q.w, q.z, O));
-                } else {
-                    *reinterpret_cast<uint2 *>(lds + off0) = make_uint2(0, 0);
-                    *reinterpret_cast<uint2 *>(lds + off1) = make_uint2(0, 0);
-                }
-            }
+            const bool isx = u < rx;
+            const int rr = u / G, cb = u % G;
+            const int offx = bx + rr * 2 * a.XS + cb * sx;
+            const int offy = by + rr * 2 * a.WS + cb * sy;
+            const bool live = u < rt;
+            const int off0 = live ? (isx ? offx : offy) : sink;
+            const int off1 = live ? off0 + (isx ? a.XS : a.WS) : sink + 4;
+            const bool ok = (okm >> u) & 1u;
+            const uint4 q = v[u];
+            const uint32_t e0 = ok ? perm(q.y, q.x, E) : 0u, e1 = ok ? perm(q.w, q.z, E) : 0u;
+            const uint32_t o0 = ok ? perm(q.y, q.x, O) : 0u, o1 = ok ? perm(q.w, q.z, O) : 0u;
+            *reinterpret_cast<uint2 *>(lds + off0) = make_uint2(e0, e1);
+            *reinterpret_cast<uint2 *>(lds + off1) = make_uint2(o0, o1);
         }
     }
 };
@@ -678,9 +681,11 @@ constexpr int max_ncb(int K, int NIB)
 }
 
 // LDS bytes: dy, then x
+// (plus 1 KB after x: the regular staging's sink for unused rounds, 16
+// bytes per lane)
 size_t wg32_lds(const Wg32Args &a)
 {
-    return 2ull * (a.x_off + static_cast<size_t>(a.CI) * a.xc);
+    return 2ull * (a.x_off + static_cast<size_t>(a.CI) * a.xc) + 1024;
 }
 
 // tiling of the pass over output channels co0 .. co0 + CO - 1 for a given
