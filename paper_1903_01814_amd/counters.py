@@ -2,7 +2,7 @@
 
     python -m paper_1903_01814_amd.counters pmc --config c4 --op bwd --kernel wgrad32_k
     python -m paper_1903_01814_amd.counters stats --config c4 --csv <kernel_stats.csv> \
-        --command "<the rocprofv3 command line>" [--bench-json <bench output>]
+        --command "<the rocprofv3 command line>" [--bench-live <bench.py output>]
 
 `stats` turns a `rocprofv3 --kernel-trace --stats` kernel_stats.csv into
 profiles/kernels_<workload>.txt (one row per kernel instantiation: calls,
@@ -131,16 +131,47 @@ def stats(args):
                 short_name(r["Name"]), r["Calls"], float(r["AverageNs"]) / 1e3,
                 float(r["MinNs"]) / 1e3, float(r["MaxNs"]) / 1e3,
                 100.0 * float(r["TotalDurationNs"]) / total))
-        if args.bench_json:
-            lines = [l for l in open(args.bench_json) if l.startswith("{")]
+        # an instantiation launched with several grids (a stack's layers
+        # sharing a kernel) is split by grid from the per-dispatch trace
+        if args.trace:
+            by = {}
+            for r in csv.DictReader(open(args.trace)):
+                if r.get("Kind") != "KERNEL_DISPATCH":
+                    continue
+                grid = (int(r["Grid_Size_X"]) * int(r["Grid_Size_Y"]) * int(r["Grid_Size_Z"])
+                        // max(1, int(r["Workgroup_Size_X"]) * int(r["Workgroup_Size_Y"])
+                               * int(r["Workgroup_Size_Z"])))
+                d = (int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3
+                by.setdefault(short_name(r["Kernel_Name"]), {}).setdefault(grid, []).append(d)
+            split = {k: v for k, v in by.items() if len(v) > 1}
+            if split:
+                fo.write("# launches by grid (blocks) for instantiations with several grids "
+                         "(from the per-dispatch trace)\n")
+                fo.write("kernel | blocks | calls | avg_us | min_us | max_us\n")
+                for k in sorted(split):
+                    for grid, ds in sorted(split[k].items(), key=lambda kv: -sum(kv[1])):
+                        fo.write("%s | %d | %d | %.2f | %.2f | %.2f\n" % (
+                            k, grid, len(ds), sum(ds) / len(ds), min(ds), max(ds)))
+        # the unprofiled bench.py run of the same GPU session (its live
+        # timing: the profiler delays the library's own events on short
+        # kernels, so the profiled run's bench line is not quoted)
+        if args.bench_live:
+            lines = [l for l in open(args.bench_live) if l.startswith("{")]
+            rec = None
             if lines:
                 b = json.loads(lines[-1])
-                roof = b.get("roofline", {})
-                fo.write("# bench line of the same run: %s %s, %.5f ms per step; dominant "
-                         "kernel %s (op %s) at %.2f us per launch (library event timing), "
-                         "roofline frac %s\n"
-                         % (b["value"], b["unit"], b["ms_per_step"], roof.get("kernel"),
-                            roof.get("op"), 1e3 * roof.get("kernel_ms", 0.0), roof.get("frac")))
+                if b.get("config", {}).get("workload") == workload:
+                    rec = b
+                else:
+                    rec = b.get("others", {}).get(workload)
+            if rec is not None:
+                roof = rec.get("roofline", {})
+                fo.write("# bench.py without the profiler, same session: %s %s, %.5f ms per "
+                         "step; dominant kernel %s (op %s) at %.2f us per launch (library "
+                         "timing: events attached to the launch), roofline %s frac %s\n"
+                         % (rec["value"], rec["unit"], rec["ms_per_step"], roof.get("kernel"),
+                            roof.get("op"), 1e3 * roof.get("kernel_ms", 0.0), roof.get("bound"),
+                            roof.get("frac")))
     print(open(dst).read())
 
 
@@ -233,7 +264,10 @@ def main():
     q.add_argument("--config", required=True, choices=["c1", "c2", "c3", "c4", "c5", "c6"])
     q.add_argument("--csv", required=True)
     q.add_argument("--command", required=True)
-    q.add_argument("--bench-json", default=None)
+    q.add_argument("--trace", default=None,
+                   help="kernel_trace.csv of the same run (splits instantiations by grid)")
+    q.add_argument("--bench-live", default=None,
+                   help="JSON line of an unprofiled bench.py run (its live timing is quoted)")
     args = p.parse_args()
     if args.cmd == "stats":
         stats(args)
