@@ -201,8 +201,8 @@ def step_distribution(torch, fn, nsets, reps=MEDIAN_REPS):
 
 def dominant_kernel(torch, fn, reps):
     """The kernel with the largest GPU time over `reps` eager calls of fn,
-    timed by the library (a HIP event pair around every launch, on the
-    stream it is launched on).  Returns (name, ms per launch, launches per
+    timed by the library (a HIP event pair attached to every launch and
+    recorded at the kernel's own start and end, on its stream).  Returns (name, ms per launch, launches per
     call, {name: ms per launch})."""
     torch.cuda.synchronize()
     hx.hexconv_timing_begin()

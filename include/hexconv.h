@@ -297,8 +297,10 @@ const char *hex_last_launch_error(void);
 /*
  * Kernel timing, for profiling (not part of the paper's operations).
  * Between hexconv_timing_begin() and hexconv_timing_end(), every kernel the
- * library launches is bracketed by a pair of HIP events recorded on the
- * stream it is launched on.  hexconv_timing_end() stops recording, waits
+ * library launches carries a pair of HIP events that the runtime records at
+ * the start and at the end of that kernel's own execution, on the stream it
+ * is launched on (so the dispatch is not counted).  hexconv_timing_end()
+ * stops recording, waits
  * for the recorded events and reports, per kernel (by the kernel's function
  * name, template arguments dropped, in order of first launch), the number
  * of launches and their summed GPU time in milliseconds.
