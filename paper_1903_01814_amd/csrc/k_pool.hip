@@ -201,98 +201,153 @@ __global__ __launch_bounds__(kPoolThreads) void pool_fwd_k(const TT *__restrict_
     }
 }
 
-// OPT: outputs per thread held in registers across the tap phases.
+// OPT: outputs per thread held in registers across the tap phases.  Every
+// global read of a block is issued before its first wait -- the outputs' dy
+// and argmax (indices clamped, so the count is fixed) and the first
+// kPoolBwdPrefetch 16-byte relu_y chunks of each thread -- so a block makes
+// one round trip to memory instead of one per output and per chunk.
+constexpr int kPoolBwdPrefetch = 4;
+
+// relu_y and dx are not restrict-qualified: without a mask the relu_y reads
+// go to dx (same shape; the values are not used), so that their count is
+// fixed and the wait before the tap phases covers dy and the argmax only.
 template <typename TT, int MODE, int K, int S, int OPT>
 __global__ __launch_bounds__(kPoolThreads) void pool_bwd_k(const TT *__restrict__ dy,
                                                            const uint8_t *__restrict__ am,
-                                                           const TT *__restrict__ relu_y,
-                                                           TT *__restrict__ dx, PoolArgs a)
+                                                           const TT *relu_y, TT *dx, PoolArgs a)
 {
     constexpr int T = num_taps(K);
+    constexpr int VEC = 16 / sizeof(TT); // W is a multiple of VEC
+    constexpr int RUP = kPoolBwdPrefetch;
     extern __shared__ __align__(16) float acc[]; // [np][H][W]
     const int p0 = blockIdx.x * a.NP;
     const int np = min(a.NP, a.nplanes - p0);
     const int H = a.H, W = a.W;
     const int HW = H * W;
     const int HWo = a.Ho * a.Wo;
+    const int nout = np * HWo;
+    const int nchunk = np * HW / VEC;
+    const size_t go0 = static_cast<size_t>(p0) * HWo;
+    const size_t g0 = static_cast<size_t>(p0) * HW;
 
-    for (int e = threadIdx.x; e < np * HW; e += kPoolThreads)
-        acc[e] = 0.f;
+    TT gv[OPT];
+    uint8_t tv[OPT];
+#pragma unroll
+    for (int u = 0; u < OPT; ++u) {
+        const int e = min(static_cast<int>(threadIdx.x) + u * kPoolThreads, nout - 1);
+        gv[u] = dy[go0 + e];
+        tv[u] = (MODE == 0) ? am[go0 + e] : 0;
+    }
+    const bool relu = relu_y != nullptr;
+    const TT *rsrc = relu ? relu_y : dx;
+    u32x4 rv[RUP];
+#pragma unroll
+    for (int u = 0; u < RUP; ++u) {
+        const int c = min(static_cast<int>(threadIdx.x) + u * kPoolThreads, nchunk - 1);
+        rv[u] = *reinterpret_cast<const u32x4 *>(rsrc + g0 + static_cast<size_t>(c) * VEC);
+    }
 
-    // this thread's outputs: dy, argmax tap and centre
+    for (int e = threadIdx.x * 4; e < np * HW; e += kPoolThreads * 4)
+        *reinterpret_cast<float4 *>(acc + e) = make_float4(0.f, 0.f, 0.f, 0.f);
+
+    // this thread's outputs: centre, plane offset, dy and (max pooling) the
+    // one pixel its gradient goes to -- under its argmax tap, -1 where that
+    // tap lies outside the input
+    constexpr TapTable<K> tt;
     float g[OPT];
-    int tap[OPT], base[OPT], rc_[OPT], cc_[OPT];
+    int tap[OPT], base[OPT], rc_[OPT], cc_[OPT], tgt[OPT];
 #pragma unroll
     for (int u = 0; u < OPT; ++u) {
         const int e = threadIdx.x + u * kPoolThreads;
-        g[u] = 0.f;
-        tap[u] = -1;
-        base[u] = 0;
-        rc_[u] = 0;
-        cc_[u] = 0;
-        if (e < np * HWo) {
-            const int pl = static_cast<int>(fdiv(static_cast<uint32_t>(e), a.fho));
-            const int o = e - pl * HWo;
-            const int i = static_cast<int>(fdiv(static_cast<uint32_t>(o), a.fwo));
-            const int j = o - i * a.Wo;
-            const size_t go = static_cast<size_t>(p0) * HWo + e;
-            g[u] = to_f(dy[go]);
-            tap[u] = (MODE == 0) ? static_cast<int>(am[go]) : T; // T: every tap
-            rc_[u] = centre_r<S>(i, j);
-            cc_[u] = S * j;
-            base[u] = pl * HW;
+        const bool live = e < nout;
+        const int ee = live ? e : 0;
+        const int pl = static_cast<int>(fdiv(static_cast<uint32_t>(ee), a.fho));
+        const int o = ee - pl * HWo;
+        const int i = static_cast<int>(fdiv(static_cast<uint32_t>(o), a.fwo));
+        const int j = o - i * a.Wo;
+        rc_[u] = centre_r<S>(i, j);
+        cc_[u] = S * j;
+        base[u] = pl * HW;
+        g[u] = to_f(gv[u]);
+        tap[u] = !live ? -1 : (MODE == 0) ? static_cast<int>(tv[u]) : T; // T: every tap
+        tgt[u] = -1;
+        if (MODE == 0) {
+            const int par = (S % 2 == 0) ? 0 : (cc_[u] & 1);
+            int dr = 0, dc = 0;
+#pragma unroll
+            for (int t = 0; t < T; ++t) {
+                const bool hit = tap[u] == t;
+                dr = hit ? (par ? tap_drow(tt.dq[t], tt.ds[t], 1) : tap_drow(tt.dq[t], tt.ds[t], 0)) : dr;
+                dc = hit ? tt.dq[t] : dc;
+            }
+            const int r = rc_[u] + dr, c = cc_[u] + dc;
+            const bool in = tap[u] >= 0 && tap[u] < T && r >= 0 && r < H && c >= 0 && c < W;
+            tgt[u] = in ? base[u] + r * W + c : -1;
         }
     }
     __syncthreads();
 
 #pragma unroll
     for (int t = 0; t < T; ++t) {
-        constexpr TapTable<K> tt;
-        const int dq = tt.dq[t], ds = tt.ds[t];
+        float cur[OPT];
+        int ad[OPT];
+        bool on[OPT];
 #pragma unroll
         for (int u = 0; u < OPT; ++u) {
-            const bool use = (MODE == 0) ? (tap[u] == t) : (tap[u] == T);
-            if (use) {
+            if (MODE == 0) {
+                on[u] = tap[u] == t && tgt[u] >= 0;
+                ad[u] = tgt[u];
+            } else {
                 const int par = (S % 2 == 0) ? 0 : (cc_[u] & 1);
-                const int r = rc_[u] + tap_drow(dq, ds, par);
-                const int c = cc_[u] + dq;
-                if (r >= 0 && r < H && c >= 0 && c < W)
-                    acc[base[u] + r * W + c] += g[u];
+                const int r = rc_[u] + (par ? tap_drow(tt.dq[t], tt.ds[t], 1) : tap_drow(tt.dq[t], tt.ds[t], 0));
+                const int c = cc_[u] + tt.dq[t];
+                on[u] = tap[u] == T && r >= 0 && r < H && c >= 0 && c < W;
+                ad[u] = base[u] + r * W + c;
             }
+            cur[u] = acc[on[u] ? ad[u] : 0];
         }
+        // two outputs never reach one pixel in the same phase, so the reads
+        // of a phase (all issued, unused ones from element 0) may all
+        // precede its writes
+#pragma unroll
+        for (int u = 0; u < OPT; ++u)
+            if (on[u])
+                acc[ad[u]] = cur[u] + g[u];
         __syncthreads(); // phase t complete before phase t+1 touches the same pixels
     }
 
-    // dx of the block's planes (contiguous in memory), VEC pixels per thread
-    // and 16-byte loads / stores when the planes hold whole 16-byte chunks
-    constexpr int VEC = 16 / sizeof(TT);
-    const size_t g0 = static_cast<size_t>(p0) * HW;
-    const int total = np * HW;
-    if (HW % VEC == 0) {
-        for (int e0 = threadIdx.x * VEC; e0 < total; e0 += kPoolThreads * VEC) {
-            TT rv[VEC], ov[VEC];
-            if (relu_y != nullptr)
-                *reinterpret_cast<uint4 *>(rv) = *reinterpret_cast<const uint4 *>(relu_y + g0 + e0);
+    // dx of the block's planes (contiguous in memory), VEC pixels per chunk
+    auto emit = [&](int c, const u32x4 &rr) {
+        const int e0 = c * VEC;
+        const TT *rt = reinterpret_cast<const TT *>(&rr);
+        TT ov[VEC];
 #pragma unroll
-            for (int q = 0; q < VEC; ++q) {
-                float v = acc[e0 + q];
+        for (int q = 0; q < VEC; q += 4) {
+            const float4 v4 = *reinterpret_cast<const float4 *>(acc + e0 + q);
+            const float vv[4] = {v4.x, v4.y, v4.z, v4.w};
+#pragma unroll
+            for (int h = 0; h < 4; ++h) {
+                float v = vv[h];
                 if (MODE == 1)
                     v = v / static_cast<float>(T);
-                if (relu_y != nullptr && !(to_f(rv[q]) > 0.f))
+                if (relu && !(to_f(rt[q + h]) > 0.f))
                     v = 0.f;
-                ov[q] = from_f<TT>(v);
+                ov[q + h] = from_f<TT>(v);
             }
-            *reinterpret_cast<uint4 *>(dx + g0 + e0) = *reinterpret_cast<const uint4 *>(ov);
         }
-    } else {
-        for (int e = threadIdx.x; e < total; e += kPoolThreads) {
-            float v = acc[e];
-            if (MODE == 1)
-                v = v / static_cast<float>(T);
-            if (relu_y != nullptr && !(to_f(relu_y[g0 + e]) > 0.f))
-                v = 0.f;
-            dx[g0 + e] = from_f<TT>(v);
-        }
+        *reinterpret_cast<u32x4 *>(dx + g0 + e0) = *reinterpret_cast<const u32x4 *>(ov);
+    };
+#pragma unroll
+    for (int u = 0; u < RUP; ++u) {
+        const int c = threadIdx.x + u * kPoolThreads;
+        if (c < nchunk)
+            emit(c, rv[u]);
+    }
+    for (int c = threadIdx.x + RUP * kPoolThreads; c < nchunk; c += kPoolThreads) {
+        u32x4 rr = {0u, 0u, 0u, 0u};
+        if (relu)
+            rr = *reinterpret_cast<const u32x4 *>(relu_y + g0 + static_cast<size_t>(c) * VEC);
+        emit(c, rr);
     }
 }
 
