@@ -62,7 +62,7 @@ std::string kernel_base_name(const char *s)
 
 } // namespace
 
-KTimer::KTimer(const char *kernel, hipStream_t st) : name_(kernel), st_(st), a_(nullptr), b_(nullptr)
+KTimer::KTimer(const char *kernel) : name_(kernel), a_(nullptr), b_(nullptr)
 {
     if (!g_timing.load(std::memory_order_relaxed))
         return;

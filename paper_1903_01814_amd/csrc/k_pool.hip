@@ -484,8 +484,9 @@ hipError_t pool_bwd_fast(const void *dy, const uint8_t *am, const void *relu_y, 
     PoolArgs a = pool_args(sh, esz);
     const size_t plane = sizeof(float) * static_cast<size_t>(sh.H) * sh.W;
     const int by_lds = static_cast<int>(kPoolLds / plane);
-    // up to 8 outputs per thread
-    const int by_opt = std::max(1, (8 * kPoolThreads) / std::max(1, sh.Ho * sh.Wo));
+    // up to 4 outputs per thread (measured: 8 and 16 were slower at the
+    // 48x48 and 24x24 stride-2 pools)
+    const int by_opt = std::max(1, (4 * kPoolThreads) / std::max(1, sh.Ho * sh.Wo));
     a.NP = std::max(1, std::min(by_lds, by_opt));
     const int opt = bwd_opt(a, a.NP);
     const int grid = cdiv(a.nplanes, a.NP);

@@ -86,12 +86,13 @@ __device__ __forceinline__ ShearTile window_of(const TileOrigin &o, const Tiling
 
 // Row-major copy of a tile of `nch` planes (no halo) staged through
 // registers: dst[ch * dstride + pr * TW + pc].  Work split: one 4-column group
-// per thread, (channel, row) pairs strided by blockDim / groups.
+// per thread, (channel, row) pairs strided by blockDim / groups.  Requires
+// W % 4 == 0 (so TW, the tile's columns and every group of 4 lie inside the
+// row): each item is one 16-byte load and, dstride being even, two 8-byte LDS
+// writes.
 template <int U> struct PlainPrefetch {
     float v[U][4];
     int da[U];
-    bool full;
-    int pc, cols;
 
     __host__ __device__ static int groups(int TW) { return (TW + 3) / 4; }
     __host__ __device__ static int rows_per_thread(int nch, int TR, int TW, int nt)
@@ -107,9 +108,7 @@ template <int U> struct PlainPrefetch {
         const int ng = groups(TW);
         const int rstep = blockDim.x / ng;
         const int g = threadIdx.x % ng, fr0 = threadIdx.x / ng;
-        pc = 4 * g;
-        cols = o.cols;
-        full = pc + 3 < o.cols;
+        const int pc = 4 * g;
         const int total = nch * TR;
 #pragma unroll
         for (int u = 0; u < U; ++u) {
@@ -118,15 +117,10 @@ template <int U> struct PlainPrefetch {
             const int pr = fr - ch * TR;
             const bool ok = fr0 < rstep && fr < total && pr < o.rows && pc < o.cols;
             da[u] = ok ? ch * dstride + pr * TW + pc : -1;
-            const float *row =
-                src + (ok ? ch * src_plane + static_cast<size_t>(o.r0 + pr) * W + o.c0 : 0);
-            if (full) {
-                Vec4Load<float>::load(row + (ok ? pc : 0), v[u]);
-            } else {
-#pragma unroll
-                for (int j = 0; j < 4; ++j)
-                    v[u][j] = row[(ok && pc + j < o.cols) ? pc + j : 0];
-            }
+            // items without data read the plane's first group (always valid)
+            const float *p =
+                src + (ok ? ch * src_plane + static_cast<size_t>(o.r0 + pr) * W + o.c0 + pc : 0);
+            Vec4Load<float>::load(p, v[u]);
         }
     }
 
@@ -135,10 +129,8 @@ template <int U> struct PlainPrefetch {
 #pragma unroll
         for (int u = 0; u < U; ++u) {
             if (da[u] >= 0) {
-#pragma unroll
-                for (int j = 0; j < 4; ++j)
-                    if (pc + j < cols)
-                        dst[da[u] + j] = v[u][j];
+                *reinterpret_cast<float2 *>(dst + da[u]) = make_float2(v[u][0], v[u][1]);
+                *reinterpret_cast<float2 *>(dst + da[u] + 2) = make_float2(v[u][2], v[u][3]);
             }
         }
     }

@@ -20,7 +20,7 @@ namespace hexk {
 // counted; otherwise the launch is a plain one and the cost is one relaxed
 // atomic load.
 struct KTimer {
-    KTimer(const char *kernel, hipStream_t st);
+    explicit KTimer(const char *kernel);
     ~KTimer();
     KTimer(const KTimer &) = delete;
     KTimer &operator=(const KTimer &) = delete;
@@ -30,7 +30,6 @@ struct KTimer {
 
   private:
     const char *name_;
-    hipStream_t st_;
     hipEvent_t a_, b_;
 };
 
@@ -41,7 +40,7 @@ struct KTimer {
 #define HEX_LAUNCH(kern, grid, block, shm, st, ...)                                          \
     do {                                                                                     \
         (void)hipGetLastError();                                                             \
-        ::hexk::KTimer hex_kt_(#kern, st);                                                   \
+        ::hexk::KTimer hex_kt_(#kern);                                                       \
         if (hex_kt_.active())                                                                \
             hipExtLaunchKernelGGL(kern, grid, block, shm, st, hex_kt_.start(), hex_kt_.stop(), \
                                   0, __VA_ARGS__);                                           \
