@@ -561,7 +561,10 @@ constexpr int kFwdTarget = 320;
 constexpr int kWgradTarget = 320;
 constexpr int kBwdR = 4;
 constexpr int kFwdBlocks = 1024;   // persistent grid caps
-constexpr int kWgradBlocks = 512;
+// weight gradient: persistent blocks per CU, as many as LDS holds up to this
+// cap (c6 weight gradient: 138 us at 2 per CU, 111 us at 4)
+constexpr int kWgradPerCu = 4;
+constexpr size_t kLdsPerCu = 160 * 1024;
 
 // prefetch depth (float4 per thread) for a sheared window, 0 if too deep
 int shear_depth(const ConvShape &sh, const Tiling &tg, int nch)
@@ -698,7 +701,12 @@ hipError_t smallc_f32_bwd_data(const float *dy, const float *w, float *dx, const
 }
 
 namespace {
-int wgrad_grid(const Tiling &tg) { return std::min(tg.ntiles, kWgradBlocks); }
+int wgrad_grid(const ConvShape &sh, const Tiling &tg)
+{
+    const int per_cu = std::max(
+        1, std::min(kWgradPerCu, static_cast<int>(kLdsPerCu / std::max<size_t>(1, wgrad_lds(sh, tg)))));
+    return std::min(tg.ntiles, device_cus() * per_cu);
+}
 } // namespace
 
 // (2-D shapes have Z = 1 and one plane per sample; the tiles of a 3-D
@@ -718,7 +726,7 @@ size_t smallc_f32_wgrad_workspace(const ConvShape &sh0)
 {
     const ConvShape sh = fwd_view(sh0);
     const Tiling tg = make_tiling(sh, kWgradTarget);
-    return sizeof(float) * static_cast<size_t>(wgrad_grid(tg)) * sh.Co *
+    return sizeof(float) * static_cast<size_t>(wgrad_grid(sh, tg)) * sh.Co *
            (sh.Ci * sh.Z * sh.T + 1);
 }
 
@@ -729,7 +737,7 @@ hipError_t smallc_f32_wgrad(const float *x, const float *dy, float *dw, float *d
     const int nch = sh.Ci * sh.Z;
     const bool d3 = sh.D != 1 || sh.Z != 1;
     const Tiling tg = make_tiling(sh, kWgradTarget);
-    const int nparts = wgrad_grid(tg);
+    const int nparts = wgrad_grid(sh, tg);
     const int NT = wgrad_nt(sh);
     const int UX = shear_depth(sh, tg, nch);
     const int UD = plain_depth(tg, 16);
