@@ -18,9 +18,12 @@
 // chunk (plus the 2kz planes a chunk shares with its neighbours).
 //
 // Thread = (column, strip of R = 2 rows) of the band; the weights sit in
-// LDS and are read with wave-uniform addresses.  The next two planes are
-// loaded into registers while the current one is computed; the loop body
-// holds two planes, so the register buffers have fixed names.
+// LDS and are read with wave-uniform addresses.  The next plane is loaded
+// into registers while the current one is computed.  One plane ahead, and
+// at most 8 staged window rows per thread (the block takes extra threads,
+// idle in the products, to get there), keep the kernel at about 90
+// registers: five waves per SIMD instead of two with two planes ahead of 12
+// rows each (215 registers; c6 data gradient 145 -> 110 us).
 #include <algorithm>
 
 #include "hexdev.h"
@@ -126,13 +129,13 @@ __global__ __launch_bounds__(kMaxThreads3) void bwd_data3d_smallc_k(
                 acc[Z - 1][ci][r] = 0.f;
     };
 
-    // one dy plane: stage it, request the plane two ahead, add its
-    // contributions to the ring, retire slot 0
+    // one dy plane: stage it, request the next plane into the same
+    // registers, add its contributions to the ring, retire slot 0
     auto plane_step = [&](ShearPrefetch<U> &p, int d) {
         __syncthreads(); // the previous plane's reads are done
         p.commit(ds3);
         __syncthreads();
-        load_plane(p, d + 2);
+        load_plane(p, d + 1);
         if (active) {
             for (int co = 0; co < Co; ++co) {
                 const float *src = ds3 + co * a.CS + a0;
@@ -173,17 +176,9 @@ __global__ __launch_bounds__(kMaxThreads3) void bwd_data3d_smallc_k(
     };
 
     // the ring starts at dx planes dlo - kz .. dlo + kz
-    ShearPrefetch<U> pa, pb;
+    ShearPrefetch<U> pa;
     load_plane(pa, dlo);
-    __builtin_amdgcn_sched_barrier(0);
-    load_plane(pb, dlo + 1);
-    __builtin_amdgcn_sched_barrier(0);
-    int d = dlo;
-    for (; d + 1 < dhi; d += 2) {
-        plane_step(pa, d);
-        plane_step(pb, d + 1);
-    }
-    if (d < dhi)
+    for (int d = dlo; d < dhi; ++d)
         plane_step(pa, d);
     // planes dhi - kz .. dhi - 1 have no further dy plane inside the range
 #pragma unroll
@@ -233,8 +228,15 @@ Bwd3Plan plan_bwd3(const ConvShape &sh)
     const int groups = ShearPrefetch<1>::groups(sh.W + 2 * K);
     if (groups > pl.threads)
         return pl;
-    const int rstep = pl.threads / groups;
-    const int rpt = cdiv(static_cast<long>(sh.Co) * (a.TR + 2 * K), rstep);
+    // staging rows per thread: more threads (idle in the products) until a
+    // thread stages at most 8 window rows (92 registers at k = 1, against
+    // 143 for 12 rows)
+    auto rows_per_thread = [&](int nt) {
+        return cdiv(static_cast<long>(sh.Co) * (a.TR + 2 * K), nt / groups);
+    };
+    while (rows_per_thread(pl.threads) > 8 && pl.threads + 64 <= kMaxThreads3)
+        pl.threads += 64;
+    const int rpt = rows_per_thread(pl.threads);
     pl.U = rpt <= 4 ? 4 : rpt <= 8 ? 8 : rpt <= 12 ? 12 : 0;
     if (pl.U == 0)
         return pl;
