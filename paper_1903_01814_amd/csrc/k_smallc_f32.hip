@@ -43,6 +43,7 @@ typedef float floatx4 __attribute__((ext_vector_type(4)));
 
 constexpr int kThreads = 256;
 constexpr int kWaves = kThreads / 64;
+constexpr int kFwdMT = 5; // 16-pixel M-tiles per wave and forward tile (tiles <= 320 pixels)
 
 // Blocks are handed to the 8 XCDs round-robin; give each XCD a contiguous
 // range of tiles so neighbouring tiles (shared halo rows) meet in one L2.
@@ -148,6 +149,7 @@ __global__ __launch_bounds__(kThreads) void fwd_smallc_k(
     const TT *__restrict__ x, const TT *__restrict__ w, const TT *__restrict__ bias,
     TT *__restrict__ y, ConvShape sh, int relu, Tiling tg, int vec4)
 {
+    (void)vec4; // W % 4 == 0 (smallc_fwd_ok)
     constexpr int T = num_taps(K);
     extern __shared__ float xs[];
     const int NCH = D3 ? sh.Ci * sh.Z : sh.Ci; // staged channels
@@ -218,11 +220,34 @@ __global__ __launch_bounds__(kThreads) void fwd_smallc_k(
         }
     }
 
+    // The pixel slots of this lane's M-tiles (mt = wave + kWaves * i; tiles
+    // hold at most kFwdMT * kWaves * 16 slots) do not depend on the tile:
+    // window address of the A row (its sheared offset is the same for every
+    // tile, the column origin being even), the slot's row and column, and
+    // the output offset of the lane's four D rows.  Computed once, so the
+    // products of a tile are LDS reads, matrix-core steps and stores.
+    const int Kh = (-K) >> 1; // floor(-K / 2)
+    const int cen0 = K * tg.P + K + Kh; // slot (0, 0)
+    int cen[kFwdMT], prc[kFwdMT], qoff[kFwdMT], qrc[kFwdMT];
+#pragma unroll
+    for (int i = 0; i < kFwdMT; ++i) {
+        const int mt = wave + kWaves * i;
+        const int p = mt * 16 + m;
+        const int pr = static_cast<int>(fdiv(p, tg.fdw));
+        const int pc = p - pr * tg.TW;
+        cen[i] = (pc + K) * tg.P + pr + K - ((pc >> 1) - Kh);
+        prc[i] = (pr << 16) | pc;
+        const int q0 = mt * 16 + 4 * kq;
+        const int qr = static_cast<int>(fdiv(q0, tg.fdw));
+        const int qc = q0 - qr * tg.TW;
+        qoff[i] = qr * sh.W + qc;
+        qrc[i] = (qr << 16) | qc;
+    }
+
     float bw[KS], bco = 0.f;
     bool have_w = false;
     for (; t < tg.ntiles; t += gridDim.x) {
         const TileOrigin o = tile_of(t, tg, sh);
-        const ShearTile tl = window_of(o, tg, K);
         __syncthreads(); // previous tile's reads of xs are done (and the weights staged)
         if (!have_w) {
 #pragma unroll
@@ -237,34 +262,29 @@ __global__ __launch_bounds__(kThreads) void fwd_smallc_k(
         if (tn < tg.ntiles)
             stage(pf, tile_of(tn, tg, sh));
 
-        const int nslot = o.rows * tg.TW;
-        const int ntile = (nslot + 15) / 16;
-        TT *yb = y + out_plane(o, co);
-        for (int mt = wave; mt < ntile; mt += kWaves) {
-            // A row of this lane: pixel slot p of the tile
-            const int p = mt * 16 + m;
-            const int pr = static_cast<int>(fdiv(p, tg.fdw));
-            const int pc = p - pr * tg.TW;
-            const bool pv = pr < o.rows && pc < o.cols;
-            // every read is issued (address clamped to 0 for padding lanes) so
-            // the KS reads overlap; padding values are then replaced by zero
-            const int centre = pv ? tl.addr(o.r0 + pr, o.c0 + pc) : 0;
+        const int ntile = (o.rows * tg.TW + 15) / 16;
+        TT *yb = y + out_plane(o, co) + static_cast<size_t>(o.r0) * sh.W + o.c0;
+#pragma unroll
+        for (int i = 0; i < kFwdMT; ++i) {
+            if (wave + kWaves * i >= ntile) // wave-uniform
+                break;
+            // A row: slots outside the tile read the taps of slot 0, inside
+            // the window (their results are not stored); K columns past the
+            // taps (off = 0) are replaced by 0
+            const bool pv = (prc[i] >> 16) < o.rows && (prc[i] & 0xffff) < o.cols;
+            const int ca = pv ? cen[i] : cen0;
             float a[KS];
 #pragma unroll
             for (int s = 0; s < KS; ++s)
-                a[s] = xs[(pv && kval[s]) ? centre + off[s] : 0];
+                a[s] = xs[ca + off[s]];
             floatx4 acc = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
             for (int s = 0; s < KS; ++s)
-                acc = __builtin_amdgcn_mfma_f32_16x16x4f32((pv && kval[s]) ? a[s] : 0.f, bw[s],
-                                                           acc, 0, 0, 0);
-            if (co >= sh.Co)
-                continue;
-            // D rows of this lane: slots q0..q0+3 (same tile row since TW % 4 == 0)
-            const int q0 = mt * 16 + 4 * kq;
-            const int qr = static_cast<int>(fdiv(q0, tg.fdw));
-            const int qc = q0 - qr * tg.TW;
-            if (qr >= o.rows)
+                acc = __builtin_amdgcn_mfma_f32_16x16x4f32(kval[s] ? a[s] : 0.f, bw[s], acc, 0,
+                                                           0, 0);
+            // D rows of this lane: slots q0..q0+3, one tile row (TW % 4 == 0,
+            // and W % 4 == 0 puts all four inside the tile or none)
+            if (co >= sh.Co || (qrc[i] >> 16) >= o.rows || (qrc[i] & 0xffff) >= o.cols)
                 continue;
             float v[4];
 #pragma unroll
@@ -273,20 +293,13 @@ __global__ __launch_bounds__(kThreads) void fwd_smallc_k(
                 if (relu)
                     v[j] = fmaxf(v[j], 0.f);
             }
-            TT *dst = yb + static_cast<size_t>(o.r0 + qr) * sh.W + o.c0 + qc;
-            if (vec4 && qc + 3 < o.cols) {
-                if constexpr (sizeof(TT) == 4) {
-                    *reinterpret_cast<float4 *>(dst) = make_float4(v[0], v[1], v[2], v[3]);
-                } else {
-                    const uint32_t lo = from_f<bf16raw>(v[0]) | (uint32_t(from_f<bf16raw>(v[1])) << 16);
-                    const uint32_t hi = from_f<bf16raw>(v[2]) | (uint32_t(from_f<bf16raw>(v[3])) << 16);
-                    *reinterpret_cast<uint2 *>(dst) = make_uint2(lo, hi);
-                }
+            TT *dst = yb + qoff[i];
+            if constexpr (sizeof(TT) == 4) {
+                *reinterpret_cast<float4 *>(dst) = make_float4(v[0], v[1], v[2], v[3]);
             } else {
-#pragma unroll
-                for (int j = 0; j < 4; ++j)
-                    if (qc + j < o.cols)
-                        dst[j] = from_f<TT>(v[j]);
+                const uint32_t lo = from_f<bf16raw>(v[0]) | (uint32_t(from_f<bf16raw>(v[1])) << 16);
+                const uint32_t hi = from_f<bf16raw>(v[2]) | (uint32_t(from_f<bf16raw>(v[3])) << 16);
+                *reinterpret_cast<uint2 *>(dst) = make_uint2(lo, hi);
             }
         }
     }
@@ -435,12 +448,19 @@ __global__ __launch_bounds__(kThreads) void wgrad_f32_k(
                     tg.TW, dstride, tg.fdtr, tg.TR);
         }
     };
+    // this lane's first pixel slot (K-step ks = wave) and its row and
+    // column in the tile; later K-steps move 16 slots on.  Window addresses
+    // are relative to the tile's window, the same for every tile (the
+    // column origin is even).
+    const int Kh = (-K) >> 1; // floor(-K / 2)
+    const int p_first = wave * 4 + kq;
+    const int pr_first = static_cast<int>(fdiv(p_first, tg.fdw));
+    const int pc_first = p_first - pr_first * tg.TW;
     int t = b;
     if (t < tg.ntiles)
         stage(tile_of(t, tg, sh));
     for (; t < tg.ntiles; t += gridDim.x) {
         const TileOrigin o = tile_of(t, tg, sh);
-        const ShearTile tl = window_of(o, tg, K);
         __syncthreads();
         px.commit(xs);
         pd.commit(dys);
@@ -450,15 +470,13 @@ __global__ __launch_bounds__(kThreads) void wgrad_f32_k(
             stage(tile_of(tn, tg, sh));
         const int nslot = o.rows * tg.TW;
         const int nks = (nslot + 3) / 4;
+        int p = p_first, pr = pr_first, pc = pc_first;
         for (int ks = wave; ks < nks; ks += kWaves) {
-            const int p = ks * 4 + kq;
-            const int pr = static_cast<int>(fdiv(p, tg.fdw));
-            const int pc = p - pr * tg.TW;
             const bool pv = pr < o.rows && pc < o.cols;
             // reads issued unconditionally (clamped addresses), then masked
             float a = dys[(pv && arow) ? m * dstride + p : 0];
             a = (pv && arow) ? a : 0.f;
-            const int centre = pv ? tl.addr(o.r0 + pr, o.c0 + pc) : 0;
+            const int centre = pv ? (pc + K) * tg.P + pr + K - ((pc >> 1) - Kh) : 0;
             float bx[NT];
 #pragma unroll
             for (int j = 0; j < NT; ++j)
@@ -467,6 +485,12 @@ __global__ __launch_bounds__(kThreads) void wgrad_f32_k(
             for (int j = 0; j < NT; ++j) {
                 const float bv = !pv ? 0.f : (kind[j] == 0 ? bx[j] : (kind[j] == 1 ? 1.f : 0.f));
                 acc[j] = __builtin_amdgcn_mfma_f32_16x16x4f32(a, bv, acc[j], 0, 0, 0);
+            }
+            p += 4 * kWaves;
+            pc += 4 * kWaves;
+            while (pc >= tg.TW) {
+                pc -= tg.TW;
+                ++pr;
             }
         }
     }
@@ -619,7 +643,8 @@ bool smallc_fwd_ok(const ConvShape &sh)
         return false;
     const ConvShape e = fwd_view(sh);
     const Tiling tg = make_tiling(e, kFwdTarget);
-    return fwd_lds(e, tg) <= kLdsLimit && shear_depth(e, tg, nch) > 0;
+    return fwd_lds(e, tg) <= kLdsLimit && shear_depth(e, tg, nch) > 0 &&
+           tg.TR * tg.TW <= kFwdMT * kWaves * 16 && tg.TW < (1 << 15) && tg.TR < (1 << 15);
 }
 
 namespace {
@@ -654,6 +679,7 @@ hipError_t smallc_fwd_t(const TT *x, const TT *w, const TT *b, TT *y, const Conv
     if (sh.k == 1) {
         if (KS <= 2) HEX_FWD_SC_U(1, 2);
         else if (KS <= 4) HEX_FWD_SC_U(1, 4);
+        else if (KS <= 6) HEX_FWD_SC_U(1, 6);
         else if (KS <= 8) HEX_FWD_SC_U(1, 8);
         else HEX_FWD_SC_U(1, 16);
     } else {
