@@ -17,9 +17,12 @@
 // ring shifts by one.  Every dy element is read from HBM once per plane
 // chunk (plus the 2kz planes a chunk shares with its neighbours).
 //
-// Thread = (column, strip of R = 2 rows) of the band; the weights sit in
-// LDS and are read with wave-uniform addresses.  The next plane is loaded
-// into registers while the current one is computed.  One plane ahead, and
+// Thread = (column, strip of R = 2 rows) of the band; the weights of an
+// output channel are read with scalar loads (block-uniform addresses): read
+// from LDS, even as broadcasts, they took two thirds of the LDS bandwidth
+// that bounds the channel loop (c6 data gradient 110 -> 89 us).  The next
+// plane is loaded into registers while the current one is computed.  One
+// plane ahead, and
 // at most 8 staged window rows per thread (the block takes extra threads,
 // idle in the products, to get there), keep the kernel at about 90
 // registers: five waves per SIMD instead of two with two planes ahead of 12
@@ -54,12 +57,6 @@ __global__ __launch_bounds__(kMaxThreads3) void bwd_data3d_smallc_k(
     constexpr int T = num_taps(K);
     constexpr int Z = 2 * KZ + 1;
     extern __shared__ float ds3[];
-    // weights staged once per block, [co][ci][s][t'] with t' the reflected
-    // tap, each (co, ci) row padded to WROW floats (16-byte aligned rows,
-    // read as wave-uniform 16-byte LDS reads: LDS reads complete in order,
-    // so the waits in the channel loop count them exactly, where scalar
-    // loads -- which may complete out of order -- would force a full wait)
-    constexpr int WROW = (Z * T + 3) / 4 * 4;
     const int W = sh.W, H = sh.H, D = sh.D, Co = sh.Co;
     const size_t HW = static_cast<size_t>(H) * W;
 
@@ -73,12 +70,6 @@ __global__ __launch_bounds__(kMaxThreads3) void bwd_data3d_smallc_k(
     const int e_lo = chunk * a.EC, e_hi = min(D, e_lo + a.EC);
     const int dlo = max(0, e_lo - KZ), dhi = min(D, e_hi + KZ);
 
-    float *wl = ds3 + Co * a.CS;
-    for (int e = threadIdx.x; e < Co * CI * WROW; e += blockDim.x) {
-        const int row = e / WROW, q = e - row * WROW; // row = co * CI + ci
-        const int s = q / T, tr = q - s * T;
-        wl[e] = q < Z * T ? w[(static_cast<size_t>(row) * Z + s) * T + (T - 1 - tr)] : 0.f;
-    }
     const ShearTile tl{r0 - K, -K, a.TR + 2 * K, W + 2 * K, a.P, a.CS};
     const int c = threadIdx.x % W, strip = threadIdx.x / W;
     const bool active = strip * R < rows; // threadIdx.x < W * ceil(TR / R)
@@ -156,10 +147,10 @@ __global__ __launch_bounds__(kMaxThreads3) void bwd_data3d_smallc_k(
                             const int tr = t0 + u; // position in the reflected row
 #pragma unroll
                             for (int ci = 0; ci < CI; ++ci) {
-                                const float *wc = wl + (co * CI + ci) * WROW;
+                                const float *wc = w + static_cast<size_t>(co * CI + ci) * Z * T;
 #pragma unroll
                                 for (int s = 0; s < Z; ++s) {
-                                    const float wv = wc[s * T + tr];
+                                    const float wv = wc[s * T + (T - 1 - tr)];
 #pragma unroll
                                     for (int r = 0; r < R; ++r)
                                         acc[s][ci][r] += wv * v[r + u];
@@ -218,10 +209,7 @@ Bwd3Plan plan_bwd3(const ConvShape &sh)
     a.P = a.TR + 2 * K + 1;
     a.CS = (sh.W + 2 * K) * a.P;
     a.fdlr = make_fastdiv(static_cast<uint32_t>(a.TR + 2 * K));
-    const int Z = 2 * sh.kz + 1;
-    const int wrow = (Z * sh.T + 3) / 4 * 4;
-    pl.lds = sizeof(float) * (static_cast<size_t>(sh.Co) * a.CS +
-                              static_cast<size_t>(sh.Co) * sh.Ci * wrow);
+    pl.lds = sizeof(float) * static_cast<size_t>(sh.Co) * a.CS;
     if (pl.lds > kLds3)
         return pl;
     // staging rows per thread (ShearPrefetch): one 4-column group per thread
