@@ -345,6 +345,8 @@ SWEEP = [
     (1, 2, 2, 2, 9, 4, 2), (3, 3, 24, 37, 8, 2, 1), (1, 2, 70, 5, 256, 1, 1),
     (2, 48, 40, 11, 32, 2, 1), (3, 2, 20, 13, 68, 2, 1), (2, 1, 24, 9, 8, 1, 1),
     (1, 2, 16, 5, 12, 2, 1),
+    # small-channel forward with a 6-step contraction (3 x 7 taps), ragged rows
+    (2, 3, 8, 10, 12, 1, 1), (1, 3, 16, 11, 40, 1, 1),
     # wide bf16 matrix-core path: registers (k=1: 32 and 64 channels, k=2: 32),
     # LDS-resident weights (long contractions), several channel chunks,
     # partial last tiles, narrow and wide rows
