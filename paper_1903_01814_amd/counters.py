@@ -39,6 +39,7 @@ import glob
 import os
 import subprocess
 import sys
+import tempfile
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 sys.path.insert(0, ROOT)
@@ -254,7 +255,8 @@ def main():
     q.add_argument("--config", required=True, choices=["c2", "c3", "c4", "c5", "c6"])
     q.add_argument("--op", required=True, help="op of the workload, as bench.py names it")
     q.add_argument("--kernel", required=True, help="kernel base name, as bench.py reports it")
-    q.add_argument("--out-dir", default=os.path.join(ROOT, "gpurun_out", "pmc"))
+    q.add_argument("--out-dir", default=os.path.join(tempfile.gettempdir(), "hexconv_pmc"),
+                   help="where rocprofv3 writes its raw CSVs")
     q.add_argument("--steps", type=int, default=3)
     q.add_argument("--dest", default=os.path.join(ROOT, "profiles"))
     q.add_argument("--reuse", action="store_true",
