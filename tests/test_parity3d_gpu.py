@@ -101,6 +101,8 @@ CASES = [
     (2, 2, 9, 7, 20, 24, 2, 1, 1, 1), (1, 1, 6, 5, 12, 12, 1, 0, 1, 1),
     (1, 2, 33, 9, 8, 16, 1, 2, 1, 1), (1, 1, 8, 4, 10, 72, 1, 1, 1, 1),
     (1, 2, 5, 6, 13, 20, 1, 1, 1, 1),
+    # 32 output channels at W = 32: the block grows to 448 staging threads
+    (1, 2, 32, 6, 11, 32, 1, 1, 1, 1),
 ]
 
 
