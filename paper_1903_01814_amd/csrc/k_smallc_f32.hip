@@ -147,9 +147,9 @@ template <int U> struct PlainPrefetch {
 template <typename TT, int K, int KS, int U, bool D3>
 __global__ __launch_bounds__(kThreads) void fwd_smallc_k(
     const TT *__restrict__ x, const TT *__restrict__ w, const TT *__restrict__ bias,
-    TT *__restrict__ y, ConvShape sh, int relu, Tiling tg, int vec4)
+    TT *__restrict__ y, ConvShape sh, int relu, Tiling tg)
 {
-    (void)vec4; // W % 4 == 0 (smallc_fwd_ok)
+    // W % 4 == 0 (smallc_fwd_ok): every 4-pixel group of a tile row is whole
     constexpr int T = num_taps(K);
     extern __shared__ float xs[];
     const int NCH = D3 ? sh.Ci * sh.Z : sh.Ci; // staged channels
@@ -664,10 +664,10 @@ hipError_t smallc_fwd_t(const TT *x, const TT *w, const TT *b, TT *y, const Conv
     do {                                                                                     \
         if (d3)                                                                              \
             HEX_LAUNCH((fwd_smallc_k<TT, KV, KSV, UV, true>), grid, dim3(kThreads), lds, st, \
-                       x, w, b, y, sh, relu ? 1 : 0, tg, 1);                                 \
+                       x, w, b, y, sh, relu ? 1 : 0, tg);                                 \
         else                                                                                 \
             HEX_LAUNCH((fwd_smallc_k<TT, KV, KSV, UV, false>), grid, dim3(kThreads), lds,    \
-                       st, x, w, b, y, sh, relu ? 1 : 0, tg, 1);                             \
+                       st, x, w, b, y, sh, relu ? 1 : 0, tg);                             \
     } while (0)
 #define HEX_FWD_SC_U(KV, KSV)                                                                \
     do {                                                                                     \
