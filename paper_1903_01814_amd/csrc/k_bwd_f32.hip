@@ -177,8 +177,9 @@ __global__ __launch_bounds__(kThreads) void bwd_smallc_k(
     const bool dxrole = wave < kDwWaves;
 
     // reflected weights (at most 3 per thread: (C_out + 1) * C_in * T <= 33 *
-    // 2 * 19 < 3 * kThreads), read before the tile loads so that waiting for
-    // them does not wait for the tiles
+    // 38 < 3 * kThreads, from C_out <= 32 and C_in * T + 1 <= 64), read
+    // before the tile loads so that waiting for them does not wait for the
+    // tiles
     const int nwl = (Co + 1) * CI * T;
     float wreg[3];
 #pragma unroll
@@ -555,11 +556,13 @@ hipError_t bwd_fused_t(const TT *x, const TT *dy, const TT *w, TT *dx, float *dw
             launch_bwd<TT, 1, 1, 1>(MT, U, bt, sh, lds, st, x, dy, w, dx, part, do_dx); // J + 1 = 8
         else
             launch_bwd<TT, 1, 2, 1>(MT, U, bt, sh, lds, st, x, dy, w, dx, part, do_dx); // 15
-    } else {
+    } else if (sh.k == 2) {
         if (sh.Ci == 1)
             launch_bwd<TT, 2, 1, 2>(MT, U, bt, sh, lds, st, x, dy, w, dx, part, do_dx); // 20
         else
             launch_bwd<TT, 2, 2, 4>(MT, U, bt, sh, lds, st, x, dy, w, dx, part, do_dx); // 39
+    } else {
+        launch_bwd<TT, 3, 1, 4>(MT, U, bt, sh, lds, st, x, dy, w, dx, part, do_dx); // 38
     }
     hipError_t e = hipGetLastError();
     if (e != hipSuccess)
@@ -571,7 +574,7 @@ hipError_t bwd_fused_t(const TT *x, const TT *dy, const TT *w, TT *dx, float *dw
 
 bool smallc_bwd_fused_ok(const ConvShape &sh, Dtype d)
 {
-    if (sh.s != 1 || (sh.k != 1 && sh.k != 2) || sh.Ci > 2 || sh.Co > 32 || sh.W % 4 != 0 ||
+    if (sh.s != 1 || sh.k < 1 || sh.k > 3 || sh.Ci > 2 || sh.Co > 32 || sh.W % 4 != 0 ||
         sh.W > kDxThreads || sh.Ci * sh.T + 1 > 64)
         return false;
     const BwdTiling bt = bwd_tiling(sh);

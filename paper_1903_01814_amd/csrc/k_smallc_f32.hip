@@ -639,7 +639,7 @@ int bwd_ic_chunk(const ConvShape &sh, const Tiling &tg)
 bool smallc_fwd_ok(const ConvShape &sh)
 {
     const int nch = sh.Ci * sh.Z;
-    if (sh.s != 1 || (sh.k != 1 && sh.k != 2) || nch * sh.T > 64 || sh.W % 4 != 0)
+    if (sh.s != 1 || sh.k < 1 || sh.k > 3 || nch * sh.T > 64 || sh.W % 4 != 0)
         return false;
     const ConvShape e = fwd_view(sh);
     const Tiling tg = make_tiling(e, kFwdTarget);
@@ -682,10 +682,12 @@ hipError_t smallc_fwd_t(const TT *x, const TT *w, const TT *b, TT *y, const Conv
         else if (KS <= 6) HEX_FWD_SC_U(1, 6);
         else if (KS <= 8) HEX_FWD_SC_U(1, 8);
         else HEX_FWD_SC_U(1, 16);
-    } else {
+    } else if (sh.k == 2) {
         if (KS <= 5) HEX_FWD_SC_U(2, 5);
         else if (KS <= 10) HEX_FWD_SC_U(2, 10);
         else HEX_FWD_SC_U(2, 16);
+    } else {
+        HEX_FWD_SC_U(3, 10); // 37 taps of one input channel (nch * T <= 64)
     }
 #undef HEX_FWD_SC_U
 #undef HEX_FWD_SC
@@ -705,7 +707,7 @@ hipError_t smallc_fwd(const void *x, const void *w, const void *b, void *y, cons
 
 bool smallc_f32_bwd_data_ok(const ConvShape &sh)
 {
-    return sh.s == 1 && (sh.k == 1 || sh.k == 2) && sh.Ci <= 4 &&
+    return sh.s == 1 && sh.k >= 1 && sh.k <= 3 && sh.Ci <= 4 &&
            shear_bytes(sh, bwd_tiling(sh), 1) <= kLdsLimit;
 }
 
@@ -720,8 +722,11 @@ hipError_t smallc_f32_bwd_data(const float *dy, const float *w, float *dx, const
     if (sh.k == 1)
         HEX_LAUNCH((bwd_data_f32_k<1, kBwdR>), grid, dim3(kThreads), lds, st, dy, w, dx,
                            sh, tg, ic_chunk, vec4);
-    else
+    else if (sh.k == 2)
         HEX_LAUNCH((bwd_data_f32_k<2, kBwdR>), grid, dim3(kThreads), lds, st, dy, w, dx,
+                           sh, tg, ic_chunk, vec4);
+    else
+        HEX_LAUNCH((bwd_data_f32_k<3, kBwdR>), grid, dim3(kThreads), lds, st, dy, w, dx,
                            sh, tg, ic_chunk, vec4);
     return hipGetLastError();
 }
@@ -741,7 +746,7 @@ bool smallc_f32_wgrad_ok(const ConvShape &sh0)
 {
     const ConvShape sh = fwd_view(sh0);
     const int nch = sh.Ci * sh.Z;
-    if (sh.s != 1 || (sh.k != 1 && sh.k != 2) || nch * sh.T + 1 > 64 || sh.W % 4 != 0)
+    if (sh.s != 1 || sh.k < 1 || sh.k > 3 || nch * sh.T + 1 > 64 || sh.W % 4 != 0)
         return false;
     const Tiling tg = make_tiling(sh, kWgradTarget);
     return wgrad_lds(sh, tg) <= kLdsLimit && shear_depth(sh, tg, nch) > 0 &&
@@ -796,10 +801,12 @@ hipError_t smallc_f32_wgrad(const float *x, const float *dy, float *dw, float *d
         if (NT == 1) HEX_WG_UX(1, 1);
         else if (NT == 2) HEX_WG_UX(1, 2);
         else HEX_WG_UX(1, 4);
-    } else {
+    } else if (sh.k == 2) {
         if (NT == 1) HEX_WG_UX(2, 1);
         else if (NT == 2) HEX_WG_UX(2, 2);
         else HEX_WG_UX(2, 4);
+    } else {
+        HEX_WG_UX(3, 4); // 37 taps of one input channel plus the bias column
     }
 #undef HEX_WG_UX
 #undef HEX_WG_UD

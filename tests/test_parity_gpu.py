@@ -347,6 +347,11 @@ SWEEP = [
     (1, 2, 16, 5, 12, 2, 1),
     # small-channel forward with a 6-step contraction (3 x 7 taps), ragged rows
     (2, 3, 8, 10, 12, 1, 1), (1, 3, 16, 11, 40, 1, 1),
+    # small-channel kernels at k = 3 (37 taps): forward, data and weight gradient
+    # and the fused backward; 32 output channels; 3 input channels (fast data
+    # gradient only)
+    (2, 1, 16, 13, 20, 3, 1), (1, 1, 32, 9, 44, 3, 1), (3, 1, 8, 40, 40, 3, 1),
+    (1, 3, 5, 10, 12, 3, 1),
     # wide bf16 matrix-core path: registers (k=1: 32 and 64 channels, k=2: 32),
     # LDS-resident weights (long contractions), several channel chunks,
     # partial last tiles, narrow and wide rows
@@ -589,7 +594,7 @@ def test_specialised_matches_generic(dt, monkeypatch):
     parity tolerance on the same inputs."""
     rng = np.random.default_rng(11)
     for (N, Ci, Co, H, W, k) in [(3, 1, 16, 40, 40, 2), (2, 16, 32, 24, 24, 2),
-                                 (1, 64, 64, 32, 128, 1)]:
+                                 (1, 64, 64, 32, 128, 1), (2, 1, 16, 40, 40, 3)]:
         T = oracle.num_taps(k)
         x = gen.round_to(rng.normal(size=(N, Ci, H, W)), dt)
         w = gen.round_to(rng.normal(size=(Co, Ci, T)) / np.sqrt(Ci * T), dt)
