@@ -93,6 +93,8 @@ CASES = [
     (2, 1, 5, 9, 12, 16, 1, 1, 1, 2), (1, 1, 3, 10, 8, 8, 1, 1, 1, 3),
     (1, 1, 7, 6, 12, 12, 1, 4, 1, 1), (1, 3, 20, 4, 12, 16, 2, 0, 1, 1),
     (3, 2, 17, 5, 10, 20, 1, 1, 1, 2), (2, 1, 4, 1, 12, 8, 1, 2, 1, 1),
+    # k = 3 with a one-plane window (37 taps of one input channel)
+    (2, 1, 8, 4, 12, 16, 3, 0, 1, 1),
     # data gradient walking the planes of a sample with a register ring of
     # the 2kz + 1 dx planes (float32, plane and in-plane stride 1, 1-2 input
     # channels): k = 2 with two input channels, kz = 0, kz = 2 over nine
