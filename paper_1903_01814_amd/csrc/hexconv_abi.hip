@@ -188,24 +188,29 @@ bool force_generic()
 
 // Weight-gradient kernel family for a shape; the workspace query and the
 // call must agree, so both go through this choice.
-enum class WgradPath { Generic, SmallF32, Bf16Mfma32, Bf16Mfma };
+enum class WgradPath { Generic, Small, Bf16Mfma32, Bf16Mfma };
 
 WgradPath wgrad_path(const ConvShape &sh, Dtype d)
 {
     if (force_generic())
         return WgradPath::Generic;
-    if (d == hexk::F32 && hexk::smallc_f32_wgrad_ok(sh))
-        return WgradPath::SmallF32;
-    if (d == hexk::BF16) {
-        // several passes re-read x once per pass: then the single-pass
-        // kernel, where it applies, is the faster one
-        const int passes = hexk::bf16_wgrad32_passes(sh);
-        if (passes == 1 || (passes > 1 && !hexk::bf16_wgrad_ok(sh)))
-            return WgradPath::Bf16Mfma32;
-    }
-    if (d == hexk::BF16 && hexk::bf16_wgrad_ok(sh))
+    const bool small = hexk::smallc_wgrad_ok(sh);
+    if (d == hexk::F32)
+        return small ? WgradPath::Small : WgradPath::Generic;
+    // bf16 with few input channels: the small-channel kernel stages x once
+    // per 16 output channels, so it wins only for one such block at k <= 2
+    // (1 -> 16 channels, 40x40, N = 256: 27 -> 18 us at k = 1, 26 -> 23 us
+    // at k = 2; 32 or 64 output channels and k = 3 favour the bf16 kernels)
+    if (small && sh.Co <= 16 && sh.k <= 2)
+        return WgradPath::Small;
+    // several passes re-read x once per pass: then the single-pass kernel,
+    // where it applies, is the faster one
+    const int passes = hexk::bf16_wgrad32_passes(sh);
+    if (passes == 1 || (passes > 1 && !hexk::bf16_wgrad_ok(sh)))
+        return WgradPath::Bf16Mfma32;
+    if (hexk::bf16_wgrad_ok(sh))
         return WgradPath::Bf16Mfma;
-    return WgradPath::Generic;
+    return small ? WgradPath::Small : WgradPath::Generic;
 }
 
 // Fused data + weight gradient (hexconv_bwd) for this shape?
@@ -217,8 +222,8 @@ bool bwd_fused(const ConvShape &sh, Dtype d)
 size_t wgrad_workspace(const ConvShape &sh, Dtype d)
 {
     switch (wgrad_path(sh, d)) {
-    case WgradPath::SmallF32:
-        return hexk::smallc_f32_wgrad_workspace(sh);
+    case WgradPath::Small:
+        return hexk::smallc_wgrad_workspace(sh);
     case WgradPath::Bf16Mfma32:
         return hexk::bf16_wgrad32_workspace(sh);
     case WgradPath::Bf16Mfma:
@@ -367,12 +372,13 @@ int hexconv_bwd_data(const void *dy, const void *w, void *dx, int N, int C_in, i
     hipStream_t st = static_cast<hipStream_t>(stream);
     const Dtype d = static_cast<Dtype>(dt);
     if (!force_generic() && sh.Ho > 0) {
-        if (d == hexk::F32 && hexk::smallc_f32_bwd_data_ok(sh))
-            return launched(hexk::smallc_f32_bwd_data(static_cast<const float *>(dy),
-                                                      static_cast<const float *>(w),
-                                                      static_cast<float *>(dx), sh, st));
+        // bf16 with 32 or more output channels: the matrix-core kernel
+        // before the small-channel one (1 -> 64 channels, 48x48, k = 2:
+        // 29 against 59 us)
         if (d == hexk::BF16 && hexk::bf16_wide_ok(sh, sh.Co, sh.Ci))
             return launched(hexk::bf16_wide_conv(dy, w, nullptr, dx, sh, true, false, st));
+        if (hexk::smallc_bwd_data_ok(sh))
+            return launched(hexk::smallc_bwd_data(dy, w, dx, sh, d, st));
         if (d == hexk::BF16 && hexk::bf16_gen_dgrad_ok(sh))
             return launched(hexk::bf16_gen_dgrad(dy, w, dx, sh, st));
     }
@@ -413,10 +419,8 @@ int hexconv_bwd_weight(const void *x, const void *dy, float *dw, float *db, void
     if (empty)
         return launched(hexk::fill_zero_f32(dw, db, sh, st));
     switch (wgrad_path(sh, d)) {
-    case WgradPath::SmallF32:
-        return launched(hexk::smallc_f32_wgrad(static_cast<const float *>(x),
-                                               static_cast<const float *>(dy), dw, db, ws, sh,
-                                               st));
+    case WgradPath::Small:
+        return launched(hexk::smallc_wgrad(x, dy, dw, db, ws, sh, d, st));
     case WgradPath::Bf16Mfma32:
         return launched(hexk::bf16_wgrad32(x, dy, dw, db, ws, sh, st));
     case WgradPath::Bf16Mfma:
@@ -596,11 +600,9 @@ int hexconv3d_bwd_data(const void *dy, const void *w, void *dx, int N, int C_in,
         return rc;
     if (dy == nullptr && sh.Ho > 0)
         return HEX_ERR_INVALID_ARG;
-    if (!force_generic() && sh.Ho > 0 && dt == HEX_F32 && hexk::smallc3d_f32_bwd_data_ok(sh))
-        return launched(hexk::smallc3d_f32_bwd_data(static_cast<const float *>(dy),
-                                                    static_cast<const float *>(w),
-                                                    static_cast<float *>(dx), sh,
-                                                    static_cast<hipStream_t>(stream)));
+    if (!force_generic() && sh.Ho > 0 && hexk::smallc3d_bwd_data_ok(sh))
+        return launched(hexk::smallc3d_bwd_data(dy, w, dx, sh, static_cast<Dtype>(dt),
+                                                static_cast<hipStream_t>(stream)));
     if (!hexk::conv_bwd_data_generic_ok(sh))
         return HEX_ERR_UNSUPPORTED;
     return launched(hexk::conv_bwd_data_generic(dy, w, dx, sh, static_cast<Dtype>(dt),
@@ -608,17 +610,17 @@ int hexconv3d_bwd_data(const void *dy, const void *w, void *dx, int N, int C_in,
 }
 
 namespace {
-// 3-D weight gradient: the small-channel fp32 kernel with the planes around
-// each output plane staged as channels where it applies, else the generic one
-bool wgrad3d_smallc(const ConvShape &sh, hex_dtype dt)
+// 3-D weight gradient: the small-channel kernel with the planes around each
+// output plane staged as channels where it applies, else the generic one
+bool wgrad3d_smallc(const ConvShape &sh)
 {
-    return !force_generic() && dt == HEX_F32 && hexk::smallc_f32_wgrad_ok(sh);
+    return !force_generic() && hexk::smallc_wgrad_ok(sh);
 }
 
-size_t wgrad3d_workspace(const ConvShape &sh, hex_dtype dt)
+size_t wgrad3d_workspace(const ConvShape &sh)
 {
-    return wgrad3d_smallc(sh, dt) ? hexk::smallc_f32_wgrad_workspace(sh)
-                                  : hexk::wgrad_generic_workspace(sh);
+    return wgrad3d_smallc(sh) ? hexk::smallc_wgrad_workspace(sh)
+                              : hexk::wgrad_generic_workspace(sh);
 }
 } // namespace
 
@@ -630,7 +632,7 @@ size_t hexconv3d_bwd_weight_workspace(int N, int C_in, int C_out, int D, int H, 
         return 0;
     if (N == 0 || sh.Ho == 0)
         return 0;
-    return wgrad3d_workspace(sh, dt);
+    return wgrad3d_workspace(sh);
 }
 
 int hexconv3d_bwd_weight(const void *x, const void *dy, float *dw, float *db, void *ws,
@@ -646,15 +648,15 @@ int hexconv3d_bwd_weight(const void *x, const void *dy, float *dw, float *db, vo
     const bool empty = (N == 0 || sh.Ho == 0);
     if (!empty && (x == nullptr || dy == nullptr))
         return HEX_ERR_INVALID_ARG;
-    const size_t need = empty ? 0 : wgrad3d_workspace(sh, dt);
+    const size_t need = empty ? 0 : wgrad3d_workspace(sh);
     if (need > 0 && (ws == nullptr || ws_bytes < need))
         return HEX_ERR_INVALID_ARG;
     hipStream_t st = static_cast<hipStream_t>(stream);
     if (empty)
         return launched(hexk::fill_zero_f32(dw, db, sh, st));
-    if (wgrad3d_smallc(sh, dt))
-        return launched(hexk::smallc_f32_wgrad(static_cast<const float *>(x),
-                                               static_cast<const float *>(dy), dw, db, ws, sh, st));
+    if (wgrad3d_smallc(sh))
+        return launched(
+            hexk::smallc_wgrad(x, dy, dw, db, ws, sh, static_cast<Dtype>(dt), st));
     return launched(hexk::wgrad_generic(x, dy, dw, db, ws, sh, static_cast<Dtype>(dt), st));
 }
 

@@ -89,8 +89,8 @@ __device__ __forceinline__ ShearTile window_of(const TileOrigin &o, const Tiling
 // registers: dst[ch * dstride + pr * TW + pc].  Work split: one 4-column group
 // per thread, (channel, row) pairs strided by blockDim / groups.  Requires
 // W % 4 == 0 (so TW, the tile's columns and every group of 4 lie inside the
-// row): each item is one 16-byte load and, dstride being even, two 8-byte LDS
-// writes.
+// row): each item is one 16-byte (fp32) or 8-byte (bf16) load and, dstride
+// being even, two 8-byte LDS writes.
 template <int U> struct PlainPrefetch {
     float v[U][4];
     int da[U];
@@ -102,8 +102,9 @@ template <int U> struct PlainPrefetch {
         return rstep > 0 ? (nch * TR + rstep - 1) / rstep : 1 << 30;
     }
 
-    __device__ __forceinline__ void load(const float *__restrict__ src, size_t src_plane,
-                                         int nch, int W, const TileOrigin &o, int TW, int dstride,
+    template <typename T>
+    __device__ __forceinline__ void load(const T *__restrict__ src, size_t src_plane, int nch,
+                                         int W, const TileOrigin &o, int TW, int dstride,
                                          const FastDiv &fdtr, int TR)
     {
         const int ng = groups(TW);
@@ -119,9 +120,9 @@ template <int U> struct PlainPrefetch {
             const bool ok = fr0 < rstep && fr < total && pr < o.rows && pc < o.cols;
             da[u] = ok ? ch * dstride + pr * TW + pc : -1;
             // items without data read the plane's first group (always valid)
-            const float *p =
+            const T *p =
                 src + (ok ? ch * src_plane + static_cast<size_t>(o.r0 + pr) * W + o.c0 + pc : 0);
-            Vec4Load<float>::load(p, v[u]);
+            Vec4Load<T>::load(p, v[u]);
         }
     }
 
@@ -310,10 +311,10 @@ __global__ __launch_bounds__(kThreads) void fwd_smallc_k(
 // dx[n][oc][p] = sum_ic sum_u w[ic][oc][T-1-u] * dy[n][ic][p + tap u]
 // (ic runs over C_out, oc over C_in).  Thread = column c, rows
 // [strip*R, strip*R + R) of the tile; one output channel per block.
-template <int K, int R>
+template <typename TT, int K, int R>
 __global__ __launch_bounds__(kThreads) void bwd_data_f32_k(
-    const float *__restrict__ dy, const float *__restrict__ w, float *__restrict__ dx,
-    ConvShape sh, Tiling tg, int ic_chunk, int vec4)
+    const TT *__restrict__ dy, const TT *__restrict__ w, TT *__restrict__ dx, ConvShape sh,
+    Tiling tg, int ic_chunk, int vec4)
 {
     constexpr int T = num_taps(K);
     extern __shared__ float ds_[];
@@ -346,7 +347,7 @@ __global__ __launch_bounds__(kThreads) void bwd_data_f32_k(
             continue;
         for (int icl = 0; icl < icn; ++icl) {
             const int ic = ic0 + icl;
-            const float *wr = w + (static_cast<size_t>(ic) * OCN + oc) * T;
+            const typename WRow<TT>::type wr(w, static_cast<uint32_t>((ic * OCN + oc) * T));
             const float *src = ds_ + icl * cs + a0;
             int t0 = 0;
 #pragma unroll
@@ -362,7 +363,7 @@ __global__ __launch_bounds__(kThreads) void bwd_data_f32_k(
 #pragma unroll
                 for (int u = 0; u < 2 * K + 1; ++u) {
                     if (u < len) {
-                        const float wv = wr[T - 1 - (t0 + u)];
+                        const float wv = wr(T - 1 - (t0 + u));
 #pragma unroll
                         for (int r = 0; r < R; ++r)
                             acc[r] += wv * v[r + u];
@@ -374,12 +375,12 @@ __global__ __launch_bounds__(kThreads) void bwd_data_f32_k(
     }
     if (!active)
         return;
-    float *dst = dx + (static_cast<size_t>(o.n) * OCN + oc) * HW + o.c0 + lc;
+    TT *dst = dx + (static_cast<size_t>(o.n) * OCN + oc) * HW + o.c0 + lc;
 #pragma unroll
     for (int r = 0; r < R; ++r) {
         const int row = strip * R + r;
         if (row < o.rows)
-            dst[static_cast<size_t>(o.r0 + row) * sh.W] = acc[r];
+            dst[static_cast<size_t>(o.r0 + row) * sh.W] = from_f<TT>(acc[r]);
     }
 }
 
@@ -388,10 +389,10 @@ __global__ __launch_bounds__(kThreads) void bwd_data_f32_k(
 // D3: three-dimensional layer, tiles over (sample, output plane) pairs with
 // the 2kz + 1 input planes around each output plane staged as channels
 // (ch = ci * Z + dz), so that column (ch, t) is dw[co][ci][dz][t].
-template <int K, int NT, int UX, int UD, bool D3>
+template <typename TT, int K, int NT, int UX, int UD, bool D3>
 __global__ __launch_bounds__(kThreads) void wgrad_f32_k(
-    const float *__restrict__ x, const float *__restrict__ dy, float *__restrict__ part,
-    ConvShape sh, Tiling tg, int dstride)
+    const TT *__restrict__ x, const TT *__restrict__ dy, float *__restrict__ part, ConvShape sh,
+    Tiling tg, int dstride)
 {
     constexpr int T = num_taps(K);
     extern __shared__ float lds[];
@@ -705,14 +706,16 @@ hipError_t smallc_fwd(const void *x, const void *w, const void *b, void *y, cons
                         static_cast<const bf16raw *>(b), static_cast<bf16raw *>(y), sh, relu, st);
 }
 
-bool smallc_f32_bwd_data_ok(const ConvShape &sh)
+bool smallc_bwd_data_ok(const ConvShape &sh)
 {
     return sh.s == 1 && sh.k >= 1 && sh.k <= 3 && sh.Ci <= 4 &&
            shear_bytes(sh, bwd_tiling(sh), 1) <= kLdsLimit;
 }
 
-hipError_t smallc_f32_bwd_data(const float *dy, const float *w, float *dx, const ConvShape &sh,
-                               hipStream_t st)
+namespace {
+template <typename TT>
+hipError_t smallc_bwd_data_t(const TT *dy, const TT *w, TT *dx, const ConvShape &sh,
+                             hipStream_t st)
 {
     const Tiling tg = bwd_tiling(sh);
     const int ic_chunk = bwd_ic_chunk(sh, tg);
@@ -720,15 +723,26 @@ hipError_t smallc_f32_bwd_data(const float *dy, const float *w, float *dx, const
     const int vec4 = (sh.W % 4 == 0) ? 1 : 0;
     dim3 grid(tg.ntiles, sh.Ci);
     if (sh.k == 1)
-        HEX_LAUNCH((bwd_data_f32_k<1, kBwdR>), grid, dim3(kThreads), lds, st, dy, w, dx,
-                           sh, tg, ic_chunk, vec4);
+        HEX_LAUNCH((bwd_data_f32_k<TT, 1, kBwdR>), grid, dim3(kThreads), lds, st, dy, w, dx,
+                   sh, tg, ic_chunk, vec4);
     else if (sh.k == 2)
-        HEX_LAUNCH((bwd_data_f32_k<2, kBwdR>), grid, dim3(kThreads), lds, st, dy, w, dx,
-                           sh, tg, ic_chunk, vec4);
+        HEX_LAUNCH((bwd_data_f32_k<TT, 2, kBwdR>), grid, dim3(kThreads), lds, st, dy, w, dx,
+                   sh, tg, ic_chunk, vec4);
     else
-        HEX_LAUNCH((bwd_data_f32_k<3, kBwdR>), grid, dim3(kThreads), lds, st, dy, w, dx,
-                           sh, tg, ic_chunk, vec4);
+        HEX_LAUNCH((bwd_data_f32_k<TT, 3, kBwdR>), grid, dim3(kThreads), lds, st, dy, w, dx,
+                   sh, tg, ic_chunk, vec4);
     return hipGetLastError();
+}
+} // namespace
+
+hipError_t smallc_bwd_data(const void *dy, const void *w, void *dx, const ConvShape &sh, Dtype d,
+                           hipStream_t st)
+{
+    if (d == F32)
+        return smallc_bwd_data_t(static_cast<const float *>(dy), static_cast<const float *>(w),
+                                 static_cast<float *>(dx), sh, st);
+    return smallc_bwd_data_t(static_cast<const bf16raw *>(dy), static_cast<const bf16raw *>(w),
+                             static_cast<bf16raw *>(dx), sh, st);
 }
 
 namespace {
@@ -742,7 +756,7 @@ int wgrad_grid(const ConvShape &sh, const Tiling &tg)
 
 // (2-D shapes have Z = 1 and one plane per sample; the tiles of a 3-D
 // shape are (sample, output plane) pairs: fwd_view)
-bool smallc_f32_wgrad_ok(const ConvShape &sh0)
+bool smallc_wgrad_ok(const ConvShape &sh0)
 {
     const ConvShape sh = fwd_view(sh0);
     const int nch = sh.Ci * sh.Z;
@@ -753,7 +767,7 @@ bool smallc_f32_wgrad_ok(const ConvShape &sh0)
            plain_depth(tg, 16) > 0;
 }
 
-size_t smallc_f32_wgrad_workspace(const ConvShape &sh0)
+size_t smallc_wgrad_workspace(const ConvShape &sh0)
 {
     const ConvShape sh = fwd_view(sh0);
     const Tiling tg = make_tiling(sh, kWgradTarget);
@@ -761,8 +775,10 @@ size_t smallc_f32_wgrad_workspace(const ConvShape &sh0)
            (sh.Ci * sh.Z * sh.T + 1);
 }
 
-hipError_t smallc_f32_wgrad(const float *x, const float *dy, float *dw, float *db, void *ws,
-                            const ConvShape &sh0, hipStream_t st)
+namespace {
+template <typename TT>
+hipError_t smallc_wgrad_t(const TT *x, const TT *dy, float *dw, float *db, void *ws,
+                          const ConvShape &sh0, hipStream_t st)
 {
     const ConvShape sh = fwd_view(sh0);
     const int nch = sh.Ci * sh.Z;
@@ -779,10 +795,10 @@ hipError_t smallc_f32_wgrad(const float *x, const float *dy, float *dw, float *d
 #define HEX_WG(KV, NTV, UXV, UDV)                                                            \
     do {                                                                                     \
         if (d3)                                                                              \
-            HEX_LAUNCH((wgrad_f32_k<KV, NTV, UXV, UDV, true>), grid, dim3(kThreads), lds,    \
+            HEX_LAUNCH((wgrad_f32_k<TT, KV, NTV, UXV, UDV, true>), grid, dim3(kThreads), lds,\
                        st, x, dy, part, sh, tg, dstride);                                    \
         else                                                                                 \
-            HEX_LAUNCH((wgrad_f32_k<KV, NTV, UXV, UDV, false>), grid, dim3(kThreads), lds,   \
+            HEX_LAUNCH((wgrad_f32_k<TT, KV, NTV, UXV, UDV, false>), grid, dim3(kThreads), lds,\
                        st, x, dy, part, sh, tg, dstride);                                    \
     } while (0)
 #define HEX_WG_UD(KV, NTV, UXV)                                                              \
@@ -815,6 +831,17 @@ hipError_t smallc_f32_wgrad(const float *x, const float *dy, float *dw, float *d
     if (e != hipSuccess)
         return e;
     return reduce_partials(part, nparts, sh.Co, nch * sh.T, dw, db, st);
+}
+} // namespace
+
+hipError_t smallc_wgrad(const void *x, const void *dy, float *dw, float *db, void *ws,
+                        const ConvShape &sh, Dtype d, hipStream_t st)
+{
+    if (d == F32)
+        return smallc_wgrad_t(static_cast<const float *>(x), static_cast<const float *>(dy), dw,
+                              db, ws, sh, st);
+    return smallc_wgrad_t(static_cast<const bf16raw *>(x), static_cast<const bf16raw *>(dy), dw,
+                          db, ws, sh, st);
 }
 
 } // namespace hexk

@@ -114,22 +114,24 @@ hipError_t pool_fwd_fast(const void *x, void *y, uint8_t *am, const ConvShape &s
 hipError_t pool_bwd_fast(const void *dy, const uint8_t *am, const void *relu_y, void *dx,
                          const ConvShape &sh, int mode, Dtype dt, hipStream_t st);
 
-// ---- float32, few input channels (C_in*T <= 64), stride 1 -------------
+// ---- few input channels (C_in*T <= 64), stride 1, fp32 or bf16 data,
+// fp32 arithmetic --------------------------------------------------------
 bool smallc_fwd_ok(const ConvShape &sh);
 hipError_t smallc_fwd(const void *x, const void *w, const void *b, void *y, const ConvShape &sh,
                       Dtype d, bool relu, hipStream_t st);
-bool smallc_f32_bwd_data_ok(const ConvShape &sh);
-hipError_t smallc_f32_bwd_data(const float *dy, const float *w, float *dx, const ConvShape &sh,
-                               hipStream_t st);
-// Data gradient of a 3-D layer with 1 or 2 input channels, float32, plane
-// and in-plane stride 1, k <= 2, kz <= 2, W % 4 == 0 (k_bwd3d.hip).
-bool smallc3d_f32_bwd_data_ok(const ConvShape &sh);
-hipError_t smallc3d_f32_bwd_data(const float *dy, const float *w, float *dx, const ConvShape &sh,
-                                 hipStream_t st);
-bool smallc_f32_wgrad_ok(const ConvShape &sh);
-size_t smallc_f32_wgrad_workspace(const ConvShape &sh);
-hipError_t smallc_f32_wgrad(const float *x, const float *dy, float *dw, float *db, void *ws,
-                            const ConvShape &sh, hipStream_t st);
+bool smallc_bwd_data_ok(const ConvShape &sh);
+hipError_t smallc_bwd_data(const void *dy, const void *w, void *dx, const ConvShape &sh, Dtype d,
+                           hipStream_t st);
+// Data gradient of a 3-D layer with 1 or 2 input channels, float32 or
+// bfloat16, plane and in-plane stride 1, k <= 2, kz <= 2, W % 4 == 0
+// (k_bwd3d.hip).
+bool smallc3d_bwd_data_ok(const ConvShape &sh);
+hipError_t smallc3d_bwd_data(const void *dy, const void *w, void *dx, const ConvShape &sh,
+                             Dtype d, hipStream_t st);
+bool smallc_wgrad_ok(const ConvShape &sh);
+size_t smallc_wgrad_workspace(const ConvShape &sh);
+hipError_t smallc_wgrad(const void *x, const void *dy, float *dw, float *db, void *ws,
+                        const ConvShape &sh, Dtype d, hipStream_t st);
 // both gradients in one pass over dy (C_in <= 2, C_out <= 32), fp32 or bf16
 bool smallc_bwd_fused_ok(const ConvShape &sh, Dtype d);
 size_t smallc_bwd_fused_workspace(const ConvShape &sh);

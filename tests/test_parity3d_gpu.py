@@ -105,6 +105,12 @@ CASES = [
     (1, 2, 5, 6, 13, 20, 1, 1, 1, 1),
     # 32 output channels at W = 32: the block grows to 448 staging threads
     (1, 2, 32, 6, 11, 32, 1, 1, 1, 1),
+    # more output channels than one staged window holds: two groups of 16
+    # (k = 2, W = 40), three groups of 24, 24 and 22 (kz = 2, 70 channels)
+    (2, 2, 32, 5, 12, 40, 2, 1, 1, 1), (1, 1, 70, 4, 9, 48, 1, 2, 1, 1),
+    # two input channels at k = 2, kz = 2 (weight rows of 5 x 19 values: the
+    # second channel's rows start at odd bfloat16 positions)
+    (1, 2, 5, 6, 12, 16, 2, 2, 1, 1),
 ]
 
 
