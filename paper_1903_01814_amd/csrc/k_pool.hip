@@ -149,6 +149,78 @@ __global__ __launch_bounds__(kPoolThreads) void pool_fwd_k(const TT *__restrict_
     const int halfs = (j & 1) * (S / 2);
     constexpr TapTable<K> tt;
 
+    // k = 1, stride 2, bfloat16, even W_out: a thread takes the outputs j
+    // and j + 1 (j even) of a row.  Their centres are (2i, 2j) and
+    // (2i + 1, 2j + 2), and their 14 taps lie in input columns 2j - 2 ..
+    // 2j + 3 and rows 2i - 1 .. 2i + 2: eight aligned 32-bit LDS reads (two
+    // columns each) instead of fourteen 16-bit ones, and one 32-bit store.
+    constexpr bool PAIRS = K == 1 && S == 2 && sizeof(TT) == 2;
+    const bool pairs = PAIRS && Wo % 2 == 0;
+    auto pool_pairs = [&](int g) __attribute__((always_inline)) {
+        const int npair = Wo / 2;
+        const int rpp2 = kPoolThreads / npair; // Wo <= 256: at least one row per pass
+        const int jp = threadIdx.x % npair, prow0 = threadIdx.x / npair;
+        if (prow0 >= rpp2)
+            return;
+        const int j2 = 2 * jp;
+        const int p0 = g * a.NP;
+        const int np = min(a.NP, a.nplanes - p0);
+        TT *yb = y + static_cast<size_t>(p0) * HWo;
+        uint8_t *ab = am != nullptr ? am + static_cast<size_t>(p0) * HWo : nullptr;
+        int pl = static_cast<int>(fdiv(static_cast<uint32_t>(prow0), a.fho_rows));
+        int i = prow0 - pl * Ho;
+        for (int row = prow0; row < np * Ho; row += rpp2) {
+            // word (two columns) c2 of window row rr: rows 2i - 1 + rr,
+            // columns 2j - 2 + 2 c2 and 2j - 1 + 2 c2
+            const uint32_t *wrow = reinterpret_cast<const uint32_t *>(
+                lds + pl * plane_l + (2 * i - 1 + K) * a.pitch + VEC + j2 * 2 - 2);
+            const int wp = a.pitch / 2; // words per LDS row
+            float v[4][6];
+            auto take = [&](int rr, int c2) {
+                const uint32_t q = wrow[rr * wp + c2];
+                v[rr][2 * c2] = __uint_as_float(q << 16);
+                v[rr][2 * c2 + 1] = __uint_as_float(q & 0xffff0000u);
+            };
+            take(0, 0); take(1, 0);
+            take(0, 1); take(1, 1); take(2, 1);
+            take(1, 2); take(2, 2); take(3, 2);
+            float res[2];
+            int arg[2] = {0, 0};
+#pragma unroll
+            for (int h = 0; h < 2; ++h) {
+                // centre of output j + h: window row 1 + h, column 2 + 2h
+                float best = 0.f, sum = 0.f;
+#pragma unroll
+                for (int t = 0; t < T; ++t) {
+                    const int dr = tap_drow(tt.dq[t], tt.ds[t], 0);
+                    const float val = v[1 + h + dr][2 + 2 * h + tt.dq[t]];
+                    if (MODE == 0) {
+                        if (t == 0 || val > best) {
+                            best = val;
+                            if (ARG)
+                                arg[h] = t;
+                        }
+                    } else {
+                        sum += val;
+                    }
+                }
+                res[h] = MODE == 0 ? best : sum / static_cast<float>(T);
+            }
+            const int o = row * Wo + j2; // plane-major, even
+            *reinterpret_cast<uint32_t *>(yb + o) =
+                static_cast<uint32_t>(from_f<TT>(res[0])) |
+                (static_cast<uint32_t>(from_f<TT>(res[1])) << 16);
+            if (ARG)
+                *reinterpret_cast<uint16_t *>(ab + o) =
+                    static_cast<uint16_t>(arg[0] | (arg[1] << 8));
+            i += rpp2;
+            while (i >= Ho) {
+                i -= Ho;
+                ++pl;
+            }
+        }
+    };
+
     if (blockIdx.x < ngroups)
         stg.load(x, a, blockIdx.x);
     for (int g = blockIdx.x; g < ngroups; g += gridDim.x) {
@@ -157,6 +229,12 @@ __global__ __launch_bounds__(kPoolThreads) void pool_fwd_k(const TT *__restrict_
         __syncthreads();
         if (g + static_cast<int>(gridDim.x) < ngroups)
             stg.load(x, a, g + gridDim.x);
+        if constexpr (PAIRS) {
+            if (pairs) {
+                pool_pairs(g);
+                continue;
+            }
+        }
         if (row0 < rpp) { // spare threads: only the staging and the barriers
             const int p0 = g * a.NP;
             const int np = min(a.NP, a.nplanes - p0);

@@ -508,7 +508,11 @@ def test_conv_matrix_core_any_stride(case):
                                   (3, 2, 11, 24, 3, 2), (1, 70, 8, 16, 3, 1),
                                   # strides 3 and 4 on the LDS-staged kernels
                                   (1, 3, 20, 24, 1, 3), (2, 2, 17, 32, 2, 4),
-                                  (1, 4, 30, 48, 3, 3), (2, 3, 9, 16, 0, 4)])
+                                  (1, 4, 30, 48, 3, 3), (2, 3, 9, 16, 0, 4),
+                                  # k = 1, stride 2 in bf16 takes two outputs
+                                  # per thread: odd H (the bottom border row
+                                  # is read), 12 output pairs per row
+                                  (2, 3, 13, 24, 1, 2), (1, 2, 9, 48, 1, 2)])
 def test_pool_sweep(case, mode, dt):
     N, C, H, W, k, s = case
     rng = np.random.default_rng(sum(case) + mode)
