@@ -206,15 +206,23 @@ def test_conv3d_empty_batch_and_output():
     assert np.all(dw == 0) and np.all(db == 0)
 
 
-def test_conv3d_weight_gradient_deterministic():
-    """Fixed-order partial sums: the same inputs give the same bits."""
+@pytest.mark.parametrize("dt", ["f32", "bf16"])
+def test_conv3d_gradients_deterministic(dt):
+    """Fixed-order sums: the same inputs give the same bits, for the generic
+    weight gradient (4 input channels), the small-channel one (planes staged
+    as channels) and the data gradient with output channels in groups."""
     rng = np.random.default_rng(77)
-    x = rng.normal(size=(2, 4, 6, 20, 20))
-    dy = rng.normal(size=(2, 16, 6, 20, 20))
-    a = run_bwd_weight3(x, dy, 1, 1, 1, 1, "f32")
-    b = run_bwd_weight3(x, dy, 1, 1, 1, 1, "f32")
-    np.testing.assert_array_equal(a[0], b[0])
-    np.testing.assert_array_equal(a[1], b[1])
+    for ci, co, W, k in [(4, 16, 20, 1), (1, 16, 20, 1), (2, 32, 40, 2)]:
+        x = gen.round_to(rng.normal(size=(2, ci, 6, 12, W)), dt)
+        dy = gen.round_to(rng.normal(size=(2, co, 6, 12, W)), dt)
+        w = gen.round_to(rng.normal(size=(co, ci, 3, oracle.num_taps(k))) * 0.1, dt)
+        a = run_bwd_weight3(x, dy, k, 1, 1, 1, dt)
+        b = run_bwd_weight3(x, dy, k, 1, 1, 1, dt)
+        np.testing.assert_array_equal(a[0], b[0])
+        np.testing.assert_array_equal(a[1], b[1])
+        d1 = run_bwd_data3(dy, w, k, 1, 1, 1, 6, 12, W, dt)
+        d2 = run_bwd_data3(dy, w, k, 1, 1, 1, 6, 12, W, dt)
+        np.testing.assert_array_equal(d1, d2)
 
 
 def test_c6_time_resolved_full():

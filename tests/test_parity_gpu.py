@@ -590,6 +590,19 @@ def test_deterministic_repeat():
     y1 = run_fwd(d["x"], d["w"], d["b"], cfg["k"], 1, "f32")
     y2 = run_fwd(d["x"], d["w"], d["b"], cfg["k"], 1, "f32")
     np.testing.assert_array_equal(y1, y2)
+    # bf16 camera layer: the small-channel weight gradient (one block of 16
+    # output channels) and data gradient called on their own
+    xb = gen.round_to(d["x"], "bf16")
+    dyb = gen.round_to(d["dy"], "bf16")
+    wb = gen.round_to(d["w"], "bf16")
+    a = run_bwd_weight(xb, dyb, cfg["k"], 1, "bf16")
+    b = run_bwd_weight(xb, dyb, cfg["k"], 1, "bf16")
+    np.testing.assert_array_equal(a[0], b[0])
+    np.testing.assert_array_equal(a[1], b[1])
+    H, W = d["x"].shape[2:]
+    dx1 = run_bwd_data(dyb, wb, cfg["k"], 1, H, W, "bf16")
+    dx2 = run_bwd_data(dyb, wb, cfg["k"], 1, H, W, "bf16")
+    np.testing.assert_array_equal(dx1, dx2)
 
 
 @pytest.mark.parametrize("dt", ["f32", "bf16"])
