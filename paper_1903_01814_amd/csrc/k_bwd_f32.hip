@@ -179,7 +179,7 @@ __global__ __launch_bounds__(kThreads) void bwd_smallc_k(
     // reflected weights (at most 3 per thread: (C_out + 1) * C_in * T <= 33 *
     // 38 < 3 * kThreads, from C_out <= 32 and C_in * T + 1 <= 64), read
     // before the tile loads so that waiting for them does not wait for the
-    // tiles
+    // tiles; without the data gradient w is not read (it may be NULL)
     const int nwl = (Co + 1) * CI * T;
     float wreg[3];
 #pragma unroll
@@ -187,7 +187,7 @@ __global__ __launch_bounds__(kThreads) void bwd_smallc_k(
         const int e = tid + u * kThreads;
         const int co = e / (CI * T), rem = e - co * (CI * T);
         const int ci = rem / T, t = rem - ci * T;
-        wreg[u] = (e < nwl && co < Co)
+        wreg[u] = (do_dx != 0 && e < nwl && co < Co)
                       ? to_f(w[(static_cast<size_t>(co) * CI + ci) * T + (T - 1 - t)])
                       : 0.f;
     }

@@ -84,7 +84,8 @@ def run_bwd(x, dy, w, k, s, dt, want_dx=True):
     nbytes = hx.hexconv_bwd_workspace(N, Ci, Co, H, W, k, s,
                                       hx.HEX_F32 if dt == "f32" else hx.HEX_BF16)
     ws = torch.empty(nbytes, dtype=torch.uint8, device="cuda:0") if nbytes else None
-    hx.hexconv_bwd(to_dev(x, dt), to_dev(dy, dt), to_dev(w, dt), dx, dw, db, ws, k, s)
+    wd = None if w is None else to_dev(w, dt)
+    hx.hexconv_bwd(to_dev(x, dt), to_dev(dy, dt), wd, dx, dw, db, ws, k, s)
     _sync()
     return (from_dev(dx) if want_dx else None), from_dev(dw), from_dev(db)
 
@@ -538,16 +539,22 @@ def test_pool_sweep(case, mode, dt):
 
 @pytest.mark.parametrize("dt", ["f32", "bf16"])
 def test_bwd_without_dx(dt):
-    """hexconv_bwd with dx = NULL (a first layer) still gives dw and db."""
+    """hexconv_bwd with dx = NULL (a first layer) still gives dw and db, with
+    or without w (the header lets w be NULL then, and the fused kernel must
+    not read it); hexconv_bwd_weight on the same shape takes the same kernel."""
     cfg = CFG["c2"]
     d = _conv_inputs(cfg, N=24)
     x, dy = gen.round_to(d["x"], dt), gen.round_to(d["dy"], dt)
     w = gen.round_to(d["w"], dt)
-    _, dw, db = run_bwd(x, dy, w, cfg["k"], 1, dt, want_dx=False)
     rw, rb = oracle.conv_bwd_weight(x, dy, cfg["k"], 1)
     mw, mb = oracle.conv_bwd_weight(np.abs(x), np.abs(dy), cfg["k"], 1)
-    check(dt, dw, rw, mw, "dw")
-    check(dt, db, rb, mb, "db")
+    for wv in (w, None):
+        _, dw, db = run_bwd(x, dy, wv, cfg["k"], 1, dt, want_dx=False)
+        check(dt, dw, rw, mw, "dw")
+        check(dt, db, rb, mb, "db")
+    dw, db = run_bwd_weight(x, dy, cfg["k"], 1, dt)
+    check(dt, dw, rw, mw, "dw (hexconv_bwd_weight)")
+    check(dt, db, rb, mb, "db (hexconv_bwd_weight)")
 
 
 def test_debug_mode_golden():
