@@ -1,5 +1,6 @@
-// k_smallc_f32.hip -- float32 kernels for few input channels at stride 1
-// (camera images: C_in*T <= 64).
+// k_smallc_f32.hip -- float32-arithmetic kernels for few input channels at
+// stride 1 (camera images: C_in*T <= 64); the data is float32 or bfloat16
+// (converted while it is staged, results rounded when they are stored).
 //
 // All three kernels stage their input tile (all channels, one batched pass)
 // into the sheared LDS layout of shear.h, where a hexagonal tap (dq, ds) is
@@ -21,7 +22,9 @@
 // With one or two output channels it is a matrix-vector product, so it runs
 // on the VALU: each thread owns R consecutive rows of one column; the
 // neighbourhood columns are contiguous runs in the sheared layout, read
-// once per input channel and reused by all taps of that column.
+// once per input channel and reused by all taps of that column.  The
+// weights are block-uniform and come by scalar loads (bfloat16 ones as
+// aligned 32-bit words, hexdev.h).
 //
 // Weight gradient: D[co][(ci,t)] = sum_pixels dy[co][p] * x[ci][p + tap t]
 // on the fp32 matrix cores with the pixels as the contraction index, so the
