@@ -152,9 +152,10 @@ size_t hexconv_bwd_workspace(int N, int C_in, int C_out, int H, int W, int k,
  * (written to dx) and of hexconv_bwd_weight (dw, db), for the same
  * arguments.  dx may be NULL (first layer: no data gradient); w may then be
  * NULL too.  db is nullable.  ws: at least hexconv_bwd_workspace(...) bytes.
- * Where a fused kernel exists for the shape (float32, few channels, stride
- * 1) dy is read from memory once for both results; otherwise the two
- * gradients are computed one after the other.  Every argument is checked
+ * Where a fused kernel exists for the shape (float32 or bfloat16, one or
+ * two input channels, at most 32 output channels, stride 1) dy is read from
+ * memory once for both results; otherwise the two gradients are computed one
+ * after the other.  Every argument is checked
  * before anything is enqueued.  Deterministic, like hexconv_bwd_weight.
  */
 int hexconv_bwd(const void *x, const void *dy, const void *w, void *dx,
