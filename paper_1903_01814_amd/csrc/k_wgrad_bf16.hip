@@ -17,7 +17,11 @@
 //
 // Block = 4 waves; a block owns 4 channel tiles (64 co) x NB column tiles
 // (grid.y enumerates the (co, column) groups); wave w owns column tiles
-// w, w + 4, ... of the group (NBW = NB / 4 per wave).
+// w, w + 4, ... of the group (NBW = NB / 4 per wave).  A column group's
+// columns span only a few input channels (ci-major, T taps each), and only
+// those are staged: at k = 3 with 64 input channels each of the 6 groups
+// stages 14 channels instead of 64, which also leaves room for two-row tiles
+// (16 x 64 -> 64 x 128 x 128: 721 -> 222 us).
 #include <algorithm>
 
 #include "hexdev.h"
@@ -45,6 +49,7 @@ struct WgTiling {
     int J, Jt;              // taps columns Ci*T, plus bias column
     int ncol_tiles;         // ceil(J / 16)
     int NB;                 // column tiles per block
+    int NCI;                // x channels a column group needs at most
     int mgroups, ngroups;   // grid.y = mgroups * ngroups
     int nparts;             // partial slots (= grid.x)
 };
@@ -61,8 +66,8 @@ __global__ __launch_bounds__(kThreads) void wgrad_bf16_k(
 {
     constexpr int T = num_taps(K);
     extern __shared__ __align__(16) bf16raw lds[];
-    bf16raw *xs = lds;                                       // [Ci][XCS]
-    bf16raw *ds_ = lds + static_cast<size_t>(sh.Ci) * tg.XCS; // [64][DP]
+    bf16raw *xs = lds;                                        // [NCI][XCS]
+    bf16raw *ds_ = lds + static_cast<size_t>(tg.NCI) * tg.XCS; // [64][DP]
 
     const int H = sh.H, W = sh.W, Wo = sh.Wo;
     const int S = SV ? SV : sh.s, SH = S >> 1;
@@ -74,6 +79,10 @@ __global__ __launch_bounds__(kThreads) void wgrad_bf16_k(
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     const int m = lane & 15, kq = lane >> 4;
 
+    // the columns (ci, t) of this block's column group span input channels
+    // ci_lo .. ci_lo + nci - 1: only those are staged
+    const int ci_lo = (ngp * tg.NB * 16) / T;
+    const int nci = min(tg.NCI, sh.Ci - ci_lo);
     // this lane's B columns: (ci, t) and the two parity offsets (in slots)
     int boff0[NBW], boff1[NBW], bch[NBW];
     bool bval[NBW];
@@ -85,7 +94,7 @@ __global__ __launch_bounds__(kThreads) void wgrad_bf16_k(
         const int ci = bval[j] ? col / T : 0, t = bval[j] ? col - ci * T : 0;
         int dq = 0, ds = 0;
         tap_axial(K, t, dq, ds);
-        bch[j] = ci;
+        bch[j] = bval[j] ? ci - ci_lo : 0;
         boff0[j] = tap_drow(dq, ds, 0) * tg.LCP + dq;
         boff1[j] = (tap_drow(dq, ds, S & 1) + SH) * tg.LCP + dq;
     }
@@ -109,7 +118,7 @@ __global__ __launch_bounds__(kThreads) void wgrad_bf16_k(
         {
             const int LR = S * (rows - 1) + SH + 2 * K + 1;
             const int cols8 = W / 8;          // 16-byte column groups of a row
-            const int items = sh.Ci * LR * cols8;
+            const int items = nci * LR * cols8;
             for (int it0 = threadIdx.x; it0 < items; it0 += 4 * kThreads) {
                 uint4 v[4];
                 int dst[4];
@@ -124,7 +133,7 @@ __global__ __launch_bounds__(kThreads) void wgrad_bf16_k(
                     const bool ok = live && r >= 0 && r < H;
                     dst[u] = live ? ci * tg.XCS + rr * tg.LCP + kXO + 8 * g : -1;
                     const uint4 q = *reinterpret_cast<const uint4 *>(
-                        x + (ok ? (static_cast<size_t>(n) * sh.Ci + ci) * HW + static_cast<size_t>(r) * W + 8 * g
+                        x + (ok ? (static_cast<size_t>(n) * sh.Ci + ci_lo + ci) * HW + static_cast<size_t>(r) * W + 8 * g
                                 : 0));
                     v[u] = ok ? q : make_uint4(0, 0, 0, 0);
                 }
@@ -133,7 +142,7 @@ __global__ __launch_bounds__(kThreads) void wgrad_bf16_k(
                     if (dst[u] >= 0)
                         *reinterpret_cast<uint4 *>(xs + dst[u]) = v[u];
             }
-            const int hitems = sh.Ci * LR * 2 * K;
+            const int hitems = nci * LR * 2 * K;
             for (int e = threadIdx.x; e < hitems; e += kThreads) {
                 const int side = e % (2 * K);
                 const int rest = e / (2 * K);
@@ -253,12 +262,19 @@ constexpr int kWgBlocks = 512; // persistent blocks (x grid.y groups)
 // x window rows of a tile of TR output rows
 int wg_win_rows(const ConvShape &sh, int TR) { return sh.s * (TR - 1) + sh.s / 2 + 2 * sh.k + 1; }
 
-size_t wg_lds_bytes(const ConvShape &sh, int TR)
+size_t wg_lds_bytes(const ConvShape &sh, int TR, int NCI)
 {
     const long LCP = sh.W + 2 * kXO;
     const long XCS = static_cast<long>(wg_win_rows(sh, TR)) * LCP + 8;
     const long DP = static_cast<long>(TR) * sh.Wo + 8;
-    return sizeof(bf16raw) * static_cast<size_t>(sh.Ci * XCS + kMB * 16 * DP);
+    return sizeof(bf16raw) * static_cast<size_t>(NCI * XCS + kMB * 16 * DP);
+}
+
+// input channels spanned by NB column tiles (16 columns each, ci-major with T
+// taps per channel) starting anywhere
+int wg_nci(const ConvShape &sh, int NB)
+{
+    return std::min(sh.Ci, (NB * 16 - 1) / sh.T + 2);
 }
 
 constexpr size_t kWgLdsTarget = 80 * 1024;  // two blocks per CU
@@ -268,9 +284,11 @@ WgTiling wg_tiling(const ConvShape &sh, int NBW)
 {
     WgTiling tg;
     // tallest full-width tile of at most 256 pixels within the LDS target
+    const int NCI = wg_nci(sh, 4 * NBW);
     int TR = std::max(1, std::min(sh.Ho, 256 / std::max(1, sh.Wo)));
-    while (TR > 1 && wg_lds_bytes(sh, TR) > kWgLdsTarget)
+    while (TR > 1 && wg_lds_bytes(sh, TR, NCI) > kWgLdsTarget)
         --TR;
+    tg.NCI = NCI;
     tg.TR = TR;
     tg.npix_max = tg.TR * sh.Wo;
     tg.tiles_per_img = cdiv(sh.Ho, tg.TR);
@@ -297,7 +315,7 @@ int wg_nbw(const ConvShape &sh)
     return cdiv(ncol, 4 * groups);
 }
 
-size_t wg_lds(const ConvShape &sh, const WgTiling &tg) { return wg_lds_bytes(sh, tg.TR); }
+size_t wg_lds(const ConvShape &sh, const WgTiling &tg) { return wg_lds_bytes(sh, tg.TR, tg.NCI); }
 
 } // namespace
 
