@@ -353,6 +353,12 @@ SWEEP = [
     # gradient only)
     (2, 1, 16, 13, 20, 3, 1), (1, 1, 32, 9, 44, 3, 1), (3, 1, 8, 40, 40, 3, 1),
     (1, 3, 5, 10, 12, 3, 1),
+    # dispatch boundaries of the few-channel gradients: the fused backward
+    # with 20 output channels (a ragged second block of 16) at W = 44; 33
+    # output channels (no fused kernel, W not a multiple of 8): the
+    # small-channel weight gradient over three 16-channel blocks and the
+    # small-channel data gradient over 33 channels, also in bf16
+    (1, 1, 20, 9, 44, 2, 1), (2, 1, 33, 7, 44, 1, 1),
     # wide bf16 matrix-core path: registers (k=1: 32 and 64 channels, k=2: 32),
     # LDS-resident weights (long contractions), several channel chunks,
     # partial last tiles, narrow and wide rows
